@@ -1,0 +1,270 @@
+"""float64 oracle for the LoCA per-block adaptation step -- TEST INFRASTRUCTURE.
+
+Only the test suite, the package's smoke check and the benchmark's CPU-baseline
+leg import this module.  It wraps the plain-C routines of ``loca_oracle.c``
+(built by ``oracle/build.py``) with numpy marshalling, and composes them into
+the steps of one block solve in the paper's order (Section S13's outer
+iteration, steps 2-5):
+
+  1. head error E_t = w_t (softmax(z_t) - onehot(y_t))         (Lemma S3.1)
+  2. feedback Y = E A~, Q = Y B~ ; per mini-batch eta_bar and the displacement
+     T = -eta_bar Q                                               (Eq. 10, S8)
+  3. streaming statistics S += X^T X, Z += X^T T (dense)          (Eq. 9, S7)
+  4. ridge solve (S + lam I) W = S W_prev + Z by Cholesky          (Thm S6.1, S7)
+  5. Eckart-Young truncation of W to rank r_a                      (Lemma S5.2)
+plus the paper-literal projected form with a random A_l            (Eqs. 6-9)
+
+It shares no code with the HIP path and never imports it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.environ.get("LOCA_ORACLE_LIB", os.path.join(_HERE, "liblocaoracle.so"))
+_lib = None
+
+_D = ctypes.POINTER(ctypes.c_double)
+_I64 = ctypes.c_int64
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            from .build import build_oracle
+            build_oracle()
+        _lib = ctypes.CDLL(_LIB_PATH)
+        for name in ("loca_oracle_credit", "loca_oracle_scaled_target", "loca_oracle_gram_acc",
+                     "loca_oracle_cross_acc", "loca_oracle_gram_entries", "loca_oracle_cholesky_solve",
+                     "loca_oracle_qr", "loca_oracle_projected_acc"):
+            getattr(_lib, name).restype = None
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"]
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+# ----------------------------------------------------------------- primitives
+
+
+def head_error(z, y, w=None) -> np.ndarray:
+    z = _f64(z)
+    n, C = z.shape
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    E = np.empty((n, C), np.float64)
+    w64 = None if w is None else _f64(w)
+    rc = _load().loca_oracle_head_error(_I64(n), _I64(C), _p(z), _p(y), _p(w64), _p(E))
+    if rc != 0:
+        raise ValueError(f"label out of range at row {-rc - 1}")
+    return E
+
+
+def credit(E, A, B, want_q=True):
+    E, A, B = _f64(E), _f64(A), _f64(B)
+    n, C = E.shape
+    k, d = B.shape
+    assert A.shape == (C, k)
+    Y = np.empty((n, k), np.float64)
+    Q = np.empty((n, d), np.float64) if want_q else None
+    _load().loca_oracle_credit(_I64(n), _I64(C), _I64(k), _I64(d), _p(E), _p(A), _p(B), _p(Y), _p(Q))
+    return Y, Q
+
+
+def scaled_target(X, Q, eta):
+    X, Q = _f64(X), _f64(Q)
+    n, d = X.shape
+    T = np.empty((n, d), np.float64)
+    info = np.empty(3, np.float64)
+    _load().loca_oracle_scaled_target(_I64(n), _I64(d), _p(X), _p(Q), ctypes.c_double(eta), _p(T), _p(info))
+    return T, {"sum_x2": info[0], "sum_q2": info[1], "eta_bar": info[2]}
+
+
+def gram_acc(X, S=None):
+    X = _f64(X)
+    n, d = X.shape
+    S = np.zeros((d, d), np.float64) if S is None else S
+    _load().loca_oracle_gram_acc(_I64(n), _I64(d), _p(X), _p(S))
+    return S
+
+
+def cross_acc(X, T, Z=None):
+    X, T = _f64(X), _f64(T)
+    n, d = X.shape
+    m = T.shape[1]
+    Z = np.zeros((d, m), np.float64) if Z is None else Z
+    _load().loca_oracle_cross_acc(_I64(n), _I64(d), _I64(m), _p(X), _p(T), _p(Z))
+    return Z
+
+
+def gram_entries(X, pairs) -> np.ndarray:
+    X = _f64(X)
+    n, d = X.shape
+    ij = np.ascontiguousarray(pairs, dtype=np.int64).reshape(-1, 2)
+    out = np.empty(ij.shape[0], np.float64)
+    _load().loca_oracle_gram_entries(_I64(n), _I64(d), _p(X), _I64(ij.shape[0]), _p(ij), _p(out))
+    return out
+
+
+def cholesky(A) -> np.ndarray:
+    L = _f64(A).copy()
+    info = _load().loca_oracle_cholesky(_I64(L.shape[0]), _p(L))
+    if info != 0:
+        raise np.linalg.LinAlgError(f"not positive definite at pivot {info}")
+    return L
+
+
+def ridge_solve(S, RHS, lam):
+    S, RHS = _f64(S), _f64(RHS)
+    d = S.shape[0]
+    m = RHS.shape[1]
+    W = np.empty((d, m), np.float64)
+    resid = ctypes.c_double(0.0)
+    info = _load().loca_oracle_ridge_solve(_I64(d), _I64(m), _p(S), _p(RHS), ctypes.c_double(lam), _p(W),
+                                           ctypes.byref(resid))
+    if info != 0:
+        raise np.linalg.LinAlgError(f"ridge system not positive definite (pivot {info})")
+    return W, resid.value
+
+
+def svd(A):
+    A = _f64(A)
+    rows, cols = A.shape
+    assert rows >= cols
+    U = np.empty((rows, cols), np.float64)
+    s = np.empty(cols, np.float64)
+    V = np.empty((cols, cols), np.float64)
+    _load().loca_oracle_svd(_I64(rows), _I64(cols), _p(A), _p(U), _p(s), _p(V))
+    return U, s, V
+
+
+def qr(A):
+    A = _f64(A)
+    rows, cols = A.shape
+    Q = np.empty((rows, cols), np.float64)
+    R = np.empty((cols, cols), np.float64)
+    _load().loca_oracle_qr(_I64(rows), _I64(cols), _p(A), _p(Q), _p(R))
+    return Q, R
+
+
+def truncate_dense(W, r):
+    W = _f64(W)
+    d = W.shape[0]
+    Wr = np.empty((d, d), np.float64)
+    sig = np.empty(d, np.float64)
+    _load().loca_oracle_truncate_dense(_I64(d), _p(W), _I64(r), _p(Wr), _p(sig))
+    return Wr, sig
+
+
+def truncate_factored(M, R, r, want_dense=True):
+    M, R = _f64(M), _f64(R)
+    d, kp = M.shape
+    assert R.shape == (kp, d) and kp <= d
+    Wr = np.empty((d, d), np.float64) if want_dense else None
+    sig = np.empty(kp, np.float64)
+    a = np.empty((r, d), np.float64)
+    b = np.empty((d, r), np.float64)
+    _load().loca_oracle_truncate_factored(_I64(d), _I64(kp), _p(M), _p(R), _I64(r), _p(Wr), _p(sig), _p(a), _p(b))
+    return Wr, sig, a, b
+
+
+def projected_acc(X, T, Aproj, Bcur=None, G=None, Cst=None):
+    X, T, Aproj = _f64(X), _f64(T), _f64(Aproj)
+    n, d = X.shape
+    r = Aproj.shape[0]
+    G = np.zeros((r, r), np.float64) if G is None else G
+    Cst = np.zeros((d, r), np.float64) if Cst is None else Cst
+    Bc = None if Bcur is None else _f64(Bcur)
+    _load().loca_oracle_projected_acc(_I64(n), _I64(d), _I64(r), _p(X), _p(T), _p(Aproj), _p(Bc), _p(G), _p(Cst))
+    return G, Cst
+
+
+def projected_solve(G, Cst, lam):
+    G, Cst = _f64(G), _f64(Cst)
+    d, r = Cst.shape
+    Bs = np.empty((d, r), np.float64)
+    resid = ctypes.c_double(0.0)
+    info = _load().loca_oracle_projected_solve(_I64(d), _I64(r), _p(G), _p(Cst), ctypes.c_double(lam), _p(Bs),
+                                               ctypes.byref(resid))
+    if info != 0:
+        raise np.linalg.LinAlgError(f"projected system not positive definite (pivot {info})")
+    return Bs, resid.value
+
+
+# ----------------------------------------------------------------- one block
+
+
+def block_step(xs: Sequence[np.ndarray], zs: Sequence[np.ndarray], ys: Sequence[np.ndarray],
+               A, B, eta: float, lambdas: Sequence[float], r_a: int,
+               ws: Optional[Sequence[np.ndarray]] = None, W_prev=None,
+               Aproj=None, Bproj_cur=None, dense_truncation: Optional[bool] = None,
+               want_dense=True) -> Dict:
+    """All steps of one block over its mini-batches, in the paper's order.
+
+    xs[m] (n_m x d), zs[m] (n_m x C), ys[m] (n_m) are float64-exact inputs of
+    mini-batch m; A (C x k), B (k x d) the credit factors.  W_prev (d x d) is the
+    current adapter in token-major form (None = frozen model).  Aproj (r_a x d),
+    when given, adds the paper-literal projected solve with current adapter
+    Bproj_cur (d x r_a, None = 0).
+    """
+    d = B.shape[1]
+    S = np.zeros((d, d), np.float64)
+    Z = np.zeros((d, d), np.float64)
+    K = np.zeros((d, B.shape[0]), np.float64)
+    G = Cst = None
+    if Aproj is not None:
+        G = np.zeros((Aproj.shape[0], Aproj.shape[0]), np.float64)
+        Cst = np.zeros((d, Aproj.shape[0]), np.float64)
+    mbs: List[Dict] = []
+    Ys, Ts, Es = [], [], []
+    for m, (X, z, y) in enumerate(zip(xs, zs, ys)):
+        E = head_error(z, y, None if ws is None else ws[m])
+        Y, Q = credit(E, A, B)
+        T, info = scaled_target(X, Q, eta)
+        gram_acc(X, S)
+        cross_acc(X, T, Z)
+        cross_acc(X, -info["eta_bar"] * Y, K)
+        if Aproj is not None:
+            projected_acc(X, T, Aproj, Bproj_cur, G, Cst)
+        mbs.append(info)
+        Es.append(E)
+        Ys.append(Y)
+        Ts.append(T)
+    out = {"S": S, "Z": Z, "K": K, "mb": mbs, "E": Es, "Y": Ys, "T": Ts, "solves": []}
+    if dense_truncation is None:
+        dense_truncation = d <= 256
+    for lam in lambdas:
+        RHS = Z.copy() if W_prev is None else S @ W_prev + Z
+        W, resid = ridge_solve(S, RHS, lam)
+        # factored form of the same solve: W = M [B~] (W_prev = None)
+        sol = {"lam": lam, "W": W, "resid": resid}
+        if W_prev is None:
+            M, _ = ridge_solve(S, K, lam)
+            sol["M"] = M
+            if dense_truncation:
+                Wr, sig = truncate_dense(W, r_a)
+            else:
+                Wr, sig, _, _ = truncate_factored(M, _f64(B), r_a, want_dense=want_dense)
+            sol["W_r"] = Wr
+            sol["sigma"] = sig
+        if Aproj is not None:
+            Bs, presid = projected_solve(G, Cst, lam)
+            sol["B_proj"] = Bs
+            sol["proj_resid"] = presid
+        out["solves"].append(sol)
+    if Aproj is not None:
+        out["G_proj"] = G
+        out["C_proj"] = Cst
+    return out
