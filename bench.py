@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark of the LoCA per-block adaptation step on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input
+for every block of the workload: per micro-batch the head error and credit
+coordinates, the streaming statistics S and K; then the ridge solves for all
+ridge strengths and the rank-r_a truncation.  Inputs are resident in HBM when
+the timed region starts.
+
+Prints ONE JSON line (rank 0).  `value` = blocks * tokens / step time: the
+number of (token, block) pairs taken through error -> target -> statistics ->
+solve per second ("tokens/s per block").
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+BF16_PEAK_TFLOPS = 2516.6    # MI355X dense bf16 MFMA
+FP64_PEAK_TFLOPS = 78.6      # MI355X dense fp64
+HBM_PEAK_GBS = 8000.0
+
+WORKLOADS = {
+    "c1": "Single block, Qwen2.5-0.5B width: d=896, N=512, C=2, k=8, r_a=8, lambda=1e-2, fp32 mode",
+    "c2": "Qwen2.5-1.5B-shaped: 28 blocks, d=1536, N=8192 (4 x 2048), C=4, k=16, r_a=16, lambda=1e-2, bf16 X",
+    "c3": "Qwen2.5-7B-shaped: 28 blocks, d=3584, N=32768 (4 x 8192), C=5, k=32, r_a=16, "
+          "lambda in {1e-3,1e-2,1e-1}, bf16 X, fp32 accumulation",
+    "c4": "Full-vocabulary error: 1 block, d=2048, N=4096, V=151936 (bf16 logits), k=64, r_a=32, bf16 X",
+    "c5": "Qwen2.5-14B-shaped: 48 blocks, d=5120, N=65536 (8 x 8192), C=5, k=64, r_a=32, lambda=1e-2, bf16 X",
+}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=2)
+    p.add_argument("--config", default="c3", choices=sorted(WORKLOADS))
+    p.add_argument("--blocks", type=int, default=0, help="override the block count (profiling runs)")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-tokens", type=int, default=0, help="tokens in the CPU-baseline sample")
+    return p.parse_args()
+
+
+def make_inputs(cfg, nb, device="cuda"):
+    import numpy as np
+    import torch
+    from paper_2608_03020_amd import inputs as gen
+    xs = []
+    A = []
+    B = []
+    for b in range(nb):
+        x, a, bb = gen.torch_gen_block_inputs(cfg, b, seed=0, device=device)
+        xs.append(x)
+        A.append(a)
+        B.append(bb)
+    x_all = torch.stack(xs)
+    del xs
+    z, y = gen.torch_gen_head(cfg, seed=0, device=device)
+    return x_all, z, y, torch.stack(A), torch.stack(B)
+
+
+def cpu_baseline(cfg, n_sample):
+    """The oracle as it stands, on a bounded sample of block 0 of the workload:
+    the per-token stages (head error, feedback, target, S, dense Z, K) on
+    `n_sample` tokens of one micro-batch, scaled to the block's N tokens, plus
+    the per-block stages (ridge solve of every lambda with the factored
+    right-hand side K, Eckart-Young truncation) at full width."""
+    import numpy as np
+    import oracle
+    from paper_2608_03020_amd import inputs as gen
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    sub = gen.custom_config("sample", blocks=1, d=cfg.d, n=n_sample, C=cfg.C, k=cfg.k, r_a=cfg.r_a,
+                            lambdas=cfg.lambdas, mode=cfg.mode, x_dist=cfg.x_dist, n_outlier=cfg.n_outlier,
+                            outlier_scale=cfg.outlier_scale, logit_std=cfg.logit_std, logit_dtype=cfg.logit_dtype,
+                            a_dtype=cfg.a_dtype, eta=cfg.eta)
+    X = gen.as_f64(gen.gen_x(sub, 0, 0), "bf16" if cfg.mode == "bf16" else "f32")
+    z = gen.as_f64(gen.gen_logits(sub, 0), cfg.logit_dtype)
+    y = gen.gen_labels(sub, 0)
+    A, Bm = gen.gen_credit(sub, 0)
+    A = gen.as_f64(A, cfg.a_dtype)
+    Bm = np.asarray(Bm, np.float64)
+    t0 = time.perf_counter()
+    E = oracle.head_error(z, y)
+    Y, Q = oracle.credit(E, A, Bm)
+    T, info = oracle.scaled_target(X, Q, cfg.eta)
+    S = oracle.gram_acc(X)
+    Z = oracle.cross_acc(X, T)
+    K = oracle.cross_acc(X, -info["eta_bar"] * Y)
+    t_tok = time.perf_counter() - t0
+    # per-block stages on a well-posed full-width system (the sample's S has rank n_sample < d)
+    S_full = S + np.eye(cfg.d) * float(np.trace(S) / cfg.d)
+    t1 = time.perf_counter()
+    Ms = [oracle.ridge_solve(S_full, K, lam)[0] for lam in cfg.lambdas]
+    for M in Ms:
+        oracle.truncate_factored(M, Bm, cfg.r_a, want_dense=False)
+    t_blk = time.perf_counter() - t1
+    t_block = t_tok * (cfg.n / n_sample) + t_blk
+    return {"value": cfg.n / t_block, "unit": "tokens/s per block", "cores": threads, "kind": "oracle",
+            "sample": (f"block 0 of {cfg.name}: per-token stages on {n_sample} of {cfg.n} tokens "
+                       f"({t_tok:.2f} s, scaled x{cfg.n / n_sample:.0f}); ridge solves for {len(cfg.lambdas)} "
+                       f"lambda(s) with the factored right-hand side and truncation at d={cfg.d} ({t_blk:.2f} s)"),
+            "seconds_per_block": t_block, "_unused": float(Z[0, 0])}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding is a design only).", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2608_03020_amd import loca
+    from paper_2608_03020_amd.inputs import CONFIGS
+    from paper_2608_03020_amd.step import BlockStep
+
+    cfg = CONFIGS[args.config]
+    nb = args.blocks or cfg.blocks
+    torch.cuda.init()
+    dev = torch.device("cuda:0")
+    print(f"[bench] {args.config}: generating inputs for {nb} blocks", file=sys.stderr, flush=True)
+    x_all, z, y, A, B = make_inputs(cfg, nb)
+    step = BlockStep(cfg, nb, dev)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+
+    # events around every statistics call of the timed region (the dominant kernel)
+    n_mb = cfg.n_micro
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps * n_mb)]
+
+    def one_step(record=None):
+        step.reset()
+        for m in range(n_mb):
+            lo, hi = cfg.micro_rows(m)
+            xm = x_all[:, lo:hi]
+            yv = step.Y[:, :hi - lo]
+            loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, nb=nb)
+            if record is not None:
+                record[m][0].record(stream)
+            loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws)
+            if record is not None:
+                record[m][1].record(stream)
+        step.solve(B)
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        one_step(ev[s * n_mb:(s + 1) * n_mb])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms_step = dt * 1e3 / args.steps
+    info = step.info.cpu().numpy()
+    if np.any(info != 0):
+        print(f"[bench] warning: dev_info {info}", file=sys.stderr)
+
+    stats_ms = [a.elapsed_time(b) for a, b in ev]
+    rows = [cfg.micro_rows(m)[1] - cfg.micro_rows(m)[0] for m in range(n_mb)]
+    flops = [nb * (r * cfg.d * (cfg.d + 1) + 2 * r * cfg.d * cfg.k) for r in rows] * args.steps
+    t_avg = sum(stats_ms) / len(stats_ms)
+    f_avg = sum(flops) / len(flops)
+    achieved = f_avg / (t_avg * 1e-3) / 1e12
+    peak = FP64_PEAK_TFLOPS if cfg.mode == "fp32" else BF16_PEAK_TFLOPS
+
+    value = nb * cfg.n / (ms_step * 1e-3)
+    out = {
+        "metric": "tokens/sec per block (error->target->Gram+solve); % MFMA peak on X^T X",
+        "value": value,
+        "unit": "tokens/s per block",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64" if cfg.mode == "fp32" else "bf16",
+        "data": "synthetic (seeded; device-generated inputs with the workload's distributions)",
+        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "blocks": nb, "d": cfg.d,
+                   "tokens": cfg.n, "micro_batch": cfg.micro, "classes": cfg.C, "credit_rank": cfg.k,
+                   "adapter_rank": cfg.r_a, "lambdas": list(cfg.lambdas)},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved / peak, "traffic": None,
+                     "kernel": "loca_accumulate_stats (Gram S += X^T X and cross X^T Y of all blocks, one micro-batch)",
+                     "algorithmic_flops_per_launch": f_avg, "avg_launch_ms": t_avg},
+    }
+    if not args.no_cpu_baseline:
+        del x_all
+        torch.cuda.empty_cache()
+        n_s = args.cpu_tokens or (512 if cfg.d >= 3000 else 1024)
+        print(f"[bench] cpu baseline: oracle on {n_s} tokens", file=sys.stderr, flush=True)
+        cb = cpu_baseline(cfg, min(n_s, cfg.n))
+        cb.pop("_unused", None)
+        out["cpu_baseline"] = cb
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,228 @@
+/*
+ * loca.h -- C ABI of libloca, the gfx950 (MI355X) implementation of the
+ * forward-only per-block adaptation step of LoCA (Local Credit Assignment).
+ *
+ * After calibration, each outer iteration of the method (Section S13, steps
+ * 2-5) needs, for every transformer block l:
+ *   (a1) the frozen-head error  E_t = w_t (softmax(z_t) - onehot(y_t))
+ *        (Lemma S3.1; Eq. 4);
+ *   (a2) the tokenwise feedback through the fixed rank-k credit factors,
+ *        Y = E A~ and Q = Y B~ (Sections S3, S11), and the scale-normalised
+ *        displacement T = -eta_bar_m Q of each mini-batch m (Eq. 10, S8);
+ *   (a3) the streaming Gram S += X_m^T X_m of the block inputs (Eq. 9, S7);
+ *   (a4) the streaming cross statistic K += -eta_bar_m X_m^T Y_m, so that the
+ *        full cross statistic is Z = X^T T = K B~ (Eq. 9, S7);
+ *   (a5) the ridge solve (S + lam I) W = S W_prev + Z by Cholesky
+ *        (Eq. 7, Theorem S6.1, S7), and the paper's projected form
+ *        B* = C_l (G_l + lam I)^{-1} with a fixed random projection A_l;
+ *   (a6) the best rank-r_a approximation of W (Lemma S5.2), returned as
+ *        adapter factors A (r_a x d), B (d x r_a) with W_r = A^T B^T.
+ *
+ * Symbols: X is N x d, one token per row (the block input h_{l-1} at the
+ * selected prediction positions); the paper's head W_u^T is folded into the
+ * credit factor A~ (C x k), so C is the label-set size (or the vocabulary) and
+ * the paper's F_l = U_k S_k V_k^T corresponds to A~ = W_u V_k, B~ = S_k U_k^T.
+ *
+ * Conventions for every entry point
+ *   - All matrices are row-major.  Array pointers are DEVICE pointers owned by
+ *     the caller, except `lambdas`, which is a host array.
+ *   - Calls are batched over `nb` independent blocks (the Jacobi schedule
+ *     solves blocks independently, Section S8).  Per-block arrays of block b
+ *     start at base + b * <name>_bstride (in elements of the array's type).
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ *     The library never synchronises, never allocates device memory and
+ *     keeps no global state.  Scratch memory comes from the caller's `ws`,
+ *     at least loca_workspace_size(...) bytes, 256-byte aligned.
+ *   - Argument errors are detected on the host before anything is enqueued
+ *     and returned synchronously (LOCA_E_ARG, LOCA_E_WORKSPACE,
+ *     LOCA_E_UNSUPPORTED).  Launch failures return LOCA_E_HIP.  Conditions
+ *     found on the device are written to `dev_info` (device int32).
+ *   - Concurrent calls are safe when they use distinct output and workspace
+ *     buffers.  No C++ exception crosses this interface.
+ *   - Precision modes: "bf16 mode" = bf16 X, fp32 statistics (S, K); "fp32
+ *     mode" = fp32 X, fp64 statistics.  Other combinations are rejected.
+ */
+#ifndef LOCA_H
+#define LOCA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LOCA_OK = 0,
+  LOCA_E_ARG = 1,          /* invalid argument (null pointer, bad size, stride, lambda <= 0, ...) */
+  LOCA_E_WORKSPACE = 2,    /* ws is NULL, misaligned or smaller than loca_workspace_size() */
+  LOCA_E_HIP = 3,          /* a HIP launch failed */
+  LOCA_E_UNSUPPORTED = 4   /* valid but outside what this build implements (e.g. k > 128) */
+} loca_status;
+
+typedef enum { LOCA_F32 = 0, LOCA_BF16 = 1, LOCA_F64 = 2 } loca_dtype;
+
+typedef enum {
+  LOCA_OP_ERROR_TARGETS = 0,
+  LOCA_OP_ACCUMULATE_STATS = 1,
+  LOCA_OP_RIDGE_SOLVE = 2,
+  LOCA_OP_LOWRANK_TRUNCATE = 3,
+  LOCA_OP_RIDGE_SOLVE_PROJECTED = 4
+} loca_op;
+
+/* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
+ * Device-resident, one per block.  RMS ratios use squared Frobenius norms:
+ * eta_bar = eta * sqrt(sum_x2 / sum_q2), and eta_bar = 0 when sum_q2 = 0. */
+typedef struct {
+  double sum_q2;   /* ||Q_m||_F^2, Q_m = Y_m B~ (written by loca_error_targets)      */
+  double sum_x2;   /* ||X_m||_F^2 (written by loca_accumulate_stats)                  */
+  double eta_bar;  /* absolute step of this micro-batch (written by loca_accumulate_stats) */
+  int64_t n;       /* tokens in the micro-batch                                        */
+} loca_mb;
+
+typedef void* loca_stream_t; /* hipStream_t */
+
+/* ---------------------------------------------------------------------------
+ * (a1, a2) Head error and credit coordinates of one micro-batch.
+ *   Lemma S3.1: E_t = w_t (softmax(z_t) - onehot(y_t)) over C classes.
+ *   Sections S3, S11: Y = E A~ (n x k) for every block; and
+ *   mb[b].sum_q2 = ||Y B~_b||_F^2 = sum_t Y_t (B~ B~^T) Y_t^T, the denominator of
+ *   Eq. 10 (the displacement itself is never materialised; see
+ *   loca_dense_targets).
+ * logits : n x C (ld_logits >= C), F32 or BF16, shared by all blocks.
+ * labels : n int32 in [0, C).       w : n float loss weights, or NULL (= 1).
+ * credit_a : per block C x k (F32 or BF16), stride a_bstride.
+ * credit_b : per block k x d float, stride b_bstride.
+ * y_out : per block n x k float, stride y_bstride.
+ * e_out : n x C float, or NULL (the error rows, for tests).
+ * mb_out : nb entries; sum_q2 and n are written, sum_x2 and eta_bar zeroed.
+ * dev_info : one int32; 0, or 1 + the smallest row whose label is out of range
+ *            (that row's outputs are then unspecified).
+ * Limits: k <= 128.  Any n >= 1, C >= 1, d >= 1.
+ * ------------------------------------------------------------------------- */
+loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k,
+                               int64_t d, const void* logits, loca_dtype logits_dtype,
+                               int64_t ld_logits, const int32_t* labels, const float* w,
+                               const void* credit_a, loca_dtype a_dtype, int64_t a_bstride,
+                               const float* credit_b, int64_t b_bstride, float* y_out,
+                               int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info,
+                               void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * (a3, a4) Streaming statistics of one micro-batch (Eq. 9; Section S7):
+ *   S_b += X_b^T X_b                (d x d; the upper triangle j >= i is
+ *                                    maintained, entries below it are
+ *                                    unspecified and never read),
+ *   mb[b].sum_x2 = ||X_b||_F^2,  mb[b].eta_bar = eta sqrt(sum_x2/sum_q2) (Eq. 10),
+ *   K_b += -eta_bar X_b^T Y_b       (d x k).
+ * The caller zeroes S and K before the first micro-batch.  Each mini-batch
+ * uses its own eta_bar (Section S8).
+ * x : per block n x d, ldx >= d, x_bstride; BF16 (then acc = F32) or F32
+ *     (then acc = F64).  BF16 requires ldx % 8 == 0 and a 16-byte aligned
+ *     base; F32 requires ldx % 4 == 0 and 16-byte alignment.
+ * y : per block n x k float (from loca_error_targets), y_bstride.
+ * mb : in: sum_q2; out: sum_x2, eta_bar, n.   eta >= 0.
+ * S, K : per block, type `acc`, strides s_bstride, k_bstride.
+ * Limits: k <= 128.
+ * ------------------------------------------------------------------------- */
+loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, int64_t d, int64_t k,
+                                  const void* x, loca_dtype x_dtype, int64_t ldx, int64_t x_bstride,
+                                  const float* y, int64_t y_bstride, double eta, loca_mb* mb,
+                                  void* S, void* K, loca_dtype acc, int64_t s_bstride,
+                                  int64_t k_bstride, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * (a5) Ridge solve in factored form (Eq. 7; Theorem S6.1; Section S7's
+ * positive-definite solve without an explicit inverse).  For block b and each
+ * lam_l > 0 (host array `lambdas`, n_lambda entries):
+ *   M_{b,l} = (S_b + lam_l I)^{-1} [ S_b Lp_b | K_b ]         (d x (r_prev + k))
+ * so that the full-width solution of (S + lam I) W = S W_prev + Z, with the
+ * current adapter W_prev = Lp Rp (token-major, d x d, rank r_prev) and
+ * Z = K B~, is W = M [Rp; B~].  r_prev = 0 (lp = NULL) is the frozen model.
+ * Cholesky of the Jacobi-equilibrated matrix, in fp32 (acc = F32) or fp64
+ * (acc = F64).
+ * S, K : as produced by loca_accumulate_stats (upper triangle of S read).
+ * m_out : float, matrix (b, l) at m_out + (b * n_lambda + l) * m_bstride.
+ * w_dense_out : optional float d x d W for matrix (b, l) at
+ *               w_dense_out + (b * n_lambda + l) * w_bstride; needs rp and
+ *               credit_b (ignored when NULL).
+ * dev_info : nb * n_lambda int32; 0, or the 1-based index of the first
+ *            non-positive pivot (LAPACK potrf convention).
+ * Limits: r_prev + k <= 128.
+ * ------------------------------------------------------------------------- */
+loca_status loca_ridge_solve(loca_stream_t stream, int64_t nb, int64_t d, int64_t k, const void* S,
+                             const void* K, loca_dtype acc, int64_t s_bstride, int64_t k_bstride,
+                             const float* lp, const float* rp, int64_t r_prev, int64_t lp_bstride,
+                             int64_t rp_bstride, const double* lambdas, int64_t n_lambda,
+                             float* m_out, int64_t m_bstride, const float* credit_b,
+                             int64_t b_bstride, float* w_dense_out, int64_t w_bstride,
+                             int32_t* dev_info, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * (a6) Best rank-r_a approximation (Lemma S5.2, Eckart-Young) of W = M R,
+ * M: d x kp, R: kp x d, for nm matrices.  Matrix i reads M at
+ * m + i * m_bstride and R at r + (i / r_group) * r_bstride (r_group >= 1 lets
+ * several ridge strengths share one B~).  With W = U diag(s) V^T:
+ *   a_out = U_{r_a}^T            (r_a x d, orthonormal rows),
+ *   b_out = V_{r_a} diag(s_{r_a}) (d x r_a),   so W_{r_a} = a_out^T b_out^T
+ * and the adapter acts as h_l = h_bar_l + b_out a_out h_{l-1} (Eq. 1).
+ * sigma_out : the kp largest singular values of W, decreasing.
+ * Directions with zero singular value (W has rank < r_a) get zero rows/cols.
+ * w_dense_out : optional d x d W_{r_a} (float), stride w_bstride.
+ * dev_info : nm int32, 0 (reserved for future conditions).
+ * Limits: kp <= 128, r_a <= kp, kp <= d.
+ * ------------------------------------------------------------------------- */
+loca_status loca_lowrank_truncate(loca_stream_t stream, int64_t nm, int64_t d, int64_t kp,
+                                  int64_t r_a, const float* m, int64_t m_bstride, const float* r,
+                                  int64_t r_bstride, int64_t r_group, float* a_out,
+                                  int64_t a_bstride, float* b_out, int64_t b_bstride,
+                                  float* sigma_out, int64_t sigma_bstride, float* w_dense_out,
+                                  int64_t w_bstride, int32_t* dev_info, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * (a5, paper-literal form) Projected block fit of Eqs. 6-9 with the fixed
+ * random projection A_l (r_a x d) of Eq. 1, computed from the full-width
+ * statistics:  G_l = A_l S A_l^T,  C_l = B_cur G_l + B~^T K^T A_l^T,
+ *              B*_l = C_l (G_l + lam I)^{-1}            (d x r_a)
+ * (with features p = A_l x and residual target rho = B_cur p + T_t these are
+ * exactly the sums of Eq. 9).  b_cur (d x r_a) may be NULL (frozen model).
+ * b_out : float, matrix (b, l) at b_out + (b * n_lambda + l) * bo_bstride.
+ * g_out : optional float r_a x r_a G_l per block (stride r_a * r_a).
+ * dev_info : nb * n_lambda int32 (non-positive pivot, 1-based).
+ * Limits: r_a <= 128, k <= 128.
+ * ------------------------------------------------------------------------- */
+loca_status loca_ridge_solve_projected(loca_stream_t stream, int64_t nb, int64_t d, int64_t k,
+                                       int64_t r_a, const void* S, const void* K, loca_dtype acc,
+                                       int64_t s_bstride, int64_t k_bstride,
+                                       const float* credit_b, int64_t b_bstride,
+                                       const float* proj_a, int64_t pa_bstride,
+                                       const float* b_cur, int64_t bc_bstride,
+                                       const double* lambdas, int64_t n_lambda, float* b_out,
+                                       int64_t bo_bstride, float* g_out, int32_t* dev_info,
+                                       void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * Dense displacement T = -eta_bar Y B~ (Eq. 10; Section S8) of one micro-batch,
+ * n x d float per block (stride t_bstride), from the credit coordinates and
+ * the eta_bar written by loca_accumulate_stats.  Not on the hot path (the
+ * statistics never need T); provided for tests and callers that want it.
+ * ------------------------------------------------------------------------- */
+loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t k, int64_t d,
+                               const float* y, int64_t y_bstride, const loca_mb* mb,
+                               const float* credit_b, int64_t b_bstride, float* t_out,
+                               int64_t t_bstride);
+
+/* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
+ * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there).  `acc` selects the
+ * precision mode.  Unused arguments may be 0. */
+size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,
+                           int64_t r_a, int64_t n_lambda, loca_dtype acc);
+
+const char* loca_status_str(loca_status s);
+const char* loca_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOCA_H */

@@ -1,0 +1,327 @@
+// k_error.hip -- head error and credit coordinates (rows a1, a2 of the step).
+//
+// Lemma S3.1: E_t = w_t (softmax(z_t) - onehot(y_t)).  Sections S3 / S11: the
+// feedback is applied through the rank-k factors, Y = E A~, and the
+// denominator of the scale-normalised step (Eq. 10) is
+// ||Q||_F^2 = sum_t Y_t (B~ B~^T) Y_t^T, so Q = Y B~ is never formed.
+//
+// Two kernels:
+//  * small label sets (C <= 64): one thread per token; A~ and G = B~ B~^T are
+//    staged in LDS; softmax in fp32 with the row maximum subtracted.
+//  * large vocabularies: one workgroup per group of tokens streams the logits
+//    once with an online (running-max) softmax, accumulating the rescaled
+//    sum of exp(z - m) A~[c] alongside; Y = acc / s - A~[y].
+// Both write per-workgroup partial sums of ||Q||^2 (fp64) that a finalize
+// kernel adds in a fixed order, so results are bitwise reproducible.
+#include "loca_common.h"
+
+namespace loca {
+
+namespace {
+
+constexpr int kSmallThreads = 256;
+constexpr int kSmallMaxC = 64;
+constexpr int kSmallMaxK = 64;
+constexpr int kMaxK = 128;
+
+// G_b = B~_b B~_b^T (k x k, fp64), one thread per (a, c) entry.
+__global__ void k_credit_gram(int64_t k, int64_t d, const float* __restrict__ B, int64_t b_bstride,
+                              double* __restrict__ G) {
+  const int64_t b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= k * k) return;
+  const int64_t a = e / k, c = e % k;
+  const float* Bb = B + b * b_bstride;
+  double s = 0.0;
+  for (int64_t i = 0; i < d; ++i) s += (double)Bb[a * d + i] * (double)Bb[c * d + i];
+  G[b * k * k + e] = s;
+}
+
+template <typename LT, typename AT, int KB>
+__global__ __launch_bounds__(kSmallThreads) void k_error_small(
+    int64_t n, int64_t C, int64_t k, const LT* __restrict__ logits, int64_t ld,
+    const int32_t* __restrict__ labels, const float* __restrict__ w, const AT* __restrict__ A,
+    int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out, int64_t y_bstride,
+    float* __restrict__ e_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
+  __shared__ float sA[kSmallMaxC * KB];
+  __shared__ double sG[KB * KB];
+  __shared__ double sred[kSmallThreads / 64];
+  const int64_t b = blockIdx.y;
+  const AT* Ab = A + b * a_bstride;
+  for (int64_t e = threadIdx.x; e < C * k; e += blockDim.x) sA[e] = load_as_f32(Ab + e);
+  for (int64_t e = threadIdx.x; e < k * k; e += blockDim.x) sG[e] = G[b * k * k + e];
+  __syncthreads();
+
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  double q = 0.0;
+  if (t < n) {
+    const LT* zt = logits + t * ld;
+    const int32_t yt = labels[t];
+    if (yt < 0 || yt >= C) {
+      atomicMin(dev_info, (int32_t)(t + 1));
+    } else {
+      float m = load_as_f32(zt);
+      for (int64_t c = 1; c < C; ++c) m = fmaxf(m, load_as_f32(zt + c));
+      float s = 0.f;
+      for (int64_t c = 0; c < C; ++c) s += __expf(load_as_f32(zt + c) - m);
+      const float inv = 1.0f / s;
+      const float wt = w ? w[t] : 1.0f;
+      float y[KB];
+#pragma unroll
+      for (int j = 0; j < KB; ++j) y[j] = 0.f;
+      for (int64_t c = 0; c < C; ++c) {
+        const float e = wt * (__expf(load_as_f32(zt + c) - m) * inv - (c == yt ? 1.0f : 0.0f));
+        if (e_out) e_out[t * C + c] = e;
+#pragma unroll
+        for (int j = 0; j < KB; ++j)
+          if (j < k) y[j] = fmaf(e, sA[c * k + j], y[j]);
+      }
+      float* yo = y_out + b * y_bstride + t * k;
+#pragma unroll
+      for (int j = 0; j < KB; ++j)
+        if (j < k) yo[j] = y[j];
+      // q = y G y^T (fp64; G symmetric, so off-diagonal terms are doubled)
+#pragma unroll
+      for (int a = 0; a < KB; ++a) {
+        if (a < k) {
+          double r = 0.5 * sG[a * k + a] * (double)y[a];
+#pragma unroll
+          for (int c2 = a + 1; c2 < KB; ++c2)
+            if (c2 < k) r += sG[a * k + c2] * (double)y[c2];
+          q += 2.0 * (double)y[a] * r;
+        }
+      }
+    }
+  }
+  const double tot = block_sum(q, sred);
+  if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
+}
+
+// Large vocabulary (or k > 64): TOK tokens per workgroup, 256 threads = TOK x LPT
+// lanes per token; lane ln of a token owns credit columns j = ln + q * LPT.
+constexpr int kLargeThreads = 256;
+constexpr int kLargeTok = 16;
+constexpr int kLargeChunk = 256;
+constexpr int kLargeLPT = kLargeThreads / kLargeTok;        // 16
+constexpr int kLargeKPL = kMaxK / kLargeLPT;                // 8
+
+template <typename LT, typename AT>
+__global__ __launch_bounds__(kLargeThreads) void k_error_large(
+    int64_t n, int64_t C, int64_t k, const LT* __restrict__ logits, int64_t ld,
+    const int32_t* __restrict__ labels, const float* __restrict__ w, const AT* __restrict__ A,
+    int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out, int64_t y_bstride,
+    float* __restrict__ ms_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
+  constexpr int LPT = kLargeLPT;
+  __shared__ float sZ[kLargeTok][kLargeChunk];
+  __shared__ float sAc[kLargeChunk][kMaxK];
+  __shared__ float sY[kLargeTok][kMaxK];
+  __shared__ double sred[kLargeThreads / 64];
+  const int64_t b = blockIdx.y;
+  const AT* Ab = A + b * a_bstride;
+  const int tid = threadIdx.x;
+  const int tk = tid / LPT, ln = tid % LPT;
+  const int64_t t0 = (int64_t)blockIdx.x * kLargeTok;
+  const int64_t t = t0 + tk;
+  float acc[kLargeKPL];
+#pragma unroll
+  for (int q = 0; q < kLargeKPL; ++q) acc[q] = 0.f;
+  float m_run = -INFINITY, s_run = 0.f;  // identical in all lanes of a token
+  for (int64_t c0 = 0; c0 < C; c0 += kLargeChunk) {
+    const int cw = (int)((C - c0) < kLargeChunk ? (C - c0) : kLargeChunk);
+    __syncthreads();  // previous chunk fully consumed
+    for (int e = tid; e < kLargeTok * kLargeChunk; e += kLargeThreads) {
+      const int r = e / kLargeChunk, c = e % kLargeChunk;
+      const int64_t tr = t0 + r;
+      sZ[r][c] = (tr < n && c < cw) ? load_as_f32(logits + tr * ld + c0 + c) : -INFINITY;
+    }
+    for (int64_t e = tid; e < (int64_t)cw * k; e += kLargeThreads) {
+      const int c = (int)(e / k), j = (int)(e % k);
+      sAc[c][j] = load_as_f32(Ab + (c0 + c) * k + j);
+    }
+    __syncthreads();
+    float cm = -INFINITY;
+    for (int c = ln; c < cw; c += LPT) cm = fmaxf(cm, sZ[tk][c]);
+    for (int off = LPT / 2; off > 0; off >>= 1) cm = fmaxf(cm, __shfl_xor(cm, off, kWave));
+    const float m_new = fmaxf(m_run, cm);
+    const float scale = (m_run == -INFINITY) ? 0.f : __expf(m_run - m_new);
+    float ps = 0.f;
+    for (int c = ln; c < cw; c += LPT) {
+      const float p = (m_new == -INFINITY) ? 0.f : __expf(sZ[tk][c] - m_new);
+      sZ[tk][c] = p;
+      ps += p;
+    }
+    for (int off = LPT / 2; off > 0; off >>= 1) ps += __shfl_xor(ps, off, kWave);
+    s_run = s_run * scale + ps;
+    m_run = m_new;
+    __syncthreads();  // sZ now holds exp(z - m_new)
+#pragma unroll
+    for (int q = 0; q < kLargeKPL; ++q) acc[q] *= scale;
+    for (int c = 0; c < cw; ++c) {
+      const float p = sZ[tk][c];
+#pragma unroll
+      for (int q = 0; q < kLargeKPL; ++q) {
+        const int j = ln + q * LPT;
+        if (j < k) acc[q] = fmaf(p, sAc[c][j], acc[q]);
+      }
+    }
+  }
+  double qv = 0.0;
+  if (t < n) {
+    const int32_t yt = labels[t];
+    const bool ok = (yt >= 0 && yt < C);
+    if (!ok && ln == 0) atomicMin(dev_info, (int32_t)(t + 1));
+    const float inv = 1.0f / s_run;
+    const float wt = w ? w[t] : 1.0f;
+#pragma unroll
+    for (int q = 0; q < kLargeKPL; ++q) {
+      const int j = ln + q * LPT;
+      if (j < k) {
+        const float ay = ok ? load_as_f32(Ab + (int64_t)yt * k + j) : 0.f;
+        const float yv = wt * (acc[q] * inv - ay);
+        sY[tk][j] = yv;
+        y_out[b * y_bstride + t * k + j] = yv;
+      }
+    }
+    if (ms_out && ln == 0) { ms_out[2 * t] = m_run; ms_out[2 * t + 1] = s_run; }
+  }
+  __syncthreads();
+  if (t < n) {
+    const double* Gb = G + b * k * k;
+    for (int a2 = ln; a2 < k; a2 += LPT) {
+      double r = 0.0;
+      for (int c = 0; c < k; ++c) r += Gb[a2 * k + c] * (double)sY[tk][c];
+      qv += (double)sY[tk][a2] * r;
+    }
+  }
+  const double tot = block_sum(qv, sred);
+  if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
+}
+
+// E rows for the large-vocabulary path (optional output), from the saved (m, s).
+template <typename LT>
+__global__ void k_error_write_e(int64_t n, int64_t C, const LT* __restrict__ logits, int64_t ld,
+                                const int32_t* __restrict__ labels, const float* __restrict__ w,
+                                const float* __restrict__ ms, float* __restrict__ e_out) {
+  const int64_t t = blockIdx.y;
+  const float m = ms[2 * t], inv = 1.0f / ms[2 * t + 1];
+  const float wt = w ? w[t] : 1.0f;
+  const int32_t yt = labels[t];
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < C; c += (int64_t)gridDim.x * blockDim.x)
+    e_out[t * C + c] = wt * (__expf(load_as_f32(logits + t * ld + c) - m) * inv - (c == yt ? 1.f : 0.f));
+}
+
+// dev_info holds INT32_MAX (no bad label) or 1 + the smallest bad row; 0 means ok.
+__global__ void k_error_finalize(int64_t n, int64_t nparts, const double* __restrict__ partial,
+                                 loca_mb* __restrict__ mb, int32_t* __restrict__ dev_info) {
+  const int64_t b = blockIdx.x;
+  if (threadIdx.x != 0) return;
+  if (b == 0 && *dev_info == INT32_MAX) *dev_info = 0;
+  double s = 0.0;
+  for (int64_t i = 0; i < nparts; ++i) s += partial[b * nparts + i];
+  mb[b].sum_q2 = s;
+  mb[b].sum_x2 = 0.0;
+  mb[b].eta_bar = 0.0;
+  mb[b].n = n;
+}
+
+__global__ void k_fill_i32(int32_t* p, int64_t cnt, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < cnt) p[i] = v;
+}
+
+}  // namespace
+
+static bool use_small(int64_t C, int64_t k) { return C <= kSmallMaxC && k <= kSmallMaxK; }
+
+size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k) {
+  size_t s = align256(sizeof(double) * nb * k * k);  // G
+  const int64_t parts = use_small(C, k) ? (n + kSmallThreads - 1) / kSmallThreads : (n + kLargeTok - 1) / kLargeTok;
+  s += align256(sizeof(double) * nb * parts);          // partials
+  if (!use_small(C, k)) s += align256(sizeof(float) * 2 * n);  // (m, s) per token
+  return s;
+}
+
+template <typename LT, typename AT>
+static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial, float* ms) {
+  const LT* z = (const LT*)a.logits;
+  const AT* A = (const AT*)a.credit_a;
+  if (use_small(a.C, a.k)) {
+    dim3 grid((unsigned)((a.n + kSmallThreads - 1) / kSmallThreads), (unsigned)a.nb);
+#define LOCA_SMALL(KB)                                                                              \
+  k_error_small<LT, AT, KB><<<grid, kSmallThreads, 0, a.stream>>>(                                  \
+      a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, A, a.a_bstride, G, a.y_out, a.y_bstride, a.e_out, \
+      partial, a.dev_info)
+    if (a.k <= 16) LOCA_SMALL(16);
+    else if (a.k <= 32) LOCA_SMALL(32);
+    else LOCA_SMALL(64);
+#undef LOCA_SMALL
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, grid.x, partial, a.mb_out, a.dev_info);
+  } else {
+    dim3 grid((unsigned)((a.n + kLargeTok - 1) / kLargeTok), (unsigned)a.nb);
+    k_error_large<LT, AT><<<grid, kLargeThreads, 0, a.stream>>>(
+        a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, A, a.a_bstride, G, a.y_out, a.y_bstride,
+        a.e_out ? ms : nullptr, partial, a.dev_info);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, grid.x, partial, a.mb_out, a.dev_info);
+    if (a.e_out) {
+      dim3 g2((unsigned)((a.C + 255) / 256 < 64 ? (a.C + 255) / 256 : 64), (unsigned)a.n);
+      k_error_write_e<LT><<<g2, 256, 0, a.stream>>>(a.n, a.C, z, a.ld_logits, a.labels, a.w, ms, a.e_out);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_error_targets(const ErrorArgs& a) {
+  char* p = a.ws;
+  double* G = (double*)p;
+  p += align256(sizeof(double) * a.nb * a.k * a.k);
+  double* partial = (double*)p;
+  const int64_t parts = use_small(a.C, a.k) ? (a.n + kSmallThreads - 1) / kSmallThreads : (a.n + kLargeTok - 1) / kLargeTok;
+  p += align256(sizeof(double) * a.nb * parts);
+  float* ms = use_small(a.C, a.k) ? nullptr : (float*)p;
+
+  k_fill_i32<<<1, 64, 0, a.stream>>>(a.dev_info, 1, INT32_MAX);
+  dim3 gg((unsigned)((a.k * a.k + 255) / 256), (unsigned)a.nb);
+  k_credit_gram<<<gg, 256, 0, a.stream>>>(a.k, a.d, a.credit_b, a.b_bstride, G);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const bool zb = a.logits_dtype == LOCA_BF16, ab = a.a_dtype == LOCA_BF16;
+  if (!zb && !ab) return dispatch_error<float, float>(a, G, partial, ms);
+  if (!zb && ab) return dispatch_error<float, uint16_t>(a, G, partial, ms);
+  if (zb && !ab) return dispatch_error<uint16_t, float>(a, G, partial, ms);
+  return dispatch_error<uint16_t, uint16_t>(a, G, partial, ms);
+}
+
+// ------------------------------------------------------------------ dense targets (tests)
+
+namespace {
+__global__ void k_dense_targets(int64_t n, int64_t k, int64_t d, const float* __restrict__ y,
+                                int64_t y_bstride, const loca_mb* __restrict__ mb,
+                                const float* __restrict__ B, int64_t b_bstride,
+                                float* __restrict__ T, int64_t t_bstride) {
+  const int64_t b = blockIdx.z;
+  const int64_t t = blockIdx.y;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= d) return;
+  const double eb = mb[b].eta_bar;
+  const float* yt = y + b * y_bstride + t * k;
+  const float* Bb = B + b * b_bstride;
+  double s = 0.0;
+  for (int64_t j = 0; j < k; ++j) s += (double)yt[j] * (double)Bb[j * d + i];
+  T[b * t_bstride + t * d + i] = (float)(-eb * s);
+}
+}  // namespace
+
+hipError_t launch_dense_targets(hipStream_t s, int64_t nb, int64_t n, int64_t k, int64_t d,
+                                const float* y, int64_t y_bstride, const loca_mb* mb,
+                                const float* credit_b, int64_t b_bstride, float* t_out,
+                                int64_t t_bstride) {
+  dim3 grid((unsigned)((d + 255) / 256), (unsigned)n, (unsigned)nb);
+  k_dense_targets<<<grid, 256, 0, s>>>(n, k, d, y, y_bstride, mb, credit_b, b_bstride, t_out, t_bstride);
+  return hipGetLastError();
+}
+
+}  // namespace loca

@@ -1,0 +1,446 @@
+// k_gram.hip -- streaming statistics of one micro-batch (rows a3, a4 of the step).
+//
+// Eq. 9 / Section S7 with the identity projection: S += X^T X and the
+// factored cross statistic K += -eta_bar X^T Y (Z = X^T T = K B~), where the
+// micro-batch's eta_bar (Eq. 10) needs ||X||_F^2, taken from the diagonal of
+// this micro-batch's own Gram tiles.
+//
+// bf16 mode: X is bf16, token-major (n x d).  Both MFMA operands of X^T X need
+// 8 consecutive tokens per lane, i.e. the strided direction of X.  Tiles of X
+// are copied to LDS in their natural [token][column] layout with 16-byte
+// loads/stores and read back transposed with ds_read_b64_tr_b16, which feeds
+// v_mfma_f32_32x32x16_bf16 directly.  Only tiles on or above the diagonal of S
+// are computed.  Y (fp32) enters the cross product as two bf16 columns
+// (hi = bf16(y), lo = bf16(y - hi)), so products stay exact and the sum of the
+// two halves carries ~16 bits of y.  Every output element is owned by one
+// workgroup and summed in a fixed order: results are deterministic.
+//
+// fp32 mode: X is fp32 and the statistics are fp64 (v_mfma_f64_16x16x4f64).
+#include "loca_common.h"
+
+namespace loca {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kBK = 32;  // tokens per pipeline stage (bf16)
+
+// upper-triangular tile index -> (I, J), J >= I, T tiles per side
+LOCA_DEV void upper_tile(int u, int T, int& I, int& J) {
+  int i = 0;
+  while (u >= T - i) { u -= T - i; ++i; }
+  I = i;
+  J = i + u;
+}
+
+// ------------------------------------------------------------------ bf16 tile staging
+
+// One stage = kBK token rows x BM columns of X starting at column c0.
+template <int BM>
+struct XStage {
+  static constexpr int kChunksPerRow = BM / 8;
+  static constexpr int kChunks = kBK * kChunksPerRow;
+  static constexpr int kPerThread = kChunks / kThreads;
+  uint4 r[kPerThread];
+
+  LOCA_DEV void load(const uint16_t* __restrict__ X, int64_t ldx, int64_t n, int64_t d, int64_t t0,
+                     int64_t c0) {
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int row = e / kChunksPerRow, ch = e % kChunksPerRow;
+      const int64_t t = t0 + row, col = c0 + 8 * ch;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (t < n) {
+        const uint16_t* p = X + t * ldx + col;
+        if (col + 8 <= d) {
+          v = *(const uint4*)p;
+        } else if (col < d) {
+          uint16_t h[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u) h[u] = (col + u < d) ? p[u] : (uint16_t)0;
+          v.x = h[0] | ((uint32_t)h[1] << 16);
+          v.y = h[2] | ((uint32_t)h[3] << 16);
+          v.z = h[4] | ((uint32_t)h[5] << 16);
+          v.w = h[6] | ((uint32_t)h[7] << 16);
+        }
+      }
+      r[q] = v;
+    }
+  }
+  LOCA_DEV void store(uint16_t* s, int ld) const {
+#pragma unroll
+    for (int q = 0; q < kPerThread; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int row = e / kChunksPerRow, ch = e % kChunksPerRow;
+      *(uint4*)(s + row * ld + 8 * ch) = r[q];
+    }
+  }
+};
+
+// ------------------------------------------------------------------ S += X^T X (bf16)
+
+// BM x BM tiles, 4 waves in a 2 x 2 grid of WM x WM wave tiles.
+template <int BM>
+__global__ __launch_bounds__(kThreads) void k_gram_bf16(int64_t n, int64_t d,
+                                                        const uint16_t* __restrict__ Xall, int64_t ldx,
+                                                        int64_t x_bstride, float* __restrict__ Sall,
+                                                        int64_t s_bstride, double* __restrict__ diag_part) {
+  constexpr int WM = BM / 2;
+  constexpr int NB = WM / 32;          // 32x32 MFMA blocks per wave side
+  constexpr int LDT = BM + 16;         // padded row (conflict-free transpose reads)
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][kBK * LDT];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][kBK * LDT];
+  __shared__ double sred[kThreads / 64];
+
+  const int T = (int)((d + BM - 1) / BM);
+  int I, J;
+  upper_tile(blockIdx.x, T, I, J);
+  const bool diag = (I == J);
+  const int64_t b = blockIdx.y;
+  const uint16_t* X = Xall + b * x_bstride;
+  float* S = Sall + b * s_bstride;
+
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wi = wid >> 1, wj = wid & 1;
+  const bool active = !(diag && wi > wj);  // strictly-lower wave tile of a diagonal tile
+
+  f32x16_t acc[NB][NB];
+#pragma unroll
+  for (int m = 0; m < NB; ++m)
+#pragma unroll
+    for (int q = 0; q < NB; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][q][r] = 0.f;
+
+  XStage<BM> ra, rb;
+  const int64_t cI = (int64_t)I * BM, cJ = (int64_t)J * BM;
+  const int nk = (int)((n + kBK - 1) / kBK);
+  ra.load(X, ldx, n, d, 0, cI);
+  if (!diag) rb.load(X, ldx, n, d, 0, cJ);
+  ra.store(sA[0], LDT);
+  if (!diag) rb.store(sB[0], LDT);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      ra.load(X, ldx, n, d, (int64_t)(kt + 1) * kBK, cI);
+      if (!diag) rb.load(X, ldx, n, d, (int64_t)(kt + 1) * kBK, cJ);
+    }
+    if (active) {
+      const uint16_t* tA = sA[cur];
+      const uint16_t* tB = diag ? sA[cur] : sB[cur];
+#pragma unroll
+      for (int ks = 0; ks < kBK; ks += 16) {
+        bf16x8_t fa[NB], fb[NB];
+#pragma unroll
+        for (int m = 0; m < NB; ++m) fa[m] = frag32_tr(tA, LDT, wi * WM + 32 * m, ks, lane);
+#pragma unroll
+        for (int q = 0; q < NB; ++q) fb[q] = frag32_tr(tB, LDT, wj * WM + 32 * q, ks, lane);
+#pragma unroll
+        for (int m = 0; m < NB; ++m)
+#pragma unroll
+          for (int q = 0; q < NB; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
+      }
+    }
+    if (kt + 1 < nk) {
+      ra.store(sA[cur ^ 1], LDT);
+      if (!diag) rb.store(sB[cur ^ 1], LDT);
+    }
+    __syncthreads();
+  }
+
+  double dsum = 0.0;
+  if (active) {
+#pragma unroll
+    for (int m = 0; m < NB; ++m)
+#pragma unroll
+      for (int q = 0; q < NB; ++q)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = cI + wi * WM + 32 * m + mfma32_row(lane, r);
+          const int64_t col = cJ + wj * WM + 32 * q + mfma32_col(lane);
+          if (row < d && col < d) {
+            S[row * d + col] += acc[m][q][r];
+            if (diag && row == col) dsum += (double)acc[m][q][r];
+          }
+        }
+  }
+  if (diag) {
+    const double tot = block_sum(dsum, sred);
+    if (threadIdx.x == 0) diag_part[b * T + I] = tot;
+  }
+}
+
+// ------------------------------------------------------------------ Kraw = X^T [Y_hi | Y_lo] (bf16)
+
+// Rows: a 256-column panel of X; columns: the 2k split columns of Y padded to YB.
+// 4 waves stacked along the rows (64 rows each).
+template <int YB>
+__global__ __launch_bounds__(kThreads) void k_cross_bf16(int64_t n, int64_t d, int64_t k,
+                                                         const uint16_t* __restrict__ Xall, int64_t ldx,
+                                                         int64_t x_bstride, const float* __restrict__ Yall,
+                                                         int64_t y_bstride, float* __restrict__ Kraw) {
+  constexpr int BM = 256;
+  constexpr int LDT = BM + 16;
+  constexpr int LDY = YB + 16;
+  constexpr int NQ = YB / 32;
+  __shared__ __attribute__((aligned(16))) uint16_t sA[2][kBK * LDT];
+  __shared__ __attribute__((aligned(16))) uint16_t sY[2][kBK * LDY];
+  const int64_t b = blockIdx.y;
+  const int I = blockIdx.x;
+  const uint16_t* X = Xall + b * x_bstride;
+  const float* Y = Yall + b * y_bstride;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t cI = (int64_t)I * BM;
+
+  f32x16_t acc[2][NQ];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][q][r] = 0.f;
+
+  XStage<BM> ra;
+  // Y staging: kBK rows x k floats, converted to hi/lo bf16 columns [0,k) and [k,2k)
+  auto load_y = [&](int64_t t0, int buf) {
+    for (int e = threadIdx.x; e < kBK * YB / 2; e += kThreads) {
+      const int row = e / (YB / 2), c = e % (YB / 2);
+      const int64_t t = t0 + row;
+      float v = (t < n && c < k) ? Y[t * k + c] : 0.f;
+      const uint16_t hi = f32_to_bf16(v);
+      const uint16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
+      if (c < k) {
+        sY[buf][row * LDY + c] = hi;
+        sY[buf][row * LDY + k + c] = lo;
+      } else if (c + k < YB) {
+        sY[buf][row * LDY + k + c] = 0;  // padding columns [2k, YB)
+      }
+    }
+  };
+  const int nk = (int)((n + kBK - 1) / kBK);
+  ra.load(X, ldx, n, d, 0, cI);
+  ra.store(sA[0], LDT);
+  load_y(0, 0);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) ra.load(X, ldx, n, d, (int64_t)(kt + 1) * kBK, cI);
+#pragma unroll
+    for (int ks = 0; ks < kBK; ks += 16) {
+      bf16x8_t fa[2], fb[NQ];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) fa[m] = frag32_tr(sA[cur], LDT, wid * 64 + 32 * m, ks, lane);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) fb[q] = frag32_tr(sY[cur], LDY, 32 * q, ks, lane);
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
+    }
+    if (kt + 1 < nk) {
+      ra.store(sA[cur ^ 1], LDT);
+      load_y((int64_t)(kt + 1) * kBK, cur ^ 1);
+    }
+    __syncthreads();
+  }
+  float* Kb = Kraw + b * d * 2 * k;
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = cI + wid * 64 + 32 * m + mfma32_row(lane, r);
+        const int64_t col = 32 * q + mfma32_col(lane);
+        if (row < d && col < 2 * k) Kb[row * 2 * k + col] = acc[m][q][r];
+      }
+}
+
+// ------------------------------------------------------------------ fp64 path (fp32 mode)
+
+// 64 x 64 tiles, 4 waves of 32 x 32 (2 x 2 blocks of 16 x 16), 16 tokens per stage.
+// Jobs [0, nS) are upper tiles of S (Q = X); jobs [nS, nS + nK) are tiles of
+// Kraw = X^T Y (Q = Y, k columns).
+constexpr int kBM64 = 64, kBK64 = 16, kLD64 = kBM64 + 1;
+
+__global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int64_t k,
+                                                       const float* __restrict__ Xall, int64_t ldx,
+                                                       int64_t x_bstride, const float* __restrict__ Yall,
+                                                       int64_t y_bstride, double* __restrict__ Sall,
+                                                       int64_t s_bstride, double* __restrict__ Kraw,
+                                                       double* __restrict__ diag_part, int nS) {
+  __shared__ double sP[kBK64 * kLD64];
+  __shared__ double sQ[kBK64 * kLD64];
+  __shared__ double sred[kThreads / 64];
+  const int64_t b = blockIdx.y;
+  const int T = (int)((d + kBM64 - 1) / kBM64);
+  const bool kjob = (int)blockIdx.x >= nS;
+  int I, J;
+  if (!kjob) {
+    upper_tile(blockIdx.x, T, I, J);
+  } else {
+    const int u = blockIdx.x - nS;
+    const int TK = (int)((k + kBM64 - 1) / kBM64);
+    I = u / TK;
+    J = u % TK;
+  }
+  const bool diag = !kjob && I == J;
+  const float* X = Xall + b * x_bstride;
+  const float* Y = Yall + b * y_bstride;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wi = wid >> 1, wj = wid & 1;
+  const int64_t cI = (int64_t)I * kBM64, cJ = (int64_t)J * kBM64;
+  const int64_t qcols = kjob ? k : d;
+
+  f64x4_t acc[2][2];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int q = 0; q < 2; ++q) acc[m][q] = (f64x4_t){0.0, 0.0, 0.0, 0.0};
+
+  for (int64_t t0 = 0; t0 < n; t0 += kBK64) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < kBK64 * kBM64; e += kThreads) {
+      const int row = e / kBM64, c = e % kBM64;
+      const int64_t t = t0 + row;
+      const int64_t ci = cI + c, cj = cJ + c;
+      sP[row * kLD64 + c] = (t < n && ci < d) ? (double)X[t * ldx + ci] : 0.0;
+      double qv = 0.0;
+      if (t < n && cj < qcols) qv = kjob ? (double)Y[t * k + cj] : (double)X[t * ldx + cj];
+      sQ[row * kLD64 + c] = qv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < kBK64; ks += 4) {
+      double fa[2], fb[2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) fa[m] = sP[(ks + (lane >> 4)) * kLD64 + wi * 32 + 16 * m + (lane & 15)];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) fb[q] = sQ[(ks + (lane >> 4)) * kLD64 + wj * 32 + 16 * q + (lane & 15)];
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) acc[m][q] = mfma_f64(fa[m], fb[q], acc[m][q]);
+    }
+  }
+  double dsum = 0.0;
+  double* S = Sall + b * s_bstride;
+  double* Kb = Kraw + b * d * k;
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t row = cI + wi * 32 + 16 * m + (lane >> 4) + 4 * r;
+        const int64_t col = cJ + wj * 32 + 16 * q + (lane & 15);
+        if (row < d && col < qcols) {
+          if (kjob) {
+            Kb[row * k + col] = acc[m][q][r];
+          } else {
+            S[row * d + col] += acc[m][q][r];
+            if (diag && row == col) dsum += acc[m][q][r];
+          }
+        }
+      }
+  if (diag) {
+    const double tot = block_sum(dsum, sred);
+    if (threadIdx.x == 0) diag_part[b * T + I] = tot;
+  }
+}
+
+// ------------------------------------------------------------------ finalize: eta_bar and K
+
+template <typename AccT>
+__global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, const double* __restrict__ diag_part,
+                                 loca_mb* __restrict__ mb, double eta, const AccT* __restrict__ Kraw, int split,
+                                 AccT* __restrict__ Kall, int64_t k_bstride) {
+  const int64_t b = blockIdx.y;
+  double sx = 0.0;
+  for (int i = 0; i < ntile; ++i) sx += diag_part[b * ntile + i];
+  const double sq = mb[b].sum_q2;
+  const double eb = (sq > 0.0) ? eta * sqrt(sx / sq) : 0.0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    mb[b].sum_x2 = sx;
+    mb[b].eta_bar = eb;
+    mb[b].n = n;
+  }
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= d * k) return;
+  const int64_t i = e / k, c = e % k;
+  AccT* K = Kall + b * k_bstride;
+  const int64_t w = split ? 2 * k : k;
+  const AccT* kr = Kraw + b * d * w + i * w;
+  double v = (double)kr[c];
+  if (split) v += (double)kr[c + k];
+  K[i * k + c] = (AccT)((double)K[i * k + c] - eb * v);
+}
+
+}  // namespace
+
+size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc) {
+  (void)n;
+  const int64_t T = acc == LOCA_F64 ? (d + kBM64 - 1) / kBM64 : (d + 127) / 128;
+  const int64_t Tmax = (d + kBM64 - 1) / kBM64;  // generous: covers every tile size used
+  size_t s = align256(sizeof(double) * nb * (T > Tmax ? T : Tmax));
+  if (acc == LOCA_F64) s += align256(sizeof(double) * nb * d * k);
+  else s += align256(sizeof(float) * nb * d * 2 * k);
+  return s;
+}
+
+hipError_t launch_accumulate_stats(const StatsArgs& a) {
+  const int64_t Tmax = (a.d + kBM64 - 1) / kBM64;
+  double* diag_part = (double*)a.ws;
+  char* p = a.ws + align256(sizeof(double) * a.nb * Tmax);
+  if (a.acc == LOCA_F64) {
+    double* Kraw = (double*)p;
+    const int T = (int)((a.d + kBM64 - 1) / kBM64);
+    const int nS = T * (T + 1) / 2;
+    const int nK = T * (int)((a.k + kBM64 - 1) / kBM64);
+    dim3 grid((unsigned)(nS + nK), (unsigned)a.nb);
+    k_gram_f64<<<grid, kThreads, 0, a.stream>>>(a.n, a.d, a.k, (const float*)a.x, a.ldx, a.x_bstride, a.y,
+                                                a.y_bstride, (double*)a.S, a.s_bstride, Kraw, diag_part, nS);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
+    k_stats_finalize<double><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 0,
+                                                       (double*)a.K, a.k_bstride);
+    return hipGetLastError();
+  }
+  float* Kraw = (float*)p;
+  const uint16_t* X = (const uint16_t*)a.x;
+  // Tile size: 256 x 256 when the matrix is wide enough to fill the GPU with such tiles.
+  const bool big = a.d >= 1024;
+  const int BM = big ? 256 : 128;
+  const int T = (int)((a.d + BM - 1) / BM);
+  dim3 grid((unsigned)(T * (T + 1) / 2), (unsigned)a.nb);
+  if (big)
+    k_gram_bf16<256><<<grid, kThreads, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
+                                                      diag_part);
+  else
+    k_gram_bf16<128><<<grid, kThreads, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
+                                                      diag_part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 gc((unsigned)((a.d + 255) / 256), (unsigned)a.nb);
+  const int64_t w2 = 2 * a.k;
+  if (w2 <= 32)
+    k_cross_bf16<32><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+  else if (w2 <= 64)
+    k_cross_bf16<64><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+  else if (w2 <= 128)
+    k_cross_bf16<128><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+  else
+    k_cross_bf16<256><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
+  k_stats_finalize<float><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
+                                                    (float*)a.K, a.k_bstride);
+  return hipGetLastError();
+}
+
+}  // namespace loca

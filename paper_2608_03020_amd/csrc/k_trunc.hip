@@ -1,0 +1,509 @@
+// k_trunc.hip -- rank-r_a truncation (row a6) and the paper's projected fit (row a5, Eqs. 6-9).
+//
+// Truncation (Lemma S5.2, Eckart-Young) of W = M R with M: d x kp, R: kp x d,
+// without forming W: with the small Gram matrices Gm = M^T M, Gb = R R^T
+// (kp x kp, fp64) and Gb = Vb diag(lb) Vb^T, H = diag(sqrt(lb)),
+//   W = (M Vb H)(H^{-1} Vb^T R)  where H^{-1} Vb^T R has orthonormal rows,
+// so the singular values of W are those of P = M Vb H, whose right factor
+// comes from the eigendecomposition H Vb^T Gm Vb H = Vp diag(s^2) Vp^T.  Then
+//   U = M Vb H Vp diag(1/s),   V = R^T Vb H^{-1} Vp,
+//   a_out = U_r^T = Ca M^T,    b_out = V_r diag(s_r) = R^T Cb
+// with small Ca (r x kp) and Cb (kp x r).  Both eigendecompositions are
+// cyclic Jacobi in fp64 inside one workgroup (kp <= 64).
+#include "loca_common.h"
+
+namespace loca {
+
+namespace {
+
+constexpr int kT = 256;
+constexpr int kMaxKp = 64;
+
+// Gm = M^T M and Gb = R R^T, fp64.  blockIdx.x = matrix, blockIdx.y = 0 (M) / 1 (R).
+__global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const float* __restrict__ M,
+                                                    int64_t m_bstride, const float* __restrict__ R,
+                                                    int64_t r_bstride, int64_t r_group, double* __restrict__ Gm,
+                                                    double* __restrict__ Gb) {
+  constexpr int kRows = 32;
+  __shared__ double sX[kRows][kMaxKp + 1];
+  const int64_t mi = blockIdx.x;
+  const bool isR = blockIdx.y == 1;
+  const float* Mm = M + mi * m_bstride;
+  const float* Rm = R + (mi / r_group) * r_bstride;
+  const int npair = (int)(kp * kp);
+  double acc[(kMaxKp * kMaxKp) / kT];
+#pragma unroll
+  for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) acc[q] = 0.0;
+  for (int64_t i0 = 0; i0 < d; i0 += kRows) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < kRows * kMaxKp; e += kT) {
+      const int r = e / kMaxKp, c = e % kMaxKp;
+      const int64_t i = i0 + r;
+      double v = 0.0;
+      if (i < d && c < kp) v = isR ? (double)Rm[c * d + i] : (double)Mm[i * kp + c];
+      sX[r][c] = v;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) {
+      const int e = threadIdx.x + kT * q;
+      if (e < npair) {
+        const int a = e / (int)kp, c = e % (int)kp;
+        double s = acc[q];
+        for (int r = 0; r < kRows; ++r) s += sX[r][a] * sX[r][c];
+        acc[q] = s;
+      }
+    }
+  }
+  double* G = (isR ? Gb : Gm) + mi * kp * kp;
+#pragma unroll
+  for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) {
+    const int e = threadIdx.x + kT * q;
+    if (e < npair) G[e] = acc[q];
+  }
+}
+
+// Cyclic Jacobi eigendecomposition of the symmetric n x n matrix A (LDS, row stride ld),
+// eigenvectors accumulated into V (columns).  Round-robin pair ordering: each round
+// rotates n/2 disjoint pairs.  n must be even (callers pad with a zero row/column).
+LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* pairs, double* red) {
+  const int tid = threadIdx.x;
+  for (int e = tid; e < n * ld; e += kT) V[e] = ((e / ld) == (e % ld)) ? 1.0 : 0.0;
+  __syncthreads();
+  for (int sweep = 0; sweep < 40; ++sweep) {
+    // convergence test: off-diagonal mass vs total
+    double off = 0.0, tot = 0.0;
+    for (int e = tid; e < n * n; e += kT) {
+      const int i = e / n, j = e % n;
+      const double v = A[i * ld + j];
+      tot += v * v;
+      if (i != j) off += v * v;
+    }
+    const double offs = block_sum(off, red);
+    __syncthreads();
+    const double tots = block_sum(tot, red + 4);
+    if (tid == 0) red[8] = (offs <= 1e-30 * tots || tots == 0.0) ? 1.0 : 0.0;
+    __syncthreads();
+    if (red[8] != 0.0) break;
+    for (int round = 0; round < n - 1; ++round) {
+      // tournament pairing: positions 0..n-1, position 0 fixed, others rotate
+      if (tid < n / 2) {
+        auto pos = [&](int x) { return x == 0 ? 0 : 1 + ((x - 1 + round) % (n - 1)); };
+        int p = pos(tid), q = pos(n - 1 - tid);
+        if (p > q) { int t = p; p = q; q = t; }
+        pairs[2 * tid] = p;
+        pairs[2 * tid + 1] = q;
+        const double apq = A[p * ld + q], app = A[p * ld + p], aqq = A[q * ld + q];
+        double c = 1.0, s = 0.0;
+        if (fabs(apq) > 1e-300 && fabs(apq) > 1e-18 * sqrt(fabs(app * aqq))) {
+          const double tau = (aqq - app) / (2.0 * apq);
+          const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+          c = 1.0 / sqrt(1.0 + t * t);
+          s = t * c;
+        }
+        cs[2 * tid] = c;
+        cs[2 * tid + 1] = s;
+      }
+      __syncthreads();
+      // A <- A J (columns), V <- V J
+      for (int e = tid; e < (n / 2) * n; e += kT) {
+        const int pr = e / n, i = e % n;
+        const int p = pairs[2 * pr], q = pairs[2 * pr + 1];
+        const double c = cs[2 * pr], s = cs[2 * pr + 1];
+        const double aip = A[i * ld + p], aiq = A[i * ld + q];
+        A[i * ld + p] = c * aip - s * aiq;
+        A[i * ld + q] = s * aip + c * aiq;
+        const double vip = V[i * ld + p], viq = V[i * ld + q];
+        V[i * ld + p] = c * vip - s * viq;
+        V[i * ld + q] = s * vip + c * viq;
+      }
+      __syncthreads();
+      // A <- J^T A (rows)
+      for (int e = tid; e < (n / 2) * n; e += kT) {
+        const int pr = e / n, j = e % n;
+        const int p = pairs[2 * pr], q = pairs[2 * pr + 1];
+        const double c = cs[2 * pr], s = cs[2 * pr + 1];
+        const double apj = A[p * ld + j], aqj = A[q * ld + j];
+        A[p * ld + j] = c * apj - s * aqj;
+        A[q * ld + j] = s * apj + c * aqj;
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// One workgroup per matrix: eigendecompositions and the small factors Ca, Cb.
+__global__ __launch_bounds__(kT) void k_trunc_core(int64_t kp, int64_t r_a, const double* __restrict__ Gm_all,
+                                                   const double* __restrict__ Gb_all, double* __restrict__ Ca_all,
+                                                   double* __restrict__ Cb_all, float* __restrict__ sigma_out,
+                                                   int64_t sigma_bstride) {
+  constexpr int LD = kMaxKp + 1;
+  __shared__ double sA[kMaxKp * LD];
+  __shared__ double sV[kMaxKp * LD];
+  __shared__ double sT[kMaxKp * LD];
+  __shared__ double sH[kMaxKp], sHi[kMaxKp], sEig[kMaxKp];
+  __shared__ int sOrd[kMaxKp];
+  __shared__ double cs[kMaxKp];
+  __shared__ int pairs[kMaxKp];
+  __shared__ double red[16];
+  const int64_t mi = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int n = (int)kp + ((int)kp & 1);  // even size for the tournament ordering
+  const double* Gm = Gm_all + mi * kp * kp;
+  const double* Gb = Gb_all + mi * kp * kp;
+  // 1. Gb = Vb diag(lb) Vb^T
+  for (int e = tid; e < n * LD; e += kT) {
+    const int i = e / LD, j = e % LD;
+    sA[e] = (i < kp && j < kp) ? Gb[i * kp + j] : 0.0;
+  }
+  __syncthreads();
+  jacobi_eig(sA, sV, n, LD, cs, pairs, red);
+  __syncthreads();
+  if (tid == 0) {
+    double lmax = 0.0;
+    for (int j = 0; j < kp; ++j) lmax = fmax(lmax, sA[j * LD + j]);
+    red[12] = lmax;
+  }
+  __syncthreads();
+  for (int j = tid; j < kp; j += kT) {
+    const double lb = sA[j * LD + j];
+    const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
+    sH[j] = keep ? sqrt(lb) : 0.0;
+    sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+  }
+  // keep Vb in sT
+  for (int e = tid; e < n * LD; e += kT) sT[e] = sV[e];
+  __syncthreads();
+  // 2. P^T P = H Vb^T Gm Vb H: first sA = Gm Vb
+  for (int e = tid; e < (int)(kp * kp); e += kT) {
+    const int i = e / (int)kp, j = e % (int)kp;
+    double s = 0.0;
+    for (int c = 0; c < kp; ++c) s += Gm[i * kp + c] * sT[c * LD + j];
+    sV[i * LD + j] = s;
+  }
+  __syncthreads();
+  for (int e = tid; e < n * n; e += kT) {
+    const int i = e / n, j = e % n;
+    double s = 0.0;
+    if (i < kp && j < kp) {
+      for (int c = 0; c < kp; ++c) s += sT[c * LD + i] * sV[c * LD + j];
+      s *= sH[i] * sH[j];
+    }
+    sA[i * LD + j] = s;
+  }
+  __syncthreads();
+  // symmetrise against rounding
+  for (int e = tid; e < n * n; e += kT) {
+    const int i = e / n, j = e % n;
+    if (i < j) {
+      const double v = 0.5 * (sA[i * LD + j] + sA[j * LD + i]);
+      sA[i * LD + j] = v;
+      sA[j * LD + i] = v;
+    }
+  }
+  __syncthreads();
+  jacobi_eig(sA, sV, n, LD, cs, pairs, red);  // sV = Vp
+  __syncthreads();
+  if (tid == 0) {
+    // order by decreasing eigenvalue (insertion sort on indices)
+    for (int j = 0; j < kp; ++j) { sEig[j] = sA[j * LD + j]; sOrd[j] = j; }
+    for (int i = 1; i < kp; ++i) {
+      const int key = sOrd[i];
+      int j = i - 1;
+      while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
+      sOrd[j + 1] = key;
+    }
+  }
+  __syncthreads();
+  const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
+  for (int j = tid; j < kp; j += kT) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
+  // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
+  double* Ca = Ca_all + mi * r_a * kp;
+  double* Cb = Cb_all + mi * kp * r_a;
+  for (int e = tid; e < (int)(r_a * kp); e += kT) {
+    const int a = e / (int)kp, c = e % (int)kp;
+    const int col = sOrd[a];
+    const double sa = sqrt(fmax(sEig[col], 0.0));
+    double u = 0.0, v = 0.0;
+    for (int x = 0; x < kp; ++x) {
+      u += sT[c * LD + x] * sH[x] * sV[x * LD + col];
+      v += sT[c * LD + x] * sHi[x] * sV[x * LD + col];
+    }
+    const bool live = sa > 1e-30 * s1 && sa > 0.0;
+    Ca[a * kp + c] = live ? u / sa : 0.0;
+    Cb[c * r_a + a] = live ? v * sa : 0.0;
+  }
+}
+
+// a_out[a][i] = sum_c Ca[a][c] M[i][c];  b_out[i][a] = sum_c R[c][i] Cb[c][a]
+__global__ __launch_bounds__(kT) void k_trunc_apply(int64_t d, int64_t kp, int64_t r_a, const float* __restrict__ M,
+                                                    int64_t m_bstride, const float* __restrict__ R, int64_t r_bstride,
+                                                    int64_t r_group, const double* __restrict__ Ca_all,
+                                                    const double* __restrict__ Cb_all, float* __restrict__ a_out,
+                                                    int64_t a_bstride, float* __restrict__ b_out, int64_t b_bstride) {
+  __shared__ double sCa[kMaxKp * kMaxKp];
+  __shared__ double sCb[kMaxKp * kMaxKp];
+  const int64_t mi = blockIdx.y;
+  for (int e = threadIdx.x; e < (int)(r_a * kp); e += kT) {
+    sCa[e] = Ca_all[mi * r_a * kp + e];
+    sCb[e] = Cb_all[mi * kp * r_a + e];
+  }
+  __syncthreads();
+  const int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x;
+  if (i >= d) return;
+  const float* Mi = M + mi * m_bstride + i * kp;
+  const float* Rm = R + (mi / r_group) * r_bstride;
+  float mrow[kMaxKp], rcol[kMaxKp];
+#pragma unroll
+  for (int c = 0; c < kMaxKp; ++c) {
+    mrow[c] = (c < kp) ? Mi[c] : 0.f;
+    rcol[c] = (c < kp) ? Rm[c * d + i] : 0.f;
+  }
+  for (int a = 0; a < r_a; ++a) {
+    double sa = 0.0, sb = 0.0;
+#pragma unroll
+    for (int c = 0; c < kMaxKp; ++c) {
+      if (c < kp) {
+        sa += sCa[a * kp + c] * (double)mrow[c];
+        sb += (double)rcol[c] * sCb[c * r_a + a];
+      }
+    }
+    a_out[mi * a_bstride + a * d + i] = (float)sa;
+    b_out[mi * b_bstride + i * r_a + a] = (float)sb;
+  }
+}
+
+// out[i][j] = sum_c L(i, c) R(c, j) with general strides (fp64 accumulation).
+__global__ void k_lowrank_product(int64_t rows, int64_t cols, int64_t kk, const float* __restrict__ L,
+                                  int64_t l_bstride, int64_t l_si, int64_t l_sc, const float* __restrict__ R,
+                                  int64_t r_bstride, int64_t r_group, int64_t r_sc, int64_t r_sj,
+                                  float* __restrict__ out, int64_t out_bstride) {
+  const int64_t mi = blockIdx.z;
+  const int64_t i = blockIdx.y;
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= cols) return;
+  const float* Lm = L + mi * l_bstride + i * l_si;
+  const float* Rm = R + (mi / r_group) * r_bstride + j * r_sj;
+  double s = 0.0;
+  for (int64_t c = 0; c < kk; ++c) s += (double)Lm[c * l_sc] * (double)Rm[c * r_sc];
+  out[mi * out_bstride + i * cols + j] = (float)s;
+}
+
+__global__ void k_fill_zero(int32_t* p, int64_t cnt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < cnt) p[i] = 0;
+}
+
+}  // namespace
+
+hipError_t launch_lowrank_product(hipStream_t s, int64_t nmat, int64_t rows, int64_t cols, int64_t kk,
+                                  const float* L, int64_t l_bstride, int64_t l_ld, const float* R,
+                                  int64_t r_bstride, int64_t r_group, int64_t r_ld, float* out,
+                                  int64_t out_bstride) {
+  dim3 grid((unsigned)((cols + 255) / 256), (unsigned)rows, (unsigned)nmat);
+  k_lowrank_product<<<grid, 256, 0, s>>>(rows, cols, kk, L, l_bstride, l_ld, 1, R, r_bstride, r_group, r_ld, 1, out,
+                                         out_bstride);
+  return hipGetLastError();
+}
+
+size_t lowrank_truncate_ws(int64_t nm, int64_t d, int64_t kp, int64_t r_a) {
+  (void)d;
+  size_t s = 2 * align256(sizeof(double) * nm * kp * kp);
+  s += 2 * align256(sizeof(double) * nm * kp * r_a);
+  return s;
+}
+
+hipError_t launch_lowrank_truncate(const TruncArgs& a) {
+  char* p = a.ws;
+  double* Gm = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.kp);
+  double* Gb = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.kp);
+  double* Ca = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.r_a);
+  double* Cb = (double*)p;
+  k_fill_zero<<<(unsigned)((a.nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, a.nm);
+  k_small_grams<<<dim3((unsigned)a.nm, 2), kT, 0, a.stream>>>(a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride,
+                                                               a.r_group, Gm, Gb);
+  k_trunc_core<<<(unsigned)a.nm, kT, 0, a.stream>>>(a.kp, a.r_a, Gm, Gb, Ca, Cb, a.sigma_out, a.sigma_bstride);
+  k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm), kT, 0, a.stream>>>(
+      a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
+      a.b_bstride);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !a.w_dense_out) return e;
+  // W_r[i][j] = sum_a a_out[a][i] b_out[j][a]
+  dim3 grid((unsigned)((a.d + 255) / 256), (unsigned)a.d, (unsigned)a.nm);
+  k_lowrank_product<<<grid, 256, 0, a.stream>>>(a.d, a.d, a.r_a, a.a_out, a.a_bstride, 1, a.d, a.b_out, a.b_bstride,
+                                                1, 1, a.r_a, a.w_dense_out, a.w_bstride);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ projected form (Eqs. 6-9)
+
+namespace {
+
+// T1[b][i][a] = sum_j S_sym[i][j] PA[a][j]  (fp64, d x r_a); S_sym from the upper triangle.
+template <typename ST>
+__global__ void k_proj_sa(int64_t d, int64_t r_a, const ST* __restrict__ S, int64_t s_bstride,
+                          const float* __restrict__ PA, int64_t pa_bstride, double* __restrict__ T1) {
+  const int64_t b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= d * r_a) return;
+  const int64_t i = e / r_a, a = e % r_a;
+  const ST* Sb = S + b * s_bstride;
+  const float* P = PA + b * pa_bstride + a * d;
+  double s = 0.0;
+  for (int64_t j = 0; j < i; ++j) s += (double)Sb[j * d + i] * (double)P[j];
+  for (int64_t j = i; j < d; ++j) s += (double)Sb[i * d + j] * (double)P[j];
+  T1[b * d * r_a + e] = s;
+}
+
+// G[b] = PA T1 (r_a x r_a) and AK[b] = PA K (r_a x k), fp64.
+template <typename ST>
+__global__ void k_proj_small(int64_t d, int64_t k, int64_t r_a, const float* __restrict__ PA, int64_t pa_bstride,
+                             const double* __restrict__ T1, const ST* __restrict__ K, int64_t k_bstride,
+                             double* __restrict__ G, double* __restrict__ AK, float* __restrict__ g_out) {
+  const int64_t b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const float* P = PA + b * pa_bstride;
+  if (e < r_a * r_a) {
+    const int64_t a = e / r_a, c = e % r_a;
+    double s = 0.0;
+    for (int64_t i = 0; i < d; ++i) s += (double)P[a * d + i] * T1[b * d * r_a + i * r_a + c];
+    G[b * r_a * r_a + e] = s;
+    if (g_out) g_out[b * r_a * r_a + e] = (float)s;
+  } else if (e < r_a * r_a + r_a * k) {
+    const int64_t f = e - r_a * r_a;
+    const int64_t a = f / k, c = f % k;
+    const ST* Kb = K + b * k_bstride;
+    double s = 0.0;
+    for (int64_t i = 0; i < d; ++i) s += (double)P[a * d + i] * (double)Kb[i * k + c];
+    AK[b * r_a * k + f] = s;
+  }
+}
+
+// Per (block, lam): Cholesky of G + lam I in LDS, then for 32 rows i:
+// C[i] = B_cur[i] G + sum_c B~[c][i] AK[:, c]  and  B*[i] = C[i] (G + lam I)^{-1}.
+constexpr int kPR = 32;
+__global__ __launch_bounds__(kT) void k_proj_solve(int64_t d, int64_t k, int64_t r_a, const double* __restrict__ G,
+                                                   const double* __restrict__ AK, const float* __restrict__ Bt,
+                                                   int64_t b_bstride, const float* __restrict__ Bc,
+                                                   int64_t bc_bstride, const double* __restrict__ lam, int nl,
+                                                   float* __restrict__ out, int64_t bo_bstride,
+                                                   int32_t* __restrict__ dev_info) {
+  constexpr int LD = kMaxKp + 1;
+  __shared__ double sL[kMaxKp * LD];
+  __shared__ double sG[kMaxKp * LD];
+  __shared__ double sX[kPR * LD];
+  const int64_t mi = blockIdx.y;
+  const int64_t b = mi / nl;
+  const int l = (int)(mi % nl);
+  const int tid = threadIdx.x;
+  const int ra = (int)r_a;
+  for (int e = tid; e < ra * ra; e += kT) {
+    const int i = e / ra, j = e % ra;
+    const double g = G[b * r_a * r_a + e];
+    sG[i * LD + j] = g;
+    sL[i * LD + j] = g + (i == j ? lam[l] : 0.0);
+  }
+  __syncthreads();
+  // lower Cholesky in place (column by column)
+  for (int j = 0; j < ra; ++j) {
+    if (tid == 0) {
+      const double piv = sL[j * LD + j];
+      if (!(piv > 0.0) && blockIdx.x == 0) atomicCAS(&dev_info[mi], 0, j + 1);
+      sL[j * LD + j] = sqrt(piv);
+    }
+    __syncthreads();
+    for (int i = j + 1 + tid; i < ra; i += kT) sL[i * LD + j] /= sL[j * LD + j];
+    __syncthreads();
+    for (int e = tid; e < (ra - j - 1) * (ra - j - 1); e += kT) {
+      const int i = j + 1 + e / (ra - j - 1), c = j + 1 + e % (ra - j - 1);
+      if (c <= i) sL[i * LD + c] -= sL[i * LD + j] * sL[c * LD + j];
+    }
+    __syncthreads();
+  }
+  // rows of C
+  const int64_t i0 = (int64_t)blockIdx.x * kPR;
+  const float* Btb = Bt + b * b_bstride;
+  const double* AKb = AK + b * r_a * k;
+  for (int e = tid; e < kPR * ra; e += kT) {
+    const int r = e / ra, a = e % ra;
+    const int64_t i = i0 + r;
+    double s = 0.0;
+    if (i < d) {
+      for (int64_t c = 0; c < k; ++c) s += (double)Btb[c * d + i] * AKb[a * k + c];
+      if (Bc) {
+        const float* Bci = Bc + b * bc_bstride + i * r_a;
+        for (int c = 0; c < ra; ++c) s += (double)Bci[c] * sG[c * LD + a];
+      }
+    }
+    sX[r * LD + a] = s;
+  }
+  __syncthreads();
+  // solve x (L L^T) = C row-wise: L^T-transposed system per row; one thread per row
+  if (tid < kPR) {
+    double* x = sX + tid * LD;
+    for (int a = 0; a < ra; ++a) {  // forward: L y = c
+      double v = x[a];
+      for (int c = 0; c < a; ++c) v -= sL[a * LD + c] * x[c];
+      x[a] = v / sL[a * LD + a];
+    }
+    for (int a = ra - 1; a >= 0; --a) {  // backward: L^T z = y
+      double v = x[a];
+      for (int c = a + 1; c < ra; ++c) v -= sL[c * LD + a] * x[c];
+      x[a] = v / sL[a * LD + a];
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < kPR * ra; e += kT) {
+    const int r = e / ra, a = e % ra;
+    const int64_t i = i0 + r;
+    if (i < d) out[mi * bo_bstride + i * r_a + a] = (float)sX[r * LD + a];
+  }
+}
+
+struct Lams8 {
+  double v[8];
+};
+__global__ void k_set_lams8(Lams8 l, double* out, int cnt) {
+  if ((int)threadIdx.x < cnt) out[threadIdx.x] = l.v[threadIdx.x];
+}
+
+}  // namespace
+
+size_t projected_ws(int64_t nb, int64_t d, int64_t k, int64_t r_a, int64_t n_lambda) {
+  (void)n_lambda;
+  size_t s = align256(sizeof(double) * nb * d * r_a);  // T1
+  s += align256(sizeof(double) * nb * r_a * r_a);      // G
+  s += align256(sizeof(double) * nb * r_a * k);        // AK
+  s += 256;                                            // lambdas
+  return s;
+}
+
+hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
+  char* p = a.ws;
+  double* T1 = (double*)p; p += align256(sizeof(double) * a.nb * a.d * a.r_a);
+  double* G = (double*)p; p += align256(sizeof(double) * a.nb * a.r_a * a.r_a);
+  double* AK = (double*)p; p += align256(sizeof(double) * a.nb * a.r_a * a.k);
+  double* dlam = (double*)p;
+  Lams8 l8;
+  for (int i = 0; i < 8; ++i) l8.v[i] = (i < a.n_lambda) ? a.lambdas[i] : 0.0;
+  k_set_lams8<<<1, 64, 0, a.stream>>>(l8, dlam, (int)a.n_lambda);
+  const int64_t nm = a.nb * a.n_lambda;
+  k_fill_zero<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
+  dim3 g1((unsigned)((a.d * a.r_a + 255) / 256), (unsigned)a.nb);
+  dim3 g2((unsigned)((a.r_a * a.r_a + a.r_a * a.k + 255) / 256), (unsigned)a.nb);
+  if (a.acc == LOCA_F64) {
+    k_proj_sa<double><<<g1, 256, 0, a.stream>>>(a.d, a.r_a, (const double*)a.S, a.s_bstride, a.proj_a, a.pa_bstride, T1);
+    k_proj_small<double><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1, (const double*)a.K,
+                                                   a.k_bstride, G, AK, a.g_out);
+  } else {
+    k_proj_sa<float><<<g1, 256, 0, a.stream>>>(a.d, a.r_a, (const float*)a.S, a.s_bstride, a.proj_a, a.pa_bstride, T1);
+    k_proj_small<float><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1, (const float*)a.K,
+                                                  a.k_bstride, G, AK, a.g_out);
+  }
+  dim3 g3((unsigned)((a.d + kPR - 1) / kPR), (unsigned)nm);
+  k_proj_solve<<<g3, kT, 0, a.stream>>>(a.d, a.k, a.r_a, G, AK, a.credit_b, a.b_bstride, a.b_cur, a.bc_bstride, dlam,
+                                        (int)a.n_lambda, a.b_out, a.bo_bstride, a.dev_info);
+  return hipGetLastError();
+}
+
+}  // namespace loca

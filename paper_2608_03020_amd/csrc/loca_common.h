@@ -1,0 +1,190 @@
+// loca_common.h -- device types and helpers shared by the libloca kernels (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/loca.h"
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+
+#define LOCA_LDS __attribute__((address_space(3)))
+#define LOCA_DEV __device__ __forceinline__
+
+namespace loca {
+
+constexpr int kWave = 64;
+
+// ------------------------------------------------------------------ bf16 <-> f32
+
+LOCA_DEV float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+// round to nearest even (inputs here are finite)
+LOCA_DEV uint16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T> LOCA_DEV float load_as_f32(const T* p);
+template <> LOCA_DEV float load_as_f32<float>(const float* p) { return *p; }
+template <> LOCA_DEV float load_as_f32<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
+
+// ------------------------------------------------------------------ reductions
+
+LOCA_DEV double wave_sum(double v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+  return v;  // valid in lane 0
+}
+LOCA_DEV float wave_sum(float v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, kWave);
+  return v;
+}
+LOCA_DEV float wave_max(float v) {
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, kWave));
+  return v;  // valid in all lanes
+}
+
+// Deterministic block sum (fixed tree).  `scratch` has blockDim.x/64 entries.
+template <typename T>
+LOCA_DEV T block_sum(T v, T* scratch) {
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  v = wave_sum(v);
+  __syncthreads();
+  if (lane == 0) scratch[wid] = v;
+  __syncthreads();
+  T r = 0;
+  if (threadIdx.x == 0)
+    for (int i = 0; i < nw; ++i) r += scratch[i];
+  return r;  // valid in thread 0
+}
+
+// ------------------------------------------------------------------ LDS transpose read (gfx950)
+// ds_read_b64_tr_b16: within each 16-lane group the four 8-byte chunks given by
+// lanes 4r..4r+3 form row r of a 4 x 16 block of 16-bit values; lane c of the
+// group receives column c (rows 0..3).
+LOCA_DEV s16x4_t lds_read_tr16(const uint16_t* lds_ptr) {
+  typedef LOCA_LDS s16x4_t lds_v4;
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4*)(LOCA_LDS void*)lds_ptr);
+}
+
+// MFMA operand of v_mfma_f32_32x32x16_bf16 from a K-major LDS tile
+// tile[k][col] (row stride ld elements, ld % 4 == 0): the operand of lane l is
+// the 8 values tile[ks + 8*(l/32) + e][c0 + l%32], e = 0..7.
+LOCA_DEV bf16x8_t frag32_tr(const uint16_t* tile, int ld, int c0, int ks, int lane) {
+  const int g = lane >> 4, w = lane & 15;
+  const int col = c0 + 16 * (g & 1) + 4 * (w & 3);
+  const int row = ks + 8 * (g >> 1) + (w >> 2);
+  s16x4_t lo = lds_read_tr16(tile + row * ld + col);
+  s16x4_t hi = lds_read_tr16(tile + (row + 4) * ld + col);
+  typedef short s16x8_t __attribute__((ext_vector_type(8)));
+  s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+LOCA_DEV f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Result element r of lane l of a 32x32 MFMA block: row, col within the block.
+LOCA_DEV int mfma32_row(int lane, int r) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
+LOCA_DEV int mfma32_col(int lane) { return lane & 31; }
+
+// f64 16x16x4: A lane l = A[l%16][l/16], B lane l = B[l/16][l%16];
+// result r of lane l = D[l/16 + 4r][l%16].
+LOCA_DEV f64x4_t mfma_f64(double a, double b, f64x4_t c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+// f32 32x32x2: A lane l = A[l%32][l/32], B lane l = B[l/32][l%32]; result as mfma32_row/col.
+LOCA_DEV f32x16_t mfma_f32x2(float a, float b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+}  // namespace loca
+
+// Internal launchers (defined in the kernel files, called by loca_api.hip).
+namespace loca {
+struct ErrorArgs {
+  hipStream_t stream;
+  int64_t nb, n, C, k, d, ld_logits;
+  const void* logits; loca_dtype logits_dtype;
+  const int32_t* labels; const float* w;
+  const void* credit_a; loca_dtype a_dtype; int64_t a_bstride;
+  const float* credit_b; int64_t b_bstride;
+  float* y_out; int64_t y_bstride;
+  float* e_out; loca_mb* mb_out; int32_t* dev_info;
+  char* ws;
+};
+size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k);
+hipError_t launch_error_targets(const ErrorArgs& a);
+
+struct StatsArgs {
+  hipStream_t stream;
+  int64_t nb, n, d, k;
+  const void* x; loca_dtype x_dtype; int64_t ldx, x_bstride;
+  const float* y; int64_t y_bstride;
+  double eta; loca_mb* mb;
+  void* S; void* K; loca_dtype acc; int64_t s_bstride, k_bstride;
+  char* ws;
+};
+size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc);
+hipError_t launch_accumulate_stats(const StatsArgs& a);
+
+struct SolveArgs {
+  hipStream_t stream;
+  int64_t nb, d, k;
+  const void* S; const void* K; loca_dtype acc; int64_t s_bstride, k_bstride;
+  const float* lp; const float* rp; int64_t r_prev, lp_bstride, rp_bstride;
+  const double* lambdas; int64_t n_lambda;
+  float* m_out; int64_t m_bstride;
+  const float* credit_b; int64_t b_bstride;
+  float* w_dense_out; int64_t w_bstride;
+  int32_t* dev_info; char* ws;
+};
+size_t ridge_solve_ws(int64_t nb, int64_t d, int64_t m, int64_t n_lambda, loca_dtype acc);
+hipError_t launch_ridge_solve(const SolveArgs& a);
+
+struct TruncArgs {
+  hipStream_t stream;
+  int64_t nm, d, kp, r_a;
+  const float* m; int64_t m_bstride;
+  const float* r; int64_t r_bstride, r_group;
+  float* a_out; int64_t a_bstride;
+  float* b_out; int64_t b_bstride;
+  float* sigma_out; int64_t sigma_bstride;
+  float* w_dense_out; int64_t w_bstride;
+  int32_t* dev_info; char* ws;
+};
+size_t lowrank_truncate_ws(int64_t nm, int64_t d, int64_t kp, int64_t r_a);
+hipError_t launch_lowrank_truncate(const TruncArgs& a);
+
+struct ProjArgs {
+  hipStream_t stream;
+  int64_t nb, d, k, r_a;
+  const void* S; const void* K; loca_dtype acc; int64_t s_bstride, k_bstride;
+  const float* credit_b; int64_t b_bstride;
+  const float* proj_a; int64_t pa_bstride;
+  const float* b_cur; int64_t bc_bstride;
+  const double* lambdas; int64_t n_lambda;
+  float* b_out; int64_t bo_bstride; float* g_out;
+  int32_t* dev_info; char* ws;
+};
+size_t projected_ws(int64_t nb, int64_t d, int64_t k, int64_t r_a, int64_t n_lambda);
+hipError_t launch_ridge_solve_projected(const ProjArgs& a);
+
+hipError_t launch_dense_targets(hipStream_t s, int64_t nb, int64_t n, int64_t k, int64_t d,
+                                const float* y, int64_t y_bstride, const loca_mb* mb,
+                                const float* credit_b, int64_t b_bstride, float* t_out,
+                                int64_t t_bstride);
+// out (rows x cols) = L (rows x kk, ld kk) * R (kk x cols, ld cols), float, batched.
+hipError_t launch_lowrank_product(hipStream_t s, int64_t nmat, int64_t rows, int64_t cols,
+                                  int64_t kk, const float* L, int64_t l_bstride, int64_t l_ld,
+                                  const float* R, int64_t r_bstride, int64_t r_group, int64_t r_ld,
+                                  float* out, int64_t out_bstride);
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+}  // namespace loca

@@ -10,7 +10,7 @@ Qwen2.5-shaped widths and block counts, small label sets like the tasks' answer
 sets, and the full 151,936-token vocabulary for the full-vocabulary variant.
 
 Two backends follow the same recipe:
-  * ``numpy``  -- host arrays, Philox streams keyed by (seed, config, block,
+  * ``numpy``  -- host arrays, SFC64 streams keyed by (seed, config, block,
     tensor, micro-batch); used by CPU tests, GPU parity tests and the CPU
     baseline sample.
   * ``torch``  -- device tensors from a seeded ``torch.Generator`` on the GPU;
@@ -110,7 +110,7 @@ def bf16_to_f32(h: np.ndarray) -> np.ndarray:
 def _rng(seed: int, cfg: LocaConfig, block: int, tensor: int, micro: int = 0) -> np.random.Generator:
     cid = _CFG_ID.get(cfg.name, 99)
     ss = np.random.SeedSequence([seed, cid, block, tensor, micro, cfg.d, cfg.C, cfg.k])
-    return np.random.Generator(np.random.Philox(ss))
+    return np.random.Generator(np.random.SFC64(ss))
 
 
 def outlier_channels(cfg: LocaConfig, block: int, seed: int = 0) -> np.ndarray:

@@ -1,0 +1,220 @@
+"""Thin ctypes binding of libloca (include/loca.h).
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+Tensors are torch device tensors; the stream is torch's current stream unless
+given.  Each function has the name of the C entry point it calls.  A missing
+library raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("LOCA_LIB", os.path.join(HERE, "lib", "libloca.so"))
+
+LOCA_OK, LOCA_E_ARG, LOCA_E_WORKSPACE, LOCA_E_HIP, LOCA_E_UNSUPPORTED = range(5)
+LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
+(LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
+ LOCA_OP_RIDGE_SOLVE_PROJECTED) = range(5)
+
+EXPORTED = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
+            "loca_ridge_solve_projected", "loca_dense_targets", "loca_workspace_size", "loca_status_str",
+            "loca_version")
+
+
+class LocaMB(ctypes.Structure):
+    _fields_ = [("sum_q2", ctypes.c_double), ("sum_x2", ctypes.c_double), ("eta_bar", ctypes.c_double),
+                ("n", ctypes.c_int64)]
+
+
+MB_BYTES = ctypes.sizeof(LocaMB)  # 32
+
+
+class LocaError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {status_str(status)} ({status})")
+
+
+_lib = None
+_VP, _I64, _SZ, _D = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_double
+_I = ctypes.c_int
+
+
+def load():
+    """Load libloca.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libloca is not built ({LIB_PATH}); run paper_2608_03020_amd/build.py")
+    lib = ctypes.CDLL(LIB_PATH)
+    lib.loca_error_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _I, _I64,
+                                       _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
+    lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _D, _VP,
+                                          _VP, _VP, _I, _I64, _I64, _VP, _SZ]
+    lib.loca_ridge_solve.argtypes = [_VP, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _VP, _I64, _I64, _I64,
+                                     _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
+    lib.loca_lowrank_truncate.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _I64, _VP, _I64, _VP,
+                                          _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
+    lib.loca_ridge_solve_projected.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _I64,
+                                               _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _SZ]
+    lib.loca_dense_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _VP, _I64, _VP, _I64]
+    lib.loca_workspace_size.argtypes = [_I, _I64, _I64, _I64, _I64, _I64, _I64, _I64, _I]
+    lib.loca_workspace_size.restype = _SZ
+    lib.loca_status_str.argtypes = [_I]
+    lib.loca_status_str.restype = ctypes.c_char_p
+    lib.loca_version.restype = ctypes.c_char_p
+    for name in ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
+                 "loca_ridge_solve_projected", "loca_dense_targets"):
+        getattr(lib, name).restype = _I
+    _lib = lib
+    return lib
+
+
+def status_str(s: int) -> str:
+    return load().loca_status_str(s).decode()
+
+
+def version() -> str:
+    return load().loca_version().decode()
+
+
+def workspace_size(op: int, nb: int, n: int, d: int, k: int, C: int = 0, r_a: int = 0, n_lambda: int = 0,
+                   acc: int = LOCA_F32) -> int:
+    return int(load().loca_workspace_size(op, nb, n, d, k, C, r_a, n_lambda, acc))
+
+
+# ------------------------------------------------------------------ marshalling helpers
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _dtype(t) -> int:
+    import torch
+    return {torch.float32: LOCA_F32, torch.bfloat16: LOCA_BF16, torch.float64: LOCA_F64}[t.dtype]
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(fn: str, st: int):
+    if st != LOCA_OK:
+        raise LocaError(fn, st)
+
+
+def _bstride(t, nb: int) -> int:
+    if t is None or nb <= 1 or isinstance(t, int):
+        return 0
+    return t.stride(0) if t.dim() >= 3 or (t.dim() == 2 and nb > 1 and t.shape[0] == nb) else 0
+
+
+def alloc_workspace(nbytes: int, device="cuda"):
+    import torch
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def new_mb(nb: int, device="cuda"):
+    """Device array of nb loca_mb records, as a float64 tensor (nb, 4)."""
+    import torch
+    return torch.zeros((nb, 4), dtype=torch.float64, device=device)
+
+
+def mb_view(mb):
+    """(sum_q2, sum_x2, eta_bar, n) per block, as host floats."""
+    import numpy as np
+    h = mb.detach().cpu().numpy()
+    n = h[:, 3].copy().view(np.int64)
+    return {"sum_q2": h[:, 0].copy(), "sum_x2": h[:, 1].copy(), "eta_bar": h[:, 2].copy(), "n": n}
+
+
+# ------------------------------------------------------------------ entry points
+
+
+def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_info, ws, *, w=None, e_out=None,
+                       nb=None, stream=None):
+    """logits (n, C); labels (n,); credit_a (nb, C, k); credit_b (nb, k, d); y_out (nb, n, k)."""
+    nb = nb or credit_a.shape[0]
+    n, C = logits.shape[0], logits.shape[1]
+    k, d = credit_b.shape[-2], credit_b.shape[-1]
+    st = load().loca_error_targets(
+        _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
+        _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
+        credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(y_out), y_out.stride(0) if y_out.dim() == 3 else 0,
+        _ptr(e_out), _ptr(mb_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
+    _check("loca_error_targets", st)
+
+
+def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, stream=None):
+    """x (nb, n, d) bf16 or fp32 (row stride may exceed d); y (nb, n, k); S (nb, d, d); K (nb, d, k)."""
+    nb, n, d = x.shape
+    k = y.shape[-1]
+    acc = _dtype(S)
+    st = load().loca_accumulate_stats(
+        _stream(stream), nb, n, d, k, _ptr(x), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), float(eta),
+        _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), _ptr(ws), ws.numel() * ws.element_size())
+    _check("loca_accumulate_stats", st)
+
+
+def loca_ridge_solve(S, K, lambdas: Sequence[float], m_out, dev_info, ws, *, lp=None, rp=None, credit_b=None,
+                     w_dense_out=None, stream=None):
+    """S (nb, d, d); K (nb, d, k); m_out (nb, n_lambda, d, r_prev + k); optional W (nb, n_lambda, d, d)."""
+    nb, d, k = K.shape
+    r_prev = 0 if lp is None else lp.shape[-1]
+    lam = (ctypes.c_double * len(lambdas))(*[float(v) for v in lambdas])
+    st = load().loca_ridge_solve(
+        _stream(stream), nb, d, k, _ptr(S), _ptr(K), _dtype(S), S.stride(0), K.stride(0), _ptr(lp), _ptr(rp),
+        r_prev, lp.stride(0) if lp is not None else 0, rp.stride(0) if rp is not None else 0,
+        ctypes.cast(lam, ctypes.c_void_p), len(lambdas), _ptr(m_out), m_out.stride(1), _ptr(credit_b),
+        credit_b.stride(0) if credit_b is not None else 0, _ptr(w_dense_out),
+        w_dense_out.stride(1) if w_dense_out is not None else 0, _ptr(dev_info), _ptr(ws),
+        ws.numel() * ws.element_size())
+    _check("loca_ridge_solve", st)
+
+
+def loca_lowrank_truncate(m, r, r_a: int, a_out, b_out, sigma_out, dev_info, ws, *, r_group=1, w_dense_out=None,
+                          stream=None):
+    """m (nm, d, kp); r (nr, kp, d) shared by r_group consecutive matrices; a_out (nm, r_a, d);
+    b_out (nm, d, r_a); sigma_out (nm, kp)."""
+    nm, d, kp = m.shape
+    st = load().loca_lowrank_truncate(
+        _stream(stream), nm, d, kp, r_a, _ptr(m), m.stride(0), _ptr(r), r.stride(0), r_group, _ptr(a_out),
+        a_out.stride(0), _ptr(b_out), b_out.stride(0), _ptr(sigma_out), sigma_out.stride(0), _ptr(w_dense_out),
+        w_dense_out.stride(0) if w_dense_out is not None else 0, _ptr(dev_info), _ptr(ws),
+        ws.numel() * ws.element_size())
+    _check("loca_lowrank_truncate", st)
+
+
+def loca_ridge_solve_projected(S, K, credit_b, proj_a, lambdas: Sequence[float], b_out, dev_info, ws, *,
+                               b_cur=None, g_out=None, stream=None):
+    """S (nb, d, d); K (nb, d, k); credit_b (nb, k, d); proj_a (nb, r_a, d); b_out (nb, n_lambda, d, r_a)."""
+    nb, d, k = K.shape
+    r_a = proj_a.shape[-2]
+    lam = (ctypes.c_double * len(lambdas))(*[float(v) for v in lambdas])
+    st = load().loca_ridge_solve_projected(
+        _stream(stream), nb, d, k, r_a, _ptr(S), _ptr(K), _dtype(S), S.stride(0), K.stride(0), _ptr(credit_b),
+        credit_b.stride(0), _ptr(proj_a), proj_a.stride(0), _ptr(b_cur), b_cur.stride(0) if b_cur is not None else 0,
+        ctypes.cast(lam, ctypes.c_void_p), len(lambdas), _ptr(b_out), b_out.stride(1), _ptr(g_out), _ptr(dev_info),
+        _ptr(ws), ws.numel() * ws.element_size())
+    _check("loca_ridge_solve_projected", st)
+
+
+def loca_dense_targets(y, mb, credit_b, t_out, *, stream=None):
+    """y (nb, n, k); credit_b (nb, k, d); t_out (nb, n, d)."""
+    nb, n, k = y.shape
+    d = credit_b.shape[-1]
+    st = load().loca_dense_targets(_stream(stream), nb, n, k, d, _ptr(y), y.stride(0), _ptr(mb), _ptr(credit_b),
+                                   credit_b.stride(0), _ptr(t_out), t_out.stride(0))
+    _check("loca_dense_targets", st)

@@ -1,0 +1,87 @@
+"""One pass of the per-block adaptation step over all blocks of a workload.
+
+Owns the device buffers (torch) and issues the C-ABI calls in the order of
+the outer iteration (Section S13, steps 2-5): for every micro-batch the head
+error and credit coordinates, then the streaming statistics; then the ridge
+solves for every lambda; then the rank-r_a truncation.  Orchestration only:
+all arithmetic runs in libloca's kernels.
+"""
+from __future__ import annotations
+
+from typing import List, Optional
+
+from . import loca
+from .inputs import LocaConfig
+
+
+class BlockStep:
+    """Buffers and calls for `nb` blocks of a config, micro-batch by micro-batch.
+
+    x_blocks: device tensor (nb, n, d) with all micro-batches of every block
+    (bf16 or fp32); logits (n, C); labels (n,); credit_a (nb, C, k);
+    credit_b (nb, k, d).
+    """
+
+    def __init__(self, cfg: LocaConfig, nb: int, device="cuda", projected: bool = False, n_total: Optional[int] = None):
+        import torch
+        self.cfg, self.nb, self.device = cfg, nb, device
+        d, k, r_a = cfg.d, cfg.k, cfg.r_a
+        nl = len(cfg.lambdas)
+        acc_t = torch.float64 if cfg.mode == "fp32" else torch.float32
+        self.acc = loca.LOCA_F64 if cfg.mode == "fp32" else loca.LOCA_F32
+        n_mb = cfg.micro
+        self.S = torch.zeros((nb, d, d), dtype=acc_t, device=device)
+        self.K = torch.zeros((nb, d, k), dtype=acc_t, device=device)
+        self.Y = torch.empty((nb, n_mb, k), dtype=torch.float32, device=device)
+        self.mb = loca.new_mb(nb, device)
+        self.mb_log: List = []
+        self.info = torch.zeros(max(nb * nl, 1), dtype=torch.int32, device=device)
+        self.M = torch.empty((nb, nl, d, k), dtype=torch.float32, device=device)
+        self.A_ad = torch.empty((nb * nl, r_a, d), dtype=torch.float32, device=device)
+        self.B_ad = torch.empty((nb * nl, d, r_a), dtype=torch.float32, device=device)
+        self.sigma = torch.empty((nb * nl, k), dtype=torch.float32, device=device)
+        self.projected = projected
+        if projected:
+            self.B_proj = torch.empty((nb, nl, d, r_a), dtype=torch.float32, device=device)
+        ws = max(
+            loca.workspace_size(loca.LOCA_OP_ERROR_TARGETS, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+            loca.workspace_size(loca.LOCA_OP_ACCUMULATE_STATS, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+            loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+            loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, nb * nl, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+            loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE_PROJECTED, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+        )
+        self.ws = loca.alloc_workspace(ws, device)
+
+    def reset(self):
+        self.S.zero_()
+        self.K.zero_()
+        self.mb_log = []
+
+    def micro_batch(self, x_m, logits_m, labels_m, credit_a, credit_b, keep_log=False, stream=None):
+        """Rows a1-a4 for one micro-batch: x_m (nb, n_m, d)."""
+        n_m = x_m.shape[1]
+        y = self.Y[:, :n_m]
+        loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info, self.ws,
+                                nb=self.nb, stream=stream)
+        loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, stream=stream)
+        if keep_log:
+            self.mb_log.append(self.mb.clone())
+
+    def solve(self, credit_b, proj_a=None, stream=None):
+        """Rows a5-a6: ridge solves for every lambda and the rank-r_a truncation."""
+        cfg = self.cfg
+        nl = len(cfg.lambdas)
+        loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, stream=stream)
+        loca.loca_lowrank_truncate(self.M.view(self.nb * nl, cfg.d, cfg.k), credit_b, cfg.r_a, self.A_ad, self.B_ad,
+                                   self.sigma, self.info, self.ws, r_group=nl, stream=stream)
+        if self.projected and proj_a is not None:
+            loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj, self.info,
+                                            self.ws, stream=stream)
+
+    def run(self, x_blocks, logits, labels, credit_a, credit_b, proj_a=None, stream=None):
+        """One full pass over all micro-batches of all nb blocks."""
+        self.reset()
+        for m in range(self.cfg.n_micro):
+            lo, hi = self.cfg.micro_rows(m)
+            self.micro_batch(x_blocks[:, lo:hi], logits[lo:hi], labels[lo:hi], credit_a, credit_b, stream=stream)
+        self.solve(credit_b, proj_a, stream=stream)

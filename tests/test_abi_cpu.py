@@ -1,0 +1,156 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+declared in include/loca.h, and rejects invalid arguments synchronously
+(before anything is enqueued, so no device is touched)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "loca.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2608_03020_amd import loca
+    if not os.path.exists(loca.LIB_PATH):
+        pytest.skip("libloca.so not built (run __graft_entry__.build())")
+    return loca
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(loca_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_step_calls():
+    names = declared_functions()
+    for fn in ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate"):
+        assert fn in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    so = ctypes.CDLL(lib.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(so, name), name
+    assert set(lib.EXPORTED) == set(declared_functions())
+
+
+def test_status_strings_and_version(lib):
+    assert lib.status_str(lib.LOCA_OK) == "ok"
+    assert "argument" in lib.status_str(lib.LOCA_E_ARG)
+    assert "gfx950" in lib.version()
+
+
+def test_workspace_sizes_are_positive_and_monotone(lib):
+    a = lib.workspace_size(lib.LOCA_OP_ACCUMULATE_STATS, 1, 512, 896, 8, acc=lib.LOCA_F64)
+    b = lib.workspace_size(lib.LOCA_OP_ACCUMULATE_STATS, 2, 512, 896, 8, acc=lib.LOCA_F64)
+    assert 0 < a < b
+    s1 = lib.workspace_size(lib.LOCA_OP_RIDGE_SOLVE, 1, 0, 1536, 16, n_lambda=1)
+    s3 = lib.workspace_size(lib.LOCA_OP_RIDGE_SOLVE, 1, 0, 1536, 16, n_lambda=3)
+    assert s3 > s1 >= 4 * 1536 * 1536
+    assert lib.workspace_size(lib.LOCA_OP_ERROR_TARGETS, 0, 10, 10, 4) == 0
+
+
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def test_error_targets_rejects(lib):
+    so = lib.load()
+    ok_args = dict(stream=None, nb=1, n=8, C=4, k=2, d=16, logits=FAKE, ldt=lib.LOCA_F32, ld=4, labels=FAKE, w=None,
+                   a=FAKE, adt=lib.LOCA_F32, abs_=0, b=FAKE, bbs=0, y=FAKE, ybs=0, e=None, mb=FAKE, info=FAKE,
+                   ws=None, wsb=0)
+
+    def call(**kw):
+        a = dict(ok_args, **kw)
+        return so.loca_error_targets(a["stream"], a["nb"], a["n"], a["C"], a["k"], a["d"], a["logits"], a["ldt"],
+                                     a["ld"], a["labels"], a["w"], a["a"], a["adt"], a["abs_"], a["b"], a["bbs"],
+                                     a["y"], a["ybs"], a["e"], a["mb"], a["info"], a["ws"], a["wsb"])
+
+    assert call(n=0) == lib.LOCA_E_ARG
+    assert call(C=0) == lib.LOCA_E_ARG
+    assert call(logits=None) == lib.LOCA_E_ARG
+    assert call(ld=3) == lib.LOCA_E_ARG
+    assert call(ldt=lib.LOCA_F64) == lib.LOCA_E_ARG
+    assert call(nb=2, abs_=1) == lib.LOCA_E_ARG
+    assert call(k=129) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE                  # missing workspace
+    assert call(ws=FAKE + 1, wsb=1 << 30) == lib.LOCA_E_WORKSPACE  # misaligned
+
+
+def test_accumulate_stats_rejects(lib):
+    so = lib.load()
+    base = [None, 1, 64, 32, 4, FAKE, lib.LOCA_BF16, 32, 0, FAKE, 0, 0.01, FAKE, FAKE, FAKE, lib.LOCA_F32, 0, 0,
+            None, 0]
+
+    def call(**kw):
+        idx = dict(nb=1, n=2, d=3, k=4, x=5, xdt=6, ldx=7, xbs=8, eta=11, S=13, acc=15)
+        a = list(base)
+        for key, v in kw.items():
+            a[idx[key]] = v
+        return so.loca_accumulate_stats(*a)
+
+    assert call(d=0) == lib.LOCA_E_ARG
+    assert call(ldx=31) == lib.LOCA_E_ARG
+    assert call(ldx=36) == lib.LOCA_E_ARG                  # bf16 rows must be 16-byte multiples
+    assert call(x=FAKE + 2) == lib.LOCA_E_ARG              # misaligned base
+    assert call(eta=-1.0) == lib.LOCA_E_ARG
+    assert call(eta=float("nan")) == lib.LOCA_E_ARG
+    assert call(acc=lib.LOCA_F64) == lib.LOCA_E_ARG        # bf16 X needs fp32 statistics
+    assert call(xdt=lib.LOCA_F32) == lib.LOCA_E_ARG        # fp32 X needs fp64 statistics
+    assert call(S=None) == lib.LOCA_E_ARG
+    assert call(nb=2, xbs=10) == lib.LOCA_E_ARG
+    assert call(k=200) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE
+
+
+def _lams(*v):
+    arr = (ctypes.c_double * len(v))(*v)
+    return ctypes.cast(arr, ctypes.c_void_p), arr
+
+
+def test_ridge_solve_rejects(lib):
+    so = lib.load()
+
+    def call(lams=(1e-2,), d=16, k=4, acc=lib.LOCA_F32, S=FAKE, r_prev=0, lp=None, mbs=64, ws=None):
+        p, _keep = _lams(*lams) if lams is not None else (None, None)
+        return so.loca_ridge_solve(None, 1, d, k, S, FAKE, acc, 0, 0, lp, None, r_prev, 0, 0, p,
+                                   len(lams) if lams else 0, FAKE, mbs, None, 0, None, 0, FAKE, ws, 0)
+
+    assert call(lams=(0.0,)) == lib.LOCA_E_ARG            # the paper requires lambda > 0
+    assert call(lams=(1e-2, -1.0)) == lib.LOCA_E_ARG
+    assert call(lams=(float("inf"),)) == lib.LOCA_E_ARG
+    assert call(lams=None) == lib.LOCA_E_ARG
+    assert call(acc=lib.LOCA_BF16) == lib.LOCA_E_ARG
+    assert call(S=None) == lib.LOCA_E_ARG
+    assert call(r_prev=2, lp=None) == lib.LOCA_E_ARG
+    assert call(k=129) == lib.LOCA_E_UNSUPPORTED
+    assert call(lams=tuple([0.1] * 9)) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE
+
+
+def test_lowrank_truncate_rejects(lib):
+    so = lib.load()
+
+    def call(d=32, kp=8, r_a=4, r_group=1, m=FAKE):
+        return so.loca_lowrank_truncate(None, 1, d, kp, r_a, m, 0, FAKE, 0, r_group, FAKE, 0, FAKE, 0, FAKE, 0,
+                                        None, 0, FAKE, None, 0)
+
+    assert call(r_a=9) == lib.LOCA_E_ARG                   # r_a <= kp
+    assert call(kp=40, r_a=4) == lib.LOCA_E_ARG            # kp <= d
+    assert call(r_group=0) == lib.LOCA_E_ARG
+    assert call(m=None) == lib.LOCA_E_ARG
+    assert call(d=100, kp=65, r_a=4) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE
+
+
+def test_projected_and_dense_targets_reject(lib):
+    so = lib.load()
+    p, _keep = _lams(1e-2)
+    assert so.loca_ridge_solve_projected(None, 1, 16, 4, 0, FAKE, FAKE, lib.LOCA_F32, 0, 0, FAKE, 0, FAKE, 0, None,
+                                         0, p, 1, FAKE, 0, None, FAKE, None, 0) == lib.LOCA_E_ARG
+    assert so.loca_ridge_solve_projected(None, 1, 16, 4, 65, FAKE, FAKE, lib.LOCA_F32, 0, 0, FAKE, 0, FAKE, 0, None,
+                                         0, p, 1, FAKE, 0, None, FAKE, None, 0) == lib.LOCA_E_UNSUPPORTED
+    assert so.loca_dense_targets(None, 1, 4, 2, 8, None, 0, FAKE, FAKE, 0, FAKE, 0) == lib.LOCA_E_ARG

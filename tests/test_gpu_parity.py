@@ -1,0 +1,322 @@
+"""Parity of the HIP path (through the C ABI) with the float64 oracle.
+
+Tolerances (relative Frobenius error): statistics S and Z = X^T T, the dense
+ridge solution and the rank-r_a adapter W_r within 2e-3 in bf16 mode and 1e-5
+in fp32 mode; intermediates (credit coordinates Y, eta_bar) within 1e-5.
+Sizes span several tiles with ragged edges in d and in the token count.
+"""
+import numpy as np
+import pytest
+
+from gpu_helpers import host_inputs, log, padded_rows, rel, run_gpu, run_oracle, to_dev
+from paper_2608_03020_amd import inputs as gen
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-3, "fp32": 1e-5}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_03020_amd import loca
+    loca.load()
+
+
+def _compare(cfg, g, o, b, label):
+    tol = TOL[cfg.mode]
+    d = cfg.d
+    iu = np.triu_indices(d)
+    e = {}
+    e["S"] = rel(g["S"][b][iu], o["S"][iu])
+    e["K"] = rel(g["K"][b], o["K"])
+    for m in range(cfg.n_micro):
+        e[f"Y{m}"] = rel(g["Y"][m][b], o["Y"][m])
+        e[f"eta{m}"] = abs(g["mb"][m]["eta_bar"][b] - o["mb"][m]["eta_bar"]) / max(o["mb"][m]["eta_bar"], 1e-300)
+        e[f"x2_{m}"] = abs(g["mb"][m]["sum_x2"][b] - o["mb"][m]["sum_x2"]) / o["mb"][m]["sum_x2"]
+        e[f"q2_{m}"] = abs(g["mb"][m]["sum_q2"][b] - o["mb"][m]["sum_q2"]) / max(o["mb"][m]["sum_q2"], 1e-300)
+    nl = len(cfg.lambdas)
+    for l, sol in enumerate(o["solves"]):
+        e[f"M{l}"] = rel(g["M"][b, l], sol["M"])
+        if "W_r" in g:
+            e[f"Wr{l}"] = rel(g["W_r"][b * nl + l], sol["W_r"])
+        kk = min(cfg.r_a + 1, cfg.k)
+        e[f"sig{l}"] = rel(g["sigma"][b * nl + l][:kk], sol["sigma"][:kk])
+    log(label, {k: f"{v:.2e}" for k, v in e.items()})
+    assert e["S"] <= tol and e["K"] <= tol
+    for m in range(cfg.n_micro):
+        assert e[f"Y{m}"] <= 1e-5 and e[f"eta{m}"] <= 1e-5 and e[f"x2_{m}"] <= 1e-5 and e[f"q2_{m}"] <= 1e-5
+    for l in range(nl):
+        assert e[f"M{l}"] <= tol
+        if "W_r" in g:
+            assert e[f"Wr{l}"] <= tol
+        assert e[f"sig{l}"] <= tol
+    return e
+
+
+CASES = {
+    # ragged d on 128-wide tiles, two micro-batches (640 + 360 rows), two blocks, two lambdas
+    "bf16_d600": gen.custom_config("t1", blocks=2, d=600, n=1000, micro=640, C=5, k=16, r_a=4, lambdas=(1e-2, 1.0)),
+    # ragged d on 256-wide tiles, three micro-batches with a ragged last one.  bf16 mode keeps fp32
+    # statistics, which needs N > d: with N < d rounding in S leaks into the null space of X and is
+    # amplified by 1/lambda (fp32 mode, with fp64 statistics, covers N < d).
+    "bf16_d1100": gen.custom_config("t2", blocks=1, d=1100, n=2300, micro=1000, C=3, k=32, r_a=8),
+    # fp32 mode with fewer tokens than features (null space amplified by 1/lambda)
+    "fp32_n150_d200": gen.custom_config("t3", blocks=2, d=200, n=150, C=2, k=8, r_a=8, mode="fp32",
+                                        x_dist="gauss_outlier", n_outlier=3, outlier_scale=20.0, logit_std=2.0),
+    # large label set (online-softmax kernel), bf16 logits and credit factor, real truncation 64 -> 32
+    "vocab3000": gen.custom_config("t4", blocks=1, d=256, n=600, C=3000, k=64, r_a=32, logit_std=2.0,
+                                   logit_dtype="bf16", a_dtype="bf16"),
+    # k > 64 on a small label set goes through the large-vocabulary kernel too
+    "k96": gen.custom_config("t5", blocks=1, d=320, n=400, C=7, k=96, r_a=16),
+}
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_block_step_parity(name):
+    cfg = CASES[name]
+    if cfg.k > 64:
+        pytest.skip("truncation supports kp <= 64 in this build")
+    log(f"case {name}: d={cfg.d} n={cfg.n} C={cfg.C} k={cfg.k} blocks={cfg.blocks} mode={cfg.mode}")
+    xs, zs, ys, As, Bs = host_inputs(cfg, range(cfg.blocks))
+    g = run_gpu(cfg, xs, zs, ys, As, Bs)
+    assert np.all(g["info"] == 0) and np.all(g["info_err"] == 0)
+    for b in range(cfg.blocks):
+        o = run_oracle(cfg, xs[b], zs, ys, As[b], Bs[b])
+        _compare(cfg, g, o, b, f"{name}[block {b}]")
+
+
+def test_k96_credit_coordinates():
+    """k = 96: head error and statistics (truncation of kp > 64 is not built)."""
+    import torch
+    from paper_2608_03020_amd import loca
+    import oracle
+    cfg = CASES["k96"]
+    xs, zs, ys, As, Bs = host_inputs(cfg, [0])
+    log("case k96 statistics")
+    from paper_2608_03020_amd.step import BlockStep
+    st = BlockStep(cfg, 1)
+    x = padded_rows(np.stack([np.concatenate(xs[0])]))
+    st.reset()
+    st.micro_batch(x, to_dev(zs[0]), to_dev(ys[0]), to_dev(np.stack(As)), to_dev(np.stack(Bs)))
+    torch.cuda.synchronize()
+    E = oracle.head_error(zs[0], ys[0])
+    Y, Q = oracle.credit(E, As[0], Bs[0])
+    assert rel(st.Y[0].cpu().numpy(), Y) < 1e-5
+    mbv = loca.mb_view(st.mb)
+    assert abs(mbv["sum_q2"][0] - np.sum(Q ** 2)) / np.sum(Q ** 2) < 1e-5
+
+
+def test_dense_targets_and_cross_statistic():
+    """T = -eta_bar Y B~ (dense) and Z = X^T T = K B~ against the oracle's dense Z."""
+    import torch
+    from paper_2608_03020_amd import loca
+    cfg = CASES["bf16_d600"]
+    xs, zs, ys, As, Bs = host_inputs(cfg, [0])
+    g = run_gpu(cfg, xs, zs, ys, As, Bs, want_dense=False)
+    o = run_oracle(cfg, xs[0], zs, ys, As[0], Bs[0])
+    Z_gpu = g["K"][0].astype(np.float64) @ np.asarray(Bs[0], np.float64)
+    log("dense Z rel err", rel(Z_gpu, o["Z"]))
+    assert rel(Z_gpu, o["Z"]) <= TOL["bf16"]
+    # dense T of the last micro-batch
+    m = cfg.n_micro - 1
+    y = torch.from_numpy(g["Y"][m]).cuda()
+    mbt = torch.from_numpy(np.stack([[g["mb"][m]["sum_q2"][0], g["mb"][m]["sum_x2"][0], g["mb"][m]["eta_bar"][0],
+                                      np.int64(g["mb"][m]["n"][0]).view(np.float64)]])).cuda()
+    T = torch.empty((1, y.shape[1], cfg.d), dtype=torch.float32, device="cuda")
+    loca.loca_dense_targets(y, mbt, torch.from_numpy(np.stack(Bs)).cuda(), T)
+    torch.cuda.synchronize()
+    assert rel(T[0].cpu().numpy(), o["T"][m]) <= 1e-5
+
+
+def test_ridge_solve_from_oracle_statistics():
+    """The solve alone, fed the oracle's statistics: M = (S + lam I)^{-1} K per lambda, and dense W."""
+    import torch
+    from paper_2608_03020_amd import loca
+    cfg = gen.custom_config("t6", blocks=1, d=777, n=2000, C=5, k=32, r_a=8, lambdas=(1e-3, 1e-2, 1e-1))
+    xs, zs, ys, As, Bs = host_inputs(cfg, [0])
+    o = run_oracle(cfg, xs[0], zs, ys, As[0], Bs[0])
+    S = torch.from_numpy(o["S"].astype(np.float32))[None].cuda()
+    K = torch.from_numpy(o["K"].astype(np.float32))[None].cuda()
+    M = torch.empty((1, 3, cfg.d, cfg.k), dtype=torch.float32, device="cuda")
+    W = torch.empty((1, 3, cfg.d, cfg.d), dtype=torch.float32, device="cuda")
+    info = torch.zeros(3, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE, 1, 0, cfg.d, cfg.k, n_lambda=3))
+    B = torch.from_numpy(Bs[0])[None].cuda()
+    loca.loca_ridge_solve(S, K, cfg.lambdas, M, info, ws, credit_b=B, w_dense_out=W)
+    torch.cuda.synchronize()
+    assert np.all(info.cpu().numpy() == 0)
+    for l, sol in enumerate(o["solves"]):
+        em, ew = rel(M[0, l].cpu().numpy(), sol["M"]), rel(W[0, l].cpu().numpy(), sol["W"])
+        log(f"solve lam={cfg.lambdas[l]}: M {em:.2e} W {ew:.2e}")
+        assert em < 2e-4 and ew < 2e-4
+
+
+def test_ridge_solve_fp64_and_nonpd_pivot():
+    """fp64 solve of an exactly known system, and the potrf-style pivot report."""
+    import torch
+    from paper_2608_03020_amd import loca
+    rng = np.random.default_rng(0)
+    d, k = 130, 5
+    Xr = rng.normal(size=(300, d))
+    S = Xr.T @ Xr
+    K = rng.normal(size=(d, k))
+    lam = 0.5
+    Mref = np.linalg.solve(S + lam * np.eye(d), K)
+    St = torch.from_numpy(S)[None].cuda()
+    Kt = torch.from_numpy(K)[None].cuda()
+    M = torch.empty((1, 1, d, k), dtype=torch.float32, device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE, 1, 0, d, k, n_lambda=1,
+                                                  acc=loca.LOCA_F64))
+    loca.loca_ridge_solve(St, Kt, [lam], M, info, ws)
+    torch.cuda.synchronize()
+    assert info.item() == 0
+    assert rel(M[0, 0].cpu().numpy(), Mref) < 1e-6  # fp32 output rounding
+    # a negative diagonal entry at index 70 is the first non-positive pivot (1-based 71)
+    S2 = S.copy()
+    S2[70, 70] = -1e6
+    loca.loca_ridge_solve(torch.from_numpy(S2)[None].cuda(), Kt, [lam], M, info, ws)
+    torch.cuda.synchronize()
+    assert info.item() == 71
+
+
+def test_truncation_matches_explicit_svd():
+    """Eckart-Young truncation of W = M B~ against the oracle's dense SVD (d <= 256)."""
+    import torch
+    import oracle
+    from paper_2608_03020_amd import loca
+    rng = np.random.default_rng(1)
+    d, kp, r = 200, 24, 10
+    Mh = rng.normal(size=(d, kp)).astype(np.float32)
+    Rh = rng.normal(size=(kp, d)).astype(np.float32)
+    Wr_o, s_o = oracle.truncate_dense(Mh.astype(np.float64) @ Rh.astype(np.float64), r)
+    Mt = torch.from_numpy(Mh)[None].cuda()
+    Rt = torch.from_numpy(Rh)[None].cuda()
+    a = torch.empty((1, r, d), device="cuda")
+    b = torch.empty((1, d, r), device="cuda")
+    s = torch.empty((1, kp), device="cuda")
+    W = torch.empty((1, d, d), device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, 1, 0, d, kp, r_a=r))
+    loca.loca_lowrank_truncate(Mt, Rt, r, a, b, s, info, ws, w_dense_out=W)
+    torch.cuda.synchronize()
+    e_w = rel(W[0].cpu().numpy(), Wr_o)
+    e_s = rel(s[0].cpu().numpy(), s_o[:kp])
+    A = a[0].cpu().numpy().astype(np.float64)
+    log(f"truncation: W_r {e_w:.2e} sigma {e_s:.2e} orth {np.abs(A @ A.T - np.eye(r)).max():.2e}")
+    assert e_w < 1e-5 and e_s < 1e-5
+    assert np.abs(A @ A.T - np.eye(r)).max() < 1e-5
+    np.testing.assert_allclose(A.T @ b[0].cpu().numpy().T, W[0].cpu().numpy(), atol=1e-4 * np.abs(Wr_o).max())
+
+
+def test_projected_form_matches_oracle():
+    """Paper-literal projected solve (random A_l): B* = C_l (G_l + lam I)^{-1}."""
+    cfg = gen.custom_config("t7", blocks=2, d=300, n=500, C=4, k=16, r_a=8, lambdas=(1e-2, 1.0))
+    xs, zs, ys, As, Bs = host_inputs(cfg, range(2))
+    proj = [gen.gen_adapter_projection(cfg, b) for b in range(2)]
+    g = run_gpu(cfg, xs, zs, ys, As, Bs, want_dense=False, proj=proj)
+    for b in range(2):
+        o = run_oracle(cfg, xs[b], zs, ys, As[b], Bs[b], proj=proj[b])
+        for l, sol in enumerate(o["solves"]):
+            e = rel(g["B_proj"][b, l], sol["B_proj"])
+            log(f"projected block {b} lam {cfg.lambdas[l]}: {e:.2e}")
+            assert e <= TOL["bf16"]
+
+
+def test_degenerate_single_class_and_zero_eta():
+    """C = 1 gives E = 0, so Q = 0, eta_bar = 0 and the adapter is zero (frozen model)."""
+    cfg = gen.custom_config("t8", blocks=1, d=40, n=33, C=1, k=4, r_a=2)
+    xs, zs, ys, As, Bs = host_inputs(cfg, [0])
+    g = run_gpu(cfg, xs, zs, ys, As, Bs)
+    assert np.all(g["mb"][0]["eta_bar"] == 0.0)
+    assert np.all(g["K"] == 0.0) and np.all(g["M"] == 0.0) and np.all(g["W_r"] == 0.0)
+    o = run_oracle(cfg, xs[0], zs, ys, As[0], Bs[0])
+    assert rel(g["S"][0][np.triu_indices(40)], o["S"][np.triu_indices(40)]) < 1e-6
+
+
+def test_tiny_width_and_single_token():
+    """d = 1 (one feature, ldx padded to 8) and a single-token micro-batch."""
+    import torch
+    from paper_2608_03020_amd import loca
+    import oracle
+    rng = np.random.default_rng(2)
+    for n, d in [(1, 1), (1, 9), (37, 1)]:
+        log(f"case tiny n={n} d={d}")
+        ld = 8 * ((d + 7) // 8)
+        xh = gen.bf16_bits(rng.normal(size=(n, d)).astype(np.float32))
+        xpad = np.zeros((1, n, ld), np.uint16)
+        xpad[0, :, :d] = xh
+        x = to_dev(xpad)[:, :, :d]
+        k = 1
+        y = torch.from_numpy(rng.normal(size=(1, n, k)).astype(np.float32)).cuda()
+        mb = loca.new_mb(1)
+        mb[0, 0] = 1.0  # sum_q2 = 1
+        S = torch.zeros((1, d, d), device="cuda")
+        K = torch.zeros((1, d, k), device="cuda")
+        ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_ACCUMULATE_STATS, 1, n, d, k))
+        loca.loca_accumulate_stats(x, y, 0.5, mb, S, K, ws)
+        torch.cuda.synchronize()
+        xf = gen.as_f64(xh, "bf16")
+        So = oracle.gram_acc(xf)
+        sx = float(np.sum(xf ** 2))
+        eb = 0.5 * np.sqrt(sx / 1.0)
+        Ko = oracle.cross_acc(xf, -eb * y[0].cpu().numpy().astype(np.float64))
+        iu = np.triu_indices(d)
+        assert rel(S[0].cpu().numpy()[iu], So[iu]) < 1e-6
+        assert rel(K[0].cpu().numpy(), Ko) < 1e-5
+        assert abs(loca.mb_view(mb)["eta_bar"][0] - eb) < 1e-6 * eb
+
+
+def test_out_of_range_label_reported():
+    import torch
+    from paper_2608_03020_amd import loca
+    n, C, k, d = 300, 4, 8, 16
+    z = torch.randn((n, C), device="cuda")
+    y = torch.randint(0, C, (n,), dtype=torch.int32, device="cuda")
+    y[123] = 9
+    y[200] = -1
+    A = torch.randn((1, C, k), device="cuda")
+    B = torch.randn((1, k, d), device="cuda")
+    Y = torch.empty((1, n, k), device="cuda")
+    mb = loca.new_mb(1)
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_ERROR_TARGETS, 1, n, d, k, C))
+    loca.loca_error_targets(z, y, A, B, Y, mb, info, ws)
+    torch.cuda.synchronize()
+    assert info.item() == 124
+
+
+def test_statistics_deterministic_and_resumable():
+    """Same inputs in the same order give bitwise-equal S and K; stopping after two
+    micro-batches, saving S, K to the host and resuming gives the same bits."""
+    import torch
+    cfg = gen.custom_config("t9", blocks=2, d=520, n=1600, micro=400, C=5, k=16, r_a=4)
+    xs, zs, ys, As, Bs = host_inputs(cfg, range(2))
+    from paper_2608_03020_amd.step import BlockStep
+    x_all = padded_rows(np.stack([np.concatenate(xb) for xb in xs]))
+    z_all, y_all = to_dev(np.concatenate(zs)), to_dev(np.concatenate(ys))
+    A, B = to_dev(np.stack(As)), to_dev(np.stack(Bs))
+
+    def run(split=None):
+        st = BlockStep(cfg, 2)
+        st.reset()
+        for m in range(cfg.n_micro):
+            if split is not None and m == split:
+                S_h, K_h = st.S.cpu().numpy().copy(), st.K.cpu().numpy().copy()
+                st = BlockStep(cfg, 2)
+                st.S.copy_(torch.from_numpy(S_h))
+                st.K.copy_(torch.from_numpy(K_h))
+            lo, hi = cfg.micro_rows(m)
+            st.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B)
+        torch.cuda.synchronize()
+        return st.S.cpu().numpy(), st.K.cpu().numpy()
+
+    S1, K1 = run()
+    S2, K2 = run()
+    S3, K3 = run(split=2)
+    iu = np.triu_indices(cfg.d)
+    assert np.array_equal(S1[:, iu[0], iu[1]], S2[:, iu[0], iu[1]]) and np.array_equal(K1, K2)
+    assert np.array_equal(S1[:, iu[0], iu[1]], S3[:, iu[0], iu[1]]) and np.array_equal(K1, K3)
