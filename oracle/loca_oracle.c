@@ -38,8 +38,10 @@
  * ------------------------------------------------------------------------ */
 int loca_oracle_head_error(int64_t n, int64_t C, const double* z, const int32_t* y,
                            const double* w, double* E) {
-  for (int64_t t = 0; t < n; ++t) {
+  for (int64_t t = 0; t < n; ++t)
     if (y[t] < 0 || y[t] >= C) return (int)-(t + 1);
+#pragma omp parallel for schedule(static)
+  for (int64_t t = 0; t < n; ++t) {
     const double* zt = z + IDX(t, 0, C);
     double m = zt[0];
     for (int64_t c = 1; c < C; ++c)
@@ -62,6 +64,7 @@ int loca_oracle_head_error(int64_t n, int64_t C, const double* z, const int32_t*
  * ------------------------------------------------------------------------ */
 void loca_oracle_credit(int64_t n, int64_t C, int64_t k, int64_t d, const double* E,
                         const double* A, const double* B, double* Y, double* Q) {
+#pragma omp parallel for schedule(static)
   for (int64_t t = 0; t < n; ++t)
     for (int64_t j = 0; j < k; ++j) {
       double s = 0.0;
