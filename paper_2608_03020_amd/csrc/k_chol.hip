@@ -4,15 +4,17 @@
 //   (S + lam I) M = [S Lp | K]      (positive definite for lam > 0; no inverse)
 // solved for every (block, lam) pair of a call in one batched pass:
 //   1. Jacobi equilibration  A^ = D (S + lam I) D,  D = diag(S + lam I)^{-1/2};
-//   2. right-looking blocked Cholesky A^ = U^T U (U upper, row-major), panel
-//      width 64.  Per panel: one kernel factors the 64 x 64 diagonal block in
-//      LDS (every workgroup redundantly, so no extra launch) and applies
-//      U11^{-T} to its chunk of the row panel -- the right-hand sides ride
-//      along as extra columns, so the forward substitution is free; a second
-//      kernel applies the symmetric rank-64 update to the trailing matrix and
-//      the right-hand sides with matrix-core MFMA (fp32 32x32x2, or fp64
-//      16x16x4 in fp32 mode);
-//   3. back substitution U M' = Y by row blocks, M = D M'.
+//   2. right-looking blocked Cholesky A^ = U^T U (U upper, row-major) with
+//      P-wide panels (P = 128 in fp32, 64 in fp64).  Per panel, three launches
+//      batched over all matrices: the diagonal block is factored and inverted
+//      in LDS by one workgroup per matrix; the row panel U12 = U11^{-T} A12 is
+//      a matrix-core product with that inverse; the trailing matrix takes the
+//      symmetric rank-P update A22 -= U12^T U12.  The right-hand sides ride
+//      along as extra columns of the row panel and the update, so the forward
+//      substitution costs nothing extra.  Products use MFMA (fp32 32x32x2, or
+//      fp64 16x16x4 for fp64 statistics);
+//   3. back substitution U M' = Y by row blocks, each a product with U11^{-1},
+//      then M = D M'.
 // The first non-positive pivot is reported in dev_info (1-based).
 #include "loca_common.h"
 
@@ -20,8 +22,6 @@ namespace loca {
 
 namespace {
 
-constexpr int kP = 64;        // panel width
-constexpr int kCW = 64;       // column chunk of the panel kernel
 constexpr int kT = 256;       // threads
 constexpr int kMC = 16;       // right-hand-side columns per back-substitution workgroup
 
@@ -94,87 +94,100 @@ __global__ void k_sym_mul(int64_t d, int64_t r_prev, const ST* __restrict__ S, i
   out[b * d * r_prev + e] = s;
 }
 
-// ------------------------------------------------------------------ panel: factor U11, apply U11^{-T}
+// ------------------------------------------------------------------ matrix-core tile products
 
-// U11 of panel p is written to Ud (nm x d x kP): the workgroups of this launch still read the
-// unfactored block from F, so it must not be overwritten in place.
+// Per precision: panel width P (= output tile side), MFMA block side BLK and its K step.
+template <typename T> struct Mf;
+template <> struct Mf<float> {
+  static constexpr int P = 128, BLK = 32, KS = 2, NR = 16;
+  typedef f32x16_t acc_t;
+  static LOCA_DEV acc_t mma(float a, float b, acc_t c) { return mfma_f32x2(a, b, c); }
+  static LOCA_DEV int row(int lane, int r) { return mfma32_row(lane, r); }
+  static LOCA_DEV int col(int lane) { return lane & 31; }
+  static LOCA_DEV acc_t zero() { acc_t z; for (int r = 0; r < 16; ++r) z[r] = 0.f; return z; }
+};
+template <> struct Mf<double> {
+  static constexpr int P = 64, BLK = 16, KS = 4, NR = 4;
+  typedef f64x4_t acc_t;
+  static LOCA_DEV acc_t mma(double a, double b, acc_t c) { return mfma_f64(a, b, c); }
+  static LOCA_DEV int row(int lane, int r) { return (lane >> 4) + 4 * r; }
+  static LOCA_DEV int col(int lane) { return lane & 15; }
+  static LOCA_DEV acc_t zero() { return (acc_t){0.0, 0.0, 0.0, 0.0}; }
+};
+
+// acc[m][q] += sum_kk sP[kk][i] sQ[kk][j] over the wave's (P/2) x (P/2) quarter (wi, wj) of a
+// P x P output tile; sP, sQ are K x (P + pad) row-major LDS panels.
 template <typename T>
-__global__ __launch_bounds__(kT) void k_chol_panel(int64_t d, int64_t m, int64_t p, T* __restrict__ Fall,
-                                                   T* __restrict__ Rall, T* __restrict__ Udall,
-                                                   int32_t* __restrict__ dev_info) {
-  __shared__ T sU[kP][kP + 1];
-  __shared__ T sX[kP][kCW + 1];
-  const int64_t mi = blockIdx.y;
-  T* F = Fall + mi * d * d;
-  T* R = Rall + mi * d * m;
-  const int pw = (int)((d - p) < kP ? (d - p) : kP);
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kP * kP; e += kT) {
-    const int r = e / kP, c = e % kP;
-    sU[r][c] = (r < pw && c < pw && c >= r) ? F[(p + r) * d + p + c] : (T)0;
+LOCA_DEV void tile_mma(const T* sP, const T* sQ, int ld, int K, int wi, int wj, int lane,
+                       typename Mf<T>::acc_t (&acc)[2][2]) {
+  constexpr int BLK = Mf<T>::BLK, KS = Mf<T>::KS, WT = Mf<T>::P / 2;
+  const int kr = lane / BLK, cr = lane % BLK;
+  for (int kk = 0; kk < K; kk += KS) {
+    T a[2], b[2];
+#pragma unroll
+    for (int m = 0; m < 2; ++m) a[m] = sP[(kk + kr) * ld + wi * WT + m * BLK + cr];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) b[q] = sQ[(kk + kr) * ld + wj * WT + q * BLK + cr];
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int q = 0; q < 2; ++q) acc[m][q] = Mf<T>::mma(a[m], b[q], acc[m][q]);
   }
+}
+
+// ------------------------------------------------------------------ diagonal block: factor and invert
+
+// One workgroup per matrix: U11 = chol(A11) (upper) in LDS, then U11^{-1} by column-wise back
+// substitution.  The inverse replaces the diagonal block of F (its strict lower part is zeroed):
+// the row panel and the back substitution both apply U11^{-1} as a matrix product.
+template <typename T>
+__global__ __launch_bounds__(kT) void k_diag_block(int64_t d, int64_t p, T* __restrict__ Fall,
+                                                   int32_t* __restrict__ dev_info) {
+  constexpr int P = Mf<T>::P;
+  __shared__ T sU[P][P + 1];
+  __shared__ T sX[P][P + 1];
+  const int64_t mi = blockIdx.x;
+  T* F = Fall + mi * d * d;
+  const int pw = (int)((d - p) < P ? (d - p) : P);
+  const int tid = threadIdx.x;
+  g2s_block<T, P, P, kT>(&sU[0][0], P + 1, F + p * d + p, d, pw, pw);
   __syncthreads();
-  // unblocked right-looking Cholesky of the diagonal block (upper factor)
+  // 16 x 16 thread grid for the rank-1 updates (no runtime integer division)
+  const int ty = tid >> 4, tx = tid & 15;
   for (int j = 0; j < pw; ++j) {
     const T piv = sU[j][j];
-    if (!(piv > (T)0) && tid == 0 && blockIdx.x == 0) atomicCAS(&dev_info[mi], 0, (int32_t)(p + j + 1));
+    if (!(piv > (T)0) && tid == 0) atomicCAS(&dev_info[mi], 0, (int32_t)(p + j + 1));
     const T ujj = sqrt(piv);
     __syncthreads();
     for (int c = j + tid; c < pw; c += kT) sU[j][c] = (c == j) ? ujj : sU[j][c] / ujj;
     __syncthreads();
-    const int rem = pw - j - 1;
-    for (int e = tid; e < rem * rem; e += kT) {
-      const int r = j + 1 + e / rem, c = j + 1 + e % rem;
-      if (c >= r) sU[r][c] -= sU[j][r] * sU[j][c];
+    for (int r = j + 1 + ty; r < pw; r += 16) {
+      const T ujr = sU[j][r];
+      for (int c = j + 1 + tx; c < pw; c += 16)
+        if (c >= r) sU[r][c] -= ujr * sU[j][c];
     }
     __syncthreads();
   }
-  if (blockIdx.x == 0) {
-    T* Ud = Udall + mi * d * kP + p * kP;  // rows p..p+pw, kP columns
-    for (int e = tid; e < kP * kP; e += kT) {
-      const int r = e / kP, c = e % kP;
-      if (r < pw) Ud[r * kP + c] = (c >= r && c < pw) ? sU[r][c] : (T)0;
-    }
-  }
-  // this workgroup's chunk: columns of F right of the block, then the RHS columns
-  const int64_t nrem = d - p - pw;
-  const int64_t nchF = (nrem + kCW - 1) / kCW;
-  const bool rhs = (int64_t)blockIdx.x >= nchF;
-  const int64_t c0 = rhs ? ((int64_t)blockIdx.x - nchF) * kCW : p + pw + (int64_t)blockIdx.x * kCW;
-  const int64_t cend = rhs ? m : d;
-  if (c0 >= cend) return;
-  const int cw = (int)((cend - c0) < kCW ? (cend - c0) : kCW);
-  for (int e = tid; e < kP * kCW; e += kT) {
-    const int r = e / kCW, c = e % kCW;
-    T v = (T)0;
-    if (r < pw && c < cw) v = rhs ? R[(p + r) * m + c0 + c] : F[(p + r) * d + c0 + c];
-    sX[r][c] = v;
-  }
+  // X = U^{-1} (upper), rows from the bottom up: once row i of X is final, its
+  // contribution U[r][i] X[i][j] is added to the partial sums of every row r < i.
+  for (int r = ty; r < P; r += 16)
+    for (int c = tx; c < P; c += 16) sX[r][c] = (T)0;  // partial sums
   __syncthreads();
-  // forward substitution U11^T X = A (U11^T lower): row r final, then eliminate below
-  for (int r = 0; r < pw; ++r) {
-    for (int c = tid; c < cw; c += kT) sX[r][c] /= sU[r][r];
+  for (int i = pw - 1; i >= 0; --i) {
+    const T inv = (T)1 / sU[i][i];
+    for (int j = i + tid; j < pw; j += kT) sX[i][j] = ((j == i ? (T)1 : (T)0) - sX[i][j]) * inv;
     __syncthreads();
-    const int rem = pw - r - 1;
-    for (int e = tid; e < rem * cw; e += kT) {
-      const int s = r + 1 + e / cw, c = e % cw;
-      sX[s][c] -= sU[r][s] * sX[r][c];
+    for (int r = ty; r < i; r += 16) {
+      const T uri = sU[r][i];
+      for (int j = i + tx; j < pw; j += 16) sX[r][j] += uri * sX[i][j];
     }
     __syncthreads();
   }
-  for (int e = tid; e < pw * cw; e += kT) {
-    const int r = e / cw, c = e % cw;
-    if (rhs) R[(p + r) * m + c0 + c] = sX[r][c];
-    else F[(p + r) * d + c0 + c] = sX[r][c];
-  }
+  for (int r = ty; r < pw; r += 16)
+    for (int c = tx; c < pw; c += 16) F[(p + r) * d + p + c] = (c >= r) ? sX[r][c] : (T)0;
 }
 
-// ------------------------------------------------------------------ trailing update (fp32 MFMA)
-
-// Jobs: upper 128 x 128 tiles of the trailing matrix, then 128 x 128 tiles of the RHS rows.
-// Out -= Panel^T Q with Panel = rows [p, p+pw) of F (columns of the tile's rows) and
-// Q = the same rows of F (tile's columns) or of R.
-constexpr int kUT = 128;
+// ------------------------------------------------------------------ panel products (row panel, trailing update)
 
 LOCA_DEV void upper_tile_c(int u, int T, int& I, int& J) {
   int i = 0;
@@ -183,219 +196,193 @@ LOCA_DEV void upper_tile_c(int u, int T, int& I, int& J) {
   J = i + u;
 }
 
-__global__ __launch_bounds__(kT) void k_chol_update_f32(int64_t d, int64_t m, int64_t p, float* __restrict__ Fall,
-                                                        float* __restrict__ Rall) {
-  __shared__ float sP[kP][kUT + 4];
-  __shared__ float sQ[kP][kUT + 4];
+// Out[i][j] (op)= sum_{kk < K} Pn[kk][i] Qn[kk][j] for one P x P output tile, with the
+// K rows streamed through LDS in chunks of kKC rows, double-buffered via registers.
+//   kRowPanel: Pn = U11^{-1} (diagonal block), Qn = the chunk's columns of the row
+//              panel (F or R), Out = the same chunk, overwritten: U12 = U11^{-T} A12;
+//   kTrailing: Pn, Qn = the row panel U12 (F) / its RHS rows (R), Out -= on the upper
+//              tiles of the trailing matrix and on the RHS rows below the panel.
+constexpr int kKC = 32;
+enum PanelJob { kRowPanel = 0, kTrailing = 1 };
+
+template <typename T, int JOB>
+__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_panel_product(int64_t d, int64_t m, int64_t p, T* __restrict__ Fall,
+                                                      T* __restrict__ Rall) {
+  constexpr int P = Mf<T>::P, LD = P + 4, PER = (kKC * P) / kT;
+  __shared__ T sP[2][kKC * LD];
+  __shared__ T sQ[2][kKC * LD];
   const int64_t mi = blockIdx.y;
-  float* F = Fall + mi * d * d;
-  float* R = Rall + mi * d * m;
-  const int pw = (int)((d - p) < kP ? (d - p) : kP);
+  T* F = Fall + mi * d * d;
+  T* R = Rall + mi * d * m;
+  const int pw = (int)((d - p) < P ? (d - p) : P);
   const int64_t off = p + pw, nrem = d - off;
-  const int T2 = (int)((nrem + kUT - 1) / kUT);
-  const int nU = T2 * (T2 + 1) / 2;
-  const int TM = (int)((m + kUT - 1) / kUT);
-  int I, J;
-  bool rhs = (int)blockIdx.x >= nU;
-  if (!rhs) upper_tile_c(blockIdx.x, T2, I, J);
-  else { const int u = blockIdx.x - nU; I = u / TM; J = u % TM; }
-  const int64_t r0 = off + (int64_t)I * kUT;                 // output rows (and panel columns)
-  const int64_t c0 = rhs ? (int64_t)J * kUT : off + (int64_t)J * kUT;
-  const int64_t cend = rhs ? m : d;
+  const int64_t nchF = (nrem + P - 1) / P;
+  bool rhs, diag = false;
+  int64_t orow, ocol, ocend;  // output tile origin (row in F/R, column) and column end
+  const T* gP;                // row kk of Pn at gP + kk * ldp, column i at + i
+  const T* gQ;
+  int64_t ldq, prows_ok;
+  if (JOB == kRowPanel) {
+    rhs = (int64_t)blockIdx.x >= nchF;
+    ocol = rhs ? ((int64_t)blockIdx.x - nchF) * P : off + (int64_t)blockIdx.x * P;
+    ocend = rhs ? m : d;
+    orow = p;
+    gP = F + p * d + p;
+    prows_ok = pw;
+    gQ = rhs ? R + p * m + ocol : F + p * d + ocol;
+    ldq = rhs ? m : d;
+  } else {
+    const int T2 = (int)((nrem + P - 1) / P);
+    const int nU = T2 * (T2 + 1) / 2;
+    const int TM = (int)((m + P - 1) / P);
+    int I, J;
+    rhs = (int)blockIdx.x >= nU;
+    if (!rhs) upper_tile_c(blockIdx.x, T2, I, J);
+    else { const int u = blockIdx.x - nU; I = u / TM; J = u % TM; }
+    diag = !rhs && I == J;
+    orow = off + (int64_t)I * P;
+    ocol = rhs ? (int64_t)J * P : off + (int64_t)J * P;
+    ocend = rhs ? m : d;
+    gP = F + p * d + orow;
+    prows_ok = d - orow;  // columns of Pn that exist
+    gQ = rhs ? R + p * m + ocol : F + p * d + ocol;
+    ldq = rhs ? m : d;
+  }
+  const int64_t pcols_ok = (JOB == kRowPanel) ? pw : prows_ok;
+  const int64_t qcols_ok = ocend - ocol;
   const int tid = threadIdx.x;
-  for (int e = tid; e < kP * kUT; e += kT) {
-    const int kk = e / kUT, c = e % kUT;
-    float a = 0.f, q = 0.f;
-    if (kk < pw) {
-      if (r0 + c < d) a = F[(p + kk) * d + r0 + c];
-      if (c0 + c < cend) q = rhs ? R[(p + kk) * m + c0 + c] : F[(p + kk) * d + c0 + c];
-    }
-    sP[kk][c] = a;
-    sQ[kk][c] = q;
-  }
-  __syncthreads();
   const int lane = tid & 63, wid = tid >> 6, wi = wid >> 1, wj = wid & 1;
-  if (!rhs && I == J && wi > wj) return;  // strictly lower quarter of a diagonal tile
-  f32x16_t acc[2][2];
+  const bool active = !(diag && wi > wj);  // strictly lower quarter of a diagonal tile
+
+  T rp[PER], rq[PER];
+  auto load_chunk = [&](int k0) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = tid + q * kT;
+      const int kk = e / P, c = e % P;
+      const bool okk = k0 + kk < pw;
+      rp[q] = ld_or_zero(gP, (int64_t)(k0 + kk) * d + c, okk && c < pcols_ok);
+      rq[q] = ld_or_zero(gQ, (int64_t)(k0 + kk) * ldq + c, okk && c < qcols_ok);
+    }
+  };
+  auto store_chunk = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = tid + q * kT;
+      sP[buf][(e / P) * LD + e % P] = rp[q];
+      sQ[buf][(e / P) * LD + e % P] = rq[q];
+    }
+  };
+
+  typename Mf<T>::acc_t acc[2][2];
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-  for (int kk = 0; kk < kP; kk += 2) {
-    float fa[2], fb[2];
-#pragma unroll
-    for (int a = 0; a < 2; ++a) fa[a] = sP[kk + (lane >> 5)][wi * 64 + 32 * a + (lane & 31)];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) fb[b] = sQ[kk + (lane >> 5)][wj * 64 + 32 * b + (lane & 31)];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = mfma_f32x2(fa[a], fb[b], acc[a][b]);
+    for (int b = 0; b < 2; ++b) acc[a][b] = Mf<T>::zero();
+  const int nk = (pw + kKC - 1) / kKC;
+  load_chunk(0);
+  store_chunk(0);
+  __syncthreads();
+  for (int kc = 0; kc < nk; ++kc) {
+    const int cur = kc & 1;
+    if (kc + 1 < nk) load_chunk((kc + 1) * kKC);
+    if (active) tile_mma<T>(sP[cur], sQ[cur], LD, kKC, wi, wj, lane, acc);
+    if (kc + 1 < nk) store_chunk(cur ^ 1);
+    __syncthreads();
   }
+  if (!active) return;
+  T* Out = rhs ? R : F;
+  const int64_t ldo = rhs ? m : d;
+  const int64_t rend = (JOB == kRowPanel) ? p + pw : d;
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < 2; ++b) {
+      T old[Mf<T>::NR];
+      const int64_t col = ocol + wj * (P / 2) + b * Mf<T>::BLK + Mf<T>::col(lane);
+      const int64_t rbase = orow + wi * (P / 2) + a * Mf<T>::BLK;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = r0 + wi * 64 + 32 * a + mfma32_row(lane, r);
-        const int64_t col = c0 + wj * 64 + 32 * b + mfma32_col(lane);
-        if (row < d && col < cend) {
-          if (rhs) R[row * m + col] -= acc[a][b][r];
-          else if (col >= row) F[row * d + col] -= acc[a][b][r];
-        }
+      for (int r = 0; r < Mf<T>::NR; ++r) {
+        const int64_t row = rbase + Mf<T>::row(lane, r);
+        const bool ok = row < rend && col < ocend && (JOB == kRowPanel || rhs || col >= row);
+        if (JOB == kTrailing) old[r] = ld_or_zero(Out, row * ldo + col, ok);
       }
+#pragma unroll
+      for (int r = 0; r < Mf<T>::NR; ++r) {
+        const int64_t row = rbase + Mf<T>::row(lane, r);
+        const bool ok = row < rend && col < ocend && (JOB == kRowPanel || rhs || col >= row);
+        if (ok) Out[row * ldo + col] = (JOB == kTrailing) ? old[r] - acc[a][b][r] : acc[a][b][r];
+      }
+    }
 }
 
-// fp64 variant: 64 x 64 tiles, 4 waves of 32 x 32 (2 x 2 blocks of 16 x 16).
-constexpr int kUT64 = 64;
+// ------------------------------------------------------------------ back substitution, one row block
 
-__global__ __launch_bounds__(kT) void k_chol_update_f64(int64_t d, int64_t m, int64_t p, double* __restrict__ Fall,
-                                                        double* __restrict__ Rall) {
-  __shared__ double sP[kP][kUT64 + 1];
-  __shared__ double sQ[kP][kUT64 + 1];
-  const int64_t mi = blockIdx.y;
-  double* F = Fall + mi * d * d;
-  double* R = Rall + mi * d * m;
-  const int pw = (int)((d - p) < kP ? (d - p) : kP);
-  const int64_t off = p + pw, nrem = d - off;
-  const int T2 = (int)((nrem + kUT64 - 1) / kUT64);
-  const int nU = T2 * (T2 + 1) / 2;
-  const int TM = (int)((m + kUT64 - 1) / kUT64);
-  int I, J;
-  bool rhs = (int)blockIdx.x >= nU;
-  if (!rhs) upper_tile_c(blockIdx.x, T2, I, J);
-  else { const int u = blockIdx.x - nU; I = u / TM; J = u % TM; }
-  const int64_t r0 = off + (int64_t)I * kUT64;
-  const int64_t c0 = rhs ? (int64_t)J * kUT64 : off + (int64_t)J * kUT64;
-  const int64_t cend = rhs ? m : d;
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kP * kUT64; e += kT) {
-    const int kk = e / kUT64, c = e % kUT64;
-    double a = 0.0, q = 0.0;
-    if (kk < pw) {
-      if (r0 + c < d) a = F[(p + kk) * d + r0 + c];
-      if (c0 + c < cend) q = rhs ? R[(p + kk) * m + c0 + c] : F[(p + kk) * d + c0 + c];
-    }
-    sP[kk][c] = a;
-    sQ[kk][c] = q;
-  }
-  __syncthreads();
-  const int lane = tid & 63, wid = tid >> 6, wi = wid >> 1, wj = wid & 1;
-  f64x4_t acc[2][2];
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b) acc[a][b] = (f64x4_t){0.0, 0.0, 0.0, 0.0};
-  for (int kk = 0; kk < kP; kk += 4) {
-    double fa[2], fb[2];
-#pragma unroll
-    for (int a = 0; a < 2; ++a) fa[a] = sP[kk + (lane >> 4)][wi * 32 + 16 * a + (lane & 15)];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) fb[b] = sQ[kk + (lane >> 4)][wj * 32 + 16 * b + (lane & 15)];
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int b = 0; b < 2; ++b) acc[a][b] = mfma_f64(fa[a], fb[b], acc[a][b]);
-  }
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t row = r0 + wi * 32 + 16 * a + (lane >> 4) + 4 * r;
-        const int64_t col = c0 + wj * 32 + 16 * b + (lane & 15);
-        if (row < d && col < cend) {
-          if (rhs) R[row * m + col] -= acc[a][b][r];
-          else if (col >= row) F[row * d + col] -= acc[a][b][r];
-        }
-      }
-}
-
-// ------------------------------------------------------------------ back substitution U M' = Y, M = D M'
-
+// Rows [p, p+pw) of U M' = Y:  M'_p = U11^{-1} (Y_p - U_{p, >=p+pw} M'_{>=p+pw}); the solved
+// rows below p already hold M' in R.  One workgroup per (matrix, kMC right-hand sides).
 template <typename T>
-__global__ __launch_bounds__(kT) void k_chol_backsolve(int64_t d, int64_t m, const T* __restrict__ Fall,
-                                                       const T* __restrict__ Udall, T* __restrict__ Rall,
-                                                       const T* __restrict__ Dall, float* __restrict__ Mout,
-                                                       int64_t m_bstride) {
-  __shared__ T sU[kP][kP + 1];
-  __shared__ T sX[kP][kMC + 1];
-  __shared__ T sAcc[kP][kMC + 1];
+__global__ __launch_bounds__(kT) void k_back_block(int64_t d, int64_t m, int64_t p, const T* __restrict__ Fall,
+                                                   T* __restrict__ Rall) {
+  constexpr int P = Mf<T>::P, JC = 64, PER = (P * kMC) / kT;
+  __shared__ T sU[P][JC + 1];
+  __shared__ T sX[JC][kMC + 1];
+  __shared__ T sI[P][P + 1];
+  __shared__ T sAcc[P][kMC + 1];
   const int64_t mi = blockIdx.y;
   const T* F = Fall + mi * d * d;
   T* R = Rall + mi * d * m;
   const int64_t c0 = (int64_t)blockIdx.x * kMC;
   const int mc = (int)((m - c0) < kMC ? (m - c0) : kMC);
+  const int pw = (int)((d - p) < P ? (d - p) : P);
+  const int64_t p1 = p + pw;
   const int tid = threadIdx.x;
-  const int64_t nblk = (d + kP - 1) / kP;
-  for (int64_t pb = nblk - 1; pb >= 0; --pb) {
-    const int64_t p0 = pb * kP;
-    const int pw = (int)((d - p0) < kP ? (d - p0) : kP);
-    const int64_t p1 = p0 + pw;
-    // acc = sum_{j >= p1} U[p0 + r][j] M'[j][c]; each thread owns (r, c) pairs e = tid + 256 q
-    T acc[(kP * kMC) / kT];
+  T acc[PER];
 #pragma unroll
-    for (int q = 0; q < (kP * kMC) / kT; ++q) acc[q] = (T)0;
-    for (int64_t j0 = p1; j0 < d; j0 += kP) {
-      const int jw = (int)((d - j0) < kP ? (d - j0) : kP);
-      __syncthreads();
-      for (int e = tid; e < kP * kP; e += kT) {
-        const int r = e / kP, jj = e % kP;
-        sU[r][jj] = (r < pw && jj < jw) ? F[(p0 + r) * d + j0 + jj] : (T)0;
-      }
-      for (int e = tid; e < kP * kMC; e += kT) {
-        const int jj = e / kMC, c = e % kMC;
-        sX[jj][c] = (jj < jw && c < mc) ? R[(j0 + jj) * m + c0 + c] : (T)0;
-      }
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < (kP * kMC) / kT; ++q) {
-        const int e = tid + kT * q;
-        const int r = e / kMC, c = e % kMC;
-        T s = acc[q];
-        for (int jj = 0; jj < kP; ++jj) s += sU[r][jj] * sX[jj][c];
-        acc[q] = s;
-      }
-    }
+  for (int q = 0; q < PER; ++q) acc[q] = (T)0;
+  for (int64_t j0 = p1; j0 < d; j0 += JC) {
+    const int jw = (int)((d - j0) < JC ? (d - j0) : JC);
     __syncthreads();
-    for (int e = tid; e < kP * kP; e += kT) {
-      const int r = e / kP, c = e % kP;
-      sU[r][c] = (r < pw && c < pw) ? Udall[mi * d * kP + (p0 + r) * kP + c] : (T)0;
-    }
+    g2s_block<T, P, JC, kT>(&sU[0][0], JC + 1, F + p * d + j0, d, pw, jw);
+    g2s_block<T, JC, kMC, kT>(&sX[0][0], kMC + 1, R + j0 * m + c0, m, jw, mc);
+    __syncthreads();
 #pragma unroll
-    for (int q = 0; q < (kP * kMC) / kT; ++q) {
+    for (int q = 0; q < PER; ++q) {
       const int e = tid + kT * q;
       const int r = e / kMC, c = e % kMC;
-      sAcc[r][c] = (r < pw && c < mc) ? R[(p0 + r) * m + c0 + c] - acc[q] : (T)0;
-    }
-    __syncthreads();
-    for (int r = pw - 1; r >= 0; --r) {
-      if (tid < mc) sAcc[r][tid] /= sU[r][r];
-      __syncthreads();
-      for (int e = tid; e < r * mc; e += kT) {
-        const int s = e / mc, c = e % mc;
-        sAcc[s][c] -= sU[s][r] * sAcc[r][c];
-      }
-      __syncthreads();
-    }
-    for (int e = tid; e < pw * mc; e += kT) {
-      const int r = e / mc, c = e % mc;
-      R[(p0 + r) * m + c0 + c] = sAcc[r][c];
+      T s = acc[q];
+      for (int jj = 0; jj < JC; ++jj) s += sU[r][jj] * sX[jj][c];
+      acc[q] = s;
     }
   }
   __syncthreads();
-  const T* D = Dall + mi * d;
-  float* M = Mout + mi * m_bstride;
-  for (int64_t e = tid; e < d * mc; e += kT) {
-    const int64_t i = e / mc;
-    const int c = (int)(e % mc);
-    M[i * m + c0 + c] = (float)(D[i] * R[i * m + c0 + c]);
+  g2s_block<T, P, P, kT>(&sI[0][0], P + 1, F + p * d + p, d, pw, pw);  // U11^{-1}
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = tid + kT * q;
+    const int r = e / kMC, c = e % kMC;
+    sAcc[r][c] = ld_or_zero(R, (p + r) * m + c0 + c, r < pw && c < mc) - acc[q];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int e = tid + kT * q;
+    const int r = e / kMC, c = e % kMC;
+    T s = (T)0;
+    for (int jj = r; jj < pw; ++jj) s += sI[r][jj] * sAcc[jj][c];
+    if (r < pw && c < mc) R[(p + r) * m + c0 + c] = s;
   }
 }
+
+// M = D M' (undo the equilibration), float output.
+template <typename T>
+__global__ void k_unscale(int64_t d, int64_t m, const T* __restrict__ Rall, const T* __restrict__ Dall,
+                          float* __restrict__ Mout, int64_t m_bstride) {
+  const int64_t mi = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= d * m) return;
+  Mout[mi * m_bstride + e] = (float)(Dall[mi * d + e / m] * Rall[mi * d * m + e]);
+}
+
 
 template <typename T>
 size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) {
@@ -405,7 +392,6 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
   s += align256(sizeof(T) * nm * d);             // D
   s += align256(sizeof(double) * nb * d * (r_prev > 0 ? r_prev : 1));  // S Lp
   s += 256;                                                            // lambdas
-  s += align256(sizeof(T) * nm * d * kP);                              // diagonal blocks U11
   return s;
 }
 
@@ -420,7 +406,6 @@ hipError_t run_solve(const SolveArgs& a) {
   Lams lams;
   for (int i = 0; i < 8; ++i) lams.v[i] = (i < nl) ? a.lambdas[i] : 0.0;
   double* dlam = (double*)(p + align256(sizeof(double) * a.nb * d * (a.r_prev > 0 ? a.r_prev : 1)));
-  T* Ud = (T*)((char*)dlam + 256);
   // the host lambdas travel by value into a one-wave kernel (no copy from pageable memory)
   k_set_lambdas<<<1, 64, 0, a.stream>>>(lams, dlam, (int)nl);
   k_fill_zero_i32<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
@@ -439,25 +424,25 @@ hipError_t run_solve(const SolveArgs& a) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  for (int64_t pp = 0; pp < d; pp += kP) {
-    const int64_t pw = (d - pp) < kP ? (d - pp) : kP;
+  constexpr int P = Mf<T>::P;
+  for (int64_t pp = 0; pp < d; pp += P) {
+    const int64_t pw = (d - pp) < P ? (d - pp) : P;
     const int64_t nrem = d - pp - pw;
-    const int64_t nch = (nrem + kCW - 1) / kCW + (m + kCW - 1) / kCW;
-    k_chol_panel<T><<<dim3((unsigned)nch, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R, Ud, a.dev_info);
+    k_diag_block<T><<<(unsigned)nm, kT, 0, a.stream>>>(d, pp, F, a.dev_info);
+    const int64_t nch = (nrem + P - 1) / P + (m + P - 1) / P;
+    k_panel_product<T, kRowPanel><<<dim3((unsigned)nch, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R);
     if (nrem > 0) {
-      const int64_t ut = sizeof(T) == 4 ? kUT : kUT64;
-      const int64_t T2 = (nrem + ut - 1) / ut;
-      const int64_t jobs = T2 * (T2 + 1) / 2 + T2 * ((m + ut - 1) / ut);
-      if (sizeof(T) == 4)
-        k_chol_update_f32<<<dim3((unsigned)jobs, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, (float*)F, (float*)R);
-      else
-        k_chol_update_f64<<<dim3((unsigned)jobs, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, (double*)F, (double*)R);
+      const int64_t T2 = (nrem + P - 1) / P;
+      const int64_t jobs = T2 * (T2 + 1) / 2 + T2 * ((m + P - 1) / P);
+      k_panel_product<T, kTrailing><<<dim3((unsigned)jobs, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  k_chol_backsolve<T><<<dim3((unsigned)((m + kMC - 1) / kMC), (unsigned)nm), kT, 0, a.stream>>>(d, m, F, Ud, R, D, a.m_out,
-                                                                                                a.m_bstride);
+  for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P)
+    k_back_block<T><<<dim3((unsigned)((m + kMC - 1) / kMC), (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R);
+  k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, a.stream>>>(d, m, R, D, a.m_out,
+                                                                                          a.m_bstride);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.w_dense_out) {

@@ -35,43 +35,52 @@ LOCA_DEV void upper_tile(int u, int T, int& I, int& J) {
 
 // ------------------------------------------------------------------ bf16 tile staging
 
-// One stage = kBK token rows x BM columns of X starting at column c0.
-template <int BM>
+// One stage = kBK token rows x BM columns of X starting at column c0, loaded by NT threads
+// with 16-byte vector loads (8 columns per chunk) and zero fill outside [0, n) x [0, d).
+template <int BM, int NT>
 struct XStage {
   static constexpr int kChunksPerRow = BM / 8;
   static constexpr int kChunks = kBK * kChunksPerRow;
-  static constexpr int kPerThread = kChunks / kThreads;
+  static constexpr int kPerThread = kChunks / NT;
+  static_assert(kChunks % NT == 0, "stage must split evenly over the threads");
   uint4 r[kPerThread];
 
   LOCA_DEV void load(const uint16_t* __restrict__ X, int64_t ldx, int64_t n, int64_t d, int64_t t0,
                      int64_t c0) {
+    // full 16-byte chunks: one unconditional vector load from a valid address, then select
 #pragma unroll
     for (int q = 0; q < kPerThread; ++q) {
-      const int e = threadIdx.x + q * kThreads;
+      const int e = threadIdx.x + q * NT;
       const int row = e / kChunksPerRow, ch = e % kChunksPerRow;
       const int64_t t = t0 + row, col = c0 + 8 * ch;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (t < n) {
-        const uint16_t* p = X + t * ldx + col;
-        if (col + 8 <= d) {
-          v = *(const uint4*)p;
-        } else if (col < d) {
+      const bool full = (t < n) && (col + 8 <= d);
+      const uint4 v = *(const uint4*)(X + (full ? t * ldx + col : 0));
+      r[q] = full ? v : make_uint4(0, 0, 0, 0);
+    }
+    // the ragged last chunk of each row (only when d % 8 != 0)
+    if (d & 7) {
+#pragma unroll
+      for (int q = 0; q < kPerThread; ++q) {
+        const int e = threadIdx.x + q * NT;
+        const int row = e / kChunksPerRow, ch = e % kChunksPerRow;
+        const int64_t t = t0 + row, col = c0 + 8 * ch;
+        if (t < n && col < d && col + 8 > d) {
+          const uint16_t* p = X + t * ldx + col;
           uint16_t h[8];
 #pragma unroll
           for (int u = 0; u < 8; ++u) h[u] = (col + u < d) ? p[u] : (uint16_t)0;
-          v.x = h[0] | ((uint32_t)h[1] << 16);
-          v.y = h[2] | ((uint32_t)h[3] << 16);
-          v.z = h[4] | ((uint32_t)h[5] << 16);
-          v.w = h[6] | ((uint32_t)h[7] << 16);
+          r[q].x = h[0] | ((uint32_t)h[1] << 16);
+          r[q].y = h[2] | ((uint32_t)h[3] << 16);
+          r[q].z = h[4] | ((uint32_t)h[5] << 16);
+          r[q].w = h[6] | ((uint32_t)h[7] << 16);
         }
       }
-      r[q] = v;
     }
   }
   LOCA_DEV void store(uint16_t* s, int ld) const {
 #pragma unroll
     for (int q = 0; q < kPerThread; ++q) {
-      const int e = threadIdx.x + q * kThreads;
+      const int e = threadIdx.x + q * NT;
       const int row = e / kChunksPerRow, ch = e % kChunksPerRow;
       *(uint4*)(s + row * ld + 8 * ch) = r[q];
     }
@@ -80,18 +89,20 @@ struct XStage {
 
 // ------------------------------------------------------------------ S += X^T X (bf16)
 
-// BM x BM tiles, 4 waves in a 2 x 2 grid of WM x WM wave tiles.
-template <int BM>
-__global__ __launch_bounds__(kThreads) void k_gram_bf16(int64_t n, int64_t d,
-                                                        const uint16_t* __restrict__ Xall, int64_t ldx,
-                                                        int64_t x_bstride, float* __restrict__ Sall,
-                                                        int64_t s_bstride, double* __restrict__ diag_part) {
-  constexpr int WM = BM / 2;
-  constexpr int NB = WM / 32;          // 32x32 MFMA blocks per wave side
+// BM x BM tiles of S on or above the diagonal; WGM x WGN waves, each owning a
+// (BM/WGM) x (BM/WGN) block of 32 x 32 MFMA tiles.
+template <int BM, int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16(int64_t n, int64_t d,
+                                                             const uint16_t* __restrict__ Xall, int64_t ldx,
+                                                             int64_t x_bstride, float* __restrict__ Sall,
+                                                             int64_t s_bstride, double* __restrict__ diag_part) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BM / WGN;
+  constexpr int NBM = WM / 32, NBN = WN / 32;
   constexpr int LDT = BM + 16;         // padded row (conflict-free transpose reads)
   __shared__ __attribute__((aligned(16))) uint16_t sA[2][kBK * LDT];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][kBK * LDT];
-  __shared__ double sred[kThreads / 64];
+  __shared__ double sred[NT / 64];
 
   const int T = (int)((d + BM - 1) / BM);
   int I, J;
@@ -102,18 +113,19 @@ __global__ __launch_bounds__(kThreads) void k_gram_bf16(int64_t n, int64_t d,
   float* S = Sall + b * s_bstride;
 
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int wi = wid >> 1, wj = wid & 1;
-  const bool active = !(diag && wi > wj);  // strictly-lower wave tile of a diagonal tile
+  const int wi = wid / WGN, wj = wid % WGN;
+  // a wave tile entirely below the diagonal of a diagonal tile has nothing to do
+  const bool active = !(diag && (wj + 1) * WN <= wi * WM);
 
-  f32x16_t acc[NB][NB];
+  f32x16_t acc[NBM][NBN];
 #pragma unroll
-  for (int m = 0; m < NB; ++m)
+  for (int m = 0; m < NBM; ++m)
 #pragma unroll
-    for (int q = 0; q < NB; ++q)
+    for (int q = 0; q < NBN; ++q)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][q][r] = 0.f;
 
-  XStage<BM> ra, rb;
+  XStage<BM, NT> ra, rb;
   const int64_t cI = (int64_t)I * BM, cJ = (int64_t)J * BM;
   const int nk = (int)((n + kBK - 1) / kBK);
   ra.load(X, ldx, n, d, 0, cI);
@@ -133,15 +145,15 @@ __global__ __launch_bounds__(kThreads) void k_gram_bf16(int64_t n, int64_t d,
       const uint16_t* tB = diag ? sA[cur] : sB[cur];
 #pragma unroll
       for (int ks = 0; ks < kBK; ks += 16) {
-        bf16x8_t fa[NB], fb[NB];
+        bf16x8_t fb[NBN];
 #pragma unroll
-        for (int m = 0; m < NB; ++m) fa[m] = frag32_tr(tA, LDT, wi * WM + 32 * m, ks, lane);
+        for (int q = 0; q < NBN; ++q) fb[q] = frag32_tr(tB, LDT, wj * WN + 32 * q, ks, lane);
 #pragma unroll
-        for (int q = 0; q < NB; ++q) fb[q] = frag32_tr(tB, LDT, wj * WM + 32 * q, ks, lane);
+        for (int m = 0; m < NBM; ++m) {
+          const bf16x8_t fa = frag32_tr(tA, LDT, wi * WM + 32 * m, ks, lane);
 #pragma unroll
-        for (int m = 0; m < NB; ++m)
-#pragma unroll
-          for (int q = 0; q < NB; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
+          for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa, fb[q], acc[m][q]);
+        }
       }
     }
     if (kt + 1 < nk) {
@@ -154,18 +166,26 @@ __global__ __launch_bounds__(kThreads) void k_gram_bf16(int64_t n, int64_t d,
   double dsum = 0.0;
   if (active) {
 #pragma unroll
-    for (int m = 0; m < NB; ++m)
+    for (int m = 0; m < NBM; ++m)
 #pragma unroll
-      for (int q = 0; q < NB; ++q)
+      for (int q = 0; q < NBN; ++q) {
+        // read the 16 old values of this MFMA block together, then add and store
+        float old[16];
+        int64_t idx[16];
+        bool ok[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = cI + wi * WM + 32 * m + mfma32_row(lane, r);
-          const int64_t col = cJ + wj * WM + 32 * q + mfma32_col(lane);
-          if (row < d && col < d) {
-            S[row * d + col] += acc[m][q][r];
-            if (diag && row == col) dsum += (double)acc[m][q][r];
-          }
+          const int64_t col = cJ + wj * WN + 32 * q + mfma32_col(lane);
+          ok[r] = row < d && col < d;
+          idx[r] = row * d + col;
+          old[r] = ld_or_zero(S, idx[r], ok[r]);
+          if (diag && ok[r] && row == col) dsum += (double)acc[m][q][r];
         }
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (ok[r]) S[idx[r]] = old[r] + acc[m][q][r];
+      }
   }
   if (diag) {
     const double tot = block_sum(dsum, sred);
@@ -203,20 +223,27 @@ __global__ __launch_bounds__(kThreads) void k_cross_bf16(int64_t n, int64_t d, i
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[m][q][r] = 0.f;
 
-  XStage<BM> ra;
+  XStage<BM, kThreads> ra;
   // Y staging: kBK rows x k floats, converted to hi/lo bf16 columns [0,k) and [k,2k)
   auto load_y = [&](int64_t t0, int buf) {
-    for (int e = threadIdx.x; e < kBK * YB / 2; e += kThreads) {
-      const int row = e / (YB / 2), c = e % (YB / 2);
+    // columns [0, k): hi = bf16(y), [k, 2k): lo = bf16(y - hi), [2k, YB): zero
+    constexpr int PER = (kBK * YB + kThreads - 1) / kThreads;
+    float v[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      const int row = e / YB, c = e % YB;
       const int64_t t = t0 + row;
-      float v = (t < n && c < k) ? Y[t * k + c] : 0.f;
-      const uint16_t hi = f32_to_bf16(v);
-      const uint16_t lo = f32_to_bf16(v - bf16_to_f32(hi));
-      if (c < k) {
-        sY[buf][row * LDY + c] = hi;
-        sY[buf][row * LDY + k + c] = lo;
-      } else if (c + k < YB) {
-        sY[buf][row * LDY + k + c] = 0;  // padding columns [2k, YB)
+      const int cc = c < k ? c : c - (int)k;
+      v[q] = ld_or_zero(Y, t * k + cc, e < kBK * YB && t < n && c < 2 * k);
+    }
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int e = threadIdx.x + q * kThreads;
+      if (e < kBK * YB) {
+        const int row = e / YB, c = e % YB;
+        const uint16_t hi = f32_to_bf16(v[q]);
+        sY[buf][row * LDY + c] = (c < k) ? hi : f32_to_bf16(v[q] - bf16_to_f32(hi));
       }
     }
   };
@@ -418,11 +445,11 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   const int T = (int)((a.d + BM - 1) / BM);
   dim3 grid((unsigned)(T * (T + 1) / 2), (unsigned)a.nb);
   if (big)
-    k_gram_bf16<256><<<grid, kThreads, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
-                                                      diag_part);
+    k_gram_bf16<256, 2, 4><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
+                                                       diag_part);
   else
-    k_gram_bf16<128><<<grid, kThreads, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
-                                                      diag_part);
+    k_gram_bf16<128, 2, 2><<<grid, 256, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
+                                                       diag_part);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gc((unsigned)((a.d + 255) / 256), (unsigned)a.nb);

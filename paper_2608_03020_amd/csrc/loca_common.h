@@ -34,6 +34,42 @@ template <typename T> LOCA_DEV float load_as_f32(const T* p);
 template <> LOCA_DEV float load_as_f32<float>(const float* p) { return *p; }
 template <> LOCA_DEV float load_as_f32<uint16_t>(const uint16_t* p) { return bf16_to_f32(*p); }
 
+// ------------------------------------------------------------------ branch-free guarded loads
+// The load always reads an in-bounds address (the base when `ok` is false) and the
+// value is selected afterwards, so loops of guarded loads issue back to back instead
+// of waiting on each other behind branches.
+template <typename T>
+LOCA_DEV T ld_or_zero(const T* base, int64_t idx, bool ok) {
+  const T v = base[ok ? idx : 0];
+  return ok ? v : (T)0;
+}
+
+// Copy a ROWS x COLS block (row stride ldg) from global memory into LDS (row stride
+// lds_ld) with NT threads, zero outside rows < rows_ok, cols < cols_ok.  Loads are
+// issued in batches of BATCH before any LDS store.  g must point at a valid element.
+template <typename T, int ROWS, int COLS, int NT, int BATCH = 16>
+LOCA_DEV void g2s_block(T* s, int lds_ld, const T* __restrict__ g, int64_t ldg, int64_t rows_ok, int64_t cols_ok) {
+  constexpr int PER = (ROWS * COLS) / NT;
+  static_assert((ROWS * COLS) % NT == 0, "block must split evenly over the threads");
+#pragma unroll
+  for (int q0 = 0; q0 < PER; q0 += BATCH) {
+    T v[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      const int e = threadIdx.x + (q0 + u) * NT;
+      const int r = e / COLS, c = e % COLS;
+      v[u] = (q0 + u < PER) ? ld_or_zero(g, (int64_t)r * ldg + c, r < rows_ok && c < cols_ok) : (T)0;
+    }
+#pragma unroll
+    for (int u = 0; u < BATCH; ++u) {
+      if (q0 + u < PER) {
+        const int e = threadIdx.x + (q0 + u) * NT;
+        s[(e / COLS) * lds_ld + (e % COLS)] = v[u];
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------------ reductions
 
 LOCA_DEV double wave_sum(double v) {
