@@ -23,7 +23,6 @@ namespace loca {
 namespace {
 
 constexpr int kT = 256;       // threads
-constexpr int kMC = 16;       // right-hand-side columns per back-substitution workgroup
 
 struct Lams {
   double v[8];
@@ -137,54 +136,133 @@ LOCA_DEV void tile_mma(const T* sP, const T* sQ, int ld, int K, int wi, int wj, 
 
 // ------------------------------------------------------------------ diagonal block: factor and invert
 
-// One workgroup per matrix: U11 = chol(A11) (upper) in LDS, then U11^{-1} by column-wise back
-// substitution.  The inverse replaces the diagonal block of F (its strict lower part is zeroed):
-// the row panel and the back substitution both apply U11^{-1} as a matrix product.
+// One workgroup per matrix factors the P x P diagonal block, A11 = U11^T U11, and
+// inverts U11.  The block lives in registers: thread (ty, tx) of a 16 x 16 grid owns
+// the entries (ty + 16 i, tx + 16 k).  Step j of the factorization needs only row j,
+// which its owners publish to a double-buffered LDS row, so each step costs one
+// barrier.  The inverse X = U11^{-1} is built bottom-up the same way (row i of X is
+// final once rows > i have been applied).  X replaces the diagonal block of F (strict
+// lower part zeroed): the row panel and the back substitution apply it as a product.
 template <typename T>
 __global__ __launch_bounds__(kT) void k_diag_block(int64_t d, int64_t p, T* __restrict__ Fall,
                                                    int32_t* __restrict__ dev_info) {
-  constexpr int P = Mf<T>::P;
+  constexpr int P = Mf<T>::P, NI = P / 16;
+  __shared__ T rowbuf[2][P];
   __shared__ T sU[P][P + 1];
-  __shared__ T sX[P][P + 1];
   const int64_t mi = blockIdx.x;
   T* F = Fall + mi * d * d;
+  const T* A0 = F + p * d + p;
   const int pw = (int)((d - p) < P ? (d - p) : P);
-  const int tid = threadIdx.x;
-  g2s_block<T, P, P, kT>(&sU[0][0], P + 1, F + p * d + p, d, pw, pw);
-  __syncthreads();
-  // 16 x 16 thread grid for the rank-1 updates (no runtime integer division)
-  const int ty = tid >> 4, tx = tid & 15;
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  T a[NI][NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int k = 0; k < NI; ++k) {
+      const int r = ty + 16 * i, c = tx + 16 * k;
+      a[i][k] = ld_or_zero(A0, (int64_t)r * d + c, r < pw && c < pw && c >= r);
+    }
+  if (ty == 0)
+#pragma unroll
+    for (int k = 0; k < NI; ++k) rowbuf[0][tx + 16 * k] = a[0][k];
   for (int j = 0; j < pw; ++j) {
-    const T piv = sU[j][j];
+    __syncthreads();
+    const T* rb = rowbuf[j & 1];
+    const T piv = rb[j];
     if (!(piv > (T)0) && tid == 0) atomicCAS(&dev_info[mi], 0, (int32_t)(p + j + 1));
     const T ujj = sqrt(piv);
-    __syncthreads();
-    for (int c = j + tid; c < pw; c += kT) sU[j][c] = (c == j) ? ujj : sU[j][c] / ujj;
-    __syncthreads();
-    for (int r = j + 1 + ty; r < pw; r += 16) {
-      const T ujr = sU[j][r];
-      for (int c = j + 1 + tx; c < pw; c += 16)
-        if (c >= r) sU[r][c] -= ujr * sU[j][c];
+    const T inv = (T)1 / ujj;
+    T ur[NI], uc[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) ur[i] = rb[ty + 16 * i] * inv;
+#pragma unroll
+    for (int k = 0; k < NI; ++k) uc[k] = rb[tx + 16 * k] * inv;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = ty + 16 * i;
+      if (r == j) {  // owners of row j: final row of U
+#pragma unroll
+        for (int k = 0; k < NI; ++k) {
+          const int c = tx + 16 * k;
+          if (c >= j && c < pw) a[i][k] = (c == j) ? ujj : uc[k];
+        }
+      } else if (r > j && r < pw) {
+#pragma unroll
+        for (int k = 0; k < NI; ++k) {
+          const int c = tx + 16 * k;
+          if (c >= r && c < pw) a[i][k] -= ur[i] * uc[k];
+        }
+      }
     }
-    __syncthreads();
+    if (j + 1 < pw) {
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        if (ty + 16 * i == j + 1)
+#pragma unroll
+          for (int k = 0; k < NI; ++k) rowbuf[(j + 1) & 1][tx + 16 * k] = a[i][k];
+    }
   }
-  // X = U^{-1} (upper), rows from the bottom up: once row i of X is final, its
-  // contribution U[r][i] X[i][j] is added to the partial sums of every row r < i.
-  for (int r = ty; r < P; r += 16)
-    for (int c = tx; c < P; c += 16) sX[r][c] = (T)0;  // partial sums
+  // U to LDS (column reads below), then X = U^{-1} bottom-up in registers (t = partial sums, then X)
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int k = 0; k < NI; ++k) sU[ty + 16 * i][tx + 16 * k] = a[i][k];
   __syncthreads();
-  for (int i = pw - 1; i >= 0; --i) {
-    const T inv = (T)1 / sU[i][i];
-    for (int j = i + tid; j < pw; j += kT) sX[i][j] = ((j == i ? (T)1 : (T)0) - sX[i][j]) * inv;
-    __syncthreads();
-    for (int r = ty; r < i; r += 16) {
-      const T uri = sU[r][i];
-      for (int j = i + tx; j < pw; j += 16) sX[r][j] += uri * sX[i][j];
-    }
-    __syncthreads();
+  T t[NI][NI];
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int k = 0; k < NI; ++k) t[i][k] = (T)0;
+  {
+    const int last = pw - 1;
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      if (ty + 16 * i == last)
+#pragma unroll
+        for (int k = 0; k < NI; ++k) {
+          const int c = tx + 16 * k;
+          const T x = (c == last) ? (T)1 / sU[last][last] : (T)0;
+          t[i][k] = x;
+          rowbuf[last & 1][c] = x;
+        }
   }
-  for (int r = ty; r < pw; r += 16)
-    for (int c = tx; c < pw; c += 16) F[(p + r) * d + p + c] = (c >= r) ? sX[r][c] : (T)0;
+  for (int i0 = pw - 1; i0 >= 0; --i0) {
+    __syncthreads();
+    const T* xb = rowbuf[i0 & 1];
+    T xc[NI];
+#pragma unroll
+    for (int k = 0; k < NI; ++k) xc[k] = xb[tx + 16 * k];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = ty + 16 * i;
+      if (r < i0) {
+        const T uri = sU[r][i0];
+#pragma unroll
+        for (int k = 0; k < NI; ++k) t[i][k] += uri * xc[k];
+      }
+    }
+    const int nr = i0 - 1;  // row finalized in this step
+    if (nr >= 0) {
+      const T inv = (T)1 / sU[nr][nr];
+#pragma unroll
+      for (int i = 0; i < NI; ++i)
+        if (ty + 16 * i == nr)
+#pragma unroll
+          for (int k = 0; k < NI; ++k) {
+            const int c = tx + 16 * k;
+            const T x = (c >= nr && c < pw) ? ((c == nr ? (T)1 : (T)0) - t[i][k]) * inv : (T)0;
+            t[i][k] = x;
+            rowbuf[nr & 1][c] = x;
+          }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+#pragma unroll
+    for (int k = 0; k < NI; ++k) {
+      const int r = ty + 16 * i, c = tx + 16 * k;
+      if (r < pw && c < pw) F[(p + r) * d + p + c] = (c >= r) ? t[i][k] : (T)0;
+    }
 }
 
 // ------------------------------------------------------------------ panel products (row panel, trailing update)
@@ -318,59 +396,104 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 
 // ------------------------------------------------------------------ back substitution, one row block
 
-// Rows [p, p+pw) of U M' = Y:  M'_p = U11^{-1} (Y_p - U_{p, >=p+pw} M'_{>=p+pw}); the solved
-// rows below p already hold M' in R.  One workgroup per (matrix, kMC right-hand sides).
+// acc[m][q] += sum_kk sA[i][kk] sB[kk][j]: like tile_mma, with the first operand stored
+// with K along its rows (row stride lda, odd so that column reads are conflict-free).
 template <typename T>
-__global__ __launch_bounds__(kT) void k_back_block(int64_t d, int64_t m, int64_t p, const T* __restrict__ Fall,
-                                                   T* __restrict__ Rall) {
-  constexpr int P = Mf<T>::P, JC = 64, PER = (P * kMC) / kT;
-  __shared__ T sU[P][JC + 1];
-  __shared__ T sX[JC][kMC + 1];
-  __shared__ T sI[P][P + 1];
-  __shared__ T sAcc[P][kMC + 1];
+LOCA_DEV void tile_mma_kt(const T* sA, int lda, const T* sB, int ldb, int K, int wi, int wj, int lane,
+                          typename Mf<T>::acc_t (&acc)[2][2]) {
+  constexpr int BLK = Mf<T>::BLK, KS = Mf<T>::KS, WT = Mf<T>::P / 2;
+  const int kr = lane / BLK, cr = lane % BLK;
+  for (int kk = 0; kk < K; kk += KS) {
+    T a[2], b[2];
+#pragma unroll
+    for (int m = 0; m < 2; ++m) a[m] = sA[(wi * WT + m * BLK + cr) * lda + kk + kr];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) b[q] = sB[(kk + kr) * ldb + wj * WT + q * BLK + cr];
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int q = 0; q < 2; ++q) acc[m][q] = Mf<T>::mma(a[m], b[q], acc[m][q]);
+  }
+}
+
+// Right-looking back substitution for row block [p, p + pw) of U M' = Y, where the rows
+// of R (= Y) have already received the contributions of every block below:
+//   M'_p = U11^{-1} R_p                (computed by every workgroup, stored by x == 0)
+//   R_r -= U_{r, p:p+pw} M'_p          for the rows r < p of this workgroup's chunk.
+// Grid: x = P-row chunks above p (at least one), y = matrix.  The four waves split the
+// P rows; each covers NQ MFMA blocks of the m right-hand-side columns (m <= NQ * BLK).
+template <typename T, int NQ>
+__global__ __launch_bounds__(kT) void k_back_step(int64_t d, int64_t m, int64_t p, const T* __restrict__ Fall,
+                                                  T* __restrict__ Rall, T* __restrict__ Mpall) {
+  constexpr int P = Mf<T>::P, BLK = Mf<T>::BLK, KS = Mf<T>::KS, NMB = P / 4 / BLK;
+  constexpr int NC = NQ * BLK, LDK = P + 1, LDN = NC + 4;
+  __shared__ T sA[P * LDK];  // U11^{-1}, then the rows above
+  __shared__ T sB[P * LDN];  // R_p, then M'_p
   const int64_t mi = blockIdx.y;
   const T* F = Fall + mi * d * d;
   T* R = Rall + mi * d * m;
-  const int64_t c0 = (int64_t)blockIdx.x * kMC;
-  const int mc = (int)((m - c0) < kMC ? (m - c0) : kMC);
+  T* Mp = Mpall + mi * d * m;
   const int pw = (int)((d - p) < P ? (d - p) : P);
-  const int64_t p1 = p + pw;
-  const int tid = threadIdx.x;
-  T acc[PER];
+  const int64_t r0 = (int64_t)blockIdx.x * P;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int kr = lane / BLK, cr = lane % BLK;
+  g2s_block<T, P, P, kT>(sA, LDK, F + p * d + p, d, pw, pw);
+  g2s_block<T, P, NC, kT>(sB, LDN, R + p * m, m, pw, m);
+  __syncthreads();
+  typename Mf<T>::acc_t acc[NMB][NQ];
+  auto product = [&]() {
 #pragma unroll
-  for (int q = 0; q < PER; ++q) acc[q] = (T)0;
-  for (int64_t j0 = p1; j0 < d; j0 += JC) {
-    const int jw = (int)((d - j0) < JC ? (d - j0) : JC);
-    __syncthreads();
-    g2s_block<T, P, JC, kT>(&sU[0][0], JC + 1, F + p * d + j0, d, pw, jw);
-    g2s_block<T, JC, kMC, kT>(&sX[0][0], kMC + 1, R + j0 * m + c0, m, jw, mc);
-    __syncthreads();
+    for (int x = 0; x < NMB; ++x)
 #pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const int e = tid + kT * q;
-      const int r = e / kMC, c = e % kMC;
-      T s = acc[q];
-      for (int jj = 0; jj < JC; ++jj) s += sU[r][jj] * sX[jj][c];
-      acc[q] = s;
+      for (int y = 0; y < NQ; ++y) acc[x][y] = Mf<T>::zero();
+    for (int kk = 0; kk < pw; kk += KS) {
+      T a[NMB], b[NQ];
+#pragma unroll
+      for (int x = 0; x < NMB; ++x) a[x] = sA[(wid * (P / 4) + x * BLK + cr) * LDK + kk + kr];
+#pragma unroll
+      for (int y = 0; y < NQ; ++y) b[y] = sB[(kk + kr) * LDN + y * BLK + cr];
+#pragma unroll
+      for (int x = 0; x < NMB; ++x)
+#pragma unroll
+        for (int y = 0; y < NQ; ++y) acc[x][y] = Mf<T>::mma(a[x], b[y], acc[x][y]);
     }
-  }
-  __syncthreads();
-  g2s_block<T, P, P, kT>(&sI[0][0], P + 1, F + p * d + p, d, pw, pw);  // U11^{-1}
+  };
+  product();
+  __syncthreads();  // everyone is done reading sA / sB
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    const int e = tid + kT * q;
-    const int r = e / kMC, c = e % kMC;
-    sAcc[r][c] = ld_or_zero(R, (p + r) * m + c0 + c, r < pw && c < mc) - acc[q];
-  }
-  __syncthreads();
+  for (int x = 0; x < NMB; ++x)
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    const int e = tid + kT * q;
-    const int r = e / kMC, c = e % kMC;
-    T s = (T)0;
-    for (int jj = r; jj < pw; ++jj) s += sI[r][jj] * sAcc[jj][c];
-    if (r < pw && c < mc) R[(p + r) * m + c0 + c] = s;
-  }
+    for (int y = 0; y < NQ; ++y)
+#pragma unroll
+      for (int r = 0; r < Mf<T>::NR; ++r) {
+        const int row = wid * (P / 4) + x * BLK + Mf<T>::row(lane, r);
+        const int col = y * BLK + Mf<T>::col(lane);
+        const T v = (row < pw && col < m) ? acc[x][y][r] : (T)0;
+        sB[row * LDN + col] = v;
+        if (blockIdx.x == 0 && row < pw && col < m) Mp[(p + row) * m + col] = v;
+      }
+  if (r0 >= p) return;  // no rows above in this chunk (only chunk 0 exists when p == 0)
+  const int64_t rows = (p - r0) < P ? (p - r0) : P;
+  g2s_block<T, P, P, kT>(sA, LDK, F + r0 * d + p, d, rows, pw);
+  __syncthreads();
+  product();
+#pragma unroll
+  for (int x = 0; x < NMB; ++x)
+#pragma unroll
+    for (int y = 0; y < NQ; ++y) {
+      T old[Mf<T>::NR];
+      const int col = y * BLK + Mf<T>::col(lane);
+#pragma unroll
+      for (int r = 0; r < Mf<T>::NR; ++r) {
+        const int row = wid * (P / 4) + x * BLK + Mf<T>::row(lane, r);
+        old[r] = ld_or_zero(R, (r0 + row) * m + col, row < rows && col < m);
+      }
+#pragma unroll
+      for (int r = 0; r < Mf<T>::NR; ++r) {
+        const int row = wid * (P / 4) + x * BLK + Mf<T>::row(lane, r);
+        if (row < rows && col < m) R[(r0 + row) * m + col] = old[r] - acc[x][y][r];
+      }
+    }
 }
 
 // M = D M' (undo the equilibration), float output.
@@ -390,6 +513,7 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
   size_t s = align256(sizeof(T) * nm * d * d);  // F
   s += align256(sizeof(T) * nm * d * m);         // R
   s += align256(sizeof(T) * nm * d);             // D
+  s += align256(sizeof(T) * nm * d * m);         // M' (back substitution output)
   s += align256(sizeof(double) * nb * d * (r_prev > 0 ? r_prev : 1));  // S Lp
   s += 256;                                                            // lambdas
   return s;
@@ -402,6 +526,7 @@ hipError_t run_solve(const SolveArgs& a) {
   T* F = (T*)p; p += align256(sizeof(T) * nm * d * d);
   T* R = (T*)p; p += align256(sizeof(T) * nm * d * m);
   T* D = (T*)p; p += align256(sizeof(T) * nm * d);
+  T* Mp = (T*)p; p += align256(sizeof(T) * nm * d * m);
   double* SLp = (double*)p;
   Lams lams;
   for (int i = 0; i < 8; ++i) lams.v[i] = (i < nl) ? a.lambdas[i] : 0.0;
@@ -439,9 +564,15 @@ hipError_t run_solve(const SolveArgs& a) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P)
-    k_back_block<T><<<dim3((unsigned)((m + kMC - 1) / kMC), (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R);
-  k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, a.stream>>>(d, m, R, D, a.m_out,
+  for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P) {
+    const dim3 grid((unsigned)(pp > 0 ? (pp + P - 1) / P : 1), (unsigned)nm);
+    const int nq = (int)((m + Mf<T>::BLK - 1) / Mf<T>::BLK);  // m <= 128 (checked by the API)
+    if (nq <= 1) k_back_step<T, 1><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
+    else if (nq <= 2) k_back_step<T, 2><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
+    else if (nq <= 4 || sizeof(T) == 4) k_back_step<T, 4><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
+    else if constexpr (sizeof(T) == 8) k_back_step<T, 8><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
+  }
+  k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, a.stream>>>(d, m, Mp, D, a.m_out,
                                                                                           a.m_bstride);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
