@@ -193,6 +193,186 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16(int64_t n, int64_t
   }
 }
 
+// ------------------------------------------------------------------ S += X^T X, direct-to-LDS pipeline
+
+// Same tiles and waves as k_gram_bf16, fed by global_load_lds_dwordx4: each lane's
+// 16-byte chunk goes straight from HBM/L2 into LDS, so a 4-stage ring can run three
+// stages ahead without holding anything in registers.  A stage is 32 tokens x 256
+// columns of a panel (16 KB, rows of 512 B).  A wave's load instruction fills 1 KB of
+// consecutive LDS, so the conflict-free layout for the transpose reads comes from an
+// XOR swizzle of the 16-byte chunks instead of padding: chunk c of row r sits at
+// c ^ 4(r & 3), so the four rows x four chunks that half a wave reads in one LDS
+// cycle land on 16 distinct chunk positions (all 64 banks).  Rows past n and columns past d are read from a zeroed 16-byte area of the
+// workspace.  Requires d % 8 == 0.
+constexpr int kDLStages = 4;
+constexpr int kDLRowBytes = 512;
+
+LOCA_DEV int dl_swz(int row) { return 4 * (row & 3); }
+
+// operand of v_mfma_f32_32x32x16_bf16 from a swizzled 32 x 256 stage (see frag32_tr)
+LOCA_DEV bf16x8_t frag32_tr_swz(const uint16_t* tile, int c0, int ks, int lane) {
+  const int g = lane >> 4, w = lane & 15;
+  const int col = c0 + 16 * (g & 1) + 4 * (w & 3);
+  const int row = ks + 8 * (g >> 1) + (w >> 2);
+  const int lc = col >> 3, within = col & 7;
+  const uint16_t* p0 = tile + row * 256 + 8 * (lc ^ dl_swz(row)) + within;
+  const uint16_t* p1 = tile + (row + 4) * 256 + 8 * (lc ^ dl_swz(row + 4)) + within;
+  s16x4_t lo = lds_read_tr16(p0);
+  s16x4_t hi = lds_read_tr16(p1);
+  typedef short s16x8_t __attribute__((ext_vector_type(8)));
+  s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory operations are outstanding
+constexpr int vmcnt_imm(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
+
+// 16-byte global -> LDS copy for every lane: lane l's chunk lands at lds_base + 16 l.
+// Issued as inline assembly so that the compiler does not treat it as a store to the
+// ring slot being read and drain it before every LDS read; completion is tracked by
+// the explicit vmcnt waits of the pipeline.
+LOCA_DEV void lds_dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base) : "m0", "memory");
+}
+// Workgroup barrier without a memory fence (the pipeline waits for its own loads explicitly).
+LOCA_DEV void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
+
+__global__ __launch_bounds__(512) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
+                                                      int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
+                                                      int64_t s_bstride, double* __restrict__ diag_part,
+                                                      const uint16_t* __restrict__ zero16) {
+  constexpr int BM = 256, WGM = 2, WGN = 4, NT = 512;
+  constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
+  constexpr int TILE_ELEMS = kBK * BM;  // one panel stage (bf16 elements)
+  // one LDS object per ring slot: the loop below touches each through a static name,
+  // so the in-flight loads into one slot are not mistaken for writes to the slot read
+  __shared__ __attribute__((aligned(1024))) uint16_t sb0[2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb1[2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb2[2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb3[2 * TILE_ELEMS];
+  __shared__ double sred[NT / 64];
+  static_assert(kDLStages == 4, "the ring below is written out for four slots");
+
+  const int T = (int)((d + BM - 1) / BM);
+  int I, J;
+  upper_tile(blockIdx.x, T, I, J);
+  const bool diag = (I == J);
+  const int64_t b = blockIdx.y;
+  const uint16_t* X = Xall + b * x_bstride;
+  float* S = Sall + b * s_bstride;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wi = wid / WGN, wj = wid % WGN;
+  const bool active = !(diag && (wj + 1) * WN <= wi * WM);
+  const int64_t cI = (int64_t)I * BM, cJ = (int64_t)J * BM;
+  const int nk = (int)((n + kBK - 1) / kBK);
+
+  // per-thread source chunks: instruction q of wave w fills LDS slots (2w + q) * 64 + lane
+  int lrow[2], lcol[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int slot = (2 * wid + q) * 64 + lane;
+    lrow[q] = slot >> 5;
+    lcol[q] = 8 * ((slot & 31) ^ dl_swz(slot >> 5));
+  }
+  auto issue = [&](uint16_t* buf, int kt) {
+    const int64_t t0 = (int64_t)kt * kBK;
+#pragma unroll
+    for (int pnl = 0; pnl < 2; ++pnl) {
+      const int64_t c0 = pnl == 0 ? cI : cJ;  // a diagonal tile loads its panel twice
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int64_t t = t0 + lrow[q], col = c0 + lcol[q];
+        const uint16_t* src = (t < n && col < d) ? X + t * ldx + col : zero16;
+        const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (2 * wid + q) * 1024;
+        lds_dma16(src, __builtin_amdgcn_readfirstlane(dst));
+      }
+    }
+  };
+
+  f32x16_t acc[NBM][NBN];
+#pragma unroll
+  for (int m = 0; m < NBM; ++m)
+#pragma unroll
+    for (int q = 0; q < NBN; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][q][r] = 0.f;
+
+  // Fragments are double-buffered in registers across the two 16-token halves of a
+  // stage and across stages: the operands of the next half (or of the next stage's
+  // first half) are read from LDS while the MFMAs of the current half run.  Reading
+  // stage kt + 1 during stage kt needs it landed too, so each step waits until at most
+  // one stage of loads (four per thread) is in flight and refills the slot of kt + 3.
+  bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN];
+  auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
+#pragma unroll
+    for (int q = 0; q < NBN; ++q) fb[q] = frag32_tr_swz(buf + TILE_ELEMS, wj * WN + 32 * q, ks, lane);
+#pragma unroll
+    for (int m = 0; m < NBM; ++m) fa[m] = frag32_tr_swz(buf, wi * WM + 32 * m, ks, lane);
+  };
+  auto mma_block = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN]) {
+#pragma unroll
+    for (int m = 0; m < NBM; ++m)
+#pragma unroll
+      for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
+  };
+#define LOCA_DL_STEP(cur, nxt, fill, kt)                           \
+  {                                                                \
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(4));                      \
+    barrier_nofence();                                             \
+    issue(fill, (kt) + kDLStages - 1);                             \
+    if (active) {                                                  \
+      load_frags(cur, 16, fa1, fb1);                               \
+      mma_block(fa0, fb0);                                         \
+      if ((kt) + 1 < nk) load_frags(nxt, 0, fa0, fb0);             \
+      mma_block(fa1, fb1);                                         \
+    }                                                              \
+  }
+  issue(sb0, 0);  // stages past nk read zeros: harmless
+  issue(sb1, 1);
+  issue(sb2, 2);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));  // stage 0 landed
+  barrier_nofence();
+  if (active) load_frags(sb0, 0, fa0, fb0);
+  for (int kt = 0; kt < nk; kt += 4) {
+    LOCA_DL_STEP(sb0, sb1, sb3, kt);
+    if (kt + 1 < nk) LOCA_DL_STEP(sb1, sb2, sb0, kt + 1);
+    if (kt + 2 < nk) LOCA_DL_STEP(sb2, sb3, sb1, kt + 2);
+    if (kt + 3 < nk) LOCA_DL_STEP(sb3, sb0, sb2, kt + 3);
+  }
+#undef LOCA_DL_STEP
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // drain the look-ahead loads before the workgroup ends
+
+  double dsum = 0.0;
+  if (active) {
+#pragma unroll
+    for (int m = 0; m < NBM; ++m)
+#pragma unroll
+      for (int q = 0; q < NBN; ++q) {
+        // the 16 old values of this MFMA block are read together, then added and stored
+        const int64_t col = cJ + wj * WN + 32 * q + mfma32_col(lane);
+        const int64_t rb = cI + wi * WM + 32 * m;
+        float old[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = rb + mfma32_row(lane, r);
+          old[r] = ld_or_zero(S, row * d + col, row < d && col < d);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = rb + mfma32_row(lane, r);
+          if (row < d && col < d) {
+            S[row * d + col] = old[r] + acc[m][q][r];
+            if (diag && row == col) dsum += (double)acc[m][q][r];
+          }
+        }
+      }
+  }
+  if (diag) {
+    const double tot = block_sum(dsum, sred);
+    if (threadIdx.x == 0) diag_part[b * T + I] = tot;
+  }
+}
+
 // ------------------------------------------------------------------ Kraw = X^T [Y_hi | Y_lo] (bf16)
 
 // Rows: a 256-column panel of X; columns: the 2k split columns of Y padded to YB.
@@ -408,11 +588,15 @@ __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, con
 
 }  // namespace
 
+__global__ void k_zero_bytes(uint32_t* p, int cnt) {
+  if ((int)threadIdx.x < cnt) p[threadIdx.x] = 0u;
+}
+
 size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc) {
   (void)n;
   const int64_t T = acc == LOCA_F64 ? (d + kBM64 - 1) / kBM64 : (d + 127) / 128;
   const int64_t Tmax = (d + kBM64 - 1) / kBM64;  // generous: covers every tile size used
-  size_t s = align256(sizeof(double) * nb * (T > Tmax ? T : Tmax));
+  size_t s = 256 + align256(sizeof(double) * nb * (T > Tmax ? T : Tmax));  // zeros + tile partials
   if (acc == LOCA_F64) s += align256(sizeof(double) * nb * d * k);
   else s += align256(sizeof(float) * nb * d * 2 * k);
   return s;
@@ -420,8 +604,9 @@ size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dty
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {
   const int64_t Tmax = (a.d + kBM64 - 1) / kBM64;
-  double* diag_part = (double*)a.ws;
-  char* p = a.ws + align256(sizeof(double) * a.nb * Tmax);
+  const uint16_t* zero16 = (const uint16_t*)a.ws;  // 256 zeroed bytes
+  double* diag_part = (double*)(a.ws + 256);
+  char* p = a.ws + 256 + align256(sizeof(double) * a.nb * Tmax);
   if (a.acc == LOCA_F64) {
     double* Kraw = (double*)p;
     const int T = (int)((a.d + kBM64 - 1) / kBM64);
@@ -444,7 +629,11 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   const int BM = big ? 256 : 128;
   const int T = (int)((a.d + BM - 1) / BM);
   dim3 grid((unsigned)(T * (T + 1) / 2), (unsigned)a.nb);
-  if (big)
+  if (big && (a.d % 8) == 0) {
+    k_zero_bytes<<<1, 64, 0, a.stream>>>((uint32_t*)a.ws, 64);
+    k_gram_bf16_dl<<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part,
+                                               zero16);
+  } else if (big)
     k_gram_bf16<256, 2, 4><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
                                                        diag_part);
   else

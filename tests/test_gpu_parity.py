@@ -63,6 +63,9 @@ CASES = {
     # statistics, which needs N > d: with N < d rounding in S leaks into the null space of X and is
     # amplified by 1/lambda (fp32 mode, with fp64 statistics, covers N < d).
     "bf16_d1100": gen.custom_config("t2", blocks=1, d=1100, n=2300, micro=1000, C=3, k=32, r_a=8),
+    # d % 8 == 0 and d >= 1024: the direct-to-LDS Gram kernel; ragged against 256-wide tiles and
+    # against the 32-token stages (1400 = 43 x 32 + 24), two blocks
+    "bf16_d1040_direct": gen.custom_config("t10", blocks=2, d=1040, n=2400, micro=1400, C=4, k=16, r_a=4),
     # fp32 mode with fewer tokens than features (null space amplified by 1/lambda)
     "fp32_n150_d200": gen.custom_config("t3", blocks=2, d=200, n=150, C=2, k=8, r_a=8, mode="fp32",
                                         x_dist="gauss_outlier", n_outlier=3, outlier_scale=20.0, logit_std=2.0),
