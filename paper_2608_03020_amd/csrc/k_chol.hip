@@ -283,17 +283,23 @@ LOCA_DEV void upper_tile_c(int u, int T, int& I, int& J) {
 constexpr int kKC = 32;
 enum PanelJob { kRowPanel = 0, kTrailing = 1 };
 
+// kTrailing takes its K rows from [k0, k0 + kw) of F and R and updates the region of
+// rows and columns >= off: every upper tile plus the RHS rows (strip = 0), or only the
+// first row of tiles, rows [off, off + P) (strip = 1).  Job = blockIdx.x + job0, the
+// upper tiles first, then the RHS tiles.
 template <typename T, int JOB>
-__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_panel_product(int64_t d, int64_t m, int64_t p, T* __restrict__ Fall,
-                                                      T* __restrict__ Rall) {
+__global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_panel_product(
+    int64_t d, int64_t m, int64_t p, int64_t k0, int64_t kw, int64_t off, int strip, int job0, T* __restrict__ Fall,
+    T* __restrict__ Rall) {
   constexpr int P = Mf<T>::P, LD = P + 4, PER = (kKC * P) / kT;
   __shared__ T sP[2][kKC * LD];
   __shared__ T sQ[2][kKC * LD];
   const int64_t mi = blockIdx.y;
   T* F = Fall + mi * d * d;
   T* R = Rall + mi * d * m;
-  const int pw = (int)((d - p) < P ? (d - p) : P);
-  const int64_t off = p + pw, nrem = d - off;
+  const int pw = JOB == kRowPanel ? (int)((d - p) < P ? (d - p) : P) : (int)kw;  // K rows
+  if (JOB == kRowPanel) off = p + pw;
+  const int64_t nrem = d - off;
   const int64_t nchF = (nrem + P - 1) / P;
   bool rhs, diag = false;
   int64_t orow, ocol, ocend;  // output tile origin (row in F/R, column) and column end
@@ -311,19 +317,22 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
     ldq = rhs ? m : d;
   } else {
     const int T2 = (int)((nrem + P - 1) / P);
-    const int nU = T2 * (T2 + 1) / 2;
+    const int nU = strip ? T2 : T2 * (T2 + 1) / 2;
     const int TM = (int)((m + P - 1) / P);
+    const int job = (int)blockIdx.x + job0;
     int I, J;
-    rhs = (int)blockIdx.x >= nU;
-    if (!rhs) upper_tile_c(blockIdx.x, T2, I, J);
-    else { const int u = blockIdx.x - nU; I = u / TM; J = u % TM; }
+    rhs = job >= nU;
+    if (!rhs) {
+      if (strip) { I = 0; J = job; }
+      else upper_tile_c(job, T2, I, J);
+    } else { const int u = job - nU; I = u / TM; J = u % TM; }
     diag = !rhs && I == J;
     orow = off + (int64_t)I * P;
     ocol = rhs ? (int64_t)J * P : off + (int64_t)J * P;
     ocend = rhs ? m : d;
-    gP = F + p * d + orow;
+    gP = F + k0 * d + orow;
     prows_ok = d - orow;  // columns of Pn that exist
-    gQ = rhs ? R + p * m + ocol : F + p * d + ocol;
+    gQ = rhs ? R + k0 * m + ocol : F + k0 * d + ocol;
     ldq = rhs ? m : d;
   }
   const int64_t pcols_ok = (JOB == kRowPanel) ? pw : prows_ok;
@@ -333,14 +342,14 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const bool active = !(diag && wi > wj);  // strictly lower quarter of a diagonal tile
 
   T rp[PER], rq[PER];
-  auto load_chunk = [&](int k0) {
+  auto load_chunk = [&](int kc0) {
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int e = tid + q * kT;
       const int kk = e / P, c = e % P;
-      const bool okk = k0 + kk < pw;
-      rp[q] = ld_or_zero(gP, (int64_t)(k0 + kk) * d + c, okk && c < pcols_ok);
-      rq[q] = ld_or_zero(gQ, (int64_t)(k0 + kk) * ldq + c, okk && c < qcols_ok);
+      const bool okk = kc0 + kk < pw;
+      rp[q] = ld_or_zero(gP, (int64_t)(kc0 + kk) * d + c, okk && c < pcols_ok);
+      rq[q] = ld_or_zero(gQ, (int64_t)(kc0 + kk) * ldq + c, okk && c < qcols_ok);
     }
   };
   auto store_chunk = [&](int buf) {
@@ -390,6 +399,138 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
         const int64_t row = rbase + Mf<T>::row(lane, r);
         const bool ok = row < rend && col < ocend && (JOB == kRowPanel || rhs || col >= row);
         if (ok) Out[row * ldo + col] = (JOB == kTrailing) ? old[r] - acc[a][b][r] : acc[a][b][r];
+      }
+    }
+}
+
+// ------------------------------------------------------------------ trailing update on bf16 matrix cores
+
+// A float a is carried as three bfloat16 parts, h = bf16(a), m = bf16(a - h),
+// l = bf16(a - h - m) (each difference is exact in float), which hold a to about 2^-27
+// relative.  The product of two split values keeps the six terms of order 2^-16 and
+// larger (h*h, h*m, m*h, h*l, l*h, m*m) and drops m*l, l*m, l*l (order 2^-24 and
+// below), so the update has float-class error while running on bf16 MFMA, which
+// retires sixteen times the flops of the fp32 MFMA per cycle.
+LOCA_DEV void split3(float a, uint16_t& h, uint16_t& m, uint16_t& l) {
+  h = f32_to_bf16(a);
+  const float r1 = a - bf16_to_f32(h);
+  m = f32_to_bf16(r1);
+  l = f32_to_bf16(r1 - bf16_to_f32(m));
+}
+
+// F[i][j] -= sum_{kk in [k0, k0 + kw)} F[kk][i] F[kk][j] on the upper 256 x 256 tiles of
+// the trailing region [off, d) (grid: x = tile, y = matrix).  A stage is 16 rows of K:
+// each operand (32 KB of float) is loaded into registers one stage ahead, split, and
+// written to LDS as three bf16 planes [16][LD]; eight waves of 128 x 64 read their
+// MFMA operands with transpose reads (LD = 288: the four rows a half-wave reads start
+// 64 bytes apart modulo 256, so the reads are conflict-free).  Requires d % 4 == 0.
+constexpr int kX6BK = 16, kX6LD = 288;
+
+LOCA_DEV float4 ld4_or_zero(const float* base, int64_t idx, bool ok) {
+  const float4 v = *(const float4*)(base + (ok ? idx : 0));
+  return ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+__global__ __launch_bounds__(512) void k_trail_x6(int64_t d, int64_t k0, int64_t kw, int64_t off,
+                                                  float* __restrict__ Fall) {
+  constexpr int BM = 256, WGN = 4, WM = 128, WN = 64, NBM = WM / 32, NBN = WN / 32;
+  constexpr int LD = kX6LD, PLANE = kX6BK * LD;
+  __shared__ __attribute__((aligned(16))) uint16_t sm[2][6 * PLANE];  // [buffer][operand * 3 + part]
+  const int64_t mi = blockIdx.y;
+  float* F = Fall + mi * d * d;
+  const int T2 = (int)((d - off + BM - 1) / BM);
+  int I, J;
+  upper_tile_c((int)blockIdx.x, T2, I, J);
+  const bool diag = I == J;
+  const int64_t orow = off + (int64_t)I * BM, ocol = off + (int64_t)J * BM;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, wi = wid / WGN, wj = wid % WGN;
+  const bool active = !(diag && (wj + 1) * WN <= wi * WM);
+  const float* gP = F + k0 * d + orow;
+  const float* gQ = F + k0 * d + ocol;
+
+  // staging: float4 chunk c = tid + 512 q of the 16 x 64 chunks of an operand stage
+  float4 rp[2], rq[2];
+  auto load = [&](int kc0) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = tid + 512 * q, kk = c >> 6, c4 = 4 * (c & 63);
+      const bool okk = kc0 + kk < kw;
+      rp[q] = ld4_or_zero(gP, (int64_t)(kc0 + kk) * d + c4, okk && orow + c4 < d);
+      rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * d + c4, okk && ocol + c4 < d);
+    }
+  };
+  auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
+    uint16_t h[4], m[4], l[4];
+    split3(v.x, h[0], m[0], l[0]);
+    split3(v.y, h[1], m[1], l[1]);
+    split3(v.z, h[2], m[2], l[2]);
+    split3(v.w, h[3], m[3], l[3]);
+    const int o = kk * LD + c4;
+    *(uint2*)(base + o) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+    *(uint2*)(base + PLANE + o) = make_uint2(m[0] | ((uint32_t)m[1] << 16), m[2] | ((uint32_t)m[3] << 16));
+    *(uint2*)(base + 2 * PLANE + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+  };
+  auto store = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int c = tid + 512 * q, kk = c >> 6, c4 = 4 * (c & 63);
+      put(&sm[buf][0], kk, c4, rp[q]);
+      put(&sm[buf][3 * PLANE], kk, c4, rq[q]);
+    }
+  };
+
+  f32x16_t acc[NBM][NBN];
+#pragma unroll
+  for (int a = 0; a < NBM; ++a)
+#pragma unroll
+    for (int b = 0; b < NBN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  const int nk = (int)((kw + kX6BK - 1) / kX6BK);
+  load(0);
+  store(0);
+  __syncthreads();
+  for (int kc = 0; kc < nk; ++kc) {
+    const int cur = kc & 1;
+    if (kc + 1 < nk) load((kc + 1) * kX6BK);
+    bf16x8_t fa[3][NBM], fb[3][NBN];
+#pragma unroll
+    for (int t = 0; t < 3; ++t) {
+#pragma unroll
+      for (int a = 0; a < NBM; ++a) fa[t][a] = frag32_tr(&sm[cur][t * PLANE], LD, wi * WM + 32 * a, 0, lane);
+#pragma unroll
+      for (int b = 0; b < NBN; ++b) fb[t][b] = frag32_tr(&sm[cur][(3 + t) * PLANE], LD, wj * WN + 32 * b, 0, lane);
+    }
+    // the six kept terms, smallest first; each term runs over all blocks, so the MFMAs
+    // into one accumulator are eight instructions apart
+    constexpr int TA[6] = {2, 0, 1, 1, 0, 0}, TB[6] = {0, 2, 1, 0, 1, 0};
+#pragma unroll
+    for (int t = 0; t < 6; ++t)
+#pragma unroll
+      for (int a = 0; a < NBM; ++a)
+#pragma unroll
+        for (int b = 0; b < NBN; ++b) acc[a][b] = mfma32(fa[TA[t]][a], fb[TB[t]][b], acc[a][b]);
+    if (kc + 1 < nk) store(cur ^ 1);
+    __syncthreads();
+  }
+  if (!active) return;
+#pragma unroll
+  for (int a = 0; a < NBM; ++a)
+#pragma unroll
+    for (int b = 0; b < NBN; ++b) {
+      const int64_t col = ocol + wj * WN + 32 * b + mfma32_col(lane);
+      const int64_t rb = orow + wi * WM + 32 * a;
+      float old[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = rb + mfma32_row(lane, r);
+        old[r] = ld_or_zero(F, row * d + col, row < d && col < d && col >= row);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = rb + mfma32_row(lane, r);
+        if (row < d && col < d && col >= row) F[row * d + col] = old[r] - acc[a][b][r];
       }
     }
 }
@@ -549,17 +690,41 @@ hipError_t run_solve(const SolveArgs& a) {
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  constexpr int P = Mf<T>::P;
-  for (int64_t pp = 0; pp < d; pp += P) {
-    const int64_t pw = (d - pp) < P ? (d - pp) : P;
-    const int64_t nrem = d - pp - pw;
-    k_diag_block<T><<<(unsigned)nm, kT, 0, a.stream>>>(d, pp, F, a.dev_info);
-    const int64_t nch = (nrem + P - 1) / P + (m + P - 1) / P;
-    k_panel_product<T, kRowPanel><<<dim3((unsigned)nch, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R);
-    if (nrem > 0) {
-      const int64_t T2 = (nrem + P - 1) / P;
-      const int64_t jobs = T2 * (T2 + 1) / 2 + T2 * ((m + P - 1) / P);
-      k_panel_product<T, kTrailing><<<dim3((unsigned)jobs, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, F, R);
+  // Blocked right-looking factorization with the forward substitution of the RHS
+  // carried along.  The trailing matrix is updated once per super-panel of kSuper
+  // panels (one pass over it per kSuper * P columns); inside a super-panel each panel
+  // first receives the contributions of the super-panel's earlier panels (a strip
+  // update of its own rows), then is factored (diagonal block) and solved (row panel).
+  constexpr int P = Mf<T>::P, kSuper = 4;
+  const bool x6 = sizeof(T) == 4 && d % 4 == 0;
+  const int64_t TM = (m + P - 1) / P;
+  for (int64_t P0 = 0; P0 < d; P0 += kSuper * P) {
+    const int64_t P1 = (d - P0) < kSuper * P ? d : P0 + kSuper * P;
+    for (int64_t pp = P0; pp < P1; pp += P) {
+      const int64_t pw = (d - pp) < P ? (d - pp) : P;
+      const int64_t nrem = d - pp - pw;
+      if (pp > P0) {
+        const int64_t T2 = (d - pp + P - 1) / P;
+        k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, a.stream>>>(
+            d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
+      }
+      k_diag_block<T><<<(unsigned)nm, kT, 0, a.stream>>>(d, pp, F, a.dev_info);
+      const int64_t nch = (nrem + P - 1) / P + TM;
+      k_panel_product<T, kRowPanel><<<dim3((unsigned)nch, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, 0, 0, 0, 0, 0,
+                                                                                             F, R);
+    }
+    if (P1 < d) {
+      const int64_t T2 = (d - P1 + P - 1) / P, nU = T2 * (T2 + 1) / 2;
+      if (x6) {
+        const int64_t T6 = (d - P1 + 255) / 256;
+        k_trail_x6<<<dim3((unsigned)(T6 * (T6 + 1) / 2), (unsigned)nm), 512, 0, a.stream>>>(d, P0, P1 - P0, P1,
+                                                                                            (float*)F);
+        k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, a.stream>>>(
+            d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
+      } else {
+        k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, a.stream>>>(
+            d, m, 0, P0, P1 - P0, P1, 0, 0, F, R);
+      }
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -25,16 +25,33 @@ constexpr int kSmallMaxK = 64;
 constexpr int kMaxK = 128;
 
 // G_b = B~_b B~_b^T (k x k, fp64), one thread per (a, c) entry.
-__global__ void k_credit_gram(int64_t k, int64_t d, const float* __restrict__ B, int64_t b_bstride,
-                              double* __restrict__ G) {
-  const int64_t b = blockIdx.y;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= k * k) return;
-  const int64_t a = e / k, c = e % k;
+// G = B~ B~^T in float64, one workgroup per (block, row a, kCG columns c): the threads
+// stride over the width d with coalesced reads of row a and the kCG rows c, then each
+// entry is summed over the workgroup in a fixed order.
+constexpr int kCG = 16;
+__global__ __launch_bounds__(256) void k_credit_gram(int64_t k, int64_t d, const float* __restrict__ B,
+                                                     int64_t b_bstride, double* __restrict__ G) {
+  const int64_t b = blockIdx.z, a = blockIdx.y, c0 = (int64_t)blockIdx.x * kCG;
   const float* Bb = B + b * b_bstride;
-  double s = 0.0;
-  for (int64_t i = 0; i < d; ++i) s += (double)Bb[a * d + i] * (double)Bb[c * d + i];
-  G[b * k * k + e] = s;
+  double s[kCG];
+#pragma unroll
+  for (int j = 0; j < kCG; ++j) s[j] = 0.0;
+  for (int64_t i = threadIdx.x; i < d; i += 256) {
+    const double x = (double)Bb[a * d + i];
+#pragma unroll
+    for (int j = 0; j < kCG; ++j) s[j] += x * (double)ld_or_zero(Bb, (c0 + j) * d + i, c0 + j < k);
+  }
+  __shared__ double red[kCG][4];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int j = 0; j < kCG; ++j) {
+    const double v = wave_sum(s[j]);
+    if (lane == 0) red[j][wid] = v;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < kCG && c0 + threadIdx.x < k)
+    G[b * k * k + a * k + c0 + threadIdx.x] = ((red[threadIdx.x][0] + red[threadIdx.x][1]) + red[threadIdx.x][2]) +
+                                              red[threadIdx.x][3];
 }
 
 template <typename LT, typename AT, int KB>
@@ -284,7 +301,7 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   float* ms = use_small(a.C, a.k) ? nullptr : (float*)p;
 
   k_fill_i32<<<1, 64, 0, a.stream>>>(a.dev_info, 1, INT32_MAX);
-  dim3 gg((unsigned)((a.k * a.k + 255) / 256), (unsigned)a.nb);
+  dim3 gg((unsigned)((a.k + kCG - 1) / kCG), (unsigned)a.k, (unsigned)a.nb);
   k_credit_gram<<<gg, 256, 0, a.stream>>>(a.k, a.d, a.credit_b, a.b_bstride, G);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -16,6 +16,8 @@
 // workgroup and summed in a fixed order: results are deterministic.
 //
 // fp32 mode: X is fp32 and the statistics are fp64 (v_mfma_f64_16x16x4f64).
+#include <algorithm>
+
 #include "loca_common.h"
 
 namespace loca {
@@ -237,13 +239,30 @@ LOCA_DEV void lds_dma16(const void* gptr, uint32_t lds_base) {
 // Workgroup barrier without a memory fence (the pipeline waits for its own loads explicitly).
 LOCA_DEV void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
 
-__global__ __launch_bounds__(512) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
-                                                      int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
-                                                      int64_t s_bstride, double* __restrict__ diag_part,
-                                                      const uint16_t* __restrict__ zero16) {
-  constexpr int BM = 256, WGM = 2, WGN = 4, NT = 512;
+// The hardware hands consecutive workgroups to the eight XCDs in turn, and each XCD
+// has its own L2.  Workgroup L is therefore given logical tile x * per + idx, with
+// x = L % 8 and idx = L / 8, so that the tiles one XCD runs at the same time are
+// neighbours in the upper triangle of one block and share their column panels in L2.
+LOCA_DEV int xcd_logical(int L, int total) {
+  const int per = total / 8, rem = total % 8;
+  const int x = L % 8, idx = L / 8;
+  return x * per + (x < rem ? x : rem) + idx;
+}
+
+// WGM x WGN waves of (256 / WGM) x (256 / WGN) columns each: 2 x 4 waves (two per SIMD)
+// or 2 x 2 waves of 128 x 128 (one per SIMD, a third fewer LDS reads per MFMA).
+template <int WGM, int WGN>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
+                                                                int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
+                                                                int64_t s_bstride, double* __restrict__ diag_part,
+                                                                const uint16_t* __restrict__ zero16, int64_t b0) {
+  constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
-  constexpr int TILE_ELEMS = kBK * BM;  // one panel stage (bf16 elements)
+  constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
+  constexpr int NQ = TILE_ELEMS * 2 / 16 / NT;    // 16-byte copies per thread per panel
+  constexpr int NCP = 2 * NQ;                     // copies per thread per stage
+  constexpr int NSLOT = 2 * NBM;                  // fragment rows of MFMAs per stage
+  static_assert(NCP <= NSLOT, "at most one copy between two fragment rows");
   // one LDS object per ring slot: the loop below touches each through a static name,
   // so the in-flight loads into one slot are not mistaken for writes to the slot read
   __shared__ __attribute__((aligned(1024))) uint16_t sb0[2 * TILE_ELEMS];
@@ -254,10 +273,12 @@ __global__ __launch_bounds__(512) void k_gram_bf16_dl(int64_t n, int64_t d, cons
   static_assert(kDLStages == 4, "the ring below is written out for four slots");
 
   const int T = (int)((d + BM - 1) / BM);
+  const int ntile = T * (T + 1) / 2;
+  const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
   int I, J;
-  upper_tile(blockIdx.x, T, I, J);
+  upper_tile(logical % ntile, T, I, J);
   const bool diag = (I == J);
-  const int64_t b = blockIdx.y;
+  const int64_t b = b0 + logical / ntile;
   const uint16_t* X = Xall + b * x_bstride;
   float* S = Sall + b * s_bstride;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
@@ -266,27 +287,23 @@ __global__ __launch_bounds__(512) void k_gram_bf16_dl(int64_t n, int64_t d, cons
   const int64_t cI = (int64_t)I * BM, cJ = (int64_t)J * BM;
   const int nk = (int)((n + kBK - 1) / kBK);
 
-  // per-thread source chunks: instruction q of wave w fills LDS slots (2w + q) * 64 + lane
-  int lrow[2], lcol[2];
+  // per-thread source chunks: copy q of wave w fills LDS chunks (NQ w + q) * 64 + lane
+  int lrow[NQ], lcol[NQ];
 #pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int slot = (2 * wid + q) * 64 + lane;
+  for (int q = 0; q < NQ; ++q) {
+    const int slot = (NQ * wid + q) * 64 + lane;
     lrow[q] = slot >> 5;
     lcol[q] = 8 * ((slot & 31) ^ dl_swz(slot >> 5));
   }
-  auto issue = [&](uint16_t* buf, int kt) {
-    const int64_t t0 = (int64_t)kt * kBK;
-#pragma unroll
-    for (int pnl = 0; pnl < 2; ++pnl) {
-      const int64_t c0 = pnl == 0 ? cI : cJ;  // a diagonal tile loads its panel twice
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const int64_t t = t0 + lrow[q], col = c0 + lcol[q];
-        const uint16_t* src = (t < n && col < d) ? X + t * ldx + col : zero16;
-        const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (2 * wid + q) * 1024;
-        lds_dma16(src, __builtin_amdgcn_readfirstlane(dst));
-      }
-    }
+  // Copy j (0 .. NCP-1) of a stage: panel j / NQ (a diagonal tile loads its panel twice), chunk j % NQ.
+  auto issue = [&](uint16_t* buf, int kt, int j) {
+    const int pnl = j / NQ, q = j % NQ;
+    const int64_t t = (int64_t)kt * kBK + lrow[q], col = (pnl == 0 ? cI : cJ) + lcol[q];
+    // both addresses are formed and one selected, without a branch
+    const uint64_t in_x = (uint64_t)(uintptr_t)X + 2 * (uint64_t)(t * ldx + col);
+    const uint64_t src = (t < n && col < d) ? in_x : (uint64_t)(uintptr_t)zero16;
+    const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (NQ * wid + q) * 1024;
+    lds_dma16((const void*)(uintptr_t)src, __builtin_amdgcn_readfirstlane(dst));
   };
 
   f32x16_t acc[NBM][NBN];
@@ -301,7 +318,12 @@ __global__ __launch_bounds__(512) void k_gram_bf16_dl(int64_t n, int64_t d, cons
   // stage and across stages: the operands of the next half (or of the next stage's
   // first half) are read from LDS while the MFMAs of the current half run.  Reading
   // stage kt + 1 during stage kt needs it landed too, so each step waits until at most
-  // one stage of loads (four per thread) is in flight and refills the slot of kt + 3.
+  // one stage of copies is in flight and refills the slot of kt + 3.
+  // The copies of a step are spread between its rows of MFMAs: a wave issues in order,
+  // and copies issued back to back would queue at the address unit and hold up the
+  // MFMAs behind them.  Every wave runs the same instruction stream (waves of a
+  // diagonal tile below its diagonal compute too and only skip the write-back), so
+  // the loop has no divergent branches.
   bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN];
   auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
 #pragma unroll
@@ -309,37 +331,42 @@ __global__ __launch_bounds__(512) void k_gram_bf16_dl(int64_t n, int64_t d, cons
 #pragma unroll
     for (int m = 0; m < NBM; ++m) fa[m] = frag32_tr_swz(buf, wi * WM + 32 * m, ks, lane);
   };
-  auto mma_block = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN]) {
+  auto mma_row = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN], int m) {
 #pragma unroll
-    for (int m = 0; m < NBM; ++m)
-#pragma unroll
-      for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
+    for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
   };
-#define LOCA_DL_STEP(cur, nxt, fill, kt)                           \
-  {                                                                \
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(4));                      \
-    barrier_nofence();                                             \
-    issue(fill, (kt) + kDLStages - 1);                             \
-    if (active) {                                                  \
-      load_frags(cur, 16, fa1, fb1);                               \
-      mma_block(fa0, fb0);                                         \
-      if ((kt) + 1 < nk) load_frags(nxt, 0, fa0, fb0);             \
-      mma_block(fa1, fb1);                                         \
-    }                                                              \
-  }
-  issue(sb0, 0);  // stages past nk read zeros: harmless
-  issue(sb1, 1);
-  issue(sb2, 2);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(8));  // stage 0 landed
+  auto step = [&](uint16_t* cur, uint16_t* nxt, uint16_t* fill, int kt) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(NCP));  // stage kt + 1 landed (this thread's copies)
+    barrier_nofence();                           // ... everyone's; slot `fill` no longer read
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+      if ((sl * NCP) % NSLOT == 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        issue(fill, kt + kDLStages - 1, sl * NCP / NSLOT);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (sl == 0) load_frags(cur, 16, fa1, fb1);
+      if (sl == NBM) load_frags(nxt, 0, fa0, fb0);
+      if (sl < NBM) mma_row(fa0, fb0, sl);
+      else mma_row(fa1, fb1, sl - NBM);
+    }
+  };
+  // stages past nk read zeros: harmless
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) issue(sb0, 0, j);
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) issue(sb1, 1, j);
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) issue(sb2, 2, j);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NCP));  // stage 0 landed
   barrier_nofence();
-  if (active) load_frags(sb0, 0, fa0, fb0);
+  load_frags(sb0, 0, fa0, fb0);
   for (int kt = 0; kt < nk; kt += 4) {
-    LOCA_DL_STEP(sb0, sb1, sb3, kt);
-    if (kt + 1 < nk) LOCA_DL_STEP(sb1, sb2, sb0, kt + 1);
-    if (kt + 2 < nk) LOCA_DL_STEP(sb2, sb3, sb1, kt + 2);
-    if (kt + 3 < nk) LOCA_DL_STEP(sb3, sb0, sb2, kt + 3);
+    step(sb0, sb1, sb3, kt);
+    if (kt + 1 < nk) step(sb1, sb2, sb0, kt + 1);
+    if (kt + 2 < nk) step(sb2, sb3, sb1, kt + 2);
+    if (kt + 3 < nk) step(sb3, sb0, sb2, kt + 3);
   }
-#undef LOCA_DL_STEP
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // drain the look-ahead loads before the workgroup ends
 
   double dsum = 0.0;
@@ -631,8 +658,23 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   dim3 grid((unsigned)(T * (T + 1) / 2), (unsigned)a.nb);
   if (big && (a.d % 8) == 0) {
     k_zero_bytes<<<1, 64, 0, a.stream>>>((uint32_t*)a.ws, 64);
-    k_gram_bf16_dl<<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part,
-                                               zero16);
+    // one-dimensional grid (the XCD-aware order spans the blocks), in chunks of blocks
+    // small enough that the grid stays far below the launch limits
+    const int64_t ntile = (int64_t)T * (T + 1) / 2;
+    const int64_t chunk = std::max<int64_t>(1, ((int64_t)1 << 22) / ntile);
+    for (int64_t b0 = 0; b0 < a.nb; b0 += chunk) {
+      const int64_t nbc = std::min<int64_t>(chunk, a.nb - b0);
+#ifndef LOCA_DL_WAVES
+#define LOCA_DL_WAVES 8
+#endif
+#if LOCA_DL_WAVES == 4
+      k_gram_bf16_dl<2, 2><<<dim3((unsigned)(ntile * nbc)), 256, 0, a.stream>>>(
+          a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0);
+#else
+      k_gram_bf16_dl<2, 4><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
+          a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0);
+#endif
+    }
   } else if (big)
     k_gram_bf16<256, 2, 4><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
                                                        diag_part);
