@@ -50,29 +50,36 @@ __global__ void k_equil_diag(int64_t d, const ST* __restrict__ S, int64_t s_bstr
 }
 
 // F[i][j] = D_i (S_ij + lam delta_ij) D_j for j >= i; RHS[i][c] = D_i [S Lp | K][i][c].
+// One workgroup per (kEqRows rows, block): a row of S is read once for all nl lambdas.
+constexpr int kEqRows = 16;
 template <typename T, typename ST>
-__global__ void k_equil_setup(int64_t d, int64_t m, int64_t r_prev, const ST* __restrict__ S, int64_t s_bstride,
-                              const ST* __restrict__ K, int64_t k_bstride, const double* __restrict__ SLp,
-                              const double* __restrict__ lam, int nl, const T* __restrict__ D, T* __restrict__ F,
-                              T* __restrict__ R) {
-  const int64_t mi = blockIdx.z;
-  const int64_t b = mi / nl;
-  const int l = (int)(mi % nl);
-  const int64_t i = blockIdx.y;
-  const T* Dm = D + mi * d;
-  const double di = (double)Dm[i];
-  const ST* Si = S + b * s_bstride + i * d;
-  T* Fi = F + mi * d * d + i * d;
+__global__ __launch_bounds__(256) void k_equil_setup(int64_t d, int64_t m, int64_t r_prev, const ST* __restrict__ S,
+                                                     int64_t s_bstride, const ST* __restrict__ K, int64_t k_bstride,
+                                                     const double* __restrict__ SLp, const double* __restrict__ lam,
+                                                     int nl, const T* __restrict__ D, T* __restrict__ F,
+                                                     T* __restrict__ R) {
+  const int64_t b = blockIdx.y;
   const int64_t k = m - r_prev;
-  for (int64_t j = i + (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < d; j += (int64_t)gridDim.x * blockDim.x) {
-    const double v = (double)Si[j] + (j == i ? lam[l] : 0.0);
-    Fi[j] = (T)(di * v * (double)Dm[j]);
-  }
-  if (blockIdx.x == 0)
-    for (int64_t c = threadIdx.x; c < m; c += blockDim.x) {
-      double v = (c < r_prev) ? SLp[b * d * r_prev + i * r_prev + c] : (double)K[b * k_bstride + i * k + (c - r_prev)];
-      R[mi * d * m + i * m + c] = (T)(di * v);
+  for (int ii = 0; ii < kEqRows; ++ii) {
+    const int64_t i = (int64_t)blockIdx.x * kEqRows + ii;
+    if (i >= d) return;
+    const ST* Si = S + b * s_bstride + i * d;
+    for (int64_t j = i + threadIdx.x; j < d; j += blockDim.x) {
+      const double sij = (double)Si[j];
+      for (int l = 0; l < nl; ++l) {
+        const int64_t mi = b * nl + l;
+        const double v = sij + (j == i ? lam[l] : 0.0);
+        F[mi * d * d + i * d + j] = (T)((double)D[mi * d + i] * v * (double)D[mi * d + j]);
+      }
     }
+    for (int64_t c = threadIdx.x; c < m; c += blockDim.x) {
+      const double v = (c < r_prev) ? SLp[b * d * r_prev + i * r_prev + c] : (double)K[b * k_bstride + i * k + (c - r_prev)];
+      for (int l = 0; l < nl; ++l) {
+        const int64_t mi = b * nl + l;
+        R[mi * d * m + i * m + c] = (T)((double)D[mi * d + i] * v);
+      }
+    }
+  }
 }
 
 // SLp[b] = S_sym Lp (d x r_prev, fp64) from the upper triangle of S.
@@ -265,6 +272,164 @@ __global__ __launch_bounds__(kT) void k_diag_block(int64_t d, int64_t p, T* __re
     }
 }
 
+// ------------------------------------------------------------------ diagonal block, float, blocked by 32
+
+// acc += Aop Bop for one 32 x 32 block with K = 32 from LDS (fp32 MFMA 32x32x2, 16 steps):
+// Aop[i][k] = Am[i * lda + k] (a_rows) or Am[k * lda + i]; Bop[k][j] = Bm[k * ldb + j].
+LOCA_DEV void mm32(f32x16_t& acc, const float* Am, int lda, bool a_rows, const float* Bm, int ldb, int lane) {
+  const int i = lane & 31, kh = lane >> 5;
+#pragma unroll
+  for (int s2 = 0; s2 < 32; s2 += 2) {
+    const int k = s2 + kh;
+    const float av = a_rows ? Am[i * lda + k] : Am[k * lda + i];
+    acc = mfma_f32x2(av, Bm[k * ldb + i], acc);
+  }
+}
+LOCA_DEV void zero16(f32x16_t& acc) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+}
+
+// Wait until this wave's LDS operations are done (s_waitcnt lgkmcnt(0)); with the
+// in-order LDS of a wave, rows one lane writes are then read back by the others.
+LOCA_DEV void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  __builtin_amdgcn_wave_barrier();
+}
+
+// One wave factors the 32 x 32 block B (upper part used) as U^T U, writes U over B (zero
+// below the diagonal) and X = U^{-1} to Xo.  Lane c < 32 holds column c (rows 0..31);
+// lanes 32..63 mirror lanes 0..31 and write nothing.  Step j publishes row j of the
+// current matrix through the wave's LDS row `rb` (32 floats); the inverse is built
+// bottom-up from rows of U read back from B.  The first non-positive pivot among the
+// first `valid` is reported (1-based, offset base).
+LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, float* rb, int lane, int valid, int64_t base,
+                         int32_t* info) {
+  const int c = lane & 31;
+  const bool wr = lane < 32;
+  float a[32];
+#pragma unroll
+  for (int r = 0; r < 32; ++r) a[r] = B[r * ld + c];
+#pragma unroll
+  for (int j = 0; j < 32; ++j) {
+    if (wr) rb[c] = a[j];  // row j: B[j][c]
+    wave_lds_sync();
+    float rr[32];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const float4 t = *(const float4*)(rb + 4 * v);
+      rr[4 * v] = t.x; rr[4 * v + 1] = t.y; rr[4 * v + 2] = t.z; rr[4 * v + 3] = t.w;
+    }
+    const float piv = rr[j];
+    if (!(piv > 0.f) && j < valid && lane == 0) atomicCAS(info, 0, (int32_t)(base + j + 1));
+    const float ujj = sqrtf(piv);
+    const float inv = 1.0f / ujj;
+    const float uc = c > j ? a[j] * inv : (c == j ? ujj : 0.f);  // U[j][c]
+    a[j] = uc;
+#pragma unroll
+    for (int i = j + 1; i < 32; ++i) a[i] -= (rr[i] * inv) * uc;
+    wave_lds_sync();  // every lane has read rb before the next row is written
+  }
+  if (wr) {
+#pragma unroll
+    for (int r = 0; r < 32; ++r) B[r * ld + c] = r <= c ? a[r] : 0.f;
+  }
+  wave_lds_sync();
+  float x[32];
+#pragma unroll
+  for (int i = 31; i >= 0; --i) {
+    float ur[32];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const float4 t = *(const float4*)(B + i * ld + 4 * v);
+      ur[4 * v] = t.x; ur[4 * v + 1] = t.y; ur[4 * v + 2] = t.z; ur[4 * v + 3] = t.w;
+    }
+    float part = 0.f;
+#pragma unroll
+    for (int k = i + 1; k < 32; ++k) part += ur[k] * x[k];
+    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - part) / ur[i] : 0.f;
+  }
+  if (wr) {
+#pragma unroll
+    for (int r = 0; r < 32; ++r) Xo[r * ldx + c] = x[r];
+  }
+}
+
+// Factor and invert the P x P (P = 128) diagonal block of F at p, blocked by 32: per
+// 32-column block q, one wave factors and inverts the block (chol_inv32), the waves form
+// its row panel U_qr = X_qq^T A_qr and the update A_rs -= U_qr^T U_qs with MFMA; the
+// inverse of the whole block is then assembled column by column (wave s):
+// X_rs = -X_rr sum_{r < t <= s} U_rt X_ts.  Entries past the matrix (a ragged last block)
+// are an identity extension.  Output as for k_diag_block: X over the diagonal block, zero
+// strictly below its diagonal.
+__global__ __launch_bounds__(kT) void k_diag_f32(int64_t d, int64_t p, float* __restrict__ Fall,
+                                                 int32_t* __restrict__ dev_info) {
+  constexpr int P = 128, LD = 132;
+  __shared__ __attribute__((aligned(16))) float sA[P * LD];
+  __shared__ __attribute__((aligned(16))) float sX[P * LD];
+  __shared__ __attribute__((aligned(16))) float sT[3][32 * 36];
+  __shared__ __attribute__((aligned(16))) float su[32];  // row buffer of the factoring wave
+  const int64_t mi = blockIdx.x;
+  float* F = Fall + mi * d * d;
+  const float* A0 = F + p * d + p;
+  const int pw = (int)((d - p) < P ? (d - p) : P);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  for (int e = tid; e < P * P; e += kT) {
+    const int r = e >> 7, c = e & 127;
+    const bool in = r < pw && c < pw;
+    const float v = ld_or_zero(A0, (int64_t)r * d + c, in && c >= r);
+    sA[r * LD + c] = in ? v : (r == c ? 1.f : 0.f);
+    sX[r * LD + c] = 0.f;
+  }
+  __syncthreads();
+  for (int q = 0; q < 4; ++q) {
+    const int c0 = 32 * q;
+    if (wid == 0) chol_inv32(sA + c0 * LD + c0, LD, sX + c0 * LD + c0, LD, su, lane, pw - c0, p + c0, dev_info + mi);
+    __syncthreads();
+    const int nr = 3 - q;
+    if (wid < nr) {  // row panel block r: U_qr = X_qq^T A_qr
+      const int r = q + 1 + wid;
+      f32x16_t acc;
+      zero16(acc);
+      mm32(acc, sX + c0 * LD + c0, LD, false, sA + c0 * LD + 32 * r, LD, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sA[(c0 + mfma32_row(lane, e)) * LD + 32 * r + (lane & 31)] = acc[e];
+    }
+    __syncthreads();
+    for (int u = wid; u < nr * (nr + 1) / 2; u += 4) {  // trailing block (r, s), q < r <= s
+      int r = q + 1, rem = u;
+      while (rem >= 4 - r) { rem -= 4 - r; ++r; }
+      const int s2 = r + rem;
+      f32x16_t acc;
+      zero16(acc);
+      mm32(acc, sA + c0 * LD + 32 * r, LD, false, sA + c0 * LD + 32 * s2, LD, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sA[(32 * r + mfma32_row(lane, e)) * LD + 32 * s2 + (lane & 31)] -= acc[e];
+    }
+    __syncthreads();
+  }
+  if (wid >= 1) {  // column s = wid of the inverse
+    const int s2 = wid;
+    float* T = sT[wid - 1];
+    for (int r = s2 - 1; r >= 0; --r) {
+      f32x16_t acc;
+      zero16(acc);
+      for (int t = r + 1; t <= s2; ++t) mm32(acc, sA + 32 * r * LD + 32 * t, LD, true, sX + 32 * t * LD + 32 * s2, LD, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) T[mfma32_row(lane, e) * 36 + (lane & 31)] = acc[e];
+      zero16(acc);
+      mm32(acc, sX + 32 * r * LD + 32 * r, LD, true, T, 36, lane);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sX[(32 * r + mfma32_row(lane, e)) * LD + 32 * s2 + (lane & 31)] = -acc[e];
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < P * P; e += kT) {
+    const int r = e >> 7, c = e & 127;
+    if (r < pw && c < pw) F[(p + r) * d + p + c] = c >= r ? sX[r * LD + c] : 0.f;
+  }
+}
+
 // ------------------------------------------------------------------ panel products (row panel, trailing update)
 
 LOCA_DEV void upper_tile_c(int u, int T, int& I, int& J) {
@@ -307,8 +472,9 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
   const T* gQ;
   int64_t ldq, prows_ok;
   if (JOB == kRowPanel) {
-    rhs = (int64_t)blockIdx.x >= nchF;
-    ocol = rhs ? ((int64_t)blockIdx.x - nchF) * P : off + (int64_t)blockIdx.x * P;
+    const int64_t job = (int64_t)blockIdx.x + job0;
+    rhs = job >= nchF;
+    ocol = rhs ? (job - nchF) * P : off + job * P;
     ocend = rhs ? m : d;
     orow = p;
     gP = F + p * d + p;
@@ -418,45 +584,74 @@ LOCA_DEV void split3(float a, uint16_t& h, uint16_t& m, uint16_t& l) {
   l = f32_to_bf16(r1 - bf16_to_f32(m));
 }
 
-// F[i][j] -= sum_{kk in [k0, k0 + kw)} F[kk][i] F[kk][j] on the upper 256 x 256 tiles of
-// the trailing region [off, d) (grid: x = tile, y = matrix).  A stage is 16 rows of K:
-// each operand (32 KB of float) is loaded into registers one stage ahead, split, and
-// written to LDS as three bf16 planes [16][LD]; eight waves of 128 x 64 read their
-// MFMA operands with transpose reads (LD = 288: the four rows a half-wave reads start
-// 64 bytes apart modulo 256, so the reads are conflict-free).  Requires d % 4 == 0.
+// Panel products on bf16 matrix cores, Out[i][j] (op)= sum_kk Pn[kk][i] Qn[kk][j]:
+//   kX6Trail: F[i][j] -= sum_{kk in [k0, k0 + kw)} F[kk][i] F[kk][j] on the upper
+//             256 x 256 tiles of the trailing region [off, d);
+//   kX6Strip: the same for the rows [off, off + 128) only (128 x 256 tiles, columns
+//             from off), the update of a panel by the earlier panels of its super-panel;
+//   kX6Row:   F[p + i][j] = sum_kk X[kk][i] F[p + kk][j] for the columns j >= p + 128 of
+//             the panel rows (128 x 256 tiles), X = U11^{-1} in the diagonal block.
+// A stage is 16 rows of K: each operand is loaded into registers one stage ahead, split,
+// and written to LDS as three bf16 planes [16][LD]; eight waves (2 x 4) read their MFMA
+// operands with transpose reads (LD = 288: the four rows a half-wave reads start 64 bytes
+// apart modulo 256, so the reads are conflict-free).  Requires d % 4 == 0.
 constexpr int kX6BK = 16, kX6LD = 288;
+enum X6Mode { kX6Trail = 0, kX6Strip = 1, kX6Row = 2 };
 
 LOCA_DEV float4 ld4_or_zero(const float* base, int64_t idx, bool ok) {
   const float4 v = *(const float4*)(base + (ok ? idx : 0));
   return ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
 }
+LOCA_DEV float4 ld4_or_zero_ro(const float* __restrict__ base, int64_t idx, bool ok) { return ld4_or_zero(base, idx, ok); }
 
-__global__ __launch_bounds__(512) void k_trail_x6(int64_t d, int64_t k0, int64_t kw, int64_t off,
+template <int MODE>
+__global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t kw, int64_t off,
                                                   float* __restrict__ Fall) {
-  constexpr int BM = 256, WGN = 4, WM = 128, WN = 64, NBM = WM / 32, NBN = WN / 32;
+  constexpr int BR = MODE == kX6Trail ? 256 : 128;  // output rows per tile
+  constexpr int BC = 256, WGN = 4, WM = BR / 2, WN = BC / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int LD = kX6LD, PLANE = kX6BK * LD;
+  constexpr int QP = BR * kX6BK / 4 / 512, QQ = BC * kX6BK / 4 / 512;  // float4 loads per thread
   __shared__ __attribute__((aligned(16))) uint16_t sm[2][6 * PLANE];  // [buffer][operand * 3 + part]
   const int64_t mi = blockIdx.y;
   float* F = Fall + mi * d * d;
-  const int T2 = (int)((d - off + BM - 1) / BM);
-  int I, J;
-  upper_tile_c((int)blockIdx.x, T2, I, J);
-  const bool diag = I == J;
-  const int64_t orow = off + (int64_t)I * BM, ocol = off + (int64_t)J * BM;
+  int64_t orow, ocol, pcol;
+  bool diag;
+  if (MODE == kX6Trail) {
+    const int T2 = (int)((d - off + BC - 1) / BC);
+    int I, J;
+    upper_tile_c((int)blockIdx.x, T2, I, J);
+    diag = I == J;
+    orow = off + (int64_t)I * BC;
+    ocol = off + (int64_t)J * BC;
+    pcol = orow;
+  } else if (MODE == kX6Strip) {
+    diag = blockIdx.x == 0;
+    orow = off;
+    ocol = off + (int64_t)blockIdx.x * BC;
+    pcol = orow;
+  } else {  // kX6Row: K rows and output rows [k0, k0 + 128), Pn = the diagonal block
+    diag = false;
+    orow = k0;
+    ocol = k0 + 128 + (int64_t)blockIdx.x * BC;
+    pcol = k0;
+  }
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, wi = wid / WGN, wj = wid % WGN;
   const bool active = !(diag && (wj + 1) * WN <= wi * WM);
-  const float* gP = F + k0 * d + orow;
+  const float* gP = F + k0 * d + pcol;
   const float* gQ = F + k0 * d + ocol;
+  const int64_t pend = MODE == kX6Row ? k0 + 128 : d;  // columns of Pn that exist: < pend
 
-  // staging: float4 chunk c = tid + 512 q of the 16 x 64 chunks of an operand stage
-  float4 rp[2], rq[2];
+  float4 rp[QP], rq[QQ];
   auto load = [&](int kc0) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < QP; ++q) {
+      const int c = tid + 512 * q, kk = c / (BR / 4), c4 = 4 * (c % (BR / 4));
+      rp[q] = ld4_or_zero(gP, (int64_t)(kc0 + kk) * d + c4, kc0 + kk < kw && pcol + c4 < pend);
+    }
+#pragma unroll
+    for (int q = 0; q < QQ; ++q) {
       const int c = tid + 512 * q, kk = c >> 6, c4 = 4 * (c & 63);
-      const bool okk = kc0 + kk < kw;
-      rp[q] = ld4_or_zero(gP, (int64_t)(kc0 + kk) * d + c4, okk && orow + c4 < d);
-      rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * d + c4, okk && ocol + c4 < d);
+      rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * d + c4, kc0 + kk < kw && ocol + c4 < d);
     }
   };
   auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
@@ -472,10 +667,14 @@ __global__ __launch_bounds__(512) void k_trail_x6(int64_t d, int64_t k0, int64_t
   };
   auto store = [&](int buf) {
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-      const int c = tid + 512 * q, kk = c >> 6, c4 = 4 * (c & 63);
-      put(&sm[buf][0], kk, c4, rp[q]);
-      put(&sm[buf][3 * PLANE], kk, c4, rq[q]);
+    for (int q = 0; q < QP; ++q) {
+      const int c = tid + 512 * q;
+      put(&sm[buf][0], c / (BR / 4), 4 * (c % (BR / 4)), rp[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < QQ; ++q) {
+      const int c = tid + 512 * q;
+      put(&sm[buf][3 * PLANE], c >> 6, 4 * (c & 63), rq[q]);
     }
   };
 
@@ -503,7 +702,7 @@ __global__ __launch_bounds__(512) void k_trail_x6(int64_t d, int64_t k0, int64_t
       for (int b = 0; b < NBN; ++b) fb[t][b] = frag32_tr(&sm[cur][(3 + t) * PLANE], LD, wj * WN + 32 * b, 0, lane);
     }
     // the six kept terms, smallest first; each term runs over all blocks, so the MFMAs
-    // into one accumulator are eight instructions apart
+    // into one accumulator are NBM * NBN instructions apart
     constexpr int TA[6] = {2, 0, 1, 1, 0, 0}, TB[6] = {0, 2, 1, 0, 1, 0};
 #pragma unroll
     for (int t = 0; t < 6; ++t)
@@ -515,6 +714,7 @@ __global__ __launch_bounds__(512) void k_trail_x6(int64_t d, int64_t k0, int64_t
     __syncthreads();
   }
   if (!active) return;
+  const int64_t rend = MODE == kX6Row ? k0 + 128 : (MODE == kX6Strip ? off + 128 : d);
 #pragma unroll
   for (int a = 0; a < NBM; ++a)
 #pragma unroll
@@ -522,15 +722,18 @@ __global__ __launch_bounds__(512) void k_trail_x6(int64_t d, int64_t k0, int64_t
       const int64_t col = ocol + wj * WN + 32 * b + mfma32_col(lane);
       const int64_t rb = orow + wi * WM + 32 * a;
       float old[16];
+      if (MODE != kX6Row) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = rb + mfma32_row(lane, r);
-        old[r] = ld_or_zero(F, row * d + col, row < d && col < d && col >= row);
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = rb + mfma32_row(lane, r);
+          old[r] = ld_or_zero(F, row * d + col, row < rend && col < d && col >= row);
+        }
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = rb + mfma32_row(lane, r);
-        if (row < d && col < d && col >= row) F[row * d + col] = old[r] - acc[a][b][r];
+        if (row < rend && col < d && col >= row)
+          F[row * d + col] = MODE == kX6Row ? acc[a][b][r] : old[r] - acc[a][b][r];
       }
     }
 }
@@ -637,6 +840,132 @@ __global__ __launch_bounds__(kT) void k_back_step(int64_t d, int64_t m, int64_t 
     }
 }
 
+// ------------------------------------------------------------------ back substitution, float
+
+// One launch per row block p (descending) of U M' = Y, right-looking, with M'_p already
+// in Mp: workgroups x >= 1 apply R_r -= U_{r,p} M'_p to four row blocks r above p each;
+// workgroup 0 applies it to the block q just above p and then forms M'_q = U_qq^{-1} R_q
+// (U_qq^{-1} sits in the diagonal block of F), so the next launch finds M'_q in Mp.  With
+// `init`, workgroup 0 only forms M'_p of the last block.  The first operand of every
+// product streams from F into registers: MFMA j of a K range of 32 takes k = 16 h + j
+// in lane half h, for both operands, so a lane reads 16 consecutive floats of its row.
+// The second operand (M'_p, or the updated R_q) sits transposed in LDS.
+template <int NQ, bool V4>
+__global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p, int init, const float* __restrict__ Fall,
+                                                 float* __restrict__ Rall, float* __restrict__ Mpall) {
+  constexpr int P = 128, LDT = P + 4;
+  __shared__ __attribute__((aligned(16))) float sT[NQ * 32 * LDT];  // [column][k]
+  const int64_t mi = blockIdx.y;
+  const float* F = Fall + mi * d * d;
+  float* R = Rall + mi * d * m;
+  float* Mp = Mpall + mi * d * m;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, li = lane & 31, h = lane >> 5;
+  const int pw = (int)((d - p) < P ? (d - p) : P);
+
+  // acc[q] = sum_{k < kmax} A[32 wid + li][k] T[k][32 q + li] for the wave's 32 rows
+  // (rows >= rows_ok of A read as zero)
+  auto product = [&](const float* A, int kmax, int rows_ok, f32x16_t (&acc)[NQ]) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[q][r] = 0.f;
+    const bool rok = 32 * wid + li < rows_ok;
+    const float* arow = A + (int64_t)(rok ? 32 * wid + li : 0) * d;
+    for (int kk0 = 0; kk0 < kmax; kk0 += 32) {
+      const int kb = kk0 + 16 * h;
+      float a[16];
+      if (V4) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float4 t = ld4_or_zero_ro(arow, kb + 4 * v, rok && kb + 4 * v < kmax);
+          a[4 * v] = t.x; a[4 * v + 1] = t.y; a[4 * v + 2] = t.z; a[4 * v + 3] = t.w;
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 16; ++j) a[j] = ld_or_zero(arow, kb + j, rok && kb + j < kmax);
+      }
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const float* tb = sT + (32 * q + li) * LDT + kb;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float4 t = *(const float4*)(tb + 4 * v);
+          acc[q] = mfma_f32x2(a[4 * v], t.x, acc[q]);
+          acc[q] = mfma_f32x2(a[4 * v + 1], t.y, acc[q]);
+          acc[q] = mfma_f32x2(a[4 * v + 2], t.z, acc[q]);
+          acc[q] = mfma_f32x2(a[4 * v + 3], t.w, acc[q]);
+        }
+      }
+    }
+  };
+  // sT[c][k] = src[k][c] for k < rows, c < m (zero elsewhere)
+  auto load_t = [&](const float* src, int rows) {
+    for (int e = tid; e < NQ * 32 * P; e += kT) {
+      const int k = e / (NQ * 32), c = e % (NQ * 32);
+      sT[c * LDT + k] = ld_or_zero(src, (int64_t)k * m + c, k < rows && c < m);
+    }
+  };
+  auto store_mp = [&](int64_t r0, int rows, const f32x16_t (&acc)[NQ]) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * wid + mfma32_row(lane, r), col = 32 * q + li;
+        if (row < rows && col < m) Mp[(r0 + row) * m + col] = acc[q][r];
+      }
+  };
+
+  f32x16_t acc[NQ];
+  if (init) {  // M'_p of the last block from its forward-substituted rows
+    load_t(R + p * m, pw);
+    __syncthreads();
+    product(F + p * d + p, pw, pw, acc);
+    store_mp(p, pw, acc);
+    return;
+  }
+  load_t(Mp + p * m, pw);
+  __syncthreads();
+  const int64_t nab = p / P;  // row blocks above p
+  if (blockIdx.x == 0) {
+    const int64_t r0 = p - P;
+    product(F + r0 * d + p, pw, P, acc);
+    __syncthreads();  // done with M'_p in LDS
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * wid + mfma32_row(lane, r), col = 32 * q + li;
+        const float v = col < m ? R[(r0 + row) * m + col] - acc[q][r] : 0.f;
+        sT[col * LDT + row] = v;
+      }
+    __syncthreads();
+    product(F + r0 * d + r0, P, P, acc);
+    store_mp(r0, P, acc);
+    return;
+  }
+  for (int c = 0; c < 4; ++c) {
+    const int64_t q0 = nab - 2 - 4 * ((int64_t)blockIdx.x - 1) - c;
+    if (q0 < 0) break;
+    const int64_t r0 = q0 * P;
+    product(F + r0 * d + p, pw, P, acc);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      float old[16];
+      const int col = 32 * q + li;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * wid + mfma32_row(lane, r);
+        old[r] = ld_or_zero(R, (r0 + row) * m + col, col < m);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * wid + mfma32_row(lane, r);
+        if (col < m) R[(r0 + row) * m + col] = old[r] - acc[q][r];
+      }
+    }
+  }
+}
+
 // M = D M' (undo the equilibration), float output.
 template <typename T>
 __global__ void k_unscale(int64_t d, int64_t m, const T* __restrict__ Rall, const T* __restrict__ Dall,
@@ -660,33 +989,31 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
   return s;
 }
 
+// The solve of the blocks [b0, b0 + nbg) (all their lambdas) on stream st; workspace
+// regions are those of the whole call.  `after_diag`, when given, is recorded after the
+// first diagonal-block launch.
 template <typename T, typename ST>
-hipError_t run_solve(const SolveArgs& a) {
-  const int64_t d = a.d, m = a.r_prev + a.k, nl = a.n_lambda, nm = a.nb * nl;
-  char* p = a.ws;
-  T* F = (T*)p; p += align256(sizeof(T) * nm * d * d);
-  T* R = (T*)p; p += align256(sizeof(T) * nm * d * m);
-  T* D = (T*)p; p += align256(sizeof(T) * nm * d);
-  T* Mp = (T*)p; p += align256(sizeof(T) * nm * d * m);
-  double* SLp = (double*)p;
-  Lams lams;
-  for (int i = 0; i < 8; ++i) lams.v[i] = (i < nl) ? a.lambdas[i] : 0.0;
-  double* dlam = (double*)(p + align256(sizeof(double) * a.nb * d * (a.r_prev > 0 ? a.r_prev : 1)));
-  // the host lambdas travel by value into a one-wave kernel (no copy from pageable memory)
-  k_set_lambdas<<<1, 64, 0, a.stream>>>(lams, dlam, (int)nl);
-  k_fill_zero_i32<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
-  const ST* S = (const ST*)a.S;
-  const ST* K = (const ST*)a.K;
+hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st, T* Fw, T* Rw, T* Dw, T* Mpw,
+                     double* SLpw, const double* dlam, hipEvent_t after_diag) {
+  const int64_t d = a.d, m = a.r_prev + a.k, nl = a.n_lambda, nm = nbg * nl, mi0 = b0 * nl;
+  T* F = Fw + mi0 * d * d;
+  T* R = Rw + mi0 * d * m;
+  T* D = Dw + mi0 * d;
+  T* Mp = Mpw + mi0 * d * m;
+  double* SLp = SLpw + b0 * d * (a.r_prev > 0 ? a.r_prev : 1);
+  int32_t* info = a.dev_info + mi0;
+  const ST* S = (const ST*)a.S + b0 * a.s_bstride;
+  const ST* K = (const ST*)a.K + b0 * a.k_bstride;
   if (a.r_prev > 0) {
-    dim3 g((unsigned)((d * a.r_prev + 255) / 256), (unsigned)a.nb);
-    k_sym_mul<ST><<<g, 256, 0, a.stream>>>(d, a.r_prev, S, a.s_bstride, a.lp, a.lp_bstride, SLp);
+    dim3 g((unsigned)((d * a.r_prev + 255) / 256), (unsigned)nbg);
+    k_sym_mul<ST><<<g, 256, 0, st>>>(d, a.r_prev, S, a.s_bstride, a.lp + b0 * a.lp_bstride, a.lp_bstride, SLp);
   }
   {
     dim3 g((unsigned)((d + 255) / 256), (unsigned)nm);
-    k_equil_diag<T, ST><<<g, 256, 0, a.stream>>>(d, S, a.s_bstride, dlam, (int)nl, D);
-    dim3 g2((unsigned)((d + 255) / 256 < 8 ? (d + 255) / 256 : 8), (unsigned)d, (unsigned)nm);
-    k_equil_setup<T, ST><<<g2, 256, 0, a.stream>>>(d, m, a.r_prev, S, a.s_bstride, K, a.k_bstride, SLp, dlam,
-                                                   (int)nl, D, F, R);
+    k_equil_diag<T, ST><<<g, 256, 0, st>>>(d, S, a.s_bstride, dlam, (int)nl, D);
+    dim3 g2((unsigned)((d + kEqRows - 1) / kEqRows), (unsigned)nbg);
+    k_equil_setup<T, ST><<<g2, 256, 0, st>>>(d, m, a.r_prev, S, a.s_bstride, K, a.k_bstride, SLp, dlam, (int)nl, D,
+                                              F, R);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -703,52 +1030,148 @@ hipError_t run_solve(const SolveArgs& a) {
     for (int64_t pp = P0; pp < P1; pp += P) {
       const int64_t pw = (d - pp) < P ? (d - pp) : P;
       const int64_t nrem = d - pp - pw;
+      const int64_t nchF = (nrem + P - 1) / P;
       if (pp > P0) {
         const int64_t T2 = (d - pp + P - 1) / P;
-        k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, a.stream>>>(
-            d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
+        if (x6) {
+          k_panel_x6<kX6Strip><<<dim3((unsigned)((d - pp + 255) / 256), (unsigned)nm), 512, 0, st>>>(
+              d, P0, pp - P0, pp, (float*)F);
+          k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
+              d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
+        } else {
+          k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, st>>>(
+              d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
+        }
       }
-      k_diag_block<T><<<(unsigned)nm, kT, 0, a.stream>>>(d, pp, F, a.dev_info);
-      const int64_t nch = (nrem + P - 1) / P + TM;
-      k_panel_product<T, kRowPanel><<<dim3((unsigned)nch, (unsigned)nm), kT, 0, a.stream>>>(d, m, pp, 0, 0, 0, 0, 0,
-                                                                                             F, R);
+      if constexpr (sizeof(T) == 4) k_diag_f32<<<(unsigned)nm, kT, 0, st>>>(d, pp, (float*)F, info);
+      else k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
+      if (after_diag && pp == 0) hipEventRecord(after_diag, st);
+      if (x6 && nrem > 0) {
+        k_panel_x6<kX6Row><<<dim3((unsigned)((nrem + 255) / 256), (unsigned)nm), 512, 0, st>>>(d, pp, pw, 0,
+                                                                                                     (float*)F);
+        k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
+                                                                                             (int)nchF, F, R);
+      } else {
+        k_panel_product<T, kRowPanel><<<dim3((unsigned)(nchF + TM), (unsigned)nm), kT, 0, st>>>(
+            d, m, pp, 0, 0, 0, 0, 0, F, R);
+      }
     }
     if (P1 < d) {
       const int64_t T2 = (d - P1 + P - 1) / P, nU = T2 * (T2 + 1) / 2;
       if (x6) {
         const int64_t T6 = (d - P1 + 255) / 256;
-        k_trail_x6<<<dim3((unsigned)(T6 * (T6 + 1) / 2), (unsigned)nm), 512, 0, a.stream>>>(d, P0, P1 - P0, P1,
-                                                                                            (float*)F);
-        k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, a.stream>>>(
+        k_panel_x6<kX6Trail><<<dim3((unsigned)(T6 * (T6 + 1) / 2), (unsigned)nm), 512, 0, st>>>(
+            d, P0, P1 - P0, P1, (float*)F);
+        k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
             d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
       } else {
-        k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, a.stream>>>(
+        k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, st>>>(
             d, m, 0, P0, P1 - P0, P1, 0, 0, F, R);
       }
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P) {
-    const dim3 grid((unsigned)(pp > 0 ? (pp + P - 1) / P : 1), (unsigned)nm);
-    const int nq = (int)((m + Mf<T>::BLK - 1) / Mf<T>::BLK);  // m <= 128 (checked by the API)
-    if (nq <= 1) k_back_step<T, 1><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
-    else if (nq <= 2) k_back_step<T, 2><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
-    else if (nq <= 4 || sizeof(T) == 4) k_back_step<T, 4><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
-    else if constexpr (sizeof(T) == 8) k_back_step<T, 8><<<grid, kT, 0, a.stream>>>(d, m, pp, F, R, Mp);
+  if constexpr (sizeof(T) == 4) {
+    const int64_t plast = ((d - 1) / P) * P;
+    const int nq = (int)((m + 31) / 32);  // m <= 128 (checked by the API)
+    auto back = [&](int64_t pp, int init, unsigned gx) {
+      const dim3 grid(gx, (unsigned)nm);
+      const bool v4 = d % 4 == 0 && m <= 128;
+#define LOCA_BACK(NQ)                                                                                \
+  if (v4) k_back_f32<NQ, true><<<grid, kT, 0, st>>>(d, m, pp, init, (const float*)F, (float*)R, (float*)Mp); \
+  else k_back_f32<NQ, false><<<grid, kT, 0, st>>>(d, m, pp, init, (const float*)F, (float*)R, (float*)Mp);
+      if (nq <= 1) { LOCA_BACK(1) }
+      else if (nq <= 2) { LOCA_BACK(2) }
+      else { LOCA_BACK(4) }
+#undef LOCA_BACK
+    };
+    back(plast, 1, 1);
+    for (int64_t pp = plast; pp >= P; pp -= P) {
+      const int64_t nab = pp / P;
+      back(pp, 0, (unsigned)(1 + (nab - 1 + 3) / 4));
+    }
+  } else {
+    for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P) {
+      const dim3 grid((unsigned)(pp > 0 ? (pp + P - 1) / P : 1), (unsigned)nm);
+      const int nq = (int)((m + Mf<T>::BLK - 1) / Mf<T>::BLK);  // m <= 128 (checked by the API)
+      if (nq <= 1) k_back_step<T, 1><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+      else if (nq <= 2) k_back_step<T, 2><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+      else if (nq <= 4) k_back_step<T, 4><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+      else k_back_step<T, 8><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+    }
   }
-  k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, a.stream>>>(d, m, Mp, D, a.m_out,
+  k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, st>>>(d, m, Mp, D, a.m_out + mi0 * a.m_bstride,
                                                                                           a.m_bstride);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (a.w_dense_out) {
     // W = M [Rp; B~]: rows of the right factor come from Rp (first r_prev) then B~.
     if (a.r_prev == 0)
-      return launch_lowrank_product(a.stream, nm, d, d, m, a.m_out, a.m_bstride, m, a.credit_b, a.b_bstride, nl, d,
-                                    a.w_dense_out, a.w_bstride);
+      return launch_lowrank_product(st, nm, d, d, m, a.m_out + mi0 * a.m_bstride, a.m_bstride, m,
+                                    a.credit_b + b0 * a.b_bstride, a.b_bstride, nl, d,
+                                    a.w_dense_out + mi0 * a.w_bstride, a.w_bstride);
     return hipErrorNotSupported;
   }
   return hipSuccess;
+}
+
+
+// Second stream and events per device, made on first use.  The blocks of a call are
+// split in two halves on two streams, the second started once the first has factored
+// its first diagonal block: the diagonal-block and back-substitution launches of one
+// half (a workgroup per matrix, latency bound) then run beside the matrix-core
+// updates of the other half instead of leaving most of the GPU idle.
+struct Aux {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, stagger = nullptr, join = nullptr;
+};
+Aux g_aux[64];
+
+hipError_t get_aux(Aux** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  Aux& x = g_aux[dev];
+  if (!x.s) {
+    if ((e = hipEventCreateWithFlags(&x.fork, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&x.stagger, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&x.join, hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking)) != hipSuccess) return e;
+  }
+  *out = &x;
+  return hipSuccess;
+}
+
+template <typename T, typename ST>
+hipError_t run_solve(const SolveArgs& a) {
+  const int64_t d = a.d, m = a.r_prev + a.k, nl = a.n_lambda, nm = a.nb * nl;
+  char* p = a.ws;
+  T* F = (T*)p; p += align256(sizeof(T) * nm * d * d);
+  T* R = (T*)p; p += align256(sizeof(T) * nm * d * m);
+  T* D = (T*)p; p += align256(sizeof(T) * nm * d);
+  T* Mp = (T*)p; p += align256(sizeof(T) * nm * d * m);
+  double* SLp = (double*)p;
+  Lams lams;
+  for (int i = 0; i < 8; ++i) lams.v[i] = (i < nl) ? a.lambdas[i] : 0.0;
+  double* dlam = (double*)(p + align256(sizeof(double) * a.nb * d * (a.r_prev > 0 ? a.r_prev : 1)));
+  // the host lambdas travel by value into a one-wave kernel (no copy from pageable memory)
+  k_set_lambdas<<<1, 64, 0, a.stream>>>(lams, dlam, (int)nl);
+  k_fill_zero_i32<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (a.nb < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr);
+  Aux* x = nullptr;
+  if ((e = get_aux(&x)) != hipSuccess) return e;
+  const int64_t nb0 = a.nb / 2;
+  if ((e = hipEventRecord(x->fork, a.stream)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(x->s, x->fork, 0)) != hipSuccess) return e;
+  if ((e = run_group<T, ST>(a, 0, nb0, a.stream, F, R, D, Mp, SLp, dlam, x->stagger)) != hipSuccess) return e;
+  if ((e = hipStreamWaitEvent(x->s, x->stagger, 0)) != hipSuccess) return e;
+  if ((e = run_group<T, ST>(a, nb0, a.nb - nb0, x->s, F, R, D, Mp, SLp, dlam, nullptr)) != hipSuccess) return e;
+  if ((e = hipEventRecord(x->join, x->s)) != hipSuccess) return e;
+  return hipStreamWaitEvent(a.stream, x->join, 0);
 }
 
 }  // namespace
