@@ -251,11 +251,19 @@ LOCA_DEV int xcd_logical(int L, int total) {
 
 // WGM x WGN waves of (256 / WGM) x (256 / WGN) columns each: 2 x 4 waves (two per SIMD)
 // or 2 x 2 waves of 128 x 128 (one per SIMD, a third fewer LDS reads per MFMA).
+//
+// Cross statistic in the same launch (Yhl != nullptr): a diagonal tile needs one panel
+// only, so its second ring panel carries the split target rows Yhl = [Y_hi | Y_lo | 0]
+// (n x w2p bf16 per block, w2p = 2k rounded up to 8 <= 64) instead of a second copy of
+// its panel, and its two waves that lie below the diagonal (no Gram output) form
+// Kraw = X_I^T [Y_hi | Y_lo] for the panel's 256 columns, 128 each.
 template <int WGM, int WGN>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
                                                                 int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
                                                                 int64_t s_bstride, double* __restrict__ diag_part,
-                                                                const uint16_t* __restrict__ zero16, int64_t b0) {
+                                                                const uint16_t* __restrict__ zero16, int64_t b0,
+                                                                const uint16_t* __restrict__ Yhl_all, int64_t w2,
+                                                                int64_t w2p, float* __restrict__ Kraw_all) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -284,8 +292,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int wi = wid / WGN, wj = wid % WGN;
   const bool active = !(diag && (wj + 1) * WN <= wi * WM);
+  const bool fuse = diag && Yhl_all != nullptr;            // this tile also forms the cross statistic
+  const bool cross = fuse && !active && WGM == 2 && wj < 2;  // ... in this wave
+  const uint16_t* Yhl = fuse ? Yhl_all + b * n * w2p : zero16;
   const int64_t cI = (int64_t)I * BM, cJ = (int64_t)J * BM;
   const int nk = (int)((n + kBK - 1) / kBK);
+  // fragment sources: Gram waves of a diagonal tile read both operands from the first
+  // panel; cross waves take rows 128 wj.. of the panel and the split targets
+  const int arow0 = cross ? 128 * wj : wi * WM;
+  const int bcol0 = cross ? 0 : wj * WN;
+  const int boff = (diag && !cross) ? 0 : TILE_ELEMS;
 
   // per-thread source chunks: copy q of wave w fills LDS chunks (NQ w + q) * 64 + lane
   int lrow[NQ], lcol[NQ];
@@ -300,8 +316,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
     const int pnl = j / NQ, q = j % NQ;
     const int64_t t = (int64_t)kt * kBK + lrow[q], col = (pnl == 0 ? cI : cJ) + lcol[q];
     // both addresses are formed and one selected, without a branch
-    const uint64_t in_x = (uint64_t)(uintptr_t)X + 2 * (uint64_t)(t * ldx + col);
-    const uint64_t src = (t < n && col < d) ? in_x : (uint64_t)(uintptr_t)zero16;
+    const bool ysrc = fuse && pnl == 1;
+    const uint64_t in_x = ysrc ? (uint64_t)(uintptr_t)Yhl + 2 * (uint64_t)(t * w2p + lcol[q])
+                               : (uint64_t)(uintptr_t)X + 2 * (uint64_t)(t * ldx + col);
+    const bool ok = t < n && (ysrc ? lcol[q] < w2p : col < d);
+    const uint64_t src = ok ? in_x : (uint64_t)(uintptr_t)zero16;
     const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (NQ * wid + q) * 1024;
     lds_dma16((const void*)(uintptr_t)src, __builtin_amdgcn_readfirstlane(dst));
   };
@@ -327,9 +346,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN];
   auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
 #pragma unroll
-    for (int q = 0; q < NBN; ++q) fb[q] = frag32_tr_swz(buf + TILE_ELEMS, wj * WN + 32 * q, ks, lane);
+    for (int q = 0; q < NBN; ++q) fb[q] = frag32_tr_swz(buf + boff, bcol0 + 32 * q, ks, lane);
 #pragma unroll
-    for (int m = 0; m < NBM; ++m) fa[m] = frag32_tr_swz(buf, wi * WM + 32 * m, ks, lane);
+    for (int m = 0; m < NBM; ++m) fa[m] = frag32_tr_swz(buf, arow0 + 32 * m, ks, lane);
   };
   auto mma_row = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN], int m) {
 #pragma unroll
@@ -391,6 +410,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
             S[row * d + col] = old[r] + acc[m][q][r];
             if (diag && row == col) dsum += (double)acc[m][q][r];
           }
+        }
+      }
+  }
+  if (cross) {  // Kraw rows cI + 128 wj + .., columns < w2 (row stride w2)
+    float* Kraw = Kraw_all + b * d * w2;
+#pragma unroll
+    for (int m = 0; m < NBM; ++m)
+#pragma unroll
+      for (int q = 0; q < NBN; ++q) {
+        const int64_t col = 32 * q + mfma32_col(lane);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = cI + arow0 + 32 * m + mfma32_row(lane, r);
+          if (row < d && col < w2) Kraw[row * w2 + col] = acc[m][q][r];
         }
       }
   }
@@ -619,13 +652,30 @@ __global__ void k_zero_bytes(uint32_t* p, int cnt) {
   if ((int)threadIdx.x < cnt) p[threadIdx.x] = 0u;
 }
 
+// Yhl[b][t] = [bf16(y) | bf16(y - bf16(y)) | 0] (w2p columns) from the float targets, and
+// the 256 zero bytes at the head of the workspace.
+__global__ void k_split_y(int64_t n, int64_t k, int64_t w2p, const float* __restrict__ Yall, int64_t y_bstride,
+                          uint16_t* __restrict__ Yhl, uint32_t* __restrict__ zero_area) {
+  const int64_t b = blockIdx.y;
+  if (b == 0 && blockIdx.x == 0 && threadIdx.x < 64) zero_area[threadIdx.x] = 0u;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n * w2p) return;
+  const int64_t t = e / w2p, c = e % w2p;
+  uint16_t v = 0;
+  if (c < 2 * k) {
+    const float y = Yall[b * y_bstride + t * k + (c < k ? c : c - k)];
+    const uint16_t hi = f32_to_bf16(y);
+    v = c < k ? hi : f32_to_bf16(y - bf16_to_f32(hi));
+  }
+  Yhl[b * n * w2p + e] = v;
+}
+
 size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc) {
-  (void)n;
   const int64_t T = acc == LOCA_F64 ? (d + kBM64 - 1) / kBM64 : (d + 127) / 128;
   const int64_t Tmax = (d + kBM64 - 1) / kBM64;  // generous: covers every tile size used
   size_t s = 256 + align256(sizeof(double) * nb * (T > Tmax ? T : Tmax));  // zeros + tile partials
   if (acc == LOCA_F64) s += align256(sizeof(double) * nb * d * k);
-  else s += align256(sizeof(float) * nb * d * 2 * k);
+  else s += align256(sizeof(float) * nb * d * 2 * k) + align256(sizeof(uint16_t) * nb * n * ((2 * k + 7) / 8 * 8));
   return s;
 }
 
@@ -650,30 +700,31 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     return hipGetLastError();
   }
   float* Kraw = (float*)p;
+  uint16_t* Yhl = (uint16_t*)(p + align256(sizeof(float) * a.nb * a.d * 2 * a.k));
   const uint16_t* X = (const uint16_t*)a.x;
   // Tile size: 256 x 256 when the matrix is wide enough to fill the GPU with such tiles.
   const bool big = a.d >= 1024;
   const int BM = big ? 256 : 128;
   const int T = (int)((a.d + BM - 1) / BM);
   dim3 grid((unsigned)(T * (T + 1) / 2), (unsigned)a.nb);
+  const int64_t w2 = 2 * a.k, w2p = (w2 + 7) / 8 * 8;
+  const bool fused = big && (a.d % 8) == 0 && w2p <= 64;
   if (big && (a.d % 8) == 0) {
-    k_zero_bytes<<<1, 64, 0, a.stream>>>((uint32_t*)a.ws, 64);
+    if (fused) {
+      dim3 gy((unsigned)((a.n * w2p + 255) / 256), (unsigned)a.nb);
+      k_split_y<<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
+    } else {
+      k_zero_bytes<<<1, 64, 0, a.stream>>>((uint32_t*)a.ws, 64);
+    }
     // one-dimensional grid (the XCD-aware order spans the blocks), in chunks of blocks
     // small enough that the grid stays far below the launch limits
     const int64_t ntile = (int64_t)T * (T + 1) / 2;
     const int64_t chunk = std::max<int64_t>(1, ((int64_t)1 << 22) / ntile);
     for (int64_t b0 = 0; b0 < a.nb; b0 += chunk) {
       const int64_t nbc = std::min<int64_t>(chunk, a.nb - b0);
-#ifndef LOCA_DL_WAVES
-#define LOCA_DL_WAVES 8
-#endif
-#if LOCA_DL_WAVES == 4
-      k_gram_bf16_dl<2, 2><<<dim3((unsigned)(ntile * nbc)), 256, 0, a.stream>>>(
-          a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0);
-#else
       k_gram_bf16_dl<2, 4><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
-          a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0);
-#endif
+          a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, fused ? Yhl : nullptr,
+          w2, w2p, Kraw);
     }
   } else if (big)
     k_gram_bf16<256, 2, 4><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
@@ -684,15 +735,16 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gc((unsigned)((a.d + 255) / 256), (unsigned)a.nb);
-  const int64_t w2 = 2 * a.k;
-  if (w2 <= 32)
-    k_cross_bf16<32><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
-  else if (w2 <= 64)
-    k_cross_bf16<64><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
-  else if (w2 <= 128)
-    k_cross_bf16<128><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
-  else
-    k_cross_bf16<256><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+  if (!fused) {  // the cross statistic in a launch of its own
+    if (w2 <= 32)
+      k_cross_bf16<32><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+    else if (w2 <= 64)
+      k_cross_bf16<64><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+    else if (w2 <= 128)
+      k_cross_bf16<128><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+    else
+      k_cross_bf16<256><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);

@@ -66,6 +66,11 @@ CASES = {
     # d % 8 == 0 and d >= 1024: the direct-to-LDS Gram kernel; ragged against 256-wide tiles and
     # against the 32-token stages (1400 = 43 x 32 + 24), two blocks
     "bf16_d1040_direct": gen.custom_config("t10", blocks=2, d=1040, n=2400, micro=1400, C=4, k=16, r_a=4),
+    # cross statistic inside the Gram launch: widest split target (2k = 64), and a padded one (2k = 10 -> 16)
+    "bf16_d1536_k32_fused": gen.custom_config("t11", blocks=1, d=1536, n=2000, micro=1000, C=5, k=32, r_a=8),
+    "bf16_d1280_k5_fused": gen.custom_config("t12", blocks=2, d=1280, n=1600, micro=800, C=3, k=5, r_a=2),
+    # 2k = 128 > 64: the cross statistic in its own launch beside the direct-load Gram kernel
+    "bf16_d1024_k64": gen.custom_config("t13", blocks=1, d=1024, n=1200, C=3, k=64, r_a=8),
     # fp32 mode with fewer tokens than features (null space amplified by 1/lambda)
     "fp32_n150_d200": gen.custom_config("t3", blocks=2, d=200, n=150, C=2, k=8, r_a=8, mode="fp32",
                                         x_dist="gauss_outlier", n_outlier=3, outlier_scale=20.0, logit_std=2.0),
