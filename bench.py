@@ -26,6 +26,34 @@ BF16_PEAK_TFLOPS = 2516.6    # MI355X dense bf16 MFMA
 FP64_PEAK_TFLOPS = 78.6      # MI355X dense fp64
 HBM_PEAK_GBS = 8000.0
 
+# HBM traffic of the statistics kernel (k_gram_bf16_dl) per launch, from two rocprofv3
+# --pmc passes (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch) of
+#   bench.py --config <cfg> --steps 1 --warmup 0 --no-cpu-baseline,
+# each scaled by the factor the same counter gives for a plain device copy in the same run
+# (the bf16 stack of the inputs, 2 * N * d bytes read and written per block): 1.0 for both.
+# Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h).
+TRAFFIC = {
+    "c3": {"fetch_kib": 3101499.2, "write_kib": 852606.0, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "ddc72e8ad79e5135"},
+}
+
+
+def stats_src_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("k_gram.hip", "loca_common.h"):
+        with open(os.path.join(ROOT, "paper_2608_03020_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_bytes(cfg_name):
+    t = TRAFFIC.get(cfg_name)
+    if t is None or t["src_digest"] != stats_src_digest():
+        return None
+    return 1024.0 * (t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"])
+
+
 WORKLOADS = {
     "c1": "Single block, Qwen2.5-0.5B width: d=896, N=512, C=2, k=8, r_a=8, lambda=1e-2, fp32 mode",
     "c2": "Qwen2.5-1.5B-shaped: 28 blocks, d=1536, N=8192 (4 x 2048), C=4, k=16, r_a=16, lambda=1e-2, bf16 X",
@@ -189,7 +217,7 @@ def main():
                    "tokens": cfg.n, "micro_batch": cfg.micro, "classes": cfg.C, "credit_rank": cfg.k,
                    "adapter_rank": cfg.r_a, "lambdas": list(cfg.lambdas)},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": None,
+                     "frac": achieved / peak, "traffic": traffic_bytes(args.config),
                      "kernel": "loca_accumulate_stats (Gram S += X^T X and cross X^T Y of all blocks, one micro-batch)",
                      "algorithmic_flops_per_launch": f_avg, "avg_launch_ms": t_avg},
     }
