@@ -148,7 +148,10 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
  *               credit_b (ignored when NULL).
  * dev_info : nb * n_lambda int32; 0, or the 1-based index of the first
  *            non-positive pivot (LAPACK potrf convention).
- * Limits: r_prev + k <= 128.
+ * Limits: r_prev + k <= 128, n_lambda <= 8, nb * n_lambda <= 65535, d <= 65535.
+ * Solves of two halves of the blocks run on the caller's stream and on a second
+ * stream the library creates once per device; the call stays ordered on the
+ * caller's stream (it waits for the second).
  * ------------------------------------------------------------------------- */
 loca_status loca_ridge_solve(loca_stream_t stream, int64_t nb, int64_t d, int64_t k, const void* S,
                              const void* K, loca_dtype acc, int64_t s_bstride, int64_t k_bstride,
@@ -170,7 +173,7 @@ loca_status loca_ridge_solve(loca_stream_t stream, int64_t nb, int64_t d, int64_
  * Directions with zero singular value (W has rank < r_a) get zero rows/cols.
  * w_dense_out : optional d x d W_{r_a} (float), stride w_bstride.
  * dev_info : nm int32, 0 (reserved for future conditions).
- * Limits: kp <= 128, r_a <= kp, kp <= d.
+ * Limits: kp <= 64, r_a <= kp, kp <= d.
  * ------------------------------------------------------------------------- */
 loca_status loca_lowrank_truncate(loca_stream_t stream, int64_t nm, int64_t d, int64_t kp,
                                   int64_t r_a, const float* m, int64_t m_bstride, const float* r,
@@ -189,7 +192,7 @@ loca_status loca_lowrank_truncate(loca_stream_t stream, int64_t nm, int64_t d, i
  * b_out : float, matrix (b, l) at b_out + (b * n_lambda + l) * bo_bstride.
  * g_out : optional float r_a x r_a G_l per block (stride r_a * r_a).
  * dev_info : nb * n_lambda int32 (non-positive pivot, 1-based).
- * Limits: r_a <= 128, k <= 128.
+ * Limits: r_a <= 64, k <= 128, n_lambda <= 8.
  * ------------------------------------------------------------------------- */
 loca_status loca_ridge_solve_projected(loca_stream_t stream, int64_t nb, int64_t d, int64_t k,
                                        int64_t r_a, const void* S, const void* K, loca_dtype acc,
