@@ -604,9 +604,13 @@ LOCA_DEV float4 ld4_or_zero(const float* base, int64_t idx, bool ok) {
 }
 LOCA_DEV float4 ld4_or_zero_ro(const float* __restrict__ base, int64_t idx, bool ok) { return ld4_or_zero(base, idx, ok); }
 
+// Jobs past the nF tiles of F are right-hand-side jobs: the same product with Qn and the
+// output taken from R (d x m per matrix, m % 4 == 0): the 256-row block u of the trailing
+// region (kX6Trail), or the panel rows (kX6Strip, kX6Row), all m columns.
 template <int MODE>
 __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t kw, int64_t off,
-                                                  float* __restrict__ Fall) {
+                                                  float* __restrict__ Fall, float* __restrict__ Rall, int64_t m,
+                                                  int nF) {
   constexpr int BR = MODE == kX6Trail ? 256 : 128;  // output rows per tile
   constexpr int BC = 256, WGN = 4, WM = BR / 2, WN = BC / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int LD = kX6LD, PLANE = kX6BK * LD;
@@ -614,31 +618,40 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
   __shared__ __attribute__((aligned(16))) uint16_t sm[2][6 * PLANE];  // [buffer][operand * 3 + part]
   const int64_t mi = blockIdx.y;
   float* F = Fall + mi * d * d;
+  float* R = Rall + mi * d * m;
+  const bool rhs = (int)blockIdx.x >= nF;
+  const int job = rhs ? (int)blockIdx.x - nF : (int)blockIdx.x;
   int64_t orow, ocol, pcol;
-  bool diag;
+  bool diag = false;
   if (MODE == kX6Trail) {
-    const int T2 = (int)((d - off + BC - 1) / BC);
-    int I, J;
-    upper_tile_c((int)blockIdx.x, T2, I, J);
-    diag = I == J;
-    orow = off + (int64_t)I * BC;
-    ocol = off + (int64_t)J * BC;
+    if (rhs) {
+      orow = off + (int64_t)job * BC;
+      ocol = 0;
+    } else {
+      const int T2 = (int)((d - off + BC - 1) / BC);
+      int I, J;
+      upper_tile_c(job, T2, I, J);
+      diag = I == J;
+      orow = off + (int64_t)I * BC;
+      ocol = off + (int64_t)J * BC;
+    }
     pcol = orow;
   } else if (MODE == kX6Strip) {
-    diag = blockIdx.x == 0;
+    diag = !rhs && job == 0;
     orow = off;
-    ocol = off + (int64_t)blockIdx.x * BC;
+    ocol = rhs ? 0 : off + (int64_t)job * BC;
     pcol = orow;
   } else {  // kX6Row: K rows and output rows [k0, k0 + 128), Pn = the diagonal block
-    diag = false;
     orow = k0;
-    ocol = k0 + 128 + (int64_t)blockIdx.x * BC;
+    ocol = rhs ? 0 : k0 + 128 + (int64_t)job * BC;
     pcol = k0;
   }
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, wi = wid / WGN, wj = wid % WGN;
   const bool active = !(diag && (wj + 1) * WN <= wi * WM);
   const float* gP = F + k0 * d + pcol;
-  const float* gQ = F + k0 * d + ocol;
+  float* Out = rhs ? R : F;                          // Qn and the output
+  const int64_t ldq = rhs ? m : d, qend = rhs ? m : d;
+  const float* gQ = Out + k0 * ldq + ocol;
   const int64_t pend = MODE == kX6Row ? k0 + 128 : d;  // columns of Pn that exist: < pend
 
   float4 rp[QP], rq[QQ];
@@ -651,7 +664,7 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
 #pragma unroll
     for (int q = 0; q < QQ; ++q) {
       const int c = tid + 512 * q, kk = c >> 6, c4 = 4 * (c & 63);
-      rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * d + c4, kc0 + kk < kw && ocol + c4 < d);
+      rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * ldq + c4, kc0 + kk < kw && ocol + c4 < qend);
     }
   };
   auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
@@ -714,7 +727,8 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
     __syncthreads();
   }
   if (!active) return;
-  const int64_t rend = MODE == kX6Row ? k0 + 128 : (MODE == kX6Strip ? off + 128 : d);
+  int64_t rend = MODE == kX6Row ? k0 + 128 : (MODE == kX6Strip ? off + 128 : d);
+  if (rend > d) rend = d;  // a ragged last panel
 #pragma unroll
   for (int a = 0; a < NBM; ++a)
 #pragma unroll
@@ -726,14 +740,14 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = rb + mfma32_row(lane, r);
-          old[r] = ld_or_zero(F, row * d + col, row < rend && col < d && col >= row);
+          old[r] = ld_or_zero(Out, row * ldq + col, row < rend && col < qend && (rhs || col >= row));
         }
       }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = rb + mfma32_row(lane, r);
-        if (row < rend && col < d && col >= row)
-          F[row * d + col] = MODE == kX6Row ? acc[a][b][r] : old[r] - acc[a][b][r];
+        if (row < rend && col < qend && (rhs || col >= row))
+          Out[row * ldq + col] = MODE == kX6Row ? acc[a][b][r] : old[r] - acc[a][b][r];
       }
     }
 }
@@ -1024,6 +1038,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
   // update of its own rows), then is factored (diagonal block) and solved (row panel).
   constexpr int P = Mf<T>::P, kSuper = 4;
   const bool x6 = sizeof(T) == 4 && d % 4 == 0;
+  const bool x6r = x6 && m % 4 == 0 && m <= 256;  // right-hand sides inside the same launches
   const int64_t TM = (m + P - 1) / P;
   for (int64_t P0 = 0; P0 < d; P0 += kSuper * P) {
     const int64_t P1 = (d - P0) < kSuper * P ? d : P0 + kSuper * P;
@@ -1034,10 +1049,12 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       if (pp > P0) {
         const int64_t T2 = (d - pp + P - 1) / P;
         if (x6) {
-          k_panel_x6<kX6Strip><<<dim3((unsigned)((d - pp + 255) / 256), (unsigned)nm), 512, 0, st>>>(
-              d, P0, pp - P0, pp, (float*)F);
-          k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
-              d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
+          const int nF = (int)((d - pp + 255) / 256);
+          k_panel_x6<kX6Strip><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
+              d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF);
+          if (!x6r)
+            k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
+                d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
         } else {
           k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, st>>>(
               d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
@@ -1047,10 +1064,12 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       else k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
       if (after_diag && pp == 0) hipEventRecord(after_diag, st);
       if (x6 && nrem > 0) {
-        k_panel_x6<kX6Row><<<dim3((unsigned)((nrem + 255) / 256), (unsigned)nm), 512, 0, st>>>(d, pp, pw, 0,
-                                                                                                     (float*)F);
-        k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
-                                                                                             (int)nchF, F, R);
+        const int nF = (int)((nrem + 255) / 256);
+        k_panel_x6<kX6Row><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
+            d, pp, pw, 0, (float*)F, (float*)R, m, nF);
+        if (!x6r)
+          k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
+                                                                                               (int)nchF, F, R);
       } else {
         k_panel_product<T, kRowPanel><<<dim3((unsigned)(nchF + TM), (unsigned)nm), kT, 0, st>>>(
             d, m, pp, 0, 0, 0, 0, 0, F, R);
@@ -1060,10 +1079,12 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       const int64_t T2 = (d - P1 + P - 1) / P, nU = T2 * (T2 + 1) / 2;
       if (x6) {
         const int64_t T6 = (d - P1 + 255) / 256;
-        k_panel_x6<kX6Trail><<<dim3((unsigned)(T6 * (T6 + 1) / 2), (unsigned)nm), 512, 0, st>>>(
-            d, P0, P1 - P0, P1, (float*)F);
-        k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
-            d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
+        const int nF = (int)(T6 * (T6 + 1) / 2);
+        k_panel_x6<kX6Trail><<<dim3((unsigned)(nF + (x6r ? T6 : 0)), (unsigned)nm), 512, 0, st>>>(
+            d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF);
+        if (!x6r)
+          k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
+              d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
       } else {
         k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, st>>>(
             d, m, 0, P0, P1 - P0, P1, 0, 0, F, R);
@@ -1117,14 +1138,21 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
 }
 
 
-// Second stream and events per device, made on first use.  The blocks of a call are
-// split in two halves on two streams, the second started once the first has factored
-// its first diagonal block: the diagonal-block and back-substitution launches of one
-// half (a workgroup per matrix, latency bound) then run beside the matrix-core
-// updates of the other half instead of leaving most of the GPU idle.
+// Extra streams and events per device, made on first use.  The blocks of a call are
+// split into up to kGroups groups on the caller's stream and kGroups - 1 internal
+// streams, group g started once group g - 1 has factored its first diagonal block:
+// the latency-bound launches of one group (diagonal blocks, strips, back
+// substitution: few workgroups each) then run beside the matrix-core updates of the
+// others instead of leaving most of the GPU idle.
+#ifndef LOCA_SOLVE_GROUPS
+#define LOCA_SOLVE_GROUPS 2
+#endif
+constexpr int kGroups = LOCA_SOLVE_GROUPS;
 struct Aux {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, stagger = nullptr, join = nullptr;
+  hipStream_t s[kGroups] = {};
+  hipEvent_t fork = nullptr;
+  hipEvent_t stagger[kGroups] = {};
+  hipEvent_t join[kGroups] = {};
 };
 Aux g_aux[64];
 
@@ -1134,11 +1162,13 @@ hipError_t get_aux(Aux** out) {
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   Aux& x = g_aux[dev];
-  if (!x.s) {
+  if (!x.fork) {
+    for (int g = 1; g < kGroups; ++g) {
+      if ((e = hipEventCreateWithFlags(&x.stagger[g], hipEventDisableTiming)) != hipSuccess) return e;
+      if ((e = hipEventCreateWithFlags(&x.join[g], hipEventDisableTiming)) != hipSuccess) return e;
+      if ((e = hipStreamCreateWithFlags(&x.s[g], hipStreamNonBlocking)) != hipSuccess) return e;
+    }
     if ((e = hipEventCreateWithFlags(&x.fork, hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&x.stagger, hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&x.join, hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = hipStreamCreateWithFlags(&x.s, hipStreamNonBlocking)) != hipSuccess) return e;
   }
   *out = &x;
   return hipSuccess;
@@ -1161,17 +1191,26 @@ hipError_t run_solve(const SolveArgs& a) {
   k_fill_zero_i32<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.nb < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr);
+  const int G = (int)(a.nb < kGroups ? a.nb : kGroups);
+  if (G < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr);
   Aux* x = nullptr;
   if ((e = get_aux(&x)) != hipSuccess) return e;
-  const int64_t nb0 = a.nb / 2;
   if ((e = hipEventRecord(x->fork, a.stream)) != hipSuccess) return e;
-  if ((e = hipStreamWaitEvent(x->s, x->fork, 0)) != hipSuccess) return e;
-  if ((e = run_group<T, ST>(a, 0, nb0, a.stream, F, R, D, Mp, SLp, dlam, x->stagger)) != hipSuccess) return e;
-  if ((e = hipStreamWaitEvent(x->s, x->stagger, 0)) != hipSuccess) return e;
-  if ((e = run_group<T, ST>(a, nb0, a.nb - nb0, x->s, F, R, D, Mp, SLp, dlam, nullptr)) != hipSuccess) return e;
-  if ((e = hipEventRecord(x->join, x->s)) != hipSuccess) return e;
-  return hipStreamWaitEvent(a.stream, x->join, 0);
+  for (int g = 0; g < G; ++g) {
+    const int64_t b0 = a.nb * g / G, b1 = a.nb * (g + 1) / G;
+    hipStream_t st = g == 0 ? a.stream : x->s[g];
+    if (g > 0) {
+      if ((e = hipStreamWaitEvent(st, x->fork, 0)) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(st, x->stagger[g], 0)) != hipSuccess) return e;
+    }
+    hipEvent_t after = g + 1 < G ? x->stagger[g + 1] : nullptr;
+    if ((e = run_group<T, ST>(a, b0, b1 - b0, st, F, R, D, Mp, SLp, dlam, after)) != hipSuccess) return e;
+  }
+  for (int g = 1; g < G; ++g) {
+    if ((e = hipEventRecord(x->join[g], x->s[g])) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(a.stream, x->join[g], 0)) != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace
