@@ -94,6 +94,25 @@ def make_inputs(cfg, nb, device="cuda"):
     return x_all, z, y, torch.stack(A), torch.stack(B)
 
 
+def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None):
+    """One step of the whole path over every block: per micro-batch the head error
+    and credit coordinates, then the statistics (bracketed by the events of
+    `record[m]` when given); then the ridge solves and the truncation."""
+    from paper_2608_03020_amd import loca
+    step.reset()
+    for m in range(cfg.n_micro):
+        lo, hi = cfg.micro_rows(m)
+        xm = x_all[:, lo:hi]
+        yv = step.Y[:, :hi - lo]
+        loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, nb=nb)
+        if record is not None:
+            record[m][0].record(stream)
+        loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws)
+        if record is not None:
+            record[m][1].record(stream)
+    step.solve(B)
+
+
 def cpu_baseline(cfg, n_sample):
     """The oracle as it stands, on a bounded sample of block 0 of the workload:
     the per-token stages (head error, feedback, target, S, dense Z, K) on
@@ -164,18 +183,7 @@ def main():
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps * n_mb)]
 
     def one_step(record=None):
-        step.reset()
-        for m in range(n_mb):
-            lo, hi = cfg.micro_rows(m)
-            xm = x_all[:, lo:hi]
-            yv = step.Y[:, :hi - lo]
-            loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, nb=nb)
-            if record is not None:
-                record[m][0].record(stream)
-            loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws)
-            if record is not None:
-                record[m][1].record(stream)
-        step.solve(B)
+        run_step(step, cfg, nb, x_all, z, y, A, B, stream, record)
 
     for _ in range(args.warmup):
         one_step()
