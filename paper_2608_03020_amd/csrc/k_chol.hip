@@ -299,10 +299,12 @@ LOCA_DEV void wave_lds_sync() {
 
 // One wave factors the 32 x 32 block B (upper part used) as U^T U, writes U over B (zero
 // below the diagonal) and X = U^{-1} to Xo.  Lane c < 32 holds column c (rows 0..31);
-// lanes 32..63 mirror lanes 0..31 and write nothing.  Step j publishes row j of the
-// current matrix through the wave's LDS row `rb` (32 floats); the inverse is built
-// bottom-up from rows of U read back from B.  The first non-positive pivot among the
-// first `valid` is reported (1-based, offset base).
+// lanes 32..63 mirror lanes 0..31 and write nothing.  Rows of the current matrix are
+// published through two LDS rows rb[0..63] (row j in rb + 32 (j & 1)): step j first
+// applies its update to row j + 1 and publishes it, then finishes the other rows while
+// the row travels.  The inverse is built bottom-up from rows of U read back from B.
+// Square root and reciprocal are the hardware ones (about 1 ulp).  The first
+// non-positive pivot among the first `valid` is reported (1-based, offset base).
 LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, float* rb, int lane, int valid, int64_t base,
                          int32_t* info) {
   const int c = lane & 31;
@@ -310,25 +312,30 @@ LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, float* rb, int la
   float a[32];
 #pragma unroll
   for (int r = 0; r < 32; ++r) a[r] = B[r * ld + c];
+  if (wr) rb[c] = a[0];
+  wave_lds_sync();
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
-    if (wr) rb[c] = a[j];  // row j: B[j][c]
-    wave_lds_sync();
+    const float* row = rb + 32 * (j & 1);
     float rr[32];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const float4 t = *(const float4*)(rb + 4 * v);
+    for (int v = j >> 2; v < 8; ++v) {
+      const float4 t = *(const float4*)(row + 4 * v);
       rr[4 * v] = t.x; rr[4 * v + 1] = t.y; rr[4 * v + 2] = t.z; rr[4 * v + 3] = t.w;
     }
     const float piv = rr[j];
     if (!(piv > 0.f) && j < valid && lane == 0) atomicCAS(info, 0, (int32_t)(base + j + 1));
-    const float ujj = sqrtf(piv);
-    const float inv = 1.0f / ujj;
+    const float ujj = __builtin_amdgcn_sqrtf(piv);
+    const float inv = __builtin_amdgcn_rcpf(ujj);
     const float uc = c > j ? a[j] * inv : (c == j ? ujj : 0.f);  // U[j][c]
     a[j] = uc;
+    if (j + 1 < 32) {
+      a[j + 1] -= (rr[j + 1] * inv) * uc;
+      if (wr) rb[32 * ((j + 1) & 1) + c] = a[j + 1];  // row j + 1, final for this step
 #pragma unroll
-    for (int i = j + 1; i < 32; ++i) a[i] -= (rr[i] * inv) * uc;
-    wave_lds_sync();  // every lane has read rb before the next row is written
+      for (int i = j + 2; i < 32; ++i) a[i] -= (rr[i] * inv) * uc;
+      wave_lds_sync();
+    }
   }
   if (wr) {
 #pragma unroll
@@ -340,14 +347,15 @@ LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, float* rb, int la
   for (int i = 31; i >= 0; --i) {
     float ur[32];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) {
+    for (int v = i >> 2; v < 8; ++v) {
       const float4 t = *(const float4*)(B + i * ld + 4 * v);
       ur[4 * v] = t.x; ur[4 * v + 1] = t.y; ur[4 * v + 2] = t.z; ur[4 * v + 3] = t.w;
     }
-    float part = 0.f;
+    float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = i + 1; k < 32; ++k) part += ur[k] * x[k];
-    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - part) / ur[i] : 0.f;
+    for (int k = i + 1; k < 32; ++k) part[k & 3] += ur[k] * x[k];
+    const float tot = (part[0] + part[1]) + (part[2] + part[3]);
+    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - tot) * __builtin_amdgcn_rcpf(ur[i]) : 0.f;
   }
   if (wr) {
 #pragma unroll
@@ -368,7 +376,7 @@ __global__ __launch_bounds__(kT) void k_diag_f32(int64_t d, int64_t p, float* __
   __shared__ __attribute__((aligned(16))) float sA[P * LD];
   __shared__ __attribute__((aligned(16))) float sX[P * LD];
   __shared__ __attribute__((aligned(16))) float sT[3][32 * 36];
-  __shared__ __attribute__((aligned(16))) float su[32];  // row buffer of the factoring wave
+  __shared__ __attribute__((aligned(16))) float su[64];  // row buffers of the factoring wave
   const int64_t mi = blockIdx.x;
   float* F = Fall + mi * d * d;
   const float* A0 = F + p * d + p;
