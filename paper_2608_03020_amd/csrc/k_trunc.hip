@@ -19,28 +19,34 @@ namespace {
 constexpr int kT = 256;
 constexpr int kMaxKp = 64;
 
-// Gm = M^T M and Gb = R R^T, fp64.  blockIdx.x = matrix, blockIdx.y = 0 (M) / 1 (R).
+// Partial Gm = M^T M and Gb = R R^T (fp64) over the row range of blockIdx.z (of nsplit
+// equal ranges of 32-row multiples); blockIdx.x = matrix, blockIdx.y = 0 (M) / 1 (R).
+// The partials are summed in a fixed order by k_trunc_core.
 __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const float* __restrict__ M,
                                                     int64_t m_bstride, const float* __restrict__ R,
-                                                    int64_t r_bstride, int64_t r_group, double* __restrict__ Gm,
-                                                    double* __restrict__ Gb) {
+                                                    int64_t r_bstride, int64_t r_group, int nsplit,
+                                                    double* __restrict__ Gpart) {
   constexpr int kRows = 32;
   __shared__ double sX[kRows][kMaxKp + 1];
   const int64_t mi = blockIdx.x;
   const bool isR = blockIdx.y == 1;
+  const int64_t chunk = ((d + nsplit - 1) / nsplit + kRows - 1) / kRows * kRows;
+  const int64_t ib = (int64_t)blockIdx.z * chunk, ie = ib + chunk < d ? ib + chunk : d;
   const float* Mm = M + mi * m_bstride;
   const float* Rm = R + (mi / r_group) * r_bstride;
   const int npair = (int)(kp * kp);
   double acc[(kMaxKp * kMaxKp) / kT];
 #pragma unroll
   for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) acc[q] = 0.0;
-  for (int64_t i0 = 0; i0 < d; i0 += kRows) {
+  for (int64_t i0 = ib; i0 < ie; i0 += kRows) {
     __syncthreads();
     for (int e = threadIdx.x; e < kRows * kMaxKp; e += kT) {
-      const int r = e / kMaxKp, c = e % kMaxKp;
+      int r, c;
+      if (isR) { c = e / kRows; r = e % kRows; }  // R rows are contiguous along i
+      else { r = e / kMaxKp; c = e % kMaxKp; }
       const int64_t i = i0 + r;
       double v = 0.0;
-      if (i < d && c < kp) v = isR ? (double)Rm[c * d + i] : (double)Mm[i * kp + c];
+      if (i < ie && c < kp) v = isR ? (double)Rm[c * d + i] : (double)Mm[i * kp + c];
       sX[r][c] = v;
     }
     __syncthreads();
@@ -55,7 +61,7 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
       }
     }
   }
-  double* G = (isR ? Gb : Gm) + mi * kp * kp;
+  double* G = Gpart + ((mi * 2 + (isR ? 1 : 0)) * nsplit + blockIdx.z) * kp * kp;
 #pragma unroll
   for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) {
     const int e = threadIdx.x + kT * q;
@@ -66,14 +72,16 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
 // Cyclic Jacobi eigendecomposition of the symmetric n x n matrix A (LDS, row stride ld),
 // eigenvectors accumulated into V (columns).  Round-robin pair ordering: each round
 // rotates n/2 disjoint pairs.  n must be even (callers pad with a zero row/column).
+// Run by the kTC threads of one workgroup.
+constexpr int kTC = kT;
 LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* pairs, double* red) {
   const int tid = threadIdx.x;
-  for (int e = tid; e < n * ld; e += kT) V[e] = ((e / ld) == (e % ld)) ? 1.0 : 0.0;
+  for (int e = tid; e < n * ld; e += kTC) V[e] = ((e / ld) == (e % ld)) ? 1.0 : 0.0;
   __syncthreads();
   for (int sweep = 0; sweep < 40; ++sweep) {
     // convergence test: off-diagonal mass vs total
     double off = 0.0, tot = 0.0;
-    for (int e = tid; e < n * n; e += kT) {
+    for (int e = tid; e < n * n; e += kTC) {
       const int i = e / n, j = e % n;
       const double v = A[i * ld + j];
       tot += v * v;
@@ -106,7 +114,7 @@ LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* p
       }
       __syncthreads();
       // A <- A J (columns), V <- V J
-      for (int e = tid; e < (n / 2) * n; e += kT) {
+      for (int e = tid; e < (n / 2) * n; e += kTC) {
         const int pr = e / n, i = e % n;
         const int p = pairs[2 * pr], q = pairs[2 * pr + 1];
         const double c = cs[2 * pr], s = cs[2 * pr + 1];
@@ -119,7 +127,7 @@ LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* p
       }
       __syncthreads();
       // A <- J^T A (rows)
-      for (int e = tid; e < (n / 2) * n; e += kT) {
+      for (int e = tid; e < (n / 2) * n; e += kTC) {
         const int pr = e / n, j = e % n;
         const int p = pairs[2 * pr], q = pairs[2 * pr + 1];
         const double c = cs[2 * pr], s = cs[2 * pr + 1];
@@ -133,14 +141,15 @@ LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* p
 }
 
 // One workgroup per matrix: eigendecompositions and the small factors Ca, Cb.
-__global__ __launch_bounds__(kT) void k_trunc_core(int64_t kp, int64_t r_a, const double* __restrict__ Gm_all,
-                                                   const double* __restrict__ Gb_all, double* __restrict__ Ca_all,
-                                                   double* __restrict__ Cb_all, float* __restrict__ sigma_out,
-                                                   int64_t sigma_bstride) {
+__global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, const double* __restrict__ Gpart,
+                                                    int nsplit, double* __restrict__ Ca_all,
+                                                    double* __restrict__ Cb_all, float* __restrict__ sigma_out,
+                                                    int64_t sigma_bstride) {
   constexpr int LD = kMaxKp + 1;
   __shared__ double sA[kMaxKp * LD];
   __shared__ double sV[kMaxKp * LD];
   __shared__ double sT[kMaxKp * LD];
+  __shared__ double sG[kMaxKp * LD];  // Gm
   __shared__ double sH[kMaxKp], sHi[kMaxKp], sEig[kMaxKp];
   __shared__ int sOrd[kMaxKp];
   __shared__ double cs[kMaxKp];
@@ -149,12 +158,19 @@ __global__ __launch_bounds__(kT) void k_trunc_core(int64_t kp, int64_t r_a, cons
   const int64_t mi = blockIdx.x;
   const int tid = threadIdx.x;
   const int n = (int)kp + ((int)kp & 1);  // even size for the tournament ordering
-  const double* Gm = Gm_all + mi * kp * kp;
-  const double* Gb = Gb_all + mi * kp * kp;
-  // 1. Gb = Vb diag(lb) Vb^T
-  for (int e = tid; e < n * LD; e += kT) {
+  const double* GmP = Gpart + (mi * 2) * nsplit * kp * kp;
+  const double* GbP = Gpart + (mi * 2 + 1) * nsplit * kp * kp;
+  // 1. Gb = Vb diag(lb) Vb^T; Gm (summed over the row ranges, in order) waits in sT
+  for (int e = tid; e < n * LD; e += kTC) {
     const int i = e / LD, j = e % LD;
-    sA[e] = (i < kp && j < kp) ? Gb[i * kp + j] : 0.0;
+    double gb = 0.0, gm = 0.0;
+    if (i < kp && j < kp)
+      for (int z = 0; z < nsplit; ++z) {
+        gb += GbP[z * kp * kp + i * kp + j];
+        gm += GmP[z * kp * kp + i * kp + j];
+      }
+    sA[e] = gb;
+    sG[e] = gm;
   }
   __syncthreads();
   jacobi_eig(sA, sV, n, LD, cs, pairs, red);
@@ -165,24 +181,24 @@ __global__ __launch_bounds__(kT) void k_trunc_core(int64_t kp, int64_t r_a, cons
     red[12] = lmax;
   }
   __syncthreads();
-  for (int j = tid; j < kp; j += kT) {
+  for (int j = tid; j < kp; j += kTC) {
     const double lb = sA[j * LD + j];
     const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
     sH[j] = keep ? sqrt(lb) : 0.0;
     sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
   }
   // keep Vb in sT
-  for (int e = tid; e < n * LD; e += kT) sT[e] = sV[e];
+  for (int e = tid; e < n * LD; e += kTC) sT[e] = sV[e];
   __syncthreads();
   // 2. P^T P = H Vb^T Gm Vb H: first sA = Gm Vb
-  for (int e = tid; e < (int)(kp * kp); e += kT) {
+  for (int e = tid; e < (int)(kp * kp); e += kTC) {
     const int i = e / (int)kp, j = e % (int)kp;
     double s = 0.0;
-    for (int c = 0; c < kp; ++c) s += Gm[i * kp + c] * sT[c * LD + j];
+    for (int c = 0; c < kp; ++c) s += sG[i * LD + c] * sT[c * LD + j];
     sV[i * LD + j] = s;
   }
   __syncthreads();
-  for (int e = tid; e < n * n; e += kT) {
+  for (int e = tid; e < n * n; e += kTC) {
     const int i = e / n, j = e % n;
     double s = 0.0;
     if (i < kp && j < kp) {
@@ -193,7 +209,7 @@ __global__ __launch_bounds__(kT) void k_trunc_core(int64_t kp, int64_t r_a, cons
   }
   __syncthreads();
   // symmetrise against rounding
-  for (int e = tid; e < n * n; e += kT) {
+  for (int e = tid; e < n * n; e += kTC) {
     const int i = e / n, j = e % n;
     if (i < j) {
       const double v = 0.5 * (sA[i * LD + j] + sA[j * LD + i]);
@@ -216,11 +232,11 @@ __global__ __launch_bounds__(kT) void k_trunc_core(int64_t kp, int64_t r_a, cons
   }
   __syncthreads();
   const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
-  for (int j = tid; j < kp; j += kT) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
+  for (int j = tid; j < kp; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
   // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
-  for (int e = tid; e < (int)(r_a * kp); e += kT) {
+  for (int e = tid; e < (int)(r_a * kp); e += kTC) {
     const int a = e / (int)kp, c = e % (int)kp;
     const int col = sOrd[a];
     const double sa = sqrt(fmax(sEig[col], 0.0));
@@ -254,11 +270,18 @@ __global__ __launch_bounds__(kT) void k_trunc_apply(int64_t d, int64_t kp, int64
   const float* Mi = M + mi * m_bstride + i * kp;
   const float* Rm = R + (mi / r_group) * r_bstride;
   float mrow[kMaxKp], rcol[kMaxKp];
+  if ((kp & 3) == 0 && (m_bstride & 3) == 0 && (((uintptr_t)M) & 15) == 0) {  // rows of M as float4
 #pragma unroll
-  for (int c = 0; c < kMaxKp; ++c) {
-    mrow[c] = (c < kp) ? Mi[c] : 0.f;
-    rcol[c] = (c < kp) ? Rm[c * d + i] : 0.f;
+    for (int c = 0; c < kMaxKp; c += 4) {
+      const float4 t = c < kp ? *(const float4*)(Mi + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      mrow[c] = t.x; mrow[c + 1] = t.y; mrow[c + 2] = t.z; mrow[c + 3] = t.w;
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < kMaxKp; ++c) mrow[c] = (c < kp) ? Mi[c] : 0.f;
   }
+#pragma unroll
+  for (int c = 0; c < kMaxKp; ++c) rcol[c] = (c < kp) ? Rm[c * d + i] : 0.f;
   for (int a = 0; a < r_a; ++a) {
     double sa = 0.0, sb = 0.0;
 #pragma unroll
@@ -306,23 +329,27 @@ hipError_t launch_lowrank_product(hipStream_t s, int64_t nmat, int64_t rows, int
   return hipGetLastError();
 }
 
+int trunc_splits(int64_t d) {
+  const int64_t s = d / 256;
+  return (int)(s < 1 ? 1 : (s > 16 ? 16 : s));
+}
+
 size_t lowrank_truncate_ws(int64_t nm, int64_t d, int64_t kp, int64_t r_a) {
-  (void)d;
-  size_t s = 2 * align256(sizeof(double) * nm * kp * kp);
+  size_t s = align256(sizeof(double) * nm * 2 * trunc_splits(d) * kp * kp);
   s += 2 * align256(sizeof(double) * nm * kp * r_a);
   return s;
 }
 
 hipError_t launch_lowrank_truncate(const TruncArgs& a) {
   char* p = a.ws;
-  double* Gm = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.kp);
-  double* Gb = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.kp);
+  const int ns = trunc_splits(a.d);
+  double* Gpart = (double*)p; p += align256(sizeof(double) * a.nm * 2 * ns * a.kp * a.kp);
   double* Ca = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.r_a);
   double* Cb = (double*)p;
   k_fill_zero<<<(unsigned)((a.nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, a.nm);
-  k_small_grams<<<dim3((unsigned)a.nm, 2), kT, 0, a.stream>>>(a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride,
-                                                               a.r_group, Gm, Gb);
-  k_trunc_core<<<(unsigned)a.nm, kT, 0, a.stream>>>(a.kp, a.r_a, Gm, Gb, Ca, Cb, a.sigma_out, a.sigma_bstride);
+  k_small_grams<<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(a.d, a.kp, a.m, a.m_bstride, a.r,
+                                                                             a.r_bstride, a.r_group, ns, Gpart);
+  k_trunc_core<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.kp, a.r_a, Gpart, ns, Ca, Cb, a.sigma_out, a.sigma_bstride);
   k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm), kT, 0, a.stream>>>(
       a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
       a.b_bstride);
