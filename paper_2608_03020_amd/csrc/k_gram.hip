@@ -236,6 +236,24 @@ constexpr int vmcnt_imm(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 <
 LOCA_DEV void lds_dma16(const void* gptr, uint32_t lds_base) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base) : "m0", "memory");
 }
+// The same copy through the buffer path: `voff` is a byte offset into the buffer of the
+// resource `rsrc` (base, byte range, raw format); offsets at or past the range return zeros.
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+LOCA_DEV void lds_dma16_buf(uint32_t voff, i32x4_t rsrc, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds" ::"v"(voff), "s"(lds_base),
+               "s"(rsrc) : "m0", "memory");
+}
+LOCA_DEV i32x4_t buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  i32x4_t r;
+  r[0] = (int32_t)(uint32_t)(a & 0xffffffffu);
+  r[1] = (int32_t)(uint32_t)((a >> 32) & 0xffffu);  // stride 0
+  r[2] = (int32_t)bytes;
+  r[3] = 0x00020000;  // raw 32-bit data format
+  return r;
+}
+constexpr uint32_t kBufOutside = 0x80000000u;  // past every range used here (< 2^31 bytes)
+
 // Workgroup barrier without a memory fence (the pipeline waits for its own loads explicitly).
 LOCA_DEV void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
 
@@ -257,7 +275,7 @@ LOCA_DEV int xcd_logical(int L, int total) {
 // (n x w2p bf16 per block, w2p = 2k rounded up to 8 <= 64) instead of a second copy of
 // its panel, and its two waves that lie below the diagonal (no Gram output) form
 // Kraw = X_I^T [Y_hi | Y_lo] for the panel's 256 columns, 128 each.
-template <int WGM, int WGN>
+template <int WGM, int WGN, bool BUF>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
                                                                 int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
                                                                 int64_t s_bstride, double* __restrict__ diag_part,
@@ -312,11 +330,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
     lcol[q] = 8 * ((slot & 31) ^ dl_swz(slot >> 5));
   }
   // Copy j (0 .. NCP-1) of a stage: panel j / NQ (a diagonal tile loads its panel twice), chunk j % NQ.
+  // buffer path: one resource for the block's X, one for its split targets
+  const i32x4_t rsX = buffer_rsrc(X, (uint32_t)(n * ldx * 2));
+  const i32x4_t rsY = buffer_rsrc(Yhl, fuse ? (uint32_t)(n * w2p * 2) : 0u);
   auto issue = [&](uint16_t* buf, int kt, int j) {
     const int pnl = j / NQ, q = j % NQ;
     const int64_t t = (int64_t)kt * kBK + lrow[q], col = (pnl == 0 ? cI : cJ) + lcol[q];
-    // both addresses are formed and one selected, without a branch
     const bool ysrc = fuse && pnl == 1;
+    if (BUF) {
+      const bool ok = t < n && (ysrc ? lcol[q] < w2p : col < d);
+      const uint32_t off = ok ? (uint32_t)(2 * (ysrc ? t * w2p + lcol[q] : t * ldx + col)) : kBufOutside;
+      const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (NQ * wid + q) * 1024;
+      lds_dma16_buf(off, ysrc ? rsY : rsX, __builtin_amdgcn_readfirstlane(dst));
+      return;
+    }
+    // both addresses are formed and one selected, without a branch
     const uint64_t in_x = ysrc ? (uint64_t)(uintptr_t)Yhl + 2 * (uint64_t)(t * w2p + lcol[q])
                                : (uint64_t)(uintptr_t)X + 2 * (uint64_t)(t * ldx + col);
     const bool ok = t < n && (ysrc ? lcol[q] < w2p : col < d);
@@ -722,9 +750,21 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     const int64_t chunk = std::max<int64_t>(1, ((int64_t)1 << 22) / ntile);
     for (int64_t b0 = 0; b0 < a.nb; b0 += chunk) {
       const int64_t nbc = std::min<int64_t>(chunk, a.nb - b0);
-      k_gram_bf16_dl<2, 4><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
-          a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, fused ? Yhl : nullptr,
-          w2, w2p, Kraw);
+      // buffer-path copies when a block's X (and its split targets) fit 31-bit byte offsets
+      const bool buf = (a.n * a.ldx * 2) < ((int64_t)1 << 31);
+#ifdef LOCA_GRAM_GLOBAL_LOADS
+      const bool use_buf = false && buf;
+#else
+      const bool use_buf = buf;
+#endif
+      if (use_buf)
+        k_gram_bf16_dl<2, 4, true><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
+            a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, fused ? Yhl : nullptr,
+            w2, w2p, Kraw);
+      else
+        k_gram_bf16_dl<2, 4, false><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
+            a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, fused ? Yhl : nullptr,
+            w2, w2p, Kraw);
     }
   } else if (big)
     k_gram_bf16<256, 2, 4><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
