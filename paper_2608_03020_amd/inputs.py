@@ -79,7 +79,7 @@ CONFIGS = {
 
 _CFG_ID = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # tensor ids inside a (config, block) key
-_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT = range(8)
+_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT = range(9)
 
 
 def custom_config(name="tiny", blocks=1, d=64, n=100, micro=None, C=5, k=8, r_a=4,
@@ -179,6 +179,16 @@ def gen_adapter_projection(cfg: LocaConfig, block: int, seed: int = 0) -> np.nda
     """Fixed random adapter projection A_l (r_a x d), entries ~ N(0, 1/d)."""
     g = _rng(seed, cfg, block, _T_ADAPT)
     return g.standard_normal((cfg.r_a, cfg.d), dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d))
+
+
+def gen_current_adapter(cfg: LocaConfig, block: int, r_prev: int, seed: int = 0):
+    """A current adapter W_prev = Lp Rp of rank r_prev in factored form (float32):
+    Lp (d x r_prev) with orthonormal-ish columns ~ N(0, 1/d), Rp (r_prev x d) ~ N(0, 1/d).
+    Callers rescale Rp to the scale they need."""
+    g = _rng(seed, cfg, block, _T_CURRENT)
+    lp = g.standard_normal((cfg.d, r_prev), dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d))
+    rp = g.standard_normal((r_prev, cfg.d), dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d))
+    return lp, rp
 
 
 def as_f64(a: np.ndarray, dtype: str) -> np.ndarray:

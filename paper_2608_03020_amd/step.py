@@ -22,7 +22,8 @@ class BlockStep:
     credit_b (nb, k, d).
     """
 
-    def __init__(self, cfg: LocaConfig, nb: int, device="cuda", projected: bool = False, n_total: Optional[int] = None):
+    def __init__(self, cfg: LocaConfig, nb: int, device="cuda", projected: bool = False, n_total: Optional[int] = None,
+                 r_prev: int = 0):
         import torch
         self.cfg, self.nb, self.device = cfg, nb, device
         d, k, r_a = cfg.d, cfg.k, cfg.r_a
@@ -36,18 +37,20 @@ class BlockStep:
         self.mb = loca.new_mb(nb, device)
         self.mb_log: List = []
         self.info = torch.zeros(max(nb * nl, 1), dtype=torch.int32, device=device)
-        self.M = torch.empty((nb, nl, d, k), dtype=torch.float32, device=device)
+        self.r_prev = r_prev
+        kp = r_prev + k  # right-hand sides of the solve: [S Lp | K]
+        self.M = torch.empty((nb, nl, d, kp), dtype=torch.float32, device=device)
         self.A_ad = torch.empty((nb * nl, r_a, d), dtype=torch.float32, device=device)
         self.B_ad = torch.empty((nb * nl, d, r_a), dtype=torch.float32, device=device)
-        self.sigma = torch.empty((nb * nl, k), dtype=torch.float32, device=device)
+        self.sigma = torch.empty((nb * nl, kp), dtype=torch.float32, device=device)
         self.projected = projected
         if projected:
             self.B_proj = torch.empty((nb, nl, d, r_a), dtype=torch.float32, device=device)
         ws = max(
             loca.workspace_size(loca.LOCA_OP_ERROR_TARGETS, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
             loca.workspace_size(loca.LOCA_OP_ACCUMULATE_STATS, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
-            loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
-            loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, nb * nl, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+            loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE, nb, n_mb, d, kp, cfg.C, r_a, nl, self.acc),
+            loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, nb * nl, n_mb, d, kp, cfg.C, r_a, nl, self.acc),
             loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE_PROJECTED, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
         )
         self.ws = loca.alloc_workspace(ws, device)
@@ -67,12 +70,26 @@ class BlockStep:
         if keep_log:
             self.mb_log.append(self.mb.clone())
 
-    def solve(self, credit_b, proj_a=None, stream=None):
-        """Rows a5-a6: ridge solves for every lambda and the rank-r_a truncation."""
+    def solve(self, credit_b, proj_a=None, stream=None, lp=None, rp=None):
+        """Rows a5-a6: ridge solves for every lambda and the rank-r_a truncation.
+
+        With a current adapter W_prev = Lp Rp (lp: (nb, d, r_prev), rp: (nb, r_prev, d);
+        the outer iteration past its first step, Theorem S6.1 with W_prev != 0), the solve
+        takes the right-hand sides [S Lp | K] and W = M [Rp; B~] is truncated from its
+        factors; the stacked right factor is a copy (layout only)."""
+        import torch
         cfg = self.cfg
         nl = len(cfg.lambdas)
-        loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, stream=stream)
-        loca.loca_lowrank_truncate(self.M.view(self.nb * nl, cfg.d, cfg.k), credit_b, cfg.r_a, self.A_ad, self.B_ad,
+        kp = self.r_prev + cfg.k
+        if self.r_prev > 0:
+            assert lp is not None and rp is not None and lp.shape[-1] == self.r_prev
+            loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, lp=lp, rp=rp,
+                                  stream=stream)
+            right = torch.cat([rp, credit_b], dim=1).contiguous()
+        else:
+            loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, stream=stream)
+            right = credit_b
+        loca.loca_lowrank_truncate(self.M.view(self.nb * nl, cfg.d, kp), right, cfg.r_a, self.A_ad, self.B_ad,
                                    self.sigma, self.info, self.ws, r_group=nl, stream=stream)
         if self.projected and proj_a is not None:
             loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj, self.info,

@@ -328,3 +328,56 @@ def test_statistics_deterministic_and_resumable():
     iu = np.triu_indices(cfg.d)
     assert np.array_equal(S1[:, iu[0], iu[1]], S2[:, iu[0], iu[1]]) and np.array_equal(K1, K2)
     assert np.array_equal(S1[:, iu[0], iu[1]], S3[:, iu[0], iu[1]]) and np.array_equal(K1, K3)
+
+
+def test_outer_step_with_current_adapter():
+    """Theorem S6.1 past the first outer step: (S + lam I) W = S W_prev + Z with a current
+    adapter W_prev = Lp Rp != 0, solved in factored form M = (S + lam I)^{-1} [S Lp | K],
+    W = M [Rp; B~], and truncated to rank r_a from its factors (kp = r_prev + k)."""
+    import torch
+    import oracle
+    from paper_2608_03020_amd.step import BlockStep
+    cfg = gen.custom_config("t14", blocks=2, d=288, n=900, micro=500, C=4, k=16, r_a=8, lambdas=(1e-2, 0.1))
+    r_prev, blocks = 6, [0, 1]
+    log(f"case outer_step: d={cfg.d} n={cfg.n} k={cfg.k} r_prev={r_prev} r_a={cfg.r_a} lambdas={cfg.lambdas}")
+    xs, zs, ys, As, Bs = host_inputs(cfg, blocks)
+    xf = [[gen.as_f64(x, "bf16") for x in xs[b]] for b in blocks]
+    zf = [gen.as_f64(z, cfg.logit_dtype) for z in zs]
+    frozen = [oracle.block_step(xf[b], zf, ys, gen.as_f64(As[b], cfg.a_dtype), np.asarray(Bs[b], np.float64),
+                                cfg.eta, (cfg.lambdas[0],), cfg.r_a) for b in blocks]
+    Lps, Rps = [], []
+    for b in blocks:  # current adapter scaled so that S W_prev and Z are of one size
+        lp, rp = gen.gen_current_adapter(cfg, b, r_prev)
+        Wp = lp.astype(np.float64) @ rp.astype(np.float64)
+        scale = np.linalg.norm(frozen[b]["Z"]) / np.linalg.norm(frozen[b]["S"] @ Wp)
+        Lps.append(lp)
+        Rps.append((rp * np.float32(scale)).astype(np.float32))
+    dev = "cuda"
+    step = BlockStep(cfg, len(blocks), dev, r_prev=r_prev)
+    x_all = padded_rows(np.stack([np.concatenate(xb, axis=0) for xb in xs]), dev)
+    z_all, y_all = to_dev(np.concatenate(zs, axis=0), dev), to_dev(np.concatenate(ys, axis=0), dev)
+    A, B = to_dev(np.stack(As), dev), to_dev(np.stack(Bs), dev)
+    step.reset()
+    for m in range(cfg.n_micro):
+        lo, hi = cfg.micro_rows(m)
+        step.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B)
+    step.solve(B, lp=to_dev(np.stack(Lps), dev), rp=to_dev(np.stack(Rps), dev))
+    torch.cuda.synchronize()
+    assert int(step.info.cpu().numpy().max()) == 0
+    M = step.M.double().cpu().numpy()
+    nl = len(cfg.lambdas)
+    for b in blocks:
+        Wp = Lps[b].astype(np.float64) @ Rps[b].astype(np.float64)
+        o = oracle.block_step(xf[b], zf, ys, gen.as_f64(As[b], cfg.a_dtype), np.asarray(Bs[b], np.float64), cfg.eta,
+                              cfg.lambdas, cfg.r_a, W_prev=Wp)
+        right = np.concatenate([Rps[b].astype(np.float64), np.asarray(Bs[b], np.float64)], axis=0)
+        for l in range(nl):
+            W_ref = o["solves"][l]["W"]
+            Wr_ref, sig_ref = oracle.truncate_dense(W_ref, cfg.r_a)
+            W_gpu = M[b, l] @ right
+            mi = b * nl + l
+            Wr_gpu = step.A_ad[mi].double().cpu().numpy().T @ step.B_ad[mi].double().cpu().numpy().T
+            sig_gpu = step.sigma[mi].double().cpu().numpy()
+            e = {"W": rel(W_gpu, W_ref), "W_r": rel(Wr_gpu, Wr_ref), "sigma": rel(sig_gpu[:cfg.r_a], sig_ref[:cfg.r_a])}
+            log(f"outer_step block {b} lambda {cfg.lambdas[l]}: " + ", ".join(f"{k} {v:.2e}" for k, v in e.items()))
+            assert max(e.values()) <= 2e-3, e
