@@ -79,7 +79,7 @@ CONFIGS = {
 
 _CFG_ID = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # tensor ids inside a (config, block) key
-_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT = range(9)
+_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT, _T_WEIGHTS = range(10)
 
 
 def custom_config(name="tiny", blocks=1, d=64, n=100, micro=None, C=5, k=8, r_a=4,
@@ -189,6 +189,16 @@ def gen_current_adapter(cfg: LocaConfig, block: int, r_prev: int, seed: int = 0)
     lp = g.standard_normal((cfg.d, r_prev), dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d))
     rp = g.standard_normal((r_prev, cfg.d), dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d))
     return lp, rp
+
+
+def gen_loss_weights(cfg: LocaConfig, micro: int, masked: float = 0.2, seed: int = 0) -> np.ndarray:
+    """Per-position loss weights w_t >= 0 of micro-batch `micro` (float32): uniform on
+    [0, 2), with a fraction `masked` of positions set to 0 (masked positions)."""
+    g = _rng(seed, cfg, 0, _T_WEIGHTS, micro)
+    lo, hi = cfg.micro_rows(micro)
+    w = (2.0 * g.random(hi - lo)).astype(np.float32)
+    w[g.random(hi - lo) < masked] = 0.0
+    return w
 
 
 def as_f64(a: np.ndarray, dtype: str) -> np.ndarray:

@@ -381,3 +381,52 @@ def test_outer_step_with_current_adapter():
             e = {"W": rel(W_gpu, W_ref), "W_r": rel(Wr_gpu, Wr_ref), "sigma": rel(sig_gpu[:cfg.r_a], sig_ref[:cfg.r_a])}
             log(f"outer_step block {b} lambda {cfg.lambdas[l]}: " + ", ".join(f"{k} {v:.2e}" for k, v in e.items()))
             assert max(e.values()) <= 2e-3, e
+
+
+def test_loss_weights_and_masked_positions():
+    """Loss weights w_t >= 0 with masked positions (w_t = 0): the head error row is
+    w_t (softmax - onehot) (Lemma S3.1 with the weighted sequence loss), so masked
+    positions give zero credit coordinates while their rows still enter S and ||X||^2."""
+    import torch
+    from paper_2608_03020_amd.step import BlockStep
+    cfg = gen.custom_config("t15", blocks=2, d=320, n=1100, micro=600, C=5, k=16, r_a=8, lambdas=(1e-2,))
+    blocks = [0, 1]
+    log(f"case loss_weights: d={cfg.d} n={cfg.n} micro={cfg.micro} C={cfg.C} k={cfg.k}, 20% masked")
+    xs, zs, ys, As, Bs = host_inputs(cfg, blocks)
+    ws = [gen.gen_loss_weights(cfg, m) for m in range(cfg.n_micro)]
+    dev = "cuda"
+    step = BlockStep(cfg, len(blocks), dev)
+    x_all = padded_rows(np.stack([np.concatenate(xb, axis=0) for xb in xs]), dev)
+    z_all, y_all = to_dev(np.concatenate(zs, axis=0), dev), to_dev(np.concatenate(ys, axis=0), dev)
+    w_all = to_dev(np.concatenate(ws), dev)
+    A, B = to_dev(np.stack(As), dev), to_dev(np.stack(Bs), dev)
+    step.reset()
+    Ys, mbs = [], []
+    for m in range(cfg.n_micro):
+        lo, hi = cfg.micro_rows(m)
+        step.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B, w=w_all[lo:hi])
+        Ys.append(step.Y[:, :hi - lo].double().cpu().numpy())
+        mbs.append(step.mb.cpu().numpy().copy())
+    step.solve(B)
+    torch.cuda.synchronize()
+    assert int(step.info.cpu().numpy().max()) == 0
+    import oracle
+    for b in blocks:
+        xf = [gen.as_f64(x, "bf16") for x in xs[b]]
+        o = oracle.block_step(xf, [gen.as_f64(z, cfg.logit_dtype) for z in zs], ys, gen.as_f64(As[b], cfg.a_dtype),
+                              np.asarray(Bs[b], np.float64), cfg.eta, cfg.lambdas, cfg.r_a,
+                              ws=[np.asarray(w, np.float64) for w in ws])
+        e = {}
+        for m in range(cfg.n_micro):
+            e[f"Y{m}"] = rel(Ys[m][b], o["Y"][m])
+            masked = ws[m] == 0.0
+            assert np.all(Ys[m][b][masked] == 0.0), "masked positions must have zero credit coordinates"
+            e[f"q2_{m}"] = abs(mbs[m][b, 0] - o["mb"][m]["sum_q2"]) / o["mb"][m]["sum_q2"]
+            e[f"eta{m}"] = abs(mbs[m][b, 2] - o["mb"][m]["eta_bar"]) / o["mb"][m]["eta_bar"]
+        iu = np.triu_indices(cfg.d)
+        e["S"] = rel(step.S[b].double().cpu().numpy()[iu], o["S"][iu])
+        e["K"] = rel(step.K[b].double().cpu().numpy(), o["K"])
+        e["M"] = rel(step.M[b, 0].double().cpu().numpy(), o["solves"][0]["M"])
+        log(f"loss_weights block {b}: " + ", ".join(f"{k} {v:.2e}" for k, v in e.items()))
+        assert max(v for k, v in e.items() if k[0] in "Yqe") <= 1e-5, e
+        assert max(e["S"], e["K"], e["M"]) <= 2e-3, e
