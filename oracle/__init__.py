@@ -13,6 +13,8 @@ iteration, steps 2-5):
   4. ridge solve (S + lam I) W = S W_prev + Z by Cholesky          (Thm S6.1, S7)
   5. Eckart-Young truncation of W to rank r_a                      (Lemma S5.2)
 plus the paper-literal projected form with a random A_l            (Eqs. 6-9)
+and the one-time Stage I calibration that produces A~, B~: the feedback ridge
+fit, its rank-k truncation and the alignment diagnostic           (Section S5)
 
 It shares no code with the HIP path and never imports it.
 """
@@ -204,6 +206,44 @@ def projected_solve(G, Cst, lam):
 
 
 # ----------------------------------------------------------------- one block
+
+
+# ---------------------------------------------------------------- Stage I feedback calibration
+
+
+def feedback_fit(E, G, beta, form="dual"):
+    """The feedback ridge fit of Stage I (Section S5, Eq. 5 and the theorem on its
+    solution): F_hat = argmin_F ||F E - G||_F^2 + beta ||F||_F^2 for probe columns
+    E (top errors) and G (exact block gradients), both d x N_p.
+      dual:   F_hat = G (E^T E + beta I)^{-1} E^T   (a system in N_p unknowns)
+      primal: F_hat = G E^T (E E^T + beta I)^{-1}   (a system in d unknowns)
+    Both are linear solves (Cholesky), never explicit inverses."""
+    E, G = _f64(E), _f64(G)
+    if form == "dual":
+        Z, _ = ridge_solve(E.T @ E, np.ascontiguousarray(E.T), beta)   # (E^T E + beta I) Z = E^T
+        return G @ Z
+    Ft, _ = ridge_solve(E @ E.T, E @ G.T, beta)                         # (E E^T + beta I) F^T = E G^T
+    return np.ascontiguousarray(Ft.T)
+
+
+def feedback_factors(F_hat, k, Wu=None):
+    """Rank-k truncation F = U_k S_k V_k^T of the fitted map (Section S5, Eq. 5 and the
+    rank-truncation lemma) and the credit factors the hot path takes with W_u^T folded
+    into the first: B~ = S_k U_k^T (k x d), A~ = W_u V_k (rows of W_u: vocabulary).
+    Returns F_k, all singular values, B~, A~ (None without W_u)."""
+    U, s, V = svd(F_hat)
+    F_k = (U[:, :k] * s[:k]) @ V[:, :k].T
+    Bt = s[:k, None] * U[:, :k].T
+    At = None if Wu is None else _f64(Wu) @ V[:, :k]
+    return F_k, s, Bt, At
+
+
+def alignment(F, E, G):
+    """Alignment diagnostic of Section S5: the cosine between the stacked prediction
+    F E and the exact probe gradients G (Frobenius inner product)."""
+    P = _f64(F) @ _f64(E)
+    G = _f64(G)
+    return float(np.sum(P * G) / (np.linalg.norm(P) * np.linalg.norm(G)))
 
 
 def block_step(xs: Sequence[np.ndarray], zs: Sequence[np.ndarray], ys: Sequence[np.ndarray],
