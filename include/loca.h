@@ -67,7 +67,8 @@ typedef enum {
   LOCA_OP_ACCUMULATE_STATS = 1,
   LOCA_OP_RIDGE_SOLVE = 2,
   LOCA_OP_LOWRANK_TRUNCATE = 3,
-  LOCA_OP_RIDGE_SOLVE_PROJECTED = 4
+  LOCA_OP_RIDGE_SOLVE_PROJECTED = 4,
+  LOCA_OP_FEEDBACK_FIT = 5
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -215,9 +216,37 @@ loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
                                const float* credit_b, int64_t b_bstride, float* t_out,
                                int64_t t_bstride);
 
+/* ---------------------------------------------------------------------------
+ * Stage I calibration of the feedback map, run once before adaptation (Section S5,
+ * Eq. 5; the theorem on the feedback ridge solution; the rank-truncation lemma).
+ * For nb blocks sharing the probe top errors e (d x np float, row-major: column j
+ * is probe position j) and with exact block gradients g_b (d x np float, stride
+ * g_bstride), the ridge fit in its dual form
+ *   F_hat_b = G_b (E^T E + beta I)^{-1} E^T        (a Cholesky solve in np unknowns)
+ * its best rank-k approximation F_b = U_k S_k V_k^T and the credit factors of the
+ * hot path (W_u^T folded into the first, as loca_error_targets expects):
+ *   bt_out : per block k x d float, B~ = S_k U_k^T (stride bt_bstride);
+ *   at_out : per block vocab x k float, A~ = W_u V_k (stride at_bstride); needs
+ *            wu (vocab x d, F32 or BF16); both may be NULL (then skipped);
+ *   sigma_out : per block np floats, the singular values of F_hat_b, decreasing;
+ *   alpha_out : per block the alignment diagnostic <F_b E, G_b> / (||F_b E|| ||G_b||)
+ *               (float64).
+ * beta > 0 (finite).  dev_info : nb int32, 0 or the 1-based pivot at which
+ * E^T E + beta I failed to be positive definite (only for non-finite data).
+ * Limits: np <= 64, k <= np, k <= d.  Workspace: LOCA_OP_FEEDBACK_FIT with
+ * n = np.
+ * ------------------------------------------------------------------------- */
+loca_status loca_feedback_fit(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k,
+                              const float* e, const float* g, int64_t g_bstride, double beta,
+                              const void* wu, loca_dtype wu_dtype, int64_t vocab, float* bt_out,
+                              int64_t bt_bstride, float* at_out, int64_t at_bstride,
+                              float* sigma_out, double* alpha_out, int32_t* dev_info, void* ws,
+                              size_t ws_bytes);
+
 /* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
- * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there).  `acc` selects the
- * precision mode.  Unused arguments may be 0. */
+ * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there; n = np for
+ * LOCA_OP_FEEDBACK_FIT).  `acc` selects the precision mode.  Unused arguments
+ * may be 0. */
 size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,
                            int64_t r_a, int64_t n_lambda, loca_dtype acc);
 

@@ -1,0 +1,289 @@
+// k_calib.hip -- one-time Stage I calibration of the feedback map (Section S5).
+//
+// The feedback ridge fit of Eq. 5, F_hat = argmin ||F E - G||_F^2 + beta ||F||_F^2 for the
+// probe columns E (top errors, d x Np, shared by the blocks) and G_b (exact gradients at
+// block b, d x Np), in its dual form (Section S5's theorem): F_hat = G_b (E^T E + beta I)^{-1} E^T,
+// evaluated as a Cholesky solve in Np unknowns:
+//   1. Gamma = E^T E (fp64, split over the rows of E, fixed-order sums);
+//   2. Gamma + beta I = L L^T (one workgroup, fp64);
+//   3. R = (Gamma + beta I)^{-1} E^T (Np x d), one column of E^T per thread (forward and
+//      back substitution with L);
+//   4. the best rank-k approximation F_b = U_k S_k V_k^T of F_hat = G_b R (the rank-
+//      truncation lemma of Section S5) with the factored Eckart-Young truncation of the
+//      hot path (M = G_b, right factor R shared by all blocks);
+//   5. the credit factors B~ = S_k U_k^T, A~ = W_u V_k (W_u^T folded into A~, as on the hot
+//      path), and the alignment diagnostic alpha_b = <F_b E, G_b> / (||F_b E|| ||G_b||),
+//      with ||F_b E|| = ||S_k V_k^T E|| since U_k has orthonormal columns.
+#include "loca_common.h"
+
+namespace loca {
+
+namespace {
+
+constexpr int kT = 256;
+constexpr int kMaxNp = 64;
+constexpr int kRows = 32;
+
+// part[(b * ns + z) * kL * kR + j * kR + n] = sum_{c in rows of z} L_b(c, j) R_b(c, n), fp64,
+// L_b(c, j) = L[b * l_bs + c * l_sc + j * l_sj] (likewise R); rows split in ns equal ranges
+// of 32-row multiples (grid: x = z, y = b).
+__global__ __launch_bounds__(kT) void k_tall_cross(int64_t d, int kL, int kR, const float* __restrict__ L,
+                                                   int64_t l_bs, int64_t l_sc, int64_t l_sj,
+                                                   const float* __restrict__ R, int64_t r_bs, int64_t r_sc,
+                                                   int64_t r_sn, int ns, double* __restrict__ part) {
+  __shared__ double sL[kRows][kMaxNp + 1];
+  __shared__ double sR[kRows][kMaxNp + 1];
+  const int64_t b = blockIdx.y;
+  const int z = blockIdx.x;
+  const int64_t chunk = ((d + ns - 1) / ns + kRows - 1) / kRows * kRows;
+  const int64_t ib = (int64_t)z * chunk, ie = ib + chunk < d ? ib + chunk : d;
+  const float* Lb = L + b * l_bs;
+  const float* Rb = R + b * r_bs;
+  const int nout = kL * kR;
+  double acc[(kMaxNp * kMaxNp) / kT];
+#pragma unroll
+  for (int q = 0; q < (kMaxNp * kMaxNp) / kT; ++q) acc[q] = 0.0;
+  for (int64_t i0 = ib; i0 < ie; i0 += kRows) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < kRows * kMaxNp; e += kT) {
+      const int r = e / kMaxNp, c = e % kMaxNp;
+      const int64_t i = i0 + r;
+      sL[r][c] = (i < ie && c < kL) ? (double)Lb[i * l_sc + c * l_sj] : 0.0;
+      sR[r][c] = (i < ie && c < kR) ? (double)Rb[i * r_sc + c * r_sn] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < (kMaxNp * kMaxNp) / kT; ++q) {
+      const int e = threadIdx.x + kT * q;
+      if (e < nout) {
+        const int j = e / kR, n = e % kR;
+        double s = acc[q];
+        for (int r = 0; r < kRows; ++r) s += sL[r][j] * sR[r][n];
+        acc[q] = s;
+      }
+    }
+  }
+  double* out = part + (b * ns + z) * (int64_t)nout;
+#pragma unroll
+  for (int q = 0; q < (kMaxNp * kMaxNp) / kT; ++q) {
+    const int e = threadIdx.x + kT * q;
+    if (e < nout) out[e] = acc[q];
+  }
+}
+
+// Lmat = chol(sum_z part_z + beta I) (lower, np x np, fp64, row-major), one workgroup.
+__global__ __launch_bounds__(kT) void k_chol_small(int np_, int ns, const double* __restrict__ part, double beta,
+                                                   double* __restrict__ Lmat, int32_t* __restrict__ dev_info,
+                                                   int64_t nb) {
+  __shared__ double sA[kMaxNp][kMaxNp + 1];
+  const int tid = threadIdx.x;
+  for (int e = tid; e < np_ * np_; e += kT) {
+    const int i = e / np_, j = e % np_;
+    double s = 0.0;
+    for (int z = 0; z < ns; ++z) s += part[(int64_t)z * np_ * np_ + e];
+    sA[i][j] = s + (i == j ? beta : 0.0);
+  }
+  __syncthreads();
+  for (int j = 0; j < np_; ++j) {
+    if (tid == 0) {
+      const double piv = sA[j][j];
+      if (!(piv > 0.0))
+        for (int64_t b = 0; b < nb; ++b) atomicCAS(&dev_info[b], 0, j + 1);
+      sA[j][j] = sqrt(piv);
+    }
+    __syncthreads();
+    for (int i = j + 1 + tid; i < np_; i += kT) sA[i][j] /= sA[j][j];
+    __syncthreads();
+    for (int e = tid; e < (np_ - j - 1) * (np_ - j - 1); e += kT) {
+      const int i = j + 1 + e / (np_ - j - 1), c = j + 1 + e % (np_ - j - 1);
+      if (c <= i) sA[i][c] -= sA[i][j] * sA[c][j];
+    }
+    __syncthreads();
+  }
+  for (int e = tid; e < np_ * np_; e += kT) {
+    const int i = e / np_, j = e % np_;
+    Lmat[e] = j <= i ? sA[i][j] : 0.0;
+  }
+}
+
+// R[:, c] = (L L^T)^{-1} E[c, :]^T for every column c < d (thread per column; R is np x d).
+__global__ __launch_bounds__(kT) void k_ridge_cols(int64_t d, int np_, const float* __restrict__ E,
+                                                   const double* __restrict__ Lmat, float* __restrict__ R) {
+  __shared__ double sL[kMaxNp * kMaxNp];
+  for (int e = threadIdx.x; e < np_ * np_; e += kT) sL[e] = Lmat[e];
+  __syncthreads();
+  const int64_t c = (int64_t)blockIdx.x * kT + threadIdx.x;
+  if (c >= d) return;
+  double y[kMaxNp];
+#pragma unroll
+  for (int i = 0; i < kMaxNp; ++i) y[i] = i < np_ ? (double)E[c * np_ + i] : 0.0;
+  // forward: L y' = e
+#pragma unroll
+  for (int i = 0; i < kMaxNp; ++i) {
+    if (i < np_) {
+      double s = y[i];
+#pragma unroll
+      for (int j = 0; j < i; ++j) s -= sL[i * np_ + j] * y[j];
+      y[i] = s / sL[i * np_ + i];
+    }
+  }
+  // back: L^T x = y'
+#pragma unroll
+  for (int i = kMaxNp - 1; i >= 0; --i) {
+    if (i < np_) {
+      double s = y[i];
+#pragma unroll
+      for (int j = i + 1; j < kMaxNp; ++j)
+        if (j < np_) s -= sL[j * np_ + i] * y[j];
+      y[i] = s / sL[i * np_ + i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kMaxNp; ++i)
+    if (i < np_) R[(int64_t)i * d + c] = (float)y[i];
+}
+
+// Per block: B~ = S_k U_k^T from U_k^T (a) and sigma; V_k = (V_k S_k) / S_k from b (zero where
+// sigma = 0), kept for A~.  Grid: x over d, y = block.
+__global__ void k_calib_factors(int64_t d, int k, int np_, const float* __restrict__ a, const float* __restrict__ bvs,
+                                const float* __restrict__ sigma, float* __restrict__ bt_out, int64_t bt_bstride,
+                                float* __restrict__ vk) {
+  const int64_t b = blockIdx.y;
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= d) return;
+  for (int j = 0; j < k; ++j) {
+    const float s = sigma[b * np_ + j];
+    bt_out[b * bt_bstride + (int64_t)j * d + c] = s * a[(b * k + j) * d + c];
+    vk[(b * d + c) * k + j] = s > 0.f ? bvs[(b * d + c) * k + j] / s : 0.f;
+  }
+}
+
+// alpha_b = <P, Q> / (||Q|| ||G||) from the fixed-order sums of the partial products
+// P = U_k^T G, Q = S_k V_k^T E (k x np) and ||G||^2 (one thread per block).
+__global__ void k_calib_alpha(int64_t nb, int k, int np_, int ns, const double* __restrict__ pP,
+                              const double* __restrict__ pQ, const double* __restrict__ pG2,
+                              double* __restrict__ alpha_out) {
+  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= nb) return;
+  double pq = 0.0, qq = 0.0, gg = 0.0;
+  for (int e = 0; e < k * np_; ++e) {
+    double p = 0.0, q = 0.0;
+    for (int z = 0; z < ns; ++z) {
+      p += pP[(b * ns + z) * k * np_ + e];
+      q += pQ[(b * ns + z) * k * np_ + e];
+    }
+    pq += p * q;
+    qq += q * q;
+  }
+  for (int e = 0; e < np_; ++e)
+    for (int z = 0; z < ns; ++z) gg += pG2[(b * ns + z) * np_ * np_ + e * np_ + e];
+  const double den = sqrt(qq) * sqrt(gg);
+  alpha_out[b] = den > 0.0 ? pq / den : 0.0;
+}
+
+// A~_b = W_u V_k,b (vocab x k): one wave per row of W_u, lanes over d, k sums reduced in
+// a fixed order.  Grid: x over rows (4 waves per workgroup), y = block.
+template <typename WT>
+__global__ __launch_bounds__(kT) void k_head_fold(int64_t vocab, int64_t d, int k, const WT* __restrict__ wu,
+                                                  const float* __restrict__ vk, float* __restrict__ at_out,
+                                                  int64_t at_bstride) {
+  const int64_t b = blockIdx.y;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int64_t v = (int64_t)blockIdx.x * 4 + wid;
+  if (v >= vocab) return;
+  const float* V = vk + b * d * k;
+  float acc[kMaxNp];
+#pragma unroll
+  for (int j = 0; j < kMaxNp; ++j) acc[j] = 0.f;
+  for (int64_t c = lane; c < d; c += 64) {
+    const float w = load_as_f32(wu + v * d + c);
+#pragma unroll
+    for (int j = 0; j < kMaxNp; ++j)
+      if (j < k) acc[j] += w * V[c * k + j];
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxNp; ++j) {
+    if (j < k) {
+      const float s = wave_sum(acc[j]);
+      if (lane == 0) at_out[b * at_bstride + v * k + j] = s;
+    }
+  }
+}
+
+__global__ void k_zero_i32(int32_t* p, int64_t cnt) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < cnt) p[i] = 0;
+}
+
+int calib_splits(int64_t d) {
+  const int64_t s = d / 256;
+  return (int)(s < 1 ? 1 : (s > 16 ? 16 : s));
+}
+
+}  // namespace
+
+size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
+  const int ns = calib_splits(d);
+  size_t s = align256(sizeof(double) * ns * np_ * np_);           // Gamma partials
+  s += align256(sizeof(double) * np_ * np_);                      // L
+  s += align256(sizeof(float) * np_ * d);                         // R
+  s += align256(sizeof(float) * nb * k * d);                      // U_k^T
+  s += align256(sizeof(float) * nb * d * k);                      // V_k S_k, then V_k
+  s += align256(sizeof(float) * nb * d * k);
+  s += align256(sizeof(double) * nb * ns * (2 * k * np_ + np_ * np_));  // alpha partials
+  s += align256(sizeof(int32_t) * nb);                             // the truncation's own status
+  s += lowrank_truncate_ws(nb, d, np_, k);
+  return s;
+}
+
+hipError_t launch_feedback_fit(const CalibArgs& a) {
+  const int64_t d = a.d, np_ = a.np_, k = a.k, nb = a.nb;
+  const int ns = calib_splits(d);
+  char* p = a.ws;
+  double* gpart = (double*)p; p += align256(sizeof(double) * ns * np_ * np_);
+  double* Lmat = (double*)p; p += align256(sizeof(double) * np_ * np_);
+  float* R = (float*)p; p += align256(sizeof(float) * np_ * d);
+  float* ut = (float*)p; p += align256(sizeof(float) * nb * k * d);
+  float* vs = (float*)p; p += align256(sizeof(float) * nb * d * k);
+  float* vk = (float*)p; p += align256(sizeof(float) * nb * d * k);
+  double* apart = (double*)p; p += align256(sizeof(double) * nb * ns * (2 * k * np_ + np_ * np_));
+  int32_t* tinfo = (int32_t*)p; p += align256(sizeof(int32_t) * nb);
+  char* tws = p;
+  double* pP = apart;
+  double* pQ = apart + nb * ns * k * np_;
+  double* pG = apart + 2 * nb * ns * k * np_;
+  hipStream_t st = a.stream;
+  k_zero_i32<<<(unsigned)((nb + 255) / 256), 256, 0, st>>>(a.dev_info, nb);
+  // 1-3: Gamma, its Cholesky with beta, R = (Gamma + beta I)^{-1} E^T
+  k_tall_cross<<<dim3((unsigned)ns, 1), kT, 0, st>>>(d, (int)np_, (int)np_, a.e, 0, np_, 1, a.e, 0, np_, 1, ns, gpart);
+  k_chol_small<<<1, kT, 0, st>>>((int)np_, ns, gpart, a.beta, Lmat, a.dev_info, nb);
+  k_ridge_cols<<<(unsigned)((d + kT - 1) / kT), kT, 0, st>>>(d, (int)np_, a.e, Lmat, R);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // 4: rank-k truncation of F_hat_b = G_b R (dev_info is not touched by the truncation
+  // beyond zero-filling, so it runs on a private copy)
+  TruncArgs t{st, nb, d, np_, k, a.g, a.g_bstride, R, 0, nb, ut, k * d, vs, d * k, a.sigma_out, np_, nullptr, 0,
+              tinfo, tws};
+  if ((e = launch_lowrank_truncate(t)) != hipSuccess) return e;
+  // 5: credit factors and the alignment diagnostic
+  k_calib_factors<<<dim3((unsigned)((d + 255) / 256), (unsigned)nb), 256, 0, st>>>(
+      d, (int)k, (int)np_, ut, vs, a.sigma_out, a.bt_out, a.bt_bstride, vk);
+  // P = U_k^T G (U_k^T is k x d: L(c, j) = ut[j * d + c]); Q = (V_k S_k)^T E; ||G||^2 from G^T G
+  k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, ut, k * d, 1, d, a.g,
+                                                                 a.g_bstride, np_, 1, ns, pP);
+  k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, vs, d * k, k, 1, a.e, 0, np_, 1,
+                                                                 ns, pQ);
+  k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)np_, (int)np_, a.g, a.g_bstride, np_, 1, a.g,
+                                                                 a.g_bstride, np_, 1, ns, pG);
+  k_calib_alpha<<<(unsigned)((nb + 63) / 64), 64, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
+  if (a.wu && a.at_out) {
+    dim3 g((unsigned)((a.vocab + 3) / 4), (unsigned)nb);
+    if (a.wu_dtype == LOCA_BF16)
+      k_head_fold<uint16_t><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const uint16_t*)a.wu, vk, a.at_out, a.at_bstride);
+    else
+      k_head_fold<float><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const float*)a.wu, vk, a.at_out, a.at_bstride);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace loca

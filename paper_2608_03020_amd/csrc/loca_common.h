@@ -212,6 +212,20 @@ struct ProjArgs {
 size_t projected_ws(int64_t nb, int64_t d, int64_t k, int64_t r_a, int64_t n_lambda);
 hipError_t launch_ridge_solve_projected(const ProjArgs& a);
 
+struct CalibArgs {
+  hipStream_t stream;
+  int64_t nb, d, np_, k;
+  const float* e; const float* g; int64_t g_bstride;
+  double beta;
+  const void* wu; loca_dtype wu_dtype; int64_t vocab;
+  float* bt_out; int64_t bt_bstride;
+  float* at_out; int64_t at_bstride;
+  float* sigma_out; double* alpha_out;
+  int32_t* dev_info; int32_t* unused_; char* ws;
+};
+size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
+hipError_t launch_feedback_fit(const CalibArgs& a);
+
 hipError_t launch_dense_targets(hipStream_t s, int64_t nb, int64_t n, int64_t k, int64_t d,
                                 const float* y, int64_t y_bstride, const loca_mb* mb,
                                 const float* credit_b, int64_t b_bstride, float* t_out,

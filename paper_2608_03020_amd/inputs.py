@@ -79,7 +79,7 @@ CONFIGS = {
 
 _CFG_ID = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # tensor ids inside a (config, block) key
-_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT, _T_WEIGHTS = range(10)
+_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT, _T_WEIGHTS, _T_PROBE = range(11)
 
 
 def custom_config(name="tiny", blocks=1, d=64, n=100, micro=None, C=5, k=8, r_a=4,
@@ -199,6 +199,25 @@ def gen_loss_weights(cfg: LocaConfig, micro: int, masked: float = 0.2, seed: int
     w = (2.0 * g.random(hi - lo)).astype(np.float32)
     w[g.random(hi - lo) < masked] = 0.0
     return w
+
+
+def gen_probe_pairs(cfg: LocaConfig, n_p: int, blocks: int, rank: int = 0, noise: float = 2.0, seed: int = 0):
+    """Synthetic calibration probes (float32): top errors E (d x n_p) ~ N(0, 1) shared by
+    the blocks, and per block gradients G_b = F0_b E + noise * N(0, 1) with a seeded
+    rank-`rank` map F0_b = P_b Q_b^T (P, Q ~ N(0, 1/d); rank 0 means 2k).  The noise
+    level sets how far a fitted map can align with G (the paper reports 0.3-0.5)."""
+    g = _rng(seed, cfg, 0, _T_PROBE)
+    E = g.standard_normal((cfg.d, n_p), dtype=np.float32)
+    r = rank or 2 * cfg.k
+    Gs = []
+    for b in range(blocks):
+        gb = _rng(seed, cfg, b, _T_PROBE, 1)
+        P = gb.standard_normal((cfg.d, r), dtype=np.float32) / np.float32(np.sqrt(cfg.d))
+        Q = gb.standard_normal((cfg.d, r), dtype=np.float32) / np.float32(np.sqrt(cfg.d))
+        Gs.append((P @ (Q.T @ E) + np.float32(noise / np.sqrt(cfg.d)) * gb.standard_normal((cfg.d, n_p),
+                                                                                             dtype=np.float32))
+                  .astype(np.float32))
+    return E, np.stack(Gs)
 
 
 def as_f64(a: np.ndarray, dtype: str) -> np.ndarray:

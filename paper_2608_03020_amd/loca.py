@@ -17,11 +17,11 @@ LIB_PATH = os.environ.get("LOCA_LIB", os.path.join(HERE, "lib", "libloca.so"))
 LOCA_OK, LOCA_E_ARG, LOCA_E_WORKSPACE, LOCA_E_HIP, LOCA_E_UNSUPPORTED = range(5)
 LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
- LOCA_OP_RIDGE_SOLVE_PROJECTED) = range(5)
+ LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT) = range(6)
 
 EXPORTED = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
-            "loca_ridge_solve_projected", "loca_dense_targets", "loca_workspace_size", "loca_status_str",
-            "loca_version")
+            "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_workspace_size",
+            "loca_status_str", "loca_version")
 
 
 class LocaMB(ctypes.Structure):
@@ -62,13 +62,15 @@ def load():
     lib.loca_ridge_solve_projected.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _I64,
                                                _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _SZ]
     lib.loca_dense_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _VP, _I64, _VP, _I64]
+    lib.loca_feedback_fit.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _D, _VP, _I, _I64, _VP, _I64,
+                                      _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_workspace_size.argtypes = [_I, _I64, _I64, _I64, _I64, _I64, _I64, _I64, _I]
     lib.loca_workspace_size.restype = _SZ
     lib.loca_status_str.argtypes = [_I]
     lib.loca_status_str.restype = ctypes.c_char_p
     lib.loca_version.restype = ctypes.c_char_p
     for name in ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
-                 "loca_ridge_solve_projected", "loca_dense_targets"):
+                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit"):
         getattr(lib, name).restype = _I
     _lib = lib
     return lib
@@ -209,6 +211,22 @@ def loca_ridge_solve_projected(S, K, credit_b, proj_a, lambdas: Sequence[float],
         ctypes.cast(lam, ctypes.c_void_p), len(lambdas), _ptr(b_out), b_out.stride(1), _ptr(g_out), _ptr(dev_info),
         _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_ridge_solve_projected", st)
+
+
+def loca_feedback_fit(e, g, beta: float, bt_out, sigma_out, alpha_out, dev_info, ws, *, wu=None, at_out=None,
+                      stream=None):
+    """e (d, np) probe top errors; g (nb, d, np) exact block gradients; bt_out (nb, k, d) = B~;
+    sigma_out (nb, np); alpha_out (nb,) float64; optional wu (vocab, d) and at_out (nb, vocab, k) = A~."""
+    d, n_p = e.shape
+    nb = g.shape[0]
+    k = bt_out.shape[-2]
+    vocab = wu.shape[0] if wu is not None else 0
+    st = load().loca_feedback_fit(
+        _stream(stream), nb, d, n_p, k, _ptr(e), _ptr(g), g.stride(0), float(beta), _ptr(wu),
+        _dtype(wu) if wu is not None else LOCA_F32, vocab, _ptr(bt_out), bt_out.stride(0), _ptr(at_out),
+        at_out.stride(0) if at_out is not None else 0, _ptr(sigma_out), _ptr(alpha_out), _ptr(dev_info), _ptr(ws),
+        ws.numel() * ws.element_size())
+    _check("loca_feedback_fit", st)
 
 
 def loca_dense_targets(y, mb, credit_b, t_out, *, stream=None):

@@ -154,3 +154,26 @@ def test_projected_and_dense_targets_reject(lib):
     assert so.loca_ridge_solve_projected(None, 1, 16, 4, 65, FAKE, FAKE, lib.LOCA_F32, 0, 0, FAKE, 0, FAKE, 0, None,
                                          0, p, 1, FAKE, 0, None, FAKE, None, 0) == lib.LOCA_E_UNSUPPORTED
     assert so.loca_dense_targets(None, 1, 4, 2, 8, None, 0, FAKE, FAKE, 0, FAKE, 0) == lib.LOCA_E_ARG
+
+
+def test_feedback_fit_rejects(lib):
+    so = lib.load()
+
+    def call(nb=1, d=32, n_p=16, k=4, e=FAKE, g=FAKE, gbs=0, beta=0.1, wu=None, wdt=lib.LOCA_F32, vocab=0,
+             bt=FAKE, at=None, sig=FAKE, alpha=FAKE, ws=None, wsb=0):
+        return so.loca_feedback_fit(None, nb, d, n_p, k, e, g, gbs, beta, wu, wdt, vocab, bt, 0, at, 0, sig, alpha,
+                                    FAKE, ws, wsb)
+
+    assert call(beta=0.0) == lib.LOCA_E_ARG               # the fit needs beta > 0
+    assert call(beta=float("inf")) == lib.LOCA_E_ARG
+    assert call(beta=float("nan")) == lib.LOCA_E_ARG
+    assert call(k=17) == lib.LOCA_E_ARG                   # k <= np
+    assert call(d=3) == lib.LOCA_E_ARG                    # k <= d
+    assert call(e=None) == lib.LOCA_E_ARG
+    assert call(at=FAKE) == lib.LOCA_E_ARG                # A~ needs W_u
+    assert call(at=FAKE, wu=FAKE, vocab=10, wdt=lib.LOCA_F64) == lib.LOCA_E_ARG
+    assert call(nb=2, gbs=10) == lib.LOCA_E_ARG
+    assert call(n_p=65, k=4) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE
+    assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT, 2, 48, 300, 8, 0, 0, 0, lib.LOCA_F32) > 0
+    assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT, 2, 65, 300, 8, 0, 0, 0, lib.LOCA_F32) == 0

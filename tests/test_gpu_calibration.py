@@ -1,0 +1,57 @@
+"""GPU parity of the Stage I calibration (Section S5) through the C ABI: the feedback
+ridge fit, its rank-k truncation, the credit factors of the hot path and the
+alignment diagnostic, against the oracle on the same seeded probe pairs."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from gpu_helpers import log, rel, to_dev
+from paper_2608_03020_amd import inputs as gen
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("d,n_p,k,nb,vocab,beta,wdt", [
+    (300, 48, 8, 2, 37, 0.5, "f32"),      # ragged against the 32-row chunks
+    (1024, 64, 16, 3, 200, 0.05, "bf16"),  # largest probe count, bf16 head
+    (64, 5, 5, 1, 4, 1.0, "f32"),          # k = np, tiny
+])
+def test_feedback_fit_parity(d, n_p, k, nb, vocab, beta, wdt):
+    import torch
+    import oracle
+    from paper_2608_03020_amd import loca
+    cfg = gen.custom_config(f"calib{d}", blocks=nb, d=d, n=64, C=vocab, k=k, r_a=min(4, k))
+    log(f"case feedback_fit: d={d} np={n_p} k={k} nb={nb} vocab={vocab} beta={beta} W_u {wdt}")
+    E, G = gen.gen_probe_pairs(cfg, n_p, nb)
+    rng = np.random.default_rng(7)
+    Wu = (rng.standard_normal((vocab, d)) / np.sqrt(d)).astype(np.float32)
+    if wdt == "bf16":
+        Wu_bits = gen.bf16_bits(Wu)
+        Wu_exact = gen.as_f64(Wu_bits, "bf16")
+    else:
+        Wu_bits, Wu_exact = Wu, Wu.astype(np.float64)
+    dev = "cuda"
+    bt = torch.empty((nb, k, d), dtype=torch.float32, device=dev)
+    at = torch.empty((nb, vocab, k), dtype=torch.float32, device=dev)
+    sig = torch.empty((nb, n_p), dtype=torch.float32, device=dev)
+    alpha = torch.empty(nb, dtype=torch.float64, device=dev)
+    info = torch.full((nb,), -1, dtype=torch.int32, device=dev)
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_FEEDBACK_FIT, nb, n_p, d, k), dev)
+    loca.loca_feedback_fit(to_dev(E, dev), to_dev(G, dev), beta, bt, sig, alpha, info, ws, wu=to_dev(Wu_bits, dev),
+                           at_out=at)
+    torch.cuda.synchronize()
+    assert np.all(info.cpu().numpy() == 0)
+    for b in range(nb):
+        F = oracle.feedback_fit(E, G[b], beta)
+        F_k, s, Bt_ref, At_ref = oracle.feedback_factors(F, k, Wu_exact)
+        a_ref = oracle.alignment(F_k, E, G[b])
+        Bt_g = bt[b].double().cpu().numpy()
+        At_g = at[b].double().cpu().numpy()
+        e = {"sigma": rel(sig[b].double().cpu().numpy(), s[:n_p]),
+             "AB": rel(At_g @ Bt_g, At_ref @ Bt_ref),              # = W_u F_k^T, sign-free
+             "BtB": rel(Bt_g.T @ Bt_g, Bt_ref.T @ Bt_ref),         # = U_k S_k^2 U_k^T
+             "alpha": abs(float(alpha[b].item()) - a_ref)}
+        log(f"feedback_fit block {b}: alpha {float(alpha[b].item()):.4f} (oracle {a_ref:.4f}); " +
+            ", ".join(f"{key} {v:.2e}" for key, v in e.items()))
+        assert e["sigma"] <= 1e-4 and e["AB"] <= 1e-4 and e["BtB"] <= 1e-4 and e["alpha"] <= 1e-5, e
