@@ -85,29 +85,41 @@ def credit(E, A, B, want_q=True):
     return Y, Q
 
 
-def scaled_target(X, Q, eta):
+def _weights(a, n):
+    if a is None:
+        return None
+    a = _f64(a).reshape(-1)
+    assert a.shape == (n,)
+    return a
+
+
+def scaled_target(X, Q, eta, a=None):
+    """eta_bar and T = -eta_bar Q (Eq. 10); `a` are position weights (None = 1)."""
     X, Q = _f64(X), _f64(Q)
     n, d = X.shape
     T = np.empty((n, d), np.float64)
     info = np.empty(3, np.float64)
-    _load().loca_oracle_scaled_target(_I64(n), _I64(d), _p(X), _p(Q), ctypes.c_double(eta), _p(T), _p(info))
+    _load().loca_oracle_scaled_target(_I64(n), _I64(d), _p(X), _p(Q), _p(_weights(a, n)), ctypes.c_double(eta),
+                                      _p(T), _p(info))
     return T, {"sum_x2": info[0], "sum_q2": info[1], "eta_bar": info[2]}
 
 
-def gram_acc(X, S=None):
+def gram_acc(X, S=None, a=None):
+    """S += sum_t a_t x_t x_t^T (Eq. 9; Section S7's weighted statistics)."""
     X = _f64(X)
     n, d = X.shape
     S = np.zeros((d, d), np.float64) if S is None else S
-    _load().loca_oracle_gram_acc(_I64(n), _I64(d), _p(X), _p(S))
+    _load().loca_oracle_gram_acc(_I64(n), _I64(d), _p(X), _p(_weights(a, n)), _p(S))
     return S
 
 
-def cross_acc(X, T, Z=None):
+def cross_acc(X, T, Z=None, a=None):
+    """Z += sum_t a_t x_t T_t^T (Eq. 9; Section S7's weighted statistics)."""
     X, T = _f64(X), _f64(T)
     n, d = X.shape
     m = T.shape[1]
     Z = np.zeros((d, m), np.float64) if Z is None else Z
-    _load().loca_oracle_cross_acc(_I64(n), _I64(d), _I64(m), _p(X), _p(T), _p(Z))
+    _load().loca_oracle_cross_acc(_I64(n), _I64(d), _I64(m), _p(X), _p(_weights(a, n)), _p(T), _p(Z))
     return Z
 
 
@@ -182,14 +194,15 @@ def truncate_factored(M, R, r, want_dense=True):
     return Wr, sig, a, b
 
 
-def projected_acc(X, T, Aproj, Bcur=None, G=None, Cst=None):
+def projected_acc(X, T, Aproj, Bcur=None, G=None, Cst=None, a=None):
     X, T, Aproj = _f64(X), _f64(T), _f64(Aproj)
     n, d = X.shape
     r = Aproj.shape[0]
     G = np.zeros((r, r), np.float64) if G is None else G
     Cst = np.zeros((d, r), np.float64) if Cst is None else Cst
     Bc = None if Bcur is None else _f64(Bcur)
-    _load().loca_oracle_projected_acc(_I64(n), _I64(d), _I64(r), _p(X), _p(T), _p(Aproj), _p(Bc), _p(G), _p(Cst))
+    _load().loca_oracle_projected_acc(_I64(n), _I64(d), _I64(r), _p(X), _p(T), _p(Aproj), _p(Bc),
+                                      _p(_weights(a, n)), _p(G), _p(Cst))
     return G, Cst
 
 
@@ -250,14 +263,15 @@ def block_step(xs: Sequence[np.ndarray], zs: Sequence[np.ndarray], ys: Sequence[
                A, B, eta: float, lambdas: Sequence[float], r_a: int,
                ws: Optional[Sequence[np.ndarray]] = None, W_prev=None,
                Aproj=None, Bproj_cur=None, dense_truncation: Optional[bool] = None,
-               want_dense=True) -> Dict:
+               want_dense=True, a_ws: Optional[Sequence[np.ndarray]] = None) -> Dict:
     """All steps of one block over its mini-batches, in the paper's order.
 
     xs[m] (n_m x d), zs[m] (n_m x C), ys[m] (n_m) are float64-exact inputs of
     mini-batch m; A (C x k), B (k x d) the credit factors.  W_prev (d x d) is the
     current adapter in token-major form (None = frozen model).  Aproj (r_a x d),
     when given, adds the paper-literal projected solve with current adapter
-    Bproj_cur (d x r_a, None = 0).
+    Bproj_cur (d x r_a, None = 0).  ws[m] are the loss weights of mini-batch m
+    (Lemma S3.1), a_ws[m] its statistic weights (Section S7; None = 1).
     """
     d = B.shape[1]
     S = np.zeros((d, d), np.float64)
@@ -272,12 +286,13 @@ def block_step(xs: Sequence[np.ndarray], zs: Sequence[np.ndarray], ys: Sequence[
     for m, (X, z, y) in enumerate(zip(xs, zs, ys)):
         E = head_error(z, y, None if ws is None else ws[m])
         Y, Q = credit(E, A, B)
-        T, info = scaled_target(X, Q, eta)
-        gram_acc(X, S)
-        cross_acc(X, T, Z)
-        cross_acc(X, -info["eta_bar"] * Y, K)
+        a = None if a_ws is None else a_ws[m]
+        T, info = scaled_target(X, Q, eta, a)
+        gram_acc(X, S, a)
+        cross_acc(X, T, Z, a)
+        cross_acc(X, -info["eta_bar"] * Y, K, a)
         if Aproj is not None:
-            projected_acc(X, T, Aproj, Bproj_cur, G, Cst)
+            projected_acc(X, T, Aproj, Bproj_cur, G, Cst, a)
         mbs.append(info)
         Es.append(E)
         Ys.append(Y)

@@ -86,17 +86,27 @@ void loca_oracle_credit(int64_t n, int64_t C, int64_t k, int64_t d, const double
  *   RMS(M) = ||M||_F / sqrt(#entries),
  *   eta_bar = eta * RMS(X) / RMS(Q)  if Q != 0, and 0 if Q = 0,
  *   D^tar  = -eta_bar Q            (the displacement; row t is T_t).
- * X and Q have the same shape (n x d).  info = {||X||_F^2, ||Q||_F^2, eta_bar}.
+ * X and Q have the same shape (n x d).  With position weights a (n entries,
+ * NULL = all ones; the weighted statistics of Section S7) every mean square is
+ * taken under the same weights, RMS_a(M)^2 = sum_t a_t ||M_t||^2 / (d sum_t a_t),
+ * so a position of weight 0 has no influence.
+ * info = {sum_t a_t ||X_t||^2, sum_t a_t ||Q_t||^2, eta_bar}.
  * ------------------------------------------------------------------------ */
 void loca_oracle_scaled_target(int64_t n, int64_t d, const double* X, const double* Q,
-                               double eta, double* T, double* info) {
-  double sx = 0.0, sq = 0.0;
-  for (int64_t t = 0; t < n; ++t)
+                               const double* a, double eta, double* T, double* info) {
+  double sx = 0.0, sq = 0.0, wsum = 0.0;
+  for (int64_t t = 0; t < n; ++t) {
+    const double at = a ? a[t] : 1.0;
+    double xt = 0.0, qt = 0.0;
     for (int64_t i = 0; i < d; ++i) {
-      sx += X[IDX(t, i, d)] * X[IDX(t, i, d)];
-      sq += Q[IDX(t, i, d)] * Q[IDX(t, i, d)];
+      xt += X[IDX(t, i, d)] * X[IDX(t, i, d)];
+      qt += Q[IDX(t, i, d)] * Q[IDX(t, i, d)];
     }
-  const double cnt = (double)n * (double)d;
+    sx += at * xt;
+    sq += at * qt;
+    wsum += at;
+  }
+  const double cnt = wsum * (double)d;
   double eta_bar = 0.0;
   if (sq > 0.0) eta_bar = eta * (sqrt(sx / cnt) / sqrt(sq / cnt));
   if (T)
@@ -110,27 +120,28 @@ void loca_oracle_scaled_target(int64_t n, int64_t d, const double* X, const doub
 /* ------------------------------------------------------------------------
  * Streaming sufficient statistics (Eq. 9; Section S7), additive over
  * mini-batches.  With the identity projection the features are the block
- * inputs themselves, so
- *   S += sum_t x_t x_t^T          (d x d, full square),
- *   Z += sum_t x_t T_t^T          (d x m) for a target block T (n x m).
+ * inputs themselves, so, with explicit nonnegative position weights a_t
+ * (NULL = all ones),
+ *   S += sum_t a_t x_t x_t^T          (d x d, full square),
+ *   Z += sum_t a_t x_t T_t^T          (d x m) for a target block T (n x m).
  * ------------------------------------------------------------------------ */
-void loca_oracle_gram_acc(int64_t n, int64_t d, const double* X, double* S) {
+void loca_oracle_gram_acc(int64_t n, int64_t d, const double* X, const double* a, double* S) {
 #pragma omp parallel for schedule(dynamic, 4)
   for (int64_t i = 0; i < d; ++i)
     for (int64_t j = 0; j < d; ++j) {
       double s = 0.0;
-      for (int64_t t = 0; t < n; ++t) s += X[IDX(t, i, d)] * X[IDX(t, j, d)];
+      for (int64_t t = 0; t < n; ++t) s += (a ? a[t] : 1.0) * X[IDX(t, i, d)] * X[IDX(t, j, d)];
       S[IDX(i, j, d)] += s;
     }
 }
 
-void loca_oracle_cross_acc(int64_t n, int64_t d, int64_t m, const double* X, const double* T,
-                           double* Z) {
+void loca_oracle_cross_acc(int64_t n, int64_t d, int64_t m, const double* X, const double* a,
+                           const double* T, double* Z) {
 #pragma omp parallel for schedule(dynamic, 4)
   for (int64_t i = 0; i < d; ++i)
     for (int64_t j = 0; j < m; ++j) {
       double s = 0.0;
-      for (int64_t t = 0; t < n; ++t) s += X[IDX(t, i, d)] * T[IDX(t, j, m)];
+      for (int64_t t = 0; t < n; ++t) s += (a ? a[t] : 1.0) * X[IDX(t, i, d)] * T[IDX(t, j, m)];
       Z[IDX(i, j, m)] += s;
     }
 }
@@ -428,11 +439,13 @@ int loca_oracle_truncate_factored(int64_t d, int64_t kp, const double* M, const 
  * Paper-literal projected statistics (Eqs. 6 and 9; Section S6), streamed over
  * a mini-batch: with p_t = A_l x_t (A_l: r x d fixed random projection) and
  * residual target rho_t = B_cur p_t + T_t (B_cur: d x r current adapter, may be
- * NULL for the frozen model),
- *   G += sum_t p_t p_t^T   (r x r),     Cst += sum_t rho_t p_t^T   (d x r).
+ * NULL for the frozen model) and nonnegative position weights a_t (NULL = 1;
+ * the weighted form of Section S7),
+ *   G += sum_t a_t p_t p_t^T   (r x r),     Cst += sum_t a_t rho_t p_t^T   (d x r).
  * ------------------------------------------------------------------------ */
 void loca_oracle_projected_acc(int64_t n, int64_t d, int64_t r, const double* X, const double* T,
-                               const double* Aproj, const double* Bcur, double* G, double* Cst) {
+                               const double* Aproj, const double* Bcur, const double* a_w, double* G,
+                               double* Cst) {
   double* P = (double*)malloc(sizeof(double) * (size_t)n * (size_t)r);
   double* Rho = (double*)malloc(sizeof(double) * (size_t)n * (size_t)d);
 #pragma omp parallel for schedule(static)
@@ -453,14 +466,14 @@ void loca_oracle_projected_acc(int64_t n, int64_t d, int64_t r, const double* X,
   for (int64_t a = 0; a < r; ++a)
     for (int64_t b = 0; b < r; ++b) {
       double s = 0.0;
-      for (int64_t t = 0; t < n; ++t) s += P[IDX(t, a, r)] * P[IDX(t, b, r)];
+      for (int64_t t = 0; t < n; ++t) s += (a_w ? a_w[t] : 1.0) * P[IDX(t, a, r)] * P[IDX(t, b, r)];
       G[IDX(a, b, r)] += s;
     }
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < d; ++i)
     for (int64_t a = 0; a < r; ++a) {
       double s = 0.0;
-      for (int64_t t = 0; t < n; ++t) s += Rho[IDX(t, i, d)] * P[IDX(t, a, r)];
+      for (int64_t t = 0; t < n; ++t) s += (a_w ? a_w[t] : 1.0) * Rho[IDX(t, i, d)] * P[IDX(t, a, r)];
       Cst[IDX(i, a, r)] += s;
     }
   free(P);
