@@ -92,6 +92,9 @@ typedef void* loca_stream_t; /* hipStream_t */
  *   loca_dense_targets).
  * logits : n x C (ld_logits >= C), F32 or BF16, shared by all blocks.
  * labels : n int32 in [0, C).       w : n float loss weights, or NULL (= 1).
+ * a_w : n float statistic weights a_t >= 0 (the weighted statistics of Section S7),
+ *       or NULL (= 1); the same array is passed to loca_accumulate_stats.  Then
+ *       sum_q2 = sum_t a_t ||Q_t||^2 (the mean squares of Eq. 10 under the weights).
  * credit_a : per block C x k (F32 or BF16), stride a_bstride.
  * credit_b : per block k x d float, stride b_bstride.
  * y_out : per block n x k float, stride y_bstride.
@@ -104,31 +107,38 @@ typedef void* loca_stream_t; /* hipStream_t */
 loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k,
                                int64_t d, const void* logits, loca_dtype logits_dtype,
                                int64_t ld_logits, const int32_t* labels, const float* w,
-                               const void* credit_a, loca_dtype a_dtype, int64_t a_bstride,
+                               const float* a_w, const void* credit_a, loca_dtype a_dtype,
+                               int64_t a_bstride,
                                const float* credit_b, int64_t b_bstride, float* y_out,
                                int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info,
                                void* ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------------------
  * (a3, a4) Streaming statistics of one micro-batch (Eq. 9; Section S7):
- *   S_b += X_b^T X_b                (d x d; the upper triangle j >= i is
+ *   S_b += X_b^T diag(a) X_b        (d x d; the upper triangle j >= i is
  *                                    maintained, entries below it are
  *                                    unspecified and never read),
- *   mb[b].sum_x2 = ||X_b||_F^2,  mb[b].eta_bar = eta sqrt(sum_x2/sum_q2) (Eq. 10),
- *   K_b += -eta_bar X_b^T Y_b       (d x k).
+ *   mb[b].sum_x2 = sum_t a_t ||x_t||^2,  mb[b].eta_bar = eta sqrt(sum_x2/sum_q2) (Eq. 10),
+ *   K_b += -eta_bar X_b^T diag(a) Y_b   (d x k),
+ * with the statistic weights a (Section S7's weighted form; a = 1 when a_w is NULL).
  * The caller zeroes S and K before the first micro-batch.  Each mini-batch
  * uses its own eta_bar (Section S8).
  * x : per block n x d, ldx >= d, x_bstride; BF16 (then acc = F32) or F32
  *     (then acc = F64).  BF16 requires ldx % 8 == 0 and a 16-byte aligned
  *     base; F32 requires ldx % 4 == 0 and 16-byte alignment.
  * y : per block n x k float (from loca_error_targets), y_bstride.
+ * a_w : n float weights a_t >= 0 shared by the blocks, or NULL; it must be the
+ *       array given to loca_error_targets for this micro-batch.  In bf16 mode each
+ *       product a_t x_tj enters the matrix cores as two bf16 parts (about 16
+ *       significant bits), at twice the matrix-core work of the unweighted call.
  * mb : in: sum_q2; out: sum_x2, eta_bar, n.   eta >= 0.
  * S, K : per block, type `acc`, strides s_bstride, k_bstride.
  * Limits: k <= 128.
  * ------------------------------------------------------------------------- */
 loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, int64_t d, int64_t k,
                                   const void* x, loca_dtype x_dtype, int64_t ldx, int64_t x_bstride,
-                                  const float* y, int64_t y_bstride, double eta, loca_mb* mb,
+                                  const float* y, int64_t y_bstride, const float* a_w,
+                                  double eta, loca_mb* mb,
                                   void* S, void* K, loca_dtype acc, int64_t s_bstride,
                                   int64_t k_bstride, void* ws, size_t ws_bytes);
 

@@ -57,9 +57,9 @@ __global__ __launch_bounds__(256) void k_credit_gram(int64_t k, int64_t d, const
 template <typename LT, typename AT, int KB>
 __global__ __launch_bounds__(kSmallThreads) void k_error_small(
     int64_t n, int64_t C, int64_t k, const LT* __restrict__ logits, int64_t ld,
-    const int32_t* __restrict__ labels, const float* __restrict__ w, const AT* __restrict__ A,
-    int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out, int64_t y_bstride,
-    float* __restrict__ e_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
+    const int32_t* __restrict__ labels, const float* __restrict__ w, const float* __restrict__ aw,
+    const AT* __restrict__ A, int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out,
+    int64_t y_bstride, float* __restrict__ e_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
   __shared__ float sA[kSmallMaxC * KB];
   __shared__ double sG[KB * KB];
   __shared__ double sred[kSmallThreads / 64];
@@ -108,6 +108,7 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
           q += 2.0 * (double)y[a] * r;
         }
       }
+      if (aw) q *= (double)aw[t];  // statistic weight of the position
     }
   }
   const double tot = block_sum(q, sred);
@@ -125,9 +126,9 @@ constexpr int kLargeKPL = kMaxK / kLargeLPT;                // 8
 template <typename LT, typename AT>
 __global__ __launch_bounds__(kLargeThreads) void k_error_large(
     int64_t n, int64_t C, int64_t k, const LT* __restrict__ logits, int64_t ld,
-    const int32_t* __restrict__ labels, const float* __restrict__ w, const AT* __restrict__ A,
-    int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out, int64_t y_bstride,
-    float* __restrict__ ms_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
+    const int32_t* __restrict__ labels, const float* __restrict__ w, const float* __restrict__ aw,
+    const AT* __restrict__ A, int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out,
+    int64_t y_bstride, float* __restrict__ ms_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
   constexpr int LPT = kLargeLPT;
   __shared__ float sZ[kLargeTok][kLargeChunk];
   __shared__ float sAc[kLargeChunk][kMaxK];
@@ -209,6 +210,7 @@ __global__ __launch_bounds__(kLargeThreads) void k_error_large(
       for (int c = 0; c < k; ++c) r += Gb[a2 * k + c] * (double)sY[tk][c];
       qv += (double)sY[tk][a2] * r;
     }
+    if (aw) qv *= (double)aw[t];  // statistic weight of the position
   }
   const double tot = block_sum(qv, sred);
   if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
@@ -266,7 +268,7 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
     dim3 grid((unsigned)((a.n + kSmallThreads - 1) / kSmallThreads), (unsigned)a.nb);
 #define LOCA_SMALL(KB)                                                                              \
   k_error_small<LT, AT, KB><<<grid, kSmallThreads, 0, a.stream>>>(                                  \
-      a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, A, a.a_bstride, G, a.y_out, a.y_bstride, a.e_out, \
+      a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, a.a_w, A, a.a_bstride, G, a.y_out, a.y_bstride, a.e_out, \
       partial, a.dev_info)
     if (a.k <= 16) LOCA_SMALL(16);
     else if (a.k <= 32) LOCA_SMALL(32);
@@ -278,7 +280,7 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
   } else {
     dim3 grid((unsigned)((a.n + kLargeTok - 1) / kLargeTok), (unsigned)a.nb);
     k_error_large<LT, AT><<<grid, kLargeThreads, 0, a.stream>>>(
-        a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, A, a.a_bstride, G, a.y_out, a.y_bstride,
+        a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, a.a_w, A, a.a_bstride, G, a.y_out, a.y_bstride,
         a.e_out ? ms : nullptr, partial, a.dev_info);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -15,6 +15,13 @@
 // two halves carries ~16 bits of y.  Every output element is owned by one
 // workgroup and summed in a fixed order: results are deterministic.
 //
+// Statistic weights a_t (Section S7's weighted form, S = X^T diag(a) X): in bf16 mode
+// the second operand of every Gram product is scaled in registers, a_t x_tj as a
+// float, and enters the matrix cores as two bf16 parts hi + lo (about 16 significant
+// bits), so the weighted call does twice the MFMA work; the first operand stays the
+// exact bf16 X.  The result is symmetric up to that rounding and only its upper
+// triangle is formed, as without weights.
+//
 // fp32 mode: X is fp32 and the statistics are fp64 (v_mfma_f64_16x16x4f64).
 #include <algorithm>
 
@@ -33,6 +40,42 @@ LOCA_DEV void upper_tile(int u, int T, int& I, int& J) {
   while (u >= T - i) { u -= T - i; ++i; }
   I = i;
   J = i + u;
+}
+
+// ------------------------------------------------------------------ statistic weights (bf16 mode)
+
+// A Gram operand of lane l holds 8 consecutive tokens ks + 8 (l / 32) + e, e = 0..7, of
+// one column.  weight_split scales them by the lanes' weights and splits each float
+// product into bf16 hi and lo parts.
+LOCA_DEV void weight_split(bf16x8_t b, const float (&w)[8], bf16x8_t& hi, bf16x8_t& lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const float f = (float)b[e] * w[e];
+    const __bf16 h = (__bf16)f;  // round to nearest even
+    hi[e] = h;
+    lo[e] = (__bf16)(f - (float)h);
+  }
+}
+
+typedef int32_t i32x16_t __attribute__((ext_vector_type(16)));
+// Sixteen consecutive floats at the wave-uniform address p into scalar registers,
+// asynchronously: sload_wait must run before the values are used.
+LOCA_DEV i32x16_t sload16(const float* p) {
+  i32x16_t v;
+  asm volatile("s_load_dwordx16 %0, %1, 0x0" : "=s"(v) : "s"(p));
+  return v;
+}
+// Waits for the outstanding scalar (and LDS) loads.  The values pass through the
+// statement, so no use of them can be scheduled ahead of the wait.
+LOCA_DEV void sload_wait(i32x16_t& v) { asm volatile("s_waitcnt lgkmcnt(0)" : "+s"(v)::"memory"); }
+// The weights of a lane's 8 operand tokens from those of 16 consecutive tokens, as a
+// bit select with a per-lane mask (kept opaque so that it is not rewritten into an
+// indexed read of the 16 values).
+LOCA_DEV void lane_weights(const i32x16_t& v, int lane, float (&w)[8]) {
+  int m = -(lane >> 5);  // 0 for lanes 0..31, all ones for lanes 32..63
+  asm("" : "+v"(m));
+#pragma unroll
+  for (int e = 0; e < 8; ++e) w[e] = __int_as_float((v[e] & ~m) | (v[8 + e] & m));
 }
 
 // ------------------------------------------------------------------ bf16 tile staging
@@ -93,11 +136,13 @@ struct XStage {
 
 // BM x BM tiles of S on or above the diagonal; WGM x WGN waves, each owning a
 // (BM/WGM) x (BM/WGN) block of 32 x 32 MFMA tiles.
-template <int BM, int WGM, int WGN>
+// WT: statistic weights from `wpad` (zero past n, readable up to the next multiple of kBK).
+template <int BM, int WGM, int WGN, bool WT>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16(int64_t n, int64_t d,
                                                              const uint16_t* __restrict__ Xall, int64_t ldx,
                                                              int64_t x_bstride, float* __restrict__ Sall,
-                                                             int64_t s_bstride, double* __restrict__ diag_part) {
+                                                             int64_t s_bstride, double* __restrict__ diag_part,
+                                                             const float* __restrict__ wpad) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN;
   constexpr int NBM = WM / 32, NBN = WN / 32;
@@ -147,14 +192,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16(int64_t n, int64_t
       const uint16_t* tB = diag ? sA[cur] : sB[cur];
 #pragma unroll
       for (int ks = 0; ks < kBK; ks += 16) {
-        bf16x8_t fb[NBN];
+        bf16x8_t fb[NBN], fl[NBN];
 #pragma unroll
         for (int q = 0; q < NBN; ++q) fb[q] = frag32_tr(tB, LDT, wj * WN + 32 * q, ks, lane);
+        if (WT) {
+          const float* wl = wpad + (int64_t)kt * kBK + ks + 8 * (lane >> 5);
+          const float4 w0 = *(const float4*)wl, w1 = *(const float4*)(wl + 4);
+          const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+          for (int q = 0; q < NBN; ++q) weight_split(fb[q], wv, fb[q], fl[q]);
+        }
 #pragma unroll
         for (int m = 0; m < NBM; ++m) {
           const bf16x8_t fa = frag32_tr(tA, LDT, wi * WM + 32 * m, ks, lane);
 #pragma unroll
           for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa, fb[q], acc[m][q]);
+          if (WT)
+#pragma unroll
+            for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa, fl[q], acc[m][q]);
         }
       }
     }
@@ -275,13 +330,19 @@ LOCA_DEV int xcd_logical(int L, int total) {
 // (n x w2p bf16 per block, w2p = 2k rounded up to 8 <= 64) instead of a second copy of
 // its panel, and its two waves that lie below the diagonal (no Gram output) form
 // Kraw = X_I^T [Y_hi | Y_lo] for the panel's 256 columns, 128 each.
-template <int WGM, int WGN, bool BUF>
+//
+// WT: statistic weights, padded in `wpad` (zero past n, readable up to kBK floats past
+// the last stage).  The weights of each half stage reach scalar registers one half
+// stage ahead of use; the second operand (X_J, or the split targets of a cross wave)
+// is then scaled and split in registers, and each row of MFMAs runs on both parts.
+template <int WGM, int WGN, bool BUF, bool WT>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
                                                                 int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
                                                                 int64_t s_bstride, double* __restrict__ diag_part,
                                                                 const uint16_t* __restrict__ zero16, int64_t b0,
                                                                 const uint16_t* __restrict__ Yhl_all, int64_t w2,
-                                                                int64_t w2p, float* __restrict__ Kraw_all) {
+                                                                int64_t w2p, float* __restrict__ Kraw_all,
+                                                                const float* __restrict__ wpad) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -371,16 +432,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   // MFMAs behind them.  Every wave runs the same instruction stream (waves of a
   // diagonal tile below its diagonal compute too and only skip the write-back), so
   // the loop has no divergent branches.
-  bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN];
+  bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN], fl0[NBN], fl1[NBN];
   auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
 #pragma unroll
     for (int q = 0; q < NBN; ++q) fb[q] = frag32_tr_swz(buf + boff, bcol0 + 32 * q, ks, lane);
 #pragma unroll
     for (int m = 0; m < NBM; ++m) fa[m] = frag32_tr_swz(buf, arow0 + 32 * m, ks, lane);
   };
-  auto mma_row = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN], int m) {
+  auto mma_row = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN], const bf16x8_t (&fl)[NBN], int m) {
 #pragma unroll
     for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa[m], fb[q], acc[m][q]);
+    if (WT)
+#pragma unroll
+      for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa[m], fl[q], acc[m][q]);
+  };
+  i32x16_t wsc;
+  if (WT) wsc = sload16(wpad);  // half stage 0 of stage 0
+  // scale and split the second operands with the weights loaded one half stage ago,
+  // and start the load of the next half stage's weights
+  auto weigh = [&](bf16x8_t (&fb)[NBN], bf16x8_t (&fl)[NBN], const float* next) {
+    sload_wait(wsc);
+    float wv[8];
+    lane_weights(wsc, lane, wv);
+    wsc = sload16(next);
+#pragma unroll
+    for (int q = 0; q < NBN; ++q) weight_split(fb[q], wv, fb[q], fl[q]);
   };
   auto step = [&](uint16_t* cur, uint16_t* nxt, uint16_t* fill, int kt) {
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(NCP));  // stage kt + 1 landed (this thread's copies)
@@ -392,10 +468,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
         issue(fill, kt + kDLStages - 1, sl * NCP / NSLOT);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (sl == 0) load_frags(cur, 16, fa1, fb1);
-      if (sl == NBM) load_frags(nxt, 0, fa0, fb0);
-      if (sl < NBM) mma_row(fa0, fb0, sl);
-      else mma_row(fa1, fb1, sl - NBM);
+      if (sl == 0) {
+        if (WT) weigh(fb0, fl0, wpad + (int64_t)kt * kBK + 16);
+        load_frags(cur, 16, fa1, fb1);
+      }
+      if (sl == NBM) {
+        if (WT) weigh(fb1, fl1, wpad + (int64_t)(kt + 1) * kBK);
+        load_frags(nxt, 0, fa0, fb0);
+      }
+      if (sl < NBM) mma_row(fa0, fb0, fl0, sl);
+      else mma_row(fa1, fb1, fl1, sl - NBM);
     }
   };
   // stages past nk read zeros: harmless
@@ -469,7 +551,8 @@ template <int YB>
 __global__ __launch_bounds__(kThreads) void k_cross_bf16(int64_t n, int64_t d, int64_t k,
                                                          const uint16_t* __restrict__ Xall, int64_t ldx,
                                                          int64_t x_bstride, const float* __restrict__ Yall,
-                                                         int64_t y_bstride, float* __restrict__ Kraw) {
+                                                         int64_t y_bstride, float* __restrict__ Kraw,
+                                                         const float* __restrict__ aw) {
   constexpr int BM = 256;
   constexpr int LDT = BM + 16;
   constexpr int LDY = YB + 16;
@@ -503,7 +586,9 @@ __global__ __launch_bounds__(kThreads) void k_cross_bf16(int64_t n, int64_t d, i
       const int row = e / YB, c = e % YB;
       const int64_t t = t0 + row;
       const int cc = c < k ? c : c - (int)k;
-      v[q] = ld_or_zero(Y, t * k + cc, e < kBK * YB && t < n && c < 2 * k);
+      const bool ok = e < kBK * YB && t < n && c < 2 * k;
+      v[q] = ld_or_zero(Y, t * k + cc, ok);
+      if (aw) v[q] *= ld_or_zero(aw, t, ok);  // statistic weight, before the split
     }
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
@@ -566,7 +651,8 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
                                                        int64_t x_bstride, const float* __restrict__ Yall,
                                                        int64_t y_bstride, double* __restrict__ Sall,
                                                        int64_t s_bstride, double* __restrict__ Kraw,
-                                                       double* __restrict__ diag_part, int nS) {
+                                                       double* __restrict__ diag_part, int nS,
+                                                       const float* __restrict__ aw) {
   __shared__ double sP[kBK64 * kLD64];
   __shared__ double sQ[kBK64 * kLD64];
   __shared__ double sred[kThreads / 64];
@@ -604,7 +690,10 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
       const int64_t ci = cI + c, cj = cJ + c;
       sP[row * kLD64 + c] = (t < n && ci < d) ? (double)X[t * ldx + ci] : 0.0;
       double qv = 0.0;
-      if (t < n && cj < qcols) qv = kjob ? (double)Y[t * k + cj] : (double)X[t * ldx + cj];
+      if (t < n && cj < qcols) {
+        qv = kjob ? (double)Y[t * k + cj] : (double)X[t * ldx + cj];
+        if (aw) qv *= (double)aw[t];  // statistic weight (an exact product in fp64)
+      }
       sQ[row * kLD64 + c] = qv;
     }
     __syncthreads();
@@ -698,13 +787,32 @@ __global__ void k_split_y(int64_t n, int64_t k, int64_t w2p, const float* __rest
   Yhl[b * n * w2p + e] = v;
 }
 
+// wpad[i] = a_w[i] for i < n, 0 up to npad (the padded weights of the bf16 Gram kernels)
+__global__ void k_pad_weights(int64_t n, int64_t npad, const float* __restrict__ aw, float* __restrict__ wpad) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < npad) wpad[i] = i < n ? aw[i] : 0.f;
+}
+
+// padded length of the weights: every stage the kernels compute, plus one stage of look-ahead
+static int64_t weights_pad(int64_t n) { return ((n + kBK - 1) / kBK + 1) * kBK; }
+
 size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc) {
   const int64_t T = acc == LOCA_F64 ? (d + kBM64 - 1) / kBM64 : (d + 127) / 128;
   const int64_t Tmax = (d + kBM64 - 1) / kBM64;  // generous: covers every tile size used
   size_t s = 256 + align256(sizeof(double) * nb * (T > Tmax ? T : Tmax));  // zeros + tile partials
   if (acc == LOCA_F64) s += align256(sizeof(double) * nb * d * k);
-  else s += align256(sizeof(float) * nb * d * 2 * k) + align256(sizeof(uint16_t) * nb * n * ((2 * k + 7) / 8 * 8));
+  else s += align256(sizeof(float) * nb * d * 2 * k) + align256(sizeof(uint16_t) * nb * n * ((2 * k + 7) / 8 * 8)) +
+            align256(sizeof(float) * weights_pad(n));
   return s;
+}
+
+template <bool BUF, bool WT>
+static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_t nbc, const uint16_t* zero16,
+                           double* diag_part, const uint16_t* Yhl, int64_t w2, int64_t w2p, float* Kraw,
+                           const float* wpad) {
+  k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
+      a.n, a.d, (const uint16_t*)a.x, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, Yhl, w2,
+      w2p, Kraw, wpad);
 }
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {
@@ -719,7 +827,7 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     const int nK = T * (int)((a.k + kBM64 - 1) / kBM64);
     dim3 grid((unsigned)(nS + nK), (unsigned)a.nb);
     k_gram_f64<<<grid, kThreads, 0, a.stream>>>(a.n, a.d, a.k, (const float*)a.x, a.ldx, a.x_bstride, a.y,
-                                                a.y_bstride, (double*)a.S, a.s_bstride, Kraw, diag_part, nS);
+                                                a.y_bstride, (double*)a.S, a.s_bstride, Kraw, diag_part, nS, a.a_w);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
@@ -729,15 +837,27 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   }
   float* Kraw = (float*)p;
   uint16_t* Yhl = (uint16_t*)(p + align256(sizeof(float) * a.nb * a.d * 2 * a.k));
+  float* wpad = (float*)((char*)Yhl + align256(sizeof(uint16_t) * a.nb * a.n * ((2 * a.k + 7) / 8 * 8)));
   const uint16_t* X = (const uint16_t*)a.x;
+  const bool wt = a.a_w != nullptr;
+  if (wt) {
+    const int64_t npad = weights_pad(a.n);
+    k_pad_weights<<<(unsigned)((npad + 255) / 256), 256, 0, a.stream>>>(a.n, npad, a.a_w, wpad);
+  }
   // Tile size: 256 x 256 when the matrix is wide enough to fill the GPU with such tiles.
   const bool big = a.d >= 1024;
   const int BM = big ? 256 : 128;
   const int T = (int)((a.d + BM - 1) / BM);
   dim3 grid((unsigned)(T * (T + 1) / 2), (unsigned)a.nb);
   const int64_t w2 = 2 * a.k, w2p = (w2 + 7) / 8 * 8;
-  const bool fused = big && (a.d % 8) == 0 && w2p <= 64;
-  if (big && (a.d % 8) == 0) {
+  // buffer-path copies when a block's X (and its split targets) fit 31-bit byte offsets
+  const bool buf = (a.n * a.ldx * 2) < ((int64_t)1 << 31);
+  // direct-to-LDS kernel; with weights only on the buffer path (the global-address
+  // variant runs out of scalar registers with the weights, so blocks of X over 2 GB
+  // take the register-staged kernel when weighted)
+  const bool dl = big && (a.d % 8) == 0 && (buf || !wt);
+  const bool fused = dl && w2p <= 64;
+  if (dl) {
     if (fused) {
       dim3 gy((unsigned)((a.n * w2p + 255) / 256), (unsigned)a.nb);
       k_split_y<<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
@@ -750,40 +870,43 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     const int64_t chunk = std::max<int64_t>(1, ((int64_t)1 << 22) / ntile);
     for (int64_t b0 = 0; b0 < a.nb; b0 += chunk) {
       const int64_t nbc = std::min<int64_t>(chunk, a.nb - b0);
-      // buffer-path copies when a block's X (and its split targets) fit 31-bit byte offsets
-      const bool buf = (a.n * a.ldx * 2) < ((int64_t)1 << 31);
-#ifdef LOCA_GRAM_GLOBAL_LOADS
-      const bool use_buf = false && buf;
-#else
       const bool use_buf = buf;
-#endif
-      if (use_buf)
-        k_gram_bf16_dl<2, 4, true><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
-            a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, fused ? Yhl : nullptr,
-            w2, w2p, Kraw);
-      else
-        k_gram_bf16_dl<2, 4, false><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
-            a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, fused ? Yhl : nullptr,
-            w2, w2p, Kraw);
+      const uint16_t* yf = fused ? Yhl : nullptr;
+      if (use_buf && wt) launch_gram_dl<true, true>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, wpad);
+      else if (use_buf) launch_gram_dl<true, false>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, nullptr);
+      else launch_gram_dl<false, false>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, nullptr);
     }
-  } else if (big)
-    k_gram_bf16<256, 2, 4><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
-                                                       diag_part);
-  else
-    k_gram_bf16<128, 2, 2><<<grid, 256, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride,
-                                                       diag_part);
+  } else if (big) {
+    if (wt)
+      k_gram_bf16<256, 2, 4, true><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
+                                                               a.s_bstride, diag_part, wpad);
+    else
+      k_gram_bf16<256, 2, 4, false><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
+                                                                a.s_bstride, diag_part, nullptr);
+  } else {
+    if (wt)
+      k_gram_bf16<128, 2, 2, true><<<grid, 256, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
+                                                               a.s_bstride, diag_part, wpad);
+    else
+      k_gram_bf16<128, 2, 2, false><<<grid, 256, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
+                                                                a.s_bstride, diag_part, nullptr);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gc((unsigned)((a.d + 255) / 256), (unsigned)a.nb);
   if (!fused) {  // the cross statistic in a launch of its own
     if (w2 <= 32)
-      k_cross_bf16<32><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+      k_cross_bf16<32><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw,
+                                                       a.a_w);
     else if (w2 <= 64)
-      k_cross_bf16<64><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+      k_cross_bf16<64><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw,
+                                                        a.a_w);
     else if (w2 <= 128)
-      k_cross_bf16<128><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+      k_cross_bf16<128><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw,
+                                                        a.a_w);
     else
-      k_cross_bf16<256><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw);
+      k_cross_bf16<256><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw,
+                                                        a.a_w);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -63,7 +63,8 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
 
 loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k, int64_t d,
                                const void* logits, loca_dtype logits_dtype, int64_t ld_logits,
-                               const int32_t* labels, const float* w, const void* credit_a, loca_dtype a_dtype,
+                               const int32_t* labels, const float* w, const float* a_w, const void* credit_a,
+                               loca_dtype a_dtype,
                                int64_t a_bstride, const float* credit_b, int64_t b_bstride, float* y_out,
                                int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info, void* ws,
                                size_t ws_bytes) {
@@ -77,14 +78,15 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
   if (k > kMaxK) return LOCA_E_UNSUPPORTED;
   loca_status st = check_ws(ws, ws_bytes, error_targets_ws(nb, n, C, k));
   if (st != LOCA_OK) return st;
-  ErrorArgs a{(hipStream_t)stream, nb, n, C, k, d, ld_logits, logits, logits_dtype, labels, w, credit_a, a_dtype,
+  ErrorArgs a{(hipStream_t)stream, nb, n, C, k, d, ld_logits, logits, logits_dtype, labels, w, a_w, credit_a, a_dtype,
               a_bstride, credit_b, b_bstride, y_out, y_bstride, e_out, mb_out, dev_info, (char*)ws};
   return from_hip(launch_error_targets(a));
 }
 
 loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, int64_t d, int64_t k, const void* x,
                                   loca_dtype x_dtype, int64_t ldx, int64_t x_bstride, const float* y,
-                                  int64_t y_bstride, double eta, loca_mb* mb, void* S, void* K, loca_dtype acc,
+                                  int64_t y_bstride, const float* a_w, double eta, loca_mb* mb, void* S, void* K,
+                                  loca_dtype acc,
                                   int64_t s_bstride, int64_t k_bstride, void* ws, size_t ws_bytes) {
   if (nb < 1 || n < 1 || d < 1 || k < 1) return LOCA_E_ARG;
   if (!x || !y || !mb || !S || !K) return LOCA_E_ARG;
@@ -101,7 +103,7 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
   if (nb > 65535 || d > 65535 * 64) return LOCA_E_UNSUPPORTED;
   loca_status st = check_ws(ws, ws_bytes, accumulate_stats_ws(nb, n, d, k, acc));
   if (st != LOCA_OK) return st;
-  StatsArgs a{(hipStream_t)stream, nb, n, d, k, x, x_dtype, ldx, x_bstride, y, y_bstride, eta, mb, S, K, acc,
+  StatsArgs a{(hipStream_t)stream, nb, n, d, k, x, x_dtype, ldx, x_bstride, y, y_bstride, a_w, eta, mb, S, K, acc,
               s_bstride, k_bstride, (char*)ws};
   return from_hip(launch_accumulate_stats(a));
 }

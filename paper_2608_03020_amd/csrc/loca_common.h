@@ -148,7 +148,7 @@ struct ErrorArgs {
   hipStream_t stream;
   int64_t nb, n, C, k, d, ld_logits;
   const void* logits; loca_dtype logits_dtype;
-  const int32_t* labels; const float* w;
+  const int32_t* labels; const float* w; const float* a_w;
   const void* credit_a; loca_dtype a_dtype; int64_t a_bstride;
   const float* credit_b; int64_t b_bstride;
   float* y_out; int64_t y_bstride;
@@ -162,7 +162,7 @@ struct StatsArgs {
   hipStream_t stream;
   int64_t nb, n, d, k;
   const void* x; loca_dtype x_dtype; int64_t ldx, x_bstride;
-  const float* y; int64_t y_bstride;
+  const float* y; int64_t y_bstride; const float* a_w;
   double eta; loca_mb* mb;
   void* S; void* K; loca_dtype acc; int64_t s_bstride, k_bstride;
   char* ws;

@@ -79,7 +79,8 @@ CONFIGS = {
 
 _CFG_ID = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # tensor ids inside a (config, block) key
-_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT, _T_WEIGHTS, _T_PROBE = range(11)
+(_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT, _T_WEIGHTS, _T_PROBE,
+ _T_STATW) = range(12)
 
 
 def custom_config(name="tiny", blocks=1, d=64, n=100, micro=None, C=5, k=8, r_a=4,
@@ -199,6 +200,16 @@ def gen_loss_weights(cfg: LocaConfig, micro: int, masked: float = 0.2, seed: int
     w = (2.0 * g.random(hi - lo)).astype(np.float32)
     w[g.random(hi - lo) < masked] = 0.0
     return w
+
+
+def gen_stat_weights(cfg: LocaConfig, micro: int, zero: float = 0.2, seed: int = 0) -> np.ndarray:
+    """Per-position statistic weights a_t >= 0 of micro-batch `micro` (float32):
+    uniform on [0, 2) with a fraction `zero` of positions at 0 (dropped positions)."""
+    g = _rng(seed, cfg, 0, _T_STATW, micro)
+    lo, hi = cfg.micro_rows(micro)
+    a = (2.0 * g.random(hi - lo)).astype(np.float32)
+    a[g.random(hi - lo) < zero] = 0.0
+    return a
 
 
 def gen_probe_pairs(cfg: LocaConfig, n_p: int, blocks: int, rank: int = 0, noise: float = 2.0, seed: int = 0):

@@ -51,10 +51,10 @@ def load():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"libloca is not built ({LIB_PATH}); run paper_2608_03020_amd/build.py")
     lib = ctypes.CDLL(LIB_PATH)
-    lib.loca_error_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _I, _I64,
-                                       _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
-    lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _D, _VP,
-                                          _VP, _VP, _I, _I64, _I64, _VP, _SZ]
+    lib.loca_error_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _VP, _I,
+                                       _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
+    lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _VP, _D,
+                                          _VP, _VP, _VP, _I, _I64, _I64, _VP, _SZ]
     lib.loca_ridge_solve.argtypes = [_VP, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _VP, _I64, _I64, _I64,
                                      _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
     lib.loca_lowrank_truncate.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _I64, _VP, _I64, _VP,
@@ -145,27 +145,30 @@ def mb_view(mb):
 # ------------------------------------------------------------------ entry points
 
 
-def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_info, ws, *, w=None, e_out=None,
-                       nb=None, stream=None):
-    """logits (n, C); labels (n,); credit_a (nb, C, k); credit_b (nb, k, d); y_out (nb, n, k)."""
+def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_info, ws, *, w=None, a_w=None,
+                       e_out=None, nb=None, stream=None):
+    """logits (n, C); labels (n,); credit_a (nb, C, k); credit_b (nb, k, d); y_out (nb, n, k);
+    w (n,) loss weights and a_w (n,) statistic weights, float32, optional."""
     nb = nb or credit_a.shape[0]
     n, C = logits.shape[0], logits.shape[1]
     k, d = credit_b.shape[-2], credit_b.shape[-1]
     st = load().loca_error_targets(
         _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
-        _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
+        _ptr(a_w), _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
         credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(y_out), y_out.stride(0) if y_out.dim() == 3 else 0,
         _ptr(e_out), _ptr(mb_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_error_targets", st)
 
 
-def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, stream=None):
-    """x (nb, n, d) bf16 or fp32 (row stride may exceed d); y (nb, n, k); S (nb, d, d); K (nb, d, k)."""
+def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, stream=None):
+    """x (nb, n, d) bf16 or fp32 (row stride may exceed d); y (nb, n, k); S (nb, d, d); K (nb, d, k);
+    a_w (n,) float32 statistic weights, the array given to loca_error_targets (optional)."""
     nb, n, d = x.shape
     k = y.shape[-1]
     acc = _dtype(S)
     st = load().loca_accumulate_stats(
-        _stream(stream), nb, n, d, k, _ptr(x), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), float(eta),
+        _stream(stream), nb, n, d, k, _ptr(x), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), _ptr(a_w),
+        float(eta),
         _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_accumulate_stats", st)
 

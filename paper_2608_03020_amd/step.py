@@ -60,13 +60,14 @@ class BlockStep:
         self.K.zero_()
         self.mb_log = []
 
-    def micro_batch(self, x_m, logits_m, labels_m, credit_a, credit_b, keep_log=False, stream=None, w=None):
-        """Rows a1-a4 for one micro-batch: x_m (nb, n_m, d); w (n_m,) optional loss weights."""
+    def micro_batch(self, x_m, logits_m, labels_m, credit_a, credit_b, keep_log=False, stream=None, w=None, a=None):
+        """Rows a1-a4 for one micro-batch: x_m (nb, n_m, d); w (n_m,) optional loss weights;
+        a (n_m,) optional statistic weights (Section S7's weighted statistics)."""
         n_m = x_m.shape[1]
         y = self.Y[:, :n_m]
-        loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info, self.ws, w=w,
+        loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info, self.ws, w=w, a_w=a,
                                 nb=self.nb, stream=stream)
-        loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, stream=stream)
+        loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, a_w=a, stream=stream)
         if keep_log:
             self.mb_log.append(self.mb.clone())
 

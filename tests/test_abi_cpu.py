@@ -60,13 +60,13 @@ FAKE = 0x100000  # never dereferenced: every call below fails validation first
 def test_error_targets_rejects(lib):
     so = lib.load()
     ok_args = dict(stream=None, nb=1, n=8, C=4, k=2, d=16, logits=FAKE, ldt=lib.LOCA_F32, ld=4, labels=FAKE, w=None,
-                   a=FAKE, adt=lib.LOCA_F32, abs_=0, b=FAKE, bbs=0, y=FAKE, ybs=0, e=None, mb=FAKE, info=FAKE,
+                   aw=None, a=FAKE, adt=lib.LOCA_F32, abs_=0, b=FAKE, bbs=0, y=FAKE, ybs=0, e=None, mb=FAKE, info=FAKE,
                    ws=None, wsb=0)
 
     def call(**kw):
         a = dict(ok_args, **kw)
         return so.loca_error_targets(a["stream"], a["nb"], a["n"], a["C"], a["k"], a["d"], a["logits"], a["ldt"],
-                                     a["ld"], a["labels"], a["w"], a["a"], a["adt"], a["abs_"], a["b"], a["bbs"],
+                                     a["ld"], a["labels"], a["w"], a["aw"], a["a"], a["adt"], a["abs_"], a["b"], a["bbs"],
                                      a["y"], a["ybs"], a["e"], a["mb"], a["info"], a["ws"], a["wsb"])
 
     assert call(n=0) == lib.LOCA_E_ARG
@@ -82,11 +82,11 @@ def test_error_targets_rejects(lib):
 
 def test_accumulate_stats_rejects(lib):
     so = lib.load()
-    base = [None, 1, 64, 32, 4, FAKE, lib.LOCA_BF16, 32, 0, FAKE, 0, 0.01, FAKE, FAKE, FAKE, lib.LOCA_F32, 0, 0,
-            None, 0]
+    base = [None, 1, 64, 32, 4, FAKE, lib.LOCA_BF16, 32, 0, FAKE, 0, None, 0.01, FAKE, FAKE, FAKE, lib.LOCA_F32,
+            0, 0, None, 0]
 
     def call(**kw):
-        idx = dict(nb=1, n=2, d=3, k=4, x=5, xdt=6, ldx=7, xbs=8, eta=11, S=13, acc=15)
+        idx = dict(nb=1, n=2, d=3, k=4, x=5, xdt=6, ldx=7, xbs=8, eta=12, S=14, acc=16)
         a = list(base)
         for key, v in kw.items():
             a[idx[key]] = v
