@@ -73,6 +73,9 @@ def parse():
     p.add_argument("--blocks", type=int, default=0, help="override the block count (profiling runs)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-tokens", type=int, default=0, help="tokens in the CPU-baseline sample")
+    p.add_argument("--next", action="store_true",
+                   help="also time the widened rows (weighted statistics, outer step with a current adapter, "
+                        "Stage I calibration) on the same workload")
     return p.parse_args()
 
 
@@ -94,23 +97,170 @@ def make_inputs(cfg, nb, device="cuda"):
     return x_all, z, y, torch.stack(A), torch.stack(B)
 
 
-def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None):
+def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, lp=None, rp=None,
+             solve_record=None):
     """One step of the whole path over every block: per micro-batch the head error
     and credit coordinates, then the statistics (bracketed by the events of
-    `record[m]` when given); then the ridge solves and the truncation."""
+    `record[m]` when given); then the ridge solves and the truncation (bracketed by
+    `solve_record`).  Optional: statistic weights a_all (n,), a current adapter
+    lp (nb, d, r_prev), rp (nb, r_prev, d)."""
     from paper_2608_03020_amd import loca
     step.reset()
     for m in range(cfg.n_micro):
         lo, hi = cfg.micro_rows(m)
         xm = x_all[:, lo:hi]
         yv = step.Y[:, :hi - lo]
-        loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, nb=nb)
+        aw = None if a_all is None else a_all[lo:hi]
+        loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, a_w=aw, nb=nb)
         if record is not None:
             record[m][0].record(stream)
-        loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws)
+        loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws, a_w=aw)
         if record is not None:
             record[m][1].record(stream)
-    step.solve(B)
+    if solve_record is not None:
+        solve_record[0].record(stream)
+    step.solve(B, lp=lp, rp=rp)
+    if solve_record is not None:
+        solve_record[1].record(stream)
+
+
+def stats_flops(cfg, nb):
+    """Algorithmic flops of every statistics call of one step (d(d+1) + 2dk per token and block)."""
+    rows = [cfg.micro_rows(m)[1] - cfg.micro_rows(m)[0] for m in range(cfg.n_micro)]
+    return [nb * (r * cfg.d * (cfg.d + 1) + 2 * r * cfg.d * cfg.k) for r in rows]
+
+
+def solve_flops(cfg, nb, r_prev):
+    """Algorithmic flops of the ridge solves of one step: per block and lambda the Cholesky
+    d^3/3, the right-hand sides S Lp (2 d^2 r_prev) and the two triangular solves (2 d^2 kp)."""
+    d, kp = cfg.d, r_prev + cfg.k
+    return nb * len(cfg.lambdas) * (d ** 3 / 3.0 + 2.0 * d * d * r_prev + 2.0 * d * d * kp)
+
+
+def time_steps(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn(0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(steps):
+        fn(s)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream):
+    """The widened rows on the same workload and inputs: statistic weights on every
+    micro-batch (Section S7's weighted form), the outer step past the first with a
+    rank-r_a current adapter (Theorem S6.1), and the Stage I calibration of all blocks
+    from 64 probe pairs (Section S5).  Each with its time and the roofline of the call
+    that dominates it."""
+    import numpy as np
+    import torch
+    from paper_2608_03020_amd import inputs as gen
+    from paper_2608_03020_amd import loca
+    from paper_2608_03020_amd.step import BlockStep
+    out = {}
+    steps = max(1, min(args.steps, 5))
+    n_mb = cfg.n_micro
+    peak = FP64_PEAK_TFLOPS if cfg.mode == "fp32" else BF16_PEAK_TFLOPS
+
+    # weighted statistics: same workload, a_t uniform on [0, 2) with 20% zeros
+    a_all = gen.torch_gen_stat_weights(cfg)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps * n_mb)]
+    ms = time_steps(lambda s: run_step(step, cfg, nb, x_all, z, y, A, B, stream,
+                                       ev[s * n_mb:(s + 1) * n_mb] if s < steps else None, a_all=a_all),
+                    steps, 1)
+    t_avg = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    f_avg = sum(stats_flops(cfg, nb)) / n_mb
+    ach = f_avg / (t_avg * 1e-3) / 1e12
+    out["weighted_statistics"] = {
+        "ms_per_step": ms, "value": nb * cfg.n / (ms * 1e-3), "unit": "tokens/s per block",
+        "weights": "a_t uniform on [0, 2), 20% zero, every micro-batch",
+        "roofline": {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+                     "traffic": None, "kernel": "loca_accumulate_stats with statistic weights (all blocks, one micro-batch)",
+                     "algorithmic_flops_per_launch": f_avg, "avg_launch_ms": t_avg}}
+    print(f"[bench] next: weighted statistics {ms:.2f} ms/step", file=sys.stderr, flush=True)
+    del a_all
+
+    # outer step with a current adapter W_prev = Lp Rp of rank r_a
+    r_prev = cfg.r_a
+    if r_prev + cfg.k <= 64:
+        lp, rp = gen.torch_gen_current_adapter(cfg, nb, r_prev)
+        step2 = BlockStep(cfg, nb, torch.device("cuda:0"), r_prev=r_prev)
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        ms = time_steps(lambda s: run_step(step2, cfg, nb, x_all, z, y, A, B, stream, lp=lp, rp=rp,
+                                           solve_record=sev[s] if s < steps else None), steps, 1)
+        t_solve = sum(a.elapsed_time(b) for a, b in sev) / len(sev)
+        fl = solve_flops(cfg, nb, r_prev)
+        ach = fl / (t_solve * 1e-3) / 1e12
+        pk = FP64_PEAK_TFLOPS if cfg.mode == "fp32" else 157.3
+        out["outer_step_current_adapter"] = {
+            "ms_per_step": ms, "value": nb * cfg.n / (ms * 1e-3), "unit": "tokens/s per block", "r_prev": r_prev,
+            "roofline": {"bound": "mfma", "achieved": ach, "peak": pk, "unit": "TFLOP/s", "frac": ach / pk,
+                         "traffic": None,
+                         "kernel": "ridge solves (all blocks and lambdas, right-hand sides [S Lp | K]) and truncation",
+                         "algorithmic_flops_per_launch": fl, "avg_launch_ms": t_solve}}
+        print(f"[bench] next: outer step {ms:.2f} ms/step (solve + truncation {t_solve:.2f} ms)", file=sys.stderr,
+              flush=True)
+        del step2, lp, rp
+        torch.cuda.empty_cache()
+
+    # Stage I calibration of every block from 64 probe pairs
+    n_p, k, V = 64, cfg.k, cfg.C
+    E, G = gen.torch_gen_probe_pairs(cfg, n_p, nb)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(7)
+    Wu = torch.randn((V, cfg.d), generator=g, device="cuda", dtype=torch.float32) / np.sqrt(cfg.d)
+    bt = torch.empty((nb, k, cfg.d), dtype=torch.float32, device="cuda")
+    at = torch.empty((nb, V, k), dtype=torch.float32, device="cuda")
+    sig = torch.empty((nb, n_p), dtype=torch.float32, device="cuda")
+    alpha = torch.empty(nb, dtype=torch.float64, device="cuda")
+    info = torch.empty(nb, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_FEEDBACK_FIT, nb, n_p, cfg.d, k), "cuda")
+    reps = 20
+    cev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+
+    def calib(s):
+        if s < reps:
+            cev[s][0].record(stream)
+        loca.loca_feedback_fit(E, G, 0.05, bt, sig, alpha, info, ws, wu=Wu, at_out=at)
+        if s < reps:
+            cev[s][1].record(stream)
+    time_steps(calib, reps, 2)
+    t_cal = sum(a.elapsed_time(b) for a, b in cev) / reps
+    nbytes = 4.0 * (cfg.d * n_p + nb * cfg.d * n_p + nb * k * cfg.d + nb * V * k + V * cfg.d)
+    gbs = nbytes / (t_cal * 1e-3) / 1e9
+    cal = {"ms_per_call": t_cal, "unit": "ms per calibration of all blocks", "higher_is_better": False,
+           "config": {"blocks": nb, "d": cfg.d, "probes": n_p, "credit_rank": k, "head_rows": V, "beta": 0.05},
+           "alpha_mean": float(alpha.mean().item()),
+           "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                        "traffic": None, "kernel": "loca_feedback_fit (all blocks)",
+                        "algorithmic_bytes_per_launch": nbytes, "avg_launch_ms": t_cal}}
+    print(f"[bench] next: calibration {t_cal:.3f} ms", file=sys.stderr, flush=True)
+    if not args.no_cpu_baseline:
+        # the oracle forms the d x d map and takes its full SVD (O(d^3)): timed on the first
+        # d_s rows and columns of block 0's probes and scaled by (d / d_s)^3 and the block count
+        import oracle
+        d_s = min(cfg.d, 1024)
+        print(f"[bench] next: cpu baseline of the calibration (oracle, width {d_s})", file=sys.stderr, flush=True)
+        E_h = E[:d_s].double().cpu().numpy()
+        G_h = G[0, :d_s].double().cpu().numpy()
+        W_h = Wu[:, :d_s].double().cpu().numpy()
+        t0 = time.perf_counter()
+        F = oracle.feedback_fit(E_h, G_h, 0.05)
+        F_k, _, _, _ = oracle.feedback_factors(F, k, W_h)
+        oracle.alignment(F_k, E_h, G_h)
+        t_blk = time.perf_counter() - t0
+        scale = (cfg.d / d_s) ** 3 * nb
+        cal["cpu_baseline"] = {"value": t_blk * scale * 1e3, "unit": "ms per calibration of all blocks",
+                               "cores": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)),
+                               "kind": "oracle",
+                               "sample": f"block 0 at width {d_s} with {n_p} probes ({t_blk:.2f} s), scaled by "
+                                         f"(d/{d_s})^3 x {nb} blocks"}
+    out["feedback_fit"] = cal
+    del E, G, Wu, bt, at, ws
+    return out
 
 
 def cpu_baseline(cfg, n_sample):
@@ -229,6 +379,8 @@ def main():
                      "kernel": "loca_accumulate_stats (Gram S += X^T X and cross X^T Y of all blocks, one micro-batch)",
                      "algorithmic_flops_per_launch": f_avg, "avg_launch_ms": t_avg},
     }
+    if args.next:
+        out["next"] = next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream)
     if not args.no_cpu_baseline:
         del x_all
         torch.cuda.empty_cache()

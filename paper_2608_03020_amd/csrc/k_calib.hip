@@ -159,14 +159,15 @@ __global__ void k_calib_factors(int64_t d, int k, int np_, const float* __restri
 }
 
 // alpha_b = <P, Q> / (||Q|| ||G||) from the fixed-order sums of the partial products
-// P = U_k^T G, Q = S_k V_k^T E (k x np) and ||G||^2 (one thread per block).
-__global__ void k_calib_alpha(int64_t nb, int k, int np_, int ns, const double* __restrict__ pP,
-                              const double* __restrict__ pQ, const double* __restrict__ pG2,
-                              double* __restrict__ alpha_out) {
-  const int64_t b = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= nb) return;
+// P = U_k^T G, Q = S_k V_k^T E (k x np) and ||G||^2.  One workgroup per block: thread e sums
+// entry e over the row ranges in order, then fixed-order workgroup sums.
+__global__ __launch_bounds__(kT) void k_calib_alpha(int64_t nb, int k, int np_, int ns, const double* __restrict__ pP,
+                                                    const double* __restrict__ pQ, const double* __restrict__ pG2,
+                                                    double* __restrict__ alpha_out) {
+  __shared__ double red[3][kT / 64];
+  const int64_t b = blockIdx.x;
   double pq = 0.0, qq = 0.0, gg = 0.0;
-  for (int e = 0; e < k * np_; ++e) {
+  for (int e = threadIdx.x; e < k * np_; e += kT) {
     double p = 0.0, q = 0.0;
     for (int z = 0; z < ns; ++z) {
       p += pP[(b * ns + z) * k * np_ + e];
@@ -175,10 +176,15 @@ __global__ void k_calib_alpha(int64_t nb, int k, int np_, int ns, const double* 
     pq += p * q;
     qq += q * q;
   }
-  for (int e = 0; e < np_; ++e)
+  for (int e = threadIdx.x; e < np_; e += kT)
     for (int z = 0; z < ns; ++z) gg += pG2[(b * ns + z) * np_ * np_ + e * np_ + e];
-  const double den = sqrt(qq) * sqrt(gg);
-  alpha_out[b] = den > 0.0 ? pq / den : 0.0;
+  pq = block_sum(pq, red[0]);
+  qq = block_sum(qq, red[1]);
+  gg = block_sum(gg, red[2]);
+  if (threadIdx.x == 0) {
+    const double den = sqrt(qq) * sqrt(gg);
+    alpha_out[b] = den > 0.0 ? pq / den : 0.0;
+  }
 }
 
 // A~_b = W_u V_k,b (vocab x k): one wave per row of W_u, lanes over d, k sums reduced in
@@ -275,7 +281,7 @@ hipError_t launch_feedback_fit(const CalibArgs& a) {
                                                                  ns, pQ);
   k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)np_, (int)np_, a.g, a.g_bstride, np_, 1, a.g,
                                                                  a.g_bstride, np_, 1, ns, pG);
-  k_calib_alpha<<<(unsigned)((nb + 63) / 64), 64, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
+  k_calib_alpha<<<(unsigned)nb, kT, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
   if (a.wu && a.at_out) {
     dim3 g((unsigned)((a.vocab + 3) / 4), (unsigned)nb);
     if (a.wu_dtype == LOCA_BF16)

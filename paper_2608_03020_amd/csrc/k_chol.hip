@@ -82,22 +82,78 @@ __global__ __launch_bounds__(256) void k_equil_setup(int64_t d, int64_t m, int64
   }
 }
 
-// SLp[b] = S_sym Lp (d x r_prev, fp64) from the upper triangle of S.
-template <typename ST>
-__global__ void k_sym_mul(int64_t d, int64_t r_prev, const ST* __restrict__ S, int64_t s_bstride,
-                          const float* __restrict__ Lp, int64_t lp_bstride, double* __restrict__ out) {
+// SLp[b] = S_sym Lp (d x r_prev, fp64) from the upper triangle of S.  A workgroup owns 64
+// rows and RC columns of the product (grid: x over row tiles, y = block, z over column
+// chunks) and walks the 64-wide column tiles of S in order: tiles on or above the
+// diagonal are read row-major, tiles below it as the transpose of the stored tile above
+// (both with coalesced rows), the diagonal tile mirrored from its upper half.  Thread t
+// owns row t % 64 and all RC columns; wave q = t / 64 takes the columns 16q .. 16q + 15 of
+// each tile, and the four waves' sums are added in a fixed order at the end.
+constexpr int kSM = 64;
+template <typename ST, int RC>
+__global__ __launch_bounds__(256) void k_sym_mul(int64_t d, int64_t r_prev, const ST* __restrict__ S,
+                                                 int64_t s_bstride, const float* __restrict__ Lp,
+                                                 int64_t lp_bstride, double* __restrict__ out) {
+  __shared__ ST sS[kSM][kSM + 1];
+  __shared__ __attribute__((aligned(16))) float sL[kSM][RC];
+  __shared__ double sR[3][kSM][RC + 1];
   const int64_t b = blockIdx.y;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= d * r_prev) return;
-  const int64_t i = e / r_prev, c = e % r_prev;
+  const int64_t i0 = (int64_t)blockIdx.x * kSM;
+  const int64_t c0 = (int64_t)blockIdx.z * RC;
   const ST* Sb = S + b * s_bstride;
   const float* L = Lp + b * lp_bstride;
-  double s = 0.0;
-  for (int64_t j = 0; j < d; ++j) {
-    const double sij = (j >= i) ? (double)Sb[i * d + j] : (double)Sb[j * d + i];
-    s += sij * (double)L[j * r_prev + c];
+  const int t = threadIdx.x, r = t & 63, q = t >> 6;
+  double acc[RC];
+#pragma unroll
+  for (int u = 0; u < RC; ++u) acc[u] = 0.0;
+  for (int64_t j0 = 0; j0 < d; j0 += kSM) {
+    __syncthreads();
+    // sS[rr][cc] = S_sym[i0 + rr][j0 + cc]
+    for (int e = t; e < kSM * kSM; e += 256) {
+      const int rr = e / kSM, cc = e % kSM;
+      if (j0 >= i0) {  // rows i0 + rr, columns j0 + cc (the diagonal tile is fixed up below)
+        const int64_t gi = i0 + rr, gj = j0 + cc;
+        sS[rr][cc] = (gi < d && gj < d) ? Sb[gi * d + gj] : (ST)0;
+      } else {         // stored tile (j0, i0): rows j0 + rr, columns i0 + cc, transposed
+        const int64_t gi = j0 + rr, gj = i0 + cc;
+        sS[cc][rr] = (gi < d && gj < d) ? Sb[gi * d + gj] : (ST)0;
+      }
+    }
+    for (int e = t; e < kSM * RC; e += 256) {
+      const int rr = e / RC, cc = e % RC;
+      sL[rr][cc] = (j0 + rr < d && c0 + cc < r_prev) ? L[(j0 + rr) * r_prev + c0 + cc] : 0.f;
+    }
+    __syncthreads();
+    if (j0 == i0) {  // mirror the upper half of the diagonal tile
+      for (int e = t; e < kSM * kSM; e += 256) {
+        const int rr = e / kSM, cc = e % kSM;
+        if (cc < rr) sS[rr][cc] = sS[cc][rr];
+      }
+      __syncthreads();
+    }
+#pragma unroll 4
+    for (int jj = 16 * q; jj < 16 * q + 16; ++jj) {
+      const double sv = (double)sS[r][jj];
+#pragma unroll
+      for (int u = 0; u < RC; u += 4) {
+        const float4 l = *(const float4*)&sL[jj][u];
+        acc[u] += sv * (double)l.x;
+        acc[u + 1] += sv * (double)l.y;
+        acc[u + 2] += sv * (double)l.z;
+        acc[u + 3] += sv * (double)l.w;
+      }
+    }
   }
-  out[b * d * r_prev + e] = s;
+  if (q > 0)
+#pragma unroll
+    for (int u = 0; u < RC; ++u) sR[q - 1][r][u] = acc[u];
+  __syncthreads();
+  if (q == 0 && i0 + r < d)
+#pragma unroll
+    for (int u = 0; u < RC; ++u) {
+      const double v = ((acc[u] + sR[0][r][u]) + sR[1][r][u]) + sR[2][r][u];
+      if (c0 + u < r_prev) out[b * d * r_prev + (i0 + r) * r_prev + c0 + u] = v;
+    }
 }
 
 // ------------------------------------------------------------------ matrix-core tile products
@@ -1027,8 +1083,14 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
   const ST* S = (const ST*)a.S + b0 * a.s_bstride;
   const ST* K = (const ST*)a.K + b0 * a.k_bstride;
   if (a.r_prev > 0) {
-    dim3 g((unsigned)((d * a.r_prev + 255) / 256), (unsigned)nbg);
-    k_sym_mul<ST><<<g, 256, 0, st>>>(d, a.r_prev, S, a.s_bstride, a.lp + b0 * a.lp_bstride, a.lp_bstride, SLp);
+    const float* lp = a.lp + b0 * a.lp_bstride;
+    if (a.r_prev <= 16) {
+      dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, 1);
+      k_sym_mul<ST, 16><<<g, 256, 0, st>>>(d, a.r_prev, S, a.s_bstride, lp, a.lp_bstride, SLp);
+    } else {
+      dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, (unsigned)((a.r_prev + 31) / 32));
+      k_sym_mul<ST, 32><<<g, 256, 0, st>>>(d, a.r_prev, S, a.s_bstride, lp, a.lp_bstride, SLp);
+    }
   }
   {
     dim3 g((unsigned)((d + 255) / 256), (unsigned)nm);
@@ -1070,7 +1132,10 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       }
       if constexpr (sizeof(T) == 4) k_diag_f32<<<(unsigned)nm, kT, 0, st>>>(d, pp, (float*)F, info);
       else k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
-      if (after_diag && pp == 0) hipEventRecord(after_diag, st);
+      if (after_diag && pp == 0) {
+        const hipError_t er = hipEventRecord(after_diag, st);
+        if (er != hipSuccess) return er;
+      }
       if (x6 && nrem > 0) {
         const int nF = (int)((nrem + 255) / 256);
         k_panel_x6<kX6Row><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(

@@ -332,9 +332,11 @@ LOCA_DEV int xcd_logical(int L, int total) {
 // Kraw = X_I^T [Y_hi | Y_lo] for the panel's 256 columns, 128 each.
 //
 // WT: statistic weights, padded in `wpad` (zero past n, readable up to kBK floats past
-// the last stage).  The weights of each half stage reach scalar registers one half
-// stage ahead of use; the second operand (X_J, or the split targets of a cross wave)
-// is then scaled and split in registers, and each row of MFMAs runs on both parts.
+// the last stage).  The second operand (X_J, or the split targets of a cross wave) is
+// scaled and split in registers, and each row of MFMAs runs on both parts.  The split
+// of a half stage's operands runs in the middle of the other half's MFMA rows, so that
+// its vector work overlaps them; the weights reach scalar registers a quarter stage
+// before that.
 template <int WGM, int WGN, bool BUF, bool WT>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int64_t d, const uint16_t* __restrict__ Xall,
                                                                 int64_t ldx, int64_t x_bstride, float* __restrict__ Sall,
@@ -447,7 +449,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
       for (int q = 0; q < NBN; ++q) acc[m][q] = mfma32(fa[m], fl[q], acc[m][q]);
   };
   i32x16_t wsc;
-  if (WT) wsc = sload16(wpad);  // half stage 0 of stage 0
+  if (WT) wsc = sload16(wpad);  // stage 0, first half
   // scale and split the second operands with the weights loaded one half stage ago,
   // and start the load of the next half stage's weights
   auto weigh = [&](bf16x8_t (&fb)[NBN], bf16x8_t (&fl)[NBN], const float* next) {
@@ -468,14 +470,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
         issue(fill, kt + kDLStages - 1, sl * NCP / NSLOT);
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (sl == 0) {
-        if (WT) weigh(fb0, fl0, wpad + (int64_t)kt * kBK + 16);
-        load_frags(cur, 16, fa1, fb1);
-      }
-      if (sl == NBM) {
-        if (WT) weigh(fb1, fl1, wpad + (int64_t)(kt + 1) * kBK);
-        load_frags(nxt, 0, fa0, fb0);
-      }
+      if (sl == 0) load_frags(cur, 16, fa1, fb1);
+      if (WT && sl == NBM / 2) weigh(fb1, fl1, wpad + (int64_t)(kt + 1) * kBK);  // this stage, second half
+      if (sl == NBM) load_frags(nxt, 0, fa0, fb0);
+      if (WT && sl == NBM + NBM / 2) weigh(fb0, fl0, wpad + (int64_t)(kt + 1) * kBK + 16);  // next stage, first half
       if (sl < NBM) mma_row(fa0, fb0, fl0, sl);
       else mma_row(fa1, fb1, fl1, sl - NBM);
     }
@@ -490,6 +488,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NCP));  // stage 0 landed
   barrier_nofence();
   load_frags(sb0, 0, fa0, fb0);
+  if (WT) weigh(fb0, fl0, wpad + 16);  // stage 0, second half next
   for (int kt = 0; kt < nk; kt += 4) {
     step(sb0, sb1, sb3, kt);
     if (kt + 1 < nk) step(sb1, sb2, sb0, kt + 1);

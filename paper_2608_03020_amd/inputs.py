@@ -293,3 +293,42 @@ def torch_gen_head(cfg: LocaConfig, seed: int = 0, device="cuda", rows: Optional
         z = z.to(torch.bfloat16)
     y = torch.randint(0, cfg.C, (rows,), generator=g, device=device, dtype=torch.int32)
     return z, y
+
+
+def torch_gen_stat_weights(cfg: LocaConfig, seed: int = 0, device="cuda", zero: float = 0.2):
+    """Device statistic weights for all cfg.n positions, with the recipe of gen_stat_weights."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1000003 + _CFG_ID.get(cfg.name, 99) * 7919 + 15485863) & 0x7FFFFFFF)
+    a = 2.0 * torch.rand(cfg.n, generator=g, device=device, dtype=torch.float32)
+    a[torch.rand(cfg.n, generator=g, device=device) < zero] = 0.0
+    return a
+
+
+def torch_gen_current_adapter(cfg: LocaConfig, blocks: int, r_prev: int, seed: int = 0, device="cuda"):
+    """Device current adapters W_prev = Lp Rp of every block, with the recipe of
+    gen_current_adapter: Lp (blocks, d, r_prev), Rp (blocks, r_prev, d)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1000003 + _CFG_ID.get(cfg.name, 99) * 7919 + 32452843) & 0x7FFFFFFF)
+    s = 1.0 / np.sqrt(cfg.d)
+    lp = torch.randn((blocks, cfg.d, r_prev), generator=g, device=device, dtype=torch.float32) * s
+    rp = torch.randn((blocks, r_prev, cfg.d), generator=g, device=device, dtype=torch.float32) * s
+    return lp, rp
+
+
+def torch_gen_probe_pairs(cfg: LocaConfig, n_p: int, blocks: int, seed: int = 0, device="cuda",
+                          noise: float = 2.0):
+    """Device calibration probes with the recipe of gen_probe_pairs (rank-2k maps):
+    E (d, n_p) shared by the blocks and G (blocks, d, n_p)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1000003 + _CFG_ID.get(cfg.name, 99) * 7919 + 49979687) & 0x7FFFFFFF)
+    d, r = cfg.d, 2 * cfg.k
+    E = torch.randn((d, n_p), generator=g, device=device, dtype=torch.float32)
+    s = 1.0 / np.sqrt(d)
+    P = torch.randn((blocks, d, r), generator=g, device=device, dtype=torch.float32) * s
+    Q = torch.randn((blocks, d, r), generator=g, device=device, dtype=torch.float32) * s
+    G = P @ (Q.transpose(1, 2) @ E) + (noise * s) * torch.randn((blocks, d, n_p), generator=g, device=device,
+                                                                   dtype=torch.float32)
+    return E, G.contiguous()
