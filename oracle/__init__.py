@@ -14,7 +14,9 @@ iteration, steps 2-5):
   5. Eckart-Young truncation of W to rank r_a                      (Lemma S5.2)
 plus the paper-literal projected form with a random A_l            (Eqs. 6-9)
 and the one-time Stage I calibration that produces A~, B~: the feedback ridge
-fit, its rank-k truncation and the alignment diagnostic           (Section S5)
+fit, its rank-k truncation and the alignment diagnostic           (Section S5),
+and the head in the paper's order: the top error e_t = W_u^T E_t once, then
+V_k^T e_t per block                                               (Section S11)
 
 It shares no code with the HIP path and never imports it.
 """
@@ -257,6 +259,21 @@ def alignment(F, E, G):
     P = _f64(F) @ _f64(E)
     G = _f64(G)
     return float(np.sum(P * G) / (np.linalg.norm(P) * np.linalg.norm(G)))
+
+
+def top_error(z, y, Wu, w=None):
+    """Top-layer error at the hidden width, e_t = W_u^T (softmax(z_t) - onehot(y_t)) scaled
+    by the loss weight (the error of the target equation with Lemma S3.1's head error):
+    the head applied once per top error and shared by all blocks (Section S11's cost
+    order).  z (n x V), Wu (V x d) -> e (n x d); the product is a library matmul."""
+    return head_error(z, y, w) @ _f64(Wu)
+
+
+def credit_from_top_error(e, Vk, B):
+    """The rank-k feedback applied to top errors in the paper's order, F e = U_k (S_k (V_k^T e))
+    (Section S11): Y = e V_k (the coordinates V_k^T e_t as rows) and Q = Y B~, B~ = S_k U_k^T."""
+    Y = _f64(e) @ _f64(Vk)
+    return Y, Y @ _f64(B)
 
 
 def block_step(xs: Sequence[np.ndarray], zs: Sequence[np.ndarray], ys: Sequence[np.ndarray],
