@@ -68,7 +68,9 @@ typedef enum {
   LOCA_OP_RIDGE_SOLVE = 2,
   LOCA_OP_LOWRANK_TRUNCATE = 3,
   LOCA_OP_RIDGE_SOLVE_PROJECTED = 4,
-  LOCA_OP_FEEDBACK_FIT = 5
+  LOCA_OP_FEEDBACK_FIT = 5,
+  LOCA_OP_TOP_ERROR = 6,
+  LOCA_OP_CREDIT_FROM_TOP_ERROR = 7
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -238,6 +240,8 @@ loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
  *   bt_out : per block k x d float, B~ = S_k U_k^T (stride bt_bstride);
  *   at_out : per block vocab x k float, A~ = W_u V_k (stride at_bstride); needs
  *            wu (vocab x d, F32 or BF16); both may be NULL (then skipped);
+ *   vk_out : per block d x k float, V_k itself (stride vk_bstride), the factor of the
+ *            paper-order head (loca_credit_from_top_error); may be NULL;
  *   sigma_out : per block np floats, the singular values of F_hat_b, decreasing;
  *   alpha_out : per block the alignment diagnostic <F_b E, G_b> / (||F_b E|| ||G_b||)
  *               (float64).
@@ -249,13 +253,53 @@ loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
 loca_status loca_feedback_fit(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k,
                               const float* e, const float* g, int64_t g_bstride, double beta,
                               const void* wu, loca_dtype wu_dtype, int64_t vocab, float* bt_out,
-                              int64_t bt_bstride, float* at_out, int64_t at_bstride,
-                              float* sigma_out, double* alpha_out, int32_t* dev_info, void* ws,
-                              size_t ws_bytes);
+                              int64_t bt_bstride, float* at_out, int64_t at_bstride, float* vk_out,
+                              int64_t vk_bstride, float* sigma_out, double* alpha_out,
+                              int32_t* dev_info, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * The head in the paper's order (Section S11; the error term of the target equation
+ * with Lemma S3.1's head error): the top-layer error at the hidden width, computed
+ * once and shared by all blocks,
+ *   e_t = W_u^T E_t,   E_t = w_t (softmax(z_t) - onehot(y_t))        (e: n x d),
+ * after which each block needs only V_k^T e_t (loca_credit_from_top_error) instead
+ * of the folded factor A~ = W_u V_k (loca_error_targets).  The work is 4 n V d
+ * matrix-core flops once (the softmax weights enter as two bf16 parts) instead of
+ * 2 n V k per block, so it pays when L k > d.
+ * logits : n x V (ld_logits >= V), F32 or BF16, 16-byte aligned, ld_logits a multiple
+ *          of 8 (BF16) or 4 (F32).   labels : n int32 in [0, V).   w : n floats or NULL.
+ * wu : V x d, BF16 only (LOCA_E_UNSUPPORTED otherwise), 16-byte aligned.
+ * e_out : n x d float, row stride ld_e >= d.
+ * dev_info : one int32; 0, or 1 + the smallest row whose label is out of range.
+ * Limits: d % 8 == 0 (LOCA_E_UNSUPPORTED otherwise).  Workspace: LOCA_OP_TOP_ERROR with
+ * n, d and C = V.
+ * ------------------------------------------------------------------------- */
+loca_status loca_top_error(loca_stream_t stream, int64_t n, int64_t V, int64_t d, const void* logits,
+                           loca_dtype logits_dtype, int64_t ld_logits, const int32_t* labels,
+                           const float* w, const void* wu, loca_dtype wu_dtype, float* e_out,
+                           int64_t ld_e, int32_t* dev_info, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * Per block, the credit coordinates of the paper-order head (Section S11,
+ * F e = U_k (S_k (V_k^T e))):  Y_b = e V_k,b  (n x k; row t holds V_k^T e_t), and
+ *   mb_out[b].sum_q2 = sum_t a_t ||Y_t B~_b||^2   (B~ = S_k U_k^T),
+ * the same outputs as loca_error_targets, so loca_accumulate_stats follows as usual.
+ * e : n x d float (row stride ld_e), from loca_top_error.
+ * credit_v : per block d x k float (stride v_bstride), V_k.
+ * credit_b : per block k x d float (stride b_bstride).   a_w : n floats or NULL.
+ * y_out : per block n x k float (stride y_bstride).   mb_out : nb entries.
+ * Limits: k <= 128.  Workspace: LOCA_OP_CREDIT_FROM_TOP_ERROR with nb, n and k.
+ * ------------------------------------------------------------------------- */
+loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t n, int64_t d,
+                                       int64_t k, const float* e, int64_t ld_e,
+                                       const float* credit_v, int64_t v_bstride,
+                                       const float* credit_b, int64_t b_bstride, const float* a_w,
+                                       float* y_out, int64_t y_bstride, loca_mb* mb_out, void* ws,
+                                       size_t ws_bytes);
 
 /* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
  * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there; n = np for
- * LOCA_OP_FEEDBACK_FIT).  `acc` selects the precision mode.  Unused arguments
+ * LOCA_OP_FEEDBACK_FIT; C = V for LOCA_OP_TOP_ERROR).  `acc` selects the precision mode.  Unused arguments
  * may be 0. */
 size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,
                            int64_t r_a, int64_t n_lambda, loca_dtype acc);

@@ -216,6 +216,13 @@ __global__ __launch_bounds__(kT) void k_head_fold(int64_t vocab, int64_t d, int 
   }
 }
 
+// vk_out[b][c][j] = V_k (the internal copy, d x k per block, packed)
+__global__ void k_copy_vk(int64_t d, int k, const float* __restrict__ vk, float* __restrict__ out, int64_t bstride) {
+  const int64_t b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < d * k) out[b * bstride + e] = vk[b * d * k + e];
+}
+
 __global__ void k_zero_i32(int32_t* p, int64_t cnt) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < cnt) p[i] = 0;
@@ -282,6 +289,10 @@ hipError_t launch_feedback_fit(const CalibArgs& a) {
   k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)np_, (int)np_, a.g, a.g_bstride, np_, 1, a.g,
                                                                  a.g_bstride, np_, 1, ns, pG);
   k_calib_alpha<<<(unsigned)nb, kT, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
+  if (a.vk_out) {
+    dim3 g((unsigned)((d * k + 255) / 256), (unsigned)nb);
+    k_copy_vk<<<g, 256, 0, st>>>(d, (int)k, vk, a.vk_out, a.vk_bstride);
+  }
   if (a.wu && a.at_out) {
     dim3 g((unsigned)((a.vocab + 3) / 4), (unsigned)nb);
     if (a.wu_dtype == LOCA_BF16)

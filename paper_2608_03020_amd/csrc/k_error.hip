@@ -234,13 +234,76 @@ __global__ void k_error_finalize(int64_t n, int64_t nparts, const double* __rest
                                  loca_mb* __restrict__ mb, int32_t* __restrict__ dev_info) {
   const int64_t b = blockIdx.x;
   if (threadIdx.x != 0) return;
-  if (b == 0 && *dev_info == INT32_MAX) *dev_info = 0;
+  if (b == 0 && dev_info && *dev_info == INT32_MAX) *dev_info = 0;
   double s = 0.0;
   for (int64_t i = 0; i < nparts; ++i) s += partial[b * nparts + i];
   mb[b].sum_q2 = s;
   mb[b].sum_x2 = 0.0;
   mb[b].eta_bar = 0.0;
   mb[b].n = n;
+}
+
+// Paper-order credit coordinates (Section S11): Y_b = e V_k,b (n x k) from the top errors
+// e (n x d) and sum_q2 partials as in the error kernels.  64 tokens per workgroup, d in
+// chunks of 64 through LDS; thread t owns token t % 64 and the columns t / 64 + 4u (u < KQ),
+// fp64 accumulation.
+template <int KQ>
+__global__ __launch_bounds__(256) void k_credit_project(int64_t n, int64_t d, int64_t k, const float* __restrict__ e,
+                                                        int64_t ld_e, const float* __restrict__ Vk, int64_t v_bstride,
+                                                        const double* __restrict__ G, const float* __restrict__ aw,
+                                                        float* __restrict__ y_out, int64_t y_bstride,
+                                                        double* __restrict__ partial) {
+  constexpr int KW = 4 * KQ;
+  __shared__ float sE[64][65];
+  __shared__ float sV[64][KW];
+  __shared__ double sY[64][KW + 1];
+  __shared__ double sred[4];
+  const int64_t b = blockIdx.y;
+  const int64_t t0 = (int64_t)blockIdx.x * 64;
+  const int tid = threadIdx.x, r = tid & 63, q = tid >> 6;
+  const float* V = Vk + b * v_bstride;
+  double acc[KQ];
+#pragma unroll
+  for (int u = 0; u < KQ; ++u) acc[u] = 0.0;
+  for (int64_t c0 = 0; c0 < d; c0 += 64) {
+    __syncthreads();
+    for (int x = tid; x < 64 * 64; x += 256) {
+      const int rr = x / 64, cc = x % 64;
+      sE[rr][cc] = (t0 + rr < n && c0 + cc < d) ? e[(t0 + rr) * ld_e + c0 + cc] : 0.f;
+    }
+    for (int x = tid; x < 64 * KW; x += 256) {
+      const int cc = x / KW, j = x % KW;
+      sV[cc][j] = (c0 + cc < d && j < k) ? V[(c0 + cc) * k + j] : 0.f;
+    }
+    __syncthreads();
+    for (int cc = 0; cc < 64; ++cc) {
+      const double ev = (double)sE[r][cc];
+#pragma unroll
+      for (int u = 0; u < KQ; ++u) acc[u] += ev * (double)sV[cc][q + 4 * u];
+    }
+  }
+  const int64_t t = t0 + r;
+#pragma unroll
+  for (int u = 0; u < KQ; ++u) {
+    const int j = q + 4 * u;
+    const float yv = (float)acc[u];
+    sY[r][j] = (double)yv;
+    if (t < n && j < k) y_out[b * y_bstride + t * k + j] = yv;
+  }
+  __syncthreads();
+  // q_t = Y_t G Y_t^T of the stored (float) coordinates, weighted by the statistic weight
+  double qv = 0.0;
+  if (tid < 64 && t0 + tid < n) {
+    const double* Gb = G + b * k * k;
+    for (int a2 = 0; a2 < k; ++a2) {
+      double rr = 0.0;
+      for (int c = 0; c < k; ++c) rr += Gb[a2 * k + c] * sY[tid][c];
+      qv += sY[tid][a2] * rr;
+    }
+    if (aw) qv *= (double)aw[t0 + tid];
+  }
+  const double tot = block_sum(qv, sred);
+  if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
 }
 
 __global__ void k_fill_i32(int32_t* p, int64_t cnt, int32_t v) {
@@ -312,6 +375,32 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   if (!zb && ab) return dispatch_error<float, uint16_t>(a, G, partial, ms);
   if (zb && !ab) return dispatch_error<uint16_t, float>(a, G, partial, ms);
   return dispatch_error<uint16_t, uint16_t>(a, G, partial, ms);
+}
+
+// ------------------------------------------------------------------ paper-order credit
+
+size_t credit_from_top_error_ws(int64_t nb, int64_t n, int64_t k) {
+  return align256(sizeof(double) * nb * k * k) + align256(sizeof(double) * nb * ((n + 63) / 64));
+}
+
+hipError_t launch_credit_from_top_error(const CreditArgs& a) {
+  double* G = (double*)a.ws;
+  double* partial = (double*)(a.ws + align256(sizeof(double) * a.nb * a.k * a.k));
+  dim3 gg((unsigned)((a.k + kCG - 1) / kCG), (unsigned)a.k, (unsigned)a.nb);
+  k_credit_gram<<<gg, 256, 0, a.stream>>>(a.k, a.d, a.credit_b, a.b_bstride, G);
+  dim3 g((unsigned)((a.n + 63) / 64), (unsigned)a.nb);
+#define LOCA_PROJ(KQ)                                                                                          \
+  k_credit_project<KQ><<<g, 256, 0, a.stream>>>(a.n, a.d, a.k, a.e, a.ld_e, a.vk, a.v_bstride, G, a.a_w, a.y_out, \
+                                                 a.y_bstride, partial)
+  if (a.k <= 16) LOCA_PROJ(4);
+  else if (a.k <= 32) LOCA_PROJ(8);
+  else if (a.k <= 64) LOCA_PROJ(16);
+  else LOCA_PROJ(32);
+#undef LOCA_PROJ
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, g.x, partial, a.mb_out, nullptr);
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ dense targets (tests)

@@ -1,0 +1,277 @@
+// k_head.hip -- the head in the paper's order (Section S11): the top-layer error taken
+// to the hidden width once for all blocks,
+//   e_t = W_u^T E_t,   E_t = w_t (softmax(z_t) - onehot(y_t))   (the target's error term,
+//                                                               Lemma S3.1's head error),
+// so that each block then applies only V_k^T e_t (loca_credit_from_top_error).  It pays
+// off when the blocks' folded factors A~ = W_u V_k together are wider than the hidden
+// width (L k > d).
+//
+//   1. k_softmax_stats: per token the row maximum m_t and s_t = sum_c exp(z_tc - m_t)
+//      (one workgroup per token, fixed-order combination of the partial pairs);
+//   2. k_top_error_gemm: part_z = P W_u over the vocabulary chunk z, P_tc = w_t exp(z_tc -
+//      m_t) / s_t formed while the logits tile is staged, split into bf16 hi + lo parts
+//      (about 16 significant bits), each multiplied by the exact bf16 W_u on the matrix
+//      cores (v_mfma_f32_32x32x16_bf16; W_u read transposed from LDS);
+//   3. k_top_error_reduce: e = sum_z part_z in a fixed order (fp64), minus w_t W_u[y_t].
+#include <algorithm>
+
+#include "loca_common.h"
+
+namespace loca {
+
+namespace {
+
+constexpr int kHT = 256;
+constexpr int kHM = 128, kHN = 128, kHK = 32;  // token rows, hidden columns, vocabulary per stage
+constexpr int kLDA = kHK + 8;                  // bf16 per LDS row of P (80 bytes)
+constexpr int kLDB = kHN + 16;                 // bf16 per LDS row of W_u (conflict-free transpose reads)
+
+// dev_info: INT32_MAX while no bad label is seen, then 1 + the smallest bad row, or 0
+__global__ void k_fill_i32_head(int32_t* p) {
+  if (threadIdx.x == 0) *p = INT32_MAX;
+}
+__global__ void k_finish_info_head(int32_t* p) {
+  if (threadIdx.x == 0 && *p == INT32_MAX) *p = 0;
+}
+
+// (m, s) of two disjoint parts of a row combined into one
+LOCA_DEV void ms_combine(float& m, float& s, float m2, float s2) {
+  if (s2 == 0.f) return;
+  if (s == 0.f) { m = m2; s = s2; return; }
+  const float mm = fmaxf(m, m2);
+  s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
+  m = mm;
+}
+
+template <typename LT>
+__global__ __launch_bounds__(kHT) void k_softmax_stats(int64_t n, int64_t V, const LT* __restrict__ z, int64_t ld,
+                                                       const int32_t* __restrict__ labels, float* __restrict__ ms,
+                                                       int32_t* __restrict__ dev_info) {
+  __shared__ float sm[kHT], ss[kHT];
+  const int64_t t = blockIdx.x;
+  const LT* zt = z + t * ld;
+  float m = 0.f, s = 0.f;
+  for (int64_t c = threadIdx.x; c < V; c += kHT) {
+    const float v = load_as_f32(zt + c);
+    if (s == 0.f) { m = v; s = 1.f; }
+    else if (v > m) { s = s * __expf(m - v) + 1.f; m = v; }
+    else s += __expf(v - m);
+  }
+  sm[threadIdx.x] = m;
+  ss[threadIdx.x] = s;
+  __syncthreads();
+  for (int h = kHT / 2; h > 0; h >>= 1) {  // pairs (i, i + h): a fixed tree
+    if ((int)threadIdx.x < h) {
+      float a = sm[threadIdx.x], b = ss[threadIdx.x];
+      ms_combine(a, b, sm[threadIdx.x + h], ss[threadIdx.x + h]);
+      sm[threadIdx.x] = a;
+      ss[threadIdx.x] = b;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    ms[2 * t] = sm[0];
+    ms[2 * t + 1] = ss[0];
+    const int32_t yt = labels[t];
+    if (yt < 0 || yt >= V) atomicMin(dev_info, (int32_t)(t + 1));
+  }
+}
+
+// 8 consecutive logits as floats (a 16-byte aligned bf16 chunk or two float4)
+LOCA_DEV void load8(const uint16_t* p, float (&v)[8]) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+LOCA_DEV void load8(const float* p, float (&v)[8]) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+// Tiles of 128 tokens x 128 hidden columns, one vocabulary chunk per grid.z; 2 x 2 waves of
+// 64 x 64.  Requires ld % 8 == 0 (bf16) or % 4 == 0 (f32), d % 8 == 0, kchunk % 32 == 0.
+template <typename LT>
+__global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, int64_t d, const LT* __restrict__ z,
+                                                        int64_t ld, const float* __restrict__ w,
+                                                        const float* __restrict__ ms, const uint16_t* __restrict__ wu,
+                                                        int64_t kchunk, float* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) uint16_t sAh[2][kHM * kLDA];
+  __shared__ __attribute__((aligned(16))) uint16_t sAl[2][kHM * kLDA];
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][kHK * kLDB];
+  const int64_t t0 = (int64_t)blockIdx.x * kHM, j0 = (int64_t)blockIdx.y * kHN;
+  const int64_t cb = (int64_t)blockIdx.z * kchunk;
+  const int64_t ce = std::min<int64_t>(V, cb + kchunk);
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int wi = wid >> 1, wj = wid & 1;
+
+  // staging: A chunk q of this thread = row (tid + 256 q) / 4, vocabulary 8 ((tid + 256 q) % 4);
+  // B chunk q = vocabulary row (tid + 256 q) / 16, columns 8 ((tid + 256 q) % 16)
+  int arow[2], acol[2], brow[2], bcol[2];
+  float rmax[2], rscale[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int e = tid + kHT * q;
+    arow[q] = e >> 2;
+    acol[q] = 8 * (e & 3);
+    brow[q] = e >> 4;
+    bcol[q] = 8 * (e & 15);
+    const int64_t t = t0 + arow[q];
+    const bool ok = t < n;
+    rmax[q] = ok ? ms[2 * t] : 0.f;
+    const float st = ok ? ms[2 * t + 1] : 1.f;
+    rscale[q] = ok ? (w ? w[t] : 1.f) / st : 0.f;
+  }
+  uint4 ph[2], pl[2], wb[2];
+  auto load_stage = [&](int64_t c0) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int64_t t = t0 + arow[q], c = c0 + acol[q];
+      float v[8];
+      if (t < n && c + 8 <= ce) {
+        load8(z + t * ld + c, v);
+      } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = (t < n && c + i < ce) ? load_as_f32(z + t * ld + c + i) : -INFINITY;
+      }
+      uint32_t h[4], l[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float p0 = __expf(v[2 * i] - rmax[q]) * rscale[q];
+        const float p1 = __expf(v[2 * i + 1] - rmax[q]) * rscale[q];
+        const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
+        const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
+        h[i] = h0 | ((uint32_t)h1 << 16);
+        l[i] = l0 | ((uint32_t)l1 << 16);
+      }
+      ph[q] = make_uint4(h[0], h[1], h[2], h[3]);
+      pl[q] = make_uint4(l[0], l[1], l[2], l[3]);
+      const int64_t cr = c0 + brow[q], j = j0 + bcol[q];
+      wb[q] = (cr < ce && j < d) ? *(const uint4*)(wu + cr * d + j) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto store_stage = [&](int buf) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      *(uint4*)&sAh[buf][arow[q] * kLDA + acol[q]] = ph[q];
+      *(uint4*)&sAl[buf][arow[q] * kLDA + acol[q]] = pl[q];
+      *(uint4*)&sB[buf][brow[q] * kLDB + bcol[q]] = wb[q];
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[m][q][r] = 0.f;
+
+  const int nk = (int)((ce - cb + kHK - 1) / kHK);
+  if (nk > 0) {
+    load_stage(cb);
+    store_stage(0);
+  }
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) load_stage(cb + (int64_t)(kt + 1) * kHK);
+#pragma unroll
+    for (int ks = 0; ks < kHK; ks += 16) {
+      bf16x8_t fh[2], fl[2], fb[2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const int row = wi * 64 + 32 * m + (lane & 31);
+        const int off = row * kLDA + ks + 8 * (lane >> 5);
+        fh[m] = __builtin_bit_cast(bf16x8_t, *(const uint4*)&sAh[cur][off]);
+        fl[m] = __builtin_bit_cast(bf16x8_t, *(const uint4*)&sAl[cur][off]);
+      }
+#pragma unroll
+      for (int q = 0; q < 2; ++q) fb[q] = frag32_tr(sB[cur], kLDB, wj * 64 + 32 * q, ks, lane);
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) acc[m][q] = mfma32(fh[m], fb[q], acc[m][q]);
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) acc[m][q] = mfma32(fl[m], fb[q], acc[m][q]);
+    }
+    if (kt + 1 < nk) store_stage(cur ^ 1);
+    __syncthreads();
+  }
+  float* out = part + (int64_t)blockIdx.z * n * d;
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t t = t0 + wi * 64 + 32 * m + mfma32_row(lane, r);
+        const int64_t j = j0 + wj * 64 + 32 * q + mfma32_col(lane);
+        if (t < n && j < d) out[t * d + j] = acc[m][q][r];
+      }
+}
+
+// e[t][j] = sum_z part_z[t][j] (fp64, in order) - w_t W_u[y_t][j]
+__global__ void k_top_error_reduce(int64_t n, int64_t d, int nsplit, const float* __restrict__ part,
+                                   const float* __restrict__ w, const int32_t* __restrict__ labels, int64_t V,
+                                   const uint16_t* __restrict__ wu, float* __restrict__ e_out, int64_t ld_e) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n * d) return;
+  const int64_t t = e / d, j = e % d;
+  double s = 0.0;
+  for (int zc = 0; zc < nsplit; ++zc) s += (double)part[(int64_t)zc * n * d + e];
+  const int32_t yt = labels[t];
+  if (yt >= 0 && yt < V) s -= (double)(w ? w[t] : 1.f) * (double)bf16_to_f32(wu[(int64_t)yt * d + j]);
+  e_out[t * ld_e + j] = (float)s;
+}
+
+int head_splits(int64_t n, int64_t V, int64_t d) {
+  const int64_t tiles = ((n + kHM - 1) / kHM) * ((d + kHN - 1) / kHN);
+  int64_t s = (2048 + tiles - 1) / tiles;
+  s = std::max<int64_t>(1, std::min<int64_t>(s, 32));
+  s = std::min<int64_t>(s, std::max<int64_t>(1, (V + 255) / 256));  // at least 256 vocabulary entries a chunk
+  return (int)s;
+}
+
+}  // namespace
+
+size_t top_error_ws(int64_t n, int64_t V, int64_t d) {
+  return align256(sizeof(float) * 2 * n) + align256(sizeof(float) * (size_t)head_splits(n, V, d) * n * d);
+}
+
+hipError_t launch_top_error(const TopErrorArgs& a) {
+  float* ms = (float*)a.ws;
+  float* part = (float*)(a.ws + align256(sizeof(float) * 2 * a.n));
+  const int ns = head_splits(a.n, a.V, a.d);
+  const int64_t kchunk = ((a.V + ns - 1) / ns + kHK - 1) / kHK * kHK;
+  hipStream_t st = a.stream;
+  k_fill_i32_head<<<1, 64, 0, st>>>(a.dev_info);
+  dim3 g((unsigned)((a.n + kHM - 1) / kHM), (unsigned)((a.d + kHN - 1) / kHN), (unsigned)ns);
+  if (a.logits_dtype == LOCA_BF16) {
+    k_softmax_stats<uint16_t><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, (const uint16_t*)a.logits, a.ld_logits,
+                                                             a.labels, ms, a.dev_info);
+    k_top_error_gemm<uint16_t><<<g, kHT, 0, st>>>(a.n, a.V, a.d, (const uint16_t*)a.logits, a.ld_logits, a.w, ms,
+                                                  (const uint16_t*)a.wu, kchunk, part);
+  } else {
+    k_softmax_stats<float><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, (const float*)a.logits, a.ld_logits, a.labels,
+                                                          ms, a.dev_info);
+    k_top_error_gemm<float><<<g, kHT, 0, st>>>(a.n, a.V, a.d, (const float*)a.logits, a.ld_logits, a.w, ms,
+                                               (const uint16_t*)a.wu, kchunk, part);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_top_error_reduce<<<(unsigned)((a.n * a.d + 255) / 256), 256, 0, st>>>(
+      a.n, a.d, ns, part, a.w, a.labels, a.V, (const uint16_t*)a.wu, a.e_out, a.ld_e);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  k_finish_info_head<<<1, 64, 0, st>>>(a.dev_info);
+  return hipGetLastError();
+}
+
+}  // namespace loca

@@ -57,6 +57,8 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
     case LOCA_OP_LOWRANK_TRUNCATE: return lowrank_truncate_ws(nb, d, k, r_a);
     case LOCA_OP_RIDGE_SOLVE_PROJECTED: return projected_ws(nb, d, k, r_a, n_lambda);
     case LOCA_OP_FEEDBACK_FIT: return d < 1 || n < 1 || n > 64 ? 0 : feedback_fit_ws(nb, d, n, k);
+    case LOCA_OP_TOP_ERROR: return n < 1 || d < 1 || C < 1 ? 0 : top_error_ws(n, C, d);
+    case LOCA_OP_CREDIT_FROM_TOP_ERROR: return n < 1 ? 0 : credit_from_top_error_ws(nb, n, k);
   }
   return 0;
 }
@@ -197,7 +199,8 @@ loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
 loca_status loca_feedback_fit(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k, const float* e,
                               const float* g, int64_t g_bstride, double beta, const void* wu, loca_dtype wu_dtype,
                               int64_t vocab, float* bt_out, int64_t bt_bstride, float* at_out, int64_t at_bstride,
-                              float* sigma_out, double* alpha_out, int32_t* dev_info, void* ws, size_t ws_bytes) {
+                              float* vk_out, int64_t vk_bstride, float* sigma_out, double* alpha_out,
+                              int32_t* dev_info, void* ws, size_t ws_bytes) {
   if (nb < 1 || d < 1 || np < 1 || k < 1) return LOCA_E_ARG;
   if (!e || !g || !bt_out || !sigma_out || !alpha_out || !dev_info) return LOCA_E_ARG;
   if (!(beta > 0.0) || beta == __builtin_inf()) return LOCA_E_ARG;
@@ -206,13 +209,52 @@ loca_status loca_feedback_fit(loca_stream_t stream, int64_t nb, int64_t d, int64
   if (at_out && (!wu || vocab < 1 || (wu_dtype != LOCA_F32 && wu_dtype != LOCA_BF16) ||
                  (nb > 1 && at_bstride < vocab * k)))
     return LOCA_E_ARG;
+  if (vk_out && nb > 1 && vk_bstride < d * k) return LOCA_E_ARG;
   if (np > 64) return LOCA_E_UNSUPPORTED;
   if (nb > 65535 || d > (int64_t)1 << 30 || vocab > (int64_t)1 << 32) return LOCA_E_UNSUPPORTED;
   loca_status st = check_ws(ws, ws_bytes, feedback_fit_ws(nb, d, np, k));
   if (st != LOCA_OK) return st;
   CalibArgs a{(hipStream_t)stream, nb, d, np, k, e, g, g_bstride, beta, wu, wu_dtype, vocab, bt_out, bt_bstride,
-              at_out, at_bstride, sigma_out, alpha_out, dev_info, nullptr, (char*)ws};
+              at_out, at_bstride, vk_out, vk_bstride, sigma_out, alpha_out, dev_info, (char*)ws};
   return from_hip(launch_feedback_fit(a));
+}
+
+loca_status loca_top_error(loca_stream_t stream, int64_t n, int64_t V, int64_t d, const void* logits,
+                           loca_dtype logits_dtype, int64_t ld_logits, const int32_t* labels, const float* w,
+                           const void* wu, loca_dtype wu_dtype, float* e_out, int64_t ld_e, int32_t* dev_info,
+                           void* ws, size_t ws_bytes) {
+  if (n < 1 || V < 1 || d < 1) return LOCA_E_ARG;
+  if (!logits || !labels || !wu || !e_out || !dev_info) return LOCA_E_ARG;
+  if (ld_logits < V || ld_e < d) return LOCA_E_ARG;
+  if (logits_dtype != LOCA_F32 && logits_dtype != LOCA_BF16) return LOCA_E_ARG;
+  if (wu_dtype != LOCA_F32 && wu_dtype != LOCA_BF16) return LOCA_E_ARG;
+  if (!aligned(logits, 16) || !aligned(wu, 16)) return LOCA_E_ARG;
+  if (ld_logits % (logits_dtype == LOCA_BF16 ? 8 : 4) != 0) return LOCA_E_ARG;
+  if (wu_dtype != LOCA_BF16 || d % 8 != 0) return LOCA_E_UNSUPPORTED;
+  if (n > (int64_t)INT32_MAX - 1 || V > (int64_t)INT32_MAX || (n + 127) / 128 > 65535 || (d + 127) / 128 > 65535)
+    return LOCA_E_UNSUPPORTED;
+  loca_status st = check_ws(ws, ws_bytes, top_error_ws(n, V, d));
+  if (st != LOCA_OK) return st;
+  TopErrorArgs a{(hipStream_t)stream, n, V, d, logits, logits_dtype, ld_logits, labels, w, wu, e_out, ld_e, dev_info,
+                 (char*)ws};
+  return from_hip(launch_top_error(a));
+}
+
+loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t n, int64_t d, int64_t k,
+                                       const float* e, int64_t ld_e, const float* credit_v, int64_t v_bstride,
+                                       const float* credit_b, int64_t b_bstride, const float* a_w, float* y_out,
+                                       int64_t y_bstride, loca_mb* mb_out, void* ws, size_t ws_bytes) {
+  if (nb < 1 || n < 1 || d < 1 || k < 1) return LOCA_E_ARG;
+  if (!e || !credit_v || !credit_b || !y_out || !mb_out) return LOCA_E_ARG;
+  if (ld_e < d) return LOCA_E_ARG;
+  if (nb > 1 && (v_bstride < d * k || b_bstride < k * d || y_bstride < n * k)) return LOCA_E_ARG;
+  if (k > kMaxK) return LOCA_E_UNSUPPORTED;
+  if (nb > 65535 || (n + 63) / 64 > (int64_t)INT32_MAX) return LOCA_E_UNSUPPORTED;
+  loca_status st = check_ws(ws, ws_bytes, credit_from_top_error_ws(nb, n, k));
+  if (st != LOCA_OK) return st;
+  CreditArgs a{(hipStream_t)stream, nb, n, d, k, e, ld_e, credit_v, v_bstride, credit_b, b_bstride, a_w, y_out,
+               y_bstride, mb_out, (char*)ws};
+  return from_hip(launch_credit_from_top_error(a));
 }
 
 }  // extern "C"

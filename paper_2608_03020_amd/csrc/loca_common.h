@@ -158,6 +158,34 @@ struct ErrorArgs {
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k);
 hipError_t launch_error_targets(const ErrorArgs& a);
 
+// The head in the paper's order (Section S11): e = W_u^T E once, then V_k^T e per block.
+struct TopErrorArgs {
+  hipStream_t stream;
+  int64_t n, V, d;
+  const void* logits; loca_dtype logits_dtype; int64_t ld_logits;
+  const int32_t* labels; const float* w;
+  const void* wu;
+  float* e_out; int64_t ld_e;
+  int32_t* dev_info;
+  char* ws;
+};
+size_t top_error_ws(int64_t n, int64_t V, int64_t d);
+hipError_t launch_top_error(const TopErrorArgs& a);
+
+struct CreditArgs {
+  hipStream_t stream;
+  int64_t nb, n, d, k;
+  const float* e; int64_t ld_e;
+  const float* vk; int64_t v_bstride;
+  const float* credit_b; int64_t b_bstride;
+  const float* a_w;
+  float* y_out; int64_t y_bstride;
+  loca_mb* mb_out;
+  char* ws;
+};
+size_t credit_from_top_error_ws(int64_t nb, int64_t n, int64_t k);
+hipError_t launch_credit_from_top_error(const CreditArgs& a);
+
 struct StatsArgs {
   hipStream_t stream;
   int64_t nb, n, d, k;
@@ -220,8 +248,9 @@ struct CalibArgs {
   const void* wu; loca_dtype wu_dtype; int64_t vocab;
   float* bt_out; int64_t bt_bstride;
   float* at_out; int64_t at_bstride;
+  float* vk_out; int64_t vk_bstride;
   float* sigma_out; double* alpha_out;
-  int32_t* dev_info; int32_t* unused_; char* ws;
+  int32_t* dev_info; char* ws;
 };
 size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
 hipError_t launch_feedback_fit(const CalibArgs& a);

@@ -17,11 +17,12 @@ LIB_PATH = os.environ.get("LOCA_LIB", os.path.join(HERE, "lib", "libloca.so"))
 LOCA_OK, LOCA_E_ARG, LOCA_E_WORKSPACE, LOCA_E_HIP, LOCA_E_UNSUPPORTED = range(5)
 LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
- LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT) = range(6)
+ LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR) = range(8)
 
-EXPORTED = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
-            "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_workspace_size",
-            "loca_status_str", "loca_version")
+ENTRY_POINTS = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
+                "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_top_error",
+                "loca_credit_from_top_error")
+EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version")
 
 
 class LocaMB(ctypes.Structure):
@@ -63,14 +64,17 @@ def load():
                                                _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _SZ]
     lib.loca_dense_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _VP, _I64, _VP, _I64]
     lib.loca_feedback_fit.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _D, _VP, _I, _I64, _VP, _I64,
-                                      _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
+                                      _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
+    lib.loca_top_error.argtypes = [_VP, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _I, _VP, _I64, _VP, _VP,
+                                   _SZ]
+    lib.loca_credit_from_top_error.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP,
+                                               _VP, _I64, _VP, _VP, _SZ]
     lib.loca_workspace_size.argtypes = [_I, _I64, _I64, _I64, _I64, _I64, _I64, _I64, _I]
     lib.loca_workspace_size.restype = _SZ
     lib.loca_status_str.argtypes = [_I]
     lib.loca_status_str.restype = ctypes.c_char_p
     lib.loca_version.restype = ctypes.c_char_p
-    for name in ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
-                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit"):
+    for name in ENTRY_POINTS:
         getattr(lib, name).restype = _I
     _lib = lib
     return lib
@@ -217,9 +221,10 @@ def loca_ridge_solve_projected(S, K, credit_b, proj_a, lambdas: Sequence[float],
 
 
 def loca_feedback_fit(e, g, beta: float, bt_out, sigma_out, alpha_out, dev_info, ws, *, wu=None, at_out=None,
-                      stream=None):
+                      vk_out=None, stream=None):
     """e (d, np) probe top errors; g (nb, d, np) exact block gradients; bt_out (nb, k, d) = B~;
-    sigma_out (nb, np); alpha_out (nb,) float64; optional wu (vocab, d) and at_out (nb, vocab, k) = A~."""
+    sigma_out (nb, np); alpha_out (nb,) float64; optional wu (vocab, d) and at_out (nb, vocab, k) = A~;
+    optional vk_out (nb, d, k) = V_k (the factor of the paper-order head)."""
     d, n_p = e.shape
     nb = g.shape[0]
     k = bt_out.shape[-2]
@@ -227,9 +232,32 @@ def loca_feedback_fit(e, g, beta: float, bt_out, sigma_out, alpha_out, dev_info,
     st = load().loca_feedback_fit(
         _stream(stream), nb, d, n_p, k, _ptr(e), _ptr(g), g.stride(0), float(beta), _ptr(wu),
         _dtype(wu) if wu is not None else LOCA_F32, vocab, _ptr(bt_out), bt_out.stride(0), _ptr(at_out),
-        at_out.stride(0) if at_out is not None else 0, _ptr(sigma_out), _ptr(alpha_out), _ptr(dev_info), _ptr(ws),
-        ws.numel() * ws.element_size())
+        at_out.stride(0) if at_out is not None else 0, _ptr(vk_out), vk_out.stride(0) if vk_out is not None else 0,
+        _ptr(sigma_out), _ptr(alpha_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_feedback_fit", st)
+
+
+def loca_top_error(logits, labels, wu, e_out, dev_info, ws, *, w=None, stream=None):
+    """logits (n, V) f32 or bf16; labels (n,) int32; wu (V, d) bf16; e_out (n, d) float32:
+    e_t = W_u^T w_t (softmax(z_t) - onehot(y_t))."""
+    n, V = logits.shape
+    d = wu.shape[1]
+    st = load().loca_top_error(_stream(stream), n, V, d, _ptr(logits), _dtype(logits), logits.stride(0),
+                               _ptr(labels), _ptr(w), _ptr(wu), _dtype(wu), _ptr(e_out), e_out.stride(0),
+                               _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
+    _check("loca_top_error", st)
+
+
+def loca_credit_from_top_error(e, credit_v, credit_b, y_out, mb_out, ws, *, a_w=None, stream=None):
+    """e (n, d) float32 top errors; credit_v (nb, d, k) = V_k; credit_b (nb, k, d) = B~;
+    y_out (nb, n, k); a_w (n,) optional statistic weights."""
+    n, d = e.shape
+    nb, _, k = credit_v.shape
+    st = load().loca_credit_from_top_error(_stream(stream), nb, n, d, k, _ptr(e), e.stride(0), _ptr(credit_v),
+                                           credit_v.stride(0), _ptr(credit_b), credit_b.stride(0), _ptr(a_w),
+                                           _ptr(y_out), y_out.stride(0), _ptr(mb_out), _ptr(ws),
+                                           ws.numel() * ws.element_size())
+    _check("loca_credit_from_top_error", st)
 
 
 def loca_dense_targets(y, mb, credit_b, t_out, *, stream=None):

@@ -160,9 +160,9 @@ def test_feedback_fit_rejects(lib):
     so = lib.load()
 
     def call(nb=1, d=32, n_p=16, k=4, e=FAKE, g=FAKE, gbs=0, beta=0.1, wu=None, wdt=lib.LOCA_F32, vocab=0,
-             bt=FAKE, at=None, sig=FAKE, alpha=FAKE, ws=None, wsb=0):
-        return so.loca_feedback_fit(None, nb, d, n_p, k, e, g, gbs, beta, wu, wdt, vocab, bt, 0, at, 0, sig, alpha,
-                                    FAKE, ws, wsb)
+             bt=FAKE, at=None, vk=None, vkbs=0, sig=FAKE, alpha=FAKE, ws=None, wsb=0):
+        return so.loca_feedback_fit(None, nb, d, n_p, k, e, g, gbs, beta, wu, wdt, vocab, bt, 0, at, 0, vk, vkbs, sig,
+                                    alpha, FAKE, ws, wsb)
 
     assert call(beta=0.0) == lib.LOCA_E_ARG               # the fit needs beta > 0
     assert call(beta=float("inf")) == lib.LOCA_E_ARG
@@ -173,7 +173,44 @@ def test_feedback_fit_rejects(lib):
     assert call(at=FAKE) == lib.LOCA_E_ARG                # A~ needs W_u
     assert call(at=FAKE, wu=FAKE, vocab=10, wdt=lib.LOCA_F64) == lib.LOCA_E_ARG
     assert call(nb=2, gbs=10) == lib.LOCA_E_ARG
+    assert call(nb=2, gbs=32 * 16, vk=FAKE, vkbs=10) == lib.LOCA_E_ARG  # V_k stride below d k
     assert call(n_p=65, k=4) == lib.LOCA_E_UNSUPPORTED
     assert call() == lib.LOCA_E_WORKSPACE
     assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT, 2, 48, 300, 8, 0, 0, 0, lib.LOCA_F32) > 0
     assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT, 2, 65, 300, 8, 0, 0, 0, lib.LOCA_F32) == 0
+
+
+def test_top_error_rejects(lib):
+    so = lib.load()
+
+    def call(n=16, V=100, d=64, z=FAKE, zdt=lib.LOCA_BF16, ld=104, y=FAKE, w=None, wu=FAKE, wdt=lib.LOCA_BF16,
+             e=FAKE, lde=64, info=FAKE, ws=None, wsb=0):
+        return so.loca_top_error(None, n, V, d, z, zdt, ld, y, w, wu, wdt, e, lde, info, ws, wsb)
+
+    assert call(n=0) == lib.LOCA_E_ARG
+    assert call(z=None) == lib.LOCA_E_ARG
+    assert call(ld=99) == lib.LOCA_E_ARG                   # ld_logits >= V
+    assert call(ld=101) == lib.LOCA_E_ARG                  # bf16 rows in 16-byte multiples
+    assert call(lde=63) == lib.LOCA_E_ARG
+    assert call(z=FAKE + 2) == lib.LOCA_E_ARG              # misaligned logits
+    assert call(zdt=lib.LOCA_F64) == lib.LOCA_E_ARG
+    assert call(wdt=lib.LOCA_F32) == lib.LOCA_E_UNSUPPORTED  # W_u enters the matrix cores as bf16
+    assert call(d=60, lde=64) == lib.LOCA_E_UNSUPPORTED    # d % 8 == 0
+    assert call() == lib.LOCA_E_WORKSPACE
+    assert so.loca_workspace_size(lib.LOCA_OP_TOP_ERROR, 1, 16, 64, 1, 100, 0, 0, lib.LOCA_F32) > 0
+
+
+def test_credit_from_top_error_rejects(lib):
+    so = lib.load()
+
+    def call(nb=1, n=16, d=64, k=8, e=FAKE, lde=64, v=FAKE, vbs=0, b=FAKE, bbs=0, aw=None, y=FAKE, ybs=0, mb=FAKE,
+             ws=None, wsb=0):
+        return so.loca_credit_from_top_error(None, nb, n, d, k, e, lde, v, vbs, b, bbs, aw, y, ybs, mb, ws, wsb)
+
+    assert call(k=0) == lib.LOCA_E_ARG
+    assert call(v=None) == lib.LOCA_E_ARG
+    assert call(lde=32) == lib.LOCA_E_ARG
+    assert call(nb=2, vbs=64 * 8 - 1, bbs=8 * 64, ybs=16 * 8) == lib.LOCA_E_ARG
+    assert call(k=129) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE
+    assert so.loca_workspace_size(lib.LOCA_OP_CREDIT_FROM_TOP_ERROR, 3, 16, 64, 8, 0, 0, 0, lib.LOCA_F32) > 0

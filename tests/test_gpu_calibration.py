@@ -34,12 +34,13 @@ def test_feedback_fit_parity(d, n_p, k, nb, vocab, beta, wdt):
     dev = "cuda"
     bt = torch.empty((nb, k, d), dtype=torch.float32, device=dev)
     at = torch.empty((nb, vocab, k), dtype=torch.float32, device=dev)
+    vk = torch.empty((nb, d, k), dtype=torch.float32, device=dev)
     sig = torch.empty((nb, n_p), dtype=torch.float32, device=dev)
     alpha = torch.empty(nb, dtype=torch.float64, device=dev)
     info = torch.full((nb,), -1, dtype=torch.int32, device=dev)
     ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_FEEDBACK_FIT, nb, n_p, d, k), dev)
     loca.loca_feedback_fit(to_dev(E, dev), to_dev(G, dev), beta, bt, sig, alpha, info, ws, wu=to_dev(Wu_bits, dev),
-                           at_out=at)
+                           at_out=at, vk_out=vk)
     torch.cuda.synchronize()
     assert np.all(info.cpu().numpy() == 0)
     for b in range(nb):
@@ -48,10 +49,13 @@ def test_feedback_fit_parity(d, n_p, k, nb, vocab, beta, wdt):
         a_ref = oracle.alignment(F_k, E, G[b])
         Bt_g = bt[b].double().cpu().numpy()
         At_g = at[b].double().cpu().numpy()
+        Vk_g = vk[b].double().cpu().numpy()
         e = {"sigma": rel(sig[b].double().cpu().numpy(), s[:n_p]),
              "AB": rel(At_g @ Bt_g, At_ref @ Bt_ref),              # = W_u F_k^T, sign-free
              "BtB": rel(Bt_g.T @ Bt_g, Bt_ref.T @ Bt_ref),         # = U_k S_k^2 U_k^T
+             "F_k": rel(Bt_g.T @ Vk_g.T, F_k),                      # U_k S_k V_k^T from B~ and V_k
              "alpha": abs(float(alpha[b].item()) - a_ref)}
         log(f"feedback_fit block {b}: alpha {float(alpha[b].item()):.4f} (oracle {a_ref:.4f}); " +
             ", ".join(f"{key} {v:.2e}" for key, v in e.items()))
-        assert e["sigma"] <= 1e-4 and e["AB"] <= 1e-4 and e["BtB"] <= 1e-4 and e["alpha"] <= 1e-5, e
+        assert e["sigma"] <= 1e-4 and e["AB"] <= 1e-4 and e["BtB"] <= 1e-4 and e["F_k"] <= 1e-4, e
+        assert e["alpha"] <= 1e-5, e
