@@ -75,7 +75,8 @@ def parse():
     p.add_argument("--cpu-tokens", type=int, default=0, help="tokens in the CPU-baseline sample")
     p.add_argument("--next", action="store_true",
                    help="also time the widened rows (weighted statistics, outer step with a current adapter, "
-                        "Stage I calibration) on the same workload")
+                        "Stage I calibration on the same workload; the paper-order head on a full-vocabulary "
+                        "workload with 24 blocks)")
     return p.parse_args()
 
 
@@ -260,7 +261,66 @@ def next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream):
                                          f"(d/{d_s})^3 x {nb} blocks"}
     out["feedback_fit"] = cal
     del E, G, Wu, bt, at, ws
+    torch.cuda.empty_cache()
+    out["paper_order_head"] = paper_order_head(stream)
     return out
+
+
+def paper_order_head(stream, L=24, d=896, n=4096, V=151936, k=64, reps=5):
+    """The head in the paper's order on a full-vocabulary workload with many blocks
+    (Qwen2.5-0.5B shape: 24 blocks of width 896, 151936-token vocabulary, k = 64, so
+    L k > d): the top error e = W_u^T E once plus V_k^T e per block, against the folded
+    order (A~ = W_u V_k per block in the error kernel) on the same logits."""
+    import numpy as np
+    import torch
+    from paper_2608_03020_amd import loca
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    z = (torch.randn((n, V), generator=g, device="cuda") * 2.0).to(torch.bfloat16)
+    y = torch.randint(0, V, (n,), generator=g, device="cuda", dtype=torch.int32)
+    Wu = (torch.randn((V, d), generator=g, device="cuda") / np.sqrt(d)).to(torch.bfloat16)
+    Vk = torch.randn((L, d, k), generator=g, device="cuda") / np.sqrt(d)
+    Bt = torch.randn((L, k, d), generator=g, device="cuda") / np.sqrt(k)
+    At = torch.stack([(Wu.float() @ Vk[b]).to(torch.bfloat16) for b in range(L)])
+    e = torch.empty((n, d), dtype=torch.float32, device="cuda")
+    Y = torch.empty((L, n, k), dtype=torch.float32, device="cuda")
+    mb = loca.new_mb(L, "cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(max(loca.workspace_size(loca.LOCA_OP_TOP_ERROR, 1, n, d, 1, V),
+                                  loca.workspace_size(loca.LOCA_OP_CREDIT_FROM_TOP_ERROR, L, n, d, k),
+                                  loca.workspace_size(loca.LOCA_OP_ERROR_TARGETS, L, n, d, k, V)), "cuda")
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps)]
+
+    def paper(s):
+        if s < reps:
+            ev[s][0].record(stream)
+        loca.loca_top_error(z, y, Wu, e, info, ws)
+        if s < reps:
+            ev[s][1].record(stream)
+        loca.loca_credit_from_top_error(e, Vk, Bt, Y, mb, ws)
+        if s < reps:
+            ev[s][2].record(stream)
+
+    def folded(s):
+        loca.loca_error_targets(z, y, At, Bt, Y, mb, info, ws, nb=L)
+        if s < reps:
+            ev[s][3].record(stream)
+    ms_paper = time_steps(paper, reps, 1)
+    ms_folded = time_steps(folded, reps, 1)
+    t_top = sum(a[0].elapsed_time(a[1]) for a in ev) / reps
+    t_cred = sum(a[1].elapsed_time(a[2]) for a in ev) / reps
+    fl = 2.0 * n * V * d
+    ach = fl / (t_top * 1e-3) / 1e12
+    print(f"[bench] next: paper-order head {ms_paper:.2f} ms (top error {t_top:.2f} ms), folded {ms_folded:.2f} ms",
+          file=sys.stderr, flush=True)
+    return {"config": {"blocks": L, "d": d, "tokens": n, "vocab": V, "credit_rank": k, "logits": "bf16",
+                       "head": "bf16"},
+            "ms_paper_order": ms_paper, "ms_folded_order": ms_folded, "ms_top_error": t_top,
+            "ms_credit_all_blocks": t_cred, "speedup_vs_folded": ms_folded / ms_paper,
+            "roofline": {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": ach / BF16_PEAK_TFLOPS, "traffic": None,
+                         "kernel": "loca_top_error (softmax statistics, the split-K product e = W_u^T E, reduction)",
+                         "algorithmic_flops_per_launch": fl, "avg_launch_ms": t_top}}
 
 
 def cpu_baseline(cfg, n_sample):

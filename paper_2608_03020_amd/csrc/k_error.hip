@@ -306,6 +306,29 @@ __global__ __launch_bounds__(256) void k_credit_project(int64_t n, int64_t d, in
   if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
 }
 
+// sum_q2 partials from stored credit coordinates: one thread per token, q_t = Y_t G Y_t^T
+// (fp64) times the statistic weight; grid (ceil(n / 256), nb).
+__global__ __launch_bounds__(256) void k_q2_rows(int64_t n, int64_t k, const float* __restrict__ Y, int64_t y_bstride,
+                                                 const double* __restrict__ G, const float* __restrict__ aw,
+                                                 double* __restrict__ partial) {
+  __shared__ double sred[4];
+  const int64_t b = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  double qv = 0.0;
+  if (t < n) {
+    const float* yt = Y + b * y_bstride + t * k;
+    const double* Gb = G + b * k * k;
+    for (int64_t a2 = 0; a2 < k; ++a2) {
+      double r = 0.0;
+      for (int64_t c = 0; c < k; ++c) r += Gb[a2 * k + c] * (double)yt[c];
+      qv += (double)yt[a2] * r;
+    }
+    if (aw) qv *= (double)aw[t];
+  }
+  const double tot = block_sum(qv, sred);
+  if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
+}
+
 __global__ void k_fill_i32(int32_t* p, int64_t cnt, int32_t v) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < cnt) p[i] = v;
@@ -315,11 +338,24 @@ __global__ void k_fill_i32(int32_t* p, int64_t cnt, int32_t v) {
 
 static bool use_small(int64_t C, int64_t k) { return C <= kSmallMaxC && k <= kSmallMaxK; }
 
+// Large vocabulary with bf16 A~ (k % 8 == 0, aligned operands): Y = E A~ of every block as one
+// matrix-core product over the vocabulary (launch_softmax_product), A~ of the blocks side by side.
+static bool use_product(const ErrorArgs& a) {
+  if (use_small(a.C, a.k) || a.a_dtype != LOCA_BF16 || a.k % 8 != 0) return false;
+  if (((uintptr_t)a.credit_a % 16) != 0 || (a.nb > 1 && a.a_bstride % 8 != 0)) return false;
+  if (((uintptr_t)a.logits % 16) != 0 || a.ld_logits % (a.logits_dtype == LOCA_BF16 ? 8 : 4) != 0) return false;
+  return true;
+}
+
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k) {
   size_t s = align256(sizeof(double) * nb * k * k);  // G
   const int64_t parts = use_small(C, k) ? (n + kSmallThreads - 1) / kSmallThreads : (n + kLargeTok - 1) / kLargeTok;
   s += align256(sizeof(double) * nb * parts);          // partials
-  if (!use_small(C, k)) s += align256(sizeof(float) * 2 * n);  // (m, s) per token
+  if (!use_small(C, k)) {
+    const size_t large = align256(sizeof(float) * 2 * n);  // (m, s) per token
+    const size_t prod = (k % 8 == 0) ? softmax_product_ws(n, C, nb * k) : 0;
+    s += large > prod ? large : prod;
+  }
   return s;
 }
 
@@ -370,6 +406,30 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   k_credit_gram<<<gg, 256, 0, a.stream>>>(a.k, a.d, a.credit_b, a.b_bstride, G);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (use_product(a)) {
+    // partials of k_q2_rows: one per 256 tokens (fewer than the large kernel's, which the
+    // workspace holds); the product's statistics and partial sums after them
+    char* pw = (char*)partial + align256(sizeof(double) * a.nb * parts);
+    SoftmaxProductArgs sp{a.stream, a.n, a.C, a.logits, a.logits_dtype, a.ld_logits, a.labels, a.w,
+                          (const uint16_t*)a.credit_a, a.nb, a.k, a.nb > 1 ? a.a_bstride : 0, a.y_out, a.k,
+                          a.y_bstride, a.dev_info, pw};
+    if ((e = launch_softmax_product(sp)) != hipSuccess) return e;
+    dim3 gq((unsigned)((a.n + 255) / 256), (unsigned)a.nb);
+    k_q2_rows<<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, gq.x, partial, a.mb_out, a.dev_info);
+    if (a.e_out) {
+      const float* msv = (const float*)pw;  // (m, s) per token, first in the product's workspace
+      dim3 g2((unsigned)((a.C + 255) / 256 < 64 ? (a.C + 255) / 256 : 64), (unsigned)a.n);
+      if (a.logits_dtype == LOCA_BF16)
+        k_error_write_e<uint16_t><<<g2, 256, 0, a.stream>>>(a.n, a.C, (const uint16_t*)a.logits, a.ld_logits,
+                                                             a.labels, a.w, msv, a.e_out);
+      else
+        k_error_write_e<float><<<g2, 256, 0, a.stream>>>(a.n, a.C, (const float*)a.logits, a.ld_logits, a.labels,
+                                                          a.w, msv, a.e_out);
+    }
+    return hipGetLastError();
+  }
   const bool zb = a.logits_dtype == LOCA_BF16, ab = a.a_dtype == LOCA_BF16;
   if (!zb && !ab) return dispatch_error<float, float>(a, G, partial, ms);
   if (!zb && ab) return dispatch_error<float, uint16_t>(a, G, partial, ms);

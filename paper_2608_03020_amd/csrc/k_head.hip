@@ -13,6 +13,10 @@
 //      (about 16 significant bits), each multiplied by the exact bf16 W_u on the matrix
 //      cores (v_mfma_f32_32x32x16_bf16; W_u read transposed from LDS);
 //   3. k_top_error_reduce: e = sum_z part_z in a fixed order (fp64), minus w_t W_u[y_t].
+//
+// The same product serves the folded order for a large vocabulary (loca_error_targets
+// with bf16 A~): the right operand is then the blocks' A~ side by side (column j of
+// group j / kc), so one launch forms Y_b = E A~_b for every block.
 #include <algorithm>
 
 #include "loca_common.h"
@@ -93,13 +97,16 @@ LOCA_DEV void load8(const float* p, float (&v)[8]) {
   v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
-// Tiles of 128 tokens x 128 hidden columns, one vocabulary chunk per grid.z; 2 x 2 waves of
-// 64 x 64.  Requires ld % 8 == 0 (bf16) or % 4 == 0 (f32), d % 8 == 0, kchunk % 32 == 0.
+// Tiles of 128 tokens x 128 columns, one vocabulary chunk per grid.z; 2 x 2 waves of 64 x 64.
+// Column j of the right operand is column j % kc of group j / kc: W + (j / kc) w_bstride
+// (V x kc bf16 each).  d = total columns.  Requires ld % 8 == 0 (bf16) or % 4 == 0 (f32),
+// kc % 8 == 0, d % kc == 0, kchunk % 32 == 0.
 template <typename LT>
 __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, int64_t d, const LT* __restrict__ z,
                                                         int64_t ld, const float* __restrict__ w,
                                                         const float* __restrict__ ms, const uint16_t* __restrict__ wu,
-                                                        int64_t kchunk, float* __restrict__ part) {
+                                                        int64_t kc, int64_t w_bstride, int64_t kchunk,
+                                                        float* __restrict__ part) {
   __shared__ __attribute__((aligned(16))) uint16_t sAh[2][kHM * kLDA];
   __shared__ __attribute__((aligned(16))) uint16_t sAl[2][kHM * kLDA];
   __shared__ __attribute__((aligned(16))) uint16_t sB[2][kHK * kLDB];
@@ -151,7 +158,8 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
       ph[q] = make_uint4(h[0], h[1], h[2], h[3]);
       pl[q] = make_uint4(l[0], l[1], l[2], l[3]);
       const int64_t cr = c0 + brow[q], j = j0 + bcol[q];
-      wb[q] = (cr < ce && j < d) ? *(const uint4*)(wu + cr * d + j) : make_uint4(0, 0, 0, 0);
+      const int64_t grp = j / kc, jc = j - grp * kc;
+      wb[q] = (cr < ce && j < d) ? *(const uint4*)(wu + grp * w_bstride + cr * kc + jc) : make_uint4(0, 0, 0, 0);
     }
   };
   auto store_stage = [&](int buf) {
@@ -217,18 +225,21 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
       }
 }
 
-// e[t][j] = sum_z part_z[t][j] (fp64, in order) - w_t W_u[y_t][j]
+// out[(j / kc) o_bstride + t ld_o + j % kc] = sum_z part_z[t][j] (fp64, in order) - w_t W[y_t][j]
 __global__ void k_top_error_reduce(int64_t n, int64_t d, int nsplit, const float* __restrict__ part,
                                    const float* __restrict__ w, const int32_t* __restrict__ labels, int64_t V,
-                                   const uint16_t* __restrict__ wu, float* __restrict__ e_out, int64_t ld_e) {
+                                   const uint16_t* __restrict__ wu, int64_t kc, int64_t w_bstride,
+                                   float* __restrict__ out, int64_t ld_o, int64_t o_bstride) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= n * d) return;
   const int64_t t = e / d, j = e % d;
+  const int64_t grp = j / kc, jc = j - grp * kc;
   double s = 0.0;
   for (int zc = 0; zc < nsplit; ++zc) s += (double)part[(int64_t)zc * n * d + e];
   const int32_t yt = labels[t];
-  if (yt >= 0 && yt < V) s -= (double)(w ? w[t] : 1.f) * (double)bf16_to_f32(wu[(int64_t)yt * d + j]);
-  e_out[t * ld_e + j] = (float)s;
+  if (yt >= 0 && yt < V)
+    s -= (double)(w ? w[t] : 1.f) * (double)bf16_to_f32(wu[grp * w_bstride + (int64_t)yt * kc + jc]);
+  out[grp * o_bstride + t * ld_o + jc] = (float)s;
 }
 
 int head_splits(int64_t n, int64_t V, int64_t d) {
@@ -241,34 +252,44 @@ int head_splits(int64_t n, int64_t V, int64_t d) {
 
 }  // namespace
 
-size_t top_error_ws(int64_t n, int64_t V, int64_t d) {
-  return align256(sizeof(float) * 2 * n) + align256(sizeof(float) * (size_t)head_splits(n, V, d) * n * d);
+size_t softmax_product_ws(int64_t n, int64_t V, int64_t cols) {
+  return align256(sizeof(float) * 2 * n) + align256(sizeof(float) * (size_t)head_splits(n, V, cols) * n * cols);
 }
 
-hipError_t launch_top_error(const TopErrorArgs& a) {
+hipError_t launch_softmax_product(const SoftmaxProductArgs& a) {
   float* ms = (float*)a.ws;
   float* part = (float*)(a.ws + align256(sizeof(float) * 2 * a.n));
-  const int ns = head_splits(a.n, a.V, a.d);
+  const int64_t cols = a.groups * a.kc;
+  const int ns = head_splits(a.n, a.V, cols);
   const int64_t kchunk = ((a.V + ns - 1) / ns + kHK - 1) / kHK * kHK;
   hipStream_t st = a.stream;
-  k_fill_i32_head<<<1, 64, 0, st>>>(a.dev_info);
-  dim3 g((unsigned)((a.n + kHM - 1) / kHM), (unsigned)((a.d + kHN - 1) / kHN), (unsigned)ns);
+  dim3 g((unsigned)((a.n + kHM - 1) / kHM), (unsigned)((cols + kHN - 1) / kHN), (unsigned)ns);
   if (a.logits_dtype == LOCA_BF16) {
     k_softmax_stats<uint16_t><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, (const uint16_t*)a.logits, a.ld_logits,
                                                              a.labels, ms, a.dev_info);
-    k_top_error_gemm<uint16_t><<<g, kHT, 0, st>>>(a.n, a.V, a.d, (const uint16_t*)a.logits, a.ld_logits, a.w, ms,
-                                                  (const uint16_t*)a.wu, kchunk, part);
+    k_top_error_gemm<uint16_t><<<g, kHT, 0, st>>>(a.n, a.V, cols, (const uint16_t*)a.logits, a.ld_logits, a.w, ms,
+                                                  a.W, a.kc, a.w_bstride, kchunk, part);
   } else {
     k_softmax_stats<float><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, (const float*)a.logits, a.ld_logits, a.labels,
                                                           ms, a.dev_info);
-    k_top_error_gemm<float><<<g, kHT, 0, st>>>(a.n, a.V, a.d, (const float*)a.logits, a.ld_logits, a.w, ms,
-                                               (const uint16_t*)a.wu, kchunk, part);
+    k_top_error_gemm<float><<<g, kHT, 0, st>>>(a.n, a.V, cols, (const float*)a.logits, a.ld_logits, a.w, ms, a.W,
+                                               a.kc, a.w_bstride, kchunk, part);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  k_top_error_reduce<<<(unsigned)((a.n * a.d + 255) / 256), 256, 0, st>>>(
-      a.n, a.d, ns, part, a.w, a.labels, a.V, (const uint16_t*)a.wu, a.e_out, a.ld_e);
-  e = hipGetLastError();
+  k_top_error_reduce<<<(unsigned)((a.n * cols + 255) / 256), 256, 0, st>>>(
+      a.n, cols, ns, part, a.w, a.labels, a.V, a.W, a.kc, a.w_bstride, a.out, a.ld_o, a.o_bstride);
+  return hipGetLastError();
+}
+
+size_t top_error_ws(int64_t n, int64_t V, int64_t d) { return softmax_product_ws(n, V, d); }
+
+hipError_t launch_top_error(const TopErrorArgs& a) {
+  hipStream_t st = a.stream;
+  k_fill_i32_head<<<1, 64, 0, st>>>(a.dev_info);
+  SoftmaxProductArgs p{st, a.n, a.V, a.logits, a.logits_dtype, a.ld_logits, a.labels, a.w, (const uint16_t*)a.wu,
+                       1, a.d, 0, a.e_out, a.ld_e, 0, a.dev_info, a.ws};
+  hipError_t e = launch_softmax_product(p);
   if (e != hipSuccess) return e;
   k_finish_info_head<<<1, 64, 0, st>>>(a.dev_info);
   return hipGetLastError();

@@ -172,6 +172,22 @@ struct TopErrorArgs {
 size_t top_error_ws(int64_t n, int64_t V, int64_t d);
 hipError_t launch_top_error(const TopErrorArgs& a);
 
+// out_g = w (softmax(z) - onehot(y)) W_g for `groups` right operands W_g (V x kc bf16, stride
+// w_bstride), one matrix-core product over the vocabulary; the softmax statistics go to the
+// workspace, bad labels to dev_info (atomicMin of 1 + row; the caller initialises it).
+struct SoftmaxProductArgs {
+  hipStream_t stream;
+  int64_t n, V;
+  const void* logits; loca_dtype logits_dtype; int64_t ld_logits;
+  const int32_t* labels; const float* w;
+  const uint16_t* W; int64_t groups, kc, w_bstride;
+  float* out; int64_t ld_o, o_bstride;
+  int32_t* dev_info;
+  char* ws;
+};
+size_t softmax_product_ws(int64_t n, int64_t V, int64_t cols);
+hipError_t launch_softmax_product(const SoftmaxProductArgs& a);
+
 struct CreditArgs {
   hipStream_t stream;
   int64_t nb, n, d, k;

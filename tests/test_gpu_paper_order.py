@@ -102,20 +102,25 @@ def test_credit_from_top_error_parity(nb, n, d, k):
         assert ey <= TOL and eq <= TOL
 
 
-def test_paper_order_matches_folded_order():
+@pytest.mark.parametrize("adt", ["f32", "bf16"])
+def test_paper_order_matches_folded_order(adt):
     """The same credit coordinates two ways on the GPU: the paper's order (top error once,
-    then V_k^T e per block) and the folded factor A~ = W_u V_k in the error kernel."""
+    then V_k^T e per block) and the folded factor A~ = W_u V_k in the error kernel (fp32 A~:
+    the streaming large-vocabulary kernel; bf16 A~: one matrix-core product for all blocks,
+    compared with the oracle's folded order on the same bf16 A~)."""
     import torch
     import oracle
     from paper_2608_03020_amd import loca
     nb, n, V, d, k = 3, 257, 3000, 128, 16
-    log(f"case paper_vs_folded: nb={nb} n={n} V={V} d={d} k={k}")
+    log(f"case paper_vs_folded: nb={nb} n={n} V={V} d={d} k={k} A~ {adt}")
     z, y, w, Wu = _inputs(n, V, d, "f32", seed=34)
     rng = np.random.default_rng(35)
     Vk = (rng.standard_normal((nb, d, k)) / np.sqrt(d)).astype(np.float32)
     B = (rng.standard_normal((nb, k, d)) / np.sqrt(k)).astype(np.float32)
     Wu64 = gen.as_f64(Wu, "bf16")
     At = np.stack([(Wu64 @ Vk[b].astype(np.float64)).astype(np.float32) for b in range(nb)])
+    if adt == "bf16":
+        At = gen.bf16_bits(At)
     dev = "cuda"
     z_d, y_d, w_d = to_dev(z, dev), to_dev(y, dev), to_dev(w, dev)
     e = torch.empty((n, d), dtype=torch.float32, device=dev)
@@ -132,12 +137,15 @@ def test_paper_order_matches_folded_order():
     torch.cuda.synchronize()
     assert int(info.item()) == 0
     e_ref = oracle.top_error(z.astype(np.float64), y, Wu64, w.astype(np.float64))
+    E_ref = oracle.head_error(z.astype(np.float64), y, w.astype(np.float64))
     for b in range(nb):
         Y_ref, Q_ref = oracle.credit_from_top_error(e_ref, Vk[b], B[b])
+        Yf_ref, Qf_ref = oracle.credit(E_ref, gen.as_f64(At[b], adt), B[b])
         ep = rel(Yp[b].double().cpu().numpy(), Y_ref)
-        ef = rel(Yf[b].double().cpu().numpy(), Y_ref)
+        ef = rel(Yf[b].double().cpu().numpy(), Yf_ref)
         q2 = float(np.sum(Q_ref ** 2))
+        q2f = float(np.sum(Qf_ref ** 2))
         eqp = abs(mbp[b, 0].item() - q2) / q2
-        eqf = abs(mbf[b, 0].item() - q2) / q2
+        eqf = abs(mbf[b, 0].item() - q2f) / q2f
         log(f"paper_vs_folded block {b}: Y paper {ep:.2e}, Y folded {ef:.2e}, q2 paper {eqp:.2e}, folded {eqf:.2e}")
         assert max(ep, ef, eqp, eqf) <= TOL
