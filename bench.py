@@ -186,7 +186,7 @@ def next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream):
 
     # outer step with a current adapter W_prev = Lp Rp of rank r_a
     r_prev = cfg.r_a
-    if r_prev + cfg.k <= 64:
+    if r_prev + cfg.k <= 128:
         lp, rp = gen.torch_gen_current_adapter(cfg, nb, r_prev)
         step2 = BlockStep(cfg, nb, torch.device("cuda:0"), r_prev=r_prev)
         sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]

@@ -186,7 +186,7 @@ loca_status loca_ridge_solve(loca_stream_t stream, int64_t nb, int64_t d, int64_
  * Directions with zero singular value (W has rank < r_a) get zero rows/cols.
  * w_dense_out : optional d x d W_{r_a} (float), stride w_bstride.
  * dev_info : nm int32, 0 (reserved for future conditions).
- * Limits: kp <= 64, r_a <= kp, kp <= d.
+ * Limits: kp <= 128, r_a <= kp, r_a <= 64, kp <= d.
  * ------------------------------------------------------------------------- */
 loca_status loca_lowrank_truncate(loca_stream_t stream, int64_t nm, int64_t d, int64_t kp,
                                   int64_t r_a, const float* m, int64_t m_bstride, const float* r,

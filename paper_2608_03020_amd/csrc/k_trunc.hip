@@ -9,7 +9,10 @@
 //   U = M Vb H Vp diag(1/s),   V = R^T Vb H^{-1} Vp,
 //   a_out = U_r^T = Ca M^T,    b_out = V_r diag(s_r) = R^T Cb
 // with small Ca (r x kp) and Cb (kp x r).  Both eigendecompositions are
-// cyclic Jacobi in fp64 inside one workgroup (kp <= 64).
+// cyclic Jacobi in fp64 inside one workgroup: for kp <= 64 with both matrices in
+// LDS; for 64 < kp <= 128 with the symmetric matrix packed in LDS (fp64), the
+// eigenvectors in LDS as floats (rotations computed in fp64), and the kp x kp
+// intermediates in the workspace.
 #include "loca_common.h"
 
 namespace loca {
@@ -18,15 +21,18 @@ namespace {
 
 constexpr int kT = 256;
 constexpr int kMaxKp = 64;
+constexpr int kMaxKpBig = 128;
 
 // Partial Gm = M^T M and Gb = R R^T (fp64) over the row range of blockIdx.z (of nsplit
 // equal ranges of 32-row multiples); blockIdx.x = matrix, blockIdx.y = 0 (M) / 1 (R).
 // The partials are summed in a fixed order by k_trunc_core.
+template <int KPM>
 __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const float* __restrict__ M,
                                                     int64_t m_bstride, const float* __restrict__ R,
                                                     int64_t r_bstride, int64_t r_group, int nsplit,
                                                     double* __restrict__ Gpart) {
   constexpr int kRows = 32;
+  constexpr int kMaxKp = KPM;
   __shared__ double sX[kRows][kMaxKp + 1];
   const int64_t mi = blockIdx.x;
   const bool isR = blockIdx.y == 1;
@@ -138,6 +144,252 @@ LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* p
       __syncthreads();
     }
   }
+}
+
+// ------------------------------------------------------------------ 64 < kp <= 128
+
+// Upper-triangle packed index of (i, j) in either order, n x n.
+LOCA_DEV int pk(int i, int j, int n) {
+  if (i > j) { const int t = i; i = j; j = t; }
+  return i * n - (i * (i - 1)) / 2 + (j - i);
+}
+
+// Cyclic Jacobi on the packed symmetric n x n matrix A (n even), eigenvectors into the
+// float n x n V (row-major, columns are the vectors; rotations computed in fp64).  Each
+// round rotates the n/2 disjoint pairs of the same round-robin order as jacobi_eig, as
+// one two-sided update: every 2 x 2 block of rows {p_k, q_k} and columns {p_l, q_l} is
+// owned by one thread and becomes J_k^T B J_l.  Run by the kTC threads of one workgroup.
+LOCA_DEV void jacobi_packed(double* A, float* V, int n, double* cs, int* pairs, double* red) {
+  const int tid = threadIdx.x, m = n / 2;
+  for (int e = tid; e < n * n; e += kTC) V[e] = ((e / n) == (e % n)) ? 1.f : 0.f;
+  __syncthreads();
+  for (int sweep = 0; sweep < 40; ++sweep) {
+    double off = 0.0, tot = 0.0;
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      const double v = A[pk(i, j, n)];
+      tot += v * v;
+      if (i != j) off += v * v;
+    }
+    const double offs = block_sum(off, red);
+    __syncthreads();
+    const double tots = block_sum(tot, red + 4);
+    if (tid == 0) red[8] = (offs <= 1e-30 * tots || tots == 0.0) ? 1.0 : 0.0;
+    __syncthreads();
+    if (red[8] != 0.0) break;
+    for (int round = 0; round < n - 1; ++round) {
+      if (tid < m) {
+        auto pos = [&](int x) { return x == 0 ? 0 : 1 + ((x - 1 + round) % (n - 1)); };
+        int p = pos(tid), q = pos(n - 1 - tid);
+        if (p > q) { const int t = p; p = q; q = t; }
+        pairs[2 * tid] = p;
+        pairs[2 * tid + 1] = q;
+        const double apq = A[pk(p, q, n)], app = A[pk(p, p, n)], aqq = A[pk(q, q, n)];
+        double c = 1.0, s = 0.0;
+        if (fabs(apq) > 1e-300 && fabs(apq) > 1e-18 * sqrt(fabs(app * aqq))) {
+          const double tau = (aqq - app) / (2.0 * apq);
+          const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
+          c = 1.0 / sqrt(1.0 + t * t);
+          s = t * c;
+        }
+        cs[2 * tid] = c;
+        cs[2 * tid + 1] = s;
+      }
+      __syncthreads();
+      for (int e = tid; e < m * m; e += kTC) {
+        const int k = e / m, l = e % m;
+        if (k > l) continue;
+        const int pk_ = pairs[2 * k], qk_ = pairs[2 * k + 1], pl_ = pairs[2 * l], ql_ = pairs[2 * l + 1];
+        const double ck = cs[2 * k], sk = cs[2 * k + 1], cl = cs[2 * l], sl = cs[2 * l + 1];
+        const double b00 = A[pk(pk_, pl_, n)], b01 = A[pk(pk_, ql_, n)];
+        const double b10 = A[pk(qk_, pl_, n)], b11 = A[pk(qk_, ql_, n)];
+        const double x00 = cl * b00 - sl * b01, x01 = sl * b00 + cl * b01;  // B J_l
+        const double x10 = cl * b10 - sl * b11, x11 = sl * b10 + cl * b11;
+        const double y00 = ck * x00 - sk * x10, y01 = ck * x01 - sk * x11;  // J_k^T B J_l
+        const double y10 = sk * x00 + ck * x10, y11 = sk * x01 + ck * x11;
+        if (k == l) {
+          A[pk(pk_, pk_, n)] = y00;
+          A[pk(qk_, qk_, n)] = y11;
+          A[pk(pk_, qk_, n)] = 0.0;
+        } else {
+          A[pk(pk_, pl_, n)] = y00;
+          A[pk(pk_, ql_, n)] = y01;
+          A[pk(qk_, pl_, n)] = y10;
+          A[pk(qk_, ql_, n)] = y11;
+        }
+      }
+      for (int e = tid; e < n * m; e += kTC) {  // V <- V J
+        const int i = e / m, k = e % m;
+        const int p = pairs[2 * k], q = pairs[2 * k + 1];
+        const double c = cs[2 * k], s = cs[2 * k + 1];
+        const double vip = V[i * n + p], viq = V[i * n + q];
+        V[i * n + p] = (float)(c * vip - s * viq);
+        V[i * n + q] = (float)(s * vip + c * viq);
+      }
+      __syncthreads();
+    }
+  }
+}
+
+// The truncation core for 64 < kp <= 128 (see the file comment).  Per matrix the workspace
+// `big` holds Gm and T = Gm Vb (n x n fp64 each, n = kp rounded up to even) and a float copy
+// of Vb: big + mi * 2 kMaxKpBig^2 doubles, then after nm such pairs the float copies.
+__global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, int64_t r_a,
+                                                        const double* __restrict__ Gpart, int nsplit,
+                                                        double* __restrict__ big, double* __restrict__ Ca_all,
+                                                        double* __restrict__ Cb_all, float* __restrict__ sigma_out,
+                                                        int64_t sigma_bstride) {
+  constexpr int KB2 = kMaxKpBig * kMaxKpBig;
+  __shared__ double sA[kMaxKpBig * (kMaxKpBig + 1) / 2];
+  __shared__ float sV[KB2];
+  __shared__ double sH[kMaxKpBig], sHi[kMaxKpBig], sEig[kMaxKpBig];
+  __shared__ int sOrd[kMaxKpBig];
+  __shared__ double cs[kMaxKpBig];
+  __shared__ int pairs[kMaxKpBig];
+  __shared__ double red[16];
+  const int64_t mi = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int K = (int)kp;
+  const int n = K + (K & 1);
+  double* Gm = big + mi * 2 * KB2;
+  double* T = Gm + KB2;
+  float* Vs = (float*)(big + nm * 2 * KB2) + mi * KB2;
+  const double* GmP = Gpart + (mi * 2) * nsplit * kp * kp;
+  const double* GbP = Gpart + (mi * 2 + 1) * nsplit * kp * kp;
+  // 1. Gb into sA (packed), Gm into the workspace, each summed over the row ranges in order
+  for (int e = tid; e < n * n; e += kTC) {
+    const int i = e / n, j = e % n;
+    double gb = 0.0, gm = 0.0;
+    if (i < K && j < K)
+      for (int z = 0; z < nsplit; ++z) {
+        gb += GbP[z * kp * kp + i * kp + j];
+        gm += GmP[z * kp * kp + i * kp + j];
+      }
+    Gm[i * n + j] = gm;
+    if (i <= j) sA[pk(i, j, n)] = gb;
+  }
+  __threadfence();
+  __syncthreads();
+  jacobi_packed(sA, sV, n, cs, pairs, red);
+  __syncthreads();
+  if (tid == 0) {
+    double lmax = 0.0;
+    for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
+    red[12] = lmax;
+  }
+  __syncthreads();
+  for (int j = tid; j < n; j += kTC) {
+    const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
+    const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
+    sH[j] = keep ? sqrt(lb) : 0.0;
+    sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+  }
+  // 2. keep Vb; T = Gm Vb; P = H Vb^T T H into sA
+  for (int e = tid; e < n * n; e += kTC) Vs[e] = sV[e];
+  for (int e = tid; e < n * n; e += kTC) {
+    const int i = e / n, j = e % n;
+    double s = 0.0;
+    for (int c = 0; c < n; ++c) s += Gm[i * n + c] * (double)sV[c * n + j];
+    T[i * n + j] = s;
+  }
+  __threadfence();
+  __syncthreads();
+  for (int e = tid; e < n * n; e += kTC) {
+    const int i = e / n, j = e % n;
+    if (i > j) continue;
+    double s = 0.0;
+    for (int c = 0; c < n; ++c) s += (double)sV[c * n + i] * T[c * n + j];
+    sA[pk(i, j, n)] = s * sH[i] * sH[j];
+  }
+  __syncthreads();
+  jacobi_packed(sA, sV, n, cs, pairs, red);  // sV = Vp
+  __syncthreads();
+  if (tid == 0) {
+    for (int j = 0; j < K; ++j) { sEig[j] = sA[pk(j, j, n)]; sOrd[j] = j; }
+    for (int i = 1; i < K; ++i) {
+      const int key = sOrd[i];
+      int j = i - 1;
+      while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
+      sOrd[j + 1] = key;
+    }
+  }
+  __syncthreads();
+  const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
+  for (int j = tid; j < K; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
+  // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
+  double* Ca = Ca_all + mi * r_a * kp;
+  double* Cb = Cb_all + mi * kp * r_a;
+  for (int e = tid; e < (int)(r_a * kp); e += kTC) {
+    const int a = e / K, c = e % K;
+    const int col = sOrd[a];
+    const double sa = sqrt(fmax(sEig[col], 0.0));
+    double u = 0.0, v = 0.0;
+    for (int x = 0; x < n; ++x) {
+      const double vb = (double)Vs[c * n + x], vp = (double)sV[x * n + col];
+      u += vb * sH[x] * vp;
+      v += vb * sHi[x] * vp;
+    }
+    const bool live = sa > 1e-30 * s1 && sa > 0.0;
+    Ca[a * kp + c] = live ? u / sa : 0.0;
+    Cb[c * r_a + a] = live ? v * sa : 0.0;
+  }
+}
+
+// a_out[a][i] = sum_c Ca[a][c] M[i][c];  b_out[i][a] = sum_c R[c][i] Cb[c][a]  for kp <= 128,
+// r_a <= 64: 64 rows i per workgroup, kp in chunks of 32 through LDS; thread t owns row
+// t % 64 and the ranks a = t / 64 + 4u (fp64 sums in the order of c).
+__global__ __launch_bounds__(kT) void k_trunc_apply_tiled(int64_t d, int64_t kp, int64_t r_a,
+                                                          const float* __restrict__ M, int64_t m_bstride,
+                                                          const float* __restrict__ R, int64_t r_bstride,
+                                                          int64_t r_group, const double* __restrict__ Ca_all,
+                                                          const double* __restrict__ Cb_all, float* __restrict__ a_out,
+                                                          int64_t a_bstride, float* __restrict__ b_out,
+                                                          int64_t b_bstride) {
+  __shared__ float sM[64][33];
+  __shared__ float sR[32][65];
+  __shared__ double sCa[64][33];
+  __shared__ double sCb[32][65];
+  const int64_t mi = blockIdx.y;
+  const int64_t i0 = (int64_t)blockIdx.x * 64;
+  const int tid = threadIdx.x, r = tid & 63, q = tid >> 6;
+  const float* Mm = M + mi * m_bstride;
+  const float* Rm = R + (mi / r_group) * r_bstride;
+  const double* Ca = Ca_all + mi * r_a * kp;
+  const double* Cb = Cb_all + mi * kp * r_a;
+  double sa[16], sb[16];
+#pragma unroll
+  for (int u = 0; u < 16; ++u) { sa[u] = 0.0; sb[u] = 0.0; }
+  for (int64_t c0 = 0; c0 < kp; c0 += 32) {
+    __syncthreads();
+    for (int e = tid; e < 64 * 32; e += kT) {
+      const int rr = e / 32, cc = e % 32;
+      sM[rr][cc] = (i0 + rr < d && c0 + cc < kp) ? Mm[(i0 + rr) * kp + c0 + cc] : 0.f;
+      const int cr = e / 64, ir = e % 64;
+      sR[cr][ir] = (i0 + ir < d && c0 + cr < kp) ? Rm[(c0 + cr) * d + i0 + ir] : 0.f;
+      sCa[rr][cc] = (rr < r_a && c0 + cc < kp) ? Ca[rr * kp + c0 + cc] : 0.0;
+      sCb[cr][ir] = (ir < r_a && c0 + cr < kp) ? Cb[(c0 + cr) * r_a + ir] : 0.0;
+    }
+    __syncthreads();
+    for (int cc = 0; cc < 32; ++cc) {
+      const double mv = (double)sM[r][cc], rv = (double)sR[cc][r];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int a = q + 4 * u;
+        sa[u] += sCa[a][cc] * mv;
+        sb[u] += rv * sCb[cc][a];
+      }
+    }
+  }
+  const int64_t i = i0 + r;
+  if (i < d)
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int a = q + 4 * u;
+      if (a < r_a) {
+        a_out[mi * a_bstride + a * d + i] = (float)sa[u];
+        b_out[mi * b_bstride + i * r_a + a] = (float)sb[u];
+      }
+    }
 }
 
 // One workgroup per matrix: eigendecompositions and the small factors Ca, Cb.
@@ -337,6 +589,8 @@ int trunc_splits(int64_t d) {
 size_t lowrank_truncate_ws(int64_t nm, int64_t d, int64_t kp, int64_t r_a) {
   size_t s = align256(sizeof(double) * nm * 2 * trunc_splits(d) * kp * kp);
   s += 2 * align256(sizeof(double) * nm * kp * r_a);
+  if (kp > kMaxKp)  // Gm, T (fp64) and the float copy of Vb per matrix
+    s += align256(sizeof(double) * nm * 2 * kMaxKpBig * kMaxKpBig) + align256(sizeof(float) * nm * kMaxKpBig * kMaxKpBig);
   return s;
 }
 
@@ -345,14 +599,25 @@ hipError_t launch_lowrank_truncate(const TruncArgs& a) {
   const int ns = trunc_splits(a.d);
   double* Gpart = (double*)p; p += align256(sizeof(double) * a.nm * 2 * ns * a.kp * a.kp);
   double* Ca = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.r_a);
-  double* Cb = (double*)p;
+  double* Cb = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.r_a);
   k_fill_zero<<<(unsigned)((a.nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, a.nm);
-  k_small_grams<<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(a.d, a.kp, a.m, a.m_bstride, a.r,
-                                                                             a.r_bstride, a.r_group, ns, Gpart);
-  k_trunc_core<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.kp, a.r_a, Gpart, ns, Ca, Cb, a.sigma_out, a.sigma_bstride);
-  k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm), kT, 0, a.stream>>>(
-      a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
-      a.b_bstride);
+  if (a.kp <= kMaxKp) {
+    k_small_grams<kMaxKp><<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(
+        a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, ns, Gpart);
+    k_trunc_core<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.kp, a.r_a, Gpart, ns, Ca, Cb, a.sigma_out, a.sigma_bstride);
+    k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm), kT, 0, a.stream>>>(
+        a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
+        a.b_bstride);
+  } else {
+    double* big = (double*)p;
+    k_small_grams<kMaxKpBig><<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(
+        a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, ns, Gpart);
+    k_trunc_core_big<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.nm, a.kp, a.r_a, Gpart, ns, big, Ca, Cb, a.sigma_out,
+                                                           a.sigma_bstride);
+    k_trunc_apply_tiled<<<dim3((unsigned)((a.d + 63) / 64), (unsigned)a.nm), kT, 0, a.stream>>>(
+        a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
+        a.b_bstride);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !a.w_dense_out) return e;
   // W_r[i][j] = sum_a a_out[a][i] b_out[j][a]

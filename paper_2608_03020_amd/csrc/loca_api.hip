@@ -10,7 +10,8 @@ using namespace loca;
 namespace {
 
 constexpr int64_t kMaxK = 128;
-constexpr int64_t kMaxKpTrunc = 64;
+constexpr int64_t kMaxKpTrunc = 128;
+constexpr int64_t kMaxRankTrunc = 64;
 constexpr int64_t kMaxLambdas = 8;
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
@@ -152,7 +153,7 @@ loca_status loca_lowrank_truncate(loca_stream_t stream, int64_t nm, int64_t d, i
     return LOCA_E_ARG;
   if (nm > r_group && r_bstride < kp * d) return LOCA_E_ARG;
   if (w_dense_out && nm > 1 && w_bstride < d * d) return LOCA_E_ARG;
-  if (kp > kMaxKpTrunc) return LOCA_E_UNSUPPORTED;
+  if (kp > kMaxKpTrunc || r_a > kMaxRankTrunc) return LOCA_E_UNSUPPORTED;
   if (nm > 65535 || d > 65535) return LOCA_E_UNSUPPORTED;
   loca_status st = check_ws(ws, ws_bytes, lowrank_truncate_ws(nm, d, kp, r_a));
   if (st != LOCA_OK) return st;
@@ -176,7 +177,7 @@ loca_status loca_ridge_solve_projected(loca_stream_t stream, int64_t nb, int64_t
                  (b_cur && bc_bstride < d * r_a)))
     return LOCA_E_ARG;
   if (nb * n_lambda > 1 && bo_bstride < d * r_a) return LOCA_E_ARG;
-  if (r_a > kMaxKpTrunc || k > kMaxK || n_lambda > kMaxLambdas) return LOCA_E_UNSUPPORTED;
+  if (r_a > kMaxRankTrunc || k > kMaxK || n_lambda > kMaxLambdas) return LOCA_E_UNSUPPORTED;
   if (nb * n_lambda > 65535) return LOCA_E_UNSUPPORTED;
   loca_status st = check_ws(ws, ws_bytes, projected_ws(nb, d, k, r_a, n_lambda));
   if (st != LOCA_OK) return st;

@@ -142,7 +142,9 @@ def test_lowrank_truncate_rejects(lib):
     assert call(kp=40, r_a=4) == lib.LOCA_E_ARG            # kp <= d
     assert call(r_group=0) == lib.LOCA_E_ARG
     assert call(m=None) == lib.LOCA_E_ARG
-    assert call(d=100, kp=65, r_a=4) == lib.LOCA_E_UNSUPPORTED
+    assert call(d=200, kp=129, r_a=4) == lib.LOCA_E_UNSUPPORTED  # kp <= 128
+    assert call(d=200, kp=100, r_a=65) == lib.LOCA_E_UNSUPPORTED  # r_a <= 64
+    assert call(d=100, kp=65, r_a=4) == lib.LOCA_E_WORKSPACE     # supported: only the workspace is missing
     assert call() == lib.LOCA_E_WORKSPACE
 
 

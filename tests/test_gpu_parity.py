@@ -85,8 +85,6 @@ CASES = {
 @pytest.mark.parametrize("name", list(CASES))
 def test_block_step_parity(name):
     cfg = CASES[name]
-    if cfg.k > 64:
-        pytest.skip("truncation supports kp <= 64 in this build")
     log(f"case {name}: d={cfg.d} n={cfg.n} C={cfg.C} k={cfg.k} blocks={cfg.blocks} mode={cfg.mode}")
     xs, zs, ys, As, Bs = host_inputs(cfg, range(cfg.blocks))
     g = run_gpu(cfg, xs, zs, ys, As, Bs)
@@ -97,7 +95,7 @@ def test_block_step_parity(name):
 
 
 def test_k96_credit_coordinates():
-    """k = 96: head error and statistics (truncation of kp > 64 is not built)."""
+    """k = 96: head error (the streaming kernel: k > 64 with an fp32 A~) and ||Q||^2."""
     import torch
     from paper_2608_03020_amd import loca
     import oracle
@@ -191,13 +189,15 @@ def test_ridge_solve_fp64_and_nonpd_pivot():
     assert info.item() == 71
 
 
-def test_truncation_matches_explicit_svd():
-    """Eckart-Young truncation of W = M B~ against the oracle's dense SVD (d <= 256)."""
+@pytest.mark.parametrize("d,kp,r", [(200, 24, 10), (200, 96, 40), (230, 127, 64), (150, 128, 16)])
+def test_truncation_matches_explicit_svd(d, kp, r):
+    """Eckart-Young truncation of W = M B~ against the oracle's dense SVD (d <= 256);
+    kp > 64 takes the packed-LDS eigensolver (odd kp padded, the largest kp and rank)."""
     import torch
     import oracle
     from paper_2608_03020_amd import loca
     rng = np.random.default_rng(1)
-    d, kp, r = 200, 24, 10
+    log(f"case truncation: d={d} kp={kp} r_a={r}")
     Mh = rng.normal(size=(d, kp)).astype(np.float32)
     Rh = rng.normal(size=(kp, d)).astype(np.float32)
     Wr_o, s_o = oracle.truncate_dense(Mh.astype(np.float64) @ Rh.astype(np.float64), r)
@@ -330,7 +330,7 @@ def test_statistics_deterministic_and_resumable():
     assert np.array_equal(S1[:, iu[0], iu[1]], S3[:, iu[0], iu[1]]) and np.array_equal(K1, K3)
 
 
-@pytest.mark.parametrize("mode", ["bf16", "fp32"])
+@pytest.mark.parametrize("mode", ["bf16", "fp32", "bf16_kp88"])
 def test_outer_step_with_current_adapter(mode):
     """Theorem S6.1 past the first outer step: (S + lam I) W = S W_prev + Z with a current
     adapter W_prev = Lp Rp != 0, solved in factored form M = (S + lam I)^{-1} [S Lp | K],
@@ -341,6 +341,9 @@ def test_outer_step_with_current_adapter(mode):
     if mode == "bf16":
         cfg = gen.custom_config("t14", blocks=2, d=288, n=900, micro=500, C=4, k=16, r_a=8, lambdas=(1e-2, 0.1))
         r_prev, tol = 6, 2e-3
+    elif mode == "bf16_kp88":  # r_prev + k = 88 > 64: the packed-LDS truncation
+        cfg = gen.custom_config("t14b", blocks=2, d=300, n=1200, micro=700, C=6, k=48, r_a=24, lambdas=(1e-2,))
+        r_prev, tol = 40, 2e-3
     else:
         cfg = gen.custom_config("t14f", blocks=2, d=150, n=300, micro=180, C=3, k=8, r_a=6, lambdas=(1e-2, 0.1),
                                 mode="fp32", x_dist="gauss_outlier")
@@ -348,7 +351,7 @@ def test_outer_step_with_current_adapter(mode):
     blocks = [0, 1]
     log(f"case outer_step {mode}: d={cfg.d} n={cfg.n} k={cfg.k} r_prev={r_prev} r_a={cfg.r_a} lambdas={cfg.lambdas}")
     xs, zs, ys, As, Bs = host_inputs(cfg, blocks)
-    xf = [[gen.as_f64(x, "bf16" if mode == "bf16" else "f32") for x in xs[b]] for b in blocks]
+    xf = [[gen.as_f64(x, "f32" if mode == "fp32" else "bf16") for x in xs[b]] for b in blocks]
     zf = [gen.as_f64(z, cfg.logit_dtype) for z in zs]
     frozen = [oracle.block_step(xf[b], zf, ys, gen.as_f64(As[b], cfg.a_dtype), np.asarray(Bs[b], np.float64),
                                 cfg.eta, (cfg.lambdas[0],), cfg.r_a) for b in blocks]
