@@ -82,6 +82,80 @@ __global__ __launch_bounds__(256) void k_equil_setup(int64_t d, int64_t m, int64
   }
 }
 
+// The same for float statistics and factors when d % 4 == 0 and the rows of S are 16-byte
+// aligned, tiled so that every workgroup has the same amount of work: a workgroup takes
+// kEqRows rows and one chunk of kEqCols columns (chunks wholly below the diagonal exit),
+// each thread four consecutive columns (16-byte loads and stores of S, D and F, one load
+// of S for all lambdas); the four-column group that holds the diagonal writes only its
+// entries on or above it.  The right-hand sides are written by the workgroups of the last
+// chunk (never wholly below the diagonal).
+// The arithmetic is that of k_equil_setup, term for term.
+constexpr int kEqCols = 1024;
+__global__ __launch_bounds__(256) void k_equil_setup_v4(int64_t d, int64_t m, int64_t r_prev,
+                                                        const float* __restrict__ S, int64_t s_bstride,
+                                                        const float* __restrict__ K, int64_t k_bstride,
+                                                        const double* __restrict__ SLp,
+                                                        const double* __restrict__ lam, int nl,
+                                                        const float* __restrict__ D, float* __restrict__ F,
+                                                        float* __restrict__ R) {
+  const int64_t b = blockIdx.z;
+  const int64_t k = m - r_prev;
+  const int64_t i0 = (int64_t)blockIdx.x * kEqRows;
+  const int64_t c0 = (int64_t)blockIdx.y * kEqCols;
+  if (c0 + kEqCols <= (i0 & ~(int64_t)3)) return;  // every row of the tile starts past this chunk
+  const int64_t j = c0 + 4 * threadIdx.x;
+  const bool jin = j < d;
+  // every global load of the tile is issued before the first use: the rows of S at this
+  // thread's four columns; per lambda, D at the columns and at the tile's rows
+  float4 sv[kEqRows];
+#pragma unroll
+  for (int ii = 0; ii < kEqRows; ++ii) {
+    const int64_t i = i0 + ii;
+    const bool need = jin && i < d && j + 3 >= i;
+    sv[ii] = *(const float4*)(S + b * s_bstride + (need ? i * d + j : 0));
+  }
+  for (int l = 0; l < nl; ++l) {
+    const int64_t mi = b * nl + l;
+    const float4 dj = *(const float4*)(D + mi * d + (jin ? j : 0));
+    float di[kEqRows];
+#pragma unroll
+    for (int ii = 0; ii < kEqRows; ++ii) di[ii] = D[mi * d + (i0 + ii < d ? i0 + ii : d - 1)];
+    const double li = lam[l];
+#pragma unroll
+    for (int ii = 0; ii < kEqRows; ++ii) {
+      const int64_t i = i0 + ii;
+      if (i < d && jin && j + 3 >= i) {
+        const double dd = (double)di[ii];
+        float o[4];
+        o[0] = (float)(dd * ((double)sv[ii].x + (j == i ? li : 0.0)) * (double)dj.x);
+        o[1] = (float)(dd * ((double)sv[ii].y + (j + 1 == i ? li : 0.0)) * (double)dj.y);
+        o[2] = (float)(dd * ((double)sv[ii].z + (j + 2 == i ? li : 0.0)) * (double)dj.z);
+        o[3] = (float)(dd * ((double)sv[ii].w + (j + 3 == i ? li : 0.0)) * (double)dj.w);
+        float* dst = F + mi * d * d + i * d + j;
+        if (j >= i) {
+          *(float4*)dst = make_float4(o[0], o[1], o[2], o[3]);
+        } else {
+#pragma unroll
+          for (int u = 1; u < 4; ++u)
+            if (j + u >= i) dst[u] = o[u];
+        }
+      }
+    }
+  }
+  if (blockIdx.y == gridDim.y - 1)  // the last chunk holds column d - 1 >= i of every row
+    for (int ii = 0; ii < kEqRows; ++ii) {
+      const int64_t i = i0 + ii;
+      if (i >= d) break;
+      for (int64_t c = threadIdx.x; c < m; c += blockDim.x) {
+        const double v = (c < r_prev) ? SLp[b * d * r_prev + i * r_prev + c] : (double)K[b * k_bstride + i * k + (c - r_prev)];
+        for (int l = 0; l < nl; ++l) {
+          const int64_t mi = b * nl + l;
+          R[mi * d * m + i * m + c] = (float)((double)D[mi * d + i] * v);
+        }
+      }
+    }
+}
+
 // SLp[b] = S_sym Lp (d x r_prev, fp64) from the upper triangle of S.  A workgroup owns 64
 // rows and RC columns of the product (grid: x over row tiles, y = block, z over column
 // chunks) and walks the 64-wide column tiles of S in order: tiles on or above the
@@ -438,12 +512,42 @@ __global__ __launch_bounds__(kT) void k_diag_f32(int64_t d, int64_t p, float* __
   const float* A0 = F + p * d + p;
   const int pw = (int)((d - p) < P ? (d - p) : P);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  for (int e = tid; e < P * P; e += kT) {
-    const int r = e >> 7, c = e & 127;
-    const bool in = r < pw && c < pw;
-    const float v = ld_or_zero(A0, (int64_t)r * d + c, in && c >= r);
-    sA[r * LD + c] = in ? v : (r == c ? 1.f : 0.f);
-    sX[r * LD + c] = 0.f;
+  // the block in 16 four-column chunks per thread, all loads issued before the first use
+  // (16-byte loads when the rows are 16-byte aligned and the chunk lies inside the block)
+  {
+    constexpr int NCH = P * P / 4 / kT;
+    float4 v[NCH];
+    if ((d & 3) == 0 && pw == P) {  // a whole block with 16-byte aligned rows
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) {
+        const int e = tid + kT * u, r = e >> 5, c = 4 * (e & 31);
+        v[u] = *(const float4*)(A0 + (int64_t)r * d + c);
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < NCH; ++u) {
+        const int e = tid + kT * u, r = e >> 5, c = 4 * (e & 31);
+        const int64_t o = (int64_t)r * d + c;
+        v[u].x = ld_or_zero(A0, o, r < pw && c < pw);
+        v[u].y = ld_or_zero(A0, o + 1, r < pw && c + 1 < pw);
+        v[u].z = ld_or_zero(A0, o + 2, r < pw && c + 2 < pw);
+        v[u].w = ld_or_zero(A0, o + 3, r < pw && c + 3 < pw);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int e = tid + kT * u, r = e >> 5, c = 4 * (e & 31);
+      const float in4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+      float o4[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int cc = c + t;
+        const bool in = r < pw && cc < pw;
+        o4[t] = in ? (cc >= r ? in4[t] : 0.f) : (r == cc ? 1.f : 0.f);
+      }
+      *(float4*)&sA[r * LD + c] = make_float4(o4[0], o4[1], o4[2], o4[3]);
+      *(float4*)&sX[r * LD + c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
   }
   __syncthreads();
   for (int q = 0; q < 4; ++q) {
@@ -488,9 +592,19 @@ __global__ __launch_bounds__(kT) void k_diag_f32(int64_t d, int64_t p, float* __
     }
   }
   __syncthreads();
-  for (int e = tid; e < P * P; e += kT) {
-    const int r = e >> 7, c = e & 127;
-    if (r < pw && c < pw) F[(p + r) * d + p + c] = c >= r ? sX[r * LD + c] : 0.f;
+  for (int e = tid; e < P * P / 4; e += kT) {
+    const int r = e >> 5, c = 4 * (e & 31);
+    if (r >= pw) continue;
+    const float4 x = *(const float4*)&sX[r * LD + c];
+    const float x4[4] = {c >= r ? x.x : 0.f, c + 1 >= r ? x.y : 0.f, c + 2 >= r ? x.z : 0.f, c + 3 >= r ? x.w : 0.f};
+    float* dst = F + (p + r) * d + p + c;
+    if ((d & 3) == 0 && c + 4 <= pw) {
+      *(float4*)dst = make_float4(x4[0], x4[1], x4[2], x4[3]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (c + t < pw) dst[t] = x4[t];
+    }
   }
 }
 
@@ -660,7 +774,7 @@ LOCA_DEV void split3(float a, uint16_t& h, uint16_t& m, uint16_t& l) {
 // operands with transpose reads (LD = 288: the four rows a half-wave reads start 64 bytes
 // apart modulo 256, so the reads are conflict-free).  Requires d % 4 == 0.
 constexpr int kX6BK = 16, kX6LD = 288;
-enum X6Mode { kX6Trail = 0, kX6Strip = 1, kX6Row = 2 };
+enum X6Mode { kX6Trail = 0, kX6Strip = 1, kX6Row = 2, kX6TrailRhs = 3 };
 
 LOCA_DEV float4 ld4_or_zero(const float* base, int64_t idx, bool ok) {
   const float4 v = *(const float4*)(base + (ok ? idx : 0));
@@ -671,23 +785,39 @@ LOCA_DEV float4 ld4_or_zero_ro(const float* __restrict__ base, int64_t idx, bool
 // Jobs past the nF tiles of F are right-hand-side jobs: the same product with Qn and the
 // output taken from R (d x m per matrix, m % 4 == 0): the 256-row block u of the trailing
 // region (kX6Trail), or the panel rows (kX6Strip, kX6Row), all m columns.
+// kX6TrailRhs: only the right-hand-side jobs of kX6Trail, in a layout for their few
+// columns: a workgroup takes 256 rows x 32 columns (eight waves of 32 x 32; columns
+// 32 blockIdx.z ..), so it does an eighth of the matrix-core work of a 256 x 256 tile.
+//
+// kX6Row with Pl != nullptr also writes the three bf16 parts of every U12 entry it forms
+// into the super-panel planes Pl[t][i - p0][j] (t = h, m, l; kPlaneRows rows of d columns
+// per plane, pl_bstride elements per matrix), the operands of k_syrk_x6_dl.
+constexpr int kPlaneRows = 4 * 128;  // rows of a super-panel (kSuper panels of 128)
 template <int MODE>
 __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t kw, int64_t off,
                                                   float* __restrict__ Fall, float* __restrict__ Rall, int64_t m,
-                                                  int nF) {
-  constexpr int BR = MODE == kX6Trail ? 256 : 128;  // output rows per tile
-  constexpr int BC = 256, WGN = 4, WM = BR / 2, WN = BC / WGN, NBM = WM / 32, NBN = WN / 32;
+                                                  int nF, uint16_t* __restrict__ Plall, int64_t pl_bstride,
+                                                  int64_t p0) {
+  constexpr bool RH = MODE == kX6TrailRhs;
+  constexpr int BR = (MODE == kX6Trail || RH) ? 256 : 128;  // output rows per tile
+  constexpr int BC = RH ? 32 : 256, WGN = RH ? 1 : 4, WGM = 8 / WGN;
+  constexpr int WM = BR / WGM, WN = BC / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int LD = kX6LD, PLANE = kX6BK * LD;
-  constexpr int QP = BR * kX6BK / 4 / 512, QQ = BC * kX6BK / 4 / 512;  // float4 loads per thread
+  constexpr int NQV = BC * kX6BK / 4;                                  // float4 values of a Qn stage
+  constexpr int QP = BR * kX6BK / 4 / 512, QQ = (NQV + 511) / 512;     // float4 loads per thread
   __shared__ __attribute__((aligned(16))) uint16_t sm[2][6 * PLANE];  // [buffer][operand * 3 + part]
   const int64_t mi = blockIdx.y;
   float* F = Fall + mi * d * d;
   float* R = Rall + mi * d * m;
-  const bool rhs = (int)blockIdx.x >= nF;
-  const int job = rhs ? (int)blockIdx.x - nF : (int)blockIdx.x;
+  const bool rhs = RH || (int)blockIdx.x >= nF;
+  const int job = rhs && !RH ? (int)blockIdx.x - nF : (int)blockIdx.x;
   int64_t orow, ocol, pcol;
   bool diag = false;
-  if (MODE == kX6Trail) {
+  if (RH) {
+    orow = off + (int64_t)job * BR;
+    ocol = (int64_t)blockIdx.z * BC;
+    pcol = orow;
+  } else if (MODE == kX6Trail) {
     if (rhs) {
       orow = off + (int64_t)job * BC;
       ocol = 0;
@@ -727,8 +857,8 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
     }
 #pragma unroll
     for (int q = 0; q < QQ; ++q) {
-      const int c = tid + 512 * q, kk = c >> 6, c4 = 4 * (c & 63);
-      rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * ldq + c4, kc0 + kk < kw && ocol + c4 < qend);
+      const int c = tid + 512 * q, kk = c / (BC / 4), c4 = 4 * (c % (BC / 4));
+      if (c < NQV) rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * ldq + c4, kc0 + kk < kw && ocol + c4 < qend);
     }
   };
   auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
@@ -751,7 +881,7 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
 #pragma unroll
     for (int q = 0; q < QQ; ++q) {
       const int c = tid + 512 * q;
-      put(&sm[buf][3 * PLANE], c >> 6, 4 * (c & 63), rq[q]);
+      if (c < NQV) put(&sm[buf][3 * PLANE], c / (BC / 4), 4 * (c % (BC / 4)), rq[q]);
     }
   };
 
@@ -812,6 +942,162 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
         const int64_t row = rb + mfma32_row(lane, r);
         if (row < rend && col < qend && (rhs || col >= row))
           Out[row * ldq + col] = MODE == kX6Row ? acc[a][b][r] : old[r] - acc[a][b][r];
+      }
+      if (MODE == kX6Row && !rhs && Plall != nullptr) {
+        uint16_t* Pl = Plall + mi * pl_bstride;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int64_t row = rb + mfma32_row(lane, r);
+          if (row < rend && col < qend) {
+            uint16_t h, mm, l;
+            split3(acc[a][b][r], h, mm, l);
+            const int64_t o = (row - p0) * d + col;
+            Pl[o] = h;
+            Pl[(int64_t)kPlaneRows * d + o] = mm;
+            Pl[(int64_t)2 * kPlaneRows * d + o] = l;
+          }
+        }
+      }
+    }
+}
+
+// ------------------------------------------------------------------ trailing update from split planes
+
+// The trailing update of a super-panel, F[i][j] -= sum_kk U[kk][i] U[kk][j] over its kw
+// rows kk, on the upper 256 x 256 tiles of the trailing region [off, d), with U given as
+// its three bf16 planes Pl[t][kk][j] (t = h, m, l, from the row-panel kernel).  The six
+// kept products of split3 are one product over a stacked K of 6 kw rows: the left operand
+// runs through the planes (l, h, m, m, h, h) and the right one through (h, l, m, h, m, h),
+// kw rows per plane pair (smallest terms first).  The operands are bf16 already, so they
+// stream into LDS by direct copies: tiles, waves, the four-slot ring of 32-row stages, the
+// swizzled layout, the fragment double-buffering and the spread of the copies between the
+// MFMA rows are those of the Gram kernel; diagonal tiles load both panels (the two
+// operands differ).  The workgroup order is XCD-aware over all matrices of the launch.
+// Requires d % 8 == 0, kw % 32 == 0, and a plane buffer of each matrix below 2^31 bytes.
+__global__ __launch_bounds__(512) void k_syrk_x6_dl(int64_t d, int64_t kw, int64_t off,
+                                                    const uint16_t* __restrict__ Plall, int64_t pl_bstride,
+                                                    float* __restrict__ Fall, int ntile) {
+  constexpr int kBK = 32, BM = 256, NT = 512, WGN = 4, WM = 128, WN = 64, NBM = WM / 32, NBN = WN / 32;
+  constexpr int TILE_ELEMS = kBK * BM;          // one panel stage (bf16 elements)
+  constexpr int NQ = TILE_ELEMS * 2 / 16 / NT;  // 16-byte copies per thread per panel
+  constexpr int NCP = 2 * NQ;                   // copies per thread per stage
+  constexpr int NSLOT = 2 * NBM;                // fragment rows of MFMAs per stage
+  constexpr int kStages = 4;
+  static_assert(NCP <= NSLOT, "at most one copy between two fragment rows");
+  // plane of each operand for the six plane pairs, two bits each (l = 2, h = 0, m = 1)
+  constexpr uint32_t kPA = 2u | (0u << 2) | (1u << 4) | (1u << 6) | (0u << 8) | (0u << 10);
+  constexpr uint32_t kPB = 0u | (2u << 2) | (1u << 4) | (0u << 6) | (1u << 8) | (0u << 10);
+  __shared__ __attribute__((aligned(1024))) uint16_t sb0[2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb1[2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb2[2 * TILE_ELEMS];
+  __shared__ __attribute__((aligned(1024))) uint16_t sb3[2 * TILE_ELEMS];
+
+  const int T = (int)((d - off + BM - 1) / BM);
+  const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  int I, J;
+  upper_tile_c(logical % ntile, T, I, J);
+  const int64_t mi = logical / ntile;
+  const uint16_t* Pl = Plall + mi * pl_bstride;
+  float* F = Fall + mi * d * d;
+  const bool diag = I == J;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int wi = wid / WGN, wj = wid % WGN;
+  const bool active = !(diag && (wj + 1) * WN <= wi * WM);
+  const int64_t cI = off + (int64_t)I * BM, cJ = off + (int64_t)J * BM;
+  const int spp = (int)(kw / kBK);  // stages per plane pair
+  const int nk = 6 * spp;
+
+  int lrow[NQ], lcol[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int slot = (NQ * wid + q) * 64 + lane;
+    lrow[q] = slot >> 5;
+    lcol[q] = 8 * ((slot & 31) ^ dl_swz(slot >> 5));
+  }
+  i32x4_t rs = buffer_rsrc(Pl, (uint32_t)(3 * kPlaneRows * d * 2));
+#pragma unroll
+  for (int u = 0; u < 4; ++u) rs[u] = __builtin_amdgcn_readfirstlane(rs[u]);  // wave-uniform: scalar registers
+  // Copy j of stage kt: panel j / NQ, chunk j % NQ; stages past the last read zeros.
+  auto issue = [&](uint16_t* buf, int kt, int j) {
+    const int pnl = j / NQ, q = j % NQ;
+    const int g = kt / spp;
+    const int64_t row = (int64_t)(kt - g * spp) * kBK + lrow[q];
+    const int64_t col = (pnl == 0 ? cI : cJ) + lcol[q];
+    const int plane = (int)(((pnl == 0 ? kPA : kPB) >> (2 * (g < 6 ? g : 0))) & 3u);
+    const bool ok = g < 6 && col < d;
+    const uint32_t off_b = ok ? (uint32_t)(2 * (((int64_t)plane * kPlaneRows + row) * d + col)) : kBufOutside;
+    const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (NQ * wid + q) * 1024;
+    lds_dma16_buf(off_b, rs, __builtin_amdgcn_readfirstlane(dst));
+  };
+
+  f32x16_t acc[NBM][NBN];
+#pragma unroll
+  for (int a = 0; a < NBM; ++a)
+#pragma unroll
+    for (int b = 0; b < NBN; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN];
+  auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
+#pragma unroll
+    for (int b = 0; b < NBN; ++b) fb[b] = frag32_tr_swz(buf + TILE_ELEMS, wj * WN + 32 * b, ks, lane);
+#pragma unroll
+    for (int a = 0; a < NBM; ++a) fa[a] = frag32_tr_swz(buf, wi * WM + 32 * a, ks, lane);
+  };
+  auto mma_row = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN], int a) {
+#pragma unroll
+    for (int b = 0; b < NBN; ++b) acc[a][b] = mfma32(fa[a], fb[b], acc[a][b]);
+  };
+  auto step = [&](uint16_t* cur, uint16_t* nxt, uint16_t* fill, int kt) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(NCP));  // stage kt + 1 landed (this thread's copies)
+    barrier_nofence();                           // ... everyone's; slot `fill` no longer read
+#pragma unroll
+    for (int sl = 0; sl < NSLOT; ++sl) {
+      if ((sl * NCP) % NSLOT == 0) {
+        __builtin_amdgcn_sched_barrier(0);
+        issue(fill, kt + kStages - 1, sl * NCP / NSLOT);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (sl == 0) load_frags(cur, 16, fa1, fb1);
+      if (sl == NBM) load_frags(nxt, 0, fa0, fb0);
+      if (sl < NBM) mma_row(fa0, fb0, sl);
+      else mma_row(fa1, fb1, sl - NBM);
+    }
+  };
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) issue(sb0, 0, j);
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) issue(sb1, 1, j);
+#pragma unroll
+  for (int j = 0; j < NCP; ++j) issue(sb2, 2, j);
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NCP));  // stage 0 landed
+  barrier_nofence();
+  load_frags(sb0, 0, fa0, fb0);
+  for (int kt = 0; kt < nk; kt += 4) {
+    step(sb0, sb1, sb3, kt);
+    if (kt + 1 < nk) step(sb1, sb2, sb0, kt + 1);
+    if (kt + 2 < nk) step(sb2, sb3, sb1, kt + 2);
+    if (kt + 3 < nk) step(sb3, sb0, sb2, kt + 3);
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // drain the look-ahead copies before the workgroup ends
+  if (!active) return;
+#pragma unroll
+  for (int a = 0; a < NBM; ++a)
+#pragma unroll
+    for (int b = 0; b < NBN; ++b) {
+      const int64_t col = cJ + wj * WN + 32 * b + mfma32_col(lane);
+      const int64_t rb = cI + wi * WM + 32 * a;
+      float old[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = rb + mfma32_row(lane, r);
+        old[r] = ld_or_zero(F, row * d + col, row < d && col < d && col >= row);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int64_t row = rb + mfma32_row(lane, r);
+        if (row < d && col < d && col >= row) F[row * d + col] = old[r] - acc[a][b][r];
       }
     }
 }
@@ -949,38 +1235,54 @@ __global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p
       for (int r = 0; r < 16; ++r) acc[q][r] = 0.f;
     const bool rok = 32 * wid + li < rows_ok;
     const float* arow = A + (int64_t)(rok ? 32 * wid + li : 0) * d;
-    for (int kk0 = 0; kk0 < kmax; kk0 += 32) {
-      const int kb = kk0 + 16 * h;
-      float a[16];
+    // the lane's whole row slice (kmax <= P) is loaded before the first product
+    float a[P / 2];
+#pragma unroll
+    for (int kc = 0; kc < P / 32; ++kc) {
+      const int kb = 32 * kc + 16 * h;
       if (V4) {
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const float4 t = ld4_or_zero_ro(arow, kb + 4 * v, rok && kb + 4 * v < kmax);
-          a[4 * v] = t.x; a[4 * v + 1] = t.y; a[4 * v + 2] = t.z; a[4 * v + 3] = t.w;
+          a[16 * kc + 4 * v] = t.x; a[16 * kc + 4 * v + 1] = t.y; a[16 * kc + 4 * v + 2] = t.z;
+          a[16 * kc + 4 * v + 3] = t.w;
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) a[j] = ld_or_zero(arow, kb + j, rok && kb + j < kmax);
+        for (int j = 0; j < 16; ++j) a[16 * kc + j] = ld_or_zero(arow, kb + j, rok && kb + j < kmax);
       }
+    }
+#pragma unroll
+    for (int kc = 0; kc < P / 32; ++kc) {
+      if (32 * kc >= kmax) break;
+      const int kb = 32 * kc + 16 * h;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
         const float* tb = sT + (32 * q + li) * LDT + kb;
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
           const float4 t = *(const float4*)(tb + 4 * v);
-          acc[q] = mfma_f32x2(a[4 * v], t.x, acc[q]);
-          acc[q] = mfma_f32x2(a[4 * v + 1], t.y, acc[q]);
-          acc[q] = mfma_f32x2(a[4 * v + 2], t.z, acc[q]);
-          acc[q] = mfma_f32x2(a[4 * v + 3], t.w, acc[q]);
+          acc[q] = mfma_f32x2(a[16 * kc + 4 * v], t.x, acc[q]);
+          acc[q] = mfma_f32x2(a[16 * kc + 4 * v + 1], t.y, acc[q]);
+          acc[q] = mfma_f32x2(a[16 * kc + 4 * v + 2], t.z, acc[q]);
+          acc[q] = mfma_f32x2(a[16 * kc + 4 * v + 3], t.w, acc[q]);
         }
       }
     }
   };
-  // sT[c][k] = src[k][c] for k < rows, c < m (zero elsewhere)
+  // sT[c][k] = src[k][c] for k < rows, c < m (zero elsewhere); all loads issued first
   auto load_t = [&](const float* src, int rows) {
-    for (int e = tid; e < NQ * 32 * P; e += kT) {
-      const int k = e / (NQ * 32), c = e % (NQ * 32);
-      sT[c * LDT + k] = ld_or_zero(src, (int64_t)k * m + c, k < rows && c < m);
+    constexpr int PER = NQ * 32 * P / kT;
+    float v[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + kT * u, k = e / (NQ * 32), c = e % (NQ * 32);
+      v[u] = ld_or_zero(src, (int64_t)k * m + c, k < rows && c < m);
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + kT * u, k = e / (NQ * 32), c = e % (NQ * 32);
+      sT[c * LDT + k] = v[u];
     }
   };
   auto store_mp = [&](int64_t r0, int rows, const f32x16_t (&acc)[NQ]) {
@@ -1006,6 +1308,14 @@ __global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p
   const int64_t nab = p / P;  // row blocks above p
   if (blockIdx.x == 0) {
     const int64_t r0 = p - P;
+    float rv[NQ][16];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * wid + mfma32_row(lane, r), col = 32 * q + li;
+        rv[q][r] = ld_or_zero(R, (r0 + row) * m + col, col < m);
+      }
     product(F + r0 * d + p, pw, P, acc);
     __syncthreads();  // done with M'_p in LDS
 #pragma unroll
@@ -1013,8 +1323,7 @@ __global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = 32 * wid + mfma32_row(lane, r), col = 32 * q + li;
-        const float v = col < m ? R[(r0 + row) * m + col] - acc[q][r] : 0.f;
-        sT[col * LDT + row] = v;
+        sT[col * LDT + row] = col < m ? rv[q][r] - acc[q][r] : 0.f;
       }
     __syncthreads();
     product(F + r0 * d + r0, P, P, acc);
@@ -1025,20 +1334,25 @@ __global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p
     const int64_t q0 = nab - 2 - 4 * ((int64_t)blockIdx.x - 1) - c;
     if (q0 < 0) break;
     const int64_t r0 = q0 * P;
-    product(F + r0 * d + p, pw, P, acc);
+    // the old values of the block's right-hand sides are loaded before the product
+    float old[NQ][16];
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
-      float old[16];
       const int col = 32 * q + li;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = 32 * wid + mfma32_row(lane, r);
-        old[r] = ld_or_zero(R, (r0 + row) * m + col, col < m);
+        old[q][r] = ld_or_zero(R, (r0 + row) * m + col, col < m);
       }
+    }
+    product(F + r0 * d + p, pw, P, acc);
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int col = 32 * q + li;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = 32 * wid + mfma32_row(lane, r);
-        if (col < m) R[(r0 + row) * m + col] = old[r] - acc[q][r];
+        if (col < m) R[(r0 + row) * m + col] = old[q][r] - acc[q][r];
       }
     }
   }
@@ -1064,6 +1378,7 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
   s += align256(sizeof(T) * nm * d * m);         // M' (back substitution output)
   s += align256(sizeof(double) * nb * d * (r_prev > 0 ? r_prev : 1));  // S Lp
   s += 256;                                                            // lambdas
+  if (sizeof(T) == 4) s += align256(sizeof(uint16_t) * nm * 3 * kPlaneRows * d);  // split planes
   return s;
 }
 
@@ -1072,12 +1387,17 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
 // first diagonal-block launch.
 template <typename T, typename ST>
 hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st, T* Fw, T* Rw, T* Dw, T* Mpw,
-                     double* SLpw, const double* dlam, hipEvent_t after_diag) {
+                     double* SLpw, const double* dlam, uint16_t* Plw, hipEvent_t after_diag) {
   const int64_t d = a.d, m = a.r_prev + a.k, nl = a.n_lambda, nm = nbg * nl, mi0 = b0 * nl;
   T* F = Fw + mi0 * d * d;
   T* R = Rw + mi0 * d * m;
   T* D = Dw + mi0 * d;
   T* Mp = Mpw + mi0 * d * m;
+  const int64_t pl_bstride = 3 * kPlaneRows * d;
+  // trailing updates from the split planes (direct-to-LDS) when the columns come in
+  // 16-byte chunks and a matrix's planes fit 31-bit byte offsets
+  const bool planes = sizeof(T) == 4 && d % 8 == 0 && d % 4 == 0 && 2 * pl_bstride < ((int64_t)1 << 31);
+  uint16_t* Pl = planes ? Plw + mi0 * pl_bstride : nullptr;
   double* SLp = SLpw + b0 * d * (a.r_prev > 0 ? a.r_prev : 1);
   int32_t* info = a.dev_info + mi0;
   const ST* S = (const ST*)a.S + b0 * a.s_bstride;
@@ -1096,8 +1416,18 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
     dim3 g((unsigned)((d + 255) / 256), (unsigned)nm);
     k_equil_diag<T, ST><<<g, 256, 0, st>>>(d, S, a.s_bstride, dlam, (int)nl, D);
     dim3 g2((unsigned)((d + kEqRows - 1) / kEqRows), (unsigned)nbg);
-    k_equil_setup<T, ST><<<g2, 256, 0, st>>>(d, m, a.r_prev, S, a.s_bstride, K, a.k_bstride, SLp, dlam, (int)nl, D,
-                                              F, R);
+    bool v4 = false;
+    if constexpr (sizeof(T) == 4 && sizeof(ST) == 4)
+      v4 = d % 4 == 0 && a.s_bstride % 4 == 0 && ((uintptr_t)S & 15) == 0;
+    if (v4) {
+      const dim3 g4((unsigned)((d + kEqRows - 1) / kEqRows), (unsigned)((d + kEqCols - 1) / kEqCols), (unsigned)nbg);
+      k_equil_setup_v4<<<g4, kEqCols / 4, 0, st>>>(d, m, a.r_prev, (const float*)S, a.s_bstride, (const float*)K,
+                                                   a.k_bstride, SLp, dlam, (int)nl, (const float*)D, (float*)F,
+                                                   (float*)R);
+    }
+    else
+      k_equil_setup<T, ST><<<g2, 256, 0, st>>>(d, m, a.r_prev, S, a.s_bstride, K, a.k_bstride, SLp, dlam, (int)nl, D,
+                                                F, R);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1121,7 +1451,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
         if (x6) {
           const int nF = (int)((d - pp + 255) / 256);
           k_panel_x6<kX6Strip><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
-              d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF);
+              d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF, nullptr, 0, 0);
           if (!x6r)
             k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
                 d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
@@ -1139,7 +1469,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       if (x6 && nrem > 0) {
         const int nF = (int)((nrem + 255) / 256);
         k_panel_x6<kX6Row><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
-            d, pp, pw, 0, (float*)F, (float*)R, m, nF);
+            d, pp, pw, 0, (float*)F, (float*)R, m, nF, P1 < d ? Pl : nullptr, pl_bstride, P0);
         if (!x6r)
           k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
                                                                                                (int)nchF, F, R);
@@ -1153,8 +1483,15 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       if (x6) {
         const int64_t T6 = (d - P1 + 255) / 256;
         const int nF = (int)(T6 * (T6 + 1) / 2);
-        k_panel_x6<kX6Trail><<<dim3((unsigned)(nF + (x6r ? T6 : 0)), (unsigned)nm), 512, 0, st>>>(
-            d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF);
+        if (Pl) {
+          k_syrk_x6_dl<<<dim3((unsigned)(nF * nm)), 512, 0, st>>>(d, P1 - P0, P1, Pl, pl_bstride, (float*)F, nF);
+          if (x6r)
+            k_panel_x6<kX6TrailRhs><<<dim3((unsigned)T6, (unsigned)nm, (unsigned)((m + 31) / 32)), 512, 0, st>>>(
+                d, P0, P1 - P0, P1, (float*)F, (float*)R, m, 0, nullptr, 0, 0);
+        } else {
+          k_panel_x6<kX6Trail><<<dim3((unsigned)(nF + (x6r ? T6 : 0)), (unsigned)nm), 512, 0, st>>>(
+              d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF, nullptr, 0, 0);
+        }
         if (!x6r)
           k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
               d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
@@ -1259,13 +1596,14 @@ hipError_t run_solve(const SolveArgs& a) {
   Lams lams;
   for (int i = 0; i < 8; ++i) lams.v[i] = (i < nl) ? a.lambdas[i] : 0.0;
   double* dlam = (double*)(p + align256(sizeof(double) * a.nb * d * (a.r_prev > 0 ? a.r_prev : 1)));
+  uint16_t* Pl = (uint16_t*)((char*)dlam + 256);
   // the host lambdas travel by value into a one-wave kernel (no copy from pageable memory)
   k_set_lambdas<<<1, 64, 0, a.stream>>>(lams, dlam, (int)nl);
   k_fill_zero_i32<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int G = (int)(a.nb < kGroups ? a.nb : kGroups);
-  if (G < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr);
+  if (G < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, Pl, nullptr);
   Aux* x = nullptr;
   if ((e = get_aux(&x)) != hipSuccess) return e;
   if ((e = hipEventRecord(x->fork, a.stream)) != hipSuccess) return e;
@@ -1277,7 +1615,7 @@ hipError_t run_solve(const SolveArgs& a) {
       if ((e = hipStreamWaitEvent(st, x->stagger[g], 0)) != hipSuccess) return e;
     }
     hipEvent_t after = g + 1 < G ? x->stagger[g + 1] : nullptr;
-    if ((e = run_group<T, ST>(a, b0, b1 - b0, st, F, R, D, Mp, SLp, dlam, after)) != hipSuccess) return e;
+    if ((e = run_group<T, ST>(a, b0, b1 - b0, st, F, R, D, Mp, SLp, dlam, Pl, after)) != hipSuccess) return e;
   }
   for (int g = 1; g < G; ++g) {
     if ((e = hipEventRecord(x->join[g], x->s[g])) != hipSuccess) return e;

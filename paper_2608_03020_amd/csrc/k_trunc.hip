@@ -9,10 +9,10 @@
 //   U = M Vb H Vp diag(1/s),   V = R^T Vb H^{-1} Vp,
 //   a_out = U_r^T = Ca M^T,    b_out = V_r diag(s_r) = R^T Cb
 // with small Ca (r x kp) and Cb (kp x r).  Both eigendecompositions are
-// cyclic Jacobi in fp64 inside one workgroup: for kp <= 64 with both matrices in
-// LDS; for 64 < kp <= 128 with the symmetric matrix packed in LDS (fp64), the
-// eigenvectors in LDS as floats (rotations computed in fp64), and the kp x kp
-// intermediates in the workspace.
+// cyclic Jacobi in fp64 inside one workgroup, the symmetric matrix packed in LDS:
+// for kp <= 64 with the eigenvectors and the kp x kp intermediates in LDS (fp64);
+// for 64 < kp <= 128 with the eigenvectors in LDS as floats (rotations computed in
+// fp64) and the kp x kp intermediates in the workspace.
 #include "loca_common.h"
 
 namespace loca {
@@ -75,78 +75,9 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
   }
 }
 
-// Cyclic Jacobi eigendecomposition of the symmetric n x n matrix A (LDS, row stride ld),
-// eigenvectors accumulated into V (columns).  Round-robin pair ordering: each round
-// rotates n/2 disjoint pairs.  n must be even (callers pad with a zero row/column).
-// Run by the kTC threads of one workgroup.
-constexpr int kTC = kT;
-LOCA_DEV void jacobi_eig(double* A, double* V, int n, int ld, double* cs, int* pairs, double* red) {
-  const int tid = threadIdx.x;
-  for (int e = tid; e < n * ld; e += kTC) V[e] = ((e / ld) == (e % ld)) ? 1.0 : 0.0;
-  __syncthreads();
-  for (int sweep = 0; sweep < 40; ++sweep) {
-    // convergence test: off-diagonal mass vs total
-    double off = 0.0, tot = 0.0;
-    for (int e = tid; e < n * n; e += kTC) {
-      const int i = e / n, j = e % n;
-      const double v = A[i * ld + j];
-      tot += v * v;
-      if (i != j) off += v * v;
-    }
-    const double offs = block_sum(off, red);
-    __syncthreads();
-    const double tots = block_sum(tot, red + 4);
-    if (tid == 0) red[8] = (offs <= 1e-30 * tots || tots == 0.0) ? 1.0 : 0.0;
-    __syncthreads();
-    if (red[8] != 0.0) break;
-    for (int round = 0; round < n - 1; ++round) {
-      // tournament pairing: positions 0..n-1, position 0 fixed, others rotate
-      if (tid < n / 2) {
-        auto pos = [&](int x) { return x == 0 ? 0 : 1 + ((x - 1 + round) % (n - 1)); };
-        int p = pos(tid), q = pos(n - 1 - tid);
-        if (p > q) { int t = p; p = q; q = t; }
-        pairs[2 * tid] = p;
-        pairs[2 * tid + 1] = q;
-        const double apq = A[p * ld + q], app = A[p * ld + p], aqq = A[q * ld + q];
-        double c = 1.0, s = 0.0;
-        if (fabs(apq) > 1e-300 && fabs(apq) > 1e-18 * sqrt(fabs(app * aqq))) {
-          const double tau = (aqq - app) / (2.0 * apq);
-          const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-          c = 1.0 / sqrt(1.0 + t * t);
-          s = t * c;
-        }
-        cs[2 * tid] = c;
-        cs[2 * tid + 1] = s;
-      }
-      __syncthreads();
-      // A <- A J (columns), V <- V J
-      for (int e = tid; e < (n / 2) * n; e += kTC) {
-        const int pr = e / n, i = e % n;
-        const int p = pairs[2 * pr], q = pairs[2 * pr + 1];
-        const double c = cs[2 * pr], s = cs[2 * pr + 1];
-        const double aip = A[i * ld + p], aiq = A[i * ld + q];
-        A[i * ld + p] = c * aip - s * aiq;
-        A[i * ld + q] = s * aip + c * aiq;
-        const double vip = V[i * ld + p], viq = V[i * ld + q];
-        V[i * ld + p] = c * vip - s * viq;
-        V[i * ld + q] = s * vip + c * viq;
-      }
-      __syncthreads();
-      // A <- J^T A (rows)
-      for (int e = tid; e < (n / 2) * n; e += kTC) {
-        const int pr = e / n, j = e % n;
-        const int p = pairs[2 * pr], q = pairs[2 * pr + 1];
-        const double c = cs[2 * pr], s = cs[2 * pr + 1];
-        const double apj = A[p * ld + j], aqj = A[q * ld + j];
-        A[p * ld + j] = c * apj - s * aqj;
-        A[q * ld + j] = s * apj + c * aqj;
-      }
-      __syncthreads();
-    }
-  }
-}
+constexpr int kTC = kT;  // threads of the eigensolver workgroups
 
-// ------------------------------------------------------------------ 64 < kp <= 128
+// ------------------------------------------------------------------ symmetric eigensolver
 
 // Upper-triangle packed index of (i, j) in either order, n x n.
 LOCA_DEV int pk(int i, int j, int n) {
@@ -155,13 +86,15 @@ LOCA_DEV int pk(int i, int j, int n) {
 }
 
 // Cyclic Jacobi on the packed symmetric n x n matrix A (n even), eigenvectors into the
-// float n x n V (row-major, columns are the vectors; rotations computed in fp64).  Each
-// round rotates the n/2 disjoint pairs of the same round-robin order as jacobi_eig, as
+// n x n V of type VT (row-major, columns are the vectors; rotations computed in fp64).  Each
+// round rotates n/2 disjoint pairs (round-robin tournament order: position 0 fixed, the
+// others rotating, so that a sweep of n - 1 rounds meets every pair once) as
 // one two-sided update: every 2 x 2 block of rows {p_k, q_k} and columns {p_l, q_l} is
 // owned by one thread and becomes J_k^T B J_l.  Run by the kTC threads of one workgroup.
-LOCA_DEV void jacobi_packed(double* A, float* V, int n, double* cs, int* pairs, double* red) {
+template <typename VT>
+LOCA_DEV void jacobi_packed(double* A, VT* V, int n, double* cs, int* pairs, double* red) {
   const int tid = threadIdx.x, m = n / 2;
-  for (int e = tid; e < n * n; e += kTC) V[e] = ((e / n) == (e % n)) ? 1.f : 0.f;
+  for (int e = tid; e < n * n; e += kTC) V[e] = ((e / n) == (e % n)) ? (VT)1 : (VT)0;
   __syncthreads();
   for (int sweep = 0; sweep < 40; ++sweep) {
     double off = 0.0, tot = 0.0;
@@ -223,8 +156,8 @@ LOCA_DEV void jacobi_packed(double* A, float* V, int n, double* cs, int* pairs, 
         const int p = pairs[2 * k], q = pairs[2 * k + 1];
         const double c = cs[2 * k], s = cs[2 * k + 1];
         const double vip = V[i * n + p], viq = V[i * n + q];
-        V[i * n + p] = (float)(c * vip - s * viq);
-        V[i * n + q] = (float)(s * vip + c * viq);
+        V[i * n + p] = (VT)(c * vip - s * viq);
+        V[i * n + q] = (VT)(s * vip + c * viq);
       }
       __syncthreads();
     }
@@ -392,16 +325,18 @@ __global__ __launch_bounds__(kT) void k_trunc_apply_tiled(int64_t d, int64_t kp,
     }
 }
 
-// One workgroup per matrix: eigendecompositions and the small factors Ca, Cb.
+// One workgroup per matrix: eigendecompositions and the small factors Ca, Cb (kp <= 64).
+// Both symmetric matrices are packed in LDS and diagonalised by jacobi_packed (one
+// two-sided update per round); Gm, Vb and the eigenvectors (fp64) stay in LDS.
 __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, const double* __restrict__ Gpart,
                                                     int nsplit, double* __restrict__ Ca_all,
                                                     double* __restrict__ Cb_all, float* __restrict__ sigma_out,
                                                     int64_t sigma_bstride) {
-  constexpr int LD = kMaxKp + 1;
-  __shared__ double sA[kMaxKp * LD];
-  __shared__ double sV[kMaxKp * LD];
-  __shared__ double sT[kMaxKp * LD];
-  __shared__ double sG[kMaxKp * LD];  // Gm
+  constexpr int KB2 = kMaxKp * kMaxKp;
+  __shared__ double sA[kMaxKp * (kMaxKp + 1) / 2];
+  __shared__ double sV[KB2];   // eigenvectors of the current eigensolve; T = Gm Vb in between
+  __shared__ double sVb[KB2];  // Vb
+  __shared__ double sG[KB2];   // Gm
   __shared__ double sH[kMaxKp], sHi[kMaxKp], sEig[kMaxKp];
   __shared__ int sOrd[kMaxKp];
   __shared__ double cs[kMaxKp];
@@ -409,73 +344,61 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   __shared__ double red[16];
   const int64_t mi = blockIdx.x;
   const int tid = threadIdx.x;
-  const int n = (int)kp + ((int)kp & 1);  // even size for the tournament ordering
+  const int K = (int)kp;
+  const int n = K + (K & 1);  // even size for the tournament ordering
   const double* GmP = Gpart + (mi * 2) * nsplit * kp * kp;
   const double* GbP = Gpart + (mi * 2 + 1) * nsplit * kp * kp;
-  // 1. Gb = Vb diag(lb) Vb^T; Gm (summed over the row ranges, in order) waits in sT
-  for (int e = tid; e < n * LD; e += kTC) {
-    const int i = e / LD, j = e % LD;
+  // 1. Gb = Vb diag(lb) Vb^T; Gm (each summed over the row ranges, in order) into sG
+  for (int e = tid; e < n * n; e += kTC) {
+    const int i = e / n, j = e % n;
     double gb = 0.0, gm = 0.0;
-    if (i < kp && j < kp)
+    if (i < K && j < K)
       for (int z = 0; z < nsplit; ++z) {
         gb += GbP[z * kp * kp + i * kp + j];
         gm += GmP[z * kp * kp + i * kp + j];
       }
-    sA[e] = gb;
     sG[e] = gm;
+    if (i <= j) sA[pk(i, j, n)] = gb;
   }
   __syncthreads();
-  jacobi_eig(sA, sV, n, LD, cs, pairs, red);
+  jacobi_packed<double>(sA, sV, n, cs, pairs, red);
   __syncthreads();
   if (tid == 0) {
     double lmax = 0.0;
-    for (int j = 0; j < kp; ++j) lmax = fmax(lmax, sA[j * LD + j]);
+    for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
     red[12] = lmax;
   }
   __syncthreads();
-  for (int j = tid; j < kp; j += kTC) {
-    const double lb = sA[j * LD + j];
+  for (int j = tid; j < n; j += kTC) {
+    const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
     const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
     sH[j] = keep ? sqrt(lb) : 0.0;
     sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
   }
-  // keep Vb in sT
-  for (int e = tid; e < n * LD; e += kTC) sT[e] = sV[e];
+  for (int e = tid; e < n * n; e += kTC) sVb[e] = sV[e];
   __syncthreads();
-  // 2. P^T P = H Vb^T Gm Vb H: first sA = Gm Vb
-  for (int e = tid; e < (int)(kp * kp); e += kTC) {
-    const int i = e / (int)kp, j = e % (int)kp;
+  // 2. T = Gm Vb (into sV), then P^T P = H Vb^T T H (upper triangle, packed)
+  for (int e = tid; e < n * n; e += kTC) {
+    const int i = e / n, j = e % n;
     double s = 0.0;
-    for (int c = 0; c < kp; ++c) s += sG[i * LD + c] * sT[c * LD + j];
-    sV[i * LD + j] = s;
+    for (int c = 0; c < n; ++c) s += sG[i * n + c] * sVb[c * n + j];
+    sV[e] = s;
   }
   __syncthreads();
   for (int e = tid; e < n * n; e += kTC) {
     const int i = e / n, j = e % n;
+    if (i > j) continue;
     double s = 0.0;
-    if (i < kp && j < kp) {
-      for (int c = 0; c < kp; ++c) s += sT[c * LD + i] * sV[c * LD + j];
-      s *= sH[i] * sH[j];
-    }
-    sA[i * LD + j] = s;
+    for (int c = 0; c < n; ++c) s += sVb[c * n + i] * sV[c * n + j];
+    sA[pk(i, j, n)] = s * sH[i] * sH[j];
   }
   __syncthreads();
-  // symmetrise against rounding
-  for (int e = tid; e < n * n; e += kTC) {
-    const int i = e / n, j = e % n;
-    if (i < j) {
-      const double v = 0.5 * (sA[i * LD + j] + sA[j * LD + i]);
-      sA[i * LD + j] = v;
-      sA[j * LD + i] = v;
-    }
-  }
-  __syncthreads();
-  jacobi_eig(sA, sV, n, LD, cs, pairs, red);  // sV = Vp
+  jacobi_packed<double>(sA, sV, n, cs, pairs, red);  // sV = Vp
   __syncthreads();
   if (tid == 0) {
     // order by decreasing eigenvalue (insertion sort on indices)
-    for (int j = 0; j < kp; ++j) { sEig[j] = sA[j * LD + j]; sOrd[j] = j; }
-    for (int i = 1; i < kp; ++i) {
+    for (int j = 0; j < K; ++j) { sEig[j] = sA[pk(j, j, n)]; sOrd[j] = j; }
+    for (int i = 1; i < K; ++i) {
       const int key = sOrd[i];
       int j = i - 1;
       while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
@@ -484,18 +407,19 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   }
   __syncthreads();
   const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
-  for (int j = tid; j < kp; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
+  for (int j = tid; j < K; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
   // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
   for (int e = tid; e < (int)(r_a * kp); e += kTC) {
-    const int a = e / (int)kp, c = e % (int)kp;
+    const int a = e / K, c = e % K;
     const int col = sOrd[a];
     const double sa = sqrt(fmax(sEig[col], 0.0));
     double u = 0.0, v = 0.0;
-    for (int x = 0; x < kp; ++x) {
-      u += sT[c * LD + x] * sH[x] * sV[x * LD + col];
-      v += sT[c * LD + x] * sHi[x] * sV[x * LD + col];
+    for (int x = 0; x < n; ++x) {
+      const double vb = sVb[c * n + x], vp = sV[x * n + col];
+      u += vb * sH[x] * vp;
+      v += vb * sHi[x] * vp;
     }
     const bool live = sa > 1e-30 * s1 && sa > 0.0;
     Ca[a * kp + c] = live ? u / sa : 0.0;

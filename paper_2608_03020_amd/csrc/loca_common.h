@@ -140,6 +140,71 @@ LOCA_DEV f32x16_t mfma_f32x2(float a, float b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }
 
+// ------------------------------------------------------------------ direct-to-LDS staging (gfx950)
+// Building blocks of the pipelined kernels that copy 32-row x 256-column bf16 stages
+// straight from global memory into LDS (global_load_lds_dwordx4 / buffer_load ... lds).
+// A stage is stored with rows of 512 bytes whose 16-byte chunks are XOR-swizzled,
+// chunk c of row r at c ^ 4(r & 3), so that the transpose reads of a half wave are
+// conflict-free.
+
+LOCA_DEV int dl_swz(int row) { return 4 * (row & 3); }
+
+// operand of v_mfma_f32_32x32x16_bf16 from a swizzled 32 x 256 stage (see frag32_tr)
+LOCA_DEV bf16x8_t frag32_tr_swz(const uint16_t* tile, int c0, int ks, int lane) {
+  const int g = lane >> 4, w = lane & 15;
+  const int col = c0 + 16 * (g & 1) + 4 * (w & 3);
+  const int row = ks + 8 * (g >> 1) + (w >> 2);
+  const int lc = col >> 3, within = col & 7;
+  const uint16_t* p0 = tile + row * 256 + 8 * (lc ^ dl_swz(row)) + within;
+  const uint16_t* p1 = tile + (row + 4) * 256 + 8 * (lc ^ dl_swz(row + 4)) + within;
+  s16x4_t lo = lds_read_tr16(p0);
+  s16x4_t hi = lds_read_tr16(p1);
+  typedef short s16x8_t __attribute__((ext_vector_type(8)));
+  s16x8_t v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+// s_waitcnt immediate that waits until at most n vector-memory operations are outstanding
+constexpr int vmcnt_imm(int n) { return (n & 15) | (((n >> 4) & 3) << 14) | (7 << 4) | (15 << 8); }
+
+// 16-byte global -> LDS copy for every lane: lane l's chunk lands at lds_base + 16 l.
+// Issued as inline assembly so that the compiler does not treat it as a store to the
+// ring slot being read and drain it before every LDS read; completion is tracked by
+// the explicit vmcnt waits of the pipeline.
+LOCA_DEV void lds_dma16(const void* gptr, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(gptr), "s"(lds_base) : "m0", "memory");
+}
+// The same copy through the buffer path: `voff` is a byte offset into the buffer of the
+// resource `rsrc` (base, byte range, raw format); offsets at or past the range return zeros.
+typedef int32_t i32x4_t __attribute__((ext_vector_type(4)));
+LOCA_DEV void lds_dma16_buf(uint32_t voff, i32x4_t rsrc, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %2, 0 offen lds" ::"v"(voff), "s"(lds_base),
+               "s"(rsrc) : "m0", "memory");
+}
+LOCA_DEV i32x4_t buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  i32x4_t r;
+  r[0] = (int32_t)(uint32_t)(a & 0xffffffffu);
+  r[1] = (int32_t)(uint32_t)((a >> 32) & 0xffffu);  // stride 0
+  r[2] = (int32_t)bytes;
+  r[3] = 0x00020000;  // raw 32-bit data format
+  return r;
+}
+constexpr uint32_t kBufOutside = 0x80000000u;  // past every range used here (< 2^31 bytes)
+
+// Workgroup barrier without a memory fence (the pipeline waits for its own loads explicitly).
+LOCA_DEV void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
+
+// The hardware hands consecutive workgroups to the eight XCDs in turn, and each XCD
+// has its own L2.  Workgroup L is therefore given logical tile x * per + idx, with
+// x = L % 8 and idx = L / 8, so that the tiles one XCD runs at the same time are
+// neighbours in the upper triangle of one block and share their column panels in L2.
+LOCA_DEV int xcd_logical(int L, int total) {
+  const int per = total / 8, rem = total % 8;
+  const int x = L % 8, idx = L / 8;
+  return x * per + (x < rem ? x : rem) + idx;
+}
+
 }  // namespace loca
 
 // Internal launchers (defined in the kernel files, called by loca_api.hip).
