@@ -1014,9 +1014,7 @@ __global__ __launch_bounds__(512) void k_syrk_x6_dl(int64_t d, int64_t kw, int64
     lrow[q] = slot >> 5;
     lcol[q] = 8 * ((slot & 31) ^ dl_swz(slot >> 5));
   }
-  i32x4_t rs = buffer_rsrc(Pl, (uint32_t)(3 * kPlaneRows * d * 2));
-#pragma unroll
-  for (int u = 0; u < 4; ++u) rs[u] = __builtin_amdgcn_readfirstlane(rs[u]);  // wave-uniform: scalar registers
+  const i32x4_t rs = buffer_rsrc(Pl, (uint32_t)(3 * kPlaneRows * d * 2));
   // Copy j of stage kt: panel j / NQ, chunk j % NQ; stages past the last read zeros.
   auto issue = [&](uint16_t* buf, int kt, int j) {
     const int pnl = j / NQ, q = j % NQ;

@@ -188,6 +188,8 @@ LOCA_DEV i32x4_t buffer_rsrc(const void* base, uint32_t bytes) {
   r[1] = (int32_t)(uint32_t)((a >> 32) & 0xffffu);  // stride 0
   r[2] = (int32_t)bytes;
   r[3] = 0x00020000;  // raw 32-bit data format
+#pragma unroll
+  for (int u = 0; u < 4; ++u) r[u] = __builtin_amdgcn_readfirstlane(r[u]);  // wave-uniform: scalar registers
   return r;
 }
 constexpr uint32_t kBufOutside = 0x80000000u;  // past every range used here (< 2^31 bytes)
