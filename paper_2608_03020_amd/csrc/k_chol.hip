@@ -769,10 +769,11 @@ LOCA_DEV void split3(float a, uint16_t& h, uint16_t& m, uint16_t& l) {
 //             from off), the update of a panel by the earlier panels of its super-panel;
 //   kX6Row:   F[p + i][j] = sum_kk X[kk][i] F[p + kk][j] for the columns j >= p + 128 of
 //             the panel rows (128 x 256 tiles), X = U11^{-1} in the diagonal block.
-// A stage is 16 rows of K: each operand is loaded into registers one stage ahead, split,
-// and written to LDS as three bf16 planes [16][LD]; eight waves (2 x 4) read their MFMA
-// operands with transpose reads (LD = 288: the four rows a half-wave reads start 64 bytes
-// apart modulo 256, so the reads are conflict-free).  Requires d % 4 == 0.
+// A stage is 16 rows of K: each operand is loaded into registers several stages ahead (a
+// ring of D stages), split, and written to LDS as three bf16 planes [16][LD]; eight waves
+// (2 x 4) read their MFMA operands with transpose reads (LD = 288: the four rows a
+// half-wave reads start 64 bytes apart modulo 256, so the reads are conflict-free).
+// Requires d % 4 == 0.
 constexpr int kX6BK = 16, kX6LD = 288;
 enum X6Mode { kX6Trail = 0, kX6Strip = 1, kX6Row = 2, kX6TrailRhs = 3 };
 
@@ -788,16 +789,10 @@ LOCA_DEV float4 ld4_or_zero_ro(const float* __restrict__ base, int64_t idx, bool
 // kX6TrailRhs: only the right-hand-side jobs of kX6Trail, in a layout for their few
 // columns: a workgroup takes 256 rows x 32 columns (eight waves of 32 x 32; columns
 // 32 blockIdx.z ..), so it does an eighth of the matrix-core work of a 256 x 256 tile.
-//
-// kX6Row with Pl != nullptr also writes the three bf16 parts of every U12 entry it forms
-// into the super-panel planes Pl[t][i - p0][j] (t = h, m, l; kPlaneRows rows of d columns
-// per plane, pl_bstride elements per matrix), the operands of k_syrk_x6_dl.
-constexpr int kPlaneRows = 4 * 128;  // rows of a super-panel (kSuper panels of 128)
 template <int MODE>
 __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t kw, int64_t off,
                                                   float* __restrict__ Fall, float* __restrict__ Rall, int64_t m,
-                                                  int nF, uint16_t* __restrict__ Plall, int64_t pl_bstride,
-                                                  int64_t p0) {
+                                                  int nF) {
   constexpr bool RH = MODE == kX6TrailRhs;
   constexpr int BR = (MODE == kX6Trail || RH) ? 256 : 128;  // output rows per tile
   constexpr int BC = RH ? 32 : 256, WGN = RH ? 1 : 4, WGM = 8 / WGN;
@@ -848,17 +843,21 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
   const float* gQ = Out + k0 * ldq + ocol;
   const int64_t pend = MODE == kX6Row ? k0 + 128 : d;  // columns of Pn that exist: < pend
 
-  float4 rp[QP], rq[QQ];
-  auto load = [&](int kc0) {
+  // a ring of D stages of global loads in flight: the loads of stage kc + D are issued
+  // when stage kc is consumed, so D - 1 stages of matrix-core work cover their latency
+  constexpr int D = MODE == kX6Trail ? 2 : 4;
+  float4 rp[D][QP], rq[D][QQ];
+  auto load = [&](int slot, int kc0) {
 #pragma unroll
     for (int q = 0; q < QP; ++q) {
       const int c = tid + 512 * q, kk = c / (BR / 4), c4 = 4 * (c % (BR / 4));
-      rp[q] = ld4_or_zero(gP, (int64_t)(kc0 + kk) * d + c4, kc0 + kk < kw && pcol + c4 < pend);
+      rp[slot][q] = ld4_or_zero(gP, (int64_t)(kc0 + kk) * d + c4, kc0 + kk < kw && pcol + c4 < pend);
     }
 #pragma unroll
     for (int q = 0; q < QQ; ++q) {
       const int c = tid + 512 * q, kk = c / (BC / 4), c4 = 4 * (c % (BC / 4));
-      if (c < NQV) rq[q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * ldq + c4, kc0 + kk < kw && ocol + c4 < qend);
+      if (c < NQV)
+        rq[slot][q] = ld4_or_zero(gQ, (int64_t)(kc0 + kk) * ldq + c4, kc0 + kk < kw && ocol + c4 < qend);
     }
   };
   auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
@@ -872,16 +871,16 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
     *(uint2*)(base + PLANE + o) = make_uint2(m[0] | ((uint32_t)m[1] << 16), m[2] | ((uint32_t)m[3] << 16));
     *(uint2*)(base + 2 * PLANE + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, int slot) {
 #pragma unroll
     for (int q = 0; q < QP; ++q) {
       const int c = tid + 512 * q;
-      put(&sm[buf][0], c / (BR / 4), 4 * (c % (BR / 4)), rp[q]);
+      put(&sm[buf][0], c / (BR / 4), 4 * (c % (BR / 4)), rp[slot][q]);
     }
 #pragma unroll
     for (int q = 0; q < QQ; ++q) {
       const int c = tid + 512 * q;
-      if (c < NQV) put(&sm[buf][3 * PLANE], c / (BC / 4), 4 * (c % (BC / 4)), rq[q]);
+      if (c < NQV) put(&sm[buf][3 * PLANE], c / (BC / 4), 4 * (c % (BC / 4)), rq[slot][q]);
     }
   };
 
@@ -894,31 +893,39 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
   const int nk = (int)((kw + kX6BK - 1) / kX6BK);
-  load(0);
-  store(0);
+#pragma unroll
+  for (int u = 0; u < D; ++u)
+    if (u < nk) load(u, u * kX6BK);
+  store(0, 0);
   __syncthreads();
-  for (int kc = 0; kc < nk; ++kc) {
-    const int cur = kc & 1;
-    if (kc + 1 < nk) load((kc + 1) * kX6BK);
-    bf16x8_t fa[3][NBM], fb[3][NBN];
+  for (int kc0 = 0; kc0 < nk; kc0 += D) {
 #pragma unroll
-    for (int t = 0; t < 3; ++t) {
+    for (int u = 0; u < D; ++u) {  // stage kc = kc0 + u: in LDS buffer kc & 1; its register slot is u
+      const int kc = kc0 + u;
+      if (kc >= nk) break;
+      const int cur = kc & 1;
+      if (kc + D < nk) load(u, (kc + D) * kX6BK);
+      bf16x8_t fa[3][NBM], fb[3][NBN];
 #pragma unroll
-      for (int a = 0; a < NBM; ++a) fa[t][a] = frag32_tr(&sm[cur][t * PLANE], LD, wi * WM + 32 * a, 0, lane);
+      for (int t = 0; t < 3; ++t) {
 #pragma unroll
-      for (int b = 0; b < NBN; ++b) fb[t][b] = frag32_tr(&sm[cur][(3 + t) * PLANE], LD, wj * WN + 32 * b, 0, lane);
+        for (int a = 0; a < NBM; ++a) fa[t][a] = frag32_tr(&sm[cur][t * PLANE], LD, wi * WM + 32 * a, 0, lane);
+#pragma unroll
+        for (int b = 0; b < NBN; ++b)
+          fb[t][b] = frag32_tr(&sm[cur][(3 + t) * PLANE], LD, wj * WN + 32 * b, 0, lane);
+      }
+      // the six kept terms, smallest first; each term runs over all blocks, so the MFMAs
+      // into one accumulator are NBM * NBN instructions apart
+      constexpr int TA[6] = {2, 0, 1, 1, 0, 0}, TB[6] = {0, 2, 1, 0, 1, 0};
+#pragma unroll
+      for (int t = 0; t < 6; ++t)
+#pragma unroll
+        for (int a = 0; a < NBM; ++a)
+#pragma unroll
+          for (int b = 0; b < NBN; ++b) acc[a][b] = mfma32(fa[TA[t]][a], fb[TB[t]][b], acc[a][b]);
+      if (kc + 1 < nk) store(cur ^ 1, (u + 1) % D);
+      __syncthreads();
     }
-    // the six kept terms, smallest first; each term runs over all blocks, so the MFMAs
-    // into one accumulator are NBM * NBN instructions apart
-    constexpr int TA[6] = {2, 0, 1, 1, 0, 0}, TB[6] = {0, 2, 1, 0, 1, 0};
-#pragma unroll
-    for (int t = 0; t < 6; ++t)
-#pragma unroll
-      for (int a = 0; a < NBM; ++a)
-#pragma unroll
-        for (int b = 0; b < NBN; ++b) acc[a][b] = mfma32(fa[TA[t]][a], fb[TB[t]][b], acc[a][b]);
-    if (kc + 1 < nk) store(cur ^ 1);
-    __syncthreads();
   }
   if (!active) return;
   int64_t rend = MODE == kX6Row ? k0 + 128 : (MODE == kX6Strip ? off + 128 : d);
@@ -943,88 +950,89 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
         if (row < rend && col < qend && (rhs || col >= row))
           Out[row * ldq + col] = MODE == kX6Row ? acc[a][b][r] : old[r] - acc[a][b][r];
       }
-      if (MODE == kX6Row && !rhs && Plall != nullptr) {
-        uint16_t* Pl = Plall + mi * pl_bstride;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int64_t row = rb + mfma32_row(lane, r);
-          if (row < rend && col < qend) {
-            uint16_t h, mm, l;
-            split3(acc[a][b][r], h, mm, l);
-            const int64_t o = (row - p0) * d + col;
-            Pl[o] = h;
-            Pl[(int64_t)kPlaneRows * d + o] = mm;
-            Pl[(int64_t)2 * kPlaneRows * d + o] = l;
-          }
-        }
-      }
     }
 }
 
-// ------------------------------------------------------------------ trailing update from split planes
+// ------------------------------------------------------------------ trailing update, fp32 rows split in registers
 
-// The trailing update of a super-panel, F[i][j] -= sum_kk U[kk][i] U[kk][j] over its kw
-// rows kk, on the upper 256 x 256 tiles of the trailing region [off, d), with U given as
-// its three bf16 planes Pl[t][kk][j] (t = h, m, l, from the row-panel kernel).  The six
-// kept products of split3 are one product over a stacked K of 6 kw rows: the left operand
-// runs through the planes (l, h, m, m, h, h) and the right one through (h, l, m, h, m, h),
-// kw rows per plane pair (smallest terms first).  The operands are bf16 already, so they
-// stream into LDS by direct copies: tiles, waves, the four-slot ring of 32-row stages, the
-// swizzled layout, the fragment double-buffering and the spread of the copies between the
-// MFMA rows are those of the Gram kernel; diagonal tiles load both panels (the two
-// operands differ).  The workgroup order is XCD-aware over all matrices of the launch.
-// Requires d % 8 == 0, kw % 32 == 0, and a plane buffer of each matrix below 2^31 bytes.
-__global__ __launch_bounds__(512) void k_syrk_x6_dl(int64_t d, int64_t kw, int64_t off,
-                                                    const uint16_t* __restrict__ Plall, int64_t pl_bstride,
-                                                    float* __restrict__ Fall, int ntile) {
-  constexpr int kBK = 32, BM = 256, NT = 512, WGN = 4, WM = 128, WN = 64, NBM = WM / 32, NBN = WN / 32;
-  constexpr int TILE_ELEMS = kBK * BM;          // one panel stage (bf16 elements)
-  constexpr int NQ = TILE_ELEMS * 2 / 16 / NT;  // 16-byte copies per thread per panel
-  constexpr int NCP = 2 * NQ;                   // copies per thread per stage
-  constexpr int NSLOT = 2 * NBM;                // fragment rows of MFMAs per stage
-  constexpr int kStages = 4;
-  static_assert(NCP <= NSLOT, "at most one copy between two fragment rows");
-  // plane of each operand for the six plane pairs, two bits each (l = 2, h = 0, m = 1)
-  constexpr uint32_t kPA = 2u | (0u << 2) | (1u << 4) | (1u << 6) | (0u << 8) | (0u << 10);
-  constexpr uint32_t kPB = 0u | (2u << 2) | (1u << 4) | (0u << 6) | (1u << 8) | (0u << 10);
-  __shared__ __attribute__((aligned(1024))) uint16_t sb0[2 * TILE_ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sb1[2 * TILE_ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sb2[2 * TILE_ELEMS];
-  __shared__ __attribute__((aligned(1024))) uint16_t sb3[2 * TILE_ELEMS];
+// The trailing update of a super-panel, F[i][j] -= sum_kk U[kk][i] U[kk][j] over its kw rows
+// kk in [k0, k0 + kw), on the upper 256 x 256 tiles of the trailing region [off, d), with
+// the fp32 rows of U read straight from F.  Stages of 16 rows x 256 columns (16 KB per
+// panel) stream into a four-slot LDS ring by direct copies, three stages ahead; the 16-byte
+// chunks of stage row r sit XOR-swizzled by 8 (r / 8), so that the two half-waves of an
+// operand read (rows r and r + 8) fall on different banks.  Every operand is split into
+// its three bf16 parts in registers (split3, hardware conversions) and feeds the six kept
+// products, smallest first.  A diagonal tile needs one panel (its second ring panel reads
+// nothing).  Tiles, waves and the XCD-aware workgroup order are those of the Gram kernel.
+// Requires d % 4 == 0, kw % 16 == 0 and 4 d^2 < 2^31 bytes per matrix.
+constexpr int kS32BK = 16;  // K rows per stage
+LOCA_DEV void split3_bf16(float a, __bf16& h, __bf16& m, __bf16& l) {
+  h = (__bf16)a;  // round to nearest even
+  const float r1 = a - (float)h;
+  m = (__bf16)r1;
+  l = (__bf16)(r1 - (float)m);
+}
+// the 8 fp32 operand values of lane `lane` (rows 8 (lane / 32) + e of the stage, column
+// c0 + lane % 32 of the panel) from a swizzled stage, split into three MFMA operands
+LOCA_DEV void frag_f32_split(const float* stage, int c0, int lane, bf16x8_t& fh, bf16x8_t& fm, bf16x8_t& fl) {
+  const int hw = lane >> 5, cc = c0 + (lane & 31);
+  const float* p = stage + 8 * hw * 256 + 4 * ((cc >> 2) ^ (8 * hw)) + (cc & 3);
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = p[e * 256];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    __bf16 h, m, l;
+    split3_bf16(v[e], h, m, l);
+    fh[e] = h;
+    fm[e] = m;
+    fl[e] = l;
+  }
+}
+__global__ __launch_bounds__(512) void k_syrk_f32_dl(int64_t d, int64_t k0, int64_t kw, int64_t off,
+                                                     float* __restrict__ Fall, int ntile) {
+  constexpr int BM = 256, NT = 512, WGN = 4, WM = 128, WN = 64, NBM = WM / 32, NBN = WN / 32;
+  constexpr int TILE_F = kS32BK * BM;            // floats of one panel stage
+  constexpr int NQ = TILE_F * 4 / 16 / NT;       // 16-byte copies per thread per panel
+  constexpr int NCP = 2 * NQ;                    // copies per thread per stage
+  static_assert(NCP == NBM, "one copy per fragment row of a stage");
+  __shared__ __attribute__((aligned(1024))) float sb0[2 * TILE_F];
+  __shared__ __attribute__((aligned(1024))) float sb1[2 * TILE_F];
+  __shared__ __attribute__((aligned(1024))) float sb2[2 * TILE_F];
+  __shared__ __attribute__((aligned(1024))) float sb3[2 * TILE_F];
 
   const int T = (int)((d - off + BM - 1) / BM);
   const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
   int I, J;
   upper_tile_c(logical % ntile, T, I, J);
   const int64_t mi = logical / ntile;
-  const uint16_t* Pl = Plall + mi * pl_bstride;
   float* F = Fall + mi * d * d;
   const bool diag = I == J;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int wi = wid / WGN, wj = wid % WGN;
   const bool active = !(diag && (wj + 1) * WN <= wi * WM);
   const int64_t cI = off + (int64_t)I * BM, cJ = off + (int64_t)J * BM;
-  const int spp = (int)(kw / kBK);  // stages per plane pair
-  const int nk = 6 * spp;
+  const int nk = (int)(kw / kS32BK);
 
+  // copy q of this thread fills LDS chunk position (NQ wid + q) * 64 + lane of a panel stage:
+  // stage row slot / 64, position slot % 64, holding global chunk position ^ 8 (row / 8)
   int lrow[NQ], lcol[NQ];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
     const int slot = (NQ * wid + q) * 64 + lane;
-    lrow[q] = slot >> 5;
-    lcol[q] = 8 * ((slot & 31) ^ dl_swz(slot >> 5));
+    lrow[q] = slot >> 6;
+    lcol[q] = 4 * ((slot & 63) ^ (8 * ((slot >> 9) & 1)));
   }
-  const i32x4_t rs = buffer_rsrc(Pl, (uint32_t)(3 * kPlaneRows * d * 2));
-  // Copy j of stage kt: panel j / NQ, chunk j % NQ; stages past the last read zeros.
-  auto issue = [&](uint16_t* buf, int kt, int j) {
+  const i32x4_t rs = buffer_rsrc(F, (uint32_t)(d * d * 4));
+  // Copy j of stage kt: panel j / NQ, chunk j % NQ; stages past the last, and the second
+  // panel of a diagonal tile, read nothing (out-of-range offsets return zeros).
+  auto issue = [&](float* buf, int kt, int j) {
     const int pnl = j / NQ, q = j % NQ;
-    const int g = kt / spp;
-    const int64_t row = (int64_t)(kt - g * spp) * kBK + lrow[q];
+    const int64_t row = k0 + (int64_t)kt * kS32BK + lrow[q];
     const int64_t col = (pnl == 0 ? cI : cJ) + lcol[q];
-    const int plane = (int)(((pnl == 0 ? kPA : kPB) >> (2 * (g < 6 ? g : 0))) & 3u);
-    const bool ok = g < 6 && col < d;
-    const uint32_t off_b = ok ? (uint32_t)(2 * (((int64_t)plane * kPlaneRows + row) * d + col)) : kBufOutside;
-    const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_ELEMS * 2 + (NQ * wid + q) * 1024;
+    const bool ok = kt < nk && col < d && !(diag && pnl == 1);
+    const uint32_t off_b = ok ? (uint32_t)(4 * (row * d + col)) : kBufOutside;
+    const uint32_t dst = (uint32_t)(uintptr_t)(LOCA_LDS void*)buf + pnl * TILE_F * 4 + (NQ * wid + q) * 1024;
     lds_dma16_buf(off_b, rs, __builtin_amdgcn_readfirstlane(dst));
   };
 
@@ -1036,31 +1044,29 @@ __global__ __launch_bounds__(512) void k_syrk_x6_dl(int64_t d, int64_t kw, int64
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN];
-  auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
+  const int bpanel = diag ? 0 : TILE_F;
+  auto step = [&](float* cur, float* fill, int kt) {
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NCP));  // stage kt landed (this thread's copies)
+    barrier_nofence();                               // ... everyone's; slot `fill` no longer read
+    bf16x8_t bh[NBN], bm[NBN], bl[NBN];
 #pragma unroll
-    for (int b = 0; b < NBN; ++b) fb[b] = frag32_tr_swz(buf + TILE_ELEMS, wj * WN + 32 * b, ks, lane);
+    for (int b = 0; b < NBN; ++b) frag_f32_split(cur + bpanel, wj * WN + 32 * b, lane, bh[b], bm[b], bl[b]);
 #pragma unroll
-    for (int a = 0; a < NBM; ++a) fa[a] = frag32_tr_swz(buf, wi * WM + 32 * a, ks, lane);
-  };
-  auto mma_row = [&](const bf16x8_t (&fa)[NBM], const bf16x8_t (&fb)[NBN], int a) {
+    for (int a = 0; a < NBM; ++a) {
+      __builtin_amdgcn_sched_barrier(0);
+      issue(fill, kt + 3, a);
+      __builtin_amdgcn_sched_barrier(0);
+      bf16x8_t ah, am, al;
+      frag_f32_split(cur, wi * WM + 32 * a, lane, ah, am, al);
 #pragma unroll
-    for (int b = 0; b < NBN; ++b) acc[a][b] = mfma32(fa[a], fb[b], acc[a][b]);
-  };
-  auto step = [&](uint16_t* cur, uint16_t* nxt, uint16_t* fill, int kt) {
-    __builtin_amdgcn_s_waitcnt(vmcnt_imm(NCP));  // stage kt + 1 landed (this thread's copies)
-    barrier_nofence();                           // ... everyone's; slot `fill` no longer read
-#pragma unroll
-    for (int sl = 0; sl < NSLOT; ++sl) {
-      if ((sl * NCP) % NSLOT == 0) {
-        __builtin_amdgcn_sched_barrier(0);
-        issue(fill, kt + kStages - 1, sl * NCP / NSLOT);
-        __builtin_amdgcn_sched_barrier(0);
+      for (int b = 0; b < NBN; ++b) {
+        acc[a][b] = mfma32(al, bh[b], acc[a][b]);
+        acc[a][b] = mfma32(ah, bl[b], acc[a][b]);
+        acc[a][b] = mfma32(am, bm[b], acc[a][b]);
+        acc[a][b] = mfma32(am, bh[b], acc[a][b]);
+        acc[a][b] = mfma32(ah, bm[b], acc[a][b]);
+        acc[a][b] = mfma32(ah, bh[b], acc[a][b]);
       }
-      if (sl == 0) load_frags(cur, 16, fa1, fb1);
-      if (sl == NBM) load_frags(nxt, 0, fa0, fb0);
-      if (sl < NBM) mma_row(fa0, fb0, sl);
-      else mma_row(fa1, fb1, sl - NBM);
     }
   };
 #pragma unroll
@@ -1069,14 +1075,11 @@ __global__ __launch_bounds__(512) void k_syrk_x6_dl(int64_t d, int64_t kw, int64
   for (int j = 0; j < NCP; ++j) issue(sb1, 1, j);
 #pragma unroll
   for (int j = 0; j < NCP; ++j) issue(sb2, 2, j);
-  __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NCP));  // stage 0 landed
-  barrier_nofence();
-  load_frags(sb0, 0, fa0, fb0);
   for (int kt = 0; kt < nk; kt += 4) {
-    step(sb0, sb1, sb3, kt);
-    if (kt + 1 < nk) step(sb1, sb2, sb0, kt + 1);
-    if (kt + 2 < nk) step(sb2, sb3, sb1, kt + 2);
-    if (kt + 3 < nk) step(sb3, sb0, sb2, kt + 3);
+    step(sb0, sb3, kt);
+    if (kt + 1 < nk) step(sb1, sb0, kt + 1);
+    if (kt + 2 < nk) step(sb2, sb1, kt + 2);
+    if (kt + 3 < nk) step(sb3, sb2, kt + 3);
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // drain the look-ahead copies before the workgroup ends
   if (!active) return;
@@ -1376,7 +1379,6 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
   s += align256(sizeof(T) * nm * d * m);         // M' (back substitution output)
   s += align256(sizeof(double) * nb * d * (r_prev > 0 ? r_prev : 1));  // S Lp
   s += 256;                                                            // lambdas
-  if (sizeof(T) == 4) s += align256(sizeof(uint16_t) * nm * 3 * kPlaneRows * d);  // split planes
   return s;
 }
 
@@ -1385,17 +1387,14 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
 // first diagonal-block launch.
 template <typename T, typename ST>
 hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st, T* Fw, T* Rw, T* Dw, T* Mpw,
-                     double* SLpw, const double* dlam, uint16_t* Plw, hipEvent_t after_diag) {
+                     double* SLpw, const double* dlam, hipEvent_t after_diag) {
   const int64_t d = a.d, m = a.r_prev + a.k, nl = a.n_lambda, nm = nbg * nl, mi0 = b0 * nl;
   T* F = Fw + mi0 * d * d;
   T* R = Rw + mi0 * d * m;
   T* D = Dw + mi0 * d;
   T* Mp = Mpw + mi0 * d * m;
-  const int64_t pl_bstride = 3 * kPlaneRows * d;
-  // trailing updates from the split planes (direct-to-LDS) when the columns come in
-  // 16-byte chunks and a matrix's planes fit 31-bit byte offsets
-  const bool planes = sizeof(T) == 4 && d % 8 == 0 && d % 4 == 0 && 2 * pl_bstride < ((int64_t)1 << 31);
-  uint16_t* Pl = planes ? Plw + mi0 * pl_bstride : nullptr;
+  // trailing updates through the direct-to-LDS kernel when a matrix fits 31-bit byte offsets
+  const bool syrk_dl = sizeof(T) == 4 && d % 4 == 0 && 4 * d * d < ((int64_t)1 << 31);
   double* SLp = SLpw + b0 * d * (a.r_prev > 0 ? a.r_prev : 1);
   int32_t* info = a.dev_info + mi0;
   const ST* S = (const ST*)a.S + b0 * a.s_bstride;
@@ -1449,7 +1448,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
         if (x6) {
           const int nF = (int)((d - pp + 255) / 256);
           k_panel_x6<kX6Strip><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
-              d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF, nullptr, 0, 0);
+              d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF);
           if (!x6r)
             k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
                 d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
@@ -1467,7 +1466,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       if (x6 && nrem > 0) {
         const int nF = (int)((nrem + 255) / 256);
         k_panel_x6<kX6Row><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
-            d, pp, pw, 0, (float*)F, (float*)R, m, nF, P1 < d ? Pl : nullptr, pl_bstride, P0);
+            d, pp, pw, 0, (float*)F, (float*)R, m, nF);
         if (!x6r)
           k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
                                                                                                (int)nchF, F, R);
@@ -1481,14 +1480,14 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       if (x6) {
         const int64_t T6 = (d - P1 + 255) / 256;
         const int nF = (int)(T6 * (T6 + 1) / 2);
-        if (Pl) {
-          k_syrk_x6_dl<<<dim3((unsigned)(nF * nm)), 512, 0, st>>>(d, P1 - P0, P1, Pl, pl_bstride, (float*)F, nF);
+        if (syrk_dl) {
+          k_syrk_f32_dl<<<dim3((unsigned)(nF * nm)), 512, 0, st>>>(d, P0, P1 - P0, P1, (float*)F, nF);
           if (x6r)
             k_panel_x6<kX6TrailRhs><<<dim3((unsigned)T6, (unsigned)nm, (unsigned)((m + 31) / 32)), 512, 0, st>>>(
-                d, P0, P1 - P0, P1, (float*)F, (float*)R, m, 0, nullptr, 0, 0);
+                d, P0, P1 - P0, P1, (float*)F, (float*)R, m, 0);
         } else {
           k_panel_x6<kX6Trail><<<dim3((unsigned)(nF + (x6r ? T6 : 0)), (unsigned)nm), 512, 0, st>>>(
-              d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF, nullptr, 0, 0);
+              d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF);
         }
         if (!x6r)
           k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
@@ -1553,7 +1552,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
 // substitution: few workgroups each) then run beside the matrix-core updates of the
 // others instead of leaving most of the GPU idle.
 #ifndef LOCA_SOLVE_GROUPS
-#define LOCA_SOLVE_GROUPS 2
+#define LOCA_SOLVE_GROUPS 3
 #endif
 constexpr int kGroups = LOCA_SOLVE_GROUPS;
 struct Aux {
@@ -1594,14 +1593,13 @@ hipError_t run_solve(const SolveArgs& a) {
   Lams lams;
   for (int i = 0; i < 8; ++i) lams.v[i] = (i < nl) ? a.lambdas[i] : 0.0;
   double* dlam = (double*)(p + align256(sizeof(double) * a.nb * d * (a.r_prev > 0 ? a.r_prev : 1)));
-  uint16_t* Pl = (uint16_t*)((char*)dlam + 256);
   // the host lambdas travel by value into a one-wave kernel (no copy from pageable memory)
   k_set_lambdas<<<1, 64, 0, a.stream>>>(lams, dlam, (int)nl);
   k_fill_zero_i32<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int G = (int)(a.nb < kGroups ? a.nb : kGroups);
-  if (G < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, Pl, nullptr);
+  if (G < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr);
   Aux* x = nullptr;
   if ((e = get_aux(&x)) != hipSuccess) return e;
   if ((e = hipEventRecord(x->fork, a.stream)) != hipSuccess) return e;
@@ -1613,7 +1611,7 @@ hipError_t run_solve(const SolveArgs& a) {
       if ((e = hipStreamWaitEvent(st, x->stagger[g], 0)) != hipSuccess) return e;
     }
     hipEvent_t after = g + 1 < G ? x->stagger[g + 1] : nullptr;
-    if ((e = run_group<T, ST>(a, b0, b1 - b0, st, F, R, D, Mp, SLp, dlam, Pl, after)) != hipSuccess) return e;
+    if ((e = run_group<T, ST>(a, b0, b1 - b0, st, F, R, D, Mp, SLp, dlam, after)) != hipSuccess) return e;
   }
   for (int g = 1; g < G; ++g) {
     if ((e = hipEventRecord(x->join[g], x->s[g])) != hipSuccess) return e;

@@ -427,48 +427,70 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   }
 }
 
-// a_out[a][i] = sum_c Ca[a][c] M[i][c];  b_out[i][a] = sum_c R[c][i] Cb[c][a]
+// a_out[a][i] = sum_c Ca[a][c] M[i][c];  b_out[i][a] = sum_c R[c][i] Cb[c][a]  (kp <= 64): one
+// thread per row i and kRA ranks a0 = kRA blockIdx.z .. (fp64 sums in the order of c), the
+// small factors in LDS ([c][a], read by every lane at once), M read by rows as float4 when
+// aligned, the rows of b_out written as float4 when r_a % 4 == 0.
+constexpr int kRA = 16;
 __global__ __launch_bounds__(kT) void k_trunc_apply(int64_t d, int64_t kp, int64_t r_a, const float* __restrict__ M,
                                                     int64_t m_bstride, const float* __restrict__ R, int64_t r_bstride,
                                                     int64_t r_group, const double* __restrict__ Ca_all,
                                                     const double* __restrict__ Cb_all, float* __restrict__ a_out,
                                                     int64_t a_bstride, float* __restrict__ b_out, int64_t b_bstride) {
-  __shared__ double sCa[kMaxKp * kMaxKp];
-  __shared__ double sCb[kMaxKp * kMaxKp];
+  __shared__ __attribute__((aligned(16))) double sCa[kMaxKp * kRA];  // [c][a - a0]
+  __shared__ __attribute__((aligned(16))) double sCb[kMaxKp * kRA];  // [c][a - a0]
   const int64_t mi = blockIdx.y;
-  for (int e = threadIdx.x; e < (int)(r_a * kp); e += kT) {
-    sCa[e] = Ca_all[mi * r_a * kp + e];
-    sCb[e] = Cb_all[mi * kp * r_a + e];
+  const int a0 = kRA * (int)blockIdx.z;
+  for (int e = threadIdx.x; e < (int)kp * kRA; e += kT) {
+    const int c = e / kRA, u = e % kRA, a = a0 + u;
+    sCa[e] = a < r_a ? Ca_all[mi * r_a * kp + (int64_t)a * kp + c] : 0.0;
+    sCb[e] = a < r_a ? Cb_all[mi * kp * r_a + (int64_t)c * r_a + a] : 0.0;
   }
   __syncthreads();
   const int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x;
   if (i >= d) return;
   const float* Mi = M + mi * m_bstride + i * kp;
   const float* Rm = R + (mi / r_group) * r_bstride;
-  float mrow[kMaxKp], rcol[kMaxKp];
-  if ((kp & 3) == 0 && (m_bstride & 3) == 0 && (((uintptr_t)M) & 15) == 0) {  // rows of M as float4
+  const bool mv4 = (kp & 3) == 0 && (m_bstride & 3) == 0 && (((uintptr_t)M) & 15) == 0;
+  double sa[kRA], sb[kRA];
 #pragma unroll
-    for (int c = 0; c < kMaxKp; c += 4) {
-      const float4 t = c < kp ? *(const float4*)(Mi + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-      mrow[c] = t.x; mrow[c + 1] = t.y; mrow[c + 2] = t.z; mrow[c + 3] = t.w;
+  for (int u = 0; u < kRA; ++u) sa[u] = sb[u] = 0.0;
+  for (int c0 = 0; c0 < kp; c0 += 4) {
+    float mv[4], rv[4];
+    if (mv4) {
+      const float4 t = *(const float4*)(Mi + c0);
+      mv[0] = t.x; mv[1] = t.y; mv[2] = t.z; mv[3] = t.w;
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) mv[t] = c0 + t < kp ? Mi[c0 + t] : 0.f;
     }
-  } else {
 #pragma unroll
-    for (int c = 0; c < kMaxKp; ++c) mrow[c] = (c < kp) ? Mi[c] : 0.f;
-  }
+    for (int t = 0; t < 4; ++t) rv[t] = c0 + t < kp ? Rm[(int64_t)(c0 + t) * d + i] : 0.f;
 #pragma unroll
-  for (int c = 0; c < kMaxKp; ++c) rcol[c] = (c < kp) ? Rm[c * d + i] : 0.f;
-  for (int a = 0; a < r_a; ++a) {
-    double sa = 0.0, sb = 0.0;
+    for (int t = 0; t < 4; ++t) {
+      if (c0 + t >= kp) break;
+      const double* ca = sCa + (c0 + t) * kRA;
+      const double* cb = sCb + (c0 + t) * kRA;
 #pragma unroll
-    for (int c = 0; c < kMaxKp; ++c) {
-      if (c < kp) {
-        sa += sCa[a * kp + c] * (double)mrow[c];
-        sb += (double)rcol[c] * sCb[c * r_a + a];
+      for (int u = 0; u < kRA; ++u) {
+        sa[u] += ca[u] * (double)mv[t];
+        sb[u] += (double)rv[t] * cb[u];
       }
     }
-    a_out[mi * a_bstride + a * d + i] = (float)sa;
-    b_out[mi * b_bstride + i * r_a + a] = (float)sb;
+  }
+  const int na = (int)(r_a - a0 < kRA ? r_a - a0 : kRA);
+#pragma unroll
+  for (int u = 0; u < kRA; ++u)
+    if (u < na) a_out[mi * a_bstride + (int64_t)(a0 + u) * d + i] = (float)sa[u];
+  float* bo = b_out + mi * b_bstride + i * r_a + a0;
+  if ((r_a & 3) == 0 && (b_bstride & 3) == 0 && (((uintptr_t)b_out) & 15) == 0) {
+#pragma unroll
+    for (int u = 0; u < kRA; u += 4)
+      if (u < na) *(float4*)(bo + u) = make_float4((float)sb[u], (float)sb[u + 1], (float)sb[u + 2], (float)sb[u + 3]);
+  } else {
+#pragma unroll
+    for (int u = 0; u < kRA; ++u)
+      if (u < na) bo[u] = (float)sb[u];
   }
 }
 
@@ -529,7 +551,8 @@ hipError_t launch_lowrank_truncate(const TruncArgs& a) {
     k_small_grams<kMaxKp><<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(
         a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, ns, Gpart);
     k_trunc_core<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.kp, a.r_a, Gpart, ns, Ca, Cb, a.sigma_out, a.sigma_bstride);
-    k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm), kT, 0, a.stream>>>(
+    k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm, (unsigned)((a.r_a + kRA - 1) / kRA)), kT, 0,
+                    a.stream>>>(
         a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
         a.b_bstride);
   } else {
