@@ -273,6 +273,12 @@ constexpr int kDLRowBytes = 512;
 // its panel, and its two waves that lie below the diagonal (no Gram output) form
 // Kraw = X_I^T [Y_hi | Y_lo] for the panel's 256 columns, 128 each.
 //
+// Cross tiles (ncross > 0, for split targets wider than the fused path's 64 columns): the
+// launch has ncross = T extra tiles per block after its Gram tiles, tile T(T+1)/2 + I being
+// row panel I of X against the split targets: an off-diagonal tile whose second ring panel
+// comes from Yhl (columns past w2p read as zero, so the waves wholly past them multiply
+// zeros) and whose result is Kraw = X_I^T [Y_hi | Y_lo] (columns < w2).
+//
 // WT: statistic weights, padded in `wpad` (zero past n, readable up to kBK floats past
 // the last stage).  The second operand (X_J, or the split targets of a cross wave) is
 // scaled and split in registers, and each row of MFMAs runs on both parts.  The split
@@ -286,7 +292,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
                                                                 const uint16_t* __restrict__ zero16, int64_t b0,
                                                                 const uint16_t* __restrict__ Yhl_all, int64_t w2,
                                                                 int64_t w2p, float* __restrict__ Kraw_all,
-                                                                const float* __restrict__ wpad) {
+                                                                const float* __restrict__ wpad, int ncross) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -304,20 +310,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   static_assert(kDLStages == 4, "the ring below is written out for four slots");
 
   const int T = (int)((d + BM - 1) / BM);
-  const int ntile = T * (T + 1) / 2;
+  const int ntile = T * (T + 1) / 2, ntot = ntile + ncross;
   const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int tl = logical % ntot;
+  const bool ctile = tl >= ntile;  // a cross tile: row panel tl - ntile against the split targets
   int I, J;
-  upper_tile(logical % ntile, T, I, J);
+  if (ctile) {
+    I = tl - ntile;
+    J = -1;
+  } else {
+    upper_tile(tl, T, I, J);
+  }
   const bool diag = (I == J);
-  const int64_t b = b0 + logical / ntile;
+  const int64_t b = b0 + logical / ntot;
   const uint16_t* X = Xall + b * x_bstride;
   float* S = Sall + b * s_bstride;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int wi = wid / WGN, wj = wid % WGN;
   const bool active = !(diag && (wj + 1) * WN <= wi * WM);
-  const bool fuse = diag && Yhl_all != nullptr;            // this tile also forms the cross statistic
-  const bool cross = fuse && !active && WGM == 2 && wj < 2;  // ... in this wave
-  const uint16_t* Yhl = fuse ? Yhl_all + b * n * w2p : zero16;
+  const bool fuse = diag && Yhl_all != nullptr && ncross == 0;  // this tile also forms the cross statistic
+  const bool cross = fuse && !active && WGM == 2 && wj < 2;     // ... in this wave
+  const bool ysec = fuse || ctile;                              // the second ring panel holds Yhl
+  const uint16_t* Yhl = ysec ? Yhl_all + b * n * w2p : zero16;
   const int64_t cI = (int64_t)I * BM, cJ = (int64_t)J * BM;
   const int nk = (int)((n + kBK - 1) / kBK);
   // fragment sources: Gram waves of a diagonal tile read both operands from the first
@@ -337,11 +351,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   // Copy j (0 .. NCP-1) of a stage: panel j / NQ (a diagonal tile loads its panel twice), chunk j % NQ.
   // buffer path: one resource for the block's X, one for its split targets
   const i32x4_t rsX = buffer_rsrc(X, (uint32_t)(n * ldx * 2));
-  const i32x4_t rsY = buffer_rsrc(Yhl, fuse ? (uint32_t)(n * w2p * 2) : 0u);
+  const i32x4_t rsY = buffer_rsrc(Yhl, ysec ? (uint32_t)(n * w2p * 2) : 0u);
   auto issue = [&](uint16_t* buf, int kt, int j) {
     const int pnl = j / NQ, q = j % NQ;
     const int64_t t = (int64_t)kt * kBK + lrow[q], col = (pnl == 0 ? cI : cJ) + lcol[q];
-    const bool ysrc = fuse && pnl == 1;
+    const bool ysrc = ysec && pnl == 1;
     if (BUF) {
       const bool ok = t < n && (ysrc ? lcol[q] < w2p : col < d);
       const uint32_t off = ok ? (uint32_t)(2 * (ysrc ? t * w2p + lcol[q] : t * ldx + col)) : kBufOutside;
@@ -440,7 +454,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));  // drain the look-ahead loads before the workgroup ends
 
   double dsum = 0.0;
-  if (active) {
+  if (active && !ctile) {
 #pragma unroll
     for (int m = 0; m < NBM; ++m)
 #pragma unroll
@@ -464,13 +478,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
         }
       }
   }
-  if (cross) {  // Kraw rows cI + 128 wj + .., columns < w2 (row stride w2)
+  if (cross || ctile) {  // Kraw rows cI + arow0 + .., columns kc0 + .. < w2 (row stride w2)
     float* Kraw = Kraw_all + b * d * w2;
+    const int kc0 = ctile ? bcol0 : 0;
 #pragma unroll
     for (int m = 0; m < NBM; ++m)
 #pragma unroll
       for (int q = 0; q < NBN; ++q) {
-        const int64_t col = 32 * q + mfma32_col(lane);
+        const int64_t col = kc0 + 32 * q + mfma32_col(lane);
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = cI + arow0 + 32 * m + mfma32_row(lane, r);
@@ -750,10 +765,10 @@ size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dty
 template <bool BUF, bool WT>
 static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_t nbc, const uint16_t* zero16,
                            double* diag_part, const uint16_t* Yhl, int64_t w2, int64_t w2p, float* Kraw,
-                           const float* wpad) {
-  k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)(ntile * nbc)), 512, 0, a.stream>>>(
+                           const float* wpad, int ncross) {
+  k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)((ntile + ncross) * nbc)), 512, 0, a.stream>>>(
       a.n, a.d, (const uint16_t*)a.x, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, Yhl, w2,
-      w2p, Kraw, wpad);
+      w2p, Kraw, wpad, ncross);
 }
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {
@@ -798,8 +813,10 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   // take the register-staged kernel when weighted)
   const bool dl = big && (a.d % 8) == 0 && (buf || !wt);
   const bool fused = dl && w2p <= 64;
+  // wider split targets: cross tiles in the same launch (one per row panel of each block)
+  const bool ctiles = dl && !fused;
   if (dl) {
-    if (fused) {
+    if (fused || ctiles) {
       dim3 gy((unsigned)((a.n * w2p + 255) / 256), (unsigned)a.nb);
       k_split_y<<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
     } else {
@@ -808,14 +825,18 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     // one-dimensional grid (the XCD-aware order spans the blocks), in chunks of blocks
     // small enough that the grid stays far below the launch limits
     const int64_t ntile = (int64_t)T * (T + 1) / 2;
-    const int64_t chunk = std::max<int64_t>(1, ((int64_t)1 << 22) / ntile);
+    const int ncross = ctiles ? T : 0;
+    const int64_t chunk = std::max<int64_t>(1, ((int64_t)1 << 22) / (ntile + ncross));
     for (int64_t b0 = 0; b0 < a.nb; b0 += chunk) {
       const int64_t nbc = std::min<int64_t>(chunk, a.nb - b0);
       const bool use_buf = buf;
-      const uint16_t* yf = fused ? Yhl : nullptr;
-      if (use_buf && wt) launch_gram_dl<true, true>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, wpad);
-      else if (use_buf) launch_gram_dl<true, false>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, nullptr);
-      else launch_gram_dl<false, false>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, nullptr);
+      const uint16_t* yf = (fused || ctiles) ? Yhl : nullptr;
+      if (use_buf && wt)
+        launch_gram_dl<true, true>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, wpad, ncross);
+      else if (use_buf)
+        launch_gram_dl<true, false>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, nullptr, ncross);
+      else
+        launch_gram_dl<false, false>(a, ntile, b0, nbc, zero16, diag_part, yf, w2, w2p, Kraw, nullptr, ncross);
     }
   } else if (big) {
     if (wt)
@@ -835,7 +856,7 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   dim3 gc((unsigned)((a.d + 255) / 256), (unsigned)a.nb);
-  if (!fused) {  // the cross statistic in a launch of its own
+  if (!fused && !ctiles) {  // the cross statistic in a launch of its own
     if (w2 <= 32)
       k_cross_bf16<32><<<gc, kThreads, 0, a.stream>>>(a.n, a.d, a.k, X, a.ldx, a.x_bstride, a.y, a.y_bstride, Kraw,
                                                        a.a_w);
