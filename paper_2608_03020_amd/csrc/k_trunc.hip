@@ -325,18 +325,24 @@ __global__ __launch_bounds__(kT) void k_trunc_apply_tiled(int64_t d, int64_t kp,
     }
 }
 
-// One workgroup per matrix: eigendecompositions and the small factors Ca, Cb (kp <= 64).
-// Both symmetric matrices are packed in LDS and diagonalised by jacobi_packed (one
-// two-sided update per round); Gm, Vb and the eigenvectors (fp64) stay in LDS.
+// One workgroup per matrix: the small factors Ca, Cb (kp <= 64).  First Gb = L L^T by
+// Cholesky (fp64, in LDS): when every pivot exceeds 1e-10 of the largest diagonal entry,
+// any square root of Gb serves for H (W = (M L)(L^{-1} R), the second factor with
+// orthonormal rows), so one eigensolve remains, of P^T P = L^T Gm L = Vp diag(s^2) Vp^T, and
+//   Ca[a][c] = (L Vp)[c][a] / s_a,   Cb[c][a] = (L^{-T} Vp)[c][a] s_a.
+// Otherwise (R close to rank deficient) Gb = Vb diag(lb) Vb^T by Jacobi, directions with
+// lb <= 1e-14 max lb dropped, and H = Vb diag(sqrt(lb)) as in the file comment.  The
+// symmetric matrices of the eigensolves are packed in LDS (jacobi_packed); Gm, the factor of
+// Gb and the eigenvectors (fp64) stay in LDS.
 __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, const double* __restrict__ Gpart,
                                                     int nsplit, double* __restrict__ Ca_all,
                                                     double* __restrict__ Cb_all, float* __restrict__ sigma_out,
                                                     int64_t sigma_bstride) {
   constexpr int KB2 = kMaxKp * kMaxKp;
   __shared__ double sA[kMaxKp * (kMaxKp + 1) / 2];
-  __shared__ double sV[KB2];   // eigenvectors of the current eigensolve; T = Gm Vb in between
-  __shared__ double sVb[KB2];  // Vb
-  __shared__ double sG[KB2];   // Gm
+  __shared__ double sV[KB2];   // eigenvectors of the current eigensolve; T = Gm H in between
+  __shared__ double sVb[KB2];  // Gb, then its factor: L (Cholesky) or Vb (Jacobi)
+  __shared__ double sG[KB2];   // Gm; L^{-T} Vp after the eigensolve (Cholesky path)
   __shared__ double sH[kMaxKp], sHi[kMaxKp], sEig[kMaxKp];
   __shared__ int sOrd[kMaxKp];
   __shared__ double cs[kMaxKp];
@@ -348,7 +354,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   const int n = K + (K & 1);  // even size for the tournament ordering
   const double* GmP = Gpart + (mi * 2) * nsplit * kp * kp;
   const double* GbP = Gpart + (mi * 2 + 1) * nsplit * kp * kp;
-  // 1. Gb = Vb diag(lb) Vb^T; Gm (each summed over the row ranges, in order) into sG
+  // 1. Gm into sG and Gb into sVb (n x n, zero padded), each summed over the row ranges in order
   for (int e = tid; e < n * n; e += kTC) {
     const int i = e / n, j = e % n;
     double gb = 0.0, gm = 0.0;
@@ -358,41 +364,99 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
         gm += GmP[z * kp * kp + i * kp + j];
       }
     sG[e] = gm;
-    if (i <= j) sA[pk(i, j, n)] = gb;
+    sVb[e] = gb;
   }
   __syncthreads();
-  jacobi_packed<double>(sA, sV, n, cs, pairs, red);
-  __syncthreads();
+  // 2. Gb = L L^T in place (lower triangle of sVb), or a failed pivot
   if (tid == 0) {
-    double lmax = 0.0;
-    for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
-    red[12] = lmax;
+    double mx = 0.0;
+    for (int j = 0; j < K; ++j) mx = fmax(mx, sVb[j * n + j]);
+    red[13] = mx;
+    red[14] = 0.0;
   }
   __syncthreads();
-  for (int j = tid; j < n; j += kTC) {
-    const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
-    const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
-    sH[j] = keep ? sqrt(lb) : 0.0;
-    sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+  const double thr = 1e-10 * red[13];
+  for (int j = 0; j < K; ++j) {
+    if (tid == 0) {
+      const double piv = sVb[j * n + j];
+      if (!(piv > thr)) red[14] = 1.0;
+      sVb[j * n + j] = sqrt(fmax(piv, 0.0));
+    }
+    __syncthreads();
+    if (red[14] != 0.0) break;
+    const double ljj = sVb[j * n + j];
+    for (int i = j + 1 + tid; i < K; i += kTC) sVb[i * n + j] /= ljj;
+    __syncthreads();
+    const int rem = K - j - 1;
+    for (int e = tid; e < rem * rem; e += kTC) {
+      const int i = j + 1 + e / rem, c = j + 1 + e % rem;
+      if (c <= i) sVb[i * n + c] -= sVb[i * n + j] * sVb[c * n + j];
+    }
+    __syncthreads();
   }
-  for (int e = tid; e < n * n; e += kTC) sVb[e] = sV[e];
-  __syncthreads();
-  // 2. T = Gm Vb (into sV), then P^T P = H Vb^T T H (upper triangle, packed)
-  for (int e = tid; e < n * n; e += kTC) {
-    const int i = e / n, j = e % n;
-    double s = 0.0;
-    for (int c = 0; c < n; ++c) s += sG[i * n + c] * sVb[c * n + j];
-    sV[e] = s;
+  const bool chol = red[14] == 0.0;
+  if (chol) {
+    // 3. T = Gm L (into sV), P^T P = L^T T (upper triangle, packed; zero padding)
+    for (int e = tid; e < K * K; e += kTC) {
+      const int i = e / K, c = e % K;
+      double s = 0.0;
+      for (int x = c; x < K; ++x) s += sG[i * n + x] * sVb[x * n + c];
+      sV[i * n + c] = s;
+    }
+    __syncthreads();
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (i > j) continue;
+      double s = 0.0;
+      if (j < K)
+        for (int x = i; x < K; ++x) s += sVb[x * n + i] * sV[x * n + j];
+      sA[pk(i, j, n)] = s;
+    }
+    __syncthreads();
+  } else {
+    // 3'. Gb = Vb diag(lb) Vb^T by Jacobi; H = Vb diag(sqrt(lb)) over the kept directions
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (i > j) continue;
+      double gb = 0.0;
+      if (j < K)
+        for (int z = 0; z < nsplit; ++z) gb += GbP[z * kp * kp + i * kp + j];
+      sA[pk(i, j, n)] = gb;
+    }
+    __syncthreads();
+    jacobi_packed<double>(sA, sV, n, cs, pairs, red);
+    __syncthreads();
+    if (tid == 0) {
+      double lmax = 0.0;
+      for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
+      red[12] = lmax;
+    }
+    __syncthreads();
+    for (int j = tid; j < n; j += kTC) {
+      const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
+      const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
+      sH[j] = keep ? sqrt(lb) : 0.0;
+      sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+    }
+    for (int e = tid; e < n * n; e += kTC) sVb[e] = sV[e];
+    __syncthreads();
+    // T = Gm Vb (into sV), then P^T P = H Vb^T T H (upper triangle, packed)
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      double s = 0.0;
+      for (int c = 0; c < n; ++c) s += sG[i * n + c] * sVb[c * n + j];
+      sV[e] = s;
+    }
+    __syncthreads();
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (i > j) continue;
+      double s = 0.0;
+      for (int c = 0; c < n; ++c) s += sVb[c * n + i] * sV[c * n + j];
+      sA[pk(i, j, n)] = s * sH[i] * sH[j];
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  for (int e = tid; e < n * n; e += kTC) {
-    const int i = e / n, j = e % n;
-    if (i > j) continue;
-    double s = 0.0;
-    for (int c = 0; c < n; ++c) s += sVb[c * n + i] * sV[c * n + j];
-    sA[pk(i, j, n)] = s * sH[i] * sH[j];
-  }
-  __syncthreads();
   jacobi_packed<double>(sA, sV, n, cs, pairs, red);  // sV = Vp
   __syncthreads();
   if (tid == 0) {
@@ -405,10 +469,18 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
       sOrd[j + 1] = key;
     }
   }
+  if (chol) {  // Z = L^{-T} Vp (into sG, Gm no longer needed): one column per thread
+    for (int a = tid; a < n; a += kTC)
+      for (int c = K - 1; c >= 0; --c) {
+        double s = sV[c * n + a];
+        for (int x = c + 1; x < K; ++x) s -= sVb[x * n + c] * sG[x * n + a];
+        sG[c * n + a] = s / sVb[c * n + c];
+      }
+  }
   __syncthreads();
   const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
   for (int j = tid; j < K; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
-  // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
+  // 4. Ca[a][c] = (H Vp)[c][ord a] / s_a ;  Cb[c][a] = (H^{-T} Vp)[c][ord a] * s_a
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
   for (int e = tid; e < (int)(r_a * kp); e += kTC) {
@@ -416,10 +488,15 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
     const int col = sOrd[a];
     const double sa = sqrt(fmax(sEig[col], 0.0));
     double u = 0.0, v = 0.0;
-    for (int x = 0; x < n; ++x) {
-      const double vb = sVb[c * n + x], vp = sV[x * n + col];
-      u += vb * sH[x] * vp;
-      v += vb * sHi[x] * vp;
+    if (chol) {
+      for (int x = 0; x <= c; ++x) u += sVb[c * n + x] * sV[x * n + col];
+      v = sG[c * n + col];
+    } else {
+      for (int x = 0; x < n; ++x) {
+        const double vb = sVb[c * n + x], vp = sV[x * n + col];
+        u += vb * sH[x] * vp;
+        v += vb * sHi[x] * vp;
+      }
     }
     const bool live = sa > 1e-30 * s1 && sa > 0.0;
     Ca[a * kp + c] = live ? u / sa : 0.0;
