@@ -99,12 +99,13 @@ def make_inputs(cfg, nb, device="cuda"):
 
 
 def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, lp=None, rp=None,
-             solve_record=None):
+             solve_record=None, error_record=None):
     """One step of the whole path over every block: per micro-batch the head error
-    and credit coordinates, then the statistics (bracketed by the events of
-    `record[m]` when given); then the ridge solves and the truncation (bracketed by
-    `solve_record`).  Optional: statistic weights a_all (n,), a current adapter
-    lp (nb, d, r_prev), rp (nb, r_prev, d)."""
+    and credit coordinates (from the event error_record[m] when given), then the
+    statistics (bracketed by the events of `record[m]` when given); then the ridge
+    solves and the truncation (bracketed by `solve_record`: start, between the solves
+    and the truncation when it has three events, end).  Optional: statistic weights
+    a_all (n,), a current adapter lp (nb, d, r_prev), rp (nb, r_prev, d)."""
     from paper_2608_03020_amd import loca
     step.reset()
     for m in range(cfg.n_micro):
@@ -112,6 +113,8 @@ def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, 
         xm = x_all[:, lo:hi]
         yv = step.Y[:, :hi - lo]
         aw = None if a_all is None else a_all[lo:hi]
+        if error_record is not None:
+            error_record[m].record(stream)
         loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, a_w=aw, nb=nb)
         if record is not None:
             record[m][0].record(stream)
@@ -120,9 +123,10 @@ def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, 
             record[m][1].record(stream)
     if solve_record is not None:
         solve_record[0].record(stream)
-    step.solve(B, lp=lp, rp=rp)
+    step.solve(B, lp=lp, rp=rp, mid_event=solve_record[1] if solve_record is not None and len(solve_record) > 2
+               else None)
     if solve_record is not None:
-        solve_record[1].record(stream)
+        solve_record[-1].record(stream)
 
 
 def stats_flops(cfg, nb):
@@ -392,8 +396,13 @@ def main():
     n_mb = cfg.n_micro
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps * n_mb)]
 
-    def one_step(record=None):
-        run_step(step, cfg, nb, x_all, z, y, A, B, stream, record)
+    ev_err = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps * n_mb)]
+    ev_sol = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+
+    def one_step(record=None, s=None):
+        run_step(step, cfg, nb, x_all, z, y, A, B, stream, record,
+                 solve_record=ev_sol[s] if s is not None else None,
+                 error_record=ev_err[s * n_mb:(s + 1) * n_mb] if s is not None else None)
 
     for _ in range(args.warmup):
         one_step()
@@ -401,7 +410,7 @@ def main():
     print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     for s in range(args.steps):
-        one_step(ev[s * n_mb:(s + 1) * n_mb])
+        one_step(ev[s * n_mb:(s + 1) * n_mb], s)
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     ms_step = dt * 1e3 / args.steps
@@ -418,6 +427,14 @@ def main():
     peak = FP64_PEAK_TFLOPS if cfg.mode == "fp32" else BF16_PEAK_TFLOPS
 
     value = nb * cfg.n / (ms_step * 1e-3)
+    K = args.steps
+    breakdown = {
+        "unit": "ms per step (HIP events on the launch stream)",
+        "head_error_and_coordinates": sum(ev_err[i].elapsed_time(ev[i][0]) for i in range(K * n_mb)) / K,
+        "statistics": sum(stats_ms) / K,
+        "ridge_solves": sum(e[0].elapsed_time(e[1]) for e in ev_sol) / K,
+        "truncation": sum(e[1].elapsed_time(e[2]) for e in ev_sol) / K,
+    }
     out = {
         "metric": "tokens/sec per block (error->target->Gram+solve); % MFMA peak on X^T X",
         "value": value,
@@ -438,6 +455,7 @@ def main():
                      "frac": achieved / peak, "traffic": traffic_bytes(args.config),
                      "kernel": "loca_accumulate_stats (Gram S += X^T X and cross X^T Y of all blocks, one micro-batch)",
                      "algorithmic_flops_per_launch": f_avg, "avg_launch_ms": t_avg},
+        "breakdown": breakdown,
     }
     if args.next:
         out["next"] = next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream)

@@ -71,13 +71,14 @@ class BlockStep:
         if keep_log:
             self.mb_log.append(self.mb.clone())
 
-    def solve(self, credit_b, proj_a=None, stream=None, lp=None, rp=None):
+    def solve(self, credit_b, proj_a=None, stream=None, lp=None, rp=None, mid_event=None):
         """Rows a5-a6: ridge solves for every lambda and the rank-r_a truncation.
 
         With a current adapter W_prev = Lp Rp (lp: (nb, d, r_prev), rp: (nb, r_prev, d);
         the outer iteration past its first step, Theorem S6.1 with W_prev != 0), the solve
         takes the right-hand sides [S Lp | K] and W = M [Rp; B~] is truncated from its
-        factors; the stacked right factor is a copy (layout only)."""
+        factors; the stacked right factor is a copy (layout only).  mid_event, when given,
+        is recorded on the current stream between the solves and the truncation."""
         import torch
         cfg = self.cfg
         nl = len(cfg.lambdas)
@@ -90,6 +91,8 @@ class BlockStep:
         else:
             loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, stream=stream)
             right = credit_b
+        if mid_event is not None:
+            mid_event.record(stream if stream is not None else torch.cuda.current_stream())
         loca.loca_lowrank_truncate(self.M.view(self.nb * nl, cfg.d, kp), right, cfg.r_a, self.A_ad, self.B_ad,
                                    self.sigma, self.info, self.ws, r_group=nl, stream=stream)
         if self.projected and proj_a is not None:
