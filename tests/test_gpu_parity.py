@@ -69,8 +69,12 @@ CASES = {
     # cross statistic inside the Gram launch: widest split target (2k = 64), and a padded one (2k = 10 -> 16)
     "bf16_d1536_k32_fused": gen.custom_config("t11", blocks=1, d=1536, n=2000, micro=1000, C=5, k=32, r_a=8),
     "bf16_d1280_k5_fused": gen.custom_config("t12", blocks=2, d=1280, n=1600, micro=800, C=3, k=5, r_a=2),
-    # 2k = 128 > 64: the cross statistic in its own launch beside the direct-load Gram kernel
+    # 2k = 128 > 64: the cross statistic as cross tiles of the direct-load Gram launch (half of
+    # each cross tile's columns past the split targets)
     "bf16_d1024_k64": gen.custom_config("t13", blocks=1, d=1024, n=1200, C=3, k=64, r_a=8),
+    # 2k = 256: cross tiles at their full width, ragged d against 256-wide tiles, two blocks,
+    # two micro-batches; 128 right-hand sides in the solve and the large truncation core
+    "bf16_d1288_k128": gen.custom_config("t16", blocks=2, d=1288, n=2700, micro=1500, C=6, k=128, r_a=16),
     # fp32 mode with fewer tokens than features (null space amplified by 1/lambda)
     "fp32_n150_d200": gen.custom_config("t3", blocks=2, d=200, n=150, C=2, k=8, r_a=8, mode="fp32",
                                         x_dist="gauss_outlier", n_outlier=3, outlier_scale=20.0, logit_std=2.0),
