@@ -24,35 +24,78 @@ constexpr int kSmallMaxC = 64;
 constexpr int kSmallMaxK = 64;
 constexpr int kMaxK = 128;
 
-// G_b = B~_b B~_b^T (k x k, fp64), one thread per (a, c) entry.
-// G = B~ B~^T in float64, one workgroup per (block, row a, kCG columns c): the threads
-// stride over the width d with coalesced reads of row a and the kCG rows c, then each
-// entry is summed over the workgroup in a fixed order.
-constexpr int kCG = 16;
-__global__ __launch_bounds__(256) void k_credit_gram(int64_t k, int64_t d, const float* __restrict__ B,
-                                                     int64_t b_bstride, double* __restrict__ G) {
-  const int64_t b = blockIdx.z, a = blockIdx.y, c0 = (int64_t)blockIdx.x * kCG;
+// G_b = B~_b B~_b^T (k x k, float64) in two passes.  k_credit_gram_part: one workgroup per
+// (32 x 32 tile on or above the diagonal, one of kCGSplit ranges of the width d, block);
+// the tile's 32 + 32 rows of B~ stream through LDS in 64-column chunks (the next chunk
+// loaded while the current one is used) and each thread sums four entries in fp64 in the
+// order of the columns.  k_credit_gram_sum adds the kCGSplit partials of an entry in a fixed
+// order and writes it and its mirror: deterministic.
+constexpr int kCGSplit = 8, kCGC = 64;
+__global__ __launch_bounds__(256) void k_credit_gram_part(int64_t k, int64_t d, const float* __restrict__ B,
+                                                          int64_t b_bstride, double* __restrict__ part) {
+  __shared__ float sa[32][kCGC + 1], sc[32][kCGC + 1];
+  const int T = (int)((k + 31) / 32);
+  int u = blockIdx.x, I = 0;
+  while (u >= T - I) { u -= T - I; ++I; }
+  const int J = I + u;
+  const int64_t s = blockIdx.y, b = blockIdx.z;
   const float* Bb = B + b * b_bstride;
-  double s[kCG];
+  const int64_t a0 = 32 * (int64_t)I, c0 = 32 * (int64_t)J;
+  const int64_t chunk = ((d + kCGSplit - 1) / kCGSplit + kCGC - 1) / kCGC * kCGC;
+  const int64_t i0 = s * chunk, i1 = i0 + chunk < d ? i0 + chunk : d;
+  const int t = threadIdx.x, ra = t >> 3, c4 = 4 * (t & 7);
+  const int lrow = t >> 3, lcol = 8 * (t & 7);  // this thread's staging: row lrow, columns lcol .. lcol + 7
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  float va[8], vc[8];
+  auto load = [&](int64_t j0) {
 #pragma unroll
-  for (int j = 0; j < kCG; ++j) s[j] = 0.0;
-  for (int64_t i = threadIdx.x; i < d; i += 256) {
-    const double x = (double)Bb[a * d + i];
+    for (int e = 0; e < 8; ++e) {
+      const int64_t col = j0 + lcol + e;
+      const bool okc = col < i1;
+      va[e] = (okc && a0 + lrow < k) ? Bb[(a0 + lrow) * d + col] : 0.f;
+      vc[e] = (okc && c0 + lrow < k) ? Bb[(c0 + lrow) * d + col] : 0.f;
+    }
+  };
+  if (i0 < i1) load(i0);
+  for (int64_t j0 = i0; j0 < i1; j0 += kCGC) {
+    __syncthreads();  // the previous chunk is no longer read
 #pragma unroll
-    for (int j = 0; j < kCG; ++j) s[j] += x * (double)ld_or_zero(Bb, (c0 + j) * d + i, c0 + j < k);
+    for (int e = 0; e < 8; ++e) {
+      sa[lrow][lcol + e] = va[e];
+      sc[lrow][lcol + e] = vc[e];
+    }
+    __syncthreads();
+    if (j0 + kCGC < i1) load(j0 + kCGC);
+#pragma unroll 8
+    for (int kk = 0; kk < kCGC; ++kk) {
+      const double x = (double)sa[ra][kk];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) acc[q] += x * (double)sc[c4 + q][kk];
+    }
   }
-  __shared__ double red[kCG][4];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  double* P = part + ((s * (int64_t)gridDim.z + b) * k) * k;
 #pragma unroll
-  for (int j = 0; j < kCG; ++j) {
-    const double v = wave_sum(s[j]);
-    if (lane == 0) red[j][wid] = v;
-  }
-  __syncthreads();
-  if ((int)threadIdx.x < kCG && c0 + threadIdx.x < k)
-    G[b * k * k + a * k + c0 + threadIdx.x] = ((red[threadIdx.x][0] + red[threadIdx.x][1]) + red[threadIdx.x][2]) +
-                                              red[threadIdx.x][3];
+  for (int q = 0; q < 4; ++q)
+    if (a0 + ra < k && c0 + c4 + q < k) P[(a0 + ra) * k + c0 + c4 + q] = acc[q];
 }
+__global__ void k_credit_gram_sum(int64_t k, int64_t nb, const double* __restrict__ part, double* __restrict__ G) {
+  const int64_t b = blockIdx.y, e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= k * k) return;
+  const int64_t a = e / k, c = e % k;
+  if (a > c) return;  // written as the mirror of (c, a)
+  double v = 0.0;
+  for (int s = 0; s < kCGSplit; ++s) v += part[((s * nb + b) * k + a) * k + c];
+  G[(b * k + a) * k + c] = v;
+  G[(b * k + c) * k + a] = v;
+}
+static void launch_credit_gram(hipStream_t st, int64_t nb, int64_t k, int64_t d, const float* B, int64_t b_bstride,
+                               double* part, double* G) {
+  const int T = (int)((k + 31) / 32);
+  k_credit_gram_part<<<dim3((unsigned)(T * (T + 1) / 2), kCGSplit, (unsigned)nb), 256, 0, st>>>(k, d, B, b_bstride,
+                                                                                                  part);
+  k_credit_gram_sum<<<dim3((unsigned)((k * k + 255) / 256), (unsigned)nb), 256, 0, st>>>(k, nb, part, G);
+}
+static size_t credit_gram_part_ws(int64_t nb, int64_t k) { return align256(sizeof(double) * kCGSplit * nb * k * k); }
 
 template <typename LT, typename AT, int KB>
 __global__ __launch_bounds__(kSmallThreads) void k_error_small(
@@ -349,6 +392,7 @@ static bool use_product(const ErrorArgs& a) {
 
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k) {
   size_t s = align256(sizeof(double) * nb * k * k);  // G
+  s += credit_gram_part_ws(nb, k);                   // partials of G
   const int64_t parts = use_small(C, k) ? (n + kSmallThreads - 1) / kSmallThreads : (n + kLargeTok - 1) / kLargeTok;
   s += align256(sizeof(double) * nb * parts);          // partials
   if (!use_small(C, k)) {
@@ -396,14 +440,15 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   char* p = a.ws;
   double* G = (double*)p;
   p += align256(sizeof(double) * a.nb * a.k * a.k);
+  double* gpart = (double*)p;
+  p += credit_gram_part_ws(a.nb, a.k);
   double* partial = (double*)p;
   const int64_t parts = use_small(a.C, a.k) ? (a.n + kSmallThreads - 1) / kSmallThreads : (a.n + kLargeTok - 1) / kLargeTok;
   p += align256(sizeof(double) * a.nb * parts);
   float* ms = use_small(a.C, a.k) ? nullptr : (float*)p;
 
   k_fill_i32<<<1, 64, 0, a.stream>>>(a.dev_info, 1, INT32_MAX);
-  dim3 gg((unsigned)((a.k + kCG - 1) / kCG), (unsigned)a.k, (unsigned)a.nb);
-  k_credit_gram<<<gg, 256, 0, a.stream>>>(a.k, a.d, a.credit_b, a.b_bstride, G);
+  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_product(a)) {
@@ -440,14 +485,15 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
 // ------------------------------------------------------------------ paper-order credit
 
 size_t credit_from_top_error_ws(int64_t nb, int64_t n, int64_t k) {
-  return align256(sizeof(double) * nb * k * k) + align256(sizeof(double) * nb * ((n + 63) / 64));
+  return align256(sizeof(double) * nb * k * k) + credit_gram_part_ws(nb, k) +
+         align256(sizeof(double) * nb * ((n + 63) / 64));
 }
 
 hipError_t launch_credit_from_top_error(const CreditArgs& a) {
   double* G = (double*)a.ws;
-  double* partial = (double*)(a.ws + align256(sizeof(double) * a.nb * a.k * a.k));
-  dim3 gg((unsigned)((a.k + kCG - 1) / kCG), (unsigned)a.k, (unsigned)a.nb);
-  k_credit_gram<<<gg, 256, 0, a.stream>>>(a.k, a.d, a.credit_b, a.b_bstride, G);
+  double* gpart = (double*)(a.ws + align256(sizeof(double) * a.nb * a.k * a.k));
+  double* partial = (double*)((char*)gpart + credit_gram_part_ws(a.nb, a.k));
+  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G);
   dim3 g((unsigned)((a.n + 63) / 64), (unsigned)a.nb);
 #define LOCA_PROJ(KQ)                                                                                          \
   k_credit_project<KQ><<<g, 256, 0, a.stream>>>(a.n, a.d, a.k, a.e, a.ld_e, a.vk, a.v_bstride, G, a.a_w, a.y_out, \

@@ -319,7 +319,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
     I = tl - ntile;
     J = -1;
   } else {
-    upper_tile(tl, T, I, J);
+    upper_tile_banded(tl, T, I, J);
   }
   const bool diag = (I == J);
   const int64_t b = b0 + logical / ntot;

@@ -85,6 +85,21 @@ LOCA_DEV int pk(int i, int j, int n) {
   return i * n - (i * (i - 1)) / 2 + (j - i);
 }
 
+// 1/x and 1/sqrt(x) in double from the hardware approximations and two Newton steps each
+// (full double precision for the finite, nonzero arguments of the rotations below).
+LOCA_DEV double rcp64(double x) {
+  double y = __builtin_amdgcn_rcp(x);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) y = fma(y, fma(-x, y, 1.0), y);
+  return y;
+}
+LOCA_DEV double rsq64(double x) {
+  double y = __builtin_amdgcn_rsq(x);
+#pragma unroll
+  for (int i = 0; i < 2; ++i) y = y * fma(-0.5 * x * y, y, 1.5);
+  return y;
+}
+
 // Cyclic Jacobi on the packed symmetric n x n matrix A (n even), eigenvectors into the
 // n x n V of type VT (row-major, columns are the vectors; rotations computed in fp64).  Each
 // round rotates n/2 disjoint pairs (round-robin tournament order: position 0 fixed, the
@@ -119,10 +134,11 @@ LOCA_DEV void jacobi_packed(double* A, VT* V, int n, double* cs, int* pairs, dou
         pairs[2 * tid + 1] = q;
         const double apq = A[pk(p, q, n)], app = A[pk(p, p, n)], aqq = A[pk(q, q, n)];
         double c = 1.0, s = 0.0;
-        if (fabs(apq) > 1e-300 && fabs(apq) > 1e-18 * sqrt(fabs(app * aqq))) {
-          const double tau = (aqq - app) / (2.0 * apq);
-          const double t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-          c = 1.0 / sqrt(1.0 + t * t);
+        if (fabs(apq) > 1e-300 && apq * apq > 1e-36 * fabs(app * aqq)) {
+          const double tau = (aqq - app) * rcp64(2.0 * apq);
+          const double u = 1.0 + tau * tau;
+          const double t = (tau >= 0.0 ? 1.0 : -1.0) * rcp64(fabs(tau) + u * rsq64(u));
+          c = rsq64(1.0 + t * t);
           s = t * c;
         }
         cs[2 * tid] = c;

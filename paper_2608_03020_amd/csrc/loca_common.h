@@ -197,6 +197,31 @@ constexpr uint32_t kBufOutside = 0x80000000u;  // past every range used here (< 
 // Workgroup barrier without a memory fence (the pipeline waits for its own loads explicitly).
 LOCA_DEV void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
 
+// Upper tile u (I <= J, T tiles per side) in an order that keeps consecutive tiles
+// compact: bands of kBand tile rows, each band column by column (rows top to bottom).
+// A window of 32 consecutive tiles then spans about 4 rows x 8 columns of tiles, so the
+// tiles an XCD runs at the same time share more of their panels than in row order.
+constexpr int kBand = 4;
+LOCA_DEV void upper_tile_banded(int u, int T, int& I, int& J) {
+  int r0 = 0;
+  for (;;) {  // skip whole bands
+    const int h = T - r0 < kBand ? T - r0 : kBand;
+    const int cnt = h * (T - r0) - h * (h - 1) / 2;  // tiles of rows r0 .. r0 + h - 1 with J >= I
+    if (u < cnt) break;
+    u -= cnt;
+    r0 += h;
+  }
+  int j = r0;
+  for (;;) {  // columns of the band: column j holds rows r0 .. min(j, r0 + kBand - 1)
+    const int hc = (j - r0 + 1) < kBand ? (j - r0 + 1) : kBand;
+    if (u < hc) break;
+    u -= hc;
+    ++j;
+  }
+  I = r0 + u;
+  J = j;
+}
+
 // The hardware hands consecutive workgroups to the eight XCDs in turn, and each XCD
 // has its own L2.  Workgroup L is therefore given logical tile x * per + idx, with
 // x = L % 8 and idx = L / 8, so that the tiles one XCD runs at the same time are
