@@ -420,13 +420,6 @@ LOCA_DEV void zero16(f32x16_t& acc) {
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 }
 
-// Wait until this wave's LDS operations are done (s_waitcnt lgkmcnt(0)); with the
-// in-order LDS of a wave, rows one lane writes are then read back by the others.
-LOCA_DEV void wave_lds_sync() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);
-  __builtin_amdgcn_wave_barrier();
-}
-
 // One wave factors the 32 x 32 block B (upper part used) as U^T U, writes U over B (zero
 // below the diagonal) and X = U^{-1} to Xo.  Lane c < 32 holds column c (rows 0..31);
 // lanes 32..63 mirror lanes 0..31 and write nothing.  Rows of the current matrix are

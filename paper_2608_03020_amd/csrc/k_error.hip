@@ -78,24 +78,42 @@ __global__ __launch_bounds__(256) void k_credit_gram_part(int64_t k, int64_t d, 
   for (int q = 0; q < 4; ++q)
     if (a0 + ra < k && c0 + c4 + q < k) P[(a0 + ra) * k + c0 + c4 + q] = acc[q];
 }
-__global__ void k_credit_gram_sum(int64_t k, int64_t nb, const double* __restrict__ part, double* __restrict__ G) {
+// G is written with row stride ldg >= k, zero in the rows and columns past k.
+__global__ void k_credit_gram_sum(int64_t k, int64_t ldg, int64_t nb, const double* __restrict__ part,
+                                  double* __restrict__ G) {
   const int64_t b = blockIdx.y, e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= k * k) return;
-  const int64_t a = e / k, c = e % k;
+  if (e >= ldg * ldg) return;
+  const int64_t a = e / ldg, c = e % ldg;
   if (a > c) return;  // written as the mirror of (c, a)
   double v = 0.0;
-  for (int s = 0; s < kCGSplit; ++s) v += part[((s * nb + b) * k + a) * k + c];
-  G[(b * k + a) * k + c] = v;
-  G[(b * k + c) * k + a] = v;
+  if (c < k)
+    for (int s = 0; s < kCGSplit; ++s) v += part[((s * nb + b) * k + a) * k + c];
+  G[(b * ldg + a) * ldg + c] = v;
+  G[(b * ldg + c) * ldg + a] = v;
 }
 static void launch_credit_gram(hipStream_t st, int64_t nb, int64_t k, int64_t d, const float* B, int64_t b_bstride,
-                               double* part, double* G) {
+                               double* part, double* G, int64_t ldg) {
   const int T = (int)((k + 31) / 32);
   k_credit_gram_part<<<dim3((unsigned)(T * (T + 1) / 2), kCGSplit, (unsigned)nb), 256, 0, st>>>(k, d, B, b_bstride,
                                                                                                   part);
-  k_credit_gram_sum<<<dim3((unsigned)((k * k + 255) / 256), (unsigned)nb), 256, 0, st>>>(k, nb, part, G);
+  k_credit_gram_sum<<<dim3((unsigned)((ldg * ldg + 255) / 256), (unsigned)nb), 256, 0, st>>>(k, ldg, nb, part, G);
 }
 static size_t credit_gram_part_ws(int64_t nb, int64_t k) { return align256(sizeof(double) * kCGSplit * nb * k * k); }
+
+// One thread per token.  A~ (C x k, [c][j]) sits in LDS; G (KB x KB, zero past k, the same
+// for every lane) is read through scalar loads straight into the fp64 products.  The
+// token's Y row stays in registers and reaches HBM through a per-wave LDS transpose, so
+// that a wave writes whole rows of consecutive tokens instead of one column of 64 rows
+// per store.  The transpose buffers reuse the A~ area once it is consumed.
+static int64_t small_kb(int64_t k) { return k <= 16 ? 16 : k <= 32 ? 32 : 64; }
+template <int KB>
+struct SmallLds {
+  static constexpr int CW = KB < 32 ? KB : 32;         // Y columns per transpose pass
+  static constexpr int WST = 64 * (CW + 1);            // floats per wave (odd row stride)
+  static constexpr int IN = kSmallMaxC * KB * 4;
+  static constexpr int ST = 4 * WST * 4;
+  static constexpr int BYTES = IN > ST ? IN : ST;
+};
 
 template <typename LT, typename AT, int KB>
 __global__ __launch_bounds__(kSmallThreads) void k_error_small(
@@ -103,17 +121,22 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
     const int32_t* __restrict__ labels, const float* __restrict__ w, const float* __restrict__ aw,
     const AT* __restrict__ A, int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out,
     int64_t y_bstride, float* __restrict__ e_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
-  __shared__ float sA[kSmallMaxC * KB];
-  __shared__ double sG[KB * KB];
+  using L = SmallLds<KB>;
+  static_assert(kSmallThreads == 256, "four waves");
+  __shared__ __attribute__((aligned(16))) unsigned char lds[L::BYTES];
   __shared__ double sred[kSmallThreads / 64];
+  float* sA = (float*)lds;  // C x k, row stride k
   const int64_t b = blockIdx.y;
   const AT* Ab = A + b * a_bstride;
+  const double* Gb = G + b * KB * KB;
   for (int64_t e = threadIdx.x; e < C * k; e += blockDim.x) sA[e] = load_as_f32(Ab + e);
-  for (int64_t e = threadIdx.x; e < k * k; e += blockDim.x) sG[e] = G[b * k * k + e];
   __syncthreads();
 
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   double q = 0.0;
+  float y[KB];
+#pragma unroll
+  for (int j = 0; j < KB; ++j) y[j] = 0.f;
   if (t < n) {
     const LT* zt = logits + t * ld;
     const int32_t yt = labels[t];
@@ -126,9 +149,6 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
       for (int64_t c = 0; c < C; ++c) s += __expf(load_as_f32(zt + c) - m);
       const float inv = 1.0f / s;
       const float wt = w ? w[t] : 1.0f;
-      float y[KB];
-#pragma unroll
-      for (int j = 0; j < KB; ++j) y[j] = 0.f;
       for (int64_t c = 0; c < C; ++c) {
         const float e = wt * (__expf(load_as_f32(zt + c) - m) * inv - (c == yt ? 1.0f : 0.0f));
         if (e_out) e_out[t * C + c] = e;
@@ -136,22 +156,46 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
         for (int j = 0; j < KB; ++j)
           if (j < k) y[j] = fmaf(e, sA[c * k + j], y[j]);
       }
-      float* yo = y_out + b * y_bstride + t * k;
+      // q = y G y^T (fp64; G symmetric, so off-diagonal terms are doubled; entries past k
+      // are zero in both y and G).  Only the fp64 copy of y stays live past this point: the
+      // float values are recovered from it exactly.
+      double yd[KB];
 #pragma unroll
-      for (int j = 0; j < KB; ++j)
-        if (j < k) yo[j] = y[j];
-      // q = y G y^T (fp64; G symmetric, so off-diagonal terms are doubled)
+      for (int j = 0; j < KB; ++j) yd[j] = (double)y[j];
 #pragma unroll
       for (int a = 0; a < KB; ++a) {
-        if (a < k) {
-          double r = 0.5 * sG[a * k + a] * (double)y[a];
+        double r = 0.5 * Gb[a * KB + a] * yd[a];
 #pragma unroll
-          for (int c2 = a + 1; c2 < KB; ++c2)
-            if (c2 < k) r += sG[a * k + c2] * (double)y[c2];
-          q += 2.0 * (double)y[a] * r;
-        }
+        for (int c2 = a + 1; c2 < KB; ++c2) r += Gb[a * KB + c2] * yd[c2];
+        q += 2.0 * yd[a] * r;
       }
+#pragma unroll
+      for (int j = 0; j < KB; ++j) y[j] = (float)yd[j];
       if (aw) q *= (double)aw[t];  // statistic weight of the position
+    }
+  }
+  __syncthreads();  // every read of sA retired: the area becomes the transpose buffers
+
+  // Y through the wave's transpose buffer, CW columns per pass: lane l puts its row at
+  // l (CW + 1), then each store instruction covers 64 / CW consecutive tokens x CW columns.
+  constexpr int CW = L::CW;
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  float* sT = (float*)lds + wv * L::WST;
+  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + 64 * wv;
+  float* yb = y_out + b * y_bstride;
+#pragma unroll
+  for (int h = 0; h < KB / CW; ++h) {
+    if (h * CW < k) {
+#pragma unroll
+      for (int j = 0; j < CW; ++j) sT[lane * (CW + 1) + j] = y[h * CW + j];
+      wave_lds_sync();
+#pragma unroll
+      for (int i = 0; i < CW; ++i) {
+        const int e = lane + 64 * i, p = e / CW, c = e % CW;
+        const int64_t tp = t0 + p, col = (int64_t)h * CW + c;
+        if (tp < n && col < k) yb[tp * k + col] = sT[p * (CW + 1) + c];
+      }
+      wave_lds_sync();
     }
   }
   const double tot = block_sum(q, sred);
@@ -390,8 +434,12 @@ static bool use_product(const ErrorArgs& a) {
   return true;
 }
 
+// row stride of G in the workspace: the small kernel's padded width, else k
+static int64_t g_ld(int64_t C, int64_t k) { return use_small(C, k) ? small_kb(k) : k; }
+
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k) {
-  size_t s = align256(sizeof(double) * nb * k * k);  // G
+  const int64_t lg = g_ld(C, k);
+  size_t s = align256(sizeof(double) * nb * lg * lg);  // G
   s += credit_gram_part_ws(nb, k);                   // partials of G
   const int64_t parts = use_small(C, k) ? (n + kSmallThreads - 1) / kSmallThreads : (n + kLargeTok - 1) / kLargeTok;
   s += align256(sizeof(double) * nb * parts);          // partials
@@ -439,7 +487,8 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
 hipError_t launch_error_targets(const ErrorArgs& a) {
   char* p = a.ws;
   double* G = (double*)p;
-  p += align256(sizeof(double) * a.nb * a.k * a.k);
+  const int64_t lg = g_ld(a.C, a.k);
+  p += align256(sizeof(double) * a.nb * lg * lg);
   double* gpart = (double*)p;
   p += credit_gram_part_ws(a.nb, a.k);
   double* partial = (double*)p;
@@ -448,7 +497,7 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   float* ms = use_small(a.C, a.k) ? nullptr : (float*)p;
 
   k_fill_i32<<<1, 64, 0, a.stream>>>(a.dev_info, 1, INT32_MAX);
-  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G);
+  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G, lg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_product(a)) {
@@ -493,7 +542,7 @@ hipError_t launch_credit_from_top_error(const CreditArgs& a) {
   double* G = (double*)a.ws;
   double* gpart = (double*)(a.ws + align256(sizeof(double) * a.nb * a.k * a.k));
   double* partial = (double*)((char*)gpart + credit_gram_part_ws(a.nb, a.k));
-  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G);
+  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G, a.k);
   dim3 g((unsigned)((a.n + 63) / 64), (unsigned)a.nb);
 #define LOCA_PROJ(KQ)                                                                                          \
   k_credit_project<KQ><<<g, 256, 0, a.stream>>>(a.n, a.d, a.k, a.e, a.ld_e, a.vk, a.v_bstride, G, a.a_w, a.y_out, \

@@ -196,6 +196,11 @@ constexpr uint32_t kBufOutside = 0x80000000u;  // past every range used here (< 
 
 // Workgroup barrier without a memory fence (the pipeline waits for its own loads explicitly).
 LOCA_DEV void barrier_nofence() { asm volatile("s_barrier" ::: "memory"); }
+// this wave's LDS operations complete and visible to its own lanes (no workgroup barrier)
+LOCA_DEV void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), the other counters left alone
+  __builtin_amdgcn_wave_barrier();
+}
 
 // Upper tile u (I <= J, T tiles per side) in an order that keeps consecutive tiles
 // compact: bands of kBand tile rows, each band column by column (rows top to bottom).
