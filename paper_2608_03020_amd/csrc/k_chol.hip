@@ -18,6 +18,9 @@
 // The first non-positive pivot is reported in dev_info (1-based).
 #include "loca_common.h"
 
+#include <functional>
+#include <vector>
+
 namespace loca {
 
 namespace {
@@ -1375,12 +1378,26 @@ size_t solve_ws_t(int64_t nb, int64_t d, int64_t m, int64_t nl, int64_t r_prev) 
   return s;
 }
 
+// The launches of a solve group in submission order.  With `ops` null each launch is
+// issued at once; otherwise it is kept as a closure (every value it needs copied in) for
+// the caller, which interleaves the groups on the host: a group's launches then reach
+// its stream while the other groups are still being submitted, instead of after them.
+struct Emit {
+  std::vector<std::function<hipError_t()>>* ops = nullptr;
+  int stagger_at = -1;  // index of the op that records the stagger event, when kept
+  hipError_t operator()(std::function<hipError_t()> f) {
+    if (!ops) return f();
+    ops->push_back(std::move(f));
+    return hipSuccess;
+  }
+};
+
 // The solve of the blocks [b0, b0 + nbg) (all their lambdas) on stream st; workspace
 // regions are those of the whole call.  `after_diag`, when given, is recorded after the
 // first diagonal-block launch.
 template <typename T, typename ST>
 hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st, T* Fw, T* Rw, T* Dw, T* Mpw,
-                     double* SLpw, const double* dlam, hipEvent_t after_diag) {
+                     double* SLpw, const double* dlam, hipEvent_t after_diag, Emit& emit) {
   const int64_t d = a.d, m = a.r_prev + a.k, nl = a.n_lambda, nm = nbg * nl, mi0 = b0 * nl;
   T* F = Fw + mi0 * d * d;
   T* R = Rw + mi0 * d * m;
@@ -1392,34 +1409,35 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
   int32_t* info = a.dev_info + mi0;
   const ST* S = (const ST*)a.S + b0 * a.s_bstride;
   const ST* K = (const ST*)a.K + b0 * a.k_bstride;
-  if (a.r_prev > 0) {
-    const float* lp = a.lp + b0 * a.lp_bstride;
-    if (a.r_prev <= 16) {
-      dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, 1);
-      k_sym_mul<ST, 16><<<g, 256, 0, st>>>(d, a.r_prev, S, a.s_bstride, lp, a.lp_bstride, SLp);
-    } else {
-      dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, (unsigned)((a.r_prev + 31) / 32));
-      k_sym_mul<ST, 32><<<g, 256, 0, st>>>(d, a.r_prev, S, a.s_bstride, lp, a.lp_bstride, SLp);
+  const int64_t r_prev = a.r_prev, s_bstride = a.s_bstride, k_bstride = a.k_bstride;
+  const float* lp = a.lp ? a.lp + b0 * a.lp_bstride : nullptr;
+  const int64_t lp_bstride = a.lp_bstride;
+  hipError_t e = emit([=]() {
+    if (r_prev > 0) {
+      if (r_prev <= 16) {
+        dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, 1);
+        k_sym_mul<ST, 16><<<g, 256, 0, st>>>(d, r_prev, S, s_bstride, lp, lp_bstride, SLp);
+      } else {
+        dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, (unsigned)((r_prev + 31) / 32));
+        k_sym_mul<ST, 32><<<g, 256, 0, st>>>(d, r_prev, S, s_bstride, lp, lp_bstride, SLp);
+      }
     }
-  }
-  {
     dim3 g((unsigned)((d + 255) / 256), (unsigned)nm);
-    k_equil_diag<T, ST><<<g, 256, 0, st>>>(d, S, a.s_bstride, dlam, (int)nl, D);
+    k_equil_diag<T, ST><<<g, 256, 0, st>>>(d, S, s_bstride, dlam, (int)nl, D);
     dim3 g2((unsigned)((d + kEqRows - 1) / kEqRows), (unsigned)nbg);
     bool v4 = false;
     if constexpr (sizeof(T) == 4 && sizeof(ST) == 4)
-      v4 = d % 4 == 0 && a.s_bstride % 4 == 0 && ((uintptr_t)S & 15) == 0;
+      v4 = d % 4 == 0 && s_bstride % 4 == 0 && ((uintptr_t)S & 15) == 0;
     if (v4) {
       const dim3 g4((unsigned)((d + kEqRows - 1) / kEqRows), (unsigned)((d + kEqCols - 1) / kEqCols), (unsigned)nbg);
-      k_equil_setup_v4<<<g4, kEqCols / 4, 0, st>>>(d, m, a.r_prev, (const float*)S, a.s_bstride, (const float*)K,
-                                                   a.k_bstride, SLp, dlam, (int)nl, (const float*)D, (float*)F,
+      k_equil_setup_v4<<<g4, kEqCols / 4, 0, st>>>(d, m, r_prev, (const float*)S, s_bstride, (const float*)K,
+                                                   k_bstride, SLp, dlam, (int)nl, (const float*)D, (float*)F,
                                                    (float*)R);
+    } else {
+      k_equil_setup<T, ST><<<g2, 256, 0, st>>>(d, m, r_prev, S, s_bstride, K, k_bstride, SLp, dlam, (int)nl, D, F, R);
     }
-    else
-      k_equil_setup<T, ST><<<g2, 256, 0, st>>>(d, m, a.r_prev, S, a.s_bstride, K, a.k_bstride, SLp, dlam, (int)nl, D,
-                                                F, R);
-  }
-  hipError_t e = hipGetLastError();
+    return hipGetLastError();
+  });
   if (e != hipSuccess) return e;
   // Blocked right-looking factorization with the forward substitution of the RHS
   // carried along.  The trailing matrix is updated once per super-panel of kSuper
@@ -1437,66 +1455,80 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       const int64_t nrem = d - pp - pw;
       const int64_t nchF = (nrem + P - 1) / P;
       if (pp > P0) {
-        const int64_t T2 = (d - pp + P - 1) / P;
-        if (x6) {
-          const int nF = (int)((d - pp + 255) / 256);
-          k_panel_x6<kX6Strip><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
-              d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF);
+        e = emit([=]() {
+          const int64_t T2 = (d - pp + P - 1) / P;
+          if (x6) {
+            const int nF = (int)((d - pp + 255) / 256);
+            k_panel_x6<kX6Strip><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
+                d, P0, pp - P0, pp, (float*)F, (float*)R, m, nF);
+            if (!x6r)
+              k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
+                  d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
+          } else {
+            k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, st>>>(
+                d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
+          }
+          return hipGetLastError();
+        });
+        if (e != hipSuccess) return e;
+      }
+      const bool rec = after_diag && pp == 0;
+      if (rec && emit.ops) emit.stagger_at = (int)emit.ops->size();
+      e = emit([=]() {
+        if constexpr (sizeof(T) == 4) k_diag_f32<<<(unsigned)nm, kT, 0, st>>>(d, pp, (float*)F, info);
+        else k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
+        const hipError_t er = hipGetLastError();
+        if (er != hipSuccess || !rec) return er;
+        return hipEventRecord(after_diag, st);
+      });
+      if (e != hipSuccess) return e;
+      e = emit([=]() {
+        if (x6 && nrem > 0) {
+          const int nF = (int)((nrem + 255) / 256);
+          k_panel_x6<kX6Row><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
+              d, pp, pw, 0, (float*)F, (float*)R, m, nF);
           if (!x6r)
-            k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
-                d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
+            k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
+                                                                                                 (int)nchF, F, R);
         } else {
-          k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, st>>>(
-              d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
+          k_panel_product<T, kRowPanel><<<dim3((unsigned)(nchF + TM), (unsigned)nm), kT, 0, st>>>(
+              d, m, pp, 0, 0, 0, 0, 0, F, R);
         }
-      }
-      if constexpr (sizeof(T) == 4) k_diag_f32<<<(unsigned)nm, kT, 0, st>>>(d, pp, (float*)F, info);
-      else k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
-      if (after_diag && pp == 0) {
-        const hipError_t er = hipEventRecord(after_diag, st);
-        if (er != hipSuccess) return er;
-      }
-      if (x6 && nrem > 0) {
-        const int nF = (int)((nrem + 255) / 256);
-        k_panel_x6<kX6Row><<<dim3((unsigned)(nF + (x6r ? 1 : 0)), (unsigned)nm), 512, 0, st>>>(
-            d, pp, pw, 0, (float*)F, (float*)R, m, nF);
-        if (!x6r)
-          k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
-                                                                                               (int)nchF, F, R);
-      } else {
-        k_panel_product<T, kRowPanel><<<dim3((unsigned)(nchF + TM), (unsigned)nm), kT, 0, st>>>(
-            d, m, pp, 0, 0, 0, 0, 0, F, R);
-      }
+        return hipGetLastError();
+      });
+      if (e != hipSuccess) return e;
     }
     if (P1 < d) {
-      const int64_t T2 = (d - P1 + P - 1) / P, nU = T2 * (T2 + 1) / 2;
-      if (x6) {
-        const int64_t T6 = (d - P1 + 255) / 256;
-        const int nF = (int)(T6 * (T6 + 1) / 2);
-        if (syrk_dl) {
-          k_syrk_f32_dl<<<dim3((unsigned)(nF * nm)), 512, 0, st>>>(d, P0, P1 - P0, P1, (float*)F, nF);
-          if (x6r)
-            k_panel_x6<kX6TrailRhs><<<dim3((unsigned)T6, (unsigned)nm, (unsigned)((m + 31) / 32)), 512, 0, st>>>(
-                d, P0, P1 - P0, P1, (float*)F, (float*)R, m, 0);
+      e = emit([=]() {
+        const int64_t T2 = (d - P1 + P - 1) / P, nU = T2 * (T2 + 1) / 2;
+        if (x6) {
+          const int64_t T6 = (d - P1 + 255) / 256;
+          const int nF = (int)(T6 * (T6 + 1) / 2);
+          if (syrk_dl) {
+            k_syrk_f32_dl<<<dim3((unsigned)(nF * nm)), 512, 0, st>>>(d, P0, P1 - P0, P1, (float*)F, nF);
+            if (x6r)
+              k_panel_x6<kX6TrailRhs><<<dim3((unsigned)T6, (unsigned)nm, (unsigned)((m + 31) / 32)), 512, 0, st>>>(
+                  d, P0, P1 - P0, P1, (float*)F, (float*)R, m, 0);
+          } else {
+            k_panel_x6<kX6Trail><<<dim3((unsigned)(nF + (x6r ? T6 : 0)), (unsigned)nm), 512, 0, st>>>(
+                d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF);
+          }
+          if (!x6r)
+            k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
+                d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
         } else {
-          k_panel_x6<kX6Trail><<<dim3((unsigned)(nF + (x6r ? T6 : 0)), (unsigned)nm), 512, 0, st>>>(
-              d, P0, P1 - P0, P1, (float*)F, (float*)R, m, nF);
+          k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, st>>>(
+              d, m, 0, P0, P1 - P0, P1, 0, 0, F, R);
         }
-        if (!x6r)
-          k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
-              d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
-      } else {
-        k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, st>>>(
-            d, m, 0, P0, P1 - P0, P1, 0, 0, F, R);
-      }
+        return hipGetLastError();
+      });
+      if (e != hipSuccess) return e;
     }
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
   }
   if constexpr (sizeof(T) == 4) {
     const int64_t plast = ((d - 1) / P) * P;
     const int nq = (int)((m + 31) / 32);  // m <= 128 (checked by the API)
-    auto back = [&](int64_t pp, int init, unsigned gx) {
+    auto back = [=](int64_t pp, int init, unsigned gx) {
       const dim3 grid(gx, (unsigned)nm);
       const bool v4 = d % 4 == 0 && m <= 128;
 #define LOCA_BACK(NQ)                                                                                \
@@ -1506,37 +1538,42 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       else if (nq <= 2) { LOCA_BACK(2) }
       else { LOCA_BACK(4) }
 #undef LOCA_BACK
+      return hipGetLastError();
     };
-    back(plast, 1, 1);
+    if ((e = emit([=]() { return back(plast, 1, 1); })) != hipSuccess) return e;
     for (int64_t pp = plast; pp >= P; pp -= P) {
       const int64_t nab = pp / P;
-      back(pp, 0, (unsigned)(1 + (nab - 1 + 3) / 4));
+      if ((e = emit([=]() { return back(pp, 0, (unsigned)(1 + (nab - 1 + 3) / 4)); })) != hipSuccess) return e;
     }
   } else {
     for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P) {
-      const dim3 grid((unsigned)(pp > 0 ? (pp + P - 1) / P : 1), (unsigned)nm);
-      const int nq = (int)((m + Mf<T>::BLK - 1) / Mf<T>::BLK);  // m <= 128 (checked by the API)
-      if (nq <= 1) k_back_step<T, 1><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
-      else if (nq <= 2) k_back_step<T, 2><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
-      else if (nq <= 4) k_back_step<T, 4><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
-      else k_back_step<T, 8><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+      e = emit([=]() {
+        const dim3 grid((unsigned)(pp > 0 ? (pp + P - 1) / P : 1), (unsigned)nm);
+        const int nq = (int)((m + Mf<T>::BLK - 1) / Mf<T>::BLK);  // m <= 128 (checked by the API)
+        if (nq <= 1) k_back_step<T, 1><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+        else if (nq <= 2) k_back_step<T, 2><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+        else if (nq <= 4) k_back_step<T, 4><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+        else k_back_step<T, 8><<<grid, kT, 0, st>>>(d, m, pp, F, R, Mp);
+        return hipGetLastError();
+      });
+      if (e != hipSuccess) return e;
     }
   }
-  k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, st>>>(d, m, Mp, D, a.m_out + mi0 * a.m_bstride,
-                                                                                          a.m_bstride);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (a.w_dense_out) {
-    // W = M [Rp; B~]: rows of the right factor come from Rp (first r_prev) then B~.
-    if (a.r_prev == 0)
-      return launch_lowrank_product(st, nm, d, d, m, a.m_out + mi0 * a.m_bstride, a.m_bstride, m,
-                                    a.credit_b + b0 * a.b_bstride, a.b_bstride, nl, d,
-                                    a.w_dense_out + mi0 * a.w_bstride, a.w_bstride);
-    return hipErrorNotSupported;
-  }
-  return hipSuccess;
+  float* m_out = a.m_out + mi0 * a.m_bstride;
+  const int64_t m_bstride = a.m_bstride;
+  const bool dense = a.w_dense_out != nullptr;
+  if (dense && r_prev != 0) return hipErrorNotSupported;
+  const float* cb = dense ? a.credit_b + b0 * a.b_bstride : nullptr;
+  const int64_t b_bstride = a.b_bstride, w_bstride = a.w_bstride;
+  float* w_out = dense ? a.w_dense_out + mi0 * a.w_bstride : nullptr;
+  return emit([=]() {
+    k_unscale<T><<<dim3((unsigned)((d * m + 255) / 256), (unsigned)nm), 256, 0, st>>>(d, m, Mp, D, m_out, m_bstride);
+    const hipError_t er = hipGetLastError();
+    if (er != hipSuccess || !dense) return er;
+    // W = M B~ (no earlier adapter: the right factor is B~ alone)
+    return launch_lowrank_product(st, nm, d, d, m, m_out, m_bstride, m, cb, b_bstride, nl, d, w_out, w_bstride);
+  });
 }
-
 
 // Extra streams and events per device, made on first use.  The blocks of a call are
 // split into up to kGroups groups on the caller's stream and kGroups - 1 internal
@@ -1592,19 +1629,50 @@ hipError_t run_solve(const SolveArgs& a) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int G = (int)(a.nb < kGroups ? a.nb : kGroups);
-  if (G < 2) return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr);
+  if (G < 2) {
+    Emit now;
+    return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr, now);
+  }
   Aux* x = nullptr;
   if ((e = get_aux(&x)) != hipSuccess) return e;
   if ((e = hipEventRecord(x->fork, a.stream)) != hipSuccess) return e;
+  // Every group's launches are recorded first, then submitted round-robin, one launch
+  // per group in turn.  Group g joins once group g - 1 has submitted its first diagonal
+  // block and the event after it; its stream waits for that event, so its GPU work
+  // starts behind that block.
+  std::vector<std::function<hipError_t()>> ops[kGroups];
+  int stagger_at[kGroups];
+  hipStream_t sts[kGroups];
   for (int g = 0; g < G; ++g) {
     const int64_t b0 = a.nb * g / G, b1 = a.nb * (g + 1) / G;
-    hipStream_t st = g == 0 ? a.stream : x->s[g];
-    if (g > 0) {
-      if ((e = hipStreamWaitEvent(st, x->fork, 0)) != hipSuccess) return e;
-      if ((e = hipStreamWaitEvent(st, x->stagger[g], 0)) != hipSuccess) return e;
-    }
+    sts[g] = g == 0 ? a.stream : x->s[g];
     hipEvent_t after = g + 1 < G ? x->stagger[g + 1] : nullptr;
-    if ((e = run_group<T, ST>(a, b0, b1 - b0, st, F, R, D, Mp, SLp, dlam, after)) != hipSuccess) return e;
+    Emit keep;
+    keep.ops = &ops[g];
+    if ((e = run_group<T, ST>(a, b0, b1 - b0, sts[g], F, R, D, Mp, SLp, dlam, after, keep)) != hipSuccess) return e;
+    stagger_at[g] = keep.stagger_at;
+    if (after && keep.stagger_at < 0) return hipErrorUnknown;  // every group has a first diagonal block
+  }
+  size_t pos[kGroups] = {};
+  bool joined[kGroups] = {};
+  joined[0] = true;
+  for (bool left = true; left;) {
+    left = false;
+    for (int g = 0; g < G; ++g) {
+      if (!joined[g]) {
+        if (!joined[g - 1] || pos[g - 1] <= (size_t)stagger_at[g - 1]) {
+          left = true;
+          continue;
+        }
+        if ((e = hipStreamWaitEvent(sts[g], x->fork, 0)) != hipSuccess) return e;
+        if ((e = hipStreamWaitEvent(sts[g], x->stagger[g], 0)) != hipSuccess) return e;
+        joined[g] = true;
+      }
+      if (pos[g] < ops[g].size()) {
+        if ((e = ops[g][pos[g]++]()) != hipSuccess) return e;
+        left = left || pos[g] < ops[g].size();
+      }
+    }
   }
   for (int g = 1; g < G; ++g) {
     if ((e = hipEventRecord(x->join[g], x->s[g])) != hipSuccess) return e;
