@@ -33,8 +33,10 @@ HBM_PEAK_GBS = 8000.0
 # (the bf16 stack of the inputs, 2 * N * d bytes read and written per block): 1.0 for both.
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h).
 TRAFFIC = {
-    "c3": {"fetch_kib": 3104259.7, "write_kib": 752645.7, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "7eab9c68ea8ce340"},
+    "c3": {"fetch_kib": 2772353.8, "write_kib": 785624.8, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "8f863b668525a341"},
+    "c5": {"fetch_kib": 20494605.1, "write_kib": 2642355.9, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "8f863b668525a341"},
 }
 
 
