@@ -751,11 +751,15 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // larger (h*h, h*m, m*h, h*l, l*h, m*m) and drops m*l, l*m, l*l (order 2^-24 and
 // below), so the update has float-class error while running on bf16 MFMA, which
 // retires sixteen times the flops of the fp32 MFMA per cycle.
-LOCA_DEV void split3(float a, uint16_t& h, uint16_t& m, uint16_t& l) {
-  h = f32_to_bf16(a);
-  const float r1 = a - bf16_to_f32(h);
-  m = f32_to_bf16(r1);
-  l = f32_to_bf16(r1 - bf16_to_f32(m));
+// The conversions are the hardware's (v_cvt_pk_bf16_f32, round to nearest even).
+LOCA_DEV void split3_bf16(float a, __bf16& h, __bf16& m, __bf16& l) {
+  h = (__bf16)a;  // round to nearest even
+  const float r1 = a - (float)h;
+  m = (__bf16)r1;
+  l = (__bf16)(r1 - (float)m);
+}
+LOCA_DEV uint32_t pack_bf16x2(__bf16 a, __bf16 b) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
 }
 
 // Panel products on bf16 matrix cores, Out[i][j] (op)= sum_kk Pn[kk][i] Qn[kk][j]:
@@ -857,15 +861,15 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
     }
   };
   auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
-    uint16_t h[4], m[4], l[4];
-    split3(v.x, h[0], m[0], l[0]);
-    split3(v.y, h[1], m[1], l[1]);
-    split3(v.z, h[2], m[2], l[2]);
-    split3(v.w, h[3], m[3], l[3]);
+    __bf16 h[4], m[4], l[4];
+    split3_bf16(v.x, h[0], m[0], l[0]);
+    split3_bf16(v.y, h[1], m[1], l[1]);
+    split3_bf16(v.z, h[2], m[2], l[2]);
+    split3_bf16(v.w, h[3], m[3], l[3]);
     const int o = kk * LD + c4;
-    *(uint2*)(base + o) = make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
-    *(uint2*)(base + PLANE + o) = make_uint2(m[0] | ((uint32_t)m[1] << 16), m[2] | ((uint32_t)m[3] << 16));
-    *(uint2*)(base + 2 * PLANE + o) = make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+    *(uint2*)(base + o) = make_uint2(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]));
+    *(uint2*)(base + PLANE + o) = make_uint2(pack_bf16x2(m[0], m[1]), pack_bf16x2(m[2], m[3]));
+    *(uint2*)(base + 2 * PLANE + o) = make_uint2(pack_bf16x2(l[0], l[1]), pack_bf16x2(l[2], l[3]));
   };
   auto store = [&](int buf, int slot) {
 #pragma unroll
@@ -962,12 +966,6 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
 // nothing).  Tiles, waves and the XCD-aware workgroup order are those of the Gram kernel.
 // Requires d % 4 == 0, kw % 16 == 0 and 4 d^2 < 2^31 bytes per matrix.
 constexpr int kS32BK = 16;  // K rows per stage
-LOCA_DEV void split3_bf16(float a, __bf16& h, __bf16& m, __bf16& l) {
-  h = (__bf16)a;  // round to nearest even
-  const float r1 = a - (float)h;
-  m = (__bf16)r1;
-  l = (__bf16)(r1 - (float)m);
-}
 // the 8 fp32 operand values of lane `lane` (rows 8 (lane / 32) + e of the stage, column
 // c0 + lane % 32 of the panel) from a swizzled stage, split into three MFMA operands
 LOCA_DEV void frag_f32_split(const float* stage, int c0, int lane, bf16x8_t& fh, bf16x8_t& fm, bf16x8_t& fl) {
