@@ -75,7 +75,13 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
   }
 }
 
-constexpr int kTC = kT;  // threads of the eigensolver workgroups
+// Threads of the eigensolver workgroups (one workgroup per matrix): sixteen waves, four per
+// SIMD, so that the waves hide each other's LDS latency in the rounds of the Jacobi
+// iteration, whose updates are chains of dependent LDS reads and writes.
+constexpr int kTC = 1024;
+// the workgroup's reduction scratch (doubles): two block sums, then flags and scalars
+constexpr int kRedSum0 = 0, kRedSum1 = 16, kRedConv = 32, kRedRot = 33, kRedMax = 40, kRedDiag = 41,
+              kRedFail = 42, kRedLen = 48;
 
 // ------------------------------------------------------------------ symmetric eigensolver
 
@@ -105,10 +111,19 @@ LOCA_DEV double rsq64(double x) {
 // round rotates n/2 disjoint pairs (round-robin tournament order: position 0 fixed, the
 // others rotating, so that a sweep of n - 1 rounds meets every pair once) as
 // one two-sided update: every 2 x 2 block of rows {p_k, q_k} and columns {p_l, q_l} is
-// owned by one thread and becomes J_k^T B J_l.  Run by the kTC threads of one workgroup.
+// owned by one thread and becomes J_k^T B J_l.  A pair is rotated while
+// a_pq^2 > 1e-30 |a_pp a_qq| (|a_pq| above 1e-15 of the geometric mean of its diagonal
+// entries); the iteration ends after a sweep that rotates nothing, or once the
+// off-diagonal part is below 1e-30 of the squared Frobenius norm.  While the rotations
+// run, V holds the vectors as rows, so that a rotation combines two contiguous rows with
+// the lanes along them (no LDS bank conflicts); it is transposed at the end.  A pair is
+// read as one int2 and its (c, s) as one double2 (`pairs`, `cs` 16-byte aligned).  Run by
+// the kTC threads of one workgroup; `red` holds kRedLen doubles.
 template <typename VT>
 LOCA_DEV void jacobi_packed(double* A, VT* V, int n, double* cs, int* pairs, double* red) {
   const int tid = threadIdx.x, m = n / 2;
+  const int2* pr = (const int2*)pairs;
+  const double2* cs2 = (const double2*)cs;
   for (int e = tid; e < n * n; e += kTC) V[e] = ((e / n) == (e % n)) ? (VT)1 : (VT)0;
   __syncthreads();
   for (int sweep = 0; sweep < 40; ++sweep) {
@@ -119,65 +134,78 @@ LOCA_DEV void jacobi_packed(double* A, VT* V, int n, double* cs, int* pairs, dou
       tot += v * v;
       if (i != j) off += v * v;
     }
-    const double offs = block_sum(off, red);
+    const double offs = block_sum(off, red + kRedSum0);
     __syncthreads();
-    const double tots = block_sum(tot, red + 4);
-    if (tid == 0) red[8] = (offs <= 1e-30 * tots || tots == 0.0) ? 1.0 : 0.0;
+    const double tots = block_sum(tot, red + kRedSum1);
+    if (tid == 0) {
+      red[kRedConv] = (offs <= 1e-30 * tots || tots == 0.0) ? 1.0 : 0.0;
+      red[kRedRot] = 0.0;  // set by any rotation of this sweep
+    }
     __syncthreads();
-    if (red[8] != 0.0) break;
+    if (red[kRedConv] != 0.0) break;
     for (int round = 0; round < n - 1; ++round) {
       if (tid < m) {
         auto pos = [&](int x) { return x == 0 ? 0 : 1 + ((x - 1 + round) % (n - 1)); };
         int p = pos(tid), q = pos(n - 1 - tid);
         if (p > q) { const int t = p; p = q; q = t; }
-        pairs[2 * tid] = p;
-        pairs[2 * tid + 1] = q;
+        ((int2*)pairs)[tid] = make_int2(p, q);
         const double apq = A[pk(p, q, n)], app = A[pk(p, p, n)], aqq = A[pk(q, q, n)];
         double c = 1.0, s = 0.0;
-        if (fabs(apq) > 1e-300 && apq * apq > 1e-36 * fabs(app * aqq)) {
+        if (fabs(apq) > 1e-300 && apq * apq > 1e-30 * fabs(app * aqq)) {
           const double tau = (aqq - app) * rcp64(2.0 * apq);
           const double u = 1.0 + tau * tau;
           const double t = (tau >= 0.0 ? 1.0 : -1.0) * rcp64(fabs(tau) + u * rsq64(u));
           c = rsq64(1.0 + t * t);
           s = t * c;
+          red[kRedRot] = 1.0;
         }
-        cs[2 * tid] = c;
-        cs[2 * tid + 1] = s;
+        ((double2*)cs)[tid] = make_double2(c, s);
       }
       __syncthreads();
       for (int e = tid; e < m * m; e += kTC) {
         const int k = e / m, l = e % m;
         if (k > l) continue;
-        const int pk_ = pairs[2 * k], qk_ = pairs[2 * k + 1], pl_ = pairs[2 * l], ql_ = pairs[2 * l + 1];
-        const double ck = cs[2 * k], sk = cs[2 * k + 1], cl = cs[2 * l], sl = cs[2 * l + 1];
-        const double b00 = A[pk(pk_, pl_, n)], b01 = A[pk(pk_, ql_, n)];
-        const double b10 = A[pk(qk_, pl_, n)], b11 = A[pk(qk_, ql_, n)];
+        const int2 qk = pr[k], ql = pr[l];
+        const double2 rk = cs2[k], rl = cs2[l];
+        const double ck = rk.x, sk = rk.y, cl = rl.x, sl = rl.y;
+        const double b00 = A[pk(qk.x, ql.x, n)], b01 = A[pk(qk.x, ql.y, n)];
+        const double b10 = A[pk(qk.y, ql.x, n)], b11 = A[pk(qk.y, ql.y, n)];
         const double x00 = cl * b00 - sl * b01, x01 = sl * b00 + cl * b01;  // B J_l
         const double x10 = cl * b10 - sl * b11, x11 = sl * b10 + cl * b11;
         const double y00 = ck * x00 - sk * x10, y01 = ck * x01 - sk * x11;  // J_k^T B J_l
         const double y10 = sk * x00 + ck * x10, y11 = sk * x01 + ck * x11;
         if (k == l) {
-          A[pk(pk_, pk_, n)] = y00;
-          A[pk(qk_, qk_, n)] = y11;
-          A[pk(pk_, qk_, n)] = 0.0;
+          A[pk(qk.x, qk.x, n)] = y00;
+          A[pk(qk.y, qk.y, n)] = y11;
+          A[pk(qk.x, qk.y, n)] = 0.0;
         } else {
-          A[pk(pk_, pl_, n)] = y00;
-          A[pk(pk_, ql_, n)] = y01;
-          A[pk(qk_, pl_, n)] = y10;
-          A[pk(qk_, ql_, n)] = y11;
+          A[pk(qk.x, ql.x, n)] = y00;
+          A[pk(qk.x, ql.y, n)] = y01;
+          A[pk(qk.y, ql.x, n)] = y10;
+          A[pk(qk.y, ql.y, n)] = y11;
         }
       }
-      for (int e = tid; e < n * m; e += kTC) {  // V <- V J
-        const int i = e / m, k = e % m;
-        const int p = pairs[2 * k], q = pairs[2 * k + 1];
-        const double c = cs[2 * k], s = cs[2 * k + 1];
-        const double vip = V[i * n + p], viq = V[i * n + q];
-        V[i * n + p] = (VT)(c * vip - s * viq);
-        V[i * n + q] = (VT)(s * vip + c * viq);
+      for (int e = tid; e < n * m; e += kTC) {  // rows p, q of V^T: V^T <- J^T V^T
+        const int k = e / n, i = e % n;
+        const int2 q2 = pr[k];
+        const double2 r = cs2[k];
+        const double vp = V[q2.x * n + i], vq = V[q2.y * n + i];
+        V[q2.x * n + i] = (VT)(r.x * vp - r.y * vq);
+        V[q2.y * n + i] = (VT)(r.y * vp + r.x * vq);
       }
       __syncthreads();
     }
+    if (red[kRedRot] == 0.0) break;  // a whole sweep found every pair below the threshold
   }
+  for (int e = tid; e < n * n; e += kTC) {  // the vectors from rows to columns
+    const int i = e / n, j = e % n;
+    if (i < j) {
+      const VT x = V[i * n + j], y = V[j * n + i];
+      V[i * n + j] = y;
+      V[j * n + i] = x;
+    }
+  }
+  __syncthreads();
 }
 
 // The truncation core for 64 < kp <= 128 (see the file comment).  Per matrix the workspace
@@ -193,9 +221,9 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   __shared__ float sV[KB2];
   __shared__ double sH[kMaxKpBig], sHi[kMaxKpBig], sEig[kMaxKpBig];
   __shared__ int sOrd[kMaxKpBig];
-  __shared__ double cs[kMaxKpBig];
-  __shared__ int pairs[kMaxKpBig];
-  __shared__ double red[16];
+  __shared__ __attribute__((aligned(16))) double cs[kMaxKpBig];
+  __shared__ __attribute__((aligned(16))) int pairs[kMaxKpBig];
+  __shared__ double red[kRedLen];
   const int64_t mi = blockIdx.x;
   const int tid = threadIdx.x;
   const int K = (int)kp;
@@ -224,12 +252,12 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   if (tid == 0) {
     double lmax = 0.0;
     for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
-    red[12] = lmax;
+    red[kRedMax] = lmax;
   }
   __syncthreads();
   for (int j = tid; j < n; j += kTC) {
     const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
-    const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
+    const bool keep = lb > 1e-14 * red[kRedMax] && lb > 0.0;
     sH[j] = keep ? sqrt(lb) : 0.0;
     sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
   }
@@ -361,9 +389,9 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   __shared__ double sG[KB2];   // Gm; L^{-T} Vp after the eigensolve (Cholesky path)
   __shared__ double sH[kMaxKp], sHi[kMaxKp], sEig[kMaxKp];
   __shared__ int sOrd[kMaxKp];
-  __shared__ double cs[kMaxKp];
-  __shared__ int pairs[kMaxKp];
-  __shared__ double red[16];
+  __shared__ __attribute__((aligned(16))) double cs[kMaxKp];
+  __shared__ __attribute__((aligned(16))) int pairs[kMaxKp];
+  __shared__ double red[kRedLen];
   const int64_t mi = blockIdx.x;
   const int tid = threadIdx.x;
   const int K = (int)kp;
@@ -387,19 +415,19 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   if (tid == 0) {
     double mx = 0.0;
     for (int j = 0; j < K; ++j) mx = fmax(mx, sVb[j * n + j]);
-    red[13] = mx;
-    red[14] = 0.0;
+    red[kRedDiag] = mx;
+    red[kRedFail] = 0.0;
   }
   __syncthreads();
-  const double thr = 1e-10 * red[13];
+  const double thr = 1e-10 * red[kRedDiag];
   for (int j = 0; j < K; ++j) {
     if (tid == 0) {
       const double piv = sVb[j * n + j];
-      if (!(piv > thr)) red[14] = 1.0;
+      if (!(piv > thr)) red[kRedFail] = 1.0;
       sVb[j * n + j] = sqrt(fmax(piv, 0.0));
     }
     __syncthreads();
-    if (red[14] != 0.0) break;
+    if (red[kRedFail] != 0.0) break;
     const double ljj = sVb[j * n + j];
     for (int i = j + 1 + tid; i < K; i += kTC) sVb[i * n + j] /= ljj;
     __syncthreads();
@@ -410,7 +438,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
     }
     __syncthreads();
   }
-  const bool chol = red[14] == 0.0;
+  const bool chol = red[kRedFail] == 0.0;
   if (chol) {
     // 3. T = Gm L (into sV), P^T P = L^T T (upper triangle, packed; zero padding)
     for (int e = tid; e < K * K; e += kTC) {
@@ -445,12 +473,12 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
     if (tid == 0) {
       double lmax = 0.0;
       for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
-      red[12] = lmax;
+      red[kRedMax] = lmax;
     }
     __syncthreads();
     for (int j = tid; j < n; j += kTC) {
       const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
-      const bool keep = lb > 1e-14 * red[12] && lb > 0.0;
+      const bool keep = lb > 1e-14 * red[kRedMax] && lb > 0.0;
       sH[j] = keep ? sqrt(lb) : 0.0;
       sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
     }
