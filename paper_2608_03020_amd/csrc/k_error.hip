@@ -416,6 +416,35 @@ __global__ __launch_bounds__(256) void k_q2_rows(int64_t n, int64_t k, const flo
   if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
 }
 
+// The same for k <= KB with G padded to KB x KB (zero past k): the row of Y in registers
+// (zero past k), G through scalar loads, the symmetric half of the products (fp64).
+template <int KB>
+__global__ __launch_bounds__(256) void k_q2_rows_kb(int64_t n, int64_t k, const float* __restrict__ Y,
+                                                    int64_t y_bstride, const double* __restrict__ G,
+                                                    const float* __restrict__ aw, double* __restrict__ partial) {
+  __shared__ double sred[4];
+  const int64_t b = blockIdx.y;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const double* Gb = G + b * KB * KB;
+  double qv = 0.0;
+  if (t < n) {
+    const float* yt = Y + b * y_bstride + t * k;
+    double yd[KB];
+#pragma unroll
+    for (int j = 0; j < KB; ++j) yd[j] = j < k ? (double)yt[j] : 0.0;
+#pragma unroll
+    for (int a = 0; a < KB; ++a) {
+      double r = 0.5 * Gb[a * KB + a] * yd[a];
+#pragma unroll
+      for (int c2 = a + 1; c2 < KB; ++c2) r += Gb[a * KB + c2] * yd[c2];
+      qv += 2.0 * yd[a] * r;
+    }
+    if (aw) qv *= (double)aw[t];
+  }
+  const double tot = block_sum(qv, sred);
+  if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
+}
+
 __global__ void k_fill_i32(int32_t* p, int64_t cnt, int32_t v) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < cnt) p[i] = v;
@@ -434,11 +463,13 @@ static bool use_product(const ErrorArgs& a) {
   return true;
 }
 
-// row stride of G in the workspace: the small kernel's padded width, else k
-static int64_t g_ld(int64_t C, int64_t k) { return use_small(C, k) ? small_kb(k) : k; }
+// Row stride of G: the padded width of the register kernels (the small label-set kernel,
+// and ||Q||^2 of the product path for k <= 64), else k.  The workspace holds the widest.
+static bool g_padded(const ErrorArgs& a) { return use_small(a.C, a.k) || (use_product(a) && a.k <= kSmallMaxK); }
+static int64_t g_ld_max(int64_t k) { return k <= kSmallMaxK ? small_kb(k) : k; }
 
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k) {
-  const int64_t lg = g_ld(C, k);
+  const int64_t lg = g_ld_max(k);
   size_t s = align256(sizeof(double) * nb * lg * lg);  // G
   s += credit_gram_part_ws(nb, k);                   // partials of G
   const int64_t parts = use_small(C, k) ? (n + kSmallThreads - 1) / kSmallThreads : (n + kLargeTok - 1) / kLargeTok;
@@ -487,8 +518,8 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
 hipError_t launch_error_targets(const ErrorArgs& a) {
   char* p = a.ws;
   double* G = (double*)p;
-  const int64_t lg = g_ld(a.C, a.k);
-  p += align256(sizeof(double) * a.nb * lg * lg);
+  const int64_t lg = g_padded(a) ? small_kb(a.k) : a.k;
+  p += align256(sizeof(double) * a.nb * g_ld_max(a.k) * g_ld_max(a.k));
   double* gpart = (double*)p;
   p += credit_gram_part_ws(a.nb, a.k);
   double* partial = (double*)p;
@@ -509,7 +540,14 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
                           a.y_bstride, a.dev_info, pw};
     if ((e = launch_softmax_product(sp)) != hipSuccess) return e;
     dim3 gq((unsigned)((a.n + 255) / 256), (unsigned)a.nb);
-    k_q2_rows<<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
+    if (!g_padded(a))
+      k_q2_rows<<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
+    else if (lg == 16)
+      k_q2_rows_kb<16><<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
+    else if (lg == 32)
+      k_q2_rows_kb<32><<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
+    else
+      k_q2_rows_kb<64><<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, gq.x, partial, a.mb_out, a.dev_info);
     if (a.e_out) {

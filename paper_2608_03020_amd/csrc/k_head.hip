@@ -47,6 +47,26 @@ LOCA_DEV void ms_combine(float& m, float& s, float m2, float s2) {
   m = mm;
 }
 
+// 8 consecutive logits as floats (a 16-byte aligned bf16 chunk or two float4)
+LOCA_DEV void load8(const uint16_t* p, float (&v)[8]) {
+  const uint4 u = *(const uint4*)p;
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+LOCA_DEV void load8(const float* p, float (&v)[8]) {
+  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+// One workgroup per token.  A 16-byte aligned row is read in chunks of 8 logits, two
+// chunks in flight per thread: each chunk's maximum first rescales the running sum once,
+// then its 8 terms are added.  Other rows (and the tail past a multiple of 8) go one
+// logit at a time.
 template <typename LT>
 __global__ __launch_bounds__(kHT) void k_softmax_stats(int64_t n, int64_t V, const LT* __restrict__ z, int64_t ld,
                                                        const int32_t* __restrict__ labels, float* __restrict__ ms,
@@ -54,12 +74,44 @@ __global__ __launch_bounds__(kHT) void k_softmax_stats(int64_t n, int64_t V, con
   __shared__ float sm[kHT], ss[kHT];
   const int64_t t = blockIdx.x;
   const LT* zt = z + t * ld;
-  float m = 0.f, s = 0.f;
-  for (int64_t c = threadIdx.x; c < V; c += kHT) {
+  float m = -INFINITY, s = 0.f;  // s == 0: nothing seen yet
+  auto add8 = [&](const float (&v)[8]) {
+    float mx = v[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) mx = fmaxf(mx, v[i]);
+    if (mx > m) {
+      s *= __expf(m - mx);
+      m = mx;
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) s += __expf(v[i] - m);
+  };
+  int64_t c0 = 0;
+  if ((((uintptr_t)zt) & 15) == 0) {
+    const int64_t nch = V / 8;
+    int64_t c = threadIdx.x;
+    for (; c + kHT < nch; c += 2 * kHT) {
+      float va[8], vb[8];
+      load8(zt + 8 * c, va);
+      load8(zt + 8 * (c + kHT), vb);
+      add8(va);
+      add8(vb);
+    }
+    for (; c < nch; c += kHT) {
+      float va[8];
+      load8(zt + 8 * c, va);
+      add8(va);
+    }
+    c0 = nch * 8;
+  }
+  for (int64_t c = c0 + threadIdx.x; c < V; c += kHT) {
     const float v = load_as_f32(zt + c);
-    if (s == 0.f) { m = v; s = 1.f; }
-    else if (v > m) { s = s * __expf(m - v) + 1.f; m = v; }
-    else s += __expf(v - m);
+    if (v > m) {
+      s = s * __expf(m - v) + 1.f;
+      m = v;
+    } else {
+      s += __expf(v - m);
+    }
   }
   sm[threadIdx.x] = m;
   ss[threadIdx.x] = s;
@@ -79,22 +131,6 @@ __global__ __launch_bounds__(kHT) void k_softmax_stats(int64_t n, int64_t V, con
     const int32_t yt = labels[t];
     if (yt < 0 || yt >= V) atomicMin(dev_info, (int32_t)(t + 1));
   }
-}
-
-// 8 consecutive logits as floats (a 16-byte aligned bf16 chunk or two float4)
-LOCA_DEV void load8(const uint16_t* p, float (&v)[8]) {
-  const uint4 u = *(const uint4*)p;
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    v[2 * i] = __uint_as_float(w[i] << 16);
-    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
-}
-LOCA_DEV void load8(const float* p, float (&v)[8]) {
-  const float4 a = *(const float4*)p, b = *(const float4*)(p + 4);
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
 }
 
 // Tiles of 128 tokens x 128 columns, one vocabulary chunk per grid.z; 2 x 2 waves of 64 x 64.
