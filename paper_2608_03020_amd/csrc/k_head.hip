@@ -26,9 +26,8 @@ namespace loca {
 namespace {
 
 constexpr int kHT = 256;
-constexpr int kHM = 128, kHN = 128, kHK = 32;  // token rows, hidden columns, vocabulary per stage
+constexpr int kHM = 128, kHK = 32;  // token rows, vocabulary per stage
 constexpr int kLDA = kHK + 8;                  // bf16 per LDS row of P (80 bytes)
-constexpr int kLDB = kHN + 16;                 // bf16 per LDS row of W_u (conflict-free transpose reads)
 
 // dev_info: INT32_MAX while no bad label is seen, then 1 + the smallest bad row, or 0
 __global__ void k_fill_i32_head(int32_t* p) {
@@ -133,43 +132,51 @@ __global__ __launch_bounds__(kHT) void k_softmax_stats(int64_t n, int64_t V, con
   }
 }
 
-// Tiles of 128 tokens x 128 columns, one vocabulary chunk per grid.z; 2 x 2 waves of 64 x 64.
-// Column j of the right operand is column j % kc of group j / kc: W + (j / kc) w_bstride
-// (V x kc bf16 each).  d = total columns.  Requires ld % 8 == 0 (bf16) or % 4 == 0 (f32),
-// kc % 8 == 0, d % kc == 0, kchunk % 32 == 0.
-template <typename LT>
+// Tiles of 128 tokens x HN columns (HN = 128, or 64 when there are at most 64 columns), one
+// vocabulary chunk per grid.z; four waves of 64 columns each: 2 x 2 waves of 64 x 64 (HN =
+// 128) or 4 x 1 of 32 x 64 (HN = 64).  Column j of the right operand is column j % kc of
+// group j / kc: W + (j / kc) w_bstride (V x kc bf16 each).  d = total columns.  Requires
+// ld % 8 == 0 (bf16) or % 4 == 0 (f32), kc % 8 == 0, d % kc == 0, kchunk % 32 == 0.
+template <typename LT, int HN>
 __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, int64_t d, const LT* __restrict__ z,
                                                         int64_t ld, const float* __restrict__ w,
                                                         const float* __restrict__ ms, const uint16_t* __restrict__ wu,
                                                         int64_t kc, int64_t w_bstride, int64_t kchunk,
                                                         float* __restrict__ part) {
+  constexpr int WGN = HN / 64, WGM = 4 / WGN, WM = kHM / WGM, NBM = WM / 32;
+  constexpr int LDB = HN + 16;                  // bf16 per LDS row of W (conflict-free transpose reads)
+  constexpr int NQB = HN * kHK / 8 / kHT;       // 16-byte chunks of the W stage per thread
   __shared__ __attribute__((aligned(16))) uint16_t sAh[2][kHM * kLDA];
   __shared__ __attribute__((aligned(16))) uint16_t sAl[2][kHM * kLDA];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][kHK * kLDB];
-  const int64_t t0 = (int64_t)blockIdx.x * kHM, j0 = (int64_t)blockIdx.y * kHN;
+  __shared__ __attribute__((aligned(16))) uint16_t sB[2][kHK * LDB];
+  const int64_t t0 = (int64_t)blockIdx.x * kHM, j0 = (int64_t)blockIdx.y * HN;
   const int64_t cb = (int64_t)blockIdx.z * kchunk;
   const int64_t ce = std::min<int64_t>(V, cb + kchunk);
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  const int wi = wid >> 1, wj = wid & 1;
+  const int wi = wid / WGN, wj = wid % WGN;
 
   // staging: A chunk q of this thread = row (tid + 256 q) / 4, vocabulary 8 ((tid + 256 q) % 4);
-  // B chunk q = vocabulary row (tid + 256 q) / 16, columns 8 ((tid + 256 q) % 16)
-  int arow[2], acol[2], brow[2], bcol[2];
+  // B chunk q = vocabulary row (tid + 256 q) / (HN / 8), columns 8 ((tid + 256 q) % (HN / 8))
+  int arow[2], acol[2], brow[NQB], bcol[NQB];
   float rmax[2], rscale[2];
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int e = tid + kHT * q;
     arow[q] = e >> 2;
     acol[q] = 8 * (e & 3);
-    brow[q] = e >> 4;
-    bcol[q] = 8 * (e & 15);
     const int64_t t = t0 + arow[q];
     const bool ok = t < n;
     rmax[q] = ok ? ms[2 * t] : 0.f;
     const float st = ok ? ms[2 * t + 1] : 1.f;
     rscale[q] = ok ? (w ? w[t] : 1.f) / st : 0.f;
   }
-  uint4 ph[2], pl[2], wb[2];
+#pragma unroll
+  for (int q = 0; q < NQB; ++q) {
+    const int e = tid + kHT * q;
+    brow[q] = e / (HN / 8);
+    bcol[q] = 8 * (e % (HN / 8));
+  }
+  uint4 ph[2], pl[2], wb[NQB];
   auto load_stage = [&](int64_t c0) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -181,18 +188,22 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
 #pragma unroll
         for (int i = 0; i < 8; ++i) v[i] = (t < n && c + i < ce) ? load_as_f32(z + t * ld + c + i) : -INFINITY;
       }
+      // P = w exp(z - m) / s split into bf16 hi + lo (hardware round-to-nearest-even conversions)
       uint32_t h[4], l[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float p0 = __expf(v[2 * i] - rmax[q]) * rscale[q];
         const float p1 = __expf(v[2 * i + 1] - rmax[q]) * rscale[q];
-        const uint16_t h0 = f32_to_bf16(p0), h1 = f32_to_bf16(p1);
-        const uint16_t l0 = f32_to_bf16(p0 - bf16_to_f32(h0)), l1 = f32_to_bf16(p1 - bf16_to_f32(h1));
-        h[i] = h0 | ((uint32_t)h1 << 16);
-        l[i] = l0 | ((uint32_t)l1 << 16);
+        const __bf16 h0 = (__bf16)p0, h1 = (__bf16)p1;
+        const __bf16 l0 = (__bf16)(p0 - (float)h0), l1 = (__bf16)(p1 - (float)h1);
+        h[i] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+        l[i] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
       }
       ph[q] = make_uint4(h[0], h[1], h[2], h[3]);
       pl[q] = make_uint4(l[0], l[1], l[2], l[3]);
+    }
+#pragma unroll
+    for (int q = 0; q < NQB; ++q) {
       const int64_t cr = c0 + brow[q], j = j0 + bcol[q];
       const int64_t grp = j / kc, jc = j - grp * kc;
       wb[q] = (cr < ce && j < d) ? *(const uint4*)(wu + grp * w_bstride + cr * kc + jc) : make_uint4(0, 0, 0, 0);
@@ -203,13 +214,14 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
     for (int q = 0; q < 2; ++q) {
       *(uint4*)&sAh[buf][arow[q] * kLDA + acol[q]] = ph[q];
       *(uint4*)&sAl[buf][arow[q] * kLDA + acol[q]] = pl[q];
-      *(uint4*)&sB[buf][brow[q] * kLDB + bcol[q]] = wb[q];
     }
+#pragma unroll
+    for (int q = 0; q < NQB; ++q) *(uint4*)&sB[buf][brow[q] * LDB + bcol[q]] = wb[q];
   };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[NBM][2];
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < NBM; ++m)
 #pragma unroll
     for (int q = 0; q < 2; ++q)
 #pragma unroll
@@ -226,22 +238,22 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
     if (kt + 1 < nk) load_stage(cb + (int64_t)(kt + 1) * kHK);
 #pragma unroll
     for (int ks = 0; ks < kHK; ks += 16) {
-      bf16x8_t fh[2], fl[2], fb[2];
+      bf16x8_t fh[NBM], fl[NBM], fb[2];
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        const int row = wi * 64 + 32 * m + (lane & 31);
+      for (int m = 0; m < NBM; ++m) {
+        const int row = wi * WM + 32 * m + (lane & 31);
         const int off = row * kLDA + ks + 8 * (lane >> 5);
         fh[m] = __builtin_bit_cast(bf16x8_t, *(const uint4*)&sAh[cur][off]);
         fl[m] = __builtin_bit_cast(bf16x8_t, *(const uint4*)&sAl[cur][off]);
       }
 #pragma unroll
-      for (int q = 0; q < 2; ++q) fb[q] = frag32_tr(sB[cur], kLDB, wj * 64 + 32 * q, ks, lane);
+      for (int q = 0; q < 2; ++q) fb[q] = frag32_tr(sB[cur], LDB, wj * 64 + 32 * q, ks, lane);
 #pragma unroll
-      for (int m = 0; m < 2; ++m)
+      for (int m = 0; m < NBM; ++m)
 #pragma unroll
         for (int q = 0; q < 2; ++q) acc[m][q] = mfma32(fh[m], fb[q], acc[m][q]);
 #pragma unroll
-      for (int m = 0; m < 2; ++m)
+      for (int m = 0; m < NBM; ++m)
 #pragma unroll
         for (int q = 0; q < 2; ++q) acc[m][q] = mfma32(fl[m], fb[q], acc[m][q]);
     }
@@ -250,12 +262,12 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
   }
   float* out = part + (int64_t)blockIdx.z * n * d;
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < NBM; ++m)
 #pragma unroll
     for (int q = 0; q < 2; ++q)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t t = t0 + wi * 64 + 32 * m + mfma32_row(lane, r);
+        const int64_t t = t0 + wi * WM + 32 * m + mfma32_row(lane, r);
         const int64_t j = j0 + wj * 64 + 32 * q + mfma32_col(lane);
         if (t < n && j < d) out[t * d + j] = acc[m][q][r];
       }
@@ -278,8 +290,11 @@ __global__ void k_top_error_reduce(int64_t n, int64_t d, int nsplit, const float
   out[grp * o_bstride + t * ld_o + jc] = (float)s;
 }
 
+// columns per tile of the product: 64 when there are at most 64, else 128
+int head_hn(int64_t d) { return d <= 64 ? 64 : 128; }
+
 int head_splits(int64_t n, int64_t V, int64_t d) {
-  const int64_t tiles = ((n + kHM - 1) / kHM) * ((d + kHN - 1) / kHN);
+  const int64_t tiles = ((n + kHM - 1) / kHM) * ((d + head_hn(d) - 1) / head_hn(d));
   int64_t s = (2048 + tiles - 1) / tiles;
   s = std::max<int64_t>(1, std::min<int64_t>(s, 32));
   s = std::min<int64_t>(s, std::max<int64_t>(1, (V + 255) / 256));  // at least 256 vocabulary entries a chunk
@@ -299,17 +314,26 @@ hipError_t launch_softmax_product(const SoftmaxProductArgs& a) {
   const int ns = head_splits(a.n, a.V, cols);
   const int64_t kchunk = ((a.V + ns - 1) / ns + kHK - 1) / kHK * kHK;
   hipStream_t st = a.stream;
-  dim3 g((unsigned)((a.n + kHM - 1) / kHM), (unsigned)((cols + kHN - 1) / kHN), (unsigned)ns);
+  const int hn = head_hn(cols);
+  dim3 g((unsigned)((a.n + kHM - 1) / kHM), (unsigned)((cols + hn - 1) / hn), (unsigned)ns);
   if (a.logits_dtype == LOCA_BF16) {
-    k_softmax_stats<uint16_t><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, (const uint16_t*)a.logits, a.ld_logits,
-                                                             a.labels, ms, a.dev_info);
-    k_top_error_gemm<uint16_t><<<g, kHT, 0, st>>>(a.n, a.V, cols, (const uint16_t*)a.logits, a.ld_logits, a.w, ms,
-                                                  a.W, a.kc, a.w_bstride, kchunk, part);
+    const uint16_t* zb = (const uint16_t*)a.logits;
+    k_softmax_stats<uint16_t><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, zb, a.ld_logits, a.labels, ms, a.dev_info);
+    if (hn == 64)
+      k_top_error_gemm<uint16_t, 64><<<g, kHT, 0, st>>>(a.n, a.V, cols, zb, a.ld_logits, a.w, ms, a.W, a.kc,
+                                                        a.w_bstride, kchunk, part);
+    else
+      k_top_error_gemm<uint16_t, 128><<<g, kHT, 0, st>>>(a.n, a.V, cols, zb, a.ld_logits, a.w, ms, a.W, a.kc,
+                                                         a.w_bstride, kchunk, part);
   } else {
-    k_softmax_stats<float><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, (const float*)a.logits, a.ld_logits, a.labels,
-                                                          ms, a.dev_info);
-    k_top_error_gemm<float><<<g, kHT, 0, st>>>(a.n, a.V, cols, (const float*)a.logits, a.ld_logits, a.w, ms, a.W,
-                                               a.kc, a.w_bstride, kchunk, part);
+    const float* zf = (const float*)a.logits;
+    k_softmax_stats<float><<<(unsigned)a.n, kHT, 0, st>>>(a.n, a.V, zf, a.ld_logits, a.labels, ms, a.dev_info);
+    if (hn == 64)
+      k_top_error_gemm<float, 64><<<g, kHT, 0, st>>>(a.n, a.V, cols, zf, a.ld_logits, a.w, ms, a.W, a.kc,
+                                                     a.w_bstride, kchunk, part);
+    else
+      k_top_error_gemm<float, 128><<<g, kHT, 0, st>>>(a.n, a.V, cols, zf, a.ld_logits, a.w, ms, a.W, a.kc,
+                                                      a.w_bstride, kchunk, part);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
