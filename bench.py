@@ -33,10 +33,10 @@ HBM_PEAK_GBS = 8000.0
 # (the bf16 stack of the inputs, 2 * N * d bytes read and written per block): 1.0 for both.
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h).
 TRAFFIC = {
-    "c3": {"fetch_kib": 2772353.8, "write_kib": 785624.8, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "8f863b668525a341"},
-    "c5": {"fetch_kib": 20494605.1, "write_kib": 2642355.9, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "8f863b668525a341"},
+    "c3": {"fetch_kib": 2796235.4, "write_kib": 775783.9, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "383271194106ee5d"},
+    "c5": {"fetch_kib": 20548760.1, "write_kib": 2652752.6, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "383271194106ee5d"},
 }
 
 

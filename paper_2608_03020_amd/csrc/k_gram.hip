@@ -694,29 +694,41 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
 
 // ------------------------------------------------------------------ finalize: eta_bar and K
 
+// One workgroup per (block, 256 entries of K); its first wave forms ||X||^2 from the
+// diagonal tiles' partials (lane l sums partials l, l + 64, ... in order, then a fixed
+// butterfly across the lanes: deterministic) and eta-bar once for the workgroup.
 template <typename AccT>
 __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, const double* __restrict__ diag_part,
                                  loca_mb* __restrict__ mb, double eta, const AccT* __restrict__ Kraw, int split,
                                  AccT* __restrict__ Kall, int64_t k_bstride) {
+  __shared__ double s_eb;
   const int64_t b = blockIdx.y;
-  double sx = 0.0;
-  for (int i = 0; i < ntile; ++i) sx += diag_part[b * ntile + i];
-  const double sq = mb[b].sum_q2;
-  const double eb = (sq > 0.0) ? eta * sqrt(sx / sq) : 0.0;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    mb[b].sum_x2 = sx;
-    mb[b].eta_bar = eb;
-    mb[b].n = n;
+  if (threadIdx.x < 64) {
+    double part = 0.0;
+    for (int i = (int)threadIdx.x; i < ntile; i += 64) part += diag_part[b * ntile + i];
+    const double sx = wave_sum(part);
+    if (threadIdx.x == 0) {
+      const double sq = mb[b].sum_q2;
+      const double eb = (sq > 0.0) ? eta * sqrt(sx / sq) : 0.0;
+      s_eb = eb;
+      if (blockIdx.x == 0) {
+        mb[b].sum_x2 = sx;
+        mb[b].eta_bar = eb;
+        mb[b].n = n;
+      }
+    }
   }
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= d * k) return;
-  const int64_t i = e / k, c = e % k;
+  __syncthreads();
+  const double eb = s_eb;
+  const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;  // d k < 2^31 (d, k <= 65535, 128)
+  if (e >= (uint32_t)(d * k)) return;
+  const uint32_t ku = (uint32_t)k, i = e / ku, c = e - i * ku;
   AccT* K = Kall + b * k_bstride;
-  const int64_t w = split ? 2 * k : k;
-  const AccT* kr = Kraw + b * d * w + i * w;
+  const uint32_t w = split ? 2 * ku : ku;
+  const AccT* kr = Kraw + b * d * w + (int64_t)i * w;
   double v = (double)kr[c];
-  if (split) v += (double)kr[c + k];
-  K[i * k + c] = (AccT)((double)K[i * k + c] - eb * v);
+  if (split) v += (double)kr[c + ku];
+  K[e] = (AccT)((double)K[e] - eb * v);
 }
 
 }  // namespace
@@ -725,22 +737,39 @@ __global__ void k_zero_bytes(uint32_t* p, int cnt) {
   if ((int)threadIdx.x < cnt) p[threadIdx.x] = 0u;
 }
 
-// Yhl[b][t] = [bf16(y) | bf16(y - bf16(y)) | 0] (w2p columns) from the float targets, and
-// the 256 zero bytes at the head of the workspace.
+// Yhl[b][t] = [bf16(y) | bf16(y - bf16(y)) | 0] (w2p columns, w2p % 8 == 0) from the float
+// targets, and the 256 zero bytes at the head of the workspace.  One thread per 8 columns of a
+// row (one 16-byte store); IT is the index type (32-bit while n w2p / 8 fits).
+template <typename IT>
 __global__ void k_split_y(int64_t n, int64_t k, int64_t w2p, const float* __restrict__ Yall, int64_t y_bstride,
                           uint16_t* __restrict__ Yhl, uint32_t* __restrict__ zero_area) {
   const int64_t b = blockIdx.y;
   if (b == 0 && blockIdx.x == 0 && threadIdx.x < 64) zero_area[threadIdx.x] = 0u;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= n * w2p) return;
-  const int64_t t = e / w2p, c = e % w2p;
-  uint16_t v = 0;
-  if (c < 2 * k) {
-    const float y = Yall[b * y_bstride + t * k + (c < k ? c : c - k)];
-    const uint16_t hi = f32_to_bf16(y);
-    v = c < k ? hi : f32_to_bf16(y - bf16_to_f32(hi));
+  const IT g8 = (IT)(w2p / 8);
+  const IT e = (IT)blockIdx.x * (IT)blockDim.x + (IT)threadIdx.x;
+  if (e >= (IT)n * g8) return;
+  const IT t = e / g8;
+  const int c0 = 8 * (int)(e - t * g8);
+  const float* yr = Yall + b * y_bstride + (int64_t)t * k;
+  const int kk = (int)k;
+  uint32_t w[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t h2[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int c = c0 + 2 * i + u;
+      __bf16 v = (__bf16)0.f;
+      if (c < 2 * kk) {
+        const float y = yr[c < kk ? c : c - kk];
+        const __bf16 hi = (__bf16)y;  // round to nearest even
+        v = c < kk ? hi : (__bf16)(y - (float)hi);
+      }
+      h2[u] = (uint32_t)__builtin_bit_cast(uint16_t, v);
+    }
+    w[i] = h2[0] | (h2[1] << 16);
   }
-  Yhl[b * n * w2p + e] = v;
+  *(uint4*)(Yhl + b * n * w2p + (int64_t)t * w2p + c0) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 // wpad[i] = a_w[i] for i < n, 0 up to npad (the padded weights of the bf16 Gram kernels)
@@ -817,8 +846,12 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   const bool ctiles = dl && !fused;
   if (dl) {
     if (fused || ctiles) {
-      dim3 gy((unsigned)((a.n * w2p + 255) / 256), (unsigned)a.nb);
-      k_split_y<<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
+      const int64_t groups = a.n * (w2p / 8);
+      dim3 gy((unsigned)((groups + 255) / 256), (unsigned)a.nb);
+      if (groups < ((int64_t)1 << 31))
+        k_split_y<uint32_t><<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
+      else
+        k_split_y<int64_t><<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
     } else {
       k_zero_bytes<<<1, 64, 0, a.stream>>>((uint32_t*)a.ws, 64);
     }
