@@ -119,19 +119,21 @@ def test_k96_credit_coordinates():
     assert abs(mbv["sum_q2"][0] - np.sum(Q ** 2)) / np.sum(Q ** 2) < 1e-5
 
 
-def test_large_vocab_padded_logit_rows():
+@pytest.mark.parametrize("k,blocks", [(24, 1), (64, 1), (32, 2)])
+def test_large_vocab_padded_logit_rows(k, blocks):
     """A large vocabulary through the matrix-core product with bf16 logits in a padded buffer
     (3001 classes in rows 3008 wide): the softmax statistics' 8-wide chunks and their
-    one-logit tail, Y = E A~ and ||Q||^2 from the padded credit Gram (k = 64)."""
+    one-logit tail, Y = E A~ and ||Q||^2 from the credit Gram padded to 32 (k = 24: padding
+    inside the register rows) or 64; two blocks of k = 32 share one 64-column product tile."""
     import torch
     from paper_2608_03020_amd import loca
     from paper_2608_03020_amd.step import BlockStep
     import oracle
-    cfg = gen.custom_config("t17", blocks=1, d=256, n=300, C=3001, k=64, r_a=32, logit_std=2.0,
+    cfg = gen.custom_config("t17", blocks=blocks, d=256, n=300, C=3001, k=k, r_a=8, logit_std=2.0,
                             logit_dtype="bf16", a_dtype="bf16")
-    xs, zs, ys, As, Bs = host_inputs(cfg, [0])
-    log("case vocab 3001 in rows of 3008")
-    st = BlockStep(cfg, 1)
+    xs, zs, ys, As, Bs = host_inputs(cfg, list(range(blocks)))
+    log(f"case vocab 3001 in rows of 3008, k = {k}, {blocks} block(s)")
+    st = BlockStep(cfg, blocks)
     st.reset()
     z = zs[0]
     n = z.shape[0]
@@ -144,12 +146,13 @@ def test_large_vocab_padded_logit_rows():
     torch.cuda.synchronize()
     assert int(st.info[0].item()) == 0
     E = oracle.head_error(gen.as_f64(z, "bf16"), ys[0])
-    Y, Q = oracle.credit(E, gen.as_f64(As[0], "bf16"), np.asarray(Bs[0], np.float64))
-    ey = rel(st.Y[0, :n].cpu().numpy(), Y)
-    q2 = loca.mb_view(st.mb)["sum_q2"][0]
-    eq = abs(q2 - np.sum(Q ** 2)) / np.sum(Q ** 2)
-    log(f"Y rel err {ey:.2e}, ||Q||^2 rel err {eq:.2e}")
-    assert ey < 1e-4 and eq < 2e-4
+    q2 = loca.mb_view(st.mb)["sum_q2"]
+    for b in range(blocks):
+        Y, Q = oracle.credit(E, gen.as_f64(As[b], "bf16"), np.asarray(Bs[b], np.float64))
+        ey = rel(st.Y[b, :n].cpu().numpy(), Y)
+        eq = abs(q2[b] - np.sum(Q ** 2)) / np.sum(Q ** 2)
+        log(f"block {b}: Y rel err {ey:.2e}, ||Q||^2 rel err {eq:.2e}")
+        assert ey < 1e-4 and eq < 2e-4
 
 
 def test_dense_targets_and_cross_statistic():
