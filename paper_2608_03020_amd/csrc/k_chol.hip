@@ -751,15 +751,22 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // larger (h*h, h*m, m*h, h*l, l*h, m*m) and drops m*l, l*m, l*l (order 2^-24 and
 // below), so the update has float-class error while running on bf16 MFMA, which
 // retires sixteen times the flops of the fp32 MFMA per cycle.
-// The conversions are the hardware's (v_cvt_pk_bf16_f32, round to nearest even).
-LOCA_DEV void split3_bf16(float a, __bf16& h, __bf16& m, __bf16& l) {
-  h = (__bf16)a;  // round to nearest even
-  const float r1 = a - (float)h;
-  m = (__bf16)r1;
-  l = (__bf16)(r1 - (float)m);
+// The conversions are the hardware's (v_cvt_pk_bf16_f32, round to nearest even), two values
+// at a time: a pair of floats becomes a packed bf16 pair (a in the low half), and each
+// packed part is turned back into floats by a shift or a mask, so a value costs one
+// conversion per part and no repacking.
+typedef float f32x2_v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
+LOCA_DEV uint32_t cvt_pk_bf16(float a, float b) {
+  const f32x2_v v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
 }
-LOCA_DEV uint32_t pack_bf16x2(__bf16 a, __bf16 b) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+LOCA_DEV void split3_pair(float a0, float a1, uint32_t& hp, uint32_t& mp, uint32_t& lp) {
+  hp = cvt_pk_bf16(a0, a1);
+  const float r0 = a0 - __uint_as_float(hp << 16), r1 = a1 - __uint_as_float(hp & 0xffff0000u);
+  mp = cvt_pk_bf16(r0, r1);
+  const float s0 = r0 - __uint_as_float(mp << 16), s1 = r1 - __uint_as_float(mp & 0xffff0000u);
+  lp = cvt_pk_bf16(s0, s1);
 }
 
 // Panel products on bf16 matrix cores, Out[i][j] (op)= sum_kk Pn[kk][i] Qn[kk][j]:
@@ -861,15 +868,13 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
     }
   };
   auto put = [&](uint16_t* base, int kk, int c4, const float4& v) {
-    __bf16 h[4], m[4], l[4];
-    split3_bf16(v.x, h[0], m[0], l[0]);
-    split3_bf16(v.y, h[1], m[1], l[1]);
-    split3_bf16(v.z, h[2], m[2], l[2]);
-    split3_bf16(v.w, h[3], m[3], l[3]);
+    uint32_t h[2], m[2], l[2];
+    split3_pair(v.x, v.y, h[0], m[0], l[0]);
+    split3_pair(v.z, v.w, h[1], m[1], l[1]);
     const int o = kk * LD + c4;
-    *(uint2*)(base + o) = make_uint2(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]));
-    *(uint2*)(base + PLANE + o) = make_uint2(pack_bf16x2(m[0], m[1]), pack_bf16x2(m[2], m[3]));
-    *(uint2*)(base + 2 * PLANE + o) = make_uint2(pack_bf16x2(l[0], l[1]), pack_bf16x2(l[2], l[3]));
+    *(uint2*)(base + o) = make_uint2(h[0], h[1]);
+    *(uint2*)(base + PLANE + o) = make_uint2(m[0], m[1]);
+    *(uint2*)(base + 2 * PLANE + o) = make_uint2(l[0], l[1]);
   };
   auto store = [&](int buf, int slot) {
 #pragma unroll
@@ -974,14 +979,12 @@ LOCA_DEV void frag_f32_split(const float* stage, int c0, int lane, bf16x8_t& fh,
   float v[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] = p[e * 256];
+  uint32_t h[4], m[4], l[4];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    __bf16 h, m, l;
-    split3_bf16(v[e], h, m, l);
-    fh[e] = h;
-    fm[e] = m;
-    fl[e] = l;
-  }
+  for (int e = 0; e < 4; ++e) split3_pair(v[2 * e], v[2 * e + 1], h[e], m[e], l[e]);
+  fh = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  fm = __builtin_bit_cast(bf16x8_t, make_uint4(m[0], m[1], m[2], m[3]));
+  fl = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
 }
 __global__ __launch_bounds__(512) void k_syrk_f32_dl(int64_t d, int64_t k0, int64_t kw, int64_t off,
                                                      float* __restrict__ Fall, int ntile) {
