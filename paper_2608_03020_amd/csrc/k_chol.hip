@@ -17,6 +17,7 @@
 //      then M = D M'.
 // The first non-positive pivot is reported in dev_info (1-based).
 #include "loca_common.h"
+#include "loca_bf16.h"
 
 #include <functional>
 #include <vector>
@@ -751,23 +752,7 @@ __global__ __launch_bounds__(kT) __attribute__((amdgpu_waves_per_eu(2))) void k_
 // larger (h*h, h*m, m*h, h*l, l*h, m*m) and drops m*l, l*m, l*l (order 2^-24 and
 // below), so the update has float-class error while running on bf16 MFMA, which
 // retires sixteen times the flops of the fp32 MFMA per cycle.
-// The conversions are the hardware's (v_cvt_pk_bf16_f32, round to nearest even), two values
-// at a time: a pair of floats becomes a packed bf16 pair (a in the low half), and each
-// packed part is turned back into floats by a shift or a mask, so a value costs one
-// conversion per part and no repacking.
-typedef float f32x2_v __attribute__((ext_vector_type(2)));
-typedef __bf16 bf16x2_v __attribute__((ext_vector_type(2)));
-LOCA_DEV uint32_t cvt_pk_bf16(float a, float b) {
-  const f32x2_v v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_v));
-}
-LOCA_DEV void split3_pair(float a0, float a1, uint32_t& hp, uint32_t& mp, uint32_t& lp) {
-  hp = cvt_pk_bf16(a0, a1);
-  const float r0 = a0 - __uint_as_float(hp << 16), r1 = a1 - __uint_as_float(hp & 0xffff0000u);
-  mp = cvt_pk_bf16(r0, r1);
-  const float s0 = r0 - __uint_as_float(mp << 16), s1 = r1 - __uint_as_float(mp & 0xffff0000u);
-  lp = cvt_pk_bf16(s0, s1);
-}
+// The split is split3_pair (loca_bf16.h): hardware conversions, two values at a time.
 
 // Panel products on bf16 matrix cores, Out[i][j] (op)= sum_kk Pn[kk][i] Qn[kk][j]:
 //   kX6Trail: F[i][j] -= sum_{kk in [k0, k0 + kw)} F[kk][i] F[kk][j] on the upper

@@ -20,6 +20,7 @@
 #include <algorithm>
 
 #include "loca_common.h"
+#include "loca_bf16.h"
 
 namespace loca {
 
@@ -159,6 +160,7 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
   // B chunk q = vocabulary row (tid + 256 q) / (HN / 8), columns 8 ((tid + 256 q) % (HN / 8))
   int arow[2], acol[2], brow[NQB], bcol[NQB];
   float rmax[2], rscale[2];
+  const LT* zrow[2];  // this thread's logits rows (row 0 for rows past n: never read)
 #pragma unroll
   for (int q = 0; q < 2; ++q) {
     const int e = tid + kHT * q;
@@ -166,6 +168,7 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
     acol[q] = 8 * (e & 3);
     const int64_t t = t0 + arow[q];
     const bool ok = t < n;
+    zrow[q] = z + (ok ? t : 0) * ld;
     rmax[q] = ok ? ms[2 * t] : 0.f;
     const float st = ok ? ms[2 * t + 1] : 1.f;
     rscale[q] = ok ? (w ? w[t] : 1.f) / st : 0.f;
@@ -183,21 +186,19 @@ __global__ __launch_bounds__(kHT) void k_top_error_gemm(int64_t n, int64_t V, in
       const int64_t t = t0 + arow[q], c = c0 + acol[q];
       float v[8];
       if (t < n && c + 8 <= ce) {
-        load8(z + t * ld + c, v);
+        load8(zrow[q] + c, v);
       } else {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) v[i] = (t < n && c + i < ce) ? load_as_f32(z + t * ld + c + i) : -INFINITY;
+        for (int i = 0; i < 8; ++i) v[i] = (t < n && c + i < ce) ? load_as_f32(zrow[q] + c + i) : -INFINITY;
       }
-      // P = w exp(z - m) / s split into bf16 hi + lo (hardware round-to-nearest-even conversions)
+      // P = w exp(z - m) / s split into bf16 hi + lo (packed hardware conversions, loca_bf16.h)
       uint32_t h[4], l[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float p0 = __expf(v[2 * i] - rmax[q]) * rscale[q];
         const float p1 = __expf(v[2 * i + 1] - rmax[q]) * rscale[q];
-        const __bf16 h0 = (__bf16)p0, h1 = (__bf16)p1;
-        const __bf16 l0 = (__bf16)(p0 - (float)h0), l1 = (__bf16)(p1 - (float)h1);
-        h[i] = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
-        l[i] = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+        h[i] = cvt_pk_bf16(p0, p1);
+        l[i] = cvt_pk_bf16(p0 - bf16_lo(h[i]), p1 - bf16_hi(h[i]));
       }
       ph[q] = make_uint4(h[0], h[1], h[2], h[3]);
       pl[q] = make_uint4(l[0], l[1], l[2], l[3]);
