@@ -426,63 +426,44 @@ LOCA_DEV void zero16(f32x16_t& acc) {
 
 // One wave factors the 32 x 32 block B (upper part used) as U^T U, writes U over B (zero
 // below the diagonal) and X = U^{-1} to Xo.  Lane c < 32 holds column c (rows 0..31);
-// lanes 32..63 mirror lanes 0..31 and write nothing.  Rows of the current matrix are
-// published through two LDS rows rb[0..63] (row j in rb + 32 (j & 1)): step j first
-// applies its update to row j + 1 and publishes it, then finishes the other rows while
-// the row travels.  The inverse is built bottom-up from rows of U read back from B.
-// Square root and reciprocal are the hardware ones (about 1 ulp).  The first
-// non-positive pivot among the first `valid` is reported (1-based, offset base).
-LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, float* rb, int lane, int valid, int64_t base,
-                         int32_t* info) {
+// lanes 32..63 mirror lanes 0..31 and write nothing.  Step j of the factorization takes
+// the pivot from lane j and the scaled row j, U[j][i], from lanes i by cross-lane reads
+// (v_readlane into scalar registers), so no step waits on LDS; the inverse is built
+// bottom-up the same way, U[i][k] being lane k's entry of row i.  Square root and
+// reciprocal are the hardware ones (about 1 ulp).  The first non-positive pivot among the
+// first `valid` is reported (1-based, offset base).
+LOCA_DEV float lane_val(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, int lane, int valid, int64_t base, int32_t* info) {
   const int c = lane & 31;
   const bool wr = lane < 32;
   float a[32];
 #pragma unroll
   for (int r = 0; r < 32; ++r) a[r] = B[r * ld + c];
-  if (wr) rb[c] = a[0];
-  wave_lds_sync();
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
-    const float* row = rb + 32 * (j & 1);
-    float rr[32];
-#pragma unroll
-    for (int v = j >> 2; v < 8; ++v) {
-      const float4 t = *(const float4*)(row + 4 * v);
-      rr[4 * v] = t.x; rr[4 * v + 1] = t.y; rr[4 * v + 2] = t.z; rr[4 * v + 3] = t.w;
-    }
-    const float piv = rr[j];
+    const float piv = lane_val(a[j], j);
     if (!(piv > 0.f) && j < valid && lane == 0) atomicCAS(info, 0, (int32_t)(base + j + 1));
     const float ujj = __builtin_amdgcn_sqrtf(piv);
     const float inv = __builtin_amdgcn_rcpf(ujj);
     const float uc = c > j ? a[j] * inv : (c == j ? ujj : 0.f);  // U[j][c]
     a[j] = uc;
-    if (j + 1 < 32) {
-      a[j + 1] -= (rr[j + 1] * inv) * uc;
-      if (wr) rb[32 * ((j + 1) & 1) + c] = a[j + 1];  // row j + 1, final for this step
 #pragma unroll
-      for (int i = j + 2; i < 32; ++i) a[i] -= (rr[i] * inv) * uc;
-      wave_lds_sync();
-    }
+    for (int i = j + 1; i < 32; ++i) a[i] -= lane_val(uc, i) * uc;  // A[i][c] -= U[j][i] U[j][c]
   }
   if (wr) {
 #pragma unroll
     for (int r = 0; r < 32; ++r) B[r * ld + c] = r <= c ? a[r] : 0.f;
   }
-  wave_lds_sync();
   float x[32];
 #pragma unroll
   for (int i = 31; i >= 0; --i) {
-    float ur[32];
-#pragma unroll
-    for (int v = i >> 2; v < 8; ++v) {
-      const float4 t = *(const float4*)(B + i * ld + 4 * v);
-      ur[4 * v] = t.x; ur[4 * v + 1] = t.y; ur[4 * v + 2] = t.z; ur[4 * v + 3] = t.w;
-    }
     float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = i + 1; k < 32; ++k) part[k & 3] += ur[k] * x[k];
+    for (int k = i + 1; k < 32; ++k) part[k & 3] += lane_val(a[i], k) * x[k];  // U[i][k] x[k]
     const float tot = (part[0] + part[1]) + (part[2] + part[3]);
-    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - tot) * __builtin_amdgcn_rcpf(ur[i]) : 0.f;
+    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - tot) * __builtin_amdgcn_rcpf(lane_val(a[i], i)) : 0.f;
   }
   if (wr) {
 #pragma unroll
@@ -503,7 +484,6 @@ __global__ __launch_bounds__(kT) void k_diag_f32(int64_t d, int64_t p, float* __
   __shared__ __attribute__((aligned(16))) float sA[P * LD];
   __shared__ __attribute__((aligned(16))) float sX[P * LD];
   __shared__ __attribute__((aligned(16))) float sT[3][32 * 36];
-  __shared__ __attribute__((aligned(16))) float su[64];  // row buffers of the factoring wave
   const int64_t mi = blockIdx.x;
   float* F = Fall + mi * d * d;
   const float* A0 = F + p * d + p;
@@ -549,7 +529,7 @@ __global__ __launch_bounds__(kT) void k_diag_f32(int64_t d, int64_t p, float* __
   __syncthreads();
   for (int q = 0; q < 4; ++q) {
     const int c0 = 32 * q;
-    if (wid == 0) chol_inv32(sA + c0 * LD + c0, LD, sX + c0 * LD + c0, LD, su, lane, pw - c0, p + c0, dev_info + mi);
+    if (wid == 0) chol_inv32(sA + c0 * LD + c0, LD, sX + c0 * LD + c0, LD, lane, pw - c0, p + c0, dev_info + mi);
     __syncthreads();
     const int nr = 3 - q;
     if (wid < nr) {  // row panel block r: U_qr = X_qq^T A_qr
