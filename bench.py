@@ -375,8 +375,8 @@ def cpu_baseline(cfg, n_sample):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the multi-GPU sharding is a design only).", file=sys.stderr)
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
+              "(sharding the blocks across GPUs is described, not implemented).", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch

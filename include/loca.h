@@ -57,7 +57,7 @@ typedef enum {
   LOCA_E_ARG = 1,          /* invalid argument (null pointer, bad size, stride, lambda <= 0, ...) */
   LOCA_E_WORKSPACE = 2,    /* ws is NULL, misaligned or smaller than loca_workspace_size() */
   LOCA_E_HIP = 3,          /* a HIP launch failed */
-  LOCA_E_UNSUPPORTED = 4   /* valid but outside what this build implements (e.g. k > 128) */
+  LOCA_E_UNSUPPORTED = 4   /* valid but outside what the library implements (e.g. k > 128) */
 } loca_status;
 
 typedef enum { LOCA_F32 = 0, LOCA_BF16 = 1, LOCA_F64 = 2 } loca_dtype;
