@@ -100,16 +100,19 @@ static void launch_credit_gram(hipStream_t st, int64_t nb, int64_t k, int64_t d,
 }
 static size_t credit_gram_part_ws(int64_t nb, int64_t k) { return align256(sizeof(double) * kCGSplit * nb * k * k); }
 
-// One thread per token.  A~ (C x k, [c][j]) sits in LDS; G (KB x KB, zero past k, the same
-// for every lane) is read through scalar loads straight into the fp64 products.  The
-// token's Y row stays in registers and reaches HBM through a per-wave LDS transpose, so
-// that a wave writes whole rows of consecutive tokens instead of one column of 64 rows
-// per store.  The transpose buffers reuse the A~ area once it is consumed.
+// One thread per token; A~ (C x k, [c][j]) sits in LDS.  Each wave then stages its 64 rows of
+// Y (KB columns, zero past k and past n) in an LDS tile, from which it
+//   * writes Y to HBM as whole rows of consecutive tokens, and
+//   * forms its share of ||Q||^2 = sum_t a_t y_t G y_t^T = <G, sum_t a_t y_t y_t^T> with the
+//     fp64 matrix cores: M_w = sum over its tokens of (a_t y_t) y_t^T in 16 x 16 blocks on or
+//     above the diagonal (v_mfma_f64_16x16x4f64, products of floats exact in fp64), then
+//     each lane multiplies its entries of M_w by those of G (KB x KB, zero past k; blocks off
+//     the diagonal count twice).
+// The tile reuses the A~ area once it is consumed.
 static int64_t small_kb(int64_t k) { return k <= 16 ? 16 : k <= 32 ? 32 : 64; }
 template <int KB>
 struct SmallLds {
-  static constexpr int CW = KB < 32 ? KB : 32;         // Y columns per transpose pass
-  static constexpr int WST = 64 * (CW + 1);            // floats per wave (odd row stride)
+  static constexpr int WST = 64 * (KB + 1);            // floats of a wave's tile (odd row stride)
   static constexpr int IN = kSmallMaxC * KB * 4;
   static constexpr int ST = 4 * WST * 4;
   static constexpr int BYTES = IN > ST ? IN : ST;
@@ -123,7 +126,9 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
     int64_t y_bstride, float* __restrict__ e_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
   using L = SmallLds<KB>;
   static_assert(kSmallThreads == 256, "four waves");
+  constexpr int NB = KB / 16;  // 16-column blocks
   __shared__ __attribute__((aligned(16))) unsigned char lds[L::BYTES];
+  __shared__ float sW[kSmallThreads];  // statistic weight of each token (0 past n)
   __shared__ double sred[kSmallThreads / 64];
   float* sA = (float*)lds;  // C x k, row stride k
   const int64_t b = blockIdx.y;
@@ -133,10 +138,10 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
   __syncthreads();
 
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  double q = 0.0;
   float y[KB];
 #pragma unroll
   for (int j = 0; j < KB; ++j) y[j] = 0.f;
+  float wq = 0.f;  // weight of this token in ||Q||^2
   if (t < n) {
     const LT* zt = logits + t * ld;
     const int32_t yt = labels[t];
@@ -156,48 +161,51 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
         for (int j = 0; j < KB; ++j)
           if (j < k) y[j] = fmaf(e, sA[c * k + j], y[j]);
       }
-      // q = y G y^T (fp64; G symmetric, so off-diagonal terms are doubled; entries past k
-      // are zero in both y and G).  Only the fp64 copy of y stays live past this point: the
-      // float values are recovered from it exactly.
-      double yd[KB];
-#pragma unroll
-      for (int j = 0; j < KB; ++j) yd[j] = (double)y[j];
-#pragma unroll
-      for (int a = 0; a < KB; ++a) {
-        double r = 0.5 * Gb[a * KB + a] * yd[a];
-#pragma unroll
-        for (int c2 = a + 1; c2 < KB; ++c2) r += Gb[a * KB + c2] * yd[c2];
-        q += 2.0 * yd[a] * r;
-      }
-#pragma unroll
-      for (int j = 0; j < KB; ++j) y[j] = (float)yd[j];
-      if (aw) q *= (double)aw[t];  // statistic weight of the position
+      wq = aw ? aw[t] : 1.0f;  // statistic weight of the position
     }
   }
-  __syncthreads();  // every read of sA retired: the area becomes the transpose buffers
+  __syncthreads();  // every read of sA retired: the area becomes the waves' tiles
 
-  // Y through the wave's transpose buffer, CW columns per pass: lane l puts its row at
-  // l (CW + 1), then each store instruction covers 64 / CW consecutive tokens x CW columns.
-  constexpr int CW = L::CW;
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  float* sT = (float*)lds + wv * L::WST;
+  float* sT = (float*)lds + wv * L::WST;  // [token of the wave][KB + 1]
+#pragma unroll
+  for (int j = 0; j < KB; ++j) sT[lane * (KB + 1) + j] = y[j];
+  sW[threadIdx.x] = wq;
+  wave_lds_sync();
+
+  // Y rows to HBM: each store instruction covers 64 / KB consecutive tokens x KB columns
   const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + 64 * wv;
   float* yb = y_out + b * y_bstride;
 #pragma unroll
-  for (int h = 0; h < KB / CW; ++h) {
-    if (h * CW < k) {
-#pragma unroll
-      for (int j = 0; j < CW; ++j) sT[lane * (CW + 1) + j] = y[h * CW + j];
-      wave_lds_sync();
-#pragma unroll
-      for (int i = 0; i < CW; ++i) {
-        const int e = lane + 64 * i, p = e / CW, c = e % CW;
-        const int64_t tp = t0 + p, col = (int64_t)h * CW + c;
-        if (tp < n && col < k) yb[tp * k + col] = sT[p * (CW + 1) + c];
-      }
-      wave_lds_sync();
-    }
+  for (int i = 0; i < KB; ++i) {
+    const int e = lane + 64 * i, p = e / KB, c = e % KB;
+    const int64_t tp = t0 + p;
+    if (tp < n && c < k) yb[tp * k + c] = sT[p * (KB + 1) + c];
   }
+
+  // this wave's part of ||Q||^2
+  const float* sWw = sW + 64 * wv;
+  const int kr = lane >> 4, cr = lane & 15;
+  double q = 0.0;
+#pragma unroll
+  for (int ab = 0; ab < NB; ++ab)
+#pragma unroll
+    for (int cb = ab; cb < NB; ++cb) {
+      f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+      for (int tt = 0; tt < 64; tt += 4) {
+        const int p = tt + kr;
+        const double av = (double)sWw[p] * (double)sT[p * (KB + 1) + 16 * ab + cr];  // A[i][kk] = a_t y_t[i]
+        const double bv = (double)sT[p * (KB + 1) + 16 * cb + cr];                  // B[kk][j] = y_t[j]
+        acc = mfma_f64(av, bv, acc);
+      }
+      const double mult = ab == cb ? 1.0 : 2.0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 16 * ab + kr + 4 * r, col = 16 * cb + cr;
+        q += mult * acc[r] * Gb[row * KB + col];
+      }
+    }
   const double tot = block_sum(q, sred);
   if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
 }
