@@ -27,8 +27,8 @@ constexpr int kMaxK = 128;
 // G_b = B~_b B~_b^T (k x k, float64) in two passes.  k_credit_gram_part: one workgroup per
 // (32 x 32 tile on or above the diagonal, one of kCGSplit ranges of the width d, block);
 // the tile's 32 + 32 rows of B~ stream through LDS in 64-column chunks (the next chunk
-// loaded while the current one is used) and each thread sums four entries in fp64 in the
-// order of the columns.  k_credit_gram_sum adds the kCGSplit partials of an entry in a fixed
+// loaded while the current one is used) and each wave forms a 16 x 16 block of the tile on
+// the fp64 matrix cores, in the order of the columns.  k_credit_gram_sum adds the kCGSplit partials of an entry in a fixed
 // order and writes it and its mirror: deterministic.
 constexpr int kCGSplit = 8, kCGC = 64;
 __global__ __launch_bounds__(256) void k_credit_gram_part(int64_t k, int64_t d, const float* __restrict__ B,
@@ -43,9 +43,12 @@ __global__ __launch_bounds__(256) void k_credit_gram_part(int64_t k, int64_t d, 
   const int64_t a0 = 32 * (int64_t)I, c0 = 32 * (int64_t)J;
   const int64_t chunk = ((d + kCGSplit - 1) / kCGSplit + kCGC - 1) / kCGC * kCGC;
   const int64_t i0 = s * chunk, i1 = i0 + chunk < d ? i0 + chunk : d;
-  const int t = threadIdx.x, ra = t >> 3, c4 = 4 * (t & 7);
+  const int t = threadIdx.x;
   const int lrow = t >> 3, lcol = 8 * (t & 7);  // this thread's staging: row lrow, columns lcol .. lcol + 7
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  // wave (wa, wc) forms the 16 x 16 block (a0 + 16 wa, c0 + 16 wc) of the tile on the fp64
+  // matrix cores (v_mfma_f64_16x16x4f64; products of floats are exact in fp64)
+  const int lane = t & 63, wa = (t >> 6) >> 1, wc = (t >> 6) & 1, kr = lane >> 4, cr = lane & 15;
+  f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
   float va[8], vc[8];
   auto load = [&](int64_t j0) {
 #pragma unroll
@@ -66,17 +69,16 @@ __global__ __launch_bounds__(256) void k_credit_gram_part(int64_t k, int64_t d, 
     }
     __syncthreads();
     if (j0 + kCGC < i1) load(j0 + kCGC);
-#pragma unroll 8
-    for (int kk = 0; kk < kCGC; ++kk) {
-      const double x = (double)sa[ra][kk];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[q] += x * (double)sc[c4 + q][kk];
-    }
+    for (int kk = 0; kk < kCGC; kk += 4)  // A[i][x] = B~[a][x], B[x][j] = B~[c][x]
+      acc = mfma_f64((double)sa[16 * wa + cr][kk + kr], (double)sc[16 * wc + cr][kk + kr], acc);
   }
   double* P = part + ((s * (int64_t)gridDim.z + b) * k) * k;
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
-    if (a0 + ra < k && c0 + c4 + q < k) P[(a0 + ra) * k + c0 + c4 + q] = acc[q];
+  for (int r = 0; r < 4; ++r) {
+    const int64_t row = a0 + 16 * wa + kr + 4 * r, col = c0 + 16 * wc + cr;
+    if (row < k && col < k) P[row * k + col] = acc[r];
+  }
 }
 // G is written with row stride ldg >= k, zero in the rows and columns past k.
 __global__ void k_credit_gram_sum(int64_t k, int64_t ldg, int64_t nb, const double* __restrict__ part,
