@@ -25,53 +25,90 @@ constexpr int kMaxKpBig = 128;
 
 // Partial Gm = M^T M and Gb = R R^T (fp64) over the row range of blockIdx.z (of nsplit
 // equal ranges of 32-row multiples); blockIdx.x = matrix, blockIdx.y = 0 (M) / 1 (R).
-// The partials are summed in a fixed order by k_trunc_core.
+// The partials are summed in a fixed order by k_trunc_core.  Each 32-row chunk is staged
+// in LDS as doubles (the next one is loaded into registers meanwhile) and its products
+// are formed on the fp64 matrix cores (v_mfma_f64_16x16x4f64; products of floats are
+// exact in fp64): the kp x kp result is cut into 16 x 16 blocks, wave w taking the
+// blocks w, w + 4, ...
 template <int KPM>
 __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const float* __restrict__ M,
                                                     int64_t m_bstride, const float* __restrict__ R,
                                                     int64_t r_bstride, int64_t r_group, int nsplit,
                                                     double* __restrict__ Gpart) {
   constexpr int kRows = 32;
-  constexpr int kMaxKp = KPM;
-  __shared__ double sX[kRows][kMaxKp + 1];
+  constexpr int kLd = KPM + 1;
+  constexpr int kPer = kRows * KPM / kT;                // staged values per thread and chunk, at most
+  constexpr int kBlk = (KPM / 16) * (KPM / 16) / 4;     // output blocks per wave, at most
+  __shared__ double sX[kRows * kLd];
   const int64_t mi = blockIdx.x;
   const bool isR = blockIdx.y == 1;
   const int64_t chunk = ((d + nsplit - 1) / nsplit + kRows - 1) / kRows * kRows;
   const int64_t ib = (int64_t)blockIdx.z * chunk, ie = ib + chunk < d ? ib + chunk : d;
   const float* Mm = M + mi * m_bstride;
   const float* Rm = R + (mi / r_group) * r_bstride;
-  const int npair = (int)(kp * kp);
-  double acc[(kMaxKp * kMaxKp) / kT];
+  const int K = (int)kp, nb = (K + 15) / 16, nv = kRows * K;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, kr = lane >> 4, cr = lane & 15;
+  // staged element f of a chunk: row r, column c (R's rows are contiguous along i)
+  auto where = [&](int f, int& r, int& c) {
+    if (isR) { c = f / kRows; r = f % kRows; }
+    else { r = f / K; c = f % K; }
+  };
+  for (int e = tid; e < kRows * kLd; e += kT) sX[e] = 0.0;  // columns past kp stay zero
+  float v[kPer];
+  auto load = [&](int64_t i0) {
 #pragma unroll
-  for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) acc[q] = 0.0;
+    for (int j = 0; j < kPer; ++j) {
+      const int f = tid + kT * j;
+      float x = 0.f;
+      if (f < nv) {
+        int r, c;
+        where(f, r, c);
+        const int64_t i = i0 + r;
+        if (i < ie) x = isR ? Rm[c * d + i] : Mm[i * kp + c];
+      }
+      v[j] = x;
+    }
+  };
+  f64x4_t acc[kBlk];
+#pragma unroll
+  for (int q = 0; q < kBlk; ++q) acc[q] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+  if (ib < ie) load(ib);
   for (int64_t i0 = ib; i0 < ie; i0 += kRows) {
-    __syncthreads();
-    for (int e = threadIdx.x; e < kRows * kMaxKp; e += kT) {
-      int r, c;
-      if (isR) { c = e / kRows; r = e % kRows; }  // R rows are contiguous along i
-      else { r = e / kMaxKp; c = e % kMaxKp; }
-      const int64_t i = i0 + r;
-      double v = 0.0;
-      if (i < ie && c < kp) v = isR ? (double)Rm[c * d + i] : (double)Mm[i * kp + c];
-      sX[r][c] = v;
+    __syncthreads();  // the previous chunk is no longer read (and the zero fill is done)
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int f = tid + kT * j;
+      if (f < nv) {
+        int r, c;
+        where(f, r, c);
+        sX[r * kLd + c] = (double)v[j];
+      }
     }
     __syncthreads();
+    if (i0 + kRows < ie) load(i0 + kRows);
 #pragma unroll
-    for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) {
-      const int e = threadIdx.x + kT * q;
-      if (e < npair) {
-        const int a = e / (int)kp, c = e % (int)kp;
-        double s = acc[q];
-        for (int r = 0; r < kRows; ++r) s += sX[r][a] * sX[r][c];
-        acc[q] = s;
+    for (int q = 0; q < kBlk; ++q) {
+      const int blk = w + 4 * q;
+      if (blk < nb * nb) {  // A[i][x] = X[x][ba + i], B[x][j] = X[x][bc + j]
+        const int ba = 16 * (blk / nb), bc = 16 * (blk % nb);
+#pragma unroll
+        for (int kk = 0; kk < kRows; kk += 4)
+          acc[q] = mfma_f64(sX[(kk + kr) * kLd + ba + cr], sX[(kk + kr) * kLd + bc + cr], acc[q]);
       }
     }
   }
   double* G = Gpart + ((mi * 2 + (isR ? 1 : 0)) * nsplit + blockIdx.z) * kp * kp;
 #pragma unroll
-  for (int q = 0; q < (kMaxKp * kMaxKp) / kT; ++q) {
-    const int e = threadIdx.x + kT * q;
-    if (e < npair) G[e] = acc[q];
+  for (int q = 0; q < kBlk; ++q) {
+    const int blk = w + 4 * q;
+    if (blk < nb * nb) {
+      const int ba = 16 * (blk / nb), bc = 16 * (blk % nb);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = ba + kr + 4 * r, col = bc + cr;
+        if (row < K && col < K) G[row * kp + col] = acc[q][r];
+      }
+    }
   }
 }
 
