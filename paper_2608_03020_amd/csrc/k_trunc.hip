@@ -48,11 +48,8 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
   const float* Rm = R + (mi / r_group) * r_bstride;
   const int K = (int)kp, nb = (K + 15) / 16, nv = kRows * K;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, kr = lane >> 4, cr = lane & 15;
-  // staged element f of a chunk: row r, column c (R's rows are contiguous along i)
-  auto where = [&](int f, int& r, int& c) {
-    if (isR) { c = f / kRows; r = f % kRows; }
-    else { r = f / K; c = f % K; }
-  };
+  // staged element f of a chunk: (row, column) (R's rows are contiguous along i)
+  auto where = [&](int f) { return isR ? make_int2(f % kRows, f / kRows) : make_int2(f / K, f % K); };
   for (int e = tid; e < kRows * kLd; e += kT) sX[e] = 0.0;  // columns past kp stay zero
   float v[kPer];
   auto load = [&](int64_t i0) {
@@ -61,10 +58,9 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
       const int f = tid + kT * j;
       float x = 0.f;
       if (f < nv) {
-        int r, c;
-        where(f, r, c);
-        const int64_t i = i0 + r;
-        if (i < ie) x = isR ? Rm[c * d + i] : Mm[i * kp + c];
+        const int2 rc = where(f);
+        const int64_t i = i0 + rc.x;
+        if (i < ie) x = isR ? Rm[rc.y * d + i] : Mm[i * kp + rc.y];
       }
       v[j] = x;
     }
@@ -79,9 +75,8 @@ __global__ __launch_bounds__(kT) void k_small_grams(int64_t d, int64_t kp, const
     for (int j = 0; j < kPer; ++j) {
       const int f = tid + kT * j;
       if (f < nv) {
-        int r, c;
-        where(f, r, c);
-        sX[r * kLd + c] = (double)v[j];
+        const int2 rc = where(f);
+        sX[rc.x * kLd + rc.y] = (double)v[j];
       }
     }
     __syncthreads();
