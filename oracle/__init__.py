@@ -125,6 +125,32 @@ def cross_acc(X, T, Z=None, a=None):
     return Z
 
 
+def gram_matmul(X, a=None):
+    """The same Gram as gram_acc, S = sum_t a_t x_t x_t^T (Eq. 9; Section S7's weights),
+    with a library matrix product as its one step: fast enough for the full workload
+    widths (d up to 5120 over 65536 tokens), where the plain loops would take hours."""
+    X = _f64(X)
+    if a is None:
+        return X.T @ X
+    return X.T @ (X * _weights(a, X.shape[0])[:, None])
+
+
+def cross_matmul(X, T, a=None):
+    """The same cross statistic as cross_acc, sum_t a_t x_t T_t^T (Eq. 9), as one library
+    matrix product."""
+    X, T = _f64(X), _f64(T)
+    if a is None:
+        return X.T @ T
+    return X.T @ (T * _weights(a, X.shape[0])[:, None])
+
+
+def credit_matmul(E, A, B=None):
+    """The tokenwise feedback of `credit` (Y = E A~, Q = Y B~; Sections S3, S11) with library
+    matrix products, for a full vocabulary where E A~ has n * V * k terms."""
+    Y = _f64(E) @ _f64(A)
+    return Y, (None if B is None else Y @ _f64(B))
+
+
 def gram_entries(X, pairs) -> np.ndarray:
     X = _f64(X)
     n, d = X.shape

@@ -182,8 +182,10 @@ int loca_oracle_cholesky(int64_t d, double* A) {
   return 0;
 }
 
-/* Solve L L^T X = B for m right-hand sides (B is d x m, overwritten by X). */
+/* Solve L L^T X = B for m right-hand sides (B is d x m, overwritten by X).  The
+ * right-hand sides are independent: OpenMP gives whole columns to threads. */
 void loca_oracle_cholesky_solve(int64_t d, int64_t m, const double* L, double* B) {
+#pragma omp parallel for schedule(static)
   for (int64_t c = 0; c < m; ++c) {
     for (int64_t i = 0; i < d; ++i) { /* forward: L y = b */
       double v = B[IDX(i, c, m)];

@@ -167,6 +167,34 @@ def test_gram_cross_against_library_and_invariants(orc):
     np.testing.assert_array_equal(Ze[3], Te[2])
 
 
+def test_matmul_statistics_equal_plain_loops(orc):
+    """The library-product forms used at full workload width (gram_matmul, cross_matmul,
+    credit_matmul) against the plain loops pinned above, with and without weights; and the
+    one-hot orientation check on the product forms themselves."""
+    rng = np.random.default_rng(55)
+    X = rng.normal(size=(37, 11))
+    T = rng.normal(size=(37, 5))
+    a = rng.uniform(0.0, 2.0, 37)
+    a[::4] = 0.0
+    np.testing.assert_allclose(orc.gram_matmul(X), orc.gram_acc(X), rtol=1e-13, atol=1e-12)
+    np.testing.assert_allclose(orc.gram_matmul(X, a), orc.gram_acc(X, a=a), rtol=1e-13, atol=1e-12)
+    np.testing.assert_allclose(orc.cross_matmul(X, T), orc.cross_acc(X, T), rtol=1e-13, atol=1e-12)
+    np.testing.assert_allclose(orc.cross_matmul(X, T, a), orc.cross_acc(X, T, a=a), rtol=1e-13, atol=1e-12)
+    E = orc.head_error(rng.normal(0, 2, (37, 6)), rng.integers(0, 6, 37))
+    A = rng.normal(size=(6, 4))
+    B = rng.normal(size=(4, 11))
+    Y, Q = orc.credit(E, A, B)
+    Ym, Qm = orc.credit_matmul(E, A, B)
+    np.testing.assert_allclose(Ym, Y, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(Qm, Q, rtol=1e-13, atol=1e-13)
+    Xe = np.zeros((3, 4))
+    Xe[0, 1] = Xe[1, 1] = Xe[2, 3] = 1.0
+    Se = orc.gram_matmul(Xe)
+    assert Se[1, 1] == 2 and Se[3, 3] == 1 and Se.sum() == 3
+    Te = np.arange(12.0).reshape(3, 4)
+    np.testing.assert_array_equal(orc.cross_matmul(Xe, Te)[1], Te[0] + Te[1])
+
+
 def test_streaming_additivity(orc):
     """Section S7: statistics over the concatenation equal the sum over mini-batches."""
     rng = np.random.default_rng(6)
