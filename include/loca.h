@@ -30,15 +30,22 @@
  *     solves blocks independently, Section S8).  Per-block arrays of block b
  *     start at base + b * <name>_bstride (in elements of the array's type).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream).
- *     The library never synchronises, never allocates device memory and
- *     keeps no global state.  Scratch memory comes from the caller's `ws`,
- *     at least loca_workspace_size(...) bytes, 256-byte aligned.
+ *     The library never synchronises and never allocates device memory.
+ *     Scratch memory comes from the caller's `ws`, at least
+ *     loca_workspace_size(...) bytes, 256-byte aligned.
+ *   - State kept by the library: loca_ridge_solve creates, on its first call
+ *     on a device, two internal streams and a few events of that device, and
+ *     keeps them until the process ends; creating them and every submission
+ *     that uses them run under a per-device mutex.
  *   - Argument errors are detected on the host before anything is enqueued
  *     and returned synchronously (LOCA_E_ARG, LOCA_E_WORKSPACE,
  *     LOCA_E_UNSUPPORTED).  Launch failures return LOCA_E_HIP.  Conditions
- *     found on the device are written to `dev_info` (device int32).
- *   - Concurrent calls are safe when they use distinct output and workspace
- *     buffers.  No C++ exception crosses this interface.
+ *     found on the device are written to `dev_info` (device int32): 0 when
+ *     none, LOCA_INFO_NONFINITE for non-finite data, else the entry point's
+ *     own positive code.
+ *   - Concurrent calls from several host threads are safe when they use
+ *     distinct output, dev_info and workspace buffers.  No C++ exception
+ *     crosses this interface.
  *   - Precision modes: "bf16 mode" = bf16 X, fp32 statistics (S, K); "fp32
  *     mode" = fp32 X, fp64 statistics.  Other combinations are rejected.
  */
@@ -61,6 +68,11 @@ typedef enum {
 } loca_status;
 
 typedef enum { LOCA_F32 = 0, LOCA_BF16 = 1, LOCA_F64 = 2 } loca_dtype;
+
+/* dev_info code of every entry point that checks its data: a non-finite value (NaN, an
+ * infinity, or a square that overflows) reached a reduction of the call, whose outputs
+ * are then unspecified.  It takes precedence over the positive codes. */
+#define LOCA_INFO_NONFINITE (-1)
 
 typedef enum {
   LOCA_OP_ERROR_TARGETS = 0,
@@ -103,7 +115,9 @@ typedef void* loca_stream_t; /* hipStream_t */
  * e_out : n x C float, or NULL (the error rows, for tests).
  * mb_out : nb entries; sum_q2 and n are written, sum_x2 and eta_bar zeroed.
  * dev_info : one int32; 0, or 1 + the smallest row whose label is out of range
- *            (that row's outputs are then unspecified).
+ *            (that row's outputs are then unspecified), or LOCA_INFO_NONFINITE when
+ *            ||Q||^2 of some block is not finite (a NaN or +inf logit, or non-finite
+ *            weights or credit factors; a -inf logit is an excluded class and is fine).
  * Limits: k <= 128.  Any n >= 1, C >= 1, d >= 1.
  * ------------------------------------------------------------------------- */
 loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k,
@@ -135,6 +149,10 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
  *       significant bits), at twice the matrix-core work of the unweighted call.
  * mb : in: sum_q2; out: sum_x2, eta_bar, n.   eta >= 0.
  * S, K : per block, type `acc`, strides s_bstride, k_bstride.
+ * dev_info : nb int32 or NULL; per block 0, or LOCA_INFO_NONFINITE when ||X_m||^2 or
+ *            ||Q_m||^2 is not finite (a NaN or infinite entry of X_m, an entry whose
+ *            square overflows, or a non-finite head call); that block's S, K and
+ *            eta_bar are then unspecified.
  * Limits: k <= 128.
  * ------------------------------------------------------------------------- */
 loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, int64_t d, int64_t k,
@@ -142,7 +160,7 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
                                   const float* y, int64_t y_bstride, const float* a_w,
                                   double eta, loca_mb* mb,
                                   void* S, void* K, loca_dtype acc, int64_t s_bstride,
-                                  int64_t k_bstride, void* ws, size_t ws_bytes);
+                                  int64_t k_bstride, int32_t* dev_info, void* ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------------------
  * (a5) Ridge solve in factored form (Eq. 7; Theorem S6.1; Section S7's
@@ -159,12 +177,15 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
  * w_dense_out : optional float d x d W for matrix (b, l) at
  *               w_dense_out + (b * n_lambda + l) * w_bstride; needs rp and
  *               credit_b (ignored when NULL).
- * dev_info : nb * n_lambda int32; 0, or the 1-based index of the first
- *            non-positive pivot (LAPACK potrf convention).
+ * dev_info : nb * n_lambda int32; 0, or the 1-based index of a non-positive
+ *            pivot (LAPACK potrf convention; a NaN pivot counts as non-positive).
  * Limits: r_prev + k <= 128, n_lambda <= 8, nb * n_lambda <= 65535, d <= 65535.
- * Solves of two halves of the blocks run on the caller's stream and on a second
- * stream the library creates once per device; the call stays ordered on the
- * caller's stream (it waits for the second).
+ * With two or more blocks the blocks are split into up to three groups: the first
+ * runs on the caller's stream, the others on two internal streams the library
+ * creates on its first call on the device.  The internal streams wait for the
+ * caller's stream at entry and the caller's stream waits for them at the end, so
+ * the call stays ordered on the caller's stream; calls from several host threads
+ * are serialised on the internal streams (see the conventions above).
  * ------------------------------------------------------------------------- */
 loca_status loca_ridge_solve(loca_stream_t stream, int64_t nb, int64_t d, int64_t k, const void* S,
                              const void* K, loca_dtype acc, int64_t s_bstride, int64_t k_bstride,

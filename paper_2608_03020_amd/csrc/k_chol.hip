@@ -16,6 +16,8 @@
 //   3. back substitution U M' = Y by row blocks, each a product with U11^{-1},
 //      then M = D M'.
 // The first non-positive pivot is reported in dev_info (1-based).
+#include <mutex>
+
 #include "loca_common.h"
 #include "loca_bf16.h"
 
@@ -1541,39 +1543,44 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
   });
 }
 
-// Extra streams and events per device, made on first use.  The blocks of a call are
-// split into up to kGroups groups on the caller's stream and kGroups - 1 internal
-// streams, group g started once group g - 1 has factored its first diagonal block:
-// the latency-bound launches of one group (diagonal blocks, strips, back
-// substitution: few workgroups each) then run beside the matrix-core updates of the
+// Extra streams and events per device, made on first use: the only state the library
+// keeps.  The blocks of a call are split into up to kGroups groups on the caller's stream
+// and kGroups - 1 internal streams, group g started once group g - 1 has factored its
+// first diagonal block: the latency-bound launches of one group (diagonal blocks, strips,
+// back substitution: few workgroups each) then run beside the matrix-core updates of the
 // others instead of leaving most of the GPU idle.
+//
+// The streams and events are shared by every call on a device, so creating them and the
+// whole submission of a call that uses them (fork record, waits, launches, join records)
+// happen under the device's mutex.  A wait on an event takes the event's state at the time
+// the wait is enqueued, so once a call has left the critical section its internal work is
+// ordered behind its own fork point and the next call may record the events again.
 #ifndef LOCA_SOLVE_GROUPS
 #define LOCA_SOLVE_GROUPS 3
 #endif
 constexpr int kGroups = LOCA_SOLVE_GROUPS;
+constexpr int kMaxDevices = 64;
 struct Aux {
+  std::mutex mu;
+  bool ready = false;
   hipStream_t s[kGroups] = {};
   hipEvent_t fork = nullptr;
   hipEvent_t stagger[kGroups] = {};
   hipEvent_t join[kGroups] = {};
 };
-Aux g_aux[64];
+Aux g_aux[kMaxDevices];
 
-hipError_t get_aux(Aux** out) {
-  int dev = 0;
-  hipError_t e = hipGetDevice(&dev);
-  if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  Aux& x = g_aux[dev];
-  if (!x.fork) {
-    for (int g = 1; g < kGroups; ++g) {
-      if ((e = hipEventCreateWithFlags(&x.stagger[g], hipEventDisableTiming)) != hipSuccess) return e;
-      if ((e = hipEventCreateWithFlags(&x.join[g], hipEventDisableTiming)) != hipSuccess) return e;
-      if ((e = hipStreamCreateWithFlags(&x.s[g], hipStreamNonBlocking)) != hipSuccess) return e;
-    }
-    if ((e = hipEventCreateWithFlags(&x.fork, hipEventDisableTiming)) != hipSuccess) return e;
+// With the device's mutex held: the internal streams and events exist.
+hipError_t aux_ready(Aux& x) {
+  if (x.ready) return hipSuccess;
+  hipError_t e;
+  for (int g = 1; g < kGroups; ++g) {
+    if (!x.stagger[g] && (e = hipEventCreateWithFlags(&x.stagger[g], hipEventDisableTiming)) != hipSuccess) return e;
+    if (!x.join[g] && (e = hipEventCreateWithFlags(&x.join[g], hipEventDisableTiming)) != hipSuccess) return e;
+    if (!x.s[g] && (e = hipStreamCreateWithFlags(&x.s[g], hipStreamNonBlocking)) != hipSuccess) return e;
   }
-  *out = &x;
+  if (!x.fork && (e = hipEventCreateWithFlags(&x.fork, hipEventDisableTiming)) != hipSuccess) return e;
+  x.ready = true;
   return hipSuccess;
 }
 
@@ -1599,8 +1606,12 @@ hipError_t run_solve(const SolveArgs& a) {
     Emit now;
     return run_group<T, ST>(a, 0, a.nb, a.stream, F, R, D, Mp, SLp, dlam, nullptr, now);
   }
-  Aux* x = nullptr;
-  if ((e = get_aux(&x)) != hipSuccess) return e;
+  int dev = 0;
+  if ((e = hipGetDevice(&dev)) != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  Aux* x = &g_aux[dev];
+  std::lock_guard<std::mutex> hold(x->mu);
+  if ((e = aux_ready(*x)) != hipSuccess) return e;
   if ((e = hipEventRecord(x->fork, a.stream)) != hipSuccess) return e;
   // Every group's launches are recorded first, then submitted round-robin, one launch
   // per group in turn.  Group g joins once group g - 1 has submitted its first diagonal

@@ -314,26 +314,36 @@ __global__ __launch_bounds__(kLargeThreads) void k_error_large(
 }
 
 // E rows for the large-vocabulary path (optional output), from the saved (m, s).
+// Tokens t = blockIdx.y, blockIdx.y + gridDim.y, ... (any n with gridDim.y <= 65535).
 template <typename LT>
 __global__ void k_error_write_e(int64_t n, int64_t C, const LT* __restrict__ logits, int64_t ld,
                                 const int32_t* __restrict__ labels, const float* __restrict__ w,
                                 const float* __restrict__ ms, float* __restrict__ e_out) {
-  const int64_t t = blockIdx.y;
-  const float m = ms[2 * t], inv = 1.0f / ms[2 * t + 1];
-  const float wt = w ? w[t] : 1.0f;
-  const int32_t yt = labels[t];
-  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < C; c += (int64_t)gridDim.x * blockDim.x)
-    e_out[t * C + c] = wt * (__expf(load_as_f32(logits + t * ld + c) - m) * inv - (c == yt ? 1.f : 0.f));
+  for (int64_t t = blockIdx.y; t < n; t += gridDim.y) {
+    const float m = ms[2 * t], inv = 1.0f / ms[2 * t + 1];
+    const float wt = w ? w[t] : 1.0f;
+    const int32_t yt = labels[t];
+    for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < C; c += (int64_t)gridDim.x * blockDim.x)
+      e_out[t * C + c] = wt * (__expf(load_as_f32(logits + t * ld + c) - m) * inv - (c == yt ? 1.f : 0.f));
+  }
 }
+static unsigned write_e_rows(int64_t n) { return (unsigned)(n < 65535 ? n : 65535); }
 
-// dev_info holds INT32_MAX (no bad label) or 1 + the smallest bad row; 0 means ok.
+// On entry dev_info holds INT32_MAX (no bad label) or 1 + the smallest bad row.  A block
+// whose ||Q||^2 is not finite (a non-finite logit, loss or statistic weight, or credit
+// factor: NaN and infinities propagate into every product that uses them) lowers it to
+// LOCA_INFO_NONFINITE; INT32_MAX then becomes 0.  The exchange leaves a code another block
+// has already written in place, whatever the order of the blocks.
 __global__ void k_error_finalize(int64_t n, int64_t nparts, const double* __restrict__ partial,
                                  loca_mb* __restrict__ mb, int32_t* __restrict__ dev_info) {
   const int64_t b = blockIdx.x;
   if (threadIdx.x != 0) return;
-  if (b == 0 && dev_info && *dev_info == INT32_MAX) *dev_info = 0;
   double s = 0.0;
   for (int64_t i = 0; i < nparts; ++i) s += partial[b * nparts + i];
+  if (dev_info) {
+    if (!__builtin_isfinite(s)) atomicMin(dev_info, (int32_t)LOCA_INFO_NONFINITE);
+    if (b == 0) atomicCAS(dev_info, INT32_MAX, 0);
+  }
   mb[b].sum_q2 = s;
   mb[b].sum_x2 = 0.0;
   mb[b].eta_bar = 0.0;
@@ -518,7 +528,7 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
     if (e != hipSuccess) return e;
     k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, grid.x, partial, a.mb_out, a.dev_info);
     if (a.e_out) {
-      dim3 g2((unsigned)((a.C + 255) / 256 < 64 ? (a.C + 255) / 256 : 64), (unsigned)a.n);
+      dim3 g2((unsigned)((a.C + 255) / 256 < 64 ? (a.C + 255) / 256 : 64), write_e_rows(a.n));
       k_error_write_e<LT><<<g2, 256, 0, a.stream>>>(a.n, a.C, z, a.ld_logits, a.labels, a.w, ms, a.e_out);
     }
   }
@@ -562,7 +572,7 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
     k_error_finalize<<<(unsigned)a.nb, 64, 0, a.stream>>>(a.n, gq.x, partial, a.mb_out, a.dev_info);
     if (a.e_out) {
       const float* msv = (const float*)pw;  // (m, s) per token, first in the product's workspace
-      dim3 g2((unsigned)((a.C + 255) / 256 < 64 ? (a.C + 255) / 256 : 64), (unsigned)a.n);
+      dim3 g2((unsigned)((a.C + 255) / 256 < 64 ? (a.C + 255) / 256 : 64), write_e_rows(a.n));
       if (a.logits_dtype == LOCA_BF16)
         k_error_write_e<uint16_t><<<g2, 256, 0, a.stream>>>(a.n, a.C, (const uint16_t*)a.logits, a.ld_logits,
                                                              a.labels, a.w, msv, a.e_out);

@@ -697,10 +697,13 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
 // One workgroup per (block, 256 entries of K); its first wave forms ||X||^2 from the
 // diagonal tiles' partials (lane l sums partials l, l + 64, ... in order, then a fixed
 // butterfly across the lanes: deterministic) and eta-bar once for the workgroup.
+// dev_info (may be null) gets, per block, 0 or LOCA_INFO_NONFINITE when ||X||^2 or ||Q||^2
+// is not finite (a NaN or infinite entry of X, an entry whose square overflows, or a
+// non-finite error row in the head call).
 template <typename AccT>
 __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, const double* __restrict__ diag_part,
                                  loca_mb* __restrict__ mb, double eta, const AccT* __restrict__ Kraw, int split,
-                                 AccT* __restrict__ Kall, int64_t k_bstride) {
+                                 AccT* __restrict__ Kall, int64_t k_bstride, int32_t* __restrict__ dev_info) {
   __shared__ double s_eb;
   const int64_t b = blockIdx.y;
   if (threadIdx.x < 64) {
@@ -715,6 +718,8 @@ __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, con
         mb[b].sum_x2 = sx;
         mb[b].eta_bar = eb;
         mb[b].n = n;
+        if (dev_info)
+          dev_info[b] = (__builtin_isfinite(sx) && __builtin_isfinite(sq)) ? 0 : (int32_t)LOCA_INFO_NONFINITE;
       }
     }
   }
@@ -817,7 +822,7 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     if (e != hipSuccess) return e;
     dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
     k_stats_finalize<double><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 0,
-                                                       (double*)a.K, a.k_bstride);
+                                                       (double*)a.K, a.k_bstride, a.dev_info);
     return hipGetLastError();
   }
   float* Kraw = (float*)p;
@@ -907,7 +912,7 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   if (e != hipSuccess) return e;
   dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
   k_stats_finalize<float><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
-                                                    (float*)a.K, a.k_bstride);
+                                                    (float*)a.K, a.k_bstride, a.dev_info);
   return hipGetLastError();
 }
 

@@ -30,7 +30,8 @@ constexpr int kHT = 256;
 constexpr int kHM = 128, kHK = 32;  // token rows, vocabulary per stage
 constexpr int kLDA = kHK + 8;                  // bf16 per LDS row of P (80 bytes)
 
-// dev_info: INT32_MAX while no bad label is seen, then 1 + the smallest bad row, or 0
+// dev_info: INT32_MAX while no bad label is seen, then 1 + the smallest bad row, or
+// LOCA_INFO_NONFINITE once a row's softmax sum is not finite; INT32_MAX becomes 0 at the end
 __global__ void k_fill_i32_head(int32_t* p) {
   if (threadIdx.x == 0) *p = INT32_MAX;
 }
@@ -130,6 +131,8 @@ __global__ __launch_bounds__(kHT) void k_softmax_stats(int64_t n, int64_t V, con
     ms[2 * t + 1] = ss[0];
     const int32_t yt = labels[t];
     if (yt < 0 || yt >= V) atomicMin(dev_info, (int32_t)(t + 1));
+    // a NaN or +inf logit makes the sum NaN (a -inf logit is an excluded class and is fine)
+    if (!__builtin_isfinite(ss[0])) atomicMin(dev_info, (int32_t)LOCA_INFO_NONFINITE);
   }
 }
 

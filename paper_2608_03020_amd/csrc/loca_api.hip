@@ -64,13 +64,11 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
   return 0;
 }
 
-loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k, int64_t d,
-                               const void* logits, loca_dtype logits_dtype, int64_t ld_logits,
-                               const int32_t* labels, const float* w, const float* a_w, const void* credit_a,
-                               loca_dtype a_dtype,
-                               int64_t a_bstride, const float* credit_b, int64_t b_bstride, float* y_out,
-                               int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info, void* ws,
-                               size_t ws_bytes) {
+static loca_status check_error_args(int64_t nb, int64_t n, int64_t C, int64_t k, int64_t d, const void* logits,
+                                    loca_dtype logits_dtype, int64_t ld_logits, const int32_t* labels,
+                                    const void* credit_a, loca_dtype a_dtype, int64_t a_bstride, const float* credit_b,
+                                    int64_t b_bstride, const float* y_out, int64_t y_bstride, const loca_mb* mb_out,
+                                    const int32_t* dev_info) {
   if (nb < 1 || n < 1 || C < 1 || k < 1 || d < 1) return LOCA_E_ARG;
   if (!logits || !labels || !credit_a || !credit_b || !y_out || !mb_out || !dev_info) return LOCA_E_ARG;
   if (ld_logits < C) return LOCA_E_ARG;
@@ -79,7 +77,20 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
   if (nb > 1 && (a_bstride < C * k || b_bstride < k * d || y_bstride < n * k)) return LOCA_E_ARG;
   if (n > (int64_t)INT32_MAX - 1 || nb > 65535) return LOCA_E_UNSUPPORTED;
   if (k > kMaxK) return LOCA_E_UNSUPPORTED;
-  loca_status st = check_ws(ws, ws_bytes, error_targets_ws(nb, n, C, k));
+  return LOCA_OK;
+}
+
+loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k, int64_t d,
+                               const void* logits, loca_dtype logits_dtype, int64_t ld_logits,
+                               const int32_t* labels, const float* w, const float* a_w, const void* credit_a,
+                               loca_dtype a_dtype,
+                               int64_t a_bstride, const float* credit_b, int64_t b_bstride, float* y_out,
+                               int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info, void* ws,
+                               size_t ws_bytes) {
+  loca_status st = check_error_args(nb, n, C, k, d, logits, logits_dtype, ld_logits, labels, credit_a, a_dtype,
+                                    a_bstride, credit_b, b_bstride, y_out, y_bstride, mb_out, dev_info);
+  if (st != LOCA_OK) return st;
+  st = check_ws(ws, ws_bytes, error_targets_ws(nb, n, C, k));
   if (st != LOCA_OK) return st;
   ErrorArgs a{(hipStream_t)stream, nb, n, C, k, d, ld_logits, logits, logits_dtype, labels, w, a_w, credit_a, a_dtype,
               a_bstride, credit_b, b_bstride, y_out, y_bstride, e_out, mb_out, dev_info, (char*)ws};
@@ -90,7 +101,8 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
                                   loca_dtype x_dtype, int64_t ldx, int64_t x_bstride, const float* y,
                                   int64_t y_bstride, const float* a_w, double eta, loca_mb* mb, void* S, void* K,
                                   loca_dtype acc,
-                                  int64_t s_bstride, int64_t k_bstride, void* ws, size_t ws_bytes) {
+                                  int64_t s_bstride, int64_t k_bstride, int32_t* dev_info, void* ws,
+                                  size_t ws_bytes) {
   if (nb < 1 || n < 1 || d < 1 || k < 1) return LOCA_E_ARG;
   if (!x || !y || !mb || !S || !K) return LOCA_E_ARG;
   if (!(eta >= 0.0) || eta == __builtin_inf()) return LOCA_E_ARG;
@@ -107,7 +119,7 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
   loca_status st = check_ws(ws, ws_bytes, accumulate_stats_ws(nb, n, d, k, acc));
   if (st != LOCA_OK) return st;
   StatsArgs a{(hipStream_t)stream, nb, n, d, k, x, x_dtype, ldx, x_bstride, y, y_bstride, a_w, eta, mb, S, K, acc,
-              s_bstride, k_bstride, (char*)ws};
+              s_bstride, k_bstride, dev_info, (char*)ws};
   return from_hip(launch_accumulate_stats(a));
 }
 

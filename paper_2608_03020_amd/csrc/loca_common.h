@@ -306,6 +306,7 @@ struct StatsArgs {
   const float* y; int64_t y_bstride; const float* a_w;
   double eta; loca_mb* mb;
   void* S; void* K; loca_dtype acc; int64_t s_bstride, k_bstride;
+  int32_t* dev_info;
   char* ws;
 };
 size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc);

@@ -16,6 +16,7 @@ LIB_PATH = os.environ.get("LOCA_LIB", os.path.join(HERE, "lib", "libloca.so"))
 
 LOCA_OK, LOCA_E_ARG, LOCA_E_WORKSPACE, LOCA_E_HIP, LOCA_E_UNSUPPORTED = range(5)
 LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
+LOCA_INFO_NONFINITE = -1
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
  LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR) = range(8)
 
@@ -55,7 +56,7 @@ def load():
     lib.loca_error_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _VP, _I,
                                        _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _VP, _D,
-                                          _VP, _VP, _VP, _I, _I64, _I64, _VP, _SZ]
+                                          _VP, _VP, _VP, _I, _I64, _I64, _VP, _VP, _SZ]
     lib.loca_ridge_solve.argtypes = [_VP, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _VP, _I64, _I64, _I64,
                                      _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
     lib.loca_lowrank_truncate.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _I64, _VP, _I64, _VP,
@@ -164,16 +165,18 @@ def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_in
     _check("loca_error_targets", st)
 
 
-def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, stream=None):
+def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, dev_info=None, stream=None):
     """x (nb, n, d) bf16 or fp32 (row stride may exceed d); y (nb, n, k); S (nb, d, d); K (nb, d, k);
-    a_w (n,) float32 statistic weights, the array given to loca_error_targets (optional)."""
+    a_w (n,) float32 statistic weights, the array given to loca_error_targets (optional);
+    dev_info (nb,) int32 non-finite flags (optional)."""
     nb, n, d = x.shape
     k = y.shape[-1]
     acc = _dtype(S)
     st = load().loca_accumulate_stats(
         _stream(stream), nb, n, d, k, _ptr(x), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), _ptr(a_w),
         float(eta),
-        _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), _ptr(ws), ws.numel() * ws.element_size())
+        _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), _ptr(dev_info), _ptr(ws),
+        ws.numel() * ws.element_size())
     _check("loca_accumulate_stats", st)
 
 

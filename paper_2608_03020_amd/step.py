@@ -23,7 +23,7 @@ class BlockStep:
     """
 
     def __init__(self, cfg: LocaConfig, nb: int, device="cuda", projected: bool = False, n_total: Optional[int] = None,
-                 r_prev: int = 0):
+                 r_prev: int = 0, poison: bool = False):
         import torch
         self.cfg, self.nb, self.device = cfg, nb, device
         d, k, r_a = cfg.d, cfg.k, cfg.r_a
@@ -36,7 +36,16 @@ class BlockStep:
         self.Y = torch.empty((nb, n_mb, k), dtype=torch.float32, device=device)
         self.mb = loca.new_mb(nb, device)
         self.mb_log: List = []
-        self.info = torch.zeros(max(nb * nl, 1), dtype=torch.int32, device=device)
+        # one dev_info slice per call, so that no call's codes overwrite another's: the head
+        # error of every micro-batch, the statistics of every (micro-batch, block), the solve,
+        # the truncation and the projected solve of every (block, lambda)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.info_err = torch.zeros(cfg.n_micro, **i32)
+        self.info_stats = torch.zeros((cfg.n_micro, nb), **i32)
+        self.info_solve = torch.zeros(nb * nl, **i32)
+        self.info_trunc = torch.zeros(nb * nl, **i32)
+        self.info_proj = torch.zeros(nb * nl, **i32)
+        self._m = 0
         self.r_prev = r_prev
         kp = r_prev + k  # right-hand sides of the solve: [S Lp | K]
         self.M = torch.empty((nb, nl, d, kp), dtype=torch.float32, device=device)
@@ -54,50 +63,73 @@ class BlockStep:
             loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE_PROJECTED, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
         )
         self.ws = loca.alloc_workspace(ws, device)
+        if poison:
+            # NaN in every output and all-ones bytes in the workspace, so that a region a
+            # call should write but does not shows up as NaN in the results
+            for t in (self.Y, self.M, self.A_ad, self.B_ad, self.sigma) + ((self.B_proj,) if projected else ()):
+                t.fill_(float("nan"))
+            self.ws.fill_(255)
+
+    @property
+    def info(self):
+        """Every dev_info slice of the step, concatenated (device int32; all zero when no
+        call reported a condition)."""
+        import torch
+        return torch.cat([self.info_err, self.info_stats.reshape(-1), self.info_solve, self.info_trunc,
+                          self.info_proj])
 
     def reset(self):
         self.S.zero_()
         self.K.zero_()
         self.mb_log = []
+        self._m = 0  # every call rewrites its own dev_info slice
 
     def micro_batch(self, x_m, logits_m, labels_m, credit_a, credit_b, keep_log=False, stream=None, w=None, a=None):
         """Rows a1-a4 for one micro-batch: x_m (nb, n_m, d); w (n_m,) optional loss weights;
         a (n_m,) optional statistic weights (Section S7's weighted statistics)."""
         n_m = x_m.shape[1]
         y = self.Y[:, :n_m]
-        loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info, self.ws, w=w, a_w=a,
-                                nb=self.nb, stream=stream)
-        loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, a_w=a, stream=stream)
+        m = self._m
+        if m >= self.cfg.n_micro:
+            raise ValueError(f"more than {self.cfg.n_micro} micro-batches since reset()")
+        self._m += 1
+        loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info_err[m:m + 1], self.ws,
+                                w=w, a_w=a, nb=self.nb, stream=stream)
+        loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, a_w=a,
+                                   dev_info=self.info_stats[m], stream=stream)
         if keep_log:
             self.mb_log.append(self.mb.clone())
 
-    def solve(self, credit_b, proj_a=None, stream=None, lp=None, rp=None, mid_event=None):
+    def solve(self, credit_b, proj_a=None, stream=None, lp=None, rp=None, mid_event=None, trunc_event=None):
         """Rows a5-a6: ridge solves for every lambda and the rank-r_a truncation.
 
         With a current adapter W_prev = Lp Rp (lp: (nb, d, r_prev), rp: (nb, r_prev, d);
         the outer iteration past its first step, Theorem S6.1 with W_prev != 0), the solve
         takes the right-hand sides [S Lp | K] and W = M [Rp; B~] is truncated from its
         factors; the stacked right factor is a copy (layout only).  mid_event, when given,
-        is recorded on the current stream between the solves and the truncation."""
+        is recorded on the current stream between the solves and the truncation, and
+        trunc_event between the truncation and the projected solve."""
         import torch
         cfg = self.cfg
         nl = len(cfg.lambdas)
         kp = self.r_prev + cfg.k
         if self.r_prev > 0:
             assert lp is not None and rp is not None and lp.shape[-1] == self.r_prev
-            loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, lp=lp, rp=rp,
+            loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info_solve, self.ws, lp=lp, rp=rp,
                                   stream=stream)
             right = torch.cat([rp, credit_b], dim=1).contiguous()
         else:
-            loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info, self.ws, stream=stream)
+            loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info_solve, self.ws, stream=stream)
             right = credit_b
         if mid_event is not None:
             mid_event.record(stream if stream is not None else torch.cuda.current_stream())
         loca.loca_lowrank_truncate(self.M.view(self.nb * nl, cfg.d, kp), right, cfg.r_a, self.A_ad, self.B_ad,
-                                   self.sigma, self.info, self.ws, r_group=nl, stream=stream)
+                                   self.sigma, self.info_trunc, self.ws, r_group=nl, stream=stream)
+        if trunc_event is not None:
+            trunc_event.record(stream if stream is not None else torch.cuda.current_stream())
         if self.projected and proj_a is not None:
-            loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj, self.info,
-                                            self.ws, stream=stream)
+            loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj,
+                                            self.info_proj, self.ws, stream=stream)
 
     def run(self, x_blocks, logits, labels, credit_a, credit_b, proj_a=None, stream=None):
         """One full pass over all micro-batches of all nb blocks."""

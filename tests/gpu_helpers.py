@@ -56,7 +56,7 @@ def run_gpu(cfg, xs, zs, ys, As, Bs, want_dense=True, proj=None, device="cuda"):
     from paper_2608_03020_amd import loca
     from paper_2608_03020_amd.step import BlockStep
     nb = len(xs)
-    step = BlockStep(cfg, nb, device, projected=proj is not None)
+    step = BlockStep(cfg, nb, device, projected=proj is not None, poison=True)
     x_all = padded_rows(np.stack([np.concatenate(xb, axis=0) for xb in xs]), device)
     z_all = to_dev(np.concatenate(zs, axis=0), device)
     y_all = to_dev(np.concatenate(ys, axis=0), device)
@@ -70,9 +70,13 @@ def run_gpu(cfg, xs, zs, ys, As, Bs, want_dense=True, proj=None, device="cuda"):
         step.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B)
         Ys.append(step.Y[:, :hi - lo].cpu().numpy().copy())
         mbs.append(loca.mb_view(step.mb))
-    info_stats = step.info.cpu().numpy().copy()
+    info_stats = step.info.cpu().numpy().copy()  # head error and statistics slices
     step.solve(B, P)
     nl = len(cfg.lambdas)
+    # every output of the step was NaN before the calls (poisoned): none may survive
+    for name, t in (("M", step.M), ("A", step.A_ad), ("B", step.B_ad), ("sigma", step.sigma),
+                    ("S", step.S), ("K", step.K)) + ((("B_proj", step.B_proj),) if proj is not None else ()):
+        assert not bool(torch.isnan(t).any()), f"{name} has unwritten (NaN) entries"
     out = {"S": step.S.cpu().numpy(), "K": step.K.cpu().numpy(), "Y": Ys, "mb": mbs,
            "M": step.M.cpu().numpy(), "sigma": step.sigma.cpu().numpy(), "A": step.A_ad.cpu().numpy(),
            "B": step.B_ad.cpu().numpy(), "info_err": info_stats, "info": step.info.cpu().numpy()}
@@ -84,12 +88,15 @@ def run_gpu(cfg, xs, zs, ys, As, Bs, want_dense=True, proj=None, device="cuda"):
         info = torch.zeros(nb * nl, dtype=torch.int32, device=device)
         ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, nb * nl, 0, d, cfg.k,
                                                       r_a=cfg.r_a), device)
-        a_o = torch.empty_like(step.A_ad)
-        b_o = torch.empty_like(step.B_ad)
-        s_o = torch.empty_like(step.sigma)
+        a_o = torch.full_like(step.A_ad, float("nan"))
+        b_o = torch.full_like(step.B_ad, float("nan"))
+        s_o = torch.full_like(step.sigma, float("nan"))
+        Wr.fill_(float("nan"))
+        ws.fill_(255)
         loca.loca_lowrank_truncate(step.M.view(nb * nl, d, cfg.k), B, cfg.r_a, a_o, b_o, s_o, info, ws, r_group=nl,
                                    w_dense_out=Wr)
         out["W_r"] = Wr.cpu().numpy()
+        assert not np.isnan(out["W_r"]).any() and not bool(torch.isnan(a_o).any() | torch.isnan(b_o).any())
     torch.cuda.synchronize()
     return out
 

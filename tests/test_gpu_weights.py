@@ -42,7 +42,7 @@ def _run(cfg, blocks, xs, zs, ys, As, Bs, a_list, dev="cuda"):
         mbs.append(step.mb.cpu().numpy().copy())
     step.solve(B)
     torch.cuda.synchronize()
-    assert int(step.info.cpu().numpy().max()) == 0
+    assert np.all(step.info.cpu().numpy() == 0), step.info.cpu().numpy()
     return step, mbs
 
 
