@@ -71,7 +71,11 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=2)
-    p.add_argument("--config", default="c3", choices=sorted(WORKLOADS))
+    p.add_argument("--config", default="c5", choices=sorted(WORKLOADS),
+                   help="headline workload (default c5, the largest configuration)")
+    p.add_argument("--secondary", default="c3", type=lambda v: [x for x in v.split(",") if x],
+                   help="comma-separated workloads timed after the headline and reported under "
+                        "\"secondary\" (default c3, the first at d >= 3584; '' for none)")
     p.add_argument("--blocks", type=int, default=0, help="override the block count (profiling runs)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-tokens", type=int, default=0, help="tokens in the CPU-baseline sample")
@@ -101,13 +105,15 @@ def make_inputs(cfg, nb, device="cuda"):
 
 
 def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, lp=None, rp=None,
-             solve_record=None, error_record=None):
+             solve_record=None, error_record=None, proj=None):
     """One step of the whole path over every block: per micro-batch the head error
     and credit coordinates (from the event error_record[m] when given), then the
     statistics (bracketed by the events of `record[m]` when given); then the ridge
-    solves and the truncation (bracketed by `solve_record`: start, between the solves
-    and the truncation when it has three events, end).  Optional: statistic weights
-    a_all (n,), a current adapter lp (nb, d, r_prev), rp (nb, r_prev, d)."""
+    solves, the truncation and, with the projections `proj` (nb, r_a, d), the
+    paper-literal projected solve (bracketed by `solve_record`: start, between the
+    solves and the truncation and between the truncation and the projected solve when
+    it has four events, end).  Optional: statistic weights a_all (n,), a current
+    adapter lp (nb, d, r_prev), rp (nb, r_prev, d)."""
     from paper_2608_03020_amd import loca
     step.reset()
     for m in range(cfg.n_micro):
@@ -117,16 +123,19 @@ def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, 
         aw = None if a_all is None else a_all[lo:hi]
         if error_record is not None:
             error_record[m].record(stream)
-        loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info, step.ws, a_w=aw, nb=nb)
+        loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info_err[m:m + 1], step.ws, a_w=aw,
+                                nb=nb)
         if record is not None:
             record[m][0].record(stream)
-        loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws, a_w=aw)
+        loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws, a_w=aw,
+                                   dev_info=step.info_stats[m])
         if record is not None:
             record[m][1].record(stream)
     if solve_record is not None:
         solve_record[0].record(stream)
-    step.solve(B, lp=lp, rp=rp, mid_event=solve_record[1] if solve_record is not None and len(solve_record) > 2
-               else None)
+    marks = solve_record if solve_record is not None and len(solve_record) == 4 else None
+    step.solve(B, proj_a=proj, lp=lp, rp=rp, mid_event=marks[1] if marks else None,
+               trunc_event=marks[2] if marks else None)
     if solve_record is not None:
         solve_record[-1].record(stream)
 
@@ -331,10 +340,10 @@ def paper_order_head(stream, L=24, d=896, n=4096, V=151936, k=64, reps=5):
 
 def cpu_baseline(cfg, n_sample):
     """The oracle as it stands, on a bounded sample of block 0 of the workload:
-    the per-token stages (head error, feedback, target, S, dense Z, K) on
-    `n_sample` tokens of one micro-batch, scaled to the block's N tokens, plus
-    the per-block stages (ridge solve of every lambda with the factored
-    right-hand side K, Eckart-Young truncation) at full width."""
+    the per-token stages (head error, feedback, target, S, dense Z, K, the projected
+    statistics) on `n_sample` tokens of one micro-batch, scaled to the block's N
+    tokens, plus the per-block stages (ridge solve of every lambda with the factored
+    right-hand side K, Eckart-Young truncation, projected solve) at full width."""
     import numpy as np
     import oracle
     from paper_2608_03020_amd import inputs as gen
@@ -349,6 +358,7 @@ def cpu_baseline(cfg, n_sample):
     A, Bm = gen.gen_credit(sub, 0)
     A = gen.as_f64(A, cfg.a_dtype)
     Bm = np.asarray(Bm, np.float64)
+    Ap = np.asarray(gen.gen_adapter_projection(sub, 0), np.float64)
     t0 = time.perf_counter()
     E = oracle.head_error(z, y)
     Y, Q = oracle.credit(E, A, Bm)
@@ -356,6 +366,7 @@ def cpu_baseline(cfg, n_sample):
     S = oracle.gram_acc(X)
     Z = oracle.cross_acc(X, T)
     K = oracle.cross_acc(X, -info["eta_bar"] * Y)
+    G, Cst = oracle.projected_acc(X, T, Ap)
     t_tok = time.perf_counter() - t0
     # per-block stages on a well-posed full-width system (the sample's S has rank n_sample < d)
     S_full = S + np.eye(cfg.d) * float(np.trace(S) / cfg.d)
@@ -363,53 +374,55 @@ def cpu_baseline(cfg, n_sample):
     Ms = [oracle.ridge_solve(S_full, K, lam)[0] for lam in cfg.lambdas]
     for M in Ms:
         oracle.truncate_factored(M, Bm, cfg.r_a, want_dense=False)
+    G_full = G + np.eye(cfg.r_a) * float(np.trace(G) / cfg.r_a)
+    for lam in cfg.lambdas:
+        oracle.projected_solve(G_full, Cst, lam)
     t_blk = time.perf_counter() - t1
     t_block = t_tok * (cfg.n / n_sample) + t_blk
     return {"value": cfg.n / t_block, "unit": "tokens/s per block", "cores": threads, "kind": "oracle",
             "sample": (f"block 0 of {cfg.name}: per-token stages on {n_sample} of {cfg.n} tokens "
                        f"({t_tok:.2f} s, scaled x{cfg.n / n_sample:.0f}); ridge solves for {len(cfg.lambdas)} "
-                       f"lambda(s) with the factored right-hand side and truncation at d={cfg.d} ({t_blk:.2f} s)"),
+                       f"lambda(s) with the factored right-hand side, truncation and projected solve at d={cfg.d} "
+                       f"({t_blk:.2f} s)"),
             "seconds_per_block": t_block, "_unused": float(Z[0, 0])}
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
-              "(sharding the blocks across GPUs is described, not implemented).", file=sys.stderr)
-        sys.exit(2)
+def measure(args, name, nb_override=0, keep=False):
+    """Time args.steps steps of the whole path on workload `name` (after args.warmup
+    untimed ones): inputs resident in HBM, HIP events around every statistics call and
+    the step's phases.  Returns the JSON fields of the line; with keep=True also the
+    device state (for the widened rows)."""
     import numpy as np
     import torch
-    from paper_2608_03020_amd import loca
+    from paper_2608_03020_amd import inputs as gen
     from paper_2608_03020_amd.inputs import CONFIGS
     from paper_2608_03020_amd.step import BlockStep
 
-    cfg = CONFIGS[args.config]
-    nb = args.blocks or cfg.blocks
-    torch.cuda.init()
+    cfg = CONFIGS[name]
+    nb = nb_override or cfg.blocks
     dev = torch.device("cuda:0")
-    print(f"[bench] {args.config}: generating inputs for {nb} blocks", file=sys.stderr, flush=True)
+    print(f"[bench] {name}: generating inputs for {nb} blocks", file=sys.stderr, flush=True)
     x_all, z, y, A, B = make_inputs(cfg, nb)
-    step = BlockStep(cfg, nb, dev)
+    proj = gen.torch_gen_adapter_projection(cfg, nb)
+    step = BlockStep(cfg, nb, dev, projected=True)
     stream = torch.cuda.current_stream()
     torch.cuda.synchronize()
 
     # events around every statistics call of the timed region (the dominant kernel)
     n_mb = cfg.n_micro
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps * n_mb)]
-
     ev_err = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps * n_mb)]
-    ev_sol = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    ev_sol = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
 
     def one_step(record=None, s=None):
         run_step(step, cfg, nb, x_all, z, y, A, B, stream, record,
                  solve_record=ev_sol[s] if s is not None else None,
-                 error_record=ev_err[s * n_mb:(s + 1) * n_mb] if s is not None else None)
+                 error_record=ev_err[s * n_mb:(s + 1) * n_mb] if s is not None else None, proj=proj)
 
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
-    print(f"[bench] warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
+    print(f"[bench] {name}: warmup done; timing {args.steps} steps", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
     for s in range(args.steps):
         one_step(ev[s * n_mb:(s + 1) * n_mb], s)
@@ -421,14 +434,11 @@ def main():
         print(f"[bench] warning: dev_info {info}", file=sys.stderr)
 
     stats_ms = [a.elapsed_time(b) for a, b in ev]
-    rows = [cfg.micro_rows(m)[1] - cfg.micro_rows(m)[0] for m in range(n_mb)]
-    flops = [nb * (r * cfg.d * (cfg.d + 1) + 2 * r * cfg.d * cfg.k) for r in rows] * args.steps
+    flops = stats_flops(cfg, nb) * args.steps
     t_avg = sum(stats_ms) / len(stats_ms)
     f_avg = sum(flops) / len(flops)
     achieved = f_avg / (t_avg * 1e-3) / 1e12
     peak = FP64_PEAK_TFLOPS if cfg.mode == "fp32" else BF16_PEAK_TFLOPS
-
-    value = nb * cfg.n / (ms_step * 1e-3)
     K = args.steps
     breakdown = {
         "unit": "ms per step (HIP events on the launch stream)",
@@ -436,34 +446,67 @@ def main():
         "statistics": sum(stats_ms) / K,
         "ridge_solves": sum(e[0].elapsed_time(e[1]) for e in ev_sol) / K,
         "truncation": sum(e[1].elapsed_time(e[2]) for e in ev_sol) / K,
+        "projected_solve": sum(e[2].elapsed_time(e[3]) for e in ev_sol) / K,
     }
     out = {
-        "metric": "tokens/sec per block (error->target->Gram+solve); % MFMA peak on X^T X",
-        "value": value,
-        "unit": "tokens/s per block",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "value": nb * cfg.n / (ms_step * 1e-3),
         "ms_per_step": ms_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
         "dtype": "f64" if cfg.mode == "fp32" else "bf16",
-        "data": "synthetic (seeded; device-generated inputs with the workload's distributions)",
-        "config": {"workload": f"{args.config}: {WORKLOADS[args.config]}", "blocks": nb, "d": cfg.d,
+        "config": {"workload": f"{name}: {WORKLOADS[name]}", "blocks": nb, "d": cfg.d,
                    "tokens": cfg.n, "micro_batch": cfg.micro, "classes": cfg.C, "credit_rank": cfg.k,
                    "adapter_rank": cfg.r_a, "lambdas": list(cfg.lambdas)},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved / peak, "traffic": traffic_bytes(args.config),
+                     "frac": achieved / peak, "traffic": traffic_bytes(name),
                      "kernel": "loca_accumulate_stats (Gram S += X^T X and cross X^T Y of all blocks, one micro-batch)",
                      "algorithmic_flops_per_launch": f_avg, "avg_launch_ms": t_avg},
         "breakdown": breakdown,
     }
+    if keep:
+        return out, (cfg, nb, x_all, z, y, A, B, step, stream)
+    del x_all, z, y, A, B, proj, step
+    torch.cuda.empty_cache()
+    return out, None
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: the library runs on one GPU; --gpus {args.gpus} is not supported "
+              "(sharding the blocks across GPUs is described, not implemented).", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    torch.cuda.init()
+
+    head, state = measure(args, args.config, args.blocks, keep=args.next)
+    out = {
+        "metric": "tokens/sec per block (error->target->Gram+solve); % MFMA peak on X^T X",
+        "value": head["value"],
+        "unit": "tokens/s per block",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": head["dtype"],
+        "data": "synthetic (seeded; device-generated inputs with the workload's distributions)",
+        "config": head["config"],
+        "roofline": head["roofline"],
+        "breakdown": head["breakdown"],
+    }
     if args.next:
+        cfg, nb, x_all, z, y, A, B, step, stream = state
         out["next"] = next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream)
-    if not args.no_cpu_baseline:
-        del x_all
+        del state, x_all, z, y, A, B, step
         torch.cuda.empty_cache()
+    for name in args.secondary:
+        if name != args.config:
+            row, _ = measure(args, name)
+            out.setdefault("secondary", {})[name] = row
+    if not args.no_cpu_baseline:
+        from paper_2608_03020_amd.inputs import CONFIGS
+        cfg = CONFIGS[args.config]
         n_s = args.cpu_tokens or (512 if cfg.d >= 3000 else 1024)
         print(f"[bench] cpu baseline: oracle on {n_s} tokens", file=sys.stderr, flush=True)
         cb = cpu_baseline(cfg, min(n_s, cfg.n))

@@ -305,6 +305,15 @@ def torch_gen_stat_weights(cfg: LocaConfig, seed: int = 0, device="cuda", zero: 
     return a
 
 
+def torch_gen_adapter_projection(cfg: LocaConfig, blocks: int, seed: int = 0, device="cuda"):
+    """Device projections A_l (blocks, r_a, d) of the projected form, with the recipe of
+    gen_adapter_projection (entries ~ N(0, 1/d))."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed((seed * 1000003 + _CFG_ID.get(cfg.name, 99) * 7919 + 67867967) & 0x7FFFFFFF)
+    return torch.randn((blocks, cfg.r_a, cfg.d), generator=g, device=device, dtype=torch.float32) / np.sqrt(cfg.d)
+
+
 def torch_gen_current_adapter(cfg: LocaConfig, blocks: int, r_prev: int, seed: int = 0, device="cuda"):
     """Device current adapters W_prev = Lp Rp of every block, with the recipe of
     gen_current_adapter: Lp (blocks, d, r_prev), Rp (blocks, r_prev, d)."""
