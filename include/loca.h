@@ -36,7 +36,8 @@
  *   - State kept by the library: loca_ridge_solve creates, on its first call
  *     on a device, two internal streams and a few events of that device, and
  *     keeps them until the process ends; creating them and every submission
- *     that uses them run under a per-device mutex.
+ *     that uses them run under a per-device mutex.  loca_error_targets_noalloc
+ *     uses a fixed device array instead of a workspace (see there).
  *   - Argument errors are detected on the host before anything is enqueued
  *     and returned synchronously (LOCA_E_ARG, LOCA_E_WORKSPACE,
  *     LOCA_E_UNSUPPORTED).  Launch failures return LOCA_E_HIP.  Conditions
@@ -44,8 +45,9 @@
  *     none, LOCA_INFO_NONFINITE for non-finite data, else the entry point's
  *     own positive code.
  *   - Concurrent calls from several host threads are safe when they use
- *     distinct output, dev_info and workspace buffers.  No C++ exception
- *     crosses this interface.
+ *     distinct output, dev_info and workspace buffers (calls of
+ *     loca_error_targets_noalloc on one device share its array and must not
+ *     overlap).  No C++ exception crosses this interface.
  *   - Precision modes: "bf16 mode" = bf16 X, fp32 statistics (S, K); "fp32
  *     mode" = fp32 X, fp64 statistics.  Other combinations are rejected.
  */
@@ -128,6 +130,29 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
                                const float* credit_b, int64_t b_bstride, float* y_out,
                                int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info,
                                void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * loca_error_targets without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, kernels, outputs and dev_info codes as
+ * loca_error_targets, minus `ws` and `ws_bytes`: the scratch is a fixed array of
+ * loca_error_targets_noalloc_max_bytes() bytes (16 MiB) in the library's device
+ * memory, one copy per device, held until the process ends.  The call allocates
+ * nothing.  Sizes whose workspace (loca_workspace_size(LOCA_OP_ERROR_TARGETS, ...))
+ * exceeds the array return LOCA_E_UNSUPPORTED before anything is enqueued; every
+ * small label set up to nb = 48 blocks, n = 65536 tokens and k = 64 fits.
+ * Every call on a device uses the same array: calls that overlap on one device (two
+ * streams, or two host threads) race and must be serialised by the caller.  The first
+ * call on a device looks up the array's address there (LOCA_E_HIP if that fails).
+ * ------------------------------------------------------------------------- */
+loca_status loca_error_targets_noalloc(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k,
+                                       int64_t d, const void* logits, loca_dtype logits_dtype,
+                                       int64_t ld_logits, const int32_t* labels, const float* w,
+                                       const float* a_w, const void* credit_a, loca_dtype a_dtype,
+                                       int64_t a_bstride, const float* credit_b, int64_t b_bstride,
+                                       float* y_out, int64_t y_bstride, float* e_out, loca_mb* mb_out,
+                                       int32_t* dev_info);
+size_t loca_error_targets_noalloc_max_bytes(void);
 
 /* ---------------------------------------------------------------------------
  * (a3, a4) Streaming statistics of one micro-batch (Eq. 9; Section S7):

@@ -13,6 +13,8 @@
 //    sum of exp(z - m) A~[c] alongside; Y = acc / s - A~[y].
 // Both write per-workgroup partial sums of ||Q||^2 (fp64) that a finalize
 // kernel adds in a fixed order, so results are bitwise reproducible.
+#include <mutex>
+
 #include "loca_common.h"
 
 namespace loca {
@@ -587,6 +589,40 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   if (!zb && ab) return dispatch_error<float, uint16_t>(a, G, partial, ms);
   if (zb && !ab) return dispatch_error<uint16_t, float>(a, G, partial, ms);
   return dispatch_error<uint16_t, uint16_t>(a, G, partial, ms);
+}
+
+// ------------------------------------------------------------------ allocation-free variant
+// loca_error_targets_noalloc takes its scratch from a fixed device array instead of a
+// caller workspace.  The runtime gives each device its own copy of the array; its device
+// address is looked up once per device, with that device current, and kept.  Nothing in
+// the head-error workspace has to start at zero (every kernel writes what it later reads),
+// so the array is never cleared; calls on one device share it and must not overlap.
+
+namespace {
+constexpr size_t kScratchBytes = (size_t)16 << 20;  // 16 MiB
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kScratchDevices] = {};
+}  // namespace
+
+size_t error_targets_scratch_bytes() { return kScratchBytes; }
+
+hipError_t error_targets_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> hold(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 // ------------------------------------------------------------------ paper-order credit

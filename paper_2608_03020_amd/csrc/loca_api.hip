@@ -97,6 +97,25 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
   return from_hip(launch_error_targets(a));
 }
 
+loca_status loca_error_targets_noalloc(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k, int64_t d,
+                                       const void* logits, loca_dtype logits_dtype, int64_t ld_logits,
+                                       const int32_t* labels, const float* w, const float* a_w,
+                                       const void* credit_a, loca_dtype a_dtype, int64_t a_bstride,
+                                       const float* credit_b, int64_t b_bstride, float* y_out, int64_t y_bstride,
+                                       float* e_out, loca_mb* mb_out, int32_t* dev_info) {
+  loca_status st = check_error_args(nb, n, C, k, d, logits, logits_dtype, ld_logits, labels, credit_a, a_dtype,
+                                    a_bstride, credit_b, b_bstride, y_out, y_bstride, mb_out, dev_info);
+  if (st != LOCA_OK) return st;
+  if (error_targets_ws(nb, n, C, k) > error_targets_scratch_bytes()) return LOCA_E_UNSUPPORTED;
+  void* scratch_ptr = nullptr;
+  if (error_targets_scratch(&scratch_ptr) != hipSuccess) return LOCA_E_HIP;
+  ErrorArgs a{(hipStream_t)stream, nb, n, C, k, d, ld_logits, logits, logits_dtype, labels, w, a_w, credit_a, a_dtype,
+              a_bstride, credit_b, b_bstride, y_out, y_bstride, e_out, mb_out, dev_info, (char*)scratch_ptr};
+  return from_hip(launch_error_targets(a));
+}
+
+size_t loca_error_targets_noalloc_max_bytes(void) { return error_targets_scratch_bytes(); }
+
 loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, int64_t d, int64_t k, const void* x,
                                   loca_dtype x_dtype, int64_t ldx, int64_t x_bstride, const float* y,
                                   int64_t y_bstride, const float* a_w, double eta, loca_mb* mb, void* S, void* K,

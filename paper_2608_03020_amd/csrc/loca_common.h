@@ -254,6 +254,10 @@ struct ErrorArgs {
 };
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k);
 hipError_t launch_error_targets(const ErrorArgs& a);
+// the fixed scratch array of loca_error_targets_noalloc: its size, and its address on the
+// current device (looked up on the first call on that device)
+size_t error_targets_scratch_bytes();
+hipError_t error_targets_scratch(void** out);
 
 // The head in the paper's order (Section S11): e = W_u^T E once, then V_k^T e per block.
 struct TopErrorArgs {

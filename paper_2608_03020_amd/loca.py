@@ -22,8 +22,9 @@ LOCA_INFO_NONFINITE = -1
 
 ENTRY_POINTS = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_top_error",
-                "loca_credit_from_top_error")
-EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version")
+                "loca_credit_from_top_error", "loca_error_targets_noalloc")
+EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version",
+                           "loca_error_targets_noalloc_max_bytes")
 
 
 class LocaMB(ctypes.Structure):
@@ -55,6 +56,10 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     lib.loca_error_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _VP, _I,
                                        _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
+    lib.loca_error_targets_noalloc.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _VP,
+                                               _I, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP]
+    lib.loca_error_targets_noalloc_max_bytes.argtypes = []
+    lib.loca_error_targets_noalloc_max_bytes.restype = _SZ
     lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _VP, _D,
                                           _VP, _VP, _VP, _I, _I64, _I64, _VP, _VP, _SZ]
     lib.loca_ridge_solve.argtypes = [_VP, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _VP, _I64, _I64, _I64,
@@ -163,6 +168,24 @@ def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_in
         credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(y_out), y_out.stride(0) if y_out.dim() == 3 else 0,
         _ptr(e_out), _ptr(mb_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_error_targets", st)
+
+
+def loca_error_targets_noalloc(logits, labels, credit_a, credit_b, y_out, mb_out, dev_info, *, w=None, a_w=None,
+                               e_out=None, nb=None, stream=None):
+    """loca_error_targets with the library's fixed scratch array instead of a workspace."""
+    nb = nb or credit_a.shape[0]
+    n, C = logits.shape[0], logits.shape[1]
+    k, d = credit_b.shape[-2], credit_b.shape[-1]
+    st = load().loca_error_targets_noalloc(
+        _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
+        _ptr(a_w), _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
+        credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(y_out), y_out.stride(0) if y_out.dim() == 3 else 0,
+        _ptr(e_out), _ptr(mb_out), _ptr(dev_info))
+    _check("loca_error_targets_noalloc", st)
+
+
+def error_targets_noalloc_max_bytes() -> int:
+    return int(load().loca_error_targets_noalloc_max_bytes())
 
 
 def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, dev_info=None, stream=None):

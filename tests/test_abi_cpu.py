@@ -80,6 +80,25 @@ def test_error_targets_rejects(lib):
     assert call(ws=FAKE + 1, wsb=1 << 30) == lib.LOCA_E_WORKSPACE  # misaligned
 
 
+def test_error_targets_noalloc_rejects(lib):
+    """Argument errors and sizes whose workspace exceeds the fixed scratch array are
+    reported before the array is looked up on a device."""
+    so = lib.load()
+
+    def call(nb=1, n=8, C=4, k=2, d=16, logits=FAKE, info=FAKE):
+        return so.loca_error_targets_noalloc(None, nb, n, C, k, d, logits, lib.LOCA_F32, C, FAKE, None, None, FAKE,
+                                             lib.LOCA_F32, 0, FAKE, 0, FAKE, 0, None, FAKE, info)
+
+    assert call(n=0) == lib.LOCA_E_ARG
+    assert call(logits=None) == lib.LOCA_E_ARG
+    assert call(info=None) == lib.LOCA_E_ARG
+    assert call(k=129) == lib.LOCA_E_UNSUPPORTED
+    assert call(n=4096, C=151936, k=64, d=2048) == lib.LOCA_E_UNSUPPORTED   # ~34 MB of scratch
+    assert lib.error_targets_noalloc_max_bytes() == 16 << 20
+    big = lib.workspace_size(lib.LOCA_OP_ERROR_TARGETS, 48, 65536, 5120, 64, 5)
+    assert big <= lib.error_targets_noalloc_max_bytes()  # the largest small-label workload fits
+
+
 def test_accumulate_stats_rejects(lib):
     so = lib.load()
     base = [None, 1, 64, 32, 4, FAKE, lib.LOCA_BF16, 32, 0, FAKE, 0, None, 0.01, FAKE, FAKE, FAKE, lib.LOCA_F32,
