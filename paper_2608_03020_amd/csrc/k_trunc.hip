@@ -747,6 +747,96 @@ __global__ void k_proj_sa(int64_t d, int64_t r_a, const ST* __restrict__ S, int6
   T1[b * d * r_a + e] = s;
 }
 
+// The same product for fp32 S on the fp32 matrix cores (v_mfma_f32_32x32x2f32), reading S
+// once per use with coalesced loads.  One workgroup per (64-row panel I, block b); the
+// panel's rows of the symmetric S are staged 64 columns at a time: chunks right of the
+// diagonal straight from the stored upper triangle, chunks left of it as the transposes of
+// the stored tiles above the diagonal, the diagonal chunk mirrored in LDS; the chunk of
+// PA^T beside it.  Wave w forms the panel (64 x RA) over columns 16 w .. 16 w + 15 of every
+// chunk, and the four partial panels are added in a fixed order: deterministic.
+constexpr int kPS = 64;        // panel rows and chunk columns
+constexpr int kPSL = kPS + 1;  // LDS row stride (odd: column reads spread over the banks)
+template <int RA>
+__global__ __launch_bounds__(256) void k_proj_sa_mfma(int64_t d, int64_t r_a, const float* __restrict__ S,
+                                                      int64_t s_bstride, const float* __restrict__ PA,
+                                                      int64_t pa_bstride, double* __restrict__ T1) {
+  constexpr int NCB = RA / 32;
+  __shared__ float sS[kPS * kPSL];   // [row i][column j] of the panel chunk
+  __shared__ float sA[RA * kPSL];    // [adapter row a][column j]
+  __shared__ float sRed[4][kPS][RA + 1];
+  const int64_t b = blockIdx.y;
+  const int I = blockIdx.x;
+  const int64_t i0 = (int64_t)I * kPS;
+  const float* Sb = S + b * s_bstride;
+  const float* Pb = PA + b * pa_bstride;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  f32x16_t acc[2][NCB];
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.f;
+  const int nch = (int)((d + kPS - 1) / kPS);
+  for (int J = 0; J < nch; ++J) {
+    const int64_t j0 = (int64_t)J * kPS;
+    __syncthreads();  // the previous chunk is no longer read
+    // stored tile: rows r0.., columns c0.. of the upper triangle (transposed when left of the diagonal)
+    const bool left = J < I;
+    const int64_t r0 = left ? j0 : i0, c0 = left ? i0 : j0;
+#pragma unroll
+    for (int u = 0; u < kPS * kPS / 256; ++u) {
+      const int e = tid + 256 * u, rr = e / kPS, cc = e % kPS;
+      const int64_t gr = r0 + rr, gc = c0 + cc;
+      const float v = (gr < d && gc < d) ? Sb[gr * d + gc] : 0.f;
+      if (left) sS[cc * kPSL + rr] = v;
+      else sS[rr * kPSL + cc] = v;
+    }
+#pragma unroll
+    for (int u = 0; u < RA * kPS / 256; ++u) {
+      const int e = tid + 256 * u, a = e / kPS, cc = e % kPS;
+      sA[a * kPSL + cc] = (a < r_a && j0 + cc < d) ? Pb[(int64_t)a * d + j0 + cc] : 0.f;
+    }
+    __syncthreads();
+    if (J == I) {  // diagonal chunk: only its upper triangle is stored; mirror it
+#pragma unroll
+      for (int u = 0; u < kPS * kPS / 256; ++u) {
+        const int e = tid + 256 * u, rr = e / kPS, cc = e % kPS;
+        if (cc < rr) sS[rr * kPSL + cc] = sS[cc * kPSL + rr];
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int ks = 16 * w; ks < 16 * w + 16; ks += 2) {
+      const int kk = ks + (lane >> 5);
+      float fa[2], fb[NCB];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb) fa[rb] = sS[(32 * rb + (lane & 31)) * kPSL + kk];
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb) fb[cb] = sA[(32 * cb + (lane & 31)) * kPSL + kk];
+#pragma unroll
+      for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb) acc[rb][cb] = mfma_f32x2(fa[rb], fb[cb], acc[rb][cb]);
+    }
+  }
+#pragma unroll
+  for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        sRed[w][32 * rb + mfma32_row(lane, r)][32 * cb + mfma32_col(lane)] = acc[rb][cb][r];
+  __syncthreads();
+  for (int e = tid; e < kPS * RA; e += 256) {
+    const int rr = e / RA, a = e % RA;
+    const int64_t i = i0 + rr;
+    if (i < d && a < r_a)
+      T1[(b * d + i) * r_a + a] =
+          ((double)sRed[0][rr][a] + (double)sRed[1][rr][a]) + ((double)sRed[2][rr][a] + (double)sRed[3][rr][a]);
+  }
+}
+
 // G[b] = PA T1 (r_a x r_a) and AK[b] = PA K (r_a x k), fp64.
 template <typename ST>
 __global__ void k_proj_small(int64_t d, int64_t k, int64_t r_a, const float* __restrict__ PA, int64_t pa_bstride,
@@ -771,84 +861,102 @@ __global__ void k_proj_small(int64_t d, int64_t k, int64_t r_a, const float* __r
   }
 }
 
-// Per (block, lam): Cholesky of G + lam I in LDS, then for 32 rows i:
-// C[i] = B_cur[i] G + sum_c B~[c][i] AK[:, c]  and  B*[i] = C[i] (G + lam I)^{-1}.
-constexpr int kPR = 32;
-__global__ __launch_bounds__(kT) void k_proj_solve(int64_t d, int64_t k, int64_t r_a, const double* __restrict__ G,
-                                                   const double* __restrict__ AK, const float* __restrict__ Bt,
-                                                   int64_t b_bstride, const float* __restrict__ Bc,
-                                                   int64_t bc_bstride, const double* __restrict__ lam, int nl,
-                                                   float* __restrict__ out, int64_t bo_bstride,
-                                                   int32_t* __restrict__ dev_info) {
+// L = chol(G_b + lam_l I) once per (block, lambda), one wave (lower triangle, row-major
+// r_a x r_a in Lw); a non-positive pivot goes to dev_info[mi] (1-based).
+__global__ __launch_bounds__(64) void k_proj_chol(int64_t r_a, const double* __restrict__ G,
+                                                  const double* __restrict__ lam, int nl, double* __restrict__ Lw,
+                                                  int32_t* __restrict__ dev_info) {
   constexpr int LD = kMaxKp + 1;
   __shared__ double sL[kMaxKp * LD];
-  __shared__ double sG[kMaxKp * LD];
-  __shared__ double sX[kPR * LD];
-  const int64_t mi = blockIdx.y;
+  const int64_t mi = blockIdx.x;
   const int64_t b = mi / nl;
   const int l = (int)(mi % nl);
-  const int tid = threadIdx.x;
-  const int ra = (int)r_a;
-  for (int e = tid; e < ra * ra; e += kT) {
+  const int ra = (int)r_a, lane = threadIdx.x;
+  for (int e = lane; e < ra * ra; e += 64) {
     const int i = e / ra, j = e % ra;
-    const double g = G[b * r_a * r_a + e];
-    sG[i * LD + j] = g;
-    sL[i * LD + j] = g + (i == j ? lam[l] : 0.0);
+    sL[i * LD + j] = G[b * r_a * r_a + e] + (i == j ? lam[l] : 0.0);
   }
   __syncthreads();
-  // lower Cholesky in place (column by column)
   for (int j = 0; j < ra; ++j) {
-    if (tid == 0) {
-      const double piv = sL[j * LD + j];
-      if (!(piv > 0.0) && blockIdx.x == 0) atomicCAS(&dev_info[mi], 0, j + 1);
-      sL[j * LD + j] = sqrt(piv);
-    }
+    const double piv = sL[j * LD + j];
+    if (lane == 0 && !(piv > 0.0)) atomicCAS(&dev_info[mi], 0, j + 1);
+    const double ljj = sqrt(piv);
+    __syncthreads();  // every lane has read the pivot
+    if (lane == 0) sL[j * LD + j] = ljj;
+    for (int i = j + 1 + lane; i < ra; i += 64) sL[i * LD + j] /= ljj;
     __syncthreads();
-    for (int i = j + 1 + tid; i < ra; i += kT) sL[i * LD + j] /= sL[j * LD + j];
-    __syncthreads();
-    for (int e = tid; e < (ra - j - 1) * (ra - j - 1); e += kT) {
+    for (int e = lane; e < (ra - j - 1) * (ra - j - 1); e += 64) {
       const int i = j + 1 + e / (ra - j - 1), c = j + 1 + e % (ra - j - 1);
       if (c <= i) sL[i * LD + c] -= sL[i * LD + j] * sL[c * LD + j];
     }
     __syncthreads();
   }
-  // rows of C
-  const int64_t i0 = (int64_t)blockIdx.x * kPR;
+  for (int e = lane; e < ra * ra; e += 64) {
+    const int i = e / ra, j = e % ra;
+    Lw[mi * r_a * r_a + e] = j <= i ? sL[i * LD + j] : 0.0;
+  }
+}
+
+// One thread per row i of B*: C[i] = B_cur[i] G + sum_c B~[c][i] AK[:, c], then the row
+// solve x (L L^T) = C[i] (forward with L, backward with L^T), fp64, RA >= r_a registers.
+// The small operands (AK, G, L) are read at wave-uniform addresses.
+template <int RA>
+__global__ __launch_bounds__(256) void k_proj_rows(int64_t d, int64_t k, int64_t r_a, const double* __restrict__ G,
+                                                   const double* __restrict__ AK, const double* __restrict__ Lw,
+                                                   const float* __restrict__ Bt, int64_t b_bstride,
+                                                   const float* __restrict__ Bc, int64_t bc_bstride, int nl,
+                                                   float* __restrict__ out, int64_t bo_bstride) {
+  const int64_t mi = blockIdx.y;
+  const int64_t b = mi / nl;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool ok = i < d;
+  const int64_t ic = ok ? i : 0;
   const float* Btb = Bt + b * b_bstride;
   const double* AKb = AK + b * r_a * k;
-  for (int e = tid; e < kPR * ra; e += kT) {
-    const int r = e / ra, a = e % ra;
-    const int64_t i = i0 + r;
-    double s = 0.0;
-    if (i < d) {
-      for (int64_t c = 0; c < k; ++c) s += (double)Btb[c * d + i] * AKb[a * k + c];
-      if (Bc) {
-        const float* Bci = Bc + b * bc_bstride + i * r_a;
-        for (int c = 0; c < ra; ++c) s += (double)Bci[c] * sG[c * LD + a];
-      }
-    }
-    sX[r * LD + a] = s;
+  const double* L = Lw + mi * r_a * r_a;
+  double x[RA];
+#pragma unroll
+  for (int a = 0; a < RA; ++a) x[a] = 0.0;
+  for (int64_t c = 0; c < k; ++c) {
+    const double bt = (double)Btb[c * d + ic];
+#pragma unroll
+    for (int a = 0; a < RA; ++a)
+      if (a < r_a) x[a] += bt * AKb[a * k + c];
   }
-  __syncthreads();
-  // solve x (L L^T) = C row-wise: L^T-transposed system per row; one thread per row
-  if (tid < kPR) {
-    double* x = sX + tid * LD;
-    for (int a = 0; a < ra; ++a) {  // forward: L y = c
-      double v = x[a];
-      for (int c = 0; c < a; ++c) v -= sL[a * LD + c] * x[c];
-      x[a] = v / sL[a * LD + a];
-    }
-    for (int a = ra - 1; a >= 0; --a) {  // backward: L^T z = y
-      double v = x[a];
-      for (int c = a + 1; c < ra; ++c) v -= sL[c * LD + a] * x[c];
-      x[a] = v / sL[a * LD + a];
+  if (Bc) {
+    const float* Bci = Bc + b * bc_bstride + ic * r_a;
+    const double* Gb = G + b * r_a * r_a;
+    for (int64_t c = 0; c < r_a; ++c) {
+      const double v = (double)Bci[c];
+#pragma unroll
+      for (int a = 0; a < RA; ++a)
+        if (a < r_a) x[a] += v * Gb[c * r_a + a];
     }
   }
-  __syncthreads();
-  for (int e = tid; e < kPR * ra; e += kT) {
-    const int r = e / ra, a = e % ra;
-    const int64_t i = i0 + r;
-    if (i < d) out[mi * bo_bstride + i * r_a + a] = (float)sX[r * LD + a];
+#pragma unroll
+  for (int a = 0; a < RA; ++a) {  // forward: L y = c
+    if (a < r_a) {
+      double v = x[a];
+#pragma unroll
+      for (int c = 0; c < a; ++c) v -= L[a * r_a + c] * x[c];
+      x[a] = v / L[a * r_a + a];
+    }
+  }
+#pragma unroll
+  for (int a = RA - 1; a >= 0; --a) {  // backward: L^T z = y
+    if (a < r_a) {
+      double v = x[a];
+#pragma unroll
+      for (int c = a + 1; c < RA; ++c)
+        if (c < r_a) v -= L[c * r_a + a] * x[c];
+      x[a] = v / L[a * r_a + a];
+    }
+  }
+  if (ok) {
+    float* o = out + mi * bo_bstride + i * r_a;
+#pragma unroll
+    for (int a = 0; a < RA; ++a)
+      if (a < r_a) o[a] = (float)x[a];
   }
 }
 
@@ -862,11 +970,11 @@ __global__ void k_set_lams8(Lams8 l, double* out, int cnt) {
 }  // namespace
 
 size_t projected_ws(int64_t nb, int64_t d, int64_t k, int64_t r_a, int64_t n_lambda) {
-  (void)n_lambda;
   size_t s = align256(sizeof(double) * nb * d * r_a);  // T1
   s += align256(sizeof(double) * nb * r_a * r_a);      // G
   s += align256(sizeof(double) * nb * r_a * k);        // AK
   s += 256;                                            // lambdas
+  s += align256(sizeof(double) * nb * (n_lambda > 0 ? n_lambda : 1) * r_a * r_a);  // Cholesky factors
   return s;
 }
 
@@ -875,7 +983,8 @@ hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
   double* T1 = (double*)p; p += align256(sizeof(double) * a.nb * a.d * a.r_a);
   double* G = (double*)p; p += align256(sizeof(double) * a.nb * a.r_a * a.r_a);
   double* AK = (double*)p; p += align256(sizeof(double) * a.nb * a.r_a * a.k);
-  double* dlam = (double*)p;
+  double* dlam = (double*)p; p += 256;
+  double* Lw = (double*)p;
   Lams8 l8;
   for (int i = 0; i < 8; ++i) l8.v[i] = (i < a.n_lambda) ? a.lambdas[i] : 0.0;
   k_set_lams8<<<1, 64, 0, a.stream>>>(l8, dlam, (int)a.n_lambda);
@@ -888,13 +997,25 @@ hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
     k_proj_small<double><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1, (const double*)a.K,
                                                    a.k_bstride, G, AK, a.g_out);
   } else {
-    k_proj_sa<float><<<g1, 256, 0, a.stream>>>(a.d, a.r_a, (const float*)a.S, a.s_bstride, a.proj_a, a.pa_bstride, T1);
+    dim3 gp((unsigned)((a.d + kPS - 1) / kPS), (unsigned)a.nb);
+    if (a.r_a <= 32)
+      k_proj_sa_mfma<32><<<gp, 256, 0, a.stream>>>(a.d, a.r_a, (const float*)a.S, a.s_bstride, a.proj_a,
+                                                   a.pa_bstride, T1);
+    else
+      k_proj_sa_mfma<64><<<gp, 256, 0, a.stream>>>(a.d, a.r_a, (const float*)a.S, a.s_bstride, a.proj_a,
+                                                   a.pa_bstride, T1);
     k_proj_small<float><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1, (const float*)a.K,
                                                   a.k_bstride, G, AK, a.g_out);
   }
-  dim3 g3((unsigned)((a.d + kPR - 1) / kPR), (unsigned)nm);
-  k_proj_solve<<<g3, kT, 0, a.stream>>>(a.d, a.k, a.r_a, G, AK, a.credit_b, a.b_bstride, a.b_cur, a.bc_bstride, dlam,
-                                        (int)a.n_lambda, a.b_out, a.bo_bstride, a.dev_info);
+  k_proj_chol<<<(unsigned)nm, 64, 0, a.stream>>>(a.r_a, G, dlam, (int)a.n_lambda, Lw, a.dev_info);
+  dim3 g3((unsigned)((a.d + 255) / 256), (unsigned)nm);
+#define LOCA_PROJ_ROWS(RA)                                                                                           \
+  k_proj_rows<RA><<<g3, 256, 0, a.stream>>>(a.d, a.k, a.r_a, G, AK, Lw, a.credit_b, a.b_bstride, a.b_cur, a.bc_bstride, \
+                                            (int)a.n_lambda, a.b_out, a.bo_bstride)
+  if (a.r_a <= 16) LOCA_PROJ_ROWS(16);
+  else if (a.r_a <= 32) LOCA_PROJ_ROWS(32);
+  else LOCA_PROJ_ROWS(64);
+#undef LOCA_PROJ_ROWS
   return hipGetLastError();
 }
 
