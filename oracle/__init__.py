@@ -222,6 +222,26 @@ def truncate_factored(M, R, r, want_dense=True):
     return Wr, sig, a, b
 
 
+def realization_error(X, T, W, W_prev=None, a=None, want_e=False):
+    """Realisation error of a fitted adapter (Section S6): the fit realises the
+    displacement X (W - W_prev) (token-major: row n is (W - W_prev)^T x_n, the paper's
+    (B* - B^(t)) p_n) where the target asked for T (rows T_n, the paper's -s q), and
+        E_fit = X (W - W_prev) - T      (the data residual B* P - R),
+    formed densely by its definition (the product X (W - W_prev) by a library matmul).
+    With position weights `a` (Section S7) the squared norms are weighted.  Returns
+    {"fit2": sum_n a_n ||E_fit,n||^2, "tar2": sum_n a_n ||T_n||^2, "w2": ||W||_F^2}
+    (and E_fit itself with want_e)."""
+    X, T, W = _f64(X), _f64(T), _f64(W)
+    D = W if W_prev is None else W - _f64(W_prev)
+    E = X @ D - T
+    wa = np.ones(X.shape[0]) if a is None else _weights(a, X.shape[0])
+    out = {"fit2": float(np.sum(wa[:, None] * E * E)), "tar2": float(np.sum(wa[:, None] * T * T)),
+           "w2": float(np.sum(W * W))}
+    if want_e:
+        out["E"] = E
+    return out
+
+
 def projected_acc(X, T, Aproj, Bcur=None, G=None, Cst=None, a=None):
     X, T, Aproj = _f64(X), _f64(T), _f64(Aproj)
     n, d = X.shape

@@ -277,6 +277,48 @@ def test_ridge_gap_identity(orc):
         assert phi(Wb) > phi(W)
 
 
+def test_realization_error_pins(orc):
+    """Section S6's realisation error E_fit = X (W - W_prev) - T, pinned by consequences of
+    Theorem S6.1 rather than by its own formula:
+      * first-order condition at the ridge solution: X^T E_fit = -lam W;
+      * the ridge objective fit2 + lam w2 is the residual of the augmented least-squares
+        problem [X; sqrt(lam) I] W = [X W_prev + T; 0] solved by LAPACK;
+      * no change (W = W_prev) realises nothing: fit2 = tar2;
+      * a target inside the feature span (T = X V) is realised exactly as lam -> 0;
+      * position weights scale each row's contribution."""
+    rng = np.random.default_rng(31)
+    n, d, m = 40, 9, 9
+    X = rng.normal(size=(n, d)) * rng.uniform(0.5, 3, d)
+    T = rng.normal(size=(n, m))
+    Wp = 0.3 * rng.normal(size=(d, m))
+    lam = 0.7
+    S = X.T @ X
+    W, _ = orc.ridge_solve(S, S @ Wp + X.T @ T, lam)
+    r = orc.realization_error(X, T, W, Wp, want_e=True)
+    np.testing.assert_allclose(X.T @ r["E"], -lam * W, atol=1e-10 * np.abs(W).max() * lam)
+    aug_X = np.vstack([X, np.sqrt(lam) * np.eye(d)])
+    aug_T = np.vstack([X @ Wp + T, np.zeros((d, m))])
+    Wl, res, _, _ = np.linalg.lstsq(aug_X, aug_T, rcond=None)
+    np.testing.assert_allclose(W, Wl, rtol=1e-9, atol=1e-12)
+    assert abs((r["fit2"] + lam * r["w2"]) - res.sum()) < 1e-9 * res.sum()
+    assert abs(r["tar2"] - np.sum(T * T)) < 1e-12 * r["tar2"]
+    r0 = orc.realization_error(X, T, Wp, Wp)
+    assert abs(r0["fit2"] - r0["tar2"]) < 1e-12 * r0["tar2"]
+    V = rng.normal(size=(d, m))
+    Ts = X @ V
+    Ws, _ = orc.ridge_solve(S, X.T @ Ts, 1e-10)
+    assert orc.realization_error(X, Ts, Ws)["fit2"] < 1e-12 * np.sum(Ts * Ts)
+    a = rng.uniform(0, 2, n)
+    a[3] = 0.0
+    ra = orc.realization_error(X, T, W, Wp, a=a, want_e=True)
+    assert abs(ra["fit2"] - np.sum(a * np.sum(ra["E"] ** 2, axis=1))) < 1e-12 * ra["fit2"]
+    Xd = X.copy()
+    Xd[3] *= 100.0  # a zero-weight row has no influence
+    Td = T.copy()
+    Td[3] += 5.0
+    assert abs(orc.realization_error(Xd, Td, W, Wp, a=a)["fit2"] - ra["fit2"]) < 1e-12 * ra["fit2"]
+
+
 def test_ridge_limits(orc):
     rng = np.random.default_rng(11)
     X, T, S, Z = _ridge_problem(rng, 50, 7, 3)
