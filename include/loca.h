@@ -84,7 +84,8 @@ typedef enum {
   LOCA_OP_RIDGE_SOLVE_PROJECTED = 4,
   LOCA_OP_FEEDBACK_FIT = 5,
   LOCA_OP_TOP_ERROR = 6,
-  LOCA_OP_CREDIT_FROM_TOP_ERROR = 7
+  LOCA_OP_CREDIT_FROM_TOP_ERROR = 7,
+  LOCA_OP_REALIZATION_ERROR = 8
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -264,6 +265,32 @@ loca_status loca_ridge_solve_projected(loca_stream_t stream, int64_t nb, int64_t
                                        void* ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------------------
+ * Realisation error of the fitted adapters (Section S6): the fit realises the
+ * displacement X (W - W_prev) instead of the desired T (all micro-batches stacked), and
+ *   E_fit = X (W - W_prev) - T          (the data residual B* P - R of the paper).
+ * From the solve's outputs and the statistics, for block b and each lam_l (host array):
+ *   out[3 i + 0] = sum_n a_n ||E_fit,n||^2,  out[3 i + 1] = ||T||^2 = sum_m eta_bar_m^2 ||Q_m||^2,
+ *   out[3 i + 2] = ||W||_F^2,                i = b * n_lambda + l,
+ * so that the ridge objective of Theorem S6.1 is out[0] + lam out[2].  Since (S + lam I) W
+ * = S W_prev + Z (Z = K B~), X^T X (W - W_prev) = Z - lam W, and
+ *   ||E_fit||^2 = ||T||^2 - tr((W - W_prev)^T Z) - lam tr((W - W_prev)^T W),
+ * which needs only k x k products of the factors; the value is exact for the computed M up to
+ * the solve's residual, and loses relative accuracy when ||E_fit||^2 << ||T||^2.
+ * m : per (b, l) d x kp float (kp = r_prev + k), from loca_ridge_solve: matrix (b, l) at
+ *     m + (b * n_lambda + l) * m_bstride.   r : per block kp x d float, [Rp; B~] (r_bstride).
+ * K : per block d x k, type acc (r_prev = 0: B~ = r).   lp : per block d x r_prev, or NULL.
+ * mb_log : n_mb x nb records of the step's micro-batches, (m, b) at mb_log[m * nb + b].
+ * Limits: kp <= 64, n_lambda <= 8.  Workspace: LOCA_OP_REALIZATION_ERROR with nb, d, k,
+ * r_a = r_prev and n_lambda.
+ * ------------------------------------------------------------------------- */
+loca_status loca_realization_error(loca_stream_t stream, int64_t nb, int64_t d, int64_t k, int64_t r_prev,
+                                   const float* m, int64_t m_bstride, const float* r, int64_t r_bstride,
+                                   const void* K, loca_dtype acc, int64_t k_bstride, const float* lp,
+                                   int64_t lp_bstride, const loca_mb* mb_log, int64_t n_mb,
+                                   const double* lambdas, int64_t n_lambda, double* out, void* ws,
+                                   size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
  * Dense displacement T = -eta_bar Y B~ (Eq. 10; Section S8) of one micro-batch,
  * n x d float per block (stride t_bstride), from the credit coordinates and
  * the eta_bar written by loca_accumulate_stats.  Not on the hot path (the
@@ -345,7 +372,8 @@ loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t
 
 /* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
  * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there; n = np for
- * LOCA_OP_FEEDBACK_FIT; C = V for LOCA_OP_TOP_ERROR).  `acc` selects the precision mode.  Unused arguments
+ * LOCA_OP_FEEDBACK_FIT; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
+ * LOCA_OP_REALIZATION_ERROR).  `acc` selects the precision mode.  Unused arguments
  * may be 0. */
 size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,
                            int64_t r_a, int64_t n_lambda, loca_dtype acc);

@@ -14,6 +14,9 @@
 //   5. the credit factors B~ = S_k U_k^T, A~ = W_u V_k (W_u^T folded into A~, as on the hot
 //      path), and the alignment diagnostic alpha_b = <F_b E, G_b> / (||F_b E|| ||G_b||),
 //      with ||F_b E|| = ||S_k V_k^T E|| since U_k has orthonormal columns.
+//
+// The realisation error of a fitted adapter (Section S6) is also here: it needs the same
+// fixed-order products of tall d x (<= 64) operands.
 #include "loca_common.h"
 
 namespace loca {
@@ -27,9 +30,10 @@ constexpr int kRows = 32;
 // part[(b * ns + z) * kL * kR + j * kR + n] = sum_{c in rows of z} L_b(c, j) R_b(c, n), fp64,
 // L_b(c, j) = L[b * l_bs + c * l_sc + j * l_sj] (likewise R); rows split in ns equal ranges
 // of 32-row multiples (grid: x = z, y = b).
+template <typename RT>
 __global__ __launch_bounds__(kT) void k_tall_cross(int64_t d, int kL, int kR, const float* __restrict__ L,
                                                    int64_t l_bs, int64_t l_sc, int64_t l_sj,
-                                                   const float* __restrict__ R, int64_t r_bs, int64_t r_sc,
+                                                   const RT* __restrict__ R, int64_t r_bs, int64_t r_sc,
                                                    int64_t r_sn, int ns, double* __restrict__ part) {
   __shared__ double sL[kRows][kMaxNp + 1];
   __shared__ double sR[kRows][kMaxNp + 1];
@@ -38,7 +42,7 @@ __global__ __launch_bounds__(kT) void k_tall_cross(int64_t d, int kL, int kR, co
   const int64_t chunk = ((d + ns - 1) / ns + kRows - 1) / kRows * kRows;
   const int64_t ib = (int64_t)z * chunk, ie = ib + chunk < d ? ib + chunk : d;
   const float* Lb = L + b * l_bs;
-  const float* Rb = R + b * r_bs;
+  const RT* Rb = R + b * r_bs;
   const int nout = kL * kR;
   double acc[(kMaxNp * kMaxNp) / kT];
 #pragma unroll
@@ -233,7 +237,135 @@ int calib_splits(int64_t d) {
   return (int)(s < 1 ? 1 : (s > 16 ? 16 : s));
 }
 
+// ------------------------------------------------------------------ realisation error
+// Per (block b, lambda l), from fixed-order sums of the tall products' partials (z ranges):
+//   tZ = tr((M^T K)(B~ R^T)) - tr((Lp^T K)(B~ Rp^T)),   tW = tr((M^T M)(R R^T)) - tr((Lp^T M)(R Rp^T)),
+//   t2 = sum_m eta_bar_m^2 ||Q_m||^2,   out = {t2 - tZ - lam tW, t2, tr((M^T M)(R R^T))}.
+// B~ R^T and R Rp^T are rows / columns of R R^T, since R = [Rp; B~].
+template <typename F>
+LOCA_DEV double zsum_block(F term, int cnt, double* sred) {
+  double v = 0.0;
+  for (int e = threadIdx.x; e < cnt; e += kT) v += term(e);
+  return block_sum(v, sred);  // thread 0
+}
+__global__ __launch_bounds__(kT) void k_fit_finalize(int64_t nb, int nl, int kp, int k, int rp, int ns,
+                                                     const double* __restrict__ pMK, const double* __restrict__ pMM,
+                                                     const double* __restrict__ pRR, const double* __restrict__ pLK,
+                                                     const double* __restrict__ pLM, const loca_mb* __restrict__ mb_log,
+                                                     int64_t n_mb, const double* __restrict__ lam,
+                                                     double* __restrict__ out) {
+  __shared__ double sred[kT / 64];
+  const int64_t mi = blockIdx.x;
+  const int64_t b = mi / nl;
+  const int l = (int)(mi % nl);
+  // partial z of entry e of a product with `cnt` entries, for launch-local block index bl
+  auto zs = [&](const double* part, int64_t bl, int64_t cnt, int e) {
+    double v = 0.0;
+    for (int z = 0; z < ns; ++z) v += part[(bl * ns + z) * cnt + e];
+    return v;
+  };
+  const double* MK = pMK + (int64_t)l * nb * ns * kp * k;
+  const double* MM = pMM + (int64_t)l * nb * ns * kp * kp;
+  const double* LM = pLM + (int64_t)l * nb * ns * rp * kp;
+  const double z1 = zsum_block([&](int e) {
+    const int a = e / k, c = e % k;
+    return zs(MK, b, (int64_t)kp * k, e) * zs(pRR, b, (int64_t)kp * kp, (rp + c) * kp + a);
+  }, kp * k, sred);
+  __syncthreads();
+  const double w1 = zsum_block([&](int e) {
+    const int a = e / kp, a2 = e % kp;
+    return zs(MM, b, (int64_t)kp * kp, e) * zs(pRR, b, (int64_t)kp * kp, a2 * kp + a);
+  }, kp * kp, sred);
+  __syncthreads();
+  double z2 = 0.0, w2 = 0.0;
+  if (rp > 0) {
+    z2 = zsum_block([&](int e) {
+      const int q = e / k, c = e % k;
+      return zs(pLK, b, (int64_t)rp * k, e) * zs(pRR, b, (int64_t)kp * kp, (rp + c) * kp + q);
+    }, rp * k, sred);
+    __syncthreads();
+    w2 = zsum_block([&](int e) {
+      const int q = e / kp, a = e % kp;
+      return zs(LM, b, (int64_t)rp * kp, e) * zs(pRR, b, (int64_t)kp * kp, a * kp + q);
+    }, rp * kp, sred);
+  }
+  if (threadIdx.x == 0) {
+    double t2 = 0.0;
+    for (int64_t m = 0; m < n_mb; ++m) {
+      const loca_mb& r = mb_log[m * nb + b];
+      t2 += r.eta_bar * r.eta_bar * r.sum_q2;
+    }
+    out[3 * mi + 0] = t2 - (z1 - z2) - lam[l] * (w1 - w2);
+    out[3 * mi + 1] = t2;
+    out[3 * mi + 2] = w1;
+  }
+}
+
+struct FitLams {
+  double v[8];
+};
+__global__ void k_fit_lams(FitLams l, double* out, int cnt) {
+  if ((int)threadIdx.x < cnt) out[threadIdx.x] = l.v[threadIdx.x];
+}
+
 }  // namespace
+
+size_t realization_error_ws(int64_t nb, int64_t d, int64_t k, int64_t r_prev, int64_t n_lambda) {
+  const int64_t ns = calib_splits(d), kp = r_prev + k;
+  size_t s = 256;  // lambdas
+  s += align256(sizeof(double) * n_lambda * nb * ns * kp * k);       // M^T K
+  s += align256(sizeof(double) * n_lambda * nb * ns * kp * kp);      // M^T M
+  s += align256(sizeof(double) * nb * ns * kp * kp);                 // R R^T
+  s += align256(sizeof(double) * nb * ns * (r_prev > 0 ? r_prev : 1) * k);               // Lp^T K
+  s += align256(sizeof(double) * n_lambda * nb * ns * (r_prev > 0 ? r_prev : 1) * kp);   // Lp^T M
+  return s;
+}
+
+hipError_t launch_realization_error(const FitArgs& a) {
+  const int64_t d = a.d, k = a.k, rp = a.r_prev, kp = rp + k, nb = a.nb, nl = a.n_lambda;
+  const int ns = calib_splits(d);
+  char* p = a.ws;
+  double* dlam = (double*)p; p += 256;
+  double* pMK = (double*)p; p += align256(sizeof(double) * nl * nb * ns * kp * k);
+  double* pMM = (double*)p; p += align256(sizeof(double) * nl * nb * ns * kp * kp);
+  double* pRR = (double*)p; p += align256(sizeof(double) * nb * ns * kp * kp);
+  double* pLK = (double*)p; p += align256(sizeof(double) * nb * ns * (rp > 0 ? rp : 1) * k);
+  double* pLM = (double*)p;
+  hipStream_t st = a.stream;
+  FitLams fl;
+  for (int i = 0; i < 8; ++i) fl.v[i] = i < nl ? a.lambdas[i] : 0.0;
+  k_fit_lams<<<1, 64, 0, st>>>(fl, dlam, (int)nl);
+  const dim3 g((unsigned)ns, (unsigned)nb);
+  // R R^T from the rows of R (R^T(c, j) = R[j][c])
+  k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)kp, (int)kp, a.r, a.r_bstride, 1, d, a.r, a.r_bstride, 1, d, ns, pRR);
+  if (rp > 0) {
+    if (a.acc == LOCA_F64)
+      k_tall_cross<double><<<g, kT, 0, st>>>(d, (int)rp, (int)k, a.lp, a.lp_bstride, rp, 1, (const double*)a.K,
+                                             a.k_bstride, k, 1, ns, pLK);
+    else
+      k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)rp, (int)k, a.lp, a.lp_bstride, rp, 1, (const float*)a.K,
+                                            a.k_bstride, k, 1, ns, pLK);
+  }
+  for (int64_t l = 0; l < nl; ++l) {
+    const float* Ml = a.m + l * a.m_bstride;  // matrix (b, l) at m + (b nl + l) m_bstride
+    const int64_t mbs = nl * a.m_bstride;
+    double* oMK = pMK + l * nb * ns * kp * k;
+    double* oMM = pMM + l * nb * ns * kp * kp;
+    if (a.acc == LOCA_F64)
+      k_tall_cross<double><<<g, kT, 0, st>>>(d, (int)kp, (int)k, Ml, mbs, kp, 1, (const double*)a.K, a.k_bstride, k,
+                                             1, ns, oMK);
+    else
+      k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)kp, (int)k, Ml, mbs, kp, 1, (const float*)a.K, a.k_bstride, k,
+                                            1, ns, oMK);
+    k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)kp, (int)kp, Ml, mbs, kp, 1, Ml, mbs, kp, 1, ns, oMM);
+    if (rp > 0)
+      k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)rp, (int)kp, a.lp, a.lp_bstride, rp, 1, Ml, mbs, kp, 1, ns,
+                                            pLM + l * nb * ns * rp * kp);
+  }
+  k_fit_finalize<<<(unsigned)(nb * nl), kT, 0, st>>>(nb, (int)nl, (int)kp, (int)k, (int)rp, ns, pMK, pMM, pRR, pLK,
+                                                     pLM, a.mb_log, a.n_mb, dlam, a.out);
+  return hipGetLastError();
+}
 
 size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
   const int ns = calib_splits(d);
@@ -268,7 +400,7 @@ hipError_t launch_feedback_fit(const CalibArgs& a) {
   hipStream_t st = a.stream;
   k_zero_i32<<<(unsigned)((nb + 255) / 256), 256, 0, st>>>(a.dev_info, nb);
   // 1-3: Gamma, its Cholesky with beta, R = (Gamma + beta I)^{-1} E^T
-  k_tall_cross<<<dim3((unsigned)ns, 1), kT, 0, st>>>(d, (int)np_, (int)np_, a.e, 0, np_, 1, a.e, 0, np_, 1, ns, gpart);
+  k_tall_cross<float><<<dim3((unsigned)ns, 1), kT, 0, st>>>(d, (int)np_, (int)np_, a.e, 0, np_, 1, a.e, 0, np_, 1, ns, gpart);
   k_chol_small<<<1, kT, 0, st>>>((int)np_, ns, gpart, a.beta, Lmat, a.dev_info, nb);
   k_ridge_cols<<<(unsigned)((d + kT - 1) / kT), kT, 0, st>>>(d, (int)np_, a.e, Lmat, R);
   hipError_t e = hipGetLastError();
@@ -282,11 +414,11 @@ hipError_t launch_feedback_fit(const CalibArgs& a) {
   k_calib_factors<<<dim3((unsigned)((d + 255) / 256), (unsigned)nb), 256, 0, st>>>(
       d, (int)k, (int)np_, ut, vs, a.sigma_out, a.bt_out, a.bt_bstride, vk);
   // P = U_k^T G (U_k^T is k x d: L(c, j) = ut[j * d + c]); Q = (V_k S_k)^T E; ||G||^2 from G^T G
-  k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, ut, k * d, 1, d, a.g,
+  k_tall_cross<float><<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, ut, k * d, 1, d, a.g,
                                                                  a.g_bstride, np_, 1, ns, pP);
-  k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, vs, d * k, k, 1, a.e, 0, np_, 1,
+  k_tall_cross<float><<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, vs, d * k, k, 1, a.e, 0, np_, 1,
                                                                  ns, pQ);
-  k_tall_cross<<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)np_, (int)np_, a.g, a.g_bstride, np_, 1, a.g,
+  k_tall_cross<float><<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)np_, (int)np_, a.g, a.g_bstride, np_, 1, a.g,
                                                                  a.g_bstride, np_, 1, ns, pG);
   k_calib_alpha<<<(unsigned)nb, kT, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
   if (a.vk_out) {

@@ -60,6 +60,8 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
     case LOCA_OP_FEEDBACK_FIT: return d < 1 || n < 1 || n > 64 ? 0 : feedback_fit_ws(nb, d, n, k);
     case LOCA_OP_TOP_ERROR: return n < 1 || d < 1 || C < 1 ? 0 : top_error_ws(n, C, d);
     case LOCA_OP_CREDIT_FROM_TOP_ERROR: return n < 1 ? 0 : credit_from_top_error_ws(nb, n, k);
+    case LOCA_OP_REALIZATION_ERROR:
+      return d < 1 || n_lambda < 1 || r_a < 0 ? 0 : realization_error_ws(nb, d, k, r_a, n_lambda);
   }
   return 0;
 }
@@ -215,6 +217,28 @@ loca_status loca_ridge_solve_projected(loca_stream_t stream, int64_t nb, int64_t
   ProjArgs a{(hipStream_t)stream, nb, d, k, r_a, S, K, acc, s_bstride, k_bstride, credit_b, b_bstride, proj_a,
              pa_bstride, b_cur, bc_bstride, lambdas, n_lambda, b_out, bo_bstride, g_out, dev_info, (char*)ws};
   return from_hip(launch_ridge_solve_projected(a));
+}
+
+loca_status loca_realization_error(loca_stream_t stream, int64_t nb, int64_t d, int64_t k, int64_t r_prev,
+                                   const float* m, int64_t m_bstride, const float* r, int64_t r_bstride,
+                                   const void* K, loca_dtype acc, int64_t k_bstride, const float* lp,
+                                   int64_t lp_bstride, const loca_mb* mb_log, int64_t n_mb, const double* lambdas,
+                                   int64_t n_lambda, double* out, void* ws, size_t ws_bytes) {
+  if (nb < 1 || d < 1 || k < 1 || r_prev < 0 || n_mb < 0) return LOCA_E_ARG;
+  if (!m || !r || !K || !out || (n_mb > 0 && !mb_log)) return LOCA_E_ARG;
+  if (acc != LOCA_F32 && acc != LOCA_F64) return LOCA_E_ARG;
+  if (bad_lambdas(lambdas, n_lambda)) return LOCA_E_ARG;
+  const int64_t kp = r_prev + k;
+  if (r_prev > 0 && (!lp || (nb > 1 && lp_bstride < d * r_prev))) return LOCA_E_ARG;
+  if ((nb * n_lambda > 1 && m_bstride < d * kp) || (nb > 1 && (r_bstride < kp * d || k_bstride < d * k)))
+    return LOCA_E_ARG;
+  if (kp > 64 || n_lambda > kMaxLambdas) return LOCA_E_UNSUPPORTED;
+  if (nb > 65535 || nb * n_lambda > 65535) return LOCA_E_UNSUPPORTED;
+  loca_status st = check_ws(ws, ws_bytes, realization_error_ws(nb, d, k, r_prev, n_lambda));
+  if (st != LOCA_OK) return st;
+  FitArgs a{(hipStream_t)stream, nb, d, k, r_prev, m, m_bstride, r, r_bstride, K, acc, k_bstride, lp, lp_bstride,
+            mb_log, n_mb, lambdas, n_lambda, out, (char*)ws};
+  return from_hip(launch_realization_error(a));
 }
 
 loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int64_t k, int64_t d, const float* y,

@@ -371,6 +371,22 @@ struct CalibArgs {
   int32_t* dev_info; char* ws;
 };
 size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
+
+// Realisation error of the fitted adapters (Section S6).
+struct FitArgs {
+  hipStream_t stream;
+  int64_t nb, d, k, r_prev;
+  const float* m; int64_t m_bstride;
+  const float* r; int64_t r_bstride;
+  const void* K; loca_dtype acc; int64_t k_bstride;
+  const float* lp; int64_t lp_bstride;
+  const loca_mb* mb_log; int64_t n_mb;
+  const double* lambdas; int64_t n_lambda;
+  double* out;
+  char* ws;
+};
+size_t realization_error_ws(int64_t nb, int64_t d, int64_t k, int64_t r_prev, int64_t n_lambda);
+hipError_t launch_realization_error(const FitArgs& a);
 hipError_t launch_feedback_fit(const CalibArgs& a);
 
 hipError_t launch_dense_targets(hipStream_t s, int64_t nb, int64_t n, int64_t k, int64_t d,

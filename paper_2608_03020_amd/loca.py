@@ -18,11 +18,12 @@ LOCA_OK, LOCA_E_ARG, LOCA_E_WORKSPACE, LOCA_E_HIP, LOCA_E_UNSUPPORTED = range(5)
 LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
 LOCA_INFO_NONFINITE = -1
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
- LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR) = range(8)
+ LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR,
+ LOCA_OP_REALIZATION_ERROR) = range(9)
 
 ENTRY_POINTS = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_top_error",
-                "loca_credit_from_top_error", "loca_error_targets_noalloc")
+                "loca_credit_from_top_error", "loca_error_targets_noalloc", "loca_realization_error")
 EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version",
                            "loca_error_targets_noalloc_max_bytes")
 
@@ -68,6 +69,8 @@ def load():
                                           _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
     lib.loca_ridge_solve_projected.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _I64,
                                                _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _SZ]
+    lib.loca_realization_error.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _VP, _I, _I64, _VP,
+                                           _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
     lib.loca_dense_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _VP, _I64, _VP, _I64]
     lib.loca_feedback_fit.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _D, _VP, _I, _I64, _VP, _I64,
                                       _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
@@ -284,6 +287,22 @@ def loca_credit_from_top_error(e, credit_v, credit_b, y_out, mb_out, ws, *, a_w=
                                            _ptr(y_out), y_out.stride(0), _ptr(mb_out), _ptr(ws),
                                            ws.numel() * ws.element_size())
     _check("loca_credit_from_top_error", st)
+
+
+def loca_realization_error(m, r, K, lambdas: Sequence[float], mb_log, out, ws, *, lp=None, stream=None):
+    """m (nb, n_lambda, d, kp) from loca_ridge_solve; r (nb, kp, d) = [Rp; B~]; K (nb, d, k);
+    mb_log (n_mb, nb, 4) float64, the micro-batch records of the step; out (nb * n_lambda * 3,)
+    float64: per (block, lambda) ||E_fit||^2, ||T||^2, ||W||^2; lp (nb, d, r_prev) or None."""
+    nb, nl, d, kp = m.shape
+    k = K.shape[-1]
+    r_prev = 0 if lp is None else lp.shape[-1]
+    assert kp == r_prev + k and mb_log.shape[1] == nb
+    lam = (ctypes.c_double * len(lambdas))(*[float(v) for v in lambdas])
+    st = load().loca_realization_error(
+        _stream(stream), nb, d, k, r_prev, _ptr(m), m.stride(1), _ptr(r), r.stride(0), _ptr(K), _dtype(K),
+        K.stride(0), _ptr(lp), lp.stride(0) if lp is not None else 0, _ptr(mb_log), mb_log.shape[0],
+        ctypes.cast(lam, ctypes.c_void_p), len(lambdas), _ptr(out), _ptr(ws), ws.numel() * ws.element_size())
+    _check("loca_realization_error", st)
 
 
 def loca_dense_targets(y, mb, credit_b, t_out, *, stream=None):

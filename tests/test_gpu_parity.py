@@ -415,12 +415,25 @@ def test_outer_step_with_current_adapter(mode):
     step.reset()
     for m in range(cfg.n_micro):
         lo, hi = cfg.micro_rows(m)
-        step.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B)
-    step.solve(B, lp=to_dev(np.stack(Lps), dev), rp=to_dev(np.stack(Rps), dev))
+        step.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B, keep_log=True)
+    lp_d, rp_d = to_dev(np.stack(Lps), dev), to_dev(np.stack(Rps), dev)
+    step.solve(B, lp=lp_d, rp=rp_d)
     torch.cuda.synchronize()
     assert np.all(step.info.cpu().numpy() == 0), step.info.cpu().numpy()
     M = step.M.double().cpu().numpy()
     nl = len(cfg.lambdas)
+    kp = r_prev + cfg.k
+    fit = None
+    if kp <= 64:  # the realisation error of the fitted adapters (Section S6)
+        from paper_2608_03020_amd import loca
+        fit = torch.full((len(blocks) * nl * 3,), float("nan"), dtype=torch.float64, device=dev)
+        ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_REALIZATION_ERROR, len(blocks), 0, cfg.d, cfg.k,
+                                                      r_a=r_prev, n_lambda=nl), dev)
+        ws.fill_(255)
+        right = torch.cat([rp_d, B], dim=1).contiguous()
+        loca.loca_realization_error(step.M, right, step.K, cfg.lambdas, torch.stack(step.mb_log).contiguous(), fit,
+                                    ws, lp=lp_d)
+        fit = fit.cpu().numpy().reshape(len(blocks), nl, 3)
     for b in blocks:
         Wp = Lps[b].astype(np.float64) @ Rps[b].astype(np.float64)
         o = oracle.block_step(xf[b], zf, ys, gen.as_f64(As[b], cfg.a_dtype), np.asarray(Bs[b], np.float64), cfg.eta,
@@ -434,8 +447,66 @@ def test_outer_step_with_current_adapter(mode):
             Wr_gpu = step.A_ad[mi].double().cpu().numpy().T @ step.B_ad[mi].double().cpu().numpy().T
             sig_gpu = step.sigma[mi].double().cpu().numpy()
             e = {"W": rel(W_gpu, W_ref), "W_r": rel(Wr_gpu, Wr_ref), "sigma": rel(sig_gpu[:cfg.r_a], sig_ref[:cfg.r_a])}
+            if fit is not None:
+                ref = oracle.realization_error(np.concatenate(xf[b]), np.concatenate(o["T"]), W_ref, Wp)
+                e["fit2"] = abs(fit[b, l, 0] - ref["fit2"]) / ref["fit2"]
+                e["tar2"] = abs(fit[b, l, 1] - ref["tar2"]) / ref["tar2"]
+                e["w2"] = abs(fit[b, l, 2] - ref["w2"]) / ref["w2"]
             log(f"outer_step {mode} block {b} lambda {cfg.lambdas[l]}: " +
                 ", ".join(f"{k} {v:.2e}" for k, v in e.items()))
+            assert max(e.values()) <= tol, e
+
+
+@pytest.mark.parametrize("mode", ["bf16", "fp32"])
+def test_realization_error_frozen_step_with_weights(mode):
+    """Realisation error (Section S6) after the first outer step, with statistic weights
+    (20% of positions at a_t = 0): sum_n a_n ||E_fit,n||^2, ||T||^2 and ||W||^2 from the
+    factors against the oracle's dense E_fit = X W - T."""
+    import torch
+    import oracle
+    from paper_2608_03020_amd import loca
+    from paper_2608_03020_amd.step import BlockStep
+    if mode == "bf16":
+        cfg = gen.custom_config("t15", blocks=3, d=1040, n=2600, micro=1000, C=5, k=32, r_a=16,
+                                lambdas=(1e-3, 1e-1))
+        tol = 2e-3
+    else:
+        cfg = gen.custom_config("t15f", blocks=2, d=180, n=400, micro=150, C=4, k=12, r_a=6, lambdas=(1e-2,),
+                                mode="fp32", x_dist="gauss_outlier")
+        tol = 1e-5
+    nb, nl = cfg.blocks, len(cfg.lambdas)
+    log(f"case realisation {mode}: d={cfg.d} n={cfg.n} k={cfg.k} blocks={nb}")
+    xs, zs, ys, As, Bs = host_inputs(cfg, range(nb))
+    aw = [gen.gen_stat_weights(cfg, m) for m in range(cfg.n_micro)]
+    step = BlockStep(cfg, nb, poison=True)
+    x_all = padded_rows(np.stack([np.concatenate(xb) for xb in xs]))
+    z_all, y_all = to_dev(np.concatenate(zs)), to_dev(np.concatenate(ys))
+    a_all = to_dev(np.concatenate(aw))
+    A, B = to_dev(np.stack(As)), to_dev(np.stack(Bs))
+    step.reset()
+    for m in range(cfg.n_micro):
+        lo, hi = cfg.micro_rows(m)
+        step.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B, keep_log=True, a=a_all[lo:hi])
+    step.solve(B)
+    fit = torch.full((nb * nl * 3,), float("nan"), dtype=torch.float64, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_REALIZATION_ERROR, nb, 0, cfg.d, cfg.k,
+                                                  n_lambda=nl))
+    ws.fill_(255)
+    loca.loca_realization_error(step.M, B, step.K, cfg.lambdas, torch.stack(step.mb_log).contiguous(), fit, ws)
+    torch.cuda.synchronize()
+    assert np.all(step.info.cpu().numpy() == 0)
+    fit = fit.cpu().numpy().reshape(nb, nl, 3)
+    xmode = "f32" if mode == "fp32" else "bf16"
+    for b in range(nb):
+        xf = [gen.as_f64(x, xmode) for x in xs[b]]
+        o = oracle.block_step(xf, [gen.as_f64(z, cfg.logit_dtype) for z in zs], ys, gen.as_f64(As[b], cfg.a_dtype),
+                              np.asarray(Bs[b], np.float64), cfg.eta, cfg.lambdas, cfg.r_a, a_ws=aw)
+        for l in range(nl):
+            ref = oracle.realization_error(np.concatenate(xf), np.concatenate(o["T"]), o["solves"][l]["W"],
+                                           a=np.concatenate(aw))
+            e = {q: abs(fit[b, l, i] - ref[q]) / ref[q] for i, q in enumerate(("fit2", "tar2", "w2"))}
+            log(f"realisation {mode} block {b} lambda {cfg.lambdas[l]}: fit2/tar2 {ref['fit2'] / ref['tar2']:.3f}, " +
+                ", ".join(f"{q} {v:.2e}" for q, v in e.items()))
             assert max(e.values()) <= tol, e
 
 
