@@ -31,12 +31,13 @@ HBM_PEAK_GBS = 8000.0
 #   bench.py --config <cfg> --steps 1 --warmup 0 --no-cpu-baseline,
 # each scaled by the factor the same counter gives for a plain device copy in the same run
 # (the bf16 stack of the inputs, 2 * N * d bytes read and written per block): 1.0 for both.
-# Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h).
+# Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
+# kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 2796235.4, "write_kib": 775783.9, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "383271194106ee5d"},
-    "c5": {"fetch_kib": 20548760.1, "write_kib": 2652752.6, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "383271194106ee5d"},
+    "c3": {"fetch_kib": 2844570.9, "write_kib": 777729.5, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "dced4c501bdce7f0"},
+    "c5": {"fetch_kib": 19734767.8, "write_kib": 2655246.3, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "dced4c501bdce7f0"},
 }
 
 

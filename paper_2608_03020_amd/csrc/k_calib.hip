@@ -17,7 +17,7 @@
 //
 // The realisation error of a fitted adapter (Section S6) is also here: it needs the same
 // fixed-order products of tall d x (<= 64) operands.
-#include "loca_common.h"
+#include "loca_launch.h"
 
 namespace loca {
 

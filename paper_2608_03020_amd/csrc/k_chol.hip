@@ -18,7 +18,7 @@
 // The first non-positive pivot is reported in dev_info (1-based).
 #include <mutex>
 
-#include "loca_common.h"
+#include "loca_launch.h"
 #include "loca_bf16.h"
 
 #include <functional>

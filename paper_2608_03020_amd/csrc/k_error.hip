@@ -15,7 +15,7 @@
 // kernel adds in a fixed order, so results are bitwise reproducible.
 #include <mutex>
 
-#include "loca_common.h"
+#include "loca_launch.h"
 
 namespace loca {
 

@@ -25,7 +25,7 @@
 // fp32 mode: X is fp32 and the statistics are fp64 (v_mfma_f64_16x16x4f64).
 #include <algorithm>
 
-#include "loca_common.h"
+#include "loca_launch.h"
 
 namespace loca {
 

@@ -19,7 +19,7 @@
 // group j / kc), so one launch forms Y_b = E A~_b for every block.
 #include <algorithm>
 
-#include "loca_common.h"
+#include "loca_launch.h"
 #include "loca_bf16.h"
 
 namespace loca {

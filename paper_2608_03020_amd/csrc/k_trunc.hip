@@ -13,7 +13,7 @@
 // for kp <= 64 with the eigenvectors and the kp x kp intermediates in LDS (fp64);
 // for 64 < kp <= 128 with the eigenvectors in LDS as floats (rotations computed in
 // fp64) and the kp x kp intermediates in the workspace.
-#include "loca_common.h"
+#include "loca_launch.h"
 
 namespace loca {
 
@@ -752,15 +752,19 @@ __global__ void k_proj_sa(int64_t d, int64_t r_a, const ST* __restrict__ S, int6
 // panel's rows of the symmetric S are staged 64 columns at a time: chunks right of the
 // diagonal straight from the stored upper triangle, chunks left of it as the transposes of
 // the stored tiles above the diagonal, the diagonal chunk mirrored in LDS; the chunk of
-// PA^T beside it.  Wave w forms the panel (64 x RA) over columns 16 w .. 16 w + 15 of every
-// chunk, and the four partial panels are added in a fixed order: deterministic.
+// PA^T beside it.  The next chunk's loads are issued before the current chunk's products
+// (16-byte loads when d % 4 == 0).  Wave w forms the panel (64 x RA) over columns
+// 16 w .. 16 w + 15 of every chunk, and the four partial panels are added in a fixed
+// order: deterministic.
 constexpr int kPS = 64;        // panel rows and chunk columns
 constexpr int kPSL = kPS + 1;  // LDS row stride (odd: column reads spread over the banks)
-template <int RA>
+template <int RA, bool V4>
 __global__ __launch_bounds__(256) void k_proj_sa_mfma(int64_t d, int64_t r_a, const float* __restrict__ S,
                                                       int64_t s_bstride, const float* __restrict__ PA,
                                                       int64_t pa_bstride, double* __restrict__ T1) {
   constexpr int NCB = RA / 32;
+  constexpr int SQ = kPS * kPS / 4 / 256;  // float4 groups of the S tile per thread
+  constexpr int AQ = RA * kPS / 4 / 256;   // ... of the PA tile
   __shared__ float sS[kPS * kPSL];   // [row i][column j] of the panel chunk
   __shared__ float sA[RA * kPSL];    // [adapter row a][column j]
   __shared__ float sRed[4][kPS][RA + 1];
@@ -778,25 +782,60 @@ __global__ __launch_bounds__(256) void k_proj_sa_mfma(int64_t d, int64_t r_a, co
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[rb][cb][r] = 0.f;
   const int nch = (int)((d + kPS - 1) / kPS);
-  for (int J = 0; J < nch; ++J) {
+  float4 vS[SQ], vA[AQ];
+  // group e of a tile: row e / 16, columns 4 (e % 16) .. + 3
+  auto load4 = [&](const float* base, int64_t row, int64_t col, int64_t rows_ok) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (row < rows_ok) {
+      if (V4) {
+        if (col < d) v = *(const float4*)(base + row * d + col);
+      } else {
+        v.x = col < d ? base[row * d + col] : 0.f;
+        v.y = col + 1 < d ? base[row * d + col + 1] : 0.f;
+        v.z = col + 2 < d ? base[row * d + col + 2] : 0.f;
+        v.w = col + 3 < d ? base[row * d + col + 3] : 0.f;
+      }
+    }
+    return v;
+  };
+  auto load = [&](int J) {  // stored tile rows r0.., columns c0.. (transposed when left of the diagonal)
     const int64_t j0 = (int64_t)J * kPS;
-    __syncthreads();  // the previous chunk is no longer read
-    // stored tile: rows r0.., columns c0.. of the upper triangle (transposed when left of the diagonal)
     const bool left = J < I;
     const int64_t r0 = left ? j0 : i0, c0 = left ? i0 : j0;
 #pragma unroll
-    for (int u = 0; u < kPS * kPS / 256; ++u) {
-      const int e = tid + 256 * u, rr = e / kPS, cc = e % kPS;
-      const int64_t gr = r0 + rr, gc = c0 + cc;
-      const float v = (gr < d && gc < d) ? Sb[gr * d + gc] : 0.f;
-      if (left) sS[cc * kPSL + rr] = v;
-      else sS[rr * kPSL + cc] = v;
+    for (int u = 0; u < SQ; ++u) {
+      const int e = tid + 256 * u;
+      vS[u] = load4(Sb, r0 + e / 16, c0 + 4 * (e % 16), d);
     }
 #pragma unroll
-    for (int u = 0; u < RA * kPS / 256; ++u) {
-      const int e = tid + 256 * u, a = e / kPS, cc = e % kPS;
-      sA[a * kPSL + cc] = (a < r_a && j0 + cc < d) ? Pb[(int64_t)a * d + j0 + cc] : 0.f;
+    for (int u = 0; u < AQ; ++u) {
+      const int e = tid + 256 * u;
+      vA[u] = load4(Pb, e / 16, j0 + 4 * (e % 16), r_a);
     }
+  };
+  load(0);
+  for (int J = 0; J < nch; ++J) {
+    __syncthreads();  // the previous chunk is no longer read
+    const bool left = J < I;
+#pragma unroll
+    for (int u = 0; u < SQ; ++u) {
+      const int e = tid + 256 * u, rr = e / 16, cc = 4 * (e % 16);
+      const float v[4] = {vS[u].x, vS[u].y, vS[u].z, vS[u].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (left) sS[(cc + q) * kPSL + rr] = v[q];
+        else sS[rr * kPSL + cc + q] = v[q];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < AQ; ++u) {
+      const int e = tid + 256 * u, a = e / 16, cc = 4 * (e % 16);
+      sA[a * kPSL + cc] = vA[u].x;
+      sA[a * kPSL + cc + 1] = vA[u].y;
+      sA[a * kPSL + cc + 2] = vA[u].z;
+      sA[a * kPSL + cc + 3] = vA[u].w;
+    }
+    if (J + 1 < nch) load(J + 1);  // in flight during this chunk's products
     __syncthreads();
     if (J == I) {  // diagonal chunk: only its upper triangle is stored; mirror it
 #pragma unroll
@@ -837,27 +876,46 @@ __global__ __launch_bounds__(256) void k_proj_sa_mfma(int64_t d, int64_t r_a, co
   }
 }
 
-// G[b] = PA T1 (r_a x r_a) and AK[b] = PA K (r_a x k), fp64.
+// G[b] = PA T1 (r_a x r_a) and AK[b] = PA K (r_a x k), fp64, in two passes: partial sums
+// over kProjSplit ranges of the rows (grid.z), then a fixed-order sum.
+constexpr int kProjSplit = 16;
 template <typename ST>
-__global__ void k_proj_small(int64_t d, int64_t k, int64_t r_a, const float* __restrict__ PA, int64_t pa_bstride,
-                             const double* __restrict__ T1, const ST* __restrict__ K, int64_t k_bstride,
-                             double* __restrict__ G, double* __restrict__ AK, float* __restrict__ g_out) {
-  const int64_t b = blockIdx.y;
+__global__ void k_proj_small_part(int64_t d, int64_t k, int64_t r_a, const float* __restrict__ PA,
+                                  int64_t pa_bstride, const double* __restrict__ T1, const ST* __restrict__ K,
+                                  int64_t k_bstride, double* __restrict__ part) {
+  const int64_t b = blockIdx.y, z = blockIdx.z;
+  const int64_t nout = r_a * r_a + r_a * k;
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= nout) return;
+  const int64_t chunk = (d + kProjSplit - 1) / kProjSplit;
+  const int64_t i0 = z * chunk, i1 = i0 + chunk < d ? i0 + chunk : d;
   const float* P = PA + b * pa_bstride;
+  double s = 0.0;
   if (e < r_a * r_a) {
     const int64_t a = e / r_a, c = e % r_a;
-    double s = 0.0;
-    for (int64_t i = 0; i < d; ++i) s += (double)P[a * d + i] * T1[b * d * r_a + i * r_a + c];
-    G[b * r_a * r_a + e] = s;
-    if (g_out) g_out[b * r_a * r_a + e] = (float)s;
-  } else if (e < r_a * r_a + r_a * k) {
+    const double* T = T1 + b * d * r_a;
+    for (int64_t i = i0; i < i1; ++i) s += (double)P[a * d + i] * T[i * r_a + c];
+  } else {
     const int64_t f = e - r_a * r_a;
     const int64_t a = f / k, c = f % k;
     const ST* Kb = K + b * k_bstride;
-    double s = 0.0;
-    for (int64_t i = 0; i < d; ++i) s += (double)P[a * d + i] * (double)Kb[i * k + c];
-    AK[b * r_a * k + f] = s;
+    for (int64_t i = i0; i < i1; ++i) s += (double)P[a * d + i] * (double)Kb[i * k + c];
+  }
+  part[(b * kProjSplit + z) * nout + e] = s;
+}
+__global__ void k_proj_small_sum(int64_t k, int64_t r_a, const double* __restrict__ part, double* __restrict__ G,
+                                 double* __restrict__ AK, float* __restrict__ g_out) {
+  const int64_t b = blockIdx.y;
+  const int64_t nout = r_a * r_a + r_a * k;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= nout) return;
+  double s = 0.0;
+  for (int z = 0; z < kProjSplit; ++z) s += part[(b * kProjSplit + z) * nout + e];
+  if (e < r_a * r_a) {
+    G[b * r_a * r_a + e] = s;
+    if (g_out) g_out[b * r_a * r_a + e] = (float)s;
+  } else {
+    AK[b * r_a * k + (e - r_a * r_a)] = s;
   }
 }
 
@@ -971,6 +1029,7 @@ __global__ void k_set_lams8(Lams8 l, double* out, int cnt) {
 
 size_t projected_ws(int64_t nb, int64_t d, int64_t k, int64_t r_a, int64_t n_lambda) {
   size_t s = align256(sizeof(double) * nb * d * r_a);  // T1
+  s += align256(sizeof(double) * nb * kProjSplit * (r_a * r_a + r_a * k));  // partials of G and AK
   s += align256(sizeof(double) * nb * r_a * r_a);      // G
   s += align256(sizeof(double) * nb * r_a * k);        // AK
   s += 256;                                            // lambdas
@@ -981,6 +1040,7 @@ size_t projected_ws(int64_t nb, int64_t d, int64_t k, int64_t r_a, int64_t n_lam
 hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
   char* p = a.ws;
   double* T1 = (double*)p; p += align256(sizeof(double) * a.nb * a.d * a.r_a);
+  double* gpart = (double*)p; p += align256(sizeof(double) * a.nb * kProjSplit * (a.r_a * a.r_a + a.r_a * a.k));
   double* G = (double*)p; p += align256(sizeof(double) * a.nb * a.r_a * a.r_a);
   double* AK = (double*)p; p += align256(sizeof(double) * a.nb * a.r_a * a.k);
   double* dlam = (double*)p; p += 256;
@@ -991,22 +1051,32 @@ hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
   const int64_t nm = a.nb * a.n_lambda;
   k_fill_zero<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
   dim3 g1((unsigned)((a.d * a.r_a + 255) / 256), (unsigned)a.nb);
-  dim3 g2((unsigned)((a.r_a * a.r_a + a.r_a * a.k + 255) / 256), (unsigned)a.nb);
+  dim3 g2((unsigned)((a.r_a * a.r_a + a.r_a * a.k + 255) / 256), (unsigned)a.nb, kProjSplit);
   if (a.acc == LOCA_F64) {
     k_proj_sa<double><<<g1, 256, 0, a.stream>>>(a.d, a.r_a, (const double*)a.S, a.s_bstride, a.proj_a, a.pa_bstride, T1);
-    k_proj_small<double><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1, (const double*)a.K,
-                                                   a.k_bstride, G, AK, a.g_out);
+    k_proj_small_part<double><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
+                                                        (const double*)a.K, a.k_bstride, gpart);
   } else {
     dim3 gp((unsigned)((a.d + kPS - 1) / kPS), (unsigned)a.nb);
-    if (a.r_a <= 32)
-      k_proj_sa_mfma<32><<<gp, 256, 0, a.stream>>>(a.d, a.r_a, (const float*)a.S, a.s_bstride, a.proj_a,
-                                                   a.pa_bstride, T1);
-    else
-      k_proj_sa_mfma<64><<<gp, 256, 0, a.stream>>>(a.d, a.r_a, (const float*)a.S, a.s_bstride, a.proj_a,
-                                                   a.pa_bstride, T1);
-    k_proj_small<float><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1, (const float*)a.K,
-                                                  a.k_bstride, G, AK, a.g_out);
+    const float* Sf = (const float*)a.S;
+    // 16-byte loads of S rows and PA rows need 16-byte aligned bases and strides
+    const bool v4 = a.d % 4 == 0 && ((uintptr_t)Sf % 16) == 0 && ((uintptr_t)a.proj_a % 16) == 0 &&
+                    a.s_bstride % 4 == 0 && a.pa_bstride % 4 == 0;
+#define LOCA_PROJ_SA(RA, V)                                                                                   \
+  k_proj_sa_mfma<RA, V><<<gp, 256, 0, a.stream>>>(a.d, a.r_a, Sf, a.s_bstride, a.proj_a, a.pa_bstride, T1)
+    if (a.r_a <= 32) {
+      if (v4) LOCA_PROJ_SA(32, true);
+      else LOCA_PROJ_SA(32, false);
+    } else {
+      if (v4) LOCA_PROJ_SA(64, true);
+      else LOCA_PROJ_SA(64, false);
+    }
+#undef LOCA_PROJ_SA
+    k_proj_small_part<float><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
+                                                       (const float*)a.K, a.k_bstride, gpart);
   }
+  dim3 g2s((unsigned)((a.r_a * a.r_a + a.r_a * a.k + 255) / 256), (unsigned)a.nb);
+  k_proj_small_sum<<<g2s, 256, 0, a.stream>>>(a.k, a.r_a, gpart, G, AK, a.g_out);
   k_proj_chol<<<(unsigned)nm, 64, 0, a.stream>>>(a.r_a, G, dlam, (int)a.n_lambda, Lw, a.dev_info);
   dim3 g3((unsigned)((a.d + 255) / 256), (unsigned)nm);
 #define LOCA_PROJ_ROWS(RA)                                                                                           \

@@ -3,7 +3,7 @@
 // reported synchronously and can be tested without a GPU.
 #include <new>
 
-#include "loca_common.h"
+#include "loca_launch.h"
 
 using namespace loca;
 
