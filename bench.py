@@ -124,8 +124,10 @@ def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, 
         aw = None if a_all is None else a_all[lo:hi]
         if error_record is not None:
             error_record[m].record(stream)
+        if m == 0:  # B~ B~^T once per step, shared by the micro-batches
+            loca.loca_credit_gram(B, step.G, step.ws)
         loca.loca_error_targets(z[lo:hi], y[lo:hi], A, B, yv, step.mb, step.info_err[m:m + 1], step.ws, a_w=aw,
-                                nb=nb)
+                                nb=nb, credit_gram=step.G)
         if record is not None:
             record[m][0].record(stream)
         loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws, a_w=aw,

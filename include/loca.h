@@ -85,7 +85,8 @@ typedef enum {
   LOCA_OP_FEEDBACK_FIT = 5,
   LOCA_OP_TOP_ERROR = 6,
   LOCA_OP_CREDIT_FROM_TOP_ERROR = 7,
-  LOCA_OP_REALIZATION_ERROR = 8
+  LOCA_OP_REALIZATION_ERROR = 8,
+  LOCA_OP_CREDIT_GRAM = 9
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -114,6 +115,9 @@ typedef void* loca_stream_t; /* hipStream_t */
  *       sum_q2 = sum_t a_t ||Q_t||^2 (the mean squares of Eq. 10 under the weights).
  * credit_a : per block C x k (F32 or BF16), stride a_bstride.
  * credit_b : per block k x d float, stride b_bstride.
+ * credit_gram : NULL, or B~ B~^T of every block as written by loca_credit_gram for the same
+ *     credit_b (the call then skips forming it; B~ is fixed for a whole step, so the
+ *     micro-batches after the first can share one).
  * y_out : per block n x k float, stride y_bstride.
  * e_out : n x C float, or NULL (the error rows, for tests).
  * mb_out : nb entries; sum_q2 and n are written, sum_x2 and eta_bar zeroed.
@@ -128,9 +132,20 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
                                int64_t ld_logits, const int32_t* labels, const float* w,
                                const float* a_w, const void* credit_a, loca_dtype a_dtype,
                                int64_t a_bstride,
-                               const float* credit_b, int64_t b_bstride, float* y_out,
-                               int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info,
-                               void* ws, size_t ws_bytes);
+                               const float* credit_b, int64_t b_bstride, const double* credit_gram,
+                               float* y_out, int64_t y_bstride, float* e_out, loca_mb* mb_out,
+                               int32_t* dev_info, void* ws, size_t ws_bytes);
+
+/* ---------------------------------------------------------------------------
+ * The credit Gram B~_b B~_b^T (k x k, fp64) of every block, the matrix through which
+ * loca_error_targets forms ||Q||^2 = sum_t Y_t (B~ B~^T) Y_t^T (Eq. 10's denominator), for
+ * callers that form it once per step and pass it to every micro-batch's call.
+ * g_out : per block ld x ld doubles, ld = loca_credit_gram_ld(k) (entries past k are zero).
+ * Workspace: LOCA_OP_CREDIT_GRAM with nb, d and k.  Limits: k <= 128.
+ * ------------------------------------------------------------------------- */
+loca_status loca_credit_gram(loca_stream_t stream, int64_t nb, int64_t k, int64_t d, const float* credit_b,
+                             int64_t b_bstride, double* g_out, void* ws, size_t ws_bytes);
+int64_t loca_credit_gram_ld(int64_t k);
 
 /* ---------------------------------------------------------------------------
  * loca_error_targets without a workspace, for callers that cannot allocate device
@@ -151,8 +166,8 @@ loca_status loca_error_targets_noalloc(loca_stream_t stream, int64_t nb, int64_t
                                        int64_t ld_logits, const int32_t* labels, const float* w,
                                        const float* a_w, const void* credit_a, loca_dtype a_dtype,
                                        int64_t a_bstride, const float* credit_b, int64_t b_bstride,
-                                       float* y_out, int64_t y_bstride, float* e_out, loca_mb* mb_out,
-                                       int32_t* dev_info);
+                                       const double* credit_gram, float* y_out, int64_t y_bstride,
+                                       float* e_out, loca_mb* mb_out, int32_t* dev_info);
 size_t loca_error_targets_noalloc_max_bytes(void);
 
 /* ---------------------------------------------------------------------------

@@ -226,7 +226,7 @@ template <typename LT, typename AT>
 __global__ __launch_bounds__(kLargeThreads) void k_error_large(
     int64_t n, int64_t C, int64_t k, const LT* __restrict__ logits, int64_t ld,
     const int32_t* __restrict__ labels, const float* __restrict__ w, const float* __restrict__ aw,
-    const AT* __restrict__ A, int64_t a_bstride, const double* __restrict__ G, float* __restrict__ y_out,
+    const AT* __restrict__ A, int64_t a_bstride, const double* __restrict__ G, int64_t ldg, float* __restrict__ y_out,
     int64_t y_bstride, float* __restrict__ ms_out, double* __restrict__ partial, int32_t* __restrict__ dev_info) {
   constexpr int LPT = kLargeLPT;
   __shared__ float sZ[kLargeTok][kLargeChunk];
@@ -303,10 +303,10 @@ __global__ __launch_bounds__(kLargeThreads) void k_error_large(
   }
   __syncthreads();
   if (t < n) {
-    const double* Gb = G + b * k * k;
+    const double* Gb = G + b * ldg * ldg;
     for (int a2 = ln; a2 < k; a2 += LPT) {
       double r = 0.0;
-      for (int c = 0; c < k; ++c) r += Gb[a2 * k + c] * (double)sY[tk][c];
+      for (int c = 0; c < k; ++c) r += Gb[a2 * ldg + c] * (double)sY[tk][c];
       qv += (double)sY[tk][a2] * r;
     }
     if (aw) qv *= (double)aw[t];  // statistic weight of the position
@@ -485,9 +485,8 @@ static bool use_product(const ErrorArgs& a) {
   return true;
 }
 
-// Row stride of G: the padded width of the register kernels (the small label-set kernel,
-// and ||Q||^2 of the product path for k <= 64), else k.  The workspace holds the widest.
-static bool g_padded(const ErrorArgs& a) { return use_small(a.C, a.k) || (use_product(a) && a.k <= kSmallMaxK); }
+// Row stride of G for every path: the padded width of the register kernels (16, 32 or 64)
+// for k <= 64, else k.
 static int64_t g_ld_max(int64_t k) { return k <= kSmallMaxK ? small_kb(k) : k; }
 
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k) {
@@ -524,7 +523,7 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
   } else {
     dim3 grid((unsigned)((a.n + kLargeTok - 1) / kLargeTok), (unsigned)a.nb);
     k_error_large<LT, AT><<<grid, kLargeThreads, 0, a.stream>>>(
-        a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, a.a_w, A, a.a_bstride, G, a.y_out, a.y_bstride,
+        a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, a.a_w, A, a.a_bstride, G, g_ld_max(a.k), a.y_out, a.y_bstride,
         a.e_out ? ms : nullptr, partial, a.dev_info);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -539,8 +538,10 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
 
 hipError_t launch_error_targets(const ErrorArgs& a) {
   char* p = a.ws;
-  double* G = (double*)p;
-  const int64_t lg = g_padded(a) ? small_kb(a.k) : a.k;
+  // B~ B~^T of every block, row stride g_ld_max(k) (zero past k): from the caller
+  // (loca_credit_gram) when given, else formed here
+  double* G = a.credit_gram ? (double*)a.credit_gram : (double*)p;
+  const int64_t lg = g_ld_max(a.k);
   p += align256(sizeof(double) * a.nb * g_ld_max(a.k) * g_ld_max(a.k));
   double* gpart = (double*)p;
   p += credit_gram_part_ws(a.nb, a.k);
@@ -550,7 +551,7 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   float* ms = use_small(a.C, a.k) ? nullptr : (float*)p;
 
   k_fill_i32<<<1, 64, 0, a.stream>>>(a.dev_info, 1, INT32_MAX);
-  launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G, lg);
+  if (!a.credit_gram) launch_credit_gram(a.stream, a.nb, a.k, a.d, a.credit_b, a.b_bstride, gpart, G, lg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_product(a)) {
@@ -562,7 +563,7 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
                           a.y_bstride, a.dev_info, pw};
     if ((e = launch_softmax_product(sp)) != hipSuccess) return e;
     dim3 gq((unsigned)((a.n + 255) / 256), (unsigned)a.nb);
-    if (!g_padded(a))
+    if (a.k > kSmallMaxK)
       k_q2_rows<<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
     else if (lg == 16)
       k_q2_rows_kb<16><<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
@@ -589,6 +590,14 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   if (!zb && ab) return dispatch_error<float, uint16_t>(a, G, partial, ms);
   if (zb && !ab) return dispatch_error<uint16_t, float>(a, G, partial, ms);
   return dispatch_error<uint16_t, uint16_t>(a, G, partial, ms);
+}
+
+int64_t credit_gram_ld(int64_t k) { return g_ld_max(k); }
+size_t credit_gram_ws(int64_t nb, int64_t k) { return credit_gram_part_ws(nb, k); }
+hipError_t launch_credit_gram_only(hipStream_t st, int64_t nb, int64_t k, int64_t d, const float* B,
+                                   int64_t b_bstride, double* G, char* ws) {
+  launch_credit_gram(st, nb, k, d, B, b_bstride, (double*)ws, G, g_ld_max(k));
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ allocation-free variant

@@ -60,6 +60,7 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
     case LOCA_OP_FEEDBACK_FIT: return d < 1 || n < 1 || n > 64 ? 0 : feedback_fit_ws(nb, d, n, k);
     case LOCA_OP_TOP_ERROR: return n < 1 || d < 1 || C < 1 ? 0 : top_error_ws(n, C, d);
     case LOCA_OP_CREDIT_FROM_TOP_ERROR: return n < 1 ? 0 : credit_from_top_error_ws(nb, n, k);
+    case LOCA_OP_CREDIT_GRAM: return d < 1 ? 0 : credit_gram_ws(nb, k);
     case LOCA_OP_REALIZATION_ERROR:
       return d < 1 || n_lambda < 1 || r_a < 0 ? 0 : realization_error_ws(nb, d, k, r_a, n_lambda);
   }
@@ -86,7 +87,8 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
                                const void* logits, loca_dtype logits_dtype, int64_t ld_logits,
                                const int32_t* labels, const float* w, const float* a_w, const void* credit_a,
                                loca_dtype a_dtype,
-                               int64_t a_bstride, const float* credit_b, int64_t b_bstride, float* y_out,
+                               int64_t a_bstride, const float* credit_b, int64_t b_bstride,
+                               const double* credit_gram, float* y_out,
                                int64_t y_bstride, float* e_out, loca_mb* mb_out, int32_t* dev_info, void* ws,
                                size_t ws_bytes) {
   loca_status st = check_error_args(nb, n, C, k, d, logits, logits_dtype, ld_logits, labels, credit_a, a_dtype,
@@ -95,15 +97,28 @@ loca_status loca_error_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
   st = check_ws(ws, ws_bytes, error_targets_ws(nb, n, C, k));
   if (st != LOCA_OK) return st;
   ErrorArgs a{(hipStream_t)stream, nb, n, C, k, d, ld_logits, logits, logits_dtype, labels, w, a_w, credit_a, a_dtype,
-              a_bstride, credit_b, b_bstride, y_out, y_bstride, e_out, mb_out, dev_info, (char*)ws};
+              a_bstride, credit_b, b_bstride, credit_gram, y_out, y_bstride, e_out, mb_out, dev_info, (char*)ws};
   return from_hip(launch_error_targets(a));
+}
+
+int64_t loca_credit_gram_ld(int64_t k) { return k < 1 ? 0 : credit_gram_ld(k); }
+
+loca_status loca_credit_gram(loca_stream_t stream, int64_t nb, int64_t k, int64_t d, const float* credit_b,
+                             int64_t b_bstride, double* g_out, void* ws, size_t ws_bytes) {
+  if (nb < 1 || k < 1 || d < 1 || !credit_b || !g_out) return LOCA_E_ARG;
+  if (nb > 1 && b_bstride < k * d) return LOCA_E_ARG;
+  if (k > kMaxK || nb > 65535) return LOCA_E_UNSUPPORTED;
+  loca_status st = check_ws(ws, ws_bytes, credit_gram_ws(nb, k));
+  if (st != LOCA_OK) return st;
+  return from_hip(launch_credit_gram_only((hipStream_t)stream, nb, k, d, credit_b, b_bstride, g_out, (char*)ws));
 }
 
 loca_status loca_error_targets_noalloc(loca_stream_t stream, int64_t nb, int64_t n, int64_t C, int64_t k, int64_t d,
                                        const void* logits, loca_dtype logits_dtype, int64_t ld_logits,
                                        const int32_t* labels, const float* w, const float* a_w,
                                        const void* credit_a, loca_dtype a_dtype, int64_t a_bstride,
-                                       const float* credit_b, int64_t b_bstride, float* y_out, int64_t y_bstride,
+                                       const float* credit_b, int64_t b_bstride, const double* credit_gram,
+                                       float* y_out, int64_t y_bstride,
                                        float* e_out, loca_mb* mb_out, int32_t* dev_info) {
   loca_status st = check_error_args(nb, n, C, k, d, logits, logits_dtype, ld_logits, labels, credit_a, a_dtype,
                                     a_bstride, credit_b, b_bstride, y_out, y_bstride, mb_out, dev_info);
@@ -112,7 +127,8 @@ loca_status loca_error_targets_noalloc(loca_stream_t stream, int64_t nb, int64_t
   void* scratch_ptr = nullptr;
   if (error_targets_scratch(&scratch_ptr) != hipSuccess) return LOCA_E_HIP;
   ErrorArgs a{(hipStream_t)stream, nb, n, C, k, d, ld_logits, logits, logits_dtype, labels, w, a_w, credit_a, a_dtype,
-              a_bstride, credit_b, b_bstride, y_out, y_bstride, e_out, mb_out, dev_info, (char*)scratch_ptr};
+              a_bstride, credit_b, b_bstride, credit_gram, y_out, y_bstride, e_out, mb_out, dev_info,
+              (char*)scratch_ptr};
   return from_hip(launch_error_targets(a));
 }
 

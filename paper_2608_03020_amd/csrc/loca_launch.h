@@ -13,11 +13,16 @@ struct ErrorArgs {
   const int32_t* labels; const float* w; const float* a_w;
   const void* credit_a; loca_dtype a_dtype; int64_t a_bstride;
   const float* credit_b; int64_t b_bstride;
+  const double* credit_gram;  // B~ B~^T per block (loca_credit_gram), or null
   float* y_out; int64_t y_bstride;
   float* e_out; loca_mb* mb_out; int32_t* dev_info;
   char* ws;
 };
 size_t error_targets_ws(int64_t nb, int64_t n, int64_t C, int64_t k);
+int64_t credit_gram_ld(int64_t k);
+size_t credit_gram_ws(int64_t nb, int64_t k);
+hipError_t launch_credit_gram_only(hipStream_t st, int64_t nb, int64_t k, int64_t d, const float* B,
+                                   int64_t b_bstride, double* G, char* ws);
 hipError_t launch_error_targets(const ErrorArgs& a);
 // the fixed scratch array of loca_error_targets_noalloc: its size, and its address on the
 // current device (looked up on the first call on that device)

@@ -19,13 +19,14 @@ LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
 LOCA_INFO_NONFINITE = -1
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
  LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR,
- LOCA_OP_REALIZATION_ERROR) = range(9)
+ LOCA_OP_REALIZATION_ERROR, LOCA_OP_CREDIT_GRAM) = range(10)
 
 ENTRY_POINTS = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_top_error",
-                "loca_credit_from_top_error", "loca_error_targets_noalloc", "loca_realization_error")
+                "loca_credit_from_top_error", "loca_error_targets_noalloc", "loca_realization_error",
+                "loca_credit_gram")
 EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version",
-                           "loca_error_targets_noalloc_max_bytes")
+                           "loca_error_targets_noalloc_max_bytes", "loca_credit_gram_ld")
 
 
 class LocaMB(ctypes.Structure):
@@ -56,9 +57,12 @@ def load():
         raise RuntimeError(f"libloca is not built ({LIB_PATH}); run paper_2608_03020_amd/build.py")
     lib = ctypes.CDLL(LIB_PATH)
     lib.loca_error_targets.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _VP, _I,
-                                       _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
+                                       _I64, _VP, _I64, _VP, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_error_targets_noalloc.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _VP,
-                                               _I, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP]
+                                               _I, _I64, _VP, _I64, _VP, _VP, _I64, _VP, _VP, _VP]
+    lib.loca_credit_gram.argtypes = [_VP, _I64, _I64, _I64, _VP, _I64, _VP, _VP, _SZ]
+    lib.loca_credit_gram_ld.argtypes = [_I64]
+    lib.loca_credit_gram_ld.restype = _I64
     lib.loca_error_targets_noalloc_max_bytes.argtypes = []
     lib.loca_error_targets_noalloc_max_bytes.restype = _SZ
     lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _VP, _D,
@@ -159,22 +163,43 @@ def mb_view(mb):
 
 
 def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_info, ws, *, w=None, a_w=None,
-                       e_out=None, nb=None, stream=None):
+                       e_out=None, nb=None, credit_gram=None, stream=None):
     """logits (n, C); labels (n,); credit_a (nb, C, k); credit_b (nb, k, d); y_out (nb, n, k);
-    w (n,) loss weights and a_w (n,) statistic weights, float32, optional."""
+    w (n,) loss weights and a_w (n,) statistic weights, float32, optional; credit_gram: B~ B~^T
+    from loca_credit_gram (optional)."""
     nb = nb or credit_a.shape[0]
     n, C = logits.shape[0], logits.shape[1]
     k, d = credit_b.shape[-2], credit_b.shape[-1]
     st = load().loca_error_targets(
         _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
         _ptr(a_w), _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
-        credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(y_out), y_out.stride(0) if y_out.dim() == 3 else 0,
-        _ptr(e_out), _ptr(mb_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
+        credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(credit_gram), _ptr(y_out),
+        y_out.stride(0) if y_out.dim() == 3 else 0, _ptr(e_out), _ptr(mb_out), _ptr(dev_info), _ptr(ws),
+        ws.numel() * ws.element_size())
     _check("loca_error_targets", st)
 
 
+def credit_gram_ld(k: int) -> int:
+    return int(load().loca_credit_gram_ld(k))
+
+
+def new_credit_gram(nb: int, k: int, device="cuda"):
+    """Device buffer for loca_credit_gram: (nb, ld, ld) float64, ld = credit_gram_ld(k)."""
+    import torch
+    ld = credit_gram_ld(k)
+    return torch.zeros((nb, ld, ld), dtype=torch.float64, device=device)
+
+
+def loca_credit_gram(credit_b, g_out, ws, *, stream=None):
+    """credit_b (nb, k, d) float32 -> g_out (nb, ld, ld) float64 = B~ B~^T per block."""
+    nb, k, d = credit_b.shape
+    st = load().loca_credit_gram(_stream(stream), nb, k, d, _ptr(credit_b), credit_b.stride(0), _ptr(g_out), _ptr(ws),
+                                 ws.numel() * ws.element_size())
+    _check("loca_credit_gram", st)
+
+
 def loca_error_targets_noalloc(logits, labels, credit_a, credit_b, y_out, mb_out, dev_info, *, w=None, a_w=None,
-                               e_out=None, nb=None, stream=None):
+                               e_out=None, nb=None, credit_gram=None, stream=None):
     """loca_error_targets with the library's fixed scratch array instead of a workspace."""
     nb = nb or credit_a.shape[0]
     n, C = logits.shape[0], logits.shape[1]
@@ -182,8 +207,8 @@ def loca_error_targets_noalloc(logits, labels, credit_a, credit_b, y_out, mb_out
     st = load().loca_error_targets_noalloc(
         _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
         _ptr(a_w), _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
-        credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(y_out), y_out.stride(0) if y_out.dim() == 3 else 0,
-        _ptr(e_out), _ptr(mb_out), _ptr(dev_info))
+        credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(credit_gram), _ptr(y_out),
+        y_out.stride(0) if y_out.dim() == 3 else 0, _ptr(e_out), _ptr(mb_out), _ptr(dev_info))
     _check("loca_error_targets_noalloc", st)
 
 

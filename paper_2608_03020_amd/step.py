@@ -35,6 +35,7 @@ class BlockStep:
         self.K = torch.zeros((nb, d, k), dtype=acc_t, device=device)
         self.Y = torch.empty((nb, n_mb, k), dtype=torch.float32, device=device)
         self.mb = loca.new_mb(nb, device)
+        self.G = loca.new_credit_gram(nb, k, device)  # B~ B~^T, formed once per step
         self.mb_log: List = []
         # one dev_info slice per call, so that no call's codes overwrite another's: the head
         # error of every micro-batch, the statistics of every (micro-batch, block), the solve,
@@ -93,8 +94,10 @@ class BlockStep:
         if m >= self.cfg.n_micro:
             raise ValueError(f"more than {self.cfg.n_micro} micro-batches since reset()")
         self._m += 1
+        if m == 0:  # B~ is fixed for the step: its Gram serves every micro-batch
+            loca.loca_credit_gram(credit_b, self.G, self.ws, stream=stream)
         loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info_err[m:m + 1], self.ws,
-                                w=w, a_w=a, nb=self.nb, stream=stream)
+                                w=w, a_w=a, nb=self.nb, credit_gram=self.G, stream=stream)
         loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, a_w=a,
                                    dev_info=self.info_stats[m], stream=stream)
         if keep_log:

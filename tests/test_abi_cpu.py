@@ -67,7 +67,7 @@ def test_error_targets_rejects(lib):
         a = dict(ok_args, **kw)
         return so.loca_error_targets(a["stream"], a["nb"], a["n"], a["C"], a["k"], a["d"], a["logits"], a["ldt"],
                                      a["ld"], a["labels"], a["w"], a["aw"], a["a"], a["adt"], a["abs_"], a["b"], a["bbs"],
-                                     a["y"], a["ybs"], a["e"], a["mb"], a["info"], a["ws"], a["wsb"])
+                                     None, a["y"], a["ybs"], a["e"], a["mb"], a["info"], a["ws"], a["wsb"])
 
     assert call(n=0) == lib.LOCA_E_ARG
     assert call(C=0) == lib.LOCA_E_ARG
@@ -87,7 +87,7 @@ def test_error_targets_noalloc_rejects(lib):
 
     def call(nb=1, n=8, C=4, k=2, d=16, logits=FAKE, info=FAKE):
         return so.loca_error_targets_noalloc(None, nb, n, C, k, d, logits, lib.LOCA_F32, C, FAKE, None, None, FAKE,
-                                             lib.LOCA_F32, 0, FAKE, 0, FAKE, 0, None, FAKE, info)
+                                             lib.LOCA_F32, 0, FAKE, 0, None, FAKE, 0, None, FAKE, info)
 
     assert call(n=0) == lib.LOCA_E_ARG
     assert call(logits=None) == lib.LOCA_E_ARG
@@ -97,6 +97,16 @@ def test_error_targets_noalloc_rejects(lib):
     assert lib.error_targets_noalloc_max_bytes() == 16 << 20
     big = lib.workspace_size(lib.LOCA_OP_ERROR_TARGETS, 48, 65536, 5120, 64, 5)
     assert big <= lib.error_targets_noalloc_max_bytes()  # the largest small-label workload fits
+
+
+def test_credit_gram_rejects_and_layout(lib):
+    so = lib.load()
+    assert [lib.credit_gram_ld(k) for k in (1, 16, 17, 32, 33, 64, 65, 128)] == [16, 16, 32, 32, 64, 64, 65, 128]
+    assert so.loca_credit_gram(None, 1, 0, 16, FAKE, 0, FAKE, None, 0) == lib.LOCA_E_ARG
+    assert so.loca_credit_gram(None, 1, 4, 16, None, 0, FAKE, None, 0) == lib.LOCA_E_ARG
+    assert so.loca_credit_gram(None, 2, 4, 16, FAKE, 8, FAKE, None, 0) == lib.LOCA_E_ARG   # block stride < k d
+    assert so.loca_credit_gram(None, 1, 129, 16, FAKE, 0, FAKE, None, 0) == lib.LOCA_E_UNSUPPORTED
+    assert so.loca_credit_gram(None, 1, 4, 16, FAKE, 0, FAKE, None, 0) == lib.LOCA_E_WORKSPACE
 
 
 def test_accumulate_stats_rejects(lib):

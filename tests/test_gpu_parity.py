@@ -323,6 +323,52 @@ def test_tiny_width_and_single_token():
         assert abs(loca.mb_view(mb)["eta_bar"][0] - eb) < 1e-6 * eb
 
 
+@pytest.mark.parametrize("C,k,ldt,adt", [(5, 32, "f32", "f32"), (4, 5, "f32", "f32"), (3001, 24, "f32", "f32"),
+                                         (3001, 32, "bf16", "bf16"), (3001, 96, "bf16", "bf16"), (70, 72, "f32", "bf16")])
+def test_precomputed_credit_gram_gives_the_same_bits(C, k, ldt, adt):
+    """loca_error_targets with B~ B~^T from loca_credit_gram equals the call that forms it,
+    bit for bit, on every path (small label sets, the streaming kernel, the vocabulary
+    product with k <= 64 and k > 64) and padded Gram widths (k = 5, 24, 72)."""
+    import torch
+    from paper_2608_03020_amd import loca
+    n, d, nb = 700, 200, 3
+    g = torch.Generator(device="cuda")
+    g.manual_seed(C + k)
+    zt = torch.bfloat16 if ldt == "bf16" else torch.float32
+    ld = (C + 7) // 8 * 8
+    zbuf = torch.zeros((n, ld), device="cuda", dtype=zt)
+    zbuf[:, :C] = (torch.randn((n, C), generator=g, device="cuda") * 2).to(zt)
+    z = zbuf[:, :C]
+    y = torch.randint(0, C, (n,), generator=g, device="cuda", dtype=torch.int32)
+    A = (torch.randn((nb, C, k), generator=g, device="cuda") / np.sqrt(k)).to(
+        torch.bfloat16 if adt == "bf16" else torch.float32)
+    B = torch.randn((nb, k, d), generator=g, device="cuda") / np.sqrt(k)
+    aw = torch.rand(n, generator=g, device="cuda")
+    ws = loca.alloc_workspace(max(loca.workspace_size(loca.LOCA_OP_ERROR_TARGETS, nb, n, d, k, C),
+                                  loca.workspace_size(loca.LOCA_OP_CREDIT_GRAM, nb, 0, d, k)))
+    G = loca.new_credit_gram(nb, k)
+    G.fill_(float("nan"))
+    loca.loca_credit_gram(B, G, ws)
+    out = []
+    for gram in (None, G):
+        Y = torch.full((nb, n, k), float("nan"), device="cuda")
+        mb = loca.new_mb(nb)
+        info = torch.full((1,), 5, dtype=torch.int32, device="cuda")
+        loca.loca_error_targets(z, y, A, B, Y, mb, info, ws, a_w=aw, credit_gram=gram)
+        torch.cuda.synchronize()
+        assert info.item() == 0
+        out.append((Y.cpu().numpy(), mb.cpu().numpy()))
+    assert not np.isnan(out[1][0]).any()
+    assert np.array_equal(out[0][0], out[1][0]) and np.array_equal(out[0][1], out[1][1])
+    Gh = G.cpu().numpy()
+    ldg = Gh.shape[-1]
+    Bh = B.double().cpu().numpy()
+    for b in range(nb):
+        ref = Bh[b] @ Bh[b].T
+        assert np.abs(Gh[b, :k, :k] - ref).max() <= 1e-12 * np.abs(ref).max()
+        assert np.all(Gh[b, k:, :] == 0) and np.all(Gh[b, :, k:] == 0) and ldg >= k
+
+
 def test_out_of_range_label_reported():
     import torch
     from paper_2608_03020_amd import loca
