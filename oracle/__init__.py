@@ -386,3 +386,60 @@ def block_step(xs: Sequence[np.ndarray], zs: Sequence[np.ndarray], ys: Sequence[
         out["G_proj"] = G
         out["C_proj"] = Cst
     return out
+
+
+# ---------------------------------------------------------------- outer iteration (Section S8)
+
+
+def linear_blocks_forward(h0, Fs, Ws, Wu):
+    """Forward pass of a synthetic network of L linear residual blocks (the frozen backbone
+    stand-in for the outer iteration): h_l = h_{l-1} (I + F_l) + h_{l-1} W_l, token-major,
+    where h_{l-1} (I + F_l) is the frozen block output and h_{l-1} W_l the adapter's
+    contribution (Eq. 1 in row form, W_l = (B_l A_l)^T); logits z = h_L W_u^T.  Returns the
+    block inputs [h_0 .. h_{L-1}] and z.  The products are library matmuls."""
+    h = _f64(h0)
+    xs = []
+    for F, W in zip(Fs, Ws):
+        xs.append(h)
+        h = h + h @ _f64(F) + (0.0 if W is None else h @ _f64(W))
+    return xs, h @ _f64(Wu).T
+
+
+def cross_entropy(z, y):
+    """Mean cross-entropy of logits z (n x C) against labels y."""
+    z = _f64(z)
+    m = z.max(axis=1, keepdims=True)
+    lse = m[:, 0] + np.log(np.exp(z - m).sum(axis=1))
+    return float(np.mean(lse - z[np.arange(z.shape[0]), np.asarray(y)]))
+
+
+def jacobi_outer_loop(h0, Fs, Wu, y, As, Bs, eta, lam, r_a, steps, micro):
+    """The outer iteration of Section S8 with the Jacobi schedule on the synthetic linear
+    network: at step t one shared forward pass with the current adapters W^(t) gives every
+    block's inputs and the head error; each block then solves its ridge problem with the
+    residual target of Eq. 6 (current adapter W_prev = W^(t)_l, Theorem S6.1) from the
+    statistics of all micro-batches of `micro` rows, and its solution is truncated to rank
+    r_a (the adapter's rank); all blocks are updated at once.  Returns per step the CE of
+    the forward pass it started from and the adapters after it."""
+    L = len(Fs)
+    d = _f64(h0).shape[1]
+    W = [np.zeros((d, d)) for _ in range(L)]
+    n = _f64(h0).shape[0]
+    rows = [(lo, min(n, lo + micro)) for lo in range(0, n, micro)]
+    hist = []
+    for _ in range(steps):
+        xs, z = linear_blocks_forward(h0, Fs, W, Wu)
+        loss = cross_entropy(z, y)
+        Wn = []
+        for l in range(L):
+            res = block_step([xs[l][lo:hi] for lo, hi in rows], [z[lo:hi] for lo, hi in rows],
+                             [np.asarray(y)[lo:hi] for lo, hi in rows], As[l], Bs[l], eta, (lam,), r_a,
+                             W_prev=W[l], dense_truncation=False)
+            Wr, _ = truncate_dense(res["solves"][0]["W"], r_a)
+            Wn.append(Wr)
+        W = Wn
+        hist.append({"loss": loss, "W": [w.copy() for w in W]})
+    xs, z = linear_blocks_forward(h0, Fs, W, Wu)
+    hist.append({"loss": cross_entropy(z, y), "W": None})
+    return hist
+

@@ -80,7 +80,7 @@ CONFIGS = {
 _CFG_ID = {"c1": 1, "c2": 2, "c3": 3, "c4": 4, "c5": 5}
 # tensor ids inside a (config, block) key
 (_T_X, _T_LOGITS, _T_LABELS, _T_A, _T_B, _T_OUTL, _T_SCALE, _T_ADAPT, _T_CURRENT, _T_WEIGHTS, _T_PROBE,
- _T_STATW) = range(12)
+ _T_STATW, _T_LINNET) = range(13)
 
 
 def custom_config(name="tiny", blocks=1, d=64, n=100, micro=None, C=5, k=8, r_a=4,
@@ -229,6 +229,20 @@ def gen_probe_pairs(cfg: LocaConfig, n_p: int, blocks: int, rank: int = 0, noise
                                                                                              dtype=np.float32))
                   .astype(np.float32))
     return E, np.stack(Gs)
+
+
+def gen_linear_network(cfg: LocaConfig, seed: int = 0, mix: float = 0.5):
+    """A synthetic network of cfg.blocks linear residual blocks, the frozen-backbone
+    stand-in of the outer-iteration tests: token features h0 (n x d, N(0,1)), block maps
+    F_l (d x d, N(0, mix^2/d)) with h_l = h_{l-1} (I + F_l), a head W_u (C x d, N(0, 4/d))
+    and labels.  float32 values (exact in float64 as well)."""
+    g = _rng(seed, cfg, 0, _T_LINNET)
+    n, d, L, C = cfg.n, cfg.d, cfg.blocks, cfg.C
+    h0 = g.standard_normal((n, d), dtype=np.float32)
+    Fs = g.standard_normal((L, d, d), dtype=np.float32) * np.float32(mix / np.sqrt(d))
+    Wu = g.standard_normal((C, d), dtype=np.float32) * np.float32(2.0 / np.sqrt(d))
+    y = g.integers(0, C, n).astype(np.int32)
+    return h0, Fs, Wu, y
 
 
 def as_f64(a: np.ndarray, dtype: str) -> np.ndarray:
