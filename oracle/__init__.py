@@ -413,14 +413,16 @@ def cross_entropy(z, y):
     return float(np.mean(lse - z[np.arange(z.shape[0]), np.asarray(y)]))
 
 
-def jacobi_outer_loop(h0, Fs, Wu, y, As, Bs, eta, lam, r_a, steps, micro):
+def jacobi_outer_loop(h0, Fs, Wu, y, As, Bs, eta, lam, r_a, steps, micro, f32_inputs=False):
     """The outer iteration of Section S8 with the Jacobi schedule on the synthetic linear
     network: at step t one shared forward pass with the current adapters W^(t) gives every
     block's inputs and the head error; each block then solves its ridge problem with the
     residual target of Eq. 6 (current adapter W_prev = W^(t)_l, Theorem S6.1) from the
     statistics of all micro-batches of `micro` rows, and its solution is truncated to rank
     r_a (the adapter's rank); all blocks are updated at once.  Returns per step the CE of
-    the forward pass it started from and the adapters after it."""
+    the forward pass it started from and the adapters after it.  With f32_inputs the block
+    inputs and logits of every forward pass are rounded to float32 before the step (the
+    values a float32 caller passes)."""
     L = len(Fs)
     d = _f64(h0).shape[1]
     W = [np.zeros((d, d)) for _ in range(L)]
@@ -430,6 +432,9 @@ def jacobi_outer_loop(h0, Fs, Wu, y, As, Bs, eta, lam, r_a, steps, micro):
     for _ in range(steps):
         xs, z = linear_blocks_forward(h0, Fs, W, Wu)
         loss = cross_entropy(z, y)
+        if f32_inputs:
+            xs = [x.astype(np.float32).astype(np.float64) for x in xs]
+            z = z.astype(np.float32).astype(np.float64)
         Wn = []
         for l in range(L):
             res = block_step([xs[l][lo:hi] for lo, hi in rows], [z[lo:hi] for lo, hi in rows],

@@ -109,11 +109,19 @@ def workspace_size(op: int, nb: int, n: int, d: int, k: int, C: int = 0, r_a: in
 # ------------------------------------------------------------------ marshalling helpers
 
 
-def _ptr(t) -> Optional[int]:
+def _ptr(t, rows: bool = True) -> Optional[int]:
+    """Device address of a tensor whose layout the C ABI describes: the last dimension
+    contiguous, and with rows=True (arrays passed without a leading dimension) rows packed
+    one after another.  Other layouts raise instead of being read with the wrong strides."""
     if t is None:
         return None
     if isinstance(t, int):
         return t
+    if t.dim() >= 1 and t.shape[-1] > 1 and t.stride(-1) != 1:
+        raise ValueError(f"tensor of shape {tuple(t.shape)} and strides {t.stride()}: last dimension not contiguous")
+    if rows and t.dim() >= 2 and t.shape[-2] > 1 and t.stride(-2) != t.shape[-1]:
+        raise ValueError(f"tensor of shape {tuple(t.shape)} and strides {t.stride()}: rows not packed "
+                         "(the C ABI takes this array without a row stride; pass a contiguous copy)")
     return t.data_ptr()
 
 
@@ -171,7 +179,7 @@ def loca_error_targets(logits, labels, credit_a, credit_b, y_out, mb_out, dev_in
     n, C = logits.shape[0], logits.shape[1]
     k, d = credit_b.shape[-2], credit_b.shape[-1]
     st = load().loca_error_targets(
-        _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
+        _stream(stream), nb, n, C, k, d, _ptr(logits, False), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
         _ptr(a_w), _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
         credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(credit_gram), _ptr(y_out),
         y_out.stride(0) if y_out.dim() == 3 else 0, _ptr(e_out), _ptr(mb_out), _ptr(dev_info), _ptr(ws),
@@ -205,7 +213,7 @@ def loca_error_targets_noalloc(logits, labels, credit_a, credit_b, y_out, mb_out
     n, C = logits.shape[0], logits.shape[1]
     k, d = credit_b.shape[-2], credit_b.shape[-1]
     st = load().loca_error_targets_noalloc(
-        _stream(stream), nb, n, C, k, d, _ptr(logits), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
+        _stream(stream), nb, n, C, k, d, _ptr(logits, False), _dtype(logits), logits.stride(0), _ptr(labels), _ptr(w),
         _ptr(a_w), _ptr(credit_a), _dtype(credit_a), credit_a.stride(0) if credit_a.dim() == 3 else 0, _ptr(credit_b),
         credit_b.stride(0) if credit_b.dim() == 3 else 0, _ptr(credit_gram), _ptr(y_out),
         y_out.stride(0) if y_out.dim() == 3 else 0, _ptr(e_out), _ptr(mb_out), _ptr(dev_info))
@@ -224,7 +232,7 @@ def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, dev_info=None, s
     k = y.shape[-1]
     acc = _dtype(S)
     st = load().loca_accumulate_stats(
-        _stream(stream), nb, n, d, k, _ptr(x), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), _ptr(a_w),
+        _stream(stream), nb, n, d, k, _ptr(x, False), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), _ptr(a_w),
         float(eta),
         _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), _ptr(dev_info), _ptr(ws),
         ws.numel() * ws.element_size())
@@ -296,8 +304,8 @@ def loca_top_error(logits, labels, wu, e_out, dev_info, ws, *, w=None, stream=No
     e_t = W_u^T w_t (softmax(z_t) - onehot(y_t))."""
     n, V = logits.shape
     d = wu.shape[1]
-    st = load().loca_top_error(_stream(stream), n, V, d, _ptr(logits), _dtype(logits), logits.stride(0),
-                               _ptr(labels), _ptr(w), _ptr(wu), _dtype(wu), _ptr(e_out), e_out.stride(0),
+    st = load().loca_top_error(_stream(stream), n, V, d, _ptr(logits, False), _dtype(logits), logits.stride(0),
+                               _ptr(labels), _ptr(w), _ptr(wu), _dtype(wu), _ptr(e_out, False), e_out.stride(0),
                                _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_top_error", st)
 
@@ -307,7 +315,7 @@ def loca_credit_from_top_error(e, credit_v, credit_b, y_out, mb_out, ws, *, a_w=
     y_out (nb, n, k); a_w (n,) optional statistic weights."""
     n, d = e.shape
     nb, _, k = credit_v.shape
-    st = load().loca_credit_from_top_error(_stream(stream), nb, n, d, k, _ptr(e), e.stride(0), _ptr(credit_v),
+    st = load().loca_credit_from_top_error(_stream(stream), nb, n, d, k, _ptr(e, False), e.stride(0), _ptr(credit_v),
                                            credit_v.stride(0), _ptr(credit_b), credit_b.stride(0), _ptr(a_w),
                                            _ptr(y_out), y_out.stride(0), _ptr(mb_out), _ptr(ws),
                                            ws.numel() * ws.element_size())

@@ -134,10 +134,40 @@ class BlockStep:
             loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj,
                                             self.info_proj, self.ws, stream=stream)
 
-    def run(self, x_blocks, logits, labels, credit_a, credit_b, proj_a=None, stream=None):
-        """One full pass over all micro-batches of all nb blocks."""
+    def run(self, x_blocks, logits, labels, credit_a, credit_b, proj_a=None, stream=None, lp=None, rp=None):
+        """One full pass over all micro-batches of all nb blocks (with the current adapter
+        W_prev = lp rp when given)."""
         self.reset()
         for m in range(self.cfg.n_micro):
             lo, hi = self.cfg.micro_rows(m)
             self.micro_batch(x_blocks[:, lo:hi], logits[lo:hi], labels[lo:hi], credit_a, credit_b, stream=stream)
-        self.solve(credit_b, proj_a, stream=stream)
+        self.solve(credit_b, proj_a, stream=stream, lp=lp, rp=rp)
+
+
+class JacobiOuterLoop:
+    """The outer iteration with the Jacobi schedule (Section S8): the caller runs one
+    forward pass of the adapted model and passes every block's inputs and the shared
+    logits to update(); each block then takes its step from that same forward pass with
+    the residual target of its current adapter W_prev = Lp Rp (Eq. 6, Theorem S6.1), and
+    the rank-r_a truncation of its solution becomes its next current adapter.  The first
+    update starts from the frozen model (Lp = Rp = 0).  Orchestration only: every step runs
+    in libloca's kernels; the factor transposes are layout copies."""
+
+    def __init__(self, cfg: LocaConfig, nb: int, device="cuda"):
+        import torch
+        if len(cfg.lambdas) != 1:
+            raise ValueError("the outer iteration keeps one adapter per block: give one lambda")
+        self.cfg, self.nb = cfg, nb
+        self.step = BlockStep(cfg, nb, device, r_prev=cfg.r_a)
+        self.lp = torch.zeros((nb, cfg.d, cfg.r_a), dtype=torch.float32, device=device)
+        self.rp = torch.zeros((nb, cfg.r_a, cfg.d), dtype=torch.float32, device=device)
+
+    def adapters(self):
+        """Current adapters as factors (Lp (nb, d, r_a), Rp (nb, r_a, d)): W_l = Lp_l Rp_l."""
+        return self.lp, self.rp
+
+    def update(self, x_blocks, logits, labels, credit_a, credit_b, stream=None):
+        self.step.run(x_blocks, logits, labels, credit_a, credit_b, stream=stream, lp=self.lp, rp=self.rp)
+        # W_r = A^T B^T with A (r_a x d), B (d x r_a): Lp = A^T, Rp = B^T
+        self.lp.copy_(self.step.A_ad.transpose(1, 2))
+        self.rp.copy_(self.step.B_ad.transpose(1, 2))

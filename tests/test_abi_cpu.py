@@ -245,3 +245,18 @@ def test_credit_from_top_error_rejects(lib):
     assert call(k=129) == lib.LOCA_E_UNSUPPORTED
     assert call() == lib.LOCA_E_WORKSPACE
     assert so.loca_workspace_size(lib.LOCA_OP_CREDIT_FROM_TOP_ERROR, 3, 16, 64, 8, 0, 0, 0, lib.LOCA_F32) > 0
+
+
+def test_binding_rejects_layouts_the_abi_cannot_describe(lib):
+    """Arrays the C ABI takes without a row stride must have packed rows; a transposed or
+    column-sliced tensor raises in the binding instead of being read with wrong strides."""
+    import torch
+    with pytest.raises(ValueError):
+        lib._ptr(torch.zeros(8, 96).T)                    # rows not contiguous
+    with pytest.raises(ValueError):
+        lib._ptr(torch.zeros(3, 8, 96).transpose(1, 2))   # block of a transposed stack
+    with pytest.raises(ValueError):
+        lib._ptr(torch.zeros(10, 16)[:, :8])              # rows not packed
+    assert lib._ptr(torch.zeros(10, 16)[:, :8], False) is not None  # arrays with a leading dimension
+    assert lib._ptr(torch.zeros(10, 16)[2:5]) is not None
+    assert lib._ptr(torch.zeros(4, 1, 3)) is not None
