@@ -86,7 +86,8 @@ typedef enum {
   LOCA_OP_TOP_ERROR = 6,
   LOCA_OP_CREDIT_FROM_TOP_ERROR = 7,
   LOCA_OP_REALIZATION_ERROR = 8,
-  LOCA_OP_CREDIT_GRAM = 9
+  LOCA_OP_CREDIT_GRAM = 9,
+  LOCA_OP_FEEDBACK_FIT_PRIMAL = 10
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -335,7 +336,7 @@ loca_status loca_dense_targets(loca_stream_t stream, int64_t nb, int64_t n, int6
  *               (float64).
  * beta > 0 (finite).  dev_info : nb int32, 0 or the 1-based pivot at which
  * E^T E + beta I failed to be positive definite (only for non-finite data).
- * Limits: np <= 64, k <= np, k <= d.  Workspace: LOCA_OP_FEEDBACK_FIT with
+ * Limits: np <= 64, np <= d, k <= np.  Workspace: LOCA_OP_FEEDBACK_FIT with
  * n = np.
  * ------------------------------------------------------------------------- */
 loca_status loca_feedback_fit(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k,
@@ -344,6 +345,26 @@ loca_status loca_feedback_fit(loca_stream_t stream, int64_t nb, int64_t d, int64
                               int64_t bt_bstride, float* at_out, int64_t at_bstride, float* vk_out,
                               int64_t vk_bstride, float* sigma_out, double* alpha_out,
                               int32_t* dev_info, void* ws, size_t ws_bytes);
+
+/* -------------------------------------------------------------------------
+ * The same Stage I calibration through the primal form of the ridge fit
+ * (Section S5, the theorem on the feedback ridge solution):
+ *   F_hat_b = G_b E^T (E E^T + beta I)^{-1}        (a Cholesky solve in d unknowns)
+ * which equals the dual form up to rounding (push-through identity) and serves probe
+ * counts beyond the dual form's limit.  E E^T is formed in float64, the solve runs
+ * in float64 (np right-hand sides), then every step after R = E^T (E E^T + beta I)^{-1}
+ * is the one loca_feedback_fit takes.  Arguments, layouts and outputs are those of
+ * loca_feedback_fit.  dev_info : nb int32, each 0 or the 1-based pivot at which
+ * E E^T + beta I failed to be positive definite (the one solve serves every block).
+ * Limits: np <= 128, np <= d <= 65535, k <= 64, k <= np.  Workspace:
+ * LOCA_OP_FEEDBACK_FIT_PRIMAL with n = np (d x d float64 among it).
+ * ------------------------------------------------------------------------- */
+loca_status loca_feedback_fit_primal(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k,
+                                     const float* e, const float* g, int64_t g_bstride, double beta,
+                                     const void* wu, loca_dtype wu_dtype, int64_t vocab, float* bt_out,
+                                     int64_t bt_bstride, float* at_out, int64_t at_bstride, float* vk_out,
+                                     int64_t vk_bstride, float* sigma_out, double* alpha_out,
+                                     int32_t* dev_info, void* ws, size_t ws_bytes);
 
 /* ---------------------------------------------------------------------------
  * The head in the paper's order (Section S11; the error term of the target equation
@@ -387,7 +408,7 @@ loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t
 
 /* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
  * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there; n = np for
- * LOCA_OP_FEEDBACK_FIT; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
+ * LOCA_OP_FEEDBACK_FIT and LOCA_OP_FEEDBACK_FIT_PRIMAL; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
  * LOCA_OP_REALIZATION_ERROR).  `acc` selects the precision mode.  Unused arguments
  * may be 0. */
 size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,

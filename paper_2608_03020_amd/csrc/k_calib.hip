@@ -163,31 +163,75 @@ __global__ void k_calib_factors(int64_t d, int k, int np_, const float* __restri
 }
 
 // alpha_b = <P, Q> / (||Q|| ||G||) from the fixed-order sums of the partial products
-// P = U_k^T G, Q = S_k V_k^T E (k x np) and ||G||^2.  One workgroup per block: thread e sums
-// entry e over the row ranges in order, then fixed-order workgroup sums.
+// P = U_k^T G, Q = S_k V_k^T E (k x np) and ||G||^2, taken over the probe columns in chunks of
+// at most 64 (chunk h: columns 64 h .. 64 h + w_h - 1, partials of P and Q at
+// pP + h * nb * ns * k * 64 with row length w_h, those of G_h^T G_h at pG2 + h * nb * ns * 64 * 64).
+// One workgroup per block: thread e sums entry e over the row ranges in order, then
+// fixed-order workgroup sums.
 __global__ __launch_bounds__(kT) void k_calib_alpha(int64_t nb, int k, int np_, int ns, const double* __restrict__ pP,
                                                     const double* __restrict__ pQ, const double* __restrict__ pG2,
                                                     double* __restrict__ alpha_out) {
   __shared__ double red[3][kT / 64];
   const int64_t b = blockIdx.x;
   double pq = 0.0, qq = 0.0, gg = 0.0;
-  for (int e = threadIdx.x; e < k * np_; e += kT) {
-    double p = 0.0, q = 0.0;
-    for (int z = 0; z < ns; ++z) {
-      p += pP[(b * ns + z) * k * np_ + e];
-      q += pQ[(b * ns + z) * k * np_ + e];
+  for (int h = 0; h * kMaxNp < np_; ++h) {
+    const int w = np_ - h * kMaxNp < kMaxNp ? np_ - h * kMaxNp : kMaxNp;
+    const double* P = pP + (int64_t)h * nb * ns * k * kMaxNp;
+    const double* Q = pQ + (int64_t)h * nb * ns * k * kMaxNp;
+    const double* G2 = pG2 + (int64_t)h * nb * ns * kMaxNp * kMaxNp;
+    for (int e = threadIdx.x; e < k * w; e += kT) {
+      double p = 0.0, q = 0.0;
+      for (int z = 0; z < ns; ++z) {
+        p += P[(b * ns + z) * k * w + e];
+        q += Q[(b * ns + z) * k * w + e];
+      }
+      pq += p * q;
+      qq += q * q;
     }
-    pq += p * q;
-    qq += q * q;
+    for (int e = threadIdx.x; e < w; e += kT)
+      for (int z = 0; z < ns; ++z) gg += G2[(b * ns + z) * w * w + e * w + e];
   }
-  for (int e = threadIdx.x; e < np_; e += kT)
-    for (int z = 0; z < ns; ++z) gg += pG2[(b * ns + z) * np_ * np_ + e * np_ + e];
   pq = block_sum(pq, red[0]);
   qq = block_sum(qq, red[1]);
   gg = block_sum(gg, red[2]);
   if (threadIdx.x == 0) {
     const double den = sqrt(qq) * sqrt(gg);
     alpha_out[b] = den > 0.0 ? pq / den : 0.0;
+  }
+}
+
+// Primal form helpers.  S_E = E E^T (d x d, fp64, both triangles) from the rows of E
+// (d x np, row-major): one thread per entry on or above the diagonal, products of floats
+// summed in fp64 in the order of the probes, the mirror written too.
+__global__ void k_rows_gram(int64_t d, int np_, const float* __restrict__ E, double* __restrict__ S) {
+  const int64_t i = blockIdx.y;
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j < i || j >= d) return;
+  const float* ei = E + i * np_;
+  const float* ej = E + j * np_;
+  double s = 0.0;
+  for (int p = 0; p < np_; ++p) s += (double)ei[p] * (double)ej[p];
+  S[i * d + j] = s;
+  S[j * d + i] = s;
+}
+// out (fp64) = in (float), element by element
+__global__ void k_to_f64(int64_t cnt, const float* __restrict__ in, double* __restrict__ out) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < cnt) out[e] = (double)in[e];
+}
+// R (np x d) = Rt^T (Rt: d x np), 32 x 32 tiles through LDS
+__global__ void k_transpose_f32(int64_t d, int np_, const float* __restrict__ Rt, float* __restrict__ R) {
+  __shared__ float t[32][33];
+  const int64_t c0 = (int64_t)blockIdx.x * 32, p0 = (int64_t)blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
+  for (int r = ty; r < 32; r += 8) {
+    const int64_t c = c0 + r, p = p0 + tx;
+    t[r][tx] = (c < d && p < np_) ? Rt[c * np_ + p] : 0.f;
+  }
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8) {
+    const int64_t p = p0 + r, c = c0 + tx;
+    if (p < np_ && c < d) R[p * d + c] = t[tx][r];
   }
 }
 
@@ -225,6 +269,11 @@ __global__ void k_copy_vk(int64_t d, int k, const float* __restrict__ vk, float*
   const int64_t b = blockIdx.y;
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e < d * k) out[b * bstride + e] = vk[b * d * k + e];
+}
+
+// the primal form's single solve serves every block: its status goes to each block's dev_info
+__global__ void k_copy_info(const int32_t* __restrict__ src, int32_t* __restrict__ dst, int64_t nb) {
+  for (int64_t b = threadIdx.x; b < nb; b += blockDim.x) dst[b] = src[0];
 }
 
 __global__ void k_zero_i32(int32_t* p, int64_t cnt) {
@@ -367,59 +416,73 @@ hipError_t launch_realization_error(const FitArgs& a) {
   return hipGetLastError();
 }
 
-size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
+// Workspace of the steps both forms share (truncation, factors, alignment) and of each form.
+static size_t fit_common_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
   const int ns = calib_splits(d);
-  size_t s = align256(sizeof(double) * ns * np_ * np_);           // Gamma partials
-  s += align256(sizeof(double) * np_ * np_);                      // L
-  s += align256(sizeof(float) * np_ * d);                         // R
+  const int64_t nch = (np_ + kMaxNp - 1) / kMaxNp;
+  size_t s = align256(sizeof(float) * np_ * d);                   // R
   s += align256(sizeof(float) * nb * k * d);                      // U_k^T
   s += align256(sizeof(float) * nb * d * k);                      // V_k S_k, then V_k
   s += align256(sizeof(float) * nb * d * k);
-  s += align256(sizeof(double) * nb * ns * (2 * k * np_ + np_ * np_));  // alpha partials
+  s += align256(sizeof(double) * nch * nb * ns * (2 * k * kMaxNp + kMaxNp * kMaxNp));  // alpha partials
   s += align256(sizeof(int32_t) * nb);                             // the truncation's own status
   s += lowrank_truncate_ws(nb, d, np_, k);
   return s;
 }
 
-hipError_t launch_feedback_fit(const CalibArgs& a) {
+size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
+  const int ns = calib_splits(d);
+  size_t s = align256(sizeof(double) * ns * np_ * np_);           // Gamma partials
+  s += align256(sizeof(double) * np_ * np_);                      // L
+  return s + fit_common_ws(nb, d, np_, k);
+}
+
+size_t feedback_fit_primal_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
+  size_t s = align256(sizeof(double) * d * d);                    // S_E = E E^T
+  s += align256(sizeof(double) * d * np_);                        // E in fp64 (right-hand sides)
+  s += align256(sizeof(float) * d * np_);                         // R^T = (S_E + beta I)^{-1} E
+  s += align256(sizeof(int32_t));                                 // the solve's status
+  s += ridge_solve_ws(1, d, np_, 1, LOCA_F64);
+  return s + fit_common_ws(nb, d, np_, k);
+}
+
+// Steps shared by both forms, given R (np x d) with F_hat_b = G_b R: the rank-k truncation,
+// the credit factors, the alignment diagnostic and the folded head.
+static hipError_t fit_tail(const CalibArgs& a, const float* R, char* p) {
   const int64_t d = a.d, np_ = a.np_, k = a.k, nb = a.nb;
   const int ns = calib_splits(d);
-  char* p = a.ws;
-  double* gpart = (double*)p; p += align256(sizeof(double) * ns * np_ * np_);
-  double* Lmat = (double*)p; p += align256(sizeof(double) * np_ * np_);
-  float* R = (float*)p; p += align256(sizeof(float) * np_ * d);
+  const int64_t nch = (np_ + kMaxNp - 1) / kMaxNp;
+  p += align256(sizeof(float) * np_ * d);  // R's own slot (filled by the caller)
   float* ut = (float*)p; p += align256(sizeof(float) * nb * k * d);
   float* vs = (float*)p; p += align256(sizeof(float) * nb * d * k);
   float* vk = (float*)p; p += align256(sizeof(float) * nb * d * k);
-  double* apart = (double*)p; p += align256(sizeof(double) * nb * ns * (2 * k * np_ + np_ * np_));
+  double* apart = (double*)p; p += align256(sizeof(double) * nch * nb * ns * (2 * k * kMaxNp + kMaxNp * kMaxNp));
   int32_t* tinfo = (int32_t*)p; p += align256(sizeof(int32_t) * nb);
   char* tws = p;
   double* pP = apart;
-  double* pQ = apart + nb * ns * k * np_;
-  double* pG = apart + 2 * nb * ns * k * np_;
+  double* pQ = apart + nch * nb * ns * k * kMaxNp;
+  double* pG = apart + 2 * nch * nb * ns * k * kMaxNp;
   hipStream_t st = a.stream;
-  k_zero_i32<<<(unsigned)((nb + 255) / 256), 256, 0, st>>>(a.dev_info, nb);
-  // 1-3: Gamma, its Cholesky with beta, R = (Gamma + beta I)^{-1} E^T
-  k_tall_cross<float><<<dim3((unsigned)ns, 1), kT, 0, st>>>(d, (int)np_, (int)np_, a.e, 0, np_, 1, a.e, 0, np_, 1, ns, gpart);
-  k_chol_small<<<1, kT, 0, st>>>((int)np_, ns, gpart, a.beta, Lmat, a.dev_info, nb);
-  k_ridge_cols<<<(unsigned)((d + kT - 1) / kT), kT, 0, st>>>(d, (int)np_, a.e, Lmat, R);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // 4: rank-k truncation of F_hat_b = G_b R (dev_info is not touched by the truncation
-  // beyond zero-filling, so it runs on a private copy)
+  // rank-k truncation of F_hat_b = G_b R (its status array is private: it only zero-fills it)
   TruncArgs t{st, nb, d, np_, k, a.g, a.g_bstride, R, 0, nb, ut, k * d, vs, d * k, a.sigma_out, np_, nullptr, 0,
               tinfo, tws};
-  if ((e = launch_lowrank_truncate(t)) != hipSuccess) return e;
-  // 5: credit factors and the alignment diagnostic
+  hipError_t e = launch_lowrank_truncate(t);
+  if (e != hipSuccess) return e;
   k_calib_factors<<<dim3((unsigned)((d + 255) / 256), (unsigned)nb), 256, 0, st>>>(
       d, (int)k, (int)np_, ut, vs, a.sigma_out, a.bt_out, a.bt_bstride, vk);
-  // P = U_k^T G (U_k^T is k x d: L(c, j) = ut[j * d + c]); Q = (V_k S_k)^T E; ||G||^2 from G^T G
-  k_tall_cross<float><<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, ut, k * d, 1, d, a.g,
-                                                                 a.g_bstride, np_, 1, ns, pP);
-  k_tall_cross<float><<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)k, (int)np_, vs, d * k, k, 1, a.e, 0, np_, 1,
-                                                                 ns, pQ);
-  k_tall_cross<float><<<dim3((unsigned)ns, (unsigned)nb), kT, 0, st>>>(d, (int)np_, (int)np_, a.g, a.g_bstride, np_, 1, a.g,
-                                                                 a.g_bstride, np_, 1, ns, pG);
+  // P = U_k^T G (U_k^T is k x d: L(c, j) = ut[j * d + c]); Q = (V_k S_k)^T E; ||G||^2 from the
+  // diagonal of G^T G; each over column chunks of at most 64 probes
+  for (int64_t h = 0; h < nch; ++h) {
+    const int64_t c0 = h * kMaxNp;
+    const int w = (int)(np_ - c0 < kMaxNp ? np_ - c0 : kMaxNp);
+    const dim3 g((unsigned)ns, (unsigned)nb);
+    k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)k, w, ut, k * d, 1, d, a.g + c0, a.g_bstride, np_, 1, ns,
+                                          pP + h * nb * ns * k * kMaxNp);
+    k_tall_cross<float><<<g, kT, 0, st>>>(d, (int)k, w, vs, d * k, k, 1, a.e + c0, 0, np_, 1, ns,
+                                          pQ + h * nb * ns * k * kMaxNp);
+    k_tall_cross<float><<<g, kT, 0, st>>>(d, w, w, a.g + c0, a.g_bstride, np_, 1, a.g + c0, a.g_bstride, np_, 1, ns,
+                                          pG + h * nb * ns * kMaxNp * kMaxNp);
+  }
   k_calib_alpha<<<(unsigned)nb, kT, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
   if (a.vk_out) {
     dim3 g((unsigned)((d * k + 255) / 256), (unsigned)nb);
@@ -433,6 +496,47 @@ hipError_t launch_feedback_fit(const CalibArgs& a) {
       k_head_fold<float><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const float*)a.wu, vk, a.at_out, a.at_bstride);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_feedback_fit(const CalibArgs& a) {
+  const int64_t d = a.d, np_ = a.np_, nb = a.nb;
+  const int ns = calib_splits(d);
+  hipStream_t st = a.stream;
+  char* p = a.ws;
+  k_zero_i32<<<(unsigned)((nb + 255) / 256), 256, 0, st>>>(a.dev_info, nb);
+  if (!a.primal) {
+    // dual form: Gamma = E^T E, its Cholesky with beta, R = (Gamma + beta I)^{-1} E^T
+    double* gpart = (double*)p; p += align256(sizeof(double) * ns * np_ * np_);
+    double* Lmat = (double*)p; p += align256(sizeof(double) * np_ * np_);
+    float* R = (float*)p;
+    k_tall_cross<float><<<dim3((unsigned)ns, 1), kT, 0, st>>>(d, (int)np_, (int)np_, a.e, 0, np_, 1, a.e, 0, np_, 1,
+                                                              ns, gpart);
+    k_chol_small<<<1, kT, 0, st>>>((int)np_, ns, gpart, a.beta, Lmat, a.dev_info, nb);
+    k_ridge_cols<<<(unsigned)((d + kT - 1) / kT), kT, 0, st>>>(d, (int)np_, a.e, Lmat, R);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return fit_tail(a, R, p);
+  }
+  // primal form: (E E^T + beta I) R^T = E by the Cholesky solve in d unknowns (np right-hand
+  // sides), R = (R^T)^T, so that F_hat_b = G_b E^T (E E^T + beta I)^{-1} = G_b R
+  double* SE = (double*)p; p += align256(sizeof(double) * d * d);
+  double* E64 = (double*)p; p += align256(sizeof(double) * d * np_);
+  float* Rt = (float*)p; p += align256(sizeof(float) * d * np_);
+  int32_t* sinfo = (int32_t*)p; p += align256(sizeof(int32_t));
+  char* sws = p; p += ridge_solve_ws(1, d, np_, 1, LOCA_F64);
+  float* R = (float*)p;
+  k_rows_gram<<<dim3((unsigned)((d + 255) / 256), (unsigned)d), 256, 0, st>>>(d, (int)np_, a.e, SE);
+  k_to_f64<<<(unsigned)((d * np_ + 255) / 256), 256, 0, st>>>(d * np_, a.e, E64);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const double lam[1] = {a.beta};
+  SolveArgs sa{st, 1, d, np_, SE, E64, LOCA_F64, d * d, d * np_, nullptr, nullptr, 0, 0, 0, lam, 1, Rt, d * np_,
+               nullptr, 0, nullptr, 0, sinfo, sws};
+  if ((e = launch_ridge_solve(sa)) != hipSuccess) return e;
+  k_copy_info<<<1, 64, 0, st>>>(sinfo, a.dev_info, nb);
+  k_transpose_f32<<<dim3((unsigned)((d + 31) / 32), (unsigned)((np_ + 31) / 32)), 256, 0, st>>>(d, (int)np_, Rt, R);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return fit_tail(a, R, p);
 }
 
 }  // namespace loca

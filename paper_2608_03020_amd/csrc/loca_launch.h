@@ -139,8 +139,10 @@ struct CalibArgs {
   float* vk_out; int64_t vk_bstride;
   float* sigma_out; double* alpha_out;
   int32_t* dev_info; char* ws;
+  bool primal;  // primal form (a Cholesky solve in d unknowns) instead of the dual one
 };
 size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
+size_t feedback_fit_primal_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
 
 // Realisation error of the fitted adapters (Section S6).
 struct FitArgs {

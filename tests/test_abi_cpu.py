@@ -206,9 +206,30 @@ def test_feedback_fit_rejects(lib):
     assert call(nb=2, gbs=10) == lib.LOCA_E_ARG
     assert call(nb=2, gbs=32 * 16, vk=FAKE, vkbs=10) == lib.LOCA_E_ARG  # V_k stride below d k
     assert call(n_p=65, k=4) == lib.LOCA_E_UNSUPPORTED
+    assert call(d=8, n_p=16, k=4) == lib.LOCA_E_UNSUPPORTED  # np <= d
     assert call() == lib.LOCA_E_WORKSPACE
     assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT, 2, 48, 300, 8, 0, 0, 0, lib.LOCA_F32) > 0
     assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT, 2, 65, 300, 8, 0, 0, 0, lib.LOCA_F32) == 0
+
+
+def test_feedback_fit_primal_rejects(lib):
+    so = lib.load()
+
+    def call(nb=1, d=256, n_p=100, k=8, beta=0.1, ws=None, wsb=0):
+        return so.loca_feedback_fit_primal(None, nb, d, n_p, k, FAKE, FAKE, 0, beta, None, lib.LOCA_F32, 0, FAKE, 0,
+                                           None, 0, None, 0, FAKE, FAKE, FAKE, ws, wsb)
+
+    assert call(beta=0.0) == lib.LOCA_E_ARG
+    assert call(k=101) == lib.LOCA_E_ARG                  # k <= np
+    assert call(n_p=129) == lib.LOCA_E_UNSUPPORTED        # np <= 128
+    assert call(n_p=100, k=65) == lib.LOCA_E_UNSUPPORTED  # k <= 64 (the truncation's rank limit)
+    assert call(d=90) == lib.LOCA_E_UNSUPPORTED           # np <= d
+    assert call(d=70000) == lib.LOCA_E_UNSUPPORTED        # the d x d solve's limit
+    assert call() == lib.LOCA_E_WORKSPACE
+    need = so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT_PRIMAL, 1, 100, 256, 8, 0, 0, 0, lib.LOCA_F32)
+    assert need >= 8 * 256 * 256                          # holds E E^T in float64
+    assert call(ws=FAKE, wsb=need - 1) == lib.LOCA_E_WORKSPACE
+    assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT_PRIMAL, 1, 129, 256, 8, 0, 0, 0, lib.LOCA_F32) == 0
 
 
 def test_top_error_rejects(lib):
