@@ -76,6 +76,11 @@ typedef enum { LOCA_F32 = 0, LOCA_BF16 = 1, LOCA_F64 = 2 } loca_dtype;
  * are then unspecified.  It takes precedence over the positive codes. */
 #define LOCA_INFO_NONFINITE (-1)
 
+/* dev_info code of loca_feedback_fit_large: the subspace basis lost rank (a pivot of its
+ * Cholesky QR was not positive), so fewer than l directions of the map were found; the
+ * outputs are then unspecified. */
+#define LOCA_INFO_BASIS_RANK (-2)
+
 typedef enum {
   LOCA_OP_ERROR_TARGETS = 0,
   LOCA_OP_ACCUMULATE_STATS = 1,
@@ -87,7 +92,8 @@ typedef enum {
   LOCA_OP_CREDIT_FROM_TOP_ERROR = 7,
   LOCA_OP_REALIZATION_ERROR = 8,
   LOCA_OP_CREDIT_GRAM = 9,
-  LOCA_OP_FEEDBACK_FIT_PRIMAL = 10
+  LOCA_OP_FEEDBACK_FIT_PRIMAL = 10,
+  LOCA_OP_FEEDBACK_FIT_LARGE = 11
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -366,6 +372,34 @@ loca_status loca_feedback_fit_primal(loca_stream_t stream, int64_t nb, int64_t d
                                      int64_t vk_bstride, float* sigma_out, double* alpha_out,
                                      int32_t* dev_info, void* ws, size_t ws_bytes);
 
+/* -------------------------------------------------------------------------
+ * Stage I calibration for any probe count, in particular np > d, where the fitted map
+ * F_hat_b = G_b E^T (E E^T + beta I)^{-1} (Section S5, Eq. 5 and the theorem on the feedback
+ * ridge solution, primal form) is a full-rank d x d matrix.  R^T = (E E^T + beta I)^{-1} E
+ * is solved once (float64 Cholesky, shared by the blocks); the best rank-k approximation
+ * of F_hat_b = G_b R (the rank-truncation lemma) is then found by randomised subspace
+ * iteration, which never forms F_hat_b: from the caller's start block omega (d x l float,
+ * e.g. standard normal, shared by the blocks), q rounds of Y = orth(F_hat Omega),
+ * Omega = orth(F_hat^T Y), then Q = orth(F_hat Omega) and the exact rank-k truncation of
+ * the Ritz approximation Q Q^T F_hat (orth: Cholesky QR taken twice, float64).  The
+ * leading k singular pairs converge at the rate (sigma_{l+1} / sigma_k)^(2q+1) of subspace
+ * iteration; q and the oversampled width l are the caller's trade of time for accuracy.
+ * Arguments and outputs are those of loca_feedback_fit (e: d x np, g_b: d x np, strides
+ * as there), except:
+ *   sigma_out : per block l floats (stride l), the Ritz values, decreasing; the leading
+ *               k approximate the singular values of F_hat_b;
+ *   dev_info : nb int32; 0, the 1-based pivot at which E E^T + beta I failed to be positive
+ *              definite (any block), or LOCA_INFO_BASIS_RANK for that block.
+ * Limits: k <= l <= 128, l <= d <= 65535, k <= 64, q <= 64, np <= 2^21, nb d l <= 2^31.  Workspace:
+ * LOCA_OP_FEEDBACK_FIT_LARGE with n = np and r_a = l (d x d and d x np among it).
+ * ------------------------------------------------------------------------- */
+loca_status loca_feedback_fit_large(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k,
+                                    int64_t l, int64_t q, const float* e, const float* g, int64_t g_bstride,
+                                    const float* omega, double beta, const void* wu, loca_dtype wu_dtype,
+                                    int64_t vocab, float* bt_out, int64_t bt_bstride, float* at_out,
+                                    int64_t at_bstride, float* vk_out, int64_t vk_bstride, float* sigma_out,
+                                    double* alpha_out, int32_t* dev_info, void* ws, size_t ws_bytes);
+
 /* ---------------------------------------------------------------------------
  * The head in the paper's order (Section S11; the error term of the target equation
  * with Lemma S3.1's head error): the top-layer error at the hidden width, computed
@@ -408,7 +442,8 @@ loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t
 
 /* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
  * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there; n = np for
- * LOCA_OP_FEEDBACK_FIT and LOCA_OP_FEEDBACK_FIT_PRIMAL; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
+ * LOCA_OP_FEEDBACK_FIT and LOCA_OP_FEEDBACK_FIT_PRIMAL, n = np and r_a = l for
+ * LOCA_OP_FEEDBACK_FIT_LARGE; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
  * LOCA_OP_REALIZATION_ERROR).  `acc` selects the precision mode.  Unused arguments
  * may be 0. */
 size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,

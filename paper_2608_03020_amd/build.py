@@ -8,7 +8,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIBDIR = os.path.join(HERE, "lib")
 LIB = os.path.join(LIBDIR, "libloca.so")
-SOURCES = ["loca_api.hip", "k_error.hip", "k_gram.hip", "k_chol.hip", "k_trunc.hip", "k_calib.hip", "k_head.hip"]
+SOURCES = ["loca_api.hip", "k_error.hip", "k_gram.hip", "k_chol.hip", "k_trunc.hip", "k_calib.hip", "k_head.hip",
+           "k_subspace.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -416,18 +416,56 @@ hipError_t launch_realization_error(const FitArgs& a) {
   return hipGetLastError();
 }
 
-// Workspace of the steps both forms share (truncation, factors, alignment) and of each form.
+// The rank-k truncation of F_b = M_b R_b (kp columns; R_b shared by r_group consecutive
+// blocks) and the credit factors of Stage I: B~, V_k and the folded head A~.  Workspace:
+// U_k^T (k x d), V_k S_k and V_k (d x k) per block, the truncation's status and its own.
+size_t calib_factor_ws(int64_t nb, int64_t d, int64_t kp, int64_t k) {
+  size_t s = align256(sizeof(float) * nb * k * d);                // U_k^T
+  s += align256(sizeof(float) * nb * d * k);                      // V_k S_k
+  s += align256(sizeof(float) * nb * d * k);                      // V_k
+  s += align256(sizeof(int32_t) * nb);                             // the truncation's own status
+  s += lowrank_truncate_ws(nb, d, kp, k);
+  return s;
+}
+
+hipError_t launch_calib_factors(const CalibArgs& a, const float* M, int64_t m_bs, const float* R, int64_t r_bs,
+                                int64_t r_group, int64_t kp, char* p, float** ut_out, float** vs_out) {
+  const int64_t d = a.d, k = a.k, nb = a.nb;
+  float* ut = (float*)p; p += align256(sizeof(float) * nb * k * d);
+  float* vs = (float*)p; p += align256(sizeof(float) * nb * d * k);
+  float* vk = (float*)p; p += align256(sizeof(float) * nb * d * k);
+  int32_t* tinfo = (int32_t*)p; p += align256(sizeof(int32_t) * nb);
+  hipStream_t st = a.stream;
+  // the truncation's status array is private: its only writes are zeros
+  TruncArgs t{st, nb, d, kp, k, M, m_bs, R, r_bs, r_group, ut, k * d, vs, d * k, a.sigma_out, kp, nullptr, 0,
+              tinfo, p};
+  hipError_t e = launch_lowrank_truncate(t);
+  if (e != hipSuccess) return e;
+  k_calib_factors<<<dim3((unsigned)((d + 255) / 256), (unsigned)nb), 256, 0, st>>>(
+      d, (int)k, (int)kp, ut, vs, a.sigma_out, a.bt_out, a.bt_bstride, vk);
+  if (a.vk_out) {
+    dim3 g((unsigned)((d * k + 255) / 256), (unsigned)nb);
+    k_copy_vk<<<g, 256, 0, st>>>(d, (int)k, vk, a.vk_out, a.vk_bstride);
+  }
+  if (a.wu && a.at_out) {
+    dim3 g((unsigned)((a.vocab + 3) / 4), (unsigned)nb);
+    if (a.wu_dtype == LOCA_BF16)
+      k_head_fold<uint16_t><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const uint16_t*)a.wu, vk, a.at_out, a.at_bstride);
+    else
+      k_head_fold<float><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const float*)a.wu, vk, a.at_out, a.at_bstride);
+  }
+  *ut_out = ut;
+  *vs_out = vs;
+  return hipGetLastError();
+}
+
+// Workspace of the steps both small-probe forms share (R, the factors, the alignment).
 static size_t fit_common_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
   const int ns = calib_splits(d);
   const int64_t nch = (np_ + kMaxNp - 1) / kMaxNp;
   size_t s = align256(sizeof(float) * np_ * d);                   // R
-  s += align256(sizeof(float) * nb * k * d);                      // U_k^T
-  s += align256(sizeof(float) * nb * d * k);                      // V_k S_k, then V_k
-  s += align256(sizeof(float) * nb * d * k);
   s += align256(sizeof(double) * nch * nb * ns * (2 * k * kMaxNp + kMaxNp * kMaxNp));  // alpha partials
-  s += align256(sizeof(int32_t) * nb);                             // the truncation's own status
-  s += lowrank_truncate_ws(nb, d, np_, k);
-  return s;
+  return s + calib_factor_ws(nb, d, np_, k);
 }
 
 size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
@@ -446,30 +484,21 @@ size_t feedback_fit_primal_ws(int64_t nb, int64_t d, int64_t np_, int64_t k) {
   return s + fit_common_ws(nb, d, np_, k);
 }
 
-// Steps shared by both forms, given R (np x d) with F_hat_b = G_b R: the rank-k truncation,
-// the credit factors, the alignment diagnostic and the folded head.
+// Steps shared by both small-probe forms, given R (np x d) with F_hat_b = G_b R: the rank-k
+// truncation, the credit factors, the alignment diagnostic and the folded head.
 static hipError_t fit_tail(const CalibArgs& a, const float* R, char* p) {
   const int64_t d = a.d, np_ = a.np_, k = a.k, nb = a.nb;
   const int ns = calib_splits(d);
   const int64_t nch = (np_ + kMaxNp - 1) / kMaxNp;
   p += align256(sizeof(float) * np_ * d);  // R's own slot (filled by the caller)
-  float* ut = (float*)p; p += align256(sizeof(float) * nb * k * d);
-  float* vs = (float*)p; p += align256(sizeof(float) * nb * d * k);
-  float* vk = (float*)p; p += align256(sizeof(float) * nb * d * k);
   double* apart = (double*)p; p += align256(sizeof(double) * nch * nb * ns * (2 * k * kMaxNp + kMaxNp * kMaxNp));
-  int32_t* tinfo = (int32_t*)p; p += align256(sizeof(int32_t) * nb);
-  char* tws = p;
   double* pP = apart;
   double* pQ = apart + nch * nb * ns * k * kMaxNp;
   double* pG = apart + 2 * nch * nb * ns * k * kMaxNp;
   hipStream_t st = a.stream;
-  // rank-k truncation of F_hat_b = G_b R (its status array is private: it only zero-fills it)
-  TruncArgs t{st, nb, d, np_, k, a.g, a.g_bstride, R, 0, nb, ut, k * d, vs, d * k, a.sigma_out, np_, nullptr, 0,
-              tinfo, tws};
-  hipError_t e = launch_lowrank_truncate(t);
+  float *ut = nullptr, *vs = nullptr;
+  hipError_t e = launch_calib_factors(a, a.g, a.g_bstride, R, 0, nb, np_, p, &ut, &vs);
   if (e != hipSuccess) return e;
-  k_calib_factors<<<dim3((unsigned)((d + 255) / 256), (unsigned)nb), 256, 0, st>>>(
-      d, (int)k, (int)np_, ut, vs, a.sigma_out, a.bt_out, a.bt_bstride, vk);
   // P = U_k^T G (U_k^T is k x d: L(c, j) = ut[j * d + c]); Q = (V_k S_k)^T E; ||G||^2 from the
   // diagonal of G^T G; each over column chunks of at most 64 probes
   for (int64_t h = 0; h < nch; ++h) {
@@ -484,17 +513,6 @@ static hipError_t fit_tail(const CalibArgs& a, const float* R, char* p) {
                                           pG + h * nb * ns * kMaxNp * kMaxNp);
   }
   k_calib_alpha<<<(unsigned)nb, kT, 0, st>>>(nb, (int)k, (int)np_, ns, pP, pQ, pG, a.alpha_out);
-  if (a.vk_out) {
-    dim3 g((unsigned)((d * k + 255) / 256), (unsigned)nb);
-    k_copy_vk<<<g, 256, 0, st>>>(d, (int)k, vk, a.vk_out, a.vk_bstride);
-  }
-  if (a.wu && a.at_out) {
-    dim3 g((unsigned)((a.vocab + 3) / 4), (unsigned)nb);
-    if (a.wu_dtype == LOCA_BF16)
-      k_head_fold<uint16_t><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const uint16_t*)a.wu, vk, a.at_out, a.at_bstride);
-    else
-      k_head_fold<float><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const float*)a.wu, vk, a.at_out, a.at_bstride);
-  }
   return hipGetLastError();
 }
 

@@ -60,6 +60,8 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
     case LOCA_OP_FEEDBACK_FIT: return d < 1 || n < 1 || n > 64 ? 0 : feedback_fit_ws(nb, d, n, k);
     case LOCA_OP_FEEDBACK_FIT_PRIMAL:
       return d < 1 || n < 1 || n > kMaxKpTrunc ? 0 : feedback_fit_primal_ws(nb, d, n, k);
+    case LOCA_OP_FEEDBACK_FIT_LARGE:
+      return d < 1 || n < 1 || r_a < 1 || r_a > kMaxKpTrunc ? 0 : feedback_fit_large_ws(nb, d, n, k, r_a);
     case LOCA_OP_TOP_ERROR: return n < 1 || d < 1 || C < 1 ? 0 : top_error_ws(n, C, d);
     case LOCA_OP_CREDIT_FROM_TOP_ERROR: return n < 1 ? 0 : credit_from_top_error_ws(nb, n, k);
     case LOCA_OP_CREDIT_GRAM: return d < 1 ? 0 : credit_gram_ws(nb, k);
@@ -317,6 +319,31 @@ loca_status loca_feedback_fit_primal(loca_stream_t stream, int64_t nb, int64_t d
                                      size_t ws_bytes) {
   return feedback_fit(stream, nb, d, np, k, e, g, g_bstride, beta, wu, wu_dtype, vocab, bt_out, bt_bstride, at_out,
                       at_bstride, vk_out, vk_bstride, sigma_out, alpha_out, dev_info, ws, ws_bytes, true);
+}
+
+loca_status loca_feedback_fit_large(loca_stream_t stream, int64_t nb, int64_t d, int64_t np, int64_t k, int64_t l,
+                                    int64_t q, const float* e, const float* g, int64_t g_bstride, const float* omega,
+                                    double beta, const void* wu, loca_dtype wu_dtype, int64_t vocab, float* bt_out,
+                                    int64_t bt_bstride, float* at_out, int64_t at_bstride, float* vk_out,
+                                    int64_t vk_bstride, float* sigma_out, double* alpha_out, int32_t* dev_info,
+                                    void* ws, size_t ws_bytes) {
+  if (nb < 1 || d < 1 || np < 1 || k < 1 || l < 1 || q < 0) return LOCA_E_ARG;
+  if (!e || !g || !omega || !bt_out || !sigma_out || !alpha_out || !dev_info) return LOCA_E_ARG;
+  if (!(beta > 0.0) || beta == __builtin_inf()) return LOCA_E_ARG;
+  if (k > l || l > d) return LOCA_E_ARG;
+  if (nb > 1 && (g_bstride < d * np || bt_bstride < k * d)) return LOCA_E_ARG;
+  if (at_out && (!wu || vocab < 1 || (wu_dtype != LOCA_F32 && wu_dtype != LOCA_BF16) ||
+                 (nb > 1 && at_bstride < vocab * k)))
+    return LOCA_E_ARG;
+  if (vk_out && nb > 1 && vk_bstride < d * k) return LOCA_E_ARG;
+  if (l > kMaxKpTrunc || k > kMaxRankTrunc || q > 64) return LOCA_E_UNSUPPORTED;
+  if (nb > 65535 || d > 65535 || np > ((int64_t)1 << 21) || vocab > (int64_t)1 << 32) return LOCA_E_UNSUPPORTED;
+  if (nb * d * l > ((int64_t)1 << 31)) return LOCA_E_UNSUPPORTED;  // one-dimensional element grids
+  loca_status st = check_ws(ws, ws_bytes, feedback_fit_large_ws(nb, d, np, k, l));
+  if (st != LOCA_OK) return st;
+  CalibArgs a{(hipStream_t)stream, nb, d, np, k, e, g, g_bstride, beta, wu, wu_dtype, vocab, bt_out, bt_bstride,
+              at_out, at_bstride, vk_out, vk_bstride, sigma_out, alpha_out, dev_info, (char*)ws, true, l, q, omega};
+  return from_hip(launch_feedback_fit_large(a));
 }
 
 loca_status loca_top_error(loca_stream_t stream, int64_t n, int64_t V, int64_t d, const void* logits,

@@ -140,9 +140,20 @@ struct CalibArgs {
   float* sigma_out; double* alpha_out;
   int32_t* dev_info; char* ws;
   bool primal;  // primal form (a Cholesky solve in d unknowns) instead of the dual one
+  // subspace-iteration form (loca_feedback_fit_large): basis width, power iterations and
+  // the caller's start block (d x l float)
+  int64_t l, q;
+  const float* omega;
 };
 size_t feedback_fit_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
 size_t feedback_fit_primal_ws(int64_t nb, int64_t d, int64_t np_, int64_t k);
+size_t feedback_fit_large_ws(int64_t nb, int64_t d, int64_t np_, int64_t k, int64_t l);
+hipError_t launch_feedback_fit_large(const CalibArgs& a);
+// The rank-k truncation of F_b = M_b R_b and the Stage I credit factors (shared by the fits);
+// returns U_k^T (k x d) and V_k S_k (d x k) per block, both inside the workspace.
+size_t calib_factor_ws(int64_t nb, int64_t d, int64_t kp, int64_t k);
+hipError_t launch_calib_factors(const CalibArgs& a, const float* M, int64_t m_bs, const float* R, int64_t r_bs,
+                                int64_t r_group, int64_t kp, char* ws, float** ut, float** vs);
 
 // Realisation error of the fitted adapters (Section S6).
 struct FitArgs {

@@ -17,14 +17,15 @@ LIB_PATH = os.environ.get("LOCA_LIB", os.path.join(HERE, "lib", "libloca.so"))
 LOCA_OK, LOCA_E_ARG, LOCA_E_WORKSPACE, LOCA_E_HIP, LOCA_E_UNSUPPORTED = range(5)
 LOCA_F32, LOCA_BF16, LOCA_F64 = range(3)
 LOCA_INFO_NONFINITE = -1
+LOCA_INFO_BASIS_RANK = -2
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
  LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR,
- LOCA_OP_REALIZATION_ERROR, LOCA_OP_CREDIT_GRAM, LOCA_OP_FEEDBACK_FIT_PRIMAL) = range(11)
+ LOCA_OP_REALIZATION_ERROR, LOCA_OP_CREDIT_GRAM, LOCA_OP_FEEDBACK_FIT_PRIMAL, LOCA_OP_FEEDBACK_FIT_LARGE) = range(12)
 
 ENTRY_POINTS = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_top_error",
                 "loca_credit_from_top_error", "loca_error_targets_noalloc", "loca_realization_error",
-                "loca_credit_gram", "loca_feedback_fit_primal")
+                "loca_credit_gram", "loca_feedback_fit_primal", "loca_feedback_fit_large")
 EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version",
                            "loca_error_targets_noalloc_max_bytes", "loca_credit_gram_ld")
 
@@ -79,6 +80,8 @@ def load():
     lib.loca_feedback_fit.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _D, _VP, _I, _I64, _VP, _I64,
                                       _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_feedback_fit_primal.argtypes = lib.loca_feedback_fit.argtypes
+    lib.loca_feedback_fit_large.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _VP, _D, _VP, _I,
+                                            _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_top_error.argtypes = [_VP, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _I, _VP, _I64, _VP, _VP,
                                    _SZ]
     lib.loca_credit_from_top_error.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP,
@@ -311,6 +314,24 @@ def loca_feedback_fit_primal(e, g, beta: float, bt_out, sigma_out, alpha_out, de
     (np <= 128, k <= 64); the workspace is LOCA_OP_FEEDBACK_FIT_PRIMAL's."""
     _feedback_fit("loca_feedback_fit_primal", e, g, beta, bt_out, sigma_out, alpha_out, dev_info, ws, wu, at_out,
                   vk_out, stream)
+
+
+def loca_feedback_fit_large(e, g, omega, q: int, beta: float, bt_out, sigma_out, alpha_out, dev_info, ws, *,
+                            wu=None, at_out=None, vk_out=None, stream=None):
+    """As loca_feedback_fit for any probe count (np > d included): randomised subspace iteration
+    on the primal fit from the start block omega (d, l) with q rounds; sigma_out (nb, l) holds
+    the Ritz values; the workspace is LOCA_OP_FEEDBACK_FIT_LARGE's (n = np, r_a = l)."""
+    d, n_p = e.shape
+    nb = g.shape[0]
+    k = bt_out.shape[-2]
+    l = omega.shape[1]
+    vocab = wu.shape[0] if wu is not None else 0
+    st = load().loca_feedback_fit_large(
+        _stream(stream), nb, d, n_p, k, l, int(q), _ptr(e), _ptr(g), g.stride(0), _ptr(omega), float(beta),
+        _ptr(wu), _dtype(wu) if wu is not None else LOCA_F32, vocab, _ptr(bt_out), bt_out.stride(0), _ptr(at_out),
+        at_out.stride(0) if at_out is not None else 0, _ptr(vk_out), vk_out.stride(0) if vk_out is not None else 0,
+        _ptr(sigma_out), _ptr(alpha_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
+    _check("loca_feedback_fit_large", st)
 
 
 def loca_top_error(logits, labels, wu, e_out, dev_info, ws, *, w=None, stream=None):

@@ -232,6 +232,28 @@ def test_feedback_fit_primal_rejects(lib):
     assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT_PRIMAL, 1, 129, 256, 8, 0, 0, 0, lib.LOCA_F32) == 0
 
 
+def test_feedback_fit_large_rejects(lib):
+    so = lib.load()
+
+    def call(nb=1, d=256, n_p=600, k=8, l=32, q=3, om=FAKE, beta=0.1, ws=None, wsb=0):
+        return so.loca_feedback_fit_large(None, nb, d, n_p, k, l, q, FAKE, FAKE, 0, om, beta, None, lib.LOCA_F32, 0,
+                                          FAKE, 0, None, 0, None, 0, FAKE, FAKE, FAKE, ws, wsb)
+
+    assert call(beta=0.0) == lib.LOCA_E_ARG
+    assert call(om=None) == lib.LOCA_E_ARG                 # the start block is the caller's
+    assert call(q=-1) == lib.LOCA_E_ARG
+    assert call(k=33) == lib.LOCA_E_ARG                    # k <= l
+    assert call(d=30, l=32) == lib.LOCA_E_ARG              # l <= d
+    assert call(l=129, d=256) == lib.LOCA_E_UNSUPPORTED    # l <= 128
+    assert call(k=65, l=100) == lib.LOCA_E_UNSUPPORTED     # k <= 64
+    assert call(q=65) == lib.LOCA_E_UNSUPPORTED
+    assert call() == lib.LOCA_E_WORKSPACE
+    need = so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT_LARGE, 1, 600, 256, 8, 0, 32, 0, lib.LOCA_F32)
+    assert need >= 8 * 256 * 256 + 4 * 256 * 600          # E E^T (float64) and R^T (float)
+    assert call(ws=FAKE, wsb=need - 1) == lib.LOCA_E_WORKSPACE
+    assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT_LARGE, 1, 600, 256, 8, 0, 0, 0, lib.LOCA_F32) == 0
+
+
 def test_top_error_rejects(lib):
     so = lib.load()
 
