@@ -278,7 +278,46 @@ def next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream):
                                "sample": f"block 0 at width {d_s} with {n_p} probes ({t_blk:.2f} s), scaled by "
                                          f"(d/{d_s})^3 x {nb} blocks"}
     out["feedback_fit"] = cal
-    del E, G, Wu, bt, at, ws
+    del E, G, bt, at, ws
+    torch.cuda.empty_cache()
+
+    # Stage I calibration from 2d probe positions (np > d: a full-rank d x d fitted map),
+    # randomised subspace iteration of width l = min(2k, 128) with q = 3 rounds
+    n_p, l, q = 2 * cfg.d, min(2 * k, 128), 3
+    E, G = gen.torch_gen_probe_pairs(cfg, n_p, nb)
+    omega = torch.randn((cfg.d, l), generator=g, device="cuda", dtype=torch.float32)
+    bt = torch.empty((nb, k, cfg.d), dtype=torch.float32, device="cuda")
+    at = torch.empty((nb, V, k), dtype=torch.float32, device="cuda")
+    sig = torch.empty((nb, l), dtype=torch.float32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_FEEDBACK_FIT_LARGE, nb, n_p, cfg.d, k, r_a=l), "cuda")
+    reps_l = 2
+    lev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps_l)]
+
+    def calib_large(s):
+        if s < reps_l:
+            lev[s][0].record(stream)
+        loca.loca_feedback_fit_large(E, G, omega, q, 0.05, bt, sig, alpha, info, ws, wu=Wu, at_out=at)
+        if s < reps_l:
+            lev[s][1].record(stream)
+    time_steps(calib_large, reps_l, 1)
+    t_l = sum(a.elapsed_time(b) for a, b in lev) / reps_l
+    d_ = cfg.d
+    # algorithmic float64 flops: E E^T, one factorisation and the np right-hand sides, the
+    # 2q + 2 products with F_hat or F_hat^T (two skinny products each), 2q + 1 two-pass
+    # Cholesky QRs (Gram and basis update), and the alignment products
+    fl = (2.0 * d_ * d_ * n_p + d_ ** 3 / 3.0 + 2.0 * d_ * d_ * n_p
+          + nb * ((2 * q + 2) * 4.0 * d_ * n_p * l + (2 * q + 1) * 2 * 4.0 * d_ * l * l + 4.0 * k * d_ * n_p))
+    tfs = fl / (t_l * 1e-3) / 1e12
+    out["feedback_fit_large"] = {
+        "ms_per_call": t_l, "unit": "ms per calibration of all blocks", "higher_is_better": False,
+        "config": {"blocks": nb, "d": d_, "probes": n_p, "credit_rank": k, "basis": l, "rounds": q,
+                   "head_rows": V, "beta": 0.05},
+        "info_ok": bool((info == 0).all().item()), "alpha_mean": float(alpha.mean().item()),
+        "roofline": {"bound": "alu", "achieved": tfs, "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": tfs / FP64_PEAK_TFLOPS, "traffic": None, "kernel": "loca_feedback_fit_large (all blocks)",
+                     "algorithmic_flops_per_call": fl, "avg_launch_ms": t_l}}
+    print(f"[bench] next: calibration with {n_p} probes {t_l:.1f} ms", file=sys.stderr, flush=True)
+    del E, G, Wu, bt, at, ws, omega
     torch.cuda.empty_cache()
     out["paper_order_head"] = paper_order_head(stream)
     return out
