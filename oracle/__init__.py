@@ -16,7 +16,8 @@ plus the paper-literal projected form with a random A_l            (Eqs. 6-9)
 and the one-time Stage I calibration that produces A~, B~: the feedback ridge
 fit, its rank-k truncation and the alignment diagnostic           (Section S5),
 and the head in the paper's order: the top error e_t = W_u^T E_t once, then
-V_k^T e_t per block                                               (Section S11)
+V_k^T e_t per block                                               (Section S11),
+and the LM head from the final hidden states (logits z = W_u h_t)  (Eq. 4)
 
 It shares no code with the HIP path and never imports it.
 """
@@ -313,6 +314,14 @@ def top_error(z, y, Wu, w=None):
     the head applied once per top error and shared by all blocks (Section S11's cost
     order).  z (n x V), Wu (V x d) -> e (n x d); the product is a library matmul."""
     return head_error(z, y, w) @ _f64(Wu)
+
+
+def fused_head(h, Wu, y, Vm, w=None):
+    """The head error applied to a right operand, starting from the final hidden states
+    ("Local Targets", Eq. 4, with Lemma S3.1's head error): logits z_t = W_u h_t (a library
+    matmul), E_t = w_t (softmax(z_t) - onehot(y_t)), and out = E Vm.  Vm = W_u gives the top
+    error of the paper's order (Section S11); Vm = W_u V_k gives a block's coordinates."""
+    return head_error(_f64(h) @ _f64(Wu).T, y, w) @ _f64(Vm)
 
 
 def credit_from_top_error(e, Vk, B):

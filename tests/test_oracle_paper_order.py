@@ -60,3 +60,48 @@ def test_paper_order_equals_folded_order(orc):
     Y_f, Q_f = orc.credit(orc.head_error(z, y, w), Wu @ Vk, B)
     np.testing.assert_allclose(Y_p, Y_f, rtol=1e-11, atol=1e-12)
     np.testing.assert_allclose(Q_p, Q_f, rtol=1e-11, atol=1e-12)
+
+
+def test_fused_head_brute_force(orc):
+    # from hidden states: z_t = W_u h_t by explicit sums, softmax by explicit exponentials
+    rng = np.random.default_rng(24)
+    n, V, d, c = 5, 9, 4, 3
+    h = rng.standard_normal((n, d))
+    Wu = rng.standard_normal((V, d))
+    Vm = rng.standard_normal((V, c))
+    y = rng.integers(0, V, n).astype(np.int32)
+    w = rng.uniform(0.0, 2.0, n)
+    out = orc.fused_head(h, Wu, y, Vm, w)
+    for t in range(n):
+        z = [sum(Wu[v, j] * h[t, j] for j in range(d)) for v in range(V)]
+        den = sum(math.exp(zv) for zv in z)
+        for j in range(c):
+            ref = w[t] * sum((math.exp(z[v]) / den - (1.0 if v == y[t] else 0.0)) * Vm[v, j] for v in range(V))
+            assert abs(out[t, j] - ref) <= 1e-12 * (1 + abs(ref))
+
+
+def test_fused_head_invariances(orc):
+    rng = np.random.default_rng(25)
+    n, V, d, c = 8, 12, 6, 5
+    h = rng.standard_normal((n, d)) * 2.0
+    Wu = rng.standard_normal((V, d))
+    Vm = rng.standard_normal((V, c))
+    y = rng.integers(0, V, n).astype(np.int32)
+    out = orc.fused_head(h, Wu, y, Vm)
+    # each error row sums to zero: a vector added to every row of Vm changes nothing
+    np.testing.assert_allclose(orc.fused_head(h, Wu, y, Vm + rng.standard_normal(c)[None, :]), out,
+                               rtol=1e-11, atol=1e-12)
+    # a hidden direction orthogonal to every head row leaves the logits unchanged
+    Vs, ds = 4, 7
+    Ws = rng.standard_normal((Vs, ds))
+    hs = rng.standard_normal((n, ds))
+    ys = rng.integers(0, Vs, n).astype(np.int32)
+    Vms = rng.standard_normal((Vs, c))
+    q, _ = np.linalg.qr(np.concatenate([Ws.T, rng.standard_normal((ds, 1))], axis=1))
+    u = q[:, Vs]
+    assert np.abs(Ws @ u).max() < 1e-12
+    np.testing.assert_allclose(orc.fused_head(hs + 3.0 * u[None, :], Ws, ys, Vms), orc.fused_head(hs, Ws, ys, Vms),
+                               rtol=1e-11, atol=1e-12)
+    # Vm = W_u is the paper-order top error of the logits h W_u^T
+    np.testing.assert_allclose(orc.fused_head(h, Wu, y, Wu), orc.top_error(h @ Wu.T, y, Wu), rtol=1e-12,
+                               atol=1e-13)
