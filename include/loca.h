@@ -93,7 +93,8 @@ typedef enum {
   LOCA_OP_REALIZATION_ERROR = 8,
   LOCA_OP_CREDIT_GRAM = 9,
   LOCA_OP_FEEDBACK_FIT_PRIMAL = 10,
-  LOCA_OP_FEEDBACK_FIT_LARGE = 11
+  LOCA_OP_FEEDBACK_FIT_LARGE = 11,
+  LOCA_OP_FUSED_HEAD = 12
 } loca_op;
 
 /* Per (block, micro-batch) scalars of the scale-normalised step (Eq. 10).
@@ -440,10 +441,37 @@ loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t
                                        float* y_out, int64_t y_bstride, loca_mb* mb_out, void* ws,
                                        size_t ws_bytes);
 
+/* ---------------------------------------------------------------------------
+ * Fused LM head ("Local Targets", Eq. 4, with Lemma S3.1's head error; the head applied
+ * once per top error, Section S11): from the final hidden states instead of stored logits,
+ *   out_t = w_t ( sum_v softmax(z_t)_v Vm[v, :] - Vm[y_t, :] ),   z_t = W_u h_t,
+ * i.e. out = E Vm with E_t = w_t (softmax(z_t) - onehot(y_t)).  The logits are formed on the
+ * matrix cores tile by tile (bf16 operands, fp32 accumulation) under an online softmax and
+ * never stored; P is applied as bf16 hi + lo parts (about 16 significant bits); the
+ * vocabulary ranges are combined in a fixed order in float64.
+ *   Vm = W_u       -> out = e, the top error of the paper's order (loca_top_error's output,
+ *                     for loca_credit_from_top_error);
+ *   Vm = [A~_1 | ... | A~_L] (bf16) -> out = [Y_1 | ... | Y_L], every block's coordinates.
+ * h : n x d bf16, row stride ldh (ldh % 8 == 0, 16-byte aligned base).
+ * wu : V x d bf16, rows packed (row stride d), 16-byte aligned.
+ * labels : n int32 in [0, V).  w : n float loss weights, or NULL (= 1).
+ * vm : V x c bf16, row stride ld_vm >= c.   out : n x c float, row stride ld_out >= c.
+ * dev_info : one int32: 0, or 1 + the smallest row whose label is out of range (that
+ *            row's label term is dropped), or LOCA_INFO_NONFINITE when a token's softmax
+ *            sum is not finite (non-finite h or W_u), which takes precedence.
+ * Cost: c / 128 passes of the logits product when c > 128 (64 when c <= 64).
+ * Limits: d % 8 == 0 (LOCA_E_UNSUPPORTED otherwise), c <= 2^24.  Workspace:
+ * LOCA_OP_FUSED_HEAD with n, C = V and k = c.
+ * ------------------------------------------------------------------------- */
+loca_status loca_fused_head(loca_stream_t stream, int64_t n, int64_t V, int64_t d, int64_t c, const void* h,
+                            int64_t ldh, const void* wu, const int32_t* labels, const float* w,
+                            const void* vm, int64_t ld_vm, float* out, int64_t ld_out, int32_t* dev_info,
+                            void* ws, size_t ws_bytes);
+
 /* Workspace bytes for an entry point with the given sizes (nb = blocks, or nm
  * matrices for LOCA_OP_LOWRANK_TRUNCATE; k = kp there; n = np for
  * LOCA_OP_FEEDBACK_FIT and LOCA_OP_FEEDBACK_FIT_PRIMAL, n = np and r_a = l for
- * LOCA_OP_FEEDBACK_FIT_LARGE; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
+ * LOCA_OP_FEEDBACK_FIT_LARGE; C = V and k = c for LOCA_OP_FUSED_HEAD; C = V for LOCA_OP_TOP_ERROR; r_a = r_prev for
  * LOCA_OP_REALIZATION_ERROR).  `acc` selects the precision mode.  Unused arguments
  * may be 0. */
 size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t k, int64_t C,

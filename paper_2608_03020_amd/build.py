@@ -9,7 +9,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIBDIR = os.path.join(HERE, "lib")
 LIB = os.path.join(LIBDIR, "libloca.so")
 SOURCES = ["loca_api.hip", "k_error.hip", "k_gram.hip", "k_chol.hip", "k_trunc.hip", "k_calib.hip", "k_head.hip",
-           "k_subspace.hip"]
+           "k_subspace.hip", "k_fused.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

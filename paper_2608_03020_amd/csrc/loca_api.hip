@@ -60,6 +60,7 @@ size_t loca_workspace_size(loca_op op, int64_t nb, int64_t n, int64_t d, int64_t
     case LOCA_OP_FEEDBACK_FIT: return d < 1 || n < 1 || n > 64 ? 0 : feedback_fit_ws(nb, d, n, k);
     case LOCA_OP_FEEDBACK_FIT_PRIMAL:
       return d < 1 || n < 1 || n > kMaxKpTrunc ? 0 : feedback_fit_primal_ws(nb, d, n, k);
+    case LOCA_OP_FUSED_HEAD: return n < 1 || C < 1 || k < 1 ? 0 : fused_head_ws(n, C, k);
     case LOCA_OP_FEEDBACK_FIT_LARGE:
       return d < 1 || n < 1 || r_a < 1 || r_a > kMaxKpTrunc ? 0 : feedback_fit_large_ws(nb, d, n, k, r_a);
     case LOCA_OP_TOP_ERROR: return n < 1 || d < 1 || C < 1 ? 0 : top_error_ws(n, C, d);
@@ -344,6 +345,24 @@ loca_status loca_feedback_fit_large(loca_stream_t stream, int64_t nb, int64_t d,
   CalibArgs a{(hipStream_t)stream, nb, d, np, k, e, g, g_bstride, beta, wu, wu_dtype, vocab, bt_out, bt_bstride,
               at_out, at_bstride, vk_out, vk_bstride, sigma_out, alpha_out, dev_info, (char*)ws, true, l, q, omega};
   return from_hip(launch_feedback_fit_large(a));
+}
+
+loca_status loca_fused_head(loca_stream_t stream, int64_t n, int64_t V, int64_t d, int64_t c, const void* h,
+                            int64_t ldh, const void* wu, const int32_t* labels, const float* w, const void* vm,
+                            int64_t ld_vm, float* out, int64_t ld_out, int32_t* dev_info, void* ws,
+                            size_t ws_bytes) {
+  if (n < 1 || V < 1 || d < 1 || c < 1) return LOCA_E_ARG;
+  if (!h || !wu || !labels || !vm || !out || !dev_info) return LOCA_E_ARG;
+  if (ldh < d || ld_vm < c || ld_out < c) return LOCA_E_ARG;
+  if (!aligned(h, 16) || !aligned(wu, 16) || ldh % 8 != 0) return LOCA_E_ARG;
+  if (d % 8 != 0) return LOCA_E_UNSUPPORTED;
+  if (n > (int64_t)INT32_MAX - 1 || V > (int64_t)INT32_MAX - 128 || c > ((int64_t)1 << 24)) return LOCA_E_UNSUPPORTED;
+  if (((n + 127) / 128) * ((c + 63) / 64) * kMaxFusedSplits > (int64_t)INT32_MAX) return LOCA_E_UNSUPPORTED;
+  loca_status st = check_ws(ws, ws_bytes, fused_head_ws(n, V, c));
+  if (st != LOCA_OK) return st;
+  FusedArgs a{(hipStream_t)stream, n, V, d, c, (const uint16_t*)h, ldh, (const uint16_t*)wu, labels, w,
+              (const uint16_t*)vm, ld_vm, out, ld_out, dev_info, (char*)ws};
+  return from_hip(launch_fused_head(a));
 }
 
 loca_status loca_top_error(loca_stream_t stream, int64_t n, int64_t V, int64_t d, const void* logits,

@@ -182,5 +182,21 @@ hipError_t launch_lowrank_product(hipStream_t s, int64_t nmat, int64_t rows, int
                                   const float* R, int64_t r_bstride, int64_t r_group, int64_t r_ld,
                                   float* out, int64_t out_bstride);
 
+// The fused LM head ("Local Targets", Eq. 4; Section S11): out = E Vm with the logits formed
+// in-kernel and never stored.
+constexpr int kMaxFusedSplits = 64;  // vocabulary ranges combined per token
+struct FusedArgs {
+  hipStream_t stream;
+  int64_t n, V, d, c;
+  const uint16_t* h; int64_t ldh;
+  const uint16_t* wu;
+  const int32_t* labels; const float* w;
+  const uint16_t* vm; int64_t ld_vm;
+  float* out; int64_t ld_out;
+  int32_t* dev_info; char* ws;
+};
+size_t fused_head_ws(int64_t n, int64_t V, int64_t c);
+hipError_t launch_fused_head(const FusedArgs& a);
+
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 }  // namespace loca

@@ -20,12 +20,13 @@ LOCA_INFO_NONFINITE = -1
 LOCA_INFO_BASIS_RANK = -2
 (LOCA_OP_ERROR_TARGETS, LOCA_OP_ACCUMULATE_STATS, LOCA_OP_RIDGE_SOLVE, LOCA_OP_LOWRANK_TRUNCATE,
  LOCA_OP_RIDGE_SOLVE_PROJECTED, LOCA_OP_FEEDBACK_FIT, LOCA_OP_TOP_ERROR, LOCA_OP_CREDIT_FROM_TOP_ERROR,
- LOCA_OP_REALIZATION_ERROR, LOCA_OP_CREDIT_GRAM, LOCA_OP_FEEDBACK_FIT_PRIMAL, LOCA_OP_FEEDBACK_FIT_LARGE) = range(12)
+ LOCA_OP_REALIZATION_ERROR, LOCA_OP_CREDIT_GRAM, LOCA_OP_FEEDBACK_FIT_PRIMAL, LOCA_OP_FEEDBACK_FIT_LARGE,
+ LOCA_OP_FUSED_HEAD) = range(13)
 
 ENTRY_POINTS = ("loca_error_targets", "loca_accumulate_stats", "loca_ridge_solve", "loca_lowrank_truncate",
                 "loca_ridge_solve_projected", "loca_dense_targets", "loca_feedback_fit", "loca_top_error",
                 "loca_credit_from_top_error", "loca_error_targets_noalloc", "loca_realization_error",
-                "loca_credit_gram", "loca_feedback_fit_primal", "loca_feedback_fit_large")
+                "loca_credit_gram", "loca_feedback_fit_primal", "loca_feedback_fit_large", "loca_fused_head")
 EXPORTED = ENTRY_POINTS + ("loca_workspace_size", "loca_status_str", "loca_version",
                            "loca_error_targets_noalloc_max_bytes", "loca_credit_gram_ld")
 
@@ -80,6 +81,8 @@ def load():
     lib.loca_feedback_fit.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _D, _VP, _I, _I64, _VP, _I64,
                                       _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_feedback_fit_primal.argtypes = lib.loca_feedback_fit.argtypes
+    lib.loca_fused_head.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _I64, _VP, _I64, _VP,
+                                    _VP, _SZ]
     lib.loca_feedback_fit_large.argtypes = [_VP, _I64, _I64, _I64, _I64, _I64, _I64, _VP, _VP, _I64, _VP, _D, _VP, _I,
                                             _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _VP, _VP, _SZ]
     lib.loca_top_error.argtypes = [_VP, _I64, _I64, _I64, _VP, _I, _I64, _VP, _VP, _VP, _I, _VP, _I64, _VP, _VP,
@@ -332,6 +335,19 @@ def loca_feedback_fit_large(e, g, omega, q: int, beta: float, bt_out, sigma_out,
         at_out.stride(0) if at_out is not None else 0, _ptr(vk_out), vk_out.stride(0) if vk_out is not None else 0,
         _ptr(sigma_out), _ptr(alpha_out), _ptr(dev_info), _ptr(ws), ws.numel() * ws.element_size())
     _check("loca_feedback_fit_large", st)
+
+
+def loca_fused_head(h, wu, labels, vm, out, dev_info, ws, *, w=None, stream=None):
+    """h (n, d) bf16; wu (V, d) bf16; labels (n,) int32; vm (V, c) bf16; out (n, c) float32:
+    out_t = w_t (softmax(W_u h_t)^T Vm - Vm[y_t]), the logits never stored."""
+    n, d = h.shape
+    V = wu.shape[0]
+    c = vm.shape[1]
+    st = load().loca_fused_head(
+        _stream(stream), n, V, d, c, _ptr(h, rows=False), h.stride(0), _ptr(wu), _ptr(labels), _ptr(w),
+        _ptr(vm, rows=False), vm.stride(0), _ptr(out, rows=False), out.stride(0), _ptr(dev_info), _ptr(ws),
+        ws.numel() * ws.element_size())
+    _check("loca_fused_head", st)
 
 
 def loca_top_error(logits, labels, wu, e_out, dev_info, ws, *, w=None, stream=None):

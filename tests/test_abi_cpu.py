@@ -254,6 +254,26 @@ def test_feedback_fit_large_rejects(lib):
     assert so.loca_workspace_size(lib.LOCA_OP_FEEDBACK_FIT_LARGE, 1, 600, 256, 8, 0, 0, 0, lib.LOCA_F32) == 0
 
 
+def test_fused_head_rejects(lib):
+    so = lib.load()
+
+    def call(n=10, V=100, d=64, c=8, h=FAKE, ldh=64, wu=FAKE, y=FAKE, vm=FAKE, ldvm=8, out=FAKE, ldo=8, ws=None,
+             wsb=0):
+        return so.loca_fused_head(None, n, V, d, c, h, ldh, wu, y, None, vm, ldvm, out, ldo, FAKE, ws, wsb)
+
+    assert call(h=None) == lib.LOCA_E_ARG
+    assert call(ldh=60) == lib.LOCA_E_ARG                 # ldh >= d
+    assert call(ldh=68) == lib.LOCA_E_ARG                 # ldh % 8 == 0 (16-byte rows)
+    assert call(h=FAKE + 2) == lib.LOCA_E_ARG             # 16-byte aligned h
+    assert call(ldvm=4) == lib.LOCA_E_ARG
+    assert call(ldo=4) == lib.LOCA_E_ARG
+    assert call(d=60, ldh=64) == lib.LOCA_E_UNSUPPORTED   # d % 8 == 0
+    assert call() == lib.LOCA_E_WORKSPACE
+    need = so.loca_workspace_size(lib.LOCA_OP_FUSED_HEAD, 1, 10, 64, 8, 100, 0, 0, lib.LOCA_F32)
+    assert need >= 2 * 8 * 128                            # holds Vm^T padded to whole vocabulary chunks
+    assert call(ws=FAKE, wsb=need - 1) == lib.LOCA_E_WORKSPACE
+
+
 def test_top_error_rejects(lib):
     so = lib.load()
 
