@@ -320,6 +320,7 @@ def next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream):
     del E, G, Wu, bt, at, ws, omega
     torch.cuda.empty_cache()
     out["paper_order_head"] = paper_order_head(stream)
+    out["fused_head"] = fused_head_rows(stream)
     return out
 
 
@@ -378,6 +379,64 @@ def paper_order_head(stream, L=24, d=896, n=4096, V=151936, k=64, reps=5):
                          "frac": ach / BF16_PEAK_TFLOPS, "traffic": None,
                          "kernel": "loca_top_error (softmax statistics, the split-K product e = W_u^T E, reduction)",
                          "algorithmic_flops_per_launch": fl, "avg_launch_ms": t_top}}
+
+
+def fused_head_rows(stream, n=4096, V=151936, reps=5):
+    """The fused LM head from hidden states (logits never stored) on the two full-vocabulary
+    shapes: the folded order of one Qwen2.5-3B-width block (d = 2048, Vm = A~, k = 64) and
+    the paper's order at the 0.5B width (d = 896, Vm = W_u: the top error, then V_k^T e for
+    24 blocks)."""
+    import numpy as np
+    import torch
+    from paper_2608_03020_amd import loca
+    rows = {}
+    for name, d, k, L in (("folded_d2048_k64", 2048, 64, 1), ("paper_order_d896_L24_k64", 896, 64, 24)):
+        g = torch.Generator(device="cuda")
+        g.manual_seed(12)
+        h = (torch.randn((n, d), generator=g, device="cuda") * 2.0).to(torch.bfloat16)
+        y = torch.randint(0, V, (n,), generator=g, device="cuda", dtype=torch.int32)
+        Wu = (torch.randn((V, d), generator=g, device="cuda") / np.sqrt(d)).to(torch.bfloat16)
+        paper = name.startswith("paper")
+        if paper:
+            Vm = Wu
+            Vk = torch.randn((L, d, k), generator=g, device="cuda") / np.sqrt(d)
+            Bt = torch.randn((L, k, d), generator=g, device="cuda") / np.sqrt(k)
+            Y = torch.empty((L, n, k), dtype=torch.float32, device="cuda")
+            mb = loca.new_mb(L, "cuda")
+        else:
+            Vm = (Wu.float() @ (torch.randn((d, k), generator=g, device="cuda") / np.sqrt(d))).to(torch.bfloat16)
+        c = Vm.shape[1]
+        out = torch.empty((n, c), dtype=torch.float32, device="cuda")
+        info = torch.zeros(1, dtype=torch.int32, device="cuda")
+        nbytes = loca.workspace_size(loca.LOCA_OP_FUSED_HEAD, 1, n, d, c, V)
+        if paper:
+            nbytes = max(nbytes, loca.workspace_size(loca.LOCA_OP_CREDIT_FROM_TOP_ERROR, L, n, d, k))
+        ws = loca.alloc_workspace(nbytes, "cuda")
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+
+        def call(s):
+            if s < reps:
+                ev[s][0].record(stream)
+            loca.loca_fused_head(h, Wu, y, Vm, out, info, ws)
+            if s < reps:
+                ev[s][1].record(stream)
+            if paper:
+                loca.loca_credit_from_top_error(out, Vk, Bt, Y, mb, ws)
+        ms = time_steps(call, reps, 1)
+        t_f = sum(a[0].elapsed_time(a[1]) for a in ev) / reps
+        fl = 2.0 * n * V * (d + c)
+        ach = fl / (t_f * 1e-3) / 1e12
+        rows[name] = {"config": {"tokens": n, "vocab": V, "d": d, "columns": c, "blocks": L, "credit_rank": k},
+                      "ms_per_call": ms, "ms_fused_head": t_f, "info_ok": int(info.item()) == 0,
+                      "roofline": {"bound": "mfma", "achieved": ach, "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                   "frac": ach / BF16_PEAK_TFLOPS, "traffic": None,
+                                   "kernel": "loca_fused_head (logits on the matrix cores, online softmax, E Vm)",
+                                   "algorithmic_flops_per_launch": fl, "avg_launch_ms": t_f}}
+        print(f"[bench] next: fused head {name}: {t_f:.2f} ms ({ach / BF16_PEAK_TFLOPS:.3f} of bf16 peak)",
+              file=sys.stderr, flush=True)
+        del h, Wu, Vm, out, ws
+        torch.cuda.empty_cache()
+    return rows
 
 
 def cpu_baseline(cfg, n_sample):

@@ -459,9 +459,10 @@ loca_status loca_credit_from_top_error(loca_stream_t stream, int64_t nb, int64_t
  * dev_info : one int32: 0, or 1 + the smallest row whose label is out of range (that
  *            row's label term is dropped), or LOCA_INFO_NONFINITE when a token's softmax
  *            sum is not finite (non-finite h or W_u), which takes precedence.
- * Cost: c / 128 passes of the logits product when c > 128 (64 when c <= 64).
- * Limits: d % 8 == 0 (LOCA_E_UNSUPPORTED otherwise), c <= 2^24.  Workspace:
- * LOCA_OP_FUSED_HEAD with n, C = V and k = c.
+ * Cost: ceil(c / 64) passes of the logits product (the folded order with k <= 64 takes
+ * one; the paper's order, c = d, takes d / 64: it trades logits storage for recomputation).
+ * Limits: d % 8 == 0 (LOCA_E_UNSUPPORTED otherwise), c <= 2^24, V, d, ldh <= 2^23.
+ * Workspace: LOCA_OP_FUSED_HEAD with n, C = V and k = c.
  * ------------------------------------------------------------------------- */
 loca_status loca_fused_head(loca_stream_t stream, int64_t n, int64_t V, int64_t d, int64_t c, const void* h,
                             int64_t ldh, const void* wu, const int32_t* labels, const float* w,

@@ -8,34 +8,64 @@
 //
 // The logits are never stored.  A workgroup owns 128 tokens, a tile of at most CT columns
 // of Vm and a contiguous range of the vocabulary, and walks that range in chunks of 128:
-//   1. z (128 x 128) = h_rows W_u[chunk]^T on the matrix cores (v_mfma_f32_32x32x16_bf16,
-//      fp32 accumulation), the two operands staged through LDS in 32-wide slices of d;
-//   2. an online softmax per token: the running maximum m and sum s (fp32) are updated with
-//      the chunk, the accumulated output is rescaled by exp(m_old - m_new), and
-//      P = exp(z - m_new) is split into bf16 hi + lo parts (about 16 significant bits);
-//   3. out += (P_hi + P_lo) Vm[chunk] on the matrix cores (Vm exact in bf16).
+//   1. z^T (128 x 128) = W_u[chunk] h_rows^T on the matrix cores (v_mfma_f32_32x32x16_bf16,
+//      fp32 accumulation), both operands copied straight into LDS (buffer loads to LDS) in
+//      64-wide slices of d through a three-slot ring that runs across chunk boundaries;
+//   2. an online softmax per token, in registers: the running maximum m and sum s (fp32)
+//      are updated with the chunk, the accumulated output is rescaled by exp(m_old - m_new),
+//      and P = exp(z - m_new) is split into bf16 hi + lo parts (about 16 significant bits);
+//   3. out += (P_hi + P_lo) Vm[chunk] on the matrix cores (Vm exact in bf16), P taken from
+//      the registers of step 1 and the Vm^T slice from LDS.
 // Each vocabulary range leaves (m, s) per token and its partial output; a second kernel
 // combines the ranges in a fixed order in float64 and subtracts the label term.  Columns of
-// Vm beyond one tile recompute the logits (c / CT passes over W_u).
+// Vm beyond one 64-wide tile recompute the logits (c / 64 passes over W_u).
 #include "loca_launch.h"
 
 namespace loca {
 
 namespace {
 
-constexpr int kFT = 256;       // threads: 4 waves as 2 x 2
-constexpr int kFR = 128;       // token rows per workgroup
-constexpr int kFV = 128;       // vocabulary per chunk
-constexpr int kFK = 32;        // hidden width per staging slice
-constexpr int kFLD = kFK + 8;  // bf16 per LDS row of an h / W_u slice (80 bytes)
-constexpr int kZLD = kFV + 4;  // 32-bit words per LDS row of the logits / packed P tile
-constexpr int kVLD = kFV + 8;  // bf16 per LDS row of the transposed right operand
+constexpr int kFT = 256;        // threads: 4 waves, (vocabulary half wv) x (token half wt)
+constexpr int kFR = 128;        // tokens per tile
+constexpr int kFV = 128;        // vocabulary per chunk
+constexpr int kFK = 64;         // hidden width per stage
+constexpr int kFStages = 3;     // ring slots: two stages in flight while one is read
+constexpr int kFStage = (kFV + kFR) * kFK * 2;  // bytes per stage: W_u rows, then h rows (128 B each)
+constexpr int kFCopies = kFStage / 16 / kFT;     // 16-byte copies per thread per stage
+
+// A stage holds 256 rows of 128 bytes (64 bf16 of d): rows 0..127 the chunk's W_u rows,
+// rows 128..255 the tile's h rows.  Chunk c (16 bytes) of row r sits at position
+// c ^ ((r >> 1) & 7), so that the 16 lanes of a half wave reading one chunk of 16
+// consecutive rows hit 16 distinct bank groups.
+LOCA_DEV int fz_swz(int r) { return (r >> 1) & 7; }
+// The Vm^T slice: CT rows (columns of Vm) of 256 bytes (128 vocabulary entries), chunk c
+// of row r at position c ^ (r & 15).
+LOCA_DEV int fv_swz(int r) { return r & 15; }
 
 LOCA_DEV uint16_t rne_bf16(float f) {
   const uint32_t u = __float_as_uint(f);
   return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
+// (m, s) of two disjoint parts of a row, combined
+LOCA_DEV void fz_combine(float& m, float& s, float m2, float s2) {
+  if (s2 == 0.f) return;
+  if (s == 0.f) {
+    m = m2;
+    s = s2;
+    return;
+  }
+  const float mm = fmaxf(m, m2);
+  s = s * __expf(m - mm) + s2 * __expf(m2 - mm);
+  m = mm;
+}
+
+// The logits are formed transposed, z^T = W_u[chunk] h_tile^T (vocabulary x tokens), so
+// that lane l of a 32 x 32 result block holds token l % 32 and 16 vocabulary entries:
+// the softmax statistics of a token stay within a lane pair (l, l ^ 32) and the two
+// waves that split the chunk's vocabulary, and the exponentials of a block are already
+// the matrix-core operand of the product with Vm (the sum over the vocabulary taken in
+// the order the result layout gives).
 template <int CT>
 __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_t d, int64_t c,
                                                     const uint16_t* __restrict__ h, int64_t ldh,
@@ -43,14 +73,12 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
                                                     const uint16_t* __restrict__ vmt, int64_t ldvt, int ntr, int nct,
                                                     int64_t vper, float* __restrict__ part_o,
                                                     float2* __restrict__ part_ms) {
-  __shared__ __attribute__((aligned(16))) uint16_t sH[2][kFR * kFLD];
-  __shared__ __attribute__((aligned(16))) uint16_t sW[2][kFV * kFLD];
-  __shared__ __attribute__((aligned(16))) uint32_t sZ[kFR * kZLD];
-  __shared__ __attribute__((aligned(16))) uint16_t sVt[CT * kVLD];
-  __shared__ float sAl[kFR];
-  constexpr int NQ = CT / 64;                  // 32-column output blocks per wave
-  constexpr int NPV = CT * kFV / 8 / kFT;      // 16-byte chunks of the Vm^T slice per thread
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, wi = wid >> 1, wj = wid & 1;
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[kFStages * kFStage];
+  __shared__ __attribute__((aligned(1024))) uint8_t sVt[CT * 256];
+  __shared__ float2 sEx[2][kFR];
+  constexpr int NQ = CT / 32;            // 32-column output blocks per wave
+  constexpr int NV = CT * 256 / 16 / kFT;  // 16-byte copies of the Vm^T slice per thread
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, wv = wid >> 1, wt = wid & 1;
   const int l32 = lane & 31, lh = lane >> 5;
   // tiles that share a vocabulary range are consecutive within an XCD (W_u read once there)
   const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
@@ -58,179 +86,250 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
   const int64_t r0 = (int64_t)rt * kFR, c0 = (int64_t)ct * CT;
   const int64_t vb = (int64_t)sp * vper, ve = (vb + vper < V) ? vb + vper : V;
   const int nks = (int)((d + kFK - 1) / kFK);
+  const int nch = (int)((ve - vb + kFV - 1) / kFV);
+  const int total = nch * nks;  // stages of this workgroup
+
+  const int64_t nrow = (n - r0 < kFR) ? n - r0 : kFR;
+  const i32x4_t rsH = buffer_rsrc(h + r0 * ldh, (uint32_t)(nrow * ldh * 2));
+  const int64_t ncol = (c - c0 < CT) ? c - c0 : CT;
+  const i32x4_t rsV = buffer_rsrc(vmt + c0 * ldvt, (uint32_t)(ncol * ldvt * 2));
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)(LOCA_LDS void*)ring;
+  const uint32_t vt_lds = (uint32_t)(uintptr_t)(LOCA_LDS void*)sVt;
+
+  // stage g = (chunk g / nks, slice g % nks) into ring slot g % 3: waves 0-1 copy the 128
+  // W_u rows, waves 2-3 the 128 h rows (wave-uniform); byte offsets fit 31 bits (V, d,
+  // ldh <= 2^23 are checked by the caller)
+  const int wq = __builtin_amdgcn_readfirstlane(wid);
+  auto issue_stage = [&](int g) {
+    const int64_t v0 = vb + (int64_t)(g / nks) * kFV;
+    const int k0 = (g % nks) * kFK;
+    const uint32_t slot = ring_lds + (uint32_t)((g % kFStages) * kFStage);
+    if (wq < 2) {
+      const int64_t nvr = (V - v0 < kFV) ? V - v0 : kFV;
+      const i32x4_t rsW = buffer_rsrc(wu + v0 * d, (uint32_t)(nvr * d * 2));
+#pragma unroll
+      for (int j = 0; j < kFCopies; ++j) {
+        const int blk = wq * kFCopies + j;           // 1 KB of LDS: rows 8 blk .. 8 blk + 7
+        const int row = 8 * blk + (lane >> 3);
+        const int k = k0 + 8 * ((lane & 7) ^ fz_swz(row));
+        const uint32_t off = k < (int)d ? 2u * (uint32_t)(row * (int)d + k) : kBufOutside;
+        lds_dma16_buf(off, rsW, slot + (uint32_t)blk * 1024u);
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kFCopies; ++j) {
+        const int blk = wq * kFCopies + j;           // rows 128 .. 255 of the stage
+        const int hrow = 8 * (blk - 2 * kFCopies) + (lane >> 3);
+        const int k = k0 + 8 * ((lane & 7) ^ fz_swz(kFV + hrow));
+        const uint32_t off = k < (int)d ? 2u * (uint32_t)(hrow * (int)ldh + k) : kBufOutside;
+        lds_dma16_buf(off, rsH, slot + (uint32_t)blk * 1024u);
+      }
+    }
+  };
+  // the chunk's Vm^T slice (CT columns of Vm x 128 vocabulary entries; zero past V)
+  auto issue_vt = [&](int64_t v0) {
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int blk = wq * NV + j;                   // 1 KB: rows 4 blk .. 4 blk + 3
+      const int row = 4 * blk + (lane >> 4);
+      const uint32_t off = 2u * (uint32_t)(row * (int)ldvt + (int)v0 + 8 * ((lane & 15) ^ fv_swz(row)));
+      lds_dma16_buf(off, rsV, vt_lds + (uint32_t)blk * 1024u);
+    }
+  };
+  // wait until at most `a` of this thread's copies are outstanding (a from a small set)
+  auto wait_at_most = [&](int a) {
+    switch (a) {
+      case 0: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;
+      case 4: __builtin_amdgcn_s_waitcnt(vmcnt_imm(4)); break;
+      case 8: __builtin_amdgcn_s_waitcnt(vmcnt_imm(8)); break;
+      case 12: __builtin_amdgcn_s_waitcnt(vmcnt_imm(12)); break;
+      default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(16)); break;
+    }
+  };
 
   f32x16_t o[2][NQ];
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
     for (int q = 0; q < NQ; ++q)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[m][q][r] = 0.f;
-  float m_run = -__builtin_inff(), s_run = 0.f;  // of token row tid >> 1 (both threads of the pair)
+      for (int r = 0; r < 16; ++r) o[mt][q][r] = 0.f;
+  float m_run[2] = {-__builtin_inff(), -__builtin_inff()}, s_run[2] = {0.f, 0.f};  // token l32 of block mt
+  f32x16_t z[2][2];
 
-  uint4 ph[2], pw[2];
-  auto gload = [&](int64_t v0, int ks) {
+  issue_stage(0);
+  if (total > 1) issue_stage(1);
+  for (int g = 0; g < total; ++g) {
+    const int ks = g % nks;
+    // copies issued after stage g's: stage g + 1 and, when g - 1 began a chunk, its Vm^T slice
+    wait_at_most((g + 1 < total ? kFCopies : 0) + (g >= 1 && (g - 1) % nks == 0 ? NV : 0));
+    __syncthreads();  // every thread's copies of stage g landed; slot (g + 2) % 3 and sVt free
+    if (ks == 0) {
+      issue_vt(vb + (int64_t)(g / nks) * kFV);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int q = tid + kFT * i, row = q >> 2;
-      const int64_t k = (int64_t)ks * kFK + 8 * (q & 3);
-      const bool kin = k < d;
-      ph[i] = (r0 + row < n && kin) ? *(const uint4*)(h + (r0 + row) * ldh + k) : make_uint4(0, 0, 0, 0);
-      pw[i] = (v0 + row < V && kin) ? *(const uint4*)(wu + (v0 + row) * d + k) : make_uint4(0, 0, 0, 0);
+      for (int mv = 0; mv < 2; ++mv)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) z[mv][mt][r] = 0.f;
     }
-  };
-  auto lstore = [&](int buf) {
+    if (g + 2 < total) issue_stage(g + 2);
+    // 1. z^T += W_u[chunk, slice] h[tile, slice]^T
+    const uint8_t* st = ring + (g % kFStages) * kFStage;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int q = tid + kFT * i, row = q >> 2, part = q & 3;
-      *(uint4*)&sH[buf][row * kFLD + 8 * part] = ph[i];
-      *(uint4*)&sW[buf][row * kFLD + 8 * part] = pw[i];
-    }
-  };
-
-  for (int64_t v0 = vb; v0 < ve; v0 += kFV) {
-    // the chunk's slice of Vm^T (CT x 128; padded rows of Vm^T hold zeros past V)
-    uint4 pv[NPV];
+    for (int kk = 0; kk < kFK / 16; ++kk) {
+      bf16x8_t a[2], b[2];
+      const int ch = 2 * kk + lh;  // 16-byte chunk of the row: k = 16 kk + 8 lh
 #pragma unroll
-    for (int i = 0; i < NPV; ++i) {
-      const int q = tid + kFT * i, row = q >> 4, part = q & 15;
-      pv[i] = (c0 + row < c) ? *(const uint4*)(vmt + (c0 + row) * ldvt + v0 + 8 * part) : make_uint4(0, 0, 0, 0);
-    }
-    // 1. logits of the chunk
-    f32x16_t z[2][2];
-#pragma unroll
-    for (int m = 0; m < 2; ++m)
-#pragma unroll
-      for (int q = 0; q < 2; ++q)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) z[m][q][r] = 0.f;
-    gload(v0, 0);
-    lstore(0);
-    __syncthreads();
-    for (int ks = 0; ks < nks; ++ks) {
-      const int buf = ks & 1;
-      if (ks + 1 < nks) gload(v0, ks + 1);
-#pragma unroll
-      for (int kk = 0; kk < kFK; kk += 16) {
-        bf16x8_t a[2], b[2];
-#pragma unroll
-        for (int m = 0; m < 2; ++m) a[m] = *(const bf16x8_t*)&sH[buf][(wi * 64 + 32 * m + l32) * kFLD + kk + 8 * lh];
-#pragma unroll
-        for (int q = 0; q < 2; ++q) b[q] = *(const bf16x8_t*)&sW[buf][(wj * 64 + 32 * q + l32) * kFLD + kk + 8 * lh];
-#pragma unroll
-        for (int m = 0; m < 2; ++m)
-#pragma unroll
-          for (int q = 0; q < 2; ++q) z[m][q] = mfma32(a[m], b[q], z[m][q]);
+      for (int mv = 0; mv < 2; ++mv) {
+        const int row = wv * 64 + 32 * mv + l32;
+        a[mv] = *(const bf16x8_t*)(st + row * 128 + 16 * (ch ^ fz_swz(row)));
       }
-      if (ks + 1 < nks) lstore(buf ^ 1);
-      __syncthreads();
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const int row = kFV + wt * 64 + 32 * mt + l32;
+        b[mt] = *(const bf16x8_t*)(st + row * 128 + 16 * (ch ^ fz_swz(row)));
+      }
+#pragma unroll
+      for (int mv = 0; mv < 2; ++mv)
+#pragma unroll
+        for (int mt = 0; mt < 2; ++mt) z[mv][mt] = mfma32(a[mv], b[mt], z[mv][mt]);
     }
-    // the previous chunk's readers of sZ and sVt have passed the syncs above
+    if (ks != nks - 1) continue;
+
+    // 2. online softmax over the chunk.  Entry r of lane l in block (mv, mt): vocabulary
+    // v0 + 64 wv + 32 mv + 8 (r >> 2) + 4 lh + (r & 3), token 64 wt + 32 mt + l32.
+    const int64_t v0 = vb + (int64_t)(g / nks) * kFV;
+    const int nv = (V - v0 < kFV) ? (int)(V - v0) : kFV;
+    const bool full = nv == kFV;
+    auto valid = [&](int mv, int r) { return full || 64 * wv + 32 * mv + 8 * (r >> 2) + 4 * lh + (r & 3) < nv; };
+    float lm[2], ls[2];
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int mt = 0; mt < 2; ++mt) {
+      float mx = -__builtin_inff();
 #pragma unroll
-      for (int q = 0; q < 2; ++q)
+      for (int mv = 0; mv < 2; ++mv)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          sZ[(wi * 64 + 32 * m + mfma32_row(lane, r)) * kZLD + wj * 64 + 32 * q + l32] = __float_as_uint(z[m][q][r]);
+          if (valid(mv, r)) mx = fmaxf(mx, z[mv][mt][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      float sm = 0.f;
+      if (mx > -__builtin_inff()) {
 #pragma unroll
-    for (int i = 0; i < NPV; ++i) {
-      const int q = tid + kFT * i, row = q >> 4, part = q & 15;
-      *(uint4*)&sVt[row * kVLD + 8 * part] = pv[i];
-    }
-    __syncthreads();
-    // 2. online softmax: two threads per token, interleaved 4-column groups
-    {
-      const int row = tid >> 1, half = tid & 1;
-      const int nv = (V - v0 < kFV) ? (int)(V - v0) : kFV;
-      uint32_t* zr = sZ + row * kZLD;
-      float cm = -__builtin_inff();
+        for (int mv = 0; mv < 2; ++mv)
 #pragma unroll
-      for (int g = 0; g < 16; ++g) {
-        const int col = 8 * g + 4 * half;
-        const uint4 u = *(const uint4*)(zr + col);
-        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (col + e < nv) cm = fmaxf(cm, __uint_as_float(w4[e]));
+          for (int r = 0; r < 16; ++r)
+            if (valid(mv, r)) sm += __expf(z[mv][mt][r] - mx);
       }
-      cm = fmaxf(cm, __shfl_xor(cm, 1));
-      const float mn = fmaxf(m_run, cm);
-      const float al = __expf(m_run - mn);
-      float ps = 0.f;
-#pragma unroll
-      for (int g = 0; g < 16; ++g) {
-        const int col = 8 * g + 4 * half;
-        const uint4 u = *(const uint4*)(zr + col);
-        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
-        uint32_t pk[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float p = (col + e < nv) ? __expf(__uint_as_float(w4[e]) - mn) : 0.f;
-          ps += p;
-          const uint16_t hi = rne_bf16(p);
-          const uint16_t lo = rne_bf16(p - __uint_as_float((uint32_t)hi << 16));
-          pk[e] = (uint32_t)hi | ((uint32_t)lo << 16);
-        }
-        *(uint4*)(zr + col) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
-      }
-      ps += __shfl_xor(ps, 1);
-      s_run = s_run * al + ps;
-      m_run = mn;
-      if (half == 0) sAl[row] = al;
+      sm += __shfl_xor(sm, 32);
+      lm[mt] = mx;
+      ls[mt] = sm;
     }
-    __syncthreads();
-    // 3. rescale the output rows and add (P_hi + P_lo) Vm[chunk]
+    if (lh == 0)
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+      for (int mt = 0; mt < 2; ++mt) sEx[wv][wt * 64 + 32 * mt + l32] = make_float2(lm[mt], ls[mt]);
+    // the Vm^T slice of this chunk: issued at its first stage, followed by at most the
+    // stage copies of the chunk's other slices
+    if (nks == 1) wait_at_most(g + 2 < total ? kFCopies : 0);
+    else if (nks == 2) wait_at_most((g + 1 < total ? kFCopies : 0) + (g + 2 < total ? kFCopies : 0));
+    __syncthreads();
+    float al[2];
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt) {
+      const float2 e0 = sEx[0][wt * 64 + 32 * mt + l32], e1 = sEx[1][wt * 64 + 32 * mt + l32];
+      float cm = e0.x, cs = e0.y;
+      fz_combine(cm, cs, e1.x, e1.y);  // the same order in both waves
+      const float mn = fmaxf(m_run[mt], cm);
+      al[mt] = __expf(m_run[mt] - mn);
+      s_run[mt] = s_run[mt] * al[mt] + cs * __expf(cm - mn);
+      m_run[mt] = mn;
+    }
+    // rescale the output rows: row r of an output block is token 8 (r >> 2) + 4 lh + (r & 3)
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float al = sAl[wi * 64 + 32 * m + mfma32_row(lane, r)];
+        const float a_r = __shfl(al[mt], 8 * (r >> 2) + 4 * lh + (r & 3));
 #pragma unroll
-        for (int q = 0; q < NQ; ++q) o[m][q][r] *= al;
+        for (int q = 0; q < NQ; ++q) o[mt][q][r] *= a_r;
       }
+    // 3. out += (P_hi + P_lo) Vm[chunk]: k step (mv, ks2) takes the entries r = 8 ks2 .. 8 ks2 + 7
 #pragma unroll
-    for (int kv = 0; kv < kFV; kv += 16) {
-      bf16x8_t phi[2], plo[2], b[NQ];
+    for (int mv = 0; mv < 2; ++mv)
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        const uint32_t* src = sZ + (wi * 64 + 32 * m + l32) * kZLD + kv + 8 * lh;
-        const uint4 u0 = *(const uint4*)src, u1 = *(const uint4*)(src + 4);
-        const uint32_t wv[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
-        uint32_t hv[4], lv[4];
+      for (int ks2 = 0; ks2 < 2; ++ks2) {
+        bf16x8_t phi[2], plo[2], bv[NQ];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          hv[e] = (wv[2 * e] & 0xffffu) | (wv[2 * e + 1] << 16);
-          lv[e] = (wv[2 * e] >> 16) | (wv[2 * e + 1] & 0xffff0000u);
+        for (int mt = 0; mt < 2; ++mt) {
+          uint32_t hv[4], lv[4];
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) {
+            uint16_t hh[2], ll[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+              const int r = 8 * ks2 + 2 * e2 + u;
+              const float p = valid(mv, r) ? __expf(z[mv][mt][r] - m_run[mt]) : 0.f;
+              hh[u] = rne_bf16(p);
+              ll[u] = rne_bf16(p - __uint_as_float((uint32_t)hh[u] << 16));
+            }
+            hv[e2] = (uint32_t)hh[0] | ((uint32_t)hh[1] << 16);
+            lv[e2] = (uint32_t)ll[0] | ((uint32_t)ll[1] << 16);
+          }
+          phi[mt] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
+          plo[mt] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
         }
-        phi[m] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
-        plo[m] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
-      }
-#pragma unroll
-      for (int q = 0; q < NQ; ++q)
-        b[q] = *(const bf16x8_t*)&sVt[(wj * (CT / 2) + 32 * q + l32) * kVLD + kv + 8 * lh];
-#pragma unroll
-      for (int m = 0; m < 2; ++m)
+        // B entry e of lane (col, lh): vocabulary 64 wv + 32 mv + 16 ks2 + 8 (e >> 2) + 4 lh + (e & 3)
+        const int vb0 = 64 * wv + 32 * mv + 16 * ks2 + 4 * lh;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
-          o[m][q] = mfma32(phi[m], b[q], o[m][q]);
-          o[m][q] = mfma32(plo[m], b[q], o[m][q]);
+          const int row = 32 * q + l32;
+          const uint8_t* rp = sVt + row * 256;
+          const int va = vb0, vc = vb0 + 8;
+          const uint2 lo4 = *(const uint2*)(rp + 16 * ((va >> 3) ^ fv_swz(row)) + 2 * (va & 7));
+          const uint2 hi4 = *(const uint2*)(rp + 16 * ((vc >> 3) ^ fv_swz(row)) + 2 * (vc & 7));
+          bv[q] = __builtin_bit_cast(bf16x8_t, make_uint4(lo4.x, lo4.y, hi4.x, hi4.y));
         }
-    }
-  }
-  // this range's partial output and (m, s)
-  float* po = part_o + (int64_t)sp * n * c;
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+        for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
-    for (int q = 0; q < NQ; ++q)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = r0 + wi * 64 + 32 * m + mfma32_row(lane, r);
-        const int64_t col = c0 + wj * (CT / 2) + 32 * q + l32;
-        if (row < n && col < c) po[row * c + col] = o[m][q][r];
+          for (int q = 0; q < NQ; ++q) {
+            o[mt][q] = mfma32(phi[mt], bv[q], o[mt][q]);
+            o[mt][q] = mfma32(plo[mt], bv[q], o[mt][q]);
+          }
       }
-  if (ct == 0 && (tid & 1) == 0 && r0 + (tid >> 1) < n) part_ms[(int64_t)sp * n + r0 + (tid >> 1)] = make_float2(m_run, s_run);
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  __syncthreads();  // the ring is free: the two vocabulary halves' outputs meet there
+  float* red = (float*)ring;  // kFR x (CT + 4) floats
+  constexpr int RLD = CT + 4;
+  if (wv == 1)
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          red[(wt * 64 + 32 * mt + 8 * (r >> 2) + 4 * lh + (r & 3)) * RLD + 32 * q + l32] = o[mt][q][r];
+  __syncthreads();
+  if (wv == 0) {
+    float* po = part_o + (int64_t)sp * n * c;
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int tr = wt * 64 + 32 * mt + 8 * (r >> 2) + 4 * lh + (r & 3);
+          const int64_t row = r0 + tr, col = c0 + 32 * q + l32;
+          if (row < n && col < c) po[row * c + col] = o[mt][q][r] + red[tr * RLD + 32 * q + l32];
+        }
+    if (ct == 0 && lh == 0)
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) {
+        const int64_t row = r0 + wt * 64 + 32 * mt + l32;
+        if (row < n) part_ms[(int64_t)sp * n + row] = make_float2(m_run[mt], s_run[mt]);
+      }
+  }
 }
 
 // dev_info protocol: INT32_MAX while nothing is wrong; atomicMin with 1 + a bad row or with
@@ -305,7 +404,7 @@ struct FusedPlan {
 
 FusedPlan fused_plan(int64_t n, int64_t V, int64_t c) {
   FusedPlan p;
-  p.ct = c <= 64 ? 64 : 128;
+  p.ct = 64;  // a wider column tile holds more accumulators than the register file keeps
   p.ntr = (int)((n + kFR - 1) / kFR);
   p.nct = (int)((c + p.ct - 1) / p.ct);
   const int64_t tiles = (int64_t)p.ntr * p.nct, nchunk = (V + kFV - 1) / kFV;
@@ -340,12 +439,8 @@ hipError_t launch_fused_head(const FusedArgs& a) {
   k_vm_transpose<<<dim3((unsigned)((p.ldvt + 31) / 32), (unsigned)((a.c + 31) / 32)), 256, 0, st>>>(
       a.V, a.c, a.vm, a.ld_vm, vmt, p.ldvt);
   const unsigned grid = (unsigned)((int64_t)p.ntr * p.nct * p.nsp);
-  if (p.ct == 64)
-    k_fused_head<64><<<grid, kFT, 0, st>>>(a.n, a.V, a.d, a.c, a.h, a.ldh, a.wu, vmt, p.ldvt, p.ntr, p.nct, p.vper,
-                                            part_o, part_ms);
-  else
-    k_fused_head<128><<<grid, kFT, 0, st>>>(a.n, a.V, a.d, a.c, a.h, a.ldh, a.wu, vmt, p.ldvt, p.ntr, p.nct, p.vper,
-                                             part_o, part_ms);
+  k_fused_head<64><<<grid, kFT, 0, st>>>(a.n, a.V, a.d, a.c, a.h, a.ldh, a.wu, vmt, p.ldvt, p.ntr, p.nct, p.vper,
+                                          part_o, part_ms);
   k_fused_combine<<<(unsigned)a.n, 256, 0, st>>>(a.n, a.c, a.V, p.nsp, part_o, part_ms, a.labels, a.w, a.vm, a.ld_vm,
                                                  a.out, a.ld_out, a.dev_info);
   k_fused_info_finish<<<1, 64, 0, st>>>(a.dev_info);

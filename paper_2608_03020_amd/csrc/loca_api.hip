@@ -356,7 +356,8 @@ loca_status loca_fused_head(loca_stream_t stream, int64_t n, int64_t V, int64_t 
   if (ldh < d || ld_vm < c || ld_out < c) return LOCA_E_ARG;
   if (!aligned(h, 16) || !aligned(wu, 16) || ldh % 8 != 0) return LOCA_E_ARG;
   if (d % 8 != 0) return LOCA_E_UNSUPPORTED;
-  if (n > (int64_t)INT32_MAX - 1 || V > (int64_t)INT32_MAX - 128 || c > ((int64_t)1 << 24)) return LOCA_E_UNSUPPORTED;
+  if (n > (int64_t)INT32_MAX - 1 || V > ((int64_t)1 << 23) || c > ((int64_t)1 << 24)) return LOCA_E_UNSUPPORTED;
+  if (d > ((int64_t)1 << 23) || ldh > ((int64_t)1 << 23)) return LOCA_E_UNSUPPORTED;  // 32-bit buffer offsets
   if (((n + 127) / 128) * ((c + 63) / 64) * kMaxFusedSplits > (int64_t)INT32_MAX) return LOCA_E_UNSUPPORTED;
   loca_status st = check_ws(ws, ws_bytes, fused_head_ws(n, V, c));
   if (st != LOCA_OK) return st;
