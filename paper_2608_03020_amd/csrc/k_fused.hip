@@ -6,11 +6,12 @@
 // e_t = W_u^T E_t of the paper's order (then V_k^T e_t per block); Vm = [A~_1 | ... | A~_L]
 // gives every block's credit coordinates Y_b = E A~_b at once.
 //
-// The logits are never stored.  A workgroup owns 128 tokens, a tile of at most CT columns
-// of Vm and a contiguous range of the vocabulary, and walks that range in chunks of 128:
-//   1. z^T (128 x 128) = W_u[chunk] h_rows^T on the matrix cores (v_mfma_f32_32x32x16_bf16,
+// The logits are never stored.  A workgroup (8 waves) owns 128 tokens, a tile of at most 64
+// columns of Vm and a contiguous range of the vocabulary, and walks that range in chunks
+// of 256:
+//   1. z^T (256 x 128) = W_u[chunk] h_rows^T on the matrix cores (v_mfma_f32_32x32x16_bf16,
 //      fp32 accumulation), both operands copied straight into LDS (buffer loads to LDS) in
-//      64-wide slices of d through a three-slot ring that runs across chunk boundaries;
+//      32-wide slices of d through a four-slot ring that runs across chunk boundaries;
 //   2. an online softmax per token, in registers: the running maximum m and sum s (fp32)
 //      are updated with the chunk, the accumulated output is rescaled by exp(m_old - m_new),
 //      and P = exp(z - m_new) is split into bf16 hi + lo parts (about 16 significant bits);
@@ -25,20 +26,24 @@ namespace loca {
 
 namespace {
 
-constexpr int kFT = 256;        // threads: 4 waves, (vocabulary half wv) x (token half wt)
+constexpr int kFT = 512;        // threads: 8 waves, (vocabulary quarter wv) x (token half wt)
 constexpr int kFR = 128;        // tokens per tile
-constexpr int kFV = 128;        // vocabulary per chunk
-constexpr int kFK = 64;         // hidden width per stage
-constexpr int kFStages = 3;     // ring slots: two stages in flight while one is read
-constexpr int kFStage = (kFV + kFR) * kFK * 2;  // bytes per stage: W_u rows, then h rows (128 B each)
-constexpr int kFCopies = kFStage / 16 / kFT;     // 16-byte copies per thread per stage
+constexpr int kFV = 256;        // vocabulary per chunk
+constexpr int kFC = 64;         // columns of Vm per tile
+constexpr int kFK = 32;         // hidden width per stage
+constexpr int kFStages = 4;     // ring slots: three stages in flight while one is read
+constexpr int kFLA = kFStages - 1;
+constexpr int kFStage = (kFV + kFR) * kFK * 2;  // bytes per stage: W_u rows, then h rows (64 B each)
+constexpr int kFCopies = kFStage / 16 / kFT;     // 16-byte copies per thread per stage (3)
+constexpr int kFVt = kFC * kFV * 2;              // bytes of the Vm^T slice
+constexpr int kFNV = kFVt / 16 / kFT;            // its copies per thread (4)
 
-// A stage holds 256 rows of 128 bytes (64 bf16 of d): rows 0..127 the chunk's W_u rows,
-// rows 128..255 the tile's h rows.  Chunk c (16 bytes) of row r sits at position
-// c ^ ((r >> 1) & 7), so that the 16 lanes of a half wave reading one chunk of 16
+// A stage holds 384 rows of 64 bytes (32 bf16 of d): rows 0..255 the chunk's W_u rows,
+// rows 256..383 the tile's h rows.  Chunk c (16 bytes) of row r sits at position
+// c ^ ((r >> 2) & 3), so that the 16 lanes of a half wave reading one chunk of 16
 // consecutive rows hit 16 distinct bank groups.
-LOCA_DEV int fz_swz(int r) { return (r >> 1) & 7; }
-// The Vm^T slice: CT rows (columns of Vm) of 256 bytes (128 vocabulary entries), chunk c
+LOCA_DEV int fz_swz(int r) { return (r >> 2) & 3; }
+// The Vm^T slice: 64 rows (columns of Vm) of 512 bytes (256 vocabulary entries), chunk c
 // of row r at position c ^ (r & 15).
 LOCA_DEV int fv_swz(int r) { return r & 15; }
 
@@ -60,13 +65,30 @@ LOCA_DEV void fz_combine(float& m, float& s, float m2, float s2) {
   m = mm;
 }
 
+// s_waitcnt vmcnt(a) for a run-time a in 0..31
+LOCA_DEV void wait_vm(int a) {
+  switch (a) {
+#define LOCA_W(N) case N: __builtin_amdgcn_s_waitcnt(vmcnt_imm(N)); break;
+    LOCA_W(0) LOCA_W(1) LOCA_W(2) LOCA_W(3) LOCA_W(4) LOCA_W(5) LOCA_W(6) LOCA_W(7) LOCA_W(8) LOCA_W(9)
+    LOCA_W(10) LOCA_W(11) LOCA_W(12) LOCA_W(13) LOCA_W(14) LOCA_W(15) LOCA_W(16) LOCA_W(17) LOCA_W(18)
+    LOCA_W(19) LOCA_W(20) LOCA_W(21) LOCA_W(22) LOCA_W(23) LOCA_W(24) LOCA_W(25) LOCA_W(26) LOCA_W(27)
+    LOCA_W(28) LOCA_W(29) LOCA_W(30)
+#undef LOCA_W
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;
+  }
+}
+
 // The logits are formed transposed, z^T = W_u[chunk] h_tile^T (vocabulary x tokens), so
 // that lane l of a 32 x 32 result block holds token l % 32 and 16 vocabulary entries:
-// the softmax statistics of a token stay within a lane pair (l, l ^ 32) and the two
+// the softmax statistics of a token stay within a lane pair (l, l ^ 32) and the four
 // waves that split the chunk's vocabulary, and the exponentials of a block are already
 // the matrix-core operand of the product with Vm (the sum over the vocabulary taken in
 // the order the result layout gives).
-template <int CT>
+//
+// Copy accounting: stage s is issued kFLA iterations ahead of its use (the prologue issues
+// stages 0 .. kFLA - 1); the Vm^T slice of chunk j is issued at the top of iteration j nks,
+// before that iteration's stage.  Every wait counts the copies issued after the one it
+// needs, and vector-memory operations complete in order.
 __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_t d, int64_t c,
                                                     const uint16_t* __restrict__ h, int64_t ldh,
                                                     const uint16_t* __restrict__ wu,
@@ -74,16 +96,15 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
                                                     int64_t vper, float* __restrict__ part_o,
                                                     float2* __restrict__ part_ms) {
   __shared__ __attribute__((aligned(1024))) uint8_t ring[kFStages * kFStage];
-  __shared__ __attribute__((aligned(1024))) uint8_t sVt[CT * 256];
-  __shared__ float2 sEx[2][kFR];
-  constexpr int NQ = CT / 32;            // 32-column output blocks per wave
-  constexpr int NV = CT * 256 / 16 / kFT;  // 16-byte copies of the Vm^T slice per thread
+  __shared__ __attribute__((aligned(1024))) uint8_t sVt[kFVt];
+  __shared__ float2 sEx[4][kFR];
+  constexpr int NQ = kFC / 32;  // 32-column output blocks per wave
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, wv = wid >> 1, wt = wid & 1;
   const int l32 = lane & 31, lh = lane >> 5;
   // tiles that share a vocabulary range are consecutive within an XCD (W_u read once there)
   const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
   const int rt = logical % ntr, ct = (logical / ntr) % nct, sp = logical / (ntr * nct);
-  const int64_t r0 = (int64_t)rt * kFR, c0 = (int64_t)ct * CT;
+  const int64_t r0 = (int64_t)rt * kFR, c0 = (int64_t)ct * kFC;
   const int64_t vb = (int64_t)sp * vper, ve = (vb + vper < V) ? vb + vper : V;
   const int nks = (int)((d + kFK - 1) / kFK);
   const int nch = (int)((ve - vb + kFV - 1) / kFV);
@@ -91,60 +112,52 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
 
   const int64_t nrow = (n - r0 < kFR) ? n - r0 : kFR;
   const i32x4_t rsH = buffer_rsrc(h + r0 * ldh, (uint32_t)(nrow * ldh * 2));
-  const int64_t ncol = (c - c0 < CT) ? c - c0 : CT;
+  const int64_t ncol = (c - c0 < kFC) ? c - c0 : kFC;
   const i32x4_t rsV = buffer_rsrc(vmt + c0 * ldvt, (uint32_t)(ncol * ldvt * 2));
   const uint32_t ring_lds = (uint32_t)(uintptr_t)(LOCA_LDS void*)ring;
   const uint32_t vt_lds = (uint32_t)(uintptr_t)(LOCA_LDS void*)sVt;
-
-  // stage g = (chunk g / nks, slice g % nks) into ring slot g % 3: waves 0-1 copy the 128
-  // W_u rows, waves 2-3 the 128 h rows (wave-uniform); byte offsets fit 31 bits (V, d,
-  // ldh <= 2^23 are checked by the caller)
   const int wq = __builtin_amdgcn_readfirstlane(wid);
+
+  // stage g = (chunk g / nks, slice g % nks) into ring slot g % kFStages: 24 blocks of 1 KB
+  // (16 rows each), blocks 0..15 the W_u rows, 16..23 the h rows; byte offsets fit 31 bits
+  // (V, d, ldh <= 2^23 are checked by the caller)
   auto issue_stage = [&](int g) {
     const int64_t v0 = vb + (int64_t)(g / nks) * kFV;
     const int k0 = (g % nks) * kFK;
     const uint32_t slot = ring_lds + (uint32_t)((g % kFStages) * kFStage);
-    if (wq < 2) {
-      const int64_t nvr = (V - v0 < kFV) ? V - v0 : kFV;
-      const i32x4_t rsW = buffer_rsrc(wu + v0 * d, (uint32_t)(nvr * d * 2));
+    const int64_t nvr = (V - v0 < kFV) ? V - v0 : kFV;
+    const i32x4_t rsW = buffer_rsrc(wu + v0 * d, (uint32_t)(nvr * d * 2));
 #pragma unroll
-      for (int j = 0; j < kFCopies; ++j) {
-        const int blk = wq * kFCopies + j;           // 1 KB of LDS: rows 8 blk .. 8 blk + 7
-        const int row = 8 * blk + (lane >> 3);
-        const int k = k0 + 8 * ((lane & 7) ^ fz_swz(row));
+    for (int j = 0; j < kFCopies; ++j) {
+      const int blk = wq * kFCopies + j;
+      const int row = 16 * blk + (lane >> 2);
+      const int k = k0 + 8 * ((lane & 3) ^ fz_swz(row));
+      if (blk < kFV / 16) {
         const uint32_t off = k < (int)d ? 2u * (uint32_t)(row * (int)d + k) : kBufOutside;
         lds_dma16_buf(off, rsW, slot + (uint32_t)blk * 1024u);
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < kFCopies; ++j) {
-        const int blk = wq * kFCopies + j;           // rows 128 .. 255 of the stage
-        const int hrow = 8 * (blk - 2 * kFCopies) + (lane >> 3);
-        const int k = k0 + 8 * ((lane & 7) ^ fz_swz(kFV + hrow));
-        const uint32_t off = k < (int)d ? 2u * (uint32_t)(hrow * (int)ldh + k) : kBufOutside;
+      } else {
+        const uint32_t off = k < (int)d ? 2u * (uint32_t)((row - kFV) * (int)ldh + k) : kBufOutside;
         lds_dma16_buf(off, rsH, slot + (uint32_t)blk * 1024u);
       }
     }
   };
-  // the chunk's Vm^T slice (CT columns of Vm x 128 vocabulary entries; zero past V)
+  // the chunk's Vm^T slice (64 columns of Vm x 256 vocabulary entries; zero past V)
   auto issue_vt = [&](int64_t v0) {
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int blk = wq * NV + j;                   // 1 KB: rows 4 blk .. 4 blk + 3
-      const int row = 4 * blk + (lane >> 4);
-      const uint32_t off = 2u * (uint32_t)(row * (int)ldvt + (int)v0 + 8 * ((lane & 15) ^ fv_swz(row)));
+    for (int j = 0; j < kFNV; ++j) {
+      const int blk = wq * kFNV + j;  // 1 KB: rows 2 blk, 2 blk + 1
+      const int row = 2 * blk + (lane >> 5);
+      const uint32_t off = 2u * (uint32_t)(row * (int)ldvt + (int)v0 + 8 * ((lane & 31) ^ fv_swz(row)));
       lds_dma16_buf(off, rsV, vt_lds + (uint32_t)blk * 1024u);
     }
   };
-  // wait until at most `a` of this thread's copies are outstanding (a from a small set)
-  auto wait_at_most = [&](int a) {
-    switch (a) {
-      case 0: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;
-      case 4: __builtin_amdgcn_s_waitcnt(vmcnt_imm(4)); break;
-      case 8: __builtin_amdgcn_s_waitcnt(vmcnt_imm(8)); break;
-      case 12: __builtin_amdgcn_s_waitcnt(vmcnt_imm(12)); break;
-      default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(16)); break;
-    }
+  // copies issued before the top of iteration g, and up to and including stage s
+  auto issued_before = [&](int g) {
+    const int st = (g + kFLA < total) ? g + kFLA : total;
+    return kFCopies * st + kFNV * (g >= 1 ? (g - 1) / nks + 1 : 0);
+  };
+  auto through_stage = [&](int s) {
+    return kFCopies * (s + 1) + kFNV * (s >= kFLA ? (s - kFLA) / nks + 1 : 0);
   };
 
   f32x16_t o[2][NQ];
@@ -157,13 +170,11 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
   float m_run[2] = {-__builtin_inff(), -__builtin_inff()}, s_run[2] = {0.f, 0.f};  // token l32 of block mt
   f32x16_t z[2][2];
 
-  issue_stage(0);
-  if (total > 1) issue_stage(1);
+  for (int s = 0; s < kFLA && s < total; ++s) issue_stage(s);
   for (int g = 0; g < total; ++g) {
     const int ks = g % nks;
-    // copies issued after stage g's: stage g + 1 and, when g - 1 began a chunk, its Vm^T slice
-    wait_at_most((g + 1 < total ? kFCopies : 0) + (g >= 1 && (g - 1) % nks == 0 ? NV : 0));
-    __syncthreads();  // every thread's copies of stage g landed; slot (g + 2) % 3 and sVt free
+    wait_vm(issued_before(g) - through_stage(g));
+    __syncthreads();  // every thread's copies of stage g landed; the slot refilled below is free
     if (ks == 0) {
       issue_vt(vb + (int64_t)(g / nks) * kFV);
 #pragma unroll
@@ -173,7 +184,7 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
 #pragma unroll
           for (int r = 0; r < 16; ++r) z[mv][mt][r] = 0.f;
     }
-    if (g + 2 < total) issue_stage(g + 2);
+    if (g + kFLA < total) issue_stage(g + kFLA);
     // 1. z^T += W_u[chunk, slice] h[tile, slice]^T
     const uint8_t* st = ring + (g % kFStages) * kFStage;
 #pragma unroll
@@ -183,12 +194,12 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
 #pragma unroll
       for (int mv = 0; mv < 2; ++mv) {
         const int row = wv * 64 + 32 * mv + l32;
-        a[mv] = *(const bf16x8_t*)(st + row * 128 + 16 * (ch ^ fz_swz(row)));
+        a[mv] = *(const bf16x8_t*)(st + row * 64 + 16 * (ch ^ fz_swz(row)));
       }
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) {
         const int row = kFV + wt * 64 + 32 * mt + l32;
-        b[mt] = *(const bf16x8_t*)(st + row * 128 + 16 * (ch ^ fz_swz(row)));
+        b[mt] = *(const bf16x8_t*)(st + row * 64 + 16 * (ch ^ fz_swz(row)));
       }
 #pragma unroll
       for (int mv = 0; mv < 2; ++mv)
@@ -199,7 +210,8 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
 
     // 2. online softmax over the chunk.  Entry r of lane l in block (mv, mt): vocabulary
     // v0 + 64 wv + 32 mv + 8 (r >> 2) + 4 lh + (r & 3), token 64 wt + 32 mt + l32.
-    const int64_t v0 = vb + (int64_t)(g / nks) * kFV;
+    const int j = g / nks;
+    const int64_t v0 = vb + (int64_t)j * kFV;
     const int nv = (V - v0 < kFV) ? (int)(V - v0) : kFV;
     const bool full = nv == kFV;
     auto valid = [&](int mv, int r) { return full || 64 * wv + 32 * mv + 8 * (r >> 2) + 4 * lh + (r & 3) < nv; };
@@ -228,17 +240,22 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
     if (lh == 0)
 #pragma unroll
       for (int mt = 0; mt < 2; ++mt) sEx[wv][wt * 64 + 32 * mt + l32] = make_float2(lm[mt], ls[mt]);
-    // the Vm^T slice of this chunk: issued at its first stage, followed by at most the
-    // stage copies of the chunk's other slices
-    if (nks == 1) wait_at_most(g + 2 < total ? kFCopies : 0);
-    else if (nks == 2) wait_at_most((g + 1 < total ? kFCopies : 0) + (g + 2 < total ? kFCopies : 0));
+    // the Vm^T slice of this chunk: covered by the stage waits when a later stage was issued
+    // after it and has been waited for (nks > kFLA), else waited for here
+    if (nks <= kFLA) {
+      const int g0 = j * nks;
+      const int after_vt = kFCopies * ((g + kFLA + 1 < total ? g + kFLA + 1 : total) -
+                                       (g0 + kFLA < total ? g0 + kFLA : total));
+      wait_vm(after_vt);
+    }
     __syncthreads();
     float al[2];
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt) {
-      const float2 e0 = sEx[0][wt * 64 + 32 * mt + l32], e1 = sEx[1][wt * 64 + 32 * mt + l32];
-      float cm = e0.x, cs = e0.y;
-      fz_combine(cm, cs, e1.x, e1.y);  // the same order in both waves
+      const int tk = wt * 64 + 32 * mt + l32;
+      float cm = sEx[0][tk].x, cs = sEx[0][tk].y;
+#pragma unroll
+      for (int u = 1; u < 4; ++u) fz_combine(cm, cs, sEx[u][tk].x, sEx[u][tk].y);  // the same order in all waves
       const float mn = fmaxf(m_run[mt], cm);
       al[mt] = __expf(m_run[mt] - mn);
       s_run[mt] = s_run[mt] * al[mt] + cs * __expf(cm - mn);
@@ -279,12 +296,11 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
           plo[mt] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
         }
         // B entry e of lane (col, lh): vocabulary 64 wv + 32 mv + 16 ks2 + 8 (e >> 2) + 4 lh + (e & 3)
-        const int vb0 = 64 * wv + 32 * mv + 16 * ks2 + 4 * lh;
+        const int va = 64 * wv + 32 * mv + 16 * ks2 + 4 * lh, vc = va + 8;
 #pragma unroll
         for (int q = 0; q < NQ; ++q) {
           const int row = 32 * q + l32;
-          const uint8_t* rp = sVt + row * 256;
-          const int va = vb0, vc = vb0 + 8;
+          const uint8_t* rp = sVt + row * (2 * kFV);
           const uint2 lo4 = *(const uint2*)(rp + 16 * ((va >> 3) ^ fv_swz(row)) + 2 * (va & 7));
           const uint2 hi4 = *(const uint2*)(rp + 16 * ((vc >> 3) ^ fv_swz(row)) + 2 * (vc & 7));
           bv[q] = __builtin_bit_cast(bf16x8_t, make_uint4(lo4.x, lo4.y, hi4.x, hi4.y));
@@ -299,19 +315,36 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
       }
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
-  __syncthreads();  // the ring is free: the two vocabulary halves' outputs meet there
-  float* red = (float*)ring;  // kFR x (CT + 4) floats
-  constexpr int RLD = CT + 4;
-  if (wv == 1)
+  __syncthreads();  // the ring is free: the four vocabulary quarters' outputs meet there
+  // partial outputs summed as (O_0 + O_2) + (O_1 + O_3), in a fixed order
+  float* red = (float*)ring;  // 2 x 128 tokens x (64 + 4) floats
+  constexpr int RLD = kFC + 4;
+  auto put = [&](int slot) {
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
 #pragma unroll
       for (int q = 0; q < NQ; ++q)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
-          red[(wt * 64 + 32 * mt + 8 * (r >> 2) + 4 * lh + (r & 3)) * RLD + 32 * q + l32] = o[mt][q][r];
+          red[(slot * kFR + wt * 64 + 32 * mt + 8 * (r >> 2) + 4 * lh + (r & 3)) * RLD + 32 * q + l32] = o[mt][q][r];
+  };
+  auto add = [&](int slot) {
+#pragma unroll
+    for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          o[mt][q][r] += red[(slot * kFR + wt * 64 + 32 * mt + 8 * (r >> 2) + 4 * lh + (r & 3)) * RLD + 32 * q + l32];
+  };
+  if (wv >= 2) put(wv - 2);
+  __syncthreads();
+  if (wv < 2) add(wv);
+  __syncthreads();
+  if (wv == 1) put(0);
   __syncthreads();
   if (wv == 0) {
+    add(0);
     float* po = part_o + (int64_t)sp * n * c;
 #pragma unroll
     for (int mt = 0; mt < 2; ++mt)
@@ -321,7 +354,7 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
         for (int r = 0; r < 16; ++r) {
           const int tr = wt * 64 + 32 * mt + 8 * (r >> 2) + 4 * lh + (r & 3);
           const int64_t row = r0 + tr, col = c0 + 32 * q + l32;
-          if (row < n && col < c) po[row * c + col] = o[mt][q][r] + red[tr * RLD + 32 * q + l32];
+          if (row < n && col < c) po[row * c + col] = o[mt][q][r];
         }
     if (ct == 0 && lh == 0)
 #pragma unroll
@@ -404,7 +437,7 @@ struct FusedPlan {
 
 FusedPlan fused_plan(int64_t n, int64_t V, int64_t c) {
   FusedPlan p;
-  p.ct = 64;  // a wider column tile holds more accumulators than the register file keeps
+  p.ct = kFC;  // a wider column tile holds more accumulators than the register file keeps
   p.ntr = (int)((n + kFR - 1) / kFR);
   p.nct = (int)((c + p.ct - 1) / p.ct);
   const int64_t tiles = (int64_t)p.ntr * p.nct, nchunk = (V + kFV - 1) / kFV;
@@ -439,7 +472,7 @@ hipError_t launch_fused_head(const FusedArgs& a) {
   k_vm_transpose<<<dim3((unsigned)((p.ldvt + 31) / 32), (unsigned)((a.c + 31) / 32)), 256, 0, st>>>(
       a.V, a.c, a.vm, a.ld_vm, vmt, p.ldvt);
   const unsigned grid = (unsigned)((int64_t)p.ntr * p.nct * p.nsp);
-  k_fused_head<64><<<grid, kFT, 0, st>>>(a.n, a.V, a.d, a.c, a.h, a.ldh, a.wu, vmt, p.ldvt, p.ntr, p.nct, p.vper,
+  k_fused_head<<<grid, kFT, 0, st>>>(a.n, a.V, a.d, a.c, a.h, a.ldh, a.wu, vmt, p.ldvt, p.ntr, p.nct, p.vper,
                                           part_o, part_ms);
   k_fused_combine<<<(unsigned)a.n, 256, 0, st>>>(a.n, a.c, a.V, p.nsp, part_o, part_ms, a.labels, a.w, a.vm, a.ld_vm,
                                                  a.out, a.ld_out, a.dev_info);
