@@ -229,10 +229,41 @@ def test_ridge_solve_fp64_and_nonpd_pivot():
     assert info.item() == 71
 
 
-@pytest.mark.parametrize("d,kp,r", [(200, 24, 10), (200, 96, 40), (230, 127, 64), (150, 128, 16)])
+@pytest.mark.parametrize("kp,r", [(40, 12), (64, 30)])
+def test_truncation_rank_deficient_right_factor(kp, r):
+    """R with repeated rows (R R^T singular): the core takes the eigendecomposition of R R^T
+    instead of its Cholesky factor; W_r against the oracle's dense SVD."""
+    import torch
+    import oracle
+    from paper_2608_03020_amd import loca
+    d = 180
+    rng = np.random.default_rng(2)
+    log(f"case truncation_rank_deficient: d={d} kp={kp} r_a={r}")
+    Mh = rng.normal(size=(d, kp)).astype(np.float32)
+    half = rng.normal(size=(kp // 2, d)).astype(np.float32)
+    Rh = np.concatenate([half, half])
+    Wr_o, s_o = oracle.truncate_dense(Mh.astype(np.float64) @ Rh.astype(np.float64), r)
+    a = torch.empty((1, r, d), device="cuda")
+    b = torch.empty((1, d, r), device="cuda")
+    s = torch.empty((1, kp), device="cuda")
+    W = torch.empty((1, d, d), device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, 1, 0, d, kp, r_a=r))
+    loca.loca_lowrank_truncate(torch.from_numpy(Mh)[None].cuda(), torch.from_numpy(Rh)[None].cuda(), r, a, b, s,
+                               info, ws, w_dense_out=W)
+    torch.cuda.synchronize()
+    e_w = rel(W[0].cpu().numpy(), Wr_o)
+    e_s = rel(s[0].cpu().numpy()[:kp // 2], s_o[:kp // 2])
+    log(f"truncation (rank-deficient R): W_r {e_w:.2e} sigma {e_s:.2e}")
+    assert e_w < 1e-5 and e_s < 1e-5
+
+
+@pytest.mark.parametrize("d,kp,r", [(200, 24, 10), (200, 64, 32), (130, 63, 20), (96, 2, 1), (200, 96, 40),
+                                    (230, 127, 64), (150, 128, 16)])
 def test_truncation_matches_explicit_svd(d, kp, r):
-    """Eckart-Young truncation of W = M B~ against the oracle's dense SVD (d <= 256);
-    kp > 64 takes the packed-LDS eigensolver (odd kp padded, the largest kp and rank)."""
+    """Eckart-Young truncation of W = M B~ against the oracle's dense SVD (d <= 256): the
+    fp64-LDS core for kp <= 64 (its largest kp, an odd kp padded, kp = 2) and the core with
+    float eigenvectors for kp > 64 (odd kp padded, the largest kp and rank)."""
     import torch
     import oracle
     from paper_2608_03020_amd import loca
