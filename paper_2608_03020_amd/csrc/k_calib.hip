@@ -235,33 +235,73 @@ __global__ void k_transpose_f32(int64_t d, int np_, const float* __restrict__ Rt
   }
 }
 
-// A~_b = W_u V_k,b (vocab x k): one wave per row of W_u, lanes over d, k sums reduced in
-// a fixed order.  Grid: x over rows (4 waves per workgroup), y = block.
+// A~_b = W_u V_k,b (vocab x k, k <= 64) on the fp32 matrix cores (v_mfma_f32_32x32x2f32):
+// a workgroup of four waves takes 128 rows of W_u, wave w rows 32 w .. 32 w + 31 and all k
+// columns in two 32-wide blocks; d is walked in slices of 64 staged through LDS (W_u as
+// floats, exact for bf16 input), the next slice loaded into registers while the current one
+// is multiplied.  Grid: x over 128-row tiles, y = block.
+constexpr int kFoldR = 128, kFoldK = 64;
 template <typename WT>
 __global__ __launch_bounds__(kT) void k_head_fold(int64_t vocab, int64_t d, int k, const WT* __restrict__ wu,
                                                   const float* __restrict__ vk, float* __restrict__ at_out,
                                                   int64_t at_bstride) {
+  __shared__ float sW[kFoldR][kFoldK + 1];
+  __shared__ float sB[kFoldK][kFoldK + 1];
   const int64_t b = blockIdx.y;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int64_t v = (int64_t)blockIdx.x * 4 + wid;
-  if (v >= vocab) return;
-  const float* V = vk + b * d * k;
-  float acc[kMaxNp];
+  const int64_t v0 = (int64_t)blockIdx.x * kFoldR;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const float* Vb = vk + b * d * k;
+  constexpr int NW = kFoldR * kFoldK / kT, NB = kFoldK * kFoldK / kT;  // elements per thread
+  float rw[NW], rb[NB];
+  auto gload = [&](int64_t k0) {
 #pragma unroll
-  for (int j = 0; j < kMaxNp; ++j) acc[j] = 0.f;
-  for (int64_t c = lane; c < d; c += 64) {
-    const float w = load_as_f32(wu + v * d + c);
+    for (int t = 0; t < NW; ++t) {
+      const int e = tid + kT * t, r = e / kFoldK, c = e % kFoldK;
+      rw[t] = (v0 + r < vocab && k0 + c < d) ? load_as_f32(wu + (v0 + r) * d + k0 + c) : 0.f;
+    }
 #pragma unroll
-    for (int j = 0; j < kMaxNp; ++j)
-      if (j < k) acc[j] += w * V[c * k + j];
-  }
+    for (int t = 0; t < NB; ++t) {
+      const int e = tid + kT * t, r = e / kFoldK, c = e % kFoldK;
+      rb[t] = (k0 + r < d && c < k) ? Vb[(k0 + r) * k + c] : 0.f;
+    }
+  };
+  f32x16_t acc[2];
 #pragma unroll
-  for (int j = 0; j < kMaxNp; ++j) {
-    if (j < k) {
-      const float s = wave_sum(acc[j]);
-      if (lane == 0) at_out[b * at_bstride + v * k + j] = s;
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[q][r] = 0.f;
+  const int nq = k > 32 ? 2 : 1;
+  gload(0);
+  for (int64_t k0 = 0; k0 < d; k0 += kFoldK) {
+    __syncthreads();  // the previous slice's readers are done
+#pragma unroll
+    for (int t = 0; t < NW; ++t) {
+      const int e = tid + kT * t;
+      sW[e / kFoldK][e % kFoldK] = rw[t];
+    }
+#pragma unroll
+    for (int t = 0; t < NB; ++t) {
+      const int e = tid + kT * t;
+      sB[e / kFoldK][e % kFoldK] = rb[t];
+    }
+    __syncthreads();
+    if (k0 + kFoldK < d) gload(k0 + kFoldK);
+    // A lane l = W[row l % 32][kk + l / 32], B lane l = V_k[kk + l / 32][col l % 32]
+#pragma unroll 8
+    for (int kk = 0; kk < kFoldK; kk += 2) {
+      const float a = sW[32 * wid + (lane & 31)][kk + (lane >> 5)];
+      acc[0] = mfma_f32x2(a, sB[kk + (lane >> 5)][lane & 31], acc[0]);
+      if (nq > 1) acc[1] = mfma_f32x2(a, sB[kk + (lane >> 5)][32 + (lane & 31)], acc[1]);
     }
   }
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t row = v0 + 32 * wid + mfma32_row(lane, r);
+      const int col = 32 * q + (lane & 31);
+      if (row < vocab && col < k) at_out[b * at_bstride + row * k + col] = acc[q][r];
+    }
 }
 
 // vk_out[b][c][j] = V_k (the internal copy, d x k per block, packed)
@@ -448,7 +488,7 @@ hipError_t launch_calib_factors(const CalibArgs& a, const float* M, int64_t m_bs
     k_copy_vk<<<g, 256, 0, st>>>(d, (int)k, vk, a.vk_out, a.vk_bstride);
   }
   if (a.wu && a.at_out) {
-    dim3 g((unsigned)((a.vocab + 3) / 4), (unsigned)nb);
+    dim3 g((unsigned)((a.vocab + kFoldR - 1) / kFoldR), (unsigned)nb);
     if (a.wu_dtype == LOCA_BF16)
       k_head_fold<uint16_t><<<g, kT, 0, st>>>(a.vocab, d, (int)k, (const uint16_t*)a.wu, vk, a.at_out, a.at_bstride);
     else
