@@ -374,15 +374,16 @@ __global__ void k_fused_info_finish(int32_t* p) {
   if (threadIdx.x == 0 && *p == INT32_MAX) *p = 0;
 }
 
-// Vm^T (c x ldvt, bf16) from Vm (V x c, row stride ld_vm), zero past V; 32 x 32 tiles via LDS
-__global__ void k_vm_transpose(int64_t V, int64_t c, const uint16_t* __restrict__ vm, int64_t ld_vm,
-                               uint16_t* __restrict__ vmt, int64_t ldvt) {
+// Vm^T (c x ldvt, bf16, zero past V) from Vm given as column groups of kc: entry (v, j) at
+// vm[(j / kc) gstride + v ld_vm + j % kc] (one group: kc = c); 32 x 32 tiles via LDS
+__global__ void k_vm_transpose(int64_t V, int64_t c, const uint16_t* __restrict__ vm, int64_t ld_vm, int64_t kc,
+                               int64_t gstride, uint16_t* __restrict__ vmt, int64_t ldvt) {
   __shared__ uint16_t t[32][33];
   const int64_t v0 = (int64_t)blockIdx.x * 32, j0 = (int64_t)blockIdx.y * 32;
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
   for (int r = ty; r < 32; r += 8) {
     const int64_t v = v0 + r, j = j0 + tx;
-    t[r][tx] = (v < V && j < c) ? vm[v * ld_vm + j] : (uint16_t)0;
+    t[r][tx] = (v < V && j < c) ? vm[(j / kc) * gstride + v * ld_vm + j % kc] : (uint16_t)0;
   }
   __syncthreads();
   for (int r = ty; r < 32; r += 8) {
@@ -392,14 +393,19 @@ __global__ void k_vm_transpose(int64_t V, int64_t c, const uint16_t* __restrict_
 }
 
 // out_t = w_t (sum_i O_i[t] e^{m_i - M} / S - Vm[y_t]), S = sum_i s_i e^{m_i - M}: the ranges
-// in order, float64.  One workgroup per token.  A bad label drops the label term and is
-// reported; a sum that is not finite or not positive is reported as non-finite data.
+// in order, float64.  One workgroup per token.  Column j of Vm and of the output is column
+// j % kc of group j / kc (Vm entries as for k_vm_transpose; output at
+// out[(j / kc) o_gstride + t ld_out + j % kc]).  A bad label drops the label term and is
+// reported; a sum that is not finite or not positive is reported as non-finite data.  With
+// ms_out the token's (M, S) are also written as floats (ms_out[2 t], ms_out[2 t + 1]).
 __global__ __launch_bounds__(256) void k_fused_combine(int64_t n, int64_t c, int64_t V, int nsp,
                                                        const float* __restrict__ part_o,
                                                        const float2* __restrict__ part_ms,
                                                        const int32_t* __restrict__ labels, const float* __restrict__ w,
-                                                       const uint16_t* __restrict__ vm, int64_t ld_vm,
-                                                       float* __restrict__ out, int64_t ld_out, int32_t* __restrict__ info) {
+                                                       const uint16_t* __restrict__ vm, int64_t ld_vm, int64_t kc,
+                                                       int64_t gstride, float* __restrict__ out, int64_t ld_out,
+                                                       int64_t o_gstride, float* __restrict__ ms_out,
+                                                       int32_t* __restrict__ info) {
   __shared__ double sc[kMaxFusedSplits];
   const int64_t t = blockIdx.x;
   // every range holds a valid chunk, so each finite s_i is at least 1
@@ -419,15 +425,206 @@ __global__ __launch_bounds__(256) void k_fused_combine(int64_t n, int64_t c, int
   if (threadIdx.x == 0) {
     if (bad) atomicMin(info, (int32_t)(t + 1));
     if (nonfin) atomicMin(info, (int32_t)LOCA_INFO_NONFINITE);
+    if (ms_out) {
+      ms_out[2 * t] = (float)M;
+      ms_out[2 * t + 1] = (float)S;
+    }
   }
   const double wt = w ? (double)w[t] : 1.0;
   const double inv = nonfin ? 0.0 : 1.0 / S;
   for (int64_t j = threadIdx.x; j < c; j += blockDim.x) {
     double acc = 0.0;
     for (int i = 0; i < nsp; ++i) acc += (double)part_o[((int64_t)i * n + t) * c + j] * sc[i];
-    const double lab = bad ? 0.0 : (double)__uint_as_float((uint32_t)vm[(int64_t)y * ld_vm + j] << 16);
-    out[t * ld_out + j] = (float)(wt * (acc * inv - lab));
+    const int64_t g = j / kc, jc = j - g * kc;
+    const double lab = bad ? 0.0 : (double)__uint_as_float((uint32_t)vm[g * gstride + (int64_t)y * ld_vm + jc] << 16);
+    out[g * o_gstride + t * ld_out + jc] = (float)(wt * (acc * inv - lab));
   }
+}
+
+// ------------------------------------------------------------------ single pass over stored logits
+// The head error of Lemma S3.1 applied to a right operand from stored logits in one pass
+// (what k_softmax_stats and k_top_error_gemm compute in two): a wave owns 32 tokens and the
+// 64 columns of a tile of Vm, a workgroup 128 tokens, and walks a range of the vocabulary
+// in steps of 16 entries, one k step of v_mfma_f32_32x32x16_bf16.  The logits enter as the
+// A operand (lane l: token l % 32, the 8 entries 8 (l / 32) .. 8 (l / 32) + 7 of the step),
+// under an online softmax whose running maximum is raised only when a chunk of 64 entries
+// exceeds it (the accumulated rows are then rescaled); P = exp(z - m) is split into bf16
+// hi + lo against the bf16 Vm^T slice.  Both are copied straight into LDS by buffer loads:
+// the logits through a three-slot ring, two chunks ahead, and the Vm^T slice (read from L2,
+// where the tiles of one vocabulary range on an XCD share it) double-buffered one chunk
+// ahead; one barrier per chunk.  ZT: bf16 (uint16_t, ld % 8 == 0) or float (ld % 4 == 0) logits with
+// 16-byte aligned rows; entries past V are masked, reads stay inside the row's stride.
+constexpr int kOnlineChunk = 64;
+constexpr int kOnlineStages = 3;  // logits ring slots: two chunks in flight while one is read
+// LDS staging of a chunk's logits: 128 token rows of 64 entries (bf16: 128 bytes, 8 chunks of
+// 16 bytes; float: 256 bytes, 16 chunks), chunk c of row r at position c ^ swz(r), so that the
+// 16 lanes of a half wave reading one chunk of 16 consecutive rows hit distinct bank groups.
+template <typename ZT> LOCA_DEV int zo_swz(int r) { return sizeof(ZT) == 2 ? ((r >> 1) & 7) : (r & 15); }
+// the Vm^T slice of a chunk: 64 rows (columns of Vm) of 64 entries (128 bytes), swizzled alike
+LOCA_DEV int bo_swz(int r) { return (r >> 1) & 7; }
+template <typename ZT>
+__global__ __launch_bounds__(256) void k_head_online(int64_t n, int64_t V, const ZT* __restrict__ z, int64_t ldz,
+                                                     const uint16_t* __restrict__ vmt, int64_t ldvt, int64_t c,
+                                                     int ntr, int nct, int64_t vper, float* __restrict__ part_o,
+                                                     float2* __restrict__ part_ms) {
+  constexpr int RB = kOnlineChunk * (int)sizeof(ZT);   // bytes per staged logits row
+  constexpr int CPR = RB / 16;                         // 16-byte chunks per row
+  constexpr int STAGE = 128 * RB;                      // bytes per stage
+  constexpr int NA = STAGE / 16 / 256;                 // copies per thread per stage (4 or 8)
+  constexpr int RPB = 1024 / RB;                       // rows per 1 KB copy block
+  constexpr int KS = kOnlineChunk / 16;
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[kOnlineStages * STAGE];
+  __shared__ __attribute__((aligned(1024))) uint8_t sB[2][64 * 128];
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6, l32 = lane & 31, lh = lane >> 5;
+  const int wq = __builtin_amdgcn_readfirstlane(wid);
+  const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  const int rt = logical % ntr, ct = (logical / ntr) % nct, sp = logical / (ntr * nct);
+  const int64_t r0 = (int64_t)rt * 128;
+  const int64_t tok0 = r0 + 32 * wid;
+  const int64_t t = tok0 + l32;
+  const int64_t c0 = (int64_t)ct * 64;
+  const int64_t vb = (int64_t)sp * vper, ve = (vb + vper < V) ? vb + vper : V;
+  const int nchunk = (int)((ve - vb + kOnlineChunk - 1) / kOnlineChunk);
+  // byte offsets fit 31 bits: 128 rows x ldz and 64 rows x ldvt (V <= 2^23 is checked)
+  const int64_t nrow = (n - r0 < 128) ? n - r0 : 128;
+  const i32x4_t rsZ = buffer_rsrc(z + r0 * ldz, (uint32_t)(nrow * ldz * sizeof(ZT)));
+  const int64_t ncol = (c - c0 < 64) ? c - c0 : 64;
+  const i32x4_t rsB = buffer_rsrc(vmt + c0 * ldvt, (uint32_t)(ncol * ldvt * 2));
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)(LOCA_LDS void*)ring;
+  const uint32_t sb_lds = (uint32_t)(uintptr_t)(LOCA_LDS void*)sB;
+  auto issue_a = [&](int g) {  // chunk g's logits into ring slot g % 3 (entries past the row's data masked later)
+    const int64_t v0 = vb + (int64_t)g * kOnlineChunk;
+    const uint32_t slot = ring_lds + (uint32_t)((g % kOnlineStages) * STAGE);
+#pragma unroll
+    for (int j = 0; j < NA; ++j) {
+      const int blk = wq * NA + j;
+      const int row = RPB * blk + lane / CPR, pos = lane % CPR;
+      const int ch = pos ^ zo_swz<ZT>(row);
+      const uint32_t off = (uint32_t)((row * ldz + v0) * (int64_t)sizeof(ZT)) + 16u * (uint32_t)ch;
+      lds_dma16_buf(off, rsZ, slot + (uint32_t)blk * 1024u);
+    }
+  };
+  auto issue_b = [&](int g) {  // chunk g's Vm^T slice into sB[g & 1] (rows of 64 entries, zero past V and c)
+    const int64_t v0 = vb + (int64_t)g * kOnlineChunk;
+    const uint32_t base = sb_lds + (uint32_t)((g & 1) * 64 * 128);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int blk = wq * 2 + j;  // 1 KB = 8 rows of 128 bytes
+      const int row = 8 * blk + (lane >> 3), pos = lane & 7;
+      const uint32_t off = 2u * (uint32_t)(row * ldvt + v0 + 8 * (pos ^ bo_swz(row)));
+      lds_dma16_buf(off, rsB, base + (uint32_t)blk * 1024u);
+    }
+  };
+  auto wait_vm = [&](int a) {
+    if (a == NA) __builtin_amdgcn_s_waitcnt(vmcnt_imm(NA));
+    else __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  };
+  f32x16_t o[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[q][r] = 0.f;
+  float m_run = -__builtin_inff(), s_lane = 0.f;
+  // prologue: chunks 0 .. kOnlineStages - 2 and the first Vm^T slice
+  for (int g = 0; g < kOnlineStages - 1 && g < nchunk; ++g) issue_a(g);
+  issue_b(0);
+  const int arow = 32 * wid + l32;
+  for (int g = 0; g < nchunk; ++g) {
+    // chunk g's logits (issued kOnlineStages - 1 iterations ago) and its Vm^T slice (issued at
+    // the top of iteration g - 1, before chunk g + 1's logits): only that copy may be pending
+    wait_vm(g >= 1 && g + kOnlineStages - 2 < nchunk ? NA : 0);
+    __syncthreads();  // every thread's copies landed; the slots refilled below are free
+    if (g + 1 < nchunk) issue_b(g + 1);
+    if (g + kOnlineStages - 1 < nchunk) issue_a(g + kOnlineStages - 1);
+    const int64_t v0 = vb + (int64_t)g * kOnlineChunk;
+    const uint8_t* st = ring + (g % kOnlineStages) * STAGE;
+    const uint8_t* sb = sB[g & 1];
+    // the chunk's logits of this lane's token: entry e of step ks is vocabulary v0 + 16 ks + 8 lh + e
+    float zv[KS][8];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if constexpr (sizeof(ZT) == 2) {
+        const int ch = 2 * ks + lh;
+        const uint4 u = *(const uint4*)(st + arow * RB + 16 * (ch ^ zo_swz<ZT>(arow)));
+        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          zv[ks][2 * e] = __uint_as_float(w4[e] << 16);
+          zv[ks][2 * e + 1] = __uint_as_float(w4[e] & 0xffff0000u);
+        }
+      } else {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int ch = 4 * ks + 2 * lh + h;
+          const uint4 u = *(const uint4*)(st + arow * RB + 16 * (ch ^ zo_swz<ZT>(arow)));
+          zv[ks][4 * h] = __uint_as_float(u.x);
+          zv[ks][4 * h + 1] = __uint_as_float(u.y);
+          zv[ks][4 * h + 2] = __uint_as_float(u.z);
+          zv[ks][4 * h + 3] = __uint_as_float(u.w);
+        }
+      }
+    }
+    const bool full = v0 + kOnlineChunk <= ve;
+    auto valid = [&](int ks, int e) { return full || v0 + 16 * ks + 8 * lh + e < ve; };
+    float cm = -__builtin_inff();
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (valid(ks, e)) cm = fmaxf(cm, zv[ks][e]);
+    cm = fmaxf(cm, __shfl_xor(cm, 32));
+    if (__any(cm > m_run)) {  // raise the running maximum of the tokens that need it
+      const float mn = fmaxf(m_run, cm);
+      const float al = __expf(m_run - mn);
+      s_lane *= al;
+      m_run = mn;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float a_r = __shfl(al, 8 * (r >> 2) + 4 * lh + (r & 3));
+#pragma unroll
+        for (int q = 0; q < 2; ++q) o[q][r] *= a_r;
+      }
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      uint32_t hv[4], lv[4];
+#pragma unroll
+      for (int e2 = 0; e2 < 4; ++e2) {
+        uint16_t hh[2], ll[2];
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+          const int e = 2 * e2 + u;
+          const float p = valid(ks, e) ? __expf(zv[ks][e] - m_run) : 0.f;
+          s_lane += p;
+          hh[u] = rne_bf16(p);
+          ll[u] = rne_bf16(p - __uint_as_float((uint32_t)hh[u] << 16));
+        }
+        hv[e2] = (uint32_t)hh[0] | ((uint32_t)hh[1] << 16);
+        lv[e2] = (uint32_t)ll[0] | ((uint32_t)ll[1] << 16);
+      }
+      const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
+      const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        // B lane l: Vm[v0 + 16 ks + 8 lh + e][c0 + 32 q + l % 32] = Vm^T row 32 q + l % 32
+        const int row = 32 * q + l32, ch = 2 * ks + lh;
+        const bf16x8_t bq = *(const bf16x8_t*)(sb + row * 128 + 16 * (ch ^ bo_swz(row)));
+        o[q] = mfma32(phi, bq, o[q]);
+        o[q] = mfma32(plo, bq, o[q]);
+      }
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+  const float s_tok = s_lane + __shfl_xor(s_lane, 32);
+  float* po = part_o + (int64_t)sp * n * c;
+#pragma unroll
+  for (int q = 0; q < 2; ++q)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int64_t row = tok0 + 8 * (r >> 2) + 4 * lh + (r & 3), col = c0 + 32 * q + l32;
+      if (row < n && col < c) po[row * c + col] = o[q][r];
+    }
+  if (ct == 0 && lh == 0 && t < n) part_ms[(int64_t)sp * n + t] = make_float2(m_run, s_tok);
 }
 
 struct FusedPlan {
@@ -453,6 +650,59 @@ FusedPlan fused_plan(int64_t n, int64_t V, int64_t c) {
 
 }  // namespace
 
+namespace {
+struct OnlinePlan {
+  int ntr, nct, nsp;
+  int64_t vper, ldvt;
+};
+OnlinePlan online_plan(int64_t n, int64_t V, int64_t cols) {
+  OnlinePlan p;
+  p.ntr = (int)((n + 127) / 128);
+  p.nct = (int)((cols + 63) / 64);
+  const int64_t tiles = (int64_t)p.ntr * p.nct, nchunk = (V + kOnlineChunk - 1) / kOnlineChunk;
+  int64_t want = (512 + tiles - 1) / tiles;  // about two workgroups per compute unit
+  if (want > kMaxFusedSplits) want = kMaxFusedSplits;
+  if (want > nchunk) want = nchunk;
+  if (want < 1) want = 1;
+  p.vper = ((nchunk + want - 1) / want) * kOnlineChunk;
+  p.nsp = (int)((V + p.vper - 1) / p.vper);
+  p.ldvt = nchunk * kOnlineChunk;
+  return p;
+}
+}  // namespace
+
+size_t softmax_product_online_ws(int64_t n, int64_t V, int64_t cols) {
+  const OnlinePlan p = online_plan(n, V, cols);
+  size_t s = align256(sizeof(float) * 2 * n);  // (m, s) per token, first (the e_out writer reads it there)
+  s += align256(sizeof(float) * p.nsp * n * cols);
+  s += align256(sizeof(float2) * p.nsp * n);
+  s += align256(sizeof(uint16_t) * cols * p.ldvt);
+  return s;
+}
+
+hipError_t launch_softmax_product_online(const SoftmaxProductArgs& a) {
+  const int64_t cols = a.groups * a.kc;
+  const OnlinePlan p = online_plan(a.n, a.V, cols);
+  char* w = a.ws;
+  float* ms = (float*)w; w += align256(sizeof(float) * 2 * a.n);
+  float* part_o = (float*)w; w += align256(sizeof(float) * p.nsp * a.n * cols);
+  float2* part_ms = (float2*)w; w += align256(sizeof(float2) * p.nsp * a.n);
+  uint16_t* vmt = (uint16_t*)w;
+  hipStream_t st = a.stream;
+  k_vm_transpose<<<dim3((unsigned)((p.ldvt + 31) / 32), (unsigned)((cols + 31) / 32)), 256, 0, st>>>(
+      a.V, cols, a.W, a.kc, a.kc, a.w_bstride, vmt, p.ldvt);
+  const unsigned grid = (unsigned)((int64_t)p.ntr * p.nct * p.nsp);
+  if (a.logits_dtype == LOCA_BF16)
+    k_head_online<uint16_t><<<grid, 256, 0, st>>>(a.n, a.V, (const uint16_t*)a.logits, a.ld_logits, vmt, p.ldvt,
+                                                   cols, p.ntr, p.nct, p.vper, part_o, part_ms);
+  else
+    k_head_online<float><<<grid, 256, 0, st>>>(a.n, a.V, (const float*)a.logits, a.ld_logits, vmt, p.ldvt, cols,
+                                                p.ntr, p.nct, p.vper, part_o, part_ms);
+  k_fused_combine<<<(unsigned)a.n, 256, 0, st>>>(a.n, cols, a.V, p.nsp, part_o, part_ms, a.labels, a.w, a.W, a.kc,
+                                                 a.kc, a.w_bstride, a.out, a.ld_o, a.o_bstride, ms, a.dev_info);
+  return hipGetLastError();
+}
+
 size_t fused_head_ws(int64_t n, int64_t V, int64_t c) {
   const FusedPlan p = fused_plan(n, V, c);
   size_t s = align256(sizeof(float) * p.nsp * n * c);
@@ -470,12 +720,12 @@ hipError_t launch_fused_head(const FusedArgs& a) {
   hipStream_t st = a.stream;
   k_fused_info_init<<<1, 64, 0, st>>>(a.dev_info);
   k_vm_transpose<<<dim3((unsigned)((p.ldvt + 31) / 32), (unsigned)((a.c + 31) / 32)), 256, 0, st>>>(
-      a.V, a.c, a.vm, a.ld_vm, vmt, p.ldvt);
+      a.V, a.c, a.vm, a.ld_vm, a.c, 0, vmt, p.ldvt);
   const unsigned grid = (unsigned)((int64_t)p.ntr * p.nct * p.nsp);
   k_fused_head<<<grid, kFT, 0, st>>>(a.n, a.V, a.d, a.c, a.h, a.ldh, a.wu, vmt, p.ldvt, p.ntr, p.nct, p.vper,
                                           part_o, part_ms);
   k_fused_combine<<<(unsigned)a.n, 256, 0, st>>>(a.n, a.c, a.V, p.nsp, part_o, part_ms, a.labels, a.w, a.vm, a.ld_vm,
-                                                 a.out, a.ld_out, a.dev_info);
+                                                 a.c, 0, a.out, a.ld_out, 0, nullptr, a.dev_info);
   k_fused_info_finish<<<1, 64, 0, st>>>(a.dev_info);
   return hipGetLastError();
 }

@@ -13,6 +13,8 @@
 //      (about 16 significant bits), each multiplied by the exact bf16 W_u on the matrix
 //      cores (v_mfma_f32_32x32x16_bf16; W_u read transposed from LDS);
 //   3. k_top_error_reduce: e = sum_z part_z in a fixed order (fp64), minus w_t W_u[y_t].
+// With at most 64 columns the product takes one pass over the logits instead (an online
+// softmax feeding the matrix cores, launch_softmax_product_online in k_fused.hip).
 //
 // The same product serves the folded order for a large vocabulary (loca_error_targets
 // with bf16 A~): the right operand is then the blocks' A~ side by side (column j of
@@ -307,11 +309,30 @@ int head_splits(int64_t n, int64_t V, int64_t d) {
 
 }  // namespace
 
-size_t softmax_product_ws(int64_t n, int64_t V, int64_t cols) {
+// At most 64 columns (one tile of the single-pass kernel) the logits are read once, by the
+// online-softmax product; wider products keep the statistics pass and a product pass per
+// 128 columns.
+// (Its buffer loads take 31-bit byte offsets within 128 rows of logits and 64 rows of the
+// right operand.)
+static bool product_online(const SoftmaxProductArgs& a) {
+  const int64_t zb = a.logits_dtype == LOCA_BF16 ? 2 : 4;
+  return a.groups * a.kc <= 64 && 128 * a.ld_logits * zb < ((int64_t)1 << 31) &&
+         64 * ((a.V + 63) / 64) * 64 * 2 < ((int64_t)1 << 31);
+}
+
+static size_t two_pass_ws(int64_t n, int64_t V, int64_t cols) {
   return align256(sizeof(float) * 2 * n) + align256(sizeof(float) * (size_t)head_splits(n, V, cols) * n * cols);
 }
 
+size_t softmax_product_ws(int64_t n, int64_t V, int64_t cols) {
+  const size_t two = two_pass_ws(n, V, cols);
+  if (cols > 64) return two;
+  const size_t one = softmax_product_online_ws(n, V, cols);
+  return one > two ? one : two;  // the path is chosen at the launch (it also depends on the strides)
+}
+
 hipError_t launch_softmax_product(const SoftmaxProductArgs& a) {
+  if (product_online(a)) return launch_softmax_product_online(a);
   float* ms = (float*)a.ws;
   float* part = (float*)(a.ws + align256(sizeof(float) * 2 * a.n));
   const int64_t cols = a.groups * a.kc;

@@ -58,6 +58,9 @@ struct SoftmaxProductArgs {
 };
 size_t softmax_product_ws(int64_t n, int64_t V, int64_t cols);
 hipError_t launch_softmax_product(const SoftmaxProductArgs& a);
+// the same product in one pass over the logits (online softmax), one pass per 64 columns
+size_t softmax_product_online_ws(int64_t n, int64_t V, int64_t cols);
+hipError_t launch_softmax_product_online(const SoftmaxProductArgs& a);
 
 struct CreditArgs {
   hipStream_t stream;
