@@ -88,6 +88,18 @@ __global__ __launch_bounds__(256) void k_equil_setup(int64_t d, int64_t m, int64
   }
 }
 
+// RHS[i][c] = D_i [S Lp | K][i][c] only (the factor of an earlier call is reused).
+template <typename T, typename ST>
+__global__ void k_equil_rhs(int64_t d, int64_t m, int64_t r_prev, const ST* __restrict__ K, int64_t k_bstride,
+                            const double* __restrict__ SLp, int nl, const T* __restrict__ D, T* __restrict__ R) {
+  const int64_t mi = blockIdx.y, b = mi / nl;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= d * m) return;
+  const int64_t i = e / m, c = e % m, k = m - r_prev;
+  const double v = (c < r_prev) ? SLp[b * d * r_prev + i * r_prev + c] : (double)K[b * k_bstride + i * k + (c - r_prev)];
+  R[mi * d * m + e] = (T)((double)D[mi * d + i] * v);
+}
+
 // The same for float statistics and factors when d % 4 == 0 and the rows of S are 16-byte
 // aligned, tiled so that every workgroup has the same amount of work: a workgroup takes
 // kEqRows rows and one chunk of kEqCols columns (chunks wholly below the diagonal exit),
@@ -1373,6 +1385,9 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
   T* Mp = Mpw + mi0 * d * m;
   // trailing updates through the direct-to-LDS kernel when a matrix fits 31-bit byte offsets
   const bool syrk_dl = sizeof(T) == 4 && d % 4 == 0 && 4 * d * d < ((int64_t)1 << 31);
+  // an earlier call's factor (fp64 only): only the right-hand-side tiles of each launch run
+  const bool reuse = a.reuse_factor && sizeof(T) == 8;
+  if (a.reuse_factor && !reuse) return hipErrorNotSupported;
   double* SLp = SLpw + b0 * d * (a.r_prev > 0 ? a.r_prev : 1);
   int32_t* info = a.dev_info + mi0;
   const ST* S = (const ST*)a.S + b0 * a.s_bstride;
@@ -1389,6 +1404,11 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
         dim3 g((unsigned)((d + kSM - 1) / kSM), (unsigned)nbg, (unsigned)((r_prev + 31) / 32));
         k_sym_mul<ST, 32><<<g, 256, 0, st>>>(d, r_prev, S, s_bstride, lp, lp_bstride, SLp);
       }
+    }
+    if (reuse) {  // D and F from the earlier call: the right-hand sides only
+      dim3 gr((unsigned)((d * m + 255) / 256), (unsigned)nm);
+      k_equil_rhs<T, ST><<<gr, 256, 0, st>>>(d, m, r_prev, K, k_bstride, SLp, (int)nl, D, R);
+      return hipGetLastError();
     }
     dim3 g((unsigned)((d + 255) / 256), (unsigned)nm);
     k_equil_diag<T, ST><<<g, 256, 0, st>>>(d, S, s_bstride, dlam, (int)nl, D);
@@ -1432,6 +1452,9 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
             if (!x6r)
               k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
                   d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
+          } else if (reuse) {
+            k_panel_product<T, kTrailing><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(
+                d, m, 0, P0, pp - P0, pp, 1, (int)T2, F, R);
           } else {
             k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 + TM), (unsigned)nm), kT, 0, st>>>(
                 d, m, 0, P0, pp - P0, pp, 1, 0, F, R);
@@ -1444,7 +1467,7 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
       if (rec && emit.ops) emit.stagger_at = (int)emit.ops->size();
       e = emit([=]() {
         if constexpr (sizeof(T) == 4) k_diag_f32<<<(unsigned)nm, kT, 0, st>>>(d, pp, (float*)F, info);
-        else k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
+        else if (!reuse) k_diag_block<T><<<(unsigned)nm, kT, 0, st>>>(d, pp, F, info);
         const hipError_t er = hipGetLastError();
         if (er != hipSuccess || !rec) return er;
         return hipEventRecord(after_diag, st);
@@ -1458,6 +1481,9 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
           if (!x6r)
             k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
                                                                                                  (int)nchF, F, R);
+        } else if (reuse) {
+          k_panel_product<T, kRowPanel><<<dim3((unsigned)TM, (unsigned)nm), kT, 0, st>>>(d, m, pp, 0, 0, 0, 0,
+                                                                                          (int)nchF, F, R);
         } else {
           k_panel_product<T, kRowPanel><<<dim3((unsigned)(nchF + TM), (unsigned)nm), kT, 0, st>>>(
               d, m, pp, 0, 0, 0, 0, 0, F, R);
@@ -1484,6 +1510,9 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
           if (!x6r)
             k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
                 d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
+        } else if (reuse) {
+          k_panel_product<T, kTrailing><<<dim3((unsigned)(T2 * TM), (unsigned)nm), kT, 0, st>>>(
+              d, m, 0, P0, P1 - P0, P1, 0, (int)nU, F, R);
         } else {
           k_panel_product<T, kTrailing><<<dim3((unsigned)(nU + T2 * TM), (unsigned)nm), kT, 0, st>>>(
               d, m, 0, P0, P1 - P0, P1, 0, 0, F, R);

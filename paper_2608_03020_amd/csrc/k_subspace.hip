@@ -156,20 +156,20 @@ __global__ __launch_bounds__(kT) void k_chol_inv(int l, const double* __restrict
 }
 
 // dst (d x w, float64) = columns c0 .. c0 + w - 1 of E (d x np, float)
-__global__ void k_cols_f64(int64_t d, int64_t np_, int64_t c0, int w, const float* __restrict__ E,
+__global__ void k_cols_f64(int64_t d, int64_t np_, int64_t c0, int w, int wh, const float* __restrict__ E,
                            double* __restrict__ dst) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= d * w) return;
   const int64_t c = e / w, j = e % w;
-  dst[e] = (double)E[c * np_ + c0 + j];
+  dst[e] = j < wh ? (double)E[c * np_ + c0 + j] : 0.0;
 }
-// columns c0 .. c0 + w - 1 of Rt (d x np) = M (d x w)
-__global__ void k_cols_put(int64_t d, int64_t np_, int64_t c0, int w, const float* __restrict__ M,
+// columns c0 .. c0 + wh - 1 of Rt (d x np) = the first wh columns of M (d x w)
+__global__ void k_cols_put(int64_t d, int64_t np_, int64_t c0, int w, int wh, const float* __restrict__ M,
                            float* __restrict__ Rt) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= d * w) return;
-  const int64_t c = e / w, j = e % w;
-  Rt[c * np_ + c0 + j] = M[e];
+  if (e >= d * wh) return;
+  const int64_t c = e / wh, j = e % wh;
+  Rt[c * np_ + c0 + j] = M[c * w + j];
 }
 // per block b: dst_b (d x l, float64) = Omega (d x l, float)
 __global__ void k_start_block(int64_t cnt, const float* __restrict__ omega, double* __restrict__ dst) {
@@ -272,18 +272,20 @@ hipError_t launch_feedback_fit_large(const CalibArgs& a) {
   double* Qa = (double*)p; p += align256(sizeof(double) * nb * k * np_);
   hipError_t e;
 
-  // 1-2: S_E = E E^T, then R^T = (S_E + beta I)^{-1} E chunk by chunk
+  // 1-2: S_E = E E^T, then R^T = (S_E + beta I)^{-1} E chunk by chunk: the first chunk
+  // factors S_E + beta I, the later ones reuse that factor (same width w, the last chunk's
+  // missing columns zero; their status entries read 0, the factor's is the first)
   gemm<float, float>(st, 1, d, d, np_, a.e, 0, np_, 1, a.e, 0, 1, np_, SE, 0, d);
   const double lam[1] = {a.beta};
   for (int64_t h = 0; h < nch; ++h) {
     const int64_t c0 = h * kSolveCols;
     const int wh = (int)(np_ - c0 < kSolveCols ? np_ - c0 : kSolveCols);
-    k_cols_f64<<<cdiv(d * wh, 256), 256, 0, st>>>(d, np_, c0, wh, a.e, Ec);
+    k_cols_f64<<<cdiv(d * w, 256), 256, 0, st>>>(d, np_, c0, (int)w, wh, a.e, Ec);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    SolveArgs sa{st, 1, d, wh, SE, Ec, LOCA_F64, d * d, d * wh, nullptr, nullptr, 0, 0, 0, lam, 1, Mc, d * wh,
-                 nullptr, 0, nullptr, 0, sinfo + h, sws};
+    SolveArgs sa{st, 1, d, w, SE, Ec, LOCA_F64, d * d, d * w, nullptr, nullptr, 0, 0, 0, lam, 1, Mc, d * w,
+                 nullptr, 0, nullptr, 0, sinfo + h, sws, h > 0};
     if ((e = launch_ridge_solve(sa)) != hipSuccess) return e;
-    k_cols_put<<<cdiv(d * wh, 256), 256, 0, st>>>(d, np_, c0, wh, Mc, Rt);
+    k_cols_put<<<cdiv(d * wh, 256), 256, 0, st>>>(d, np_, c0, (int)w, wh, Mc, Rt);
   }
   k_fold_solve_info<<<1, 64, 0, st>>>(sinfo, (int)nch, a.dev_info, nb);
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -99,6 +99,11 @@ struct SolveArgs {
   const float* credit_b; int64_t b_bstride;
   float* w_dense_out; int64_t w_bstride;
   int32_t* dev_info; char* ws;
+  // Internal (acc = F64 only): the factor and the scaling of a previous call with the same
+  // S, lambdas, sizes and workspace, ordered before this one, are still in `ws`; only the
+  // right-hand sides are scaled, carried through the forward substitution and solved.
+  // dev_info then reads 0: the factor's status is the one the factoring call reported.
+  bool reuse_factor;
 };
 size_t ridge_solve_ws(int64_t nb, int64_t d, int64_t m, int64_t n_lambda, loca_dtype acc);
 hipError_t launch_ridge_solve(const SolveArgs& a);
