@@ -302,16 +302,20 @@ def next_rows(args, cfg, nb, x_all, z, y, A, B, step, stream):
     time_steps(calib_large, reps_l, 1)
     t_l = sum(a.elapsed_time(b) for a, b in lev) / reps_l
     d_ = cfg.d
-    # algorithmic float64 flops: E E^T, one factorisation and the np right-hand sides, the
-    # 2q + 2 products with F_hat or F_hat^T (two skinny products each), 2q + 1 two-pass
-    # Cholesky QRs (Gram and basis update), and the alignment products
-    fl = (2.0 * d_ * d_ * n_p + d_ ** 3 / 3.0 + 2.0 * d_ * d_ * n_p
+    # algorithmic float64 flops: E E^T, one factorisation, the triangular solves (the np
+    # columns of E when R is formed, or l columns per block and product when it is applied,
+    # whichever takes fewer solves of at most 128 columns), the 2q + 2 products with F_hat or
+    # F_hat^T (two skinny products each), 2q + 1 two-pass Cholesky QRs (Gram and basis
+    # update), and the alignment products
+    applied = 2 * (q + 1) * nb < -(-n_p // 128)
+    solve_cols = (2 * q + 2) * nb * l if applied else n_p
+    fl = (2.0 * d_ * d_ * n_p + d_ ** 3 / 3.0 + 2.0 * d_ * d_ * solve_cols
           + nb * ((2 * q + 2) * 4.0 * d_ * n_p * l + (2 * q + 1) * 2 * 4.0 * d_ * l * l + 4.0 * k * d_ * n_p))
     tfs = fl / (t_l * 1e-3) / 1e12
     out["feedback_fit_large"] = {
         "ms_per_call": t_l, "unit": "ms per calibration of all blocks", "higher_is_better": False,
         "config": {"blocks": nb, "d": d_, "probes": n_p, "credit_rank": k, "basis": l, "rounds": q,
-                   "head_rows": V, "beta": 0.05},
+                   "head_rows": V, "beta": 0.05, "R": "applied" if applied else "formed"},
         "info_ok": bool((info == 0).all().item()), "alpha_mean": float(alpha.mean().item()),
         "roofline": {"bound": "alu", "achieved": tfs, "peak": FP64_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": tfs / FP64_PEAK_TFLOPS, "traffic": None, "kernel": "loca_feedback_fit_large (all blocks)",
