@@ -131,6 +131,11 @@ LOCA_DEV double rcp64(double x) {
   for (int i = 0; i < 2; ++i) y = fma(y, fma(-x, y, 1.0), y);
   return y;
 }
+// 1/x from the hardware approximation and one Newton step (about 2^-46 relative).
+LOCA_DEV double rcp64_1(double x) {
+  const double y = __builtin_amdgcn_rcp(x);
+  return fma(y, fma(-x, y, 1.0), y);
+}
 LOCA_DEV double rsq64(double x) {
   double y = __builtin_amdgcn_rsq(x);
 #pragma unroll
@@ -238,6 +243,303 @@ LOCA_DEV void jacobi_packed(double* A, VT* V, int n, double* cs, int* pairs, dou
     }
   }
   __syncthreads();
+}
+
+// ------------------------------------------------------------------ symmetric eigensolver, leading part
+
+// A double moved between lanes of a row of 16 by a DPP pattern (CTRL: quad_perm or row_ror).
+template <int CTRL>
+LOCA_DEV double dpp_d(double v) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)b, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(b >> 32), CTRL, 0xF, 0xF, false);
+  return __longlong_as_double(((long long)hi << 32) | (long long)(unsigned)lo);
+}
+// Sum over aligned groups of 16 lanes by DPP moves (quad xor 1 and 2, then row rotations by
+// 4 and 8); every lane of a group gets the sum, possibly differing in the last bit between
+// its quads (the two rotations associate the four quad sums differently).
+LOCA_DEV double seg16_sum(double v) {
+  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_d<0x124>(v);  // row_ror:4
+  v += dpp_d<0x128>(v);  // row_ror:8
+  return v;
+}
+LOCA_DEV double readlane_d(double v, int l) {
+  const long long b = __double_as_longlong(v);
+  const int lo = __builtin_amdgcn_readlane((int)b, l);
+  const int hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+  return __longlong_as_double(((long long)hi << 32) | (long long)(unsigned)lo);
+}
+// Sum over the lanes of a wave: the sums of the four rows of 16, then their total in a
+// fixed order from lanes 0, 16, 32, 48, the same value in every lane (and in every wave
+// that sums the same data).
+LOCA_DEV double wave_sum_all(double v) {
+  v = seg16_sum(v);
+  return (readlane_d(v, 0) + readlane_d(v, 16)) + (readlane_d(v, 32) + readlane_d(v, 48));
+}
+// A pivot of magnitude below pivmin is replaced by -pivmin (a Sturm count then treats it as
+// negative, and no quotient overflows).
+LOCA_DEV double safe_pivot(double q, double pivmin) { return fabs(q) < pivmin ? -pivmin : q; }
+
+constexpr int kRedEig = 43;  // reduction-scratch slot: a check of eig_top failed
+
+// All eigenvalues of the packed symmetric K x K matrix A (packed with stride n, K <= 64) and
+// the eigenvectors of its r largest, A left unchanged:
+//   1. Householder reduction T = Q^T A Q to tridiagonal form on a dense copy in V (the
+//      trailing matrix kept whole and symmetric), two barriers per step: every wave forms
+//      the reflector v of row k itself, p = tau A v with 16 lanes per row, then every wave
+//      w = p - (tau/2)(p^T v) v and the rank-2 update A -= v w^T + w v^T over a 32 x 32
+//      grid of threads; the reflector is stored in row k right of the diagonal;
+//   2. every eigenvalue of T by multisection of Sturm counts: 16 lanes per eigenvalue test
+//      the 15 interior points of 16 equal steps of its interval, 15 times for the r largest
+//      (the Gershgorin interval shrunk 2^60 times, past the double precision of its end
+//      points) and 11 times for the others (2^44: their only use is the float sigma);
+//      the pivots' reciprocals from the hardware approximation and one Newton step;
+//   3. the eigenvector of T for each of the r largest (one lane each) from the twisted
+//      factorization of T - lambda I: the pivots of the top-down and bottom-up LDL^T, the
+//      twist index where their combination is smallest, and one solve that starts there;
+//   4. x = Q z (the reflectors applied in reverse order; 16 lanes per vector).
+// Then a check: every residual ||A x - lambda x|| within 1e-11 of the largest |lambda| and
+// every pair of the r vectors orthonormal within 1e-9.  It fails when eigenvalues among the
+// r largest lie too close together for the twisted solves to separate their vectors (a
+// repeated or clustered leading spectrum); the caller then runs Jacobi on A.  On success
+// eig[j] is the j-th largest eigenvalue (j < K) and column j of V (row-major, stride n) its
+// unit eigenvector for j < r; the other entries of V are zero.  Z: r x K doubles of scratch;
+// dT, eT, e2, tauH, pbuf: 64 doubles each.  Run by the kTC threads of one workgroup.
+LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z, double* dT, double* eT,
+                      double* e2, double* tauH, double* pbuf, double* eig, double* red) {
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  for (int e = tid; e < n * n; e += kTC) {
+    const int i = e / n, j = e % n;
+    V[e] = (i < K && j < K) ? A[pk(i, j, n)] : 0.0;
+  }
+  if (tid == 0) red[kRedEig] = 0.0;
+  __syncthreads();
+  // 1. reduction to tridiagonal form
+  {
+    const int ty = tid >> 5, tx = tid & 31;
+    for (int k = 0; k + 2 < K; ++k) {
+      const int m = K - k - 1;  // entries right of the diagonal in row k
+      // the reflector of row k, formed by every wave alike (row k is final since the
+      // last barrier); row k keeps x until the step's end, v_0 is kept apart
+      const double x = lane < m ? V[k * n + k + 1 + lane] : 0.0;
+      const double ss = wave_sum_all(x * x);
+      const double x0 = V[k * n + k + 1];
+      double tau = 0.0, alpha = x0, v0 = x0;
+      if (ss > 0.0) {
+        alpha = x0 >= 0.0 ? -sqrt(ss) : sqrt(ss);
+        v0 = x0 - alpha;
+        tau = 2.0 / (ss - x0 * x0 + v0 * v0);
+      }
+      if (tid == 0) {
+        tauH[k] = tau;
+        eT[k] = alpha;
+        dT[k] = V[k * n + k];
+      }
+      if (tau != 0.0) {  // uniform: every wave has the same ss
+        {  // p_i = tau sum_c A[k+1+i][k+1+c] v_c, 16 lanes per row i
+          const int row = tid >> 4, part = tid & 15;
+          double acc = 0.0;
+          if (row < m)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              const int c = part + 16 * u;
+              if (c < m) acc += V[(k + 1 + row) * n + k + 1 + c] * (c == 0 ? v0 : V[k * n + k + 1 + c]);
+            }
+          acc = seg16_sum(acc);
+          if (row < m && part == 0) pbuf[row] = tau * acc;
+        }
+        __syncthreads();
+        const double vl = lane == 0 ? v0 : x;
+        const double kk = 0.5 * tau * wave_sum_all(lane < m ? pbuf[lane] * vl : 0.0);
+        // A[k+1+i][k+1+c] -= v_i w_c + w_i v_c, w = p - kk v; thread (ty, tx) takes
+        // i in {ty, ty + 32}, c in {tx, tx + 32}
+#pragma unroll
+        for (int a = 0; a < 2; ++a) {
+          const int i = ty + 32 * a;
+          if (i >= m) continue;
+          const double vi = i == 0 ? v0 : V[k * n + k + 1 + i];
+          const double wi = pbuf[i] - kk * vi;
+#pragma unroll
+          for (int b = 0; b < 2; ++b) {
+            const int c = tx + 32 * b;
+            if (c >= m) continue;
+            const double vc = c == 0 ? v0 : V[k * n + k + 1 + c];
+            const double wc = pbuf[c] - kk * vc;
+            V[(k + 1 + i) * n + k + 1 + c] -= vi * wc + wi * vc;
+          }
+        }
+      }
+      __syncthreads();
+      if (tid == 0) V[k * n + k + 1] = v0;  // the reflector complete in row k (read only later)
+    }
+    if (tid == 0) {
+      if (K >= 2) {
+        dT[K - 2] = V[(K - 2) * n + K - 2];
+        eT[K - 2] = V[(K - 2) * n + K - 1];
+      }
+      dT[K - 1] = V[(K - 1) * n + K - 1];
+    }
+  }
+  __syncthreads();
+  for (int i = tid; i + 1 < K; i += kTC) e2[i] = eT[i] * eT[i];
+  // Gershgorin interval, widened as in LAPACK's bisection, and the pivot floor
+  double glo = 0.0, ghi = 0.0, emax2 = 0.0;
+  for (int i = 0; i < K; ++i) {
+    const double rad = (i > 0 ? fabs(eT[i - 1]) : 0.0) + (i + 1 < K ? fabs(eT[i]) : 0.0);
+    glo = i == 0 ? dT[i] - rad : fmin(glo, dT[i] - rad);
+    ghi = i == 0 ? dT[i] + rad : fmax(ghi, dT[i] + rad);
+    if (i + 1 < K) emax2 = fmax(emax2, eT[i] * eT[i]);
+  }
+  const double pivmin = 2.2250738585072014e-308 * fmax(1.0, emax2);
+  const double tnorm = fmax(fabs(glo), fabs(ghi));
+  glo -= 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
+  ghi += 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
+  __syncthreads();
+  // 2. multisection: group g = tid / 16 finds the g-th smallest eigenvalue, lane t of the
+  // group testing point t + 1 of 16 equal steps (the last one is hi); 15 steps (60 bits)
+  // for the r largest, whose vectors follow, 11 (44 bits) for the others
+  {
+    const int g = tid >> 4, t = tid & 15;
+    const int j = g < K ? g : K - 1;
+    const int steps = K - 1 - j < r ? 15 : 11;
+    double lo = glo, hi = ghi;
+    for (int it = 0; it < steps; ++it) {
+      const double h = (hi - lo) * (1.0 / 16.0);
+      const double x = lo + (double)(t + 1) * h;
+      double q = safe_pivot(dT[0] - x, pivmin);
+      int cnt = q < 0.0;
+      for (int i = 1; i < K; ++i) {
+        q = safe_pivot((dT[i] - x) - e2[i - 1] * rcp64_1(q), pivmin);
+        cnt += q < 0.0;
+      }
+      if (t == 15) cnt = K;
+      const unsigned long long b = __ballot(cnt > j);
+      const unsigned seg = (unsigned)(b >> (lane & 48)) & 0xFFFFu;  // lane 15 of the group always set
+      const int f = __builtin_ctz(seg);
+      const double nlo = f == 0 ? lo : lo + (double)f * h;
+      hi = f == 15 ? hi : lo + (double)(f + 1) * h;
+      lo = nlo;
+    }
+    if (g < K && t == 0) eig[K - 1 - g] = 0.5 * (lo + hi);
+  }
+  __syncthreads();
+  // 3. twisted factorizations (lane a: the a-th largest eigenvalue; scratch row Z + a K)
+  if (tid < r) {
+    const double lam = eig[tid];
+    double* w = Z + tid * K;
+    double dp = safe_pivot(dT[0] - lam, pivmin);
+    w[0] = dp;
+    for (int i = 0; i + 1 < K; ++i) {
+      dp = safe_pivot((dT[i + 1] - lam) - e2[i] / dp, pivmin);
+      w[i + 1] = dp;
+    }
+    double dm = safe_pivot(dT[K - 1] - lam, pivmin);
+    int rr = K - 1;
+    double gmin = fabs(w[K - 1]);
+    for (int i = K - 2; i >= 0; --i) {
+      const double u = eT[i] / dm;
+      const double dmi = safe_pivot((dT[i] - lam) - u * eT[i], pivmin);
+      const double gam = w[i] + dmi - (dT[i] - lam);
+      if (fabs(gam) < gmin) {
+        gmin = fabs(gam);
+        rr = i;
+      }
+      w[i] = u;  // u_i replaces the top-down pivot
+      dm = dmi;
+    }
+    double z = 1.0, nrm = 1.0;
+    for (int i = rr; i + 1 < K; ++i) {  // z_{i+1} = -u_i z_i
+      const double u = w[i];
+      w[i] = z;
+      z = -u * z;
+      nrm += z * z;
+    }
+    w[K - 1] = z;
+    if (rr > 0) {  // z_i = -l_i z_{i+1} with l_i = e_i / (top-down pivot i), recomputed
+      double dq = safe_pivot(dT[0] - lam, pivmin);
+      for (int i = 0; i < rr; ++i) {
+        const double l = eT[i] / dq;
+        w[i] = l;
+        dq = safe_pivot((dT[i + 1] - lam) - l * eT[i], pivmin);
+      }
+      double zz = 1.0;
+      for (int i = rr - 1; i >= 0; --i) {
+        zz = -w[i] * zz;
+        w[i] = zz;
+        nrm += zz * zz;
+      }
+    }
+    const double sc = 1.0 / sqrt(nrm);
+    for (int i = 0; i < K; ++i) w[i] *= sc;
+  }
+  __syncthreads();
+  // 4. x = H_0 H_1 ... H_{K-3} z: 16 lanes per vector, entries t + 16 q in registers
+  {
+    const int a = tid >> 4, t = tid & 15;
+    const bool act = a < r;
+    double zr[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int i = t + 16 * q;
+      zr[q] = (act && i < K) ? Z[a * K + i] : 0.0;
+    }
+    for (int k = K - 3; k >= 0; --k) {
+      const double tau = tauH[k];
+      if (tau == 0.0) continue;
+      double dot = 0.0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = t + 16 * q;
+        if (i > k && i < K) dot += V[k * n + i] * zr[q];
+      }
+      const double f = tau * seg16_sum(dot);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = t + 16 * q;
+        if (i > k && i < K) zr[q] -= f * V[k * n + i];
+      }
+    }
+    __syncthreads();  // the reflectors are read by every group before V is overwritten
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (j >= r || i >= K) V[e] = 0.0;
+    }
+    if (act)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int i = t + 16 * q;
+        if (i < K) V[i * n + a] = zr[q];
+      }
+  }
+  __syncthreads();
+  // the check
+  const double anorm = fmax(fabs(eig[0]), fabs(eig[K - 1]));
+  {
+    const int a = tid >> 4, t = tid & 15;
+    double rs = 0.0;
+    if (a < r) {
+      const double lam = eig[a];
+      for (int i = t; i < K; i += 16) {
+        double s = -lam * V[i * n + a];
+        for (int c = 0; c < K; ++c) s += A[pk(i, c, n)] * V[c * n + a];
+        rs += s * s;
+      }
+    }
+    rs = seg16_sum(rs);
+    const double tol = 1e-11 * anorm;
+    if (a < r && t == 0 && !(rs <= tol * tol)) red[kRedEig] = 1.0;
+  }
+  for (int e = tid; e < r * r; e += kTC) {
+    const int a = e / r, b = e % r;
+    if (a > b) continue;
+    double s = 0.0;
+    for (int i = 0; i < K; ++i) s += V[i * n + a] * V[i * n + b];
+    if (!(fabs(s - (a == b ? 1.0 : 0.0)) <= 1e-9)) red[kRedEig] = 1.0;
+  }
+  __syncthreads();
+  return red[kRedEig] == 0.0;
 }
 
 // The truncation core for 64 < kp <= 128 (see the file comment).  Per matrix the workspace
@@ -420,6 +722,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   __shared__ double sVb[KB2];  // Gb, then its factor: L (Cholesky) or Vb (Jacobi)
   __shared__ double sG[KB2];   // Gm; L^{-T} Vp after the eigensolve (Cholesky path)
   __shared__ double sH[kMaxKp], sHi[kMaxKp], sEig[kMaxKp];
+  __shared__ double sT[5][kMaxKp];  // the tridiagonal eigensolver's vectors
   __shared__ int sOrd[kMaxKp];
   __shared__ __attribute__((aligned(16))) double cs[kMaxKp];
   __shared__ __attribute__((aligned(16))) int pairs[kMaxKp];
@@ -443,33 +746,48 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
     sVb[e] = gb;
   }
   __syncthreads();
-  // 2. Gb = L L^T in place (lower triangle of sVb), or a failed pivot
-  if (tid == 0) {
+  // 2. Gb = L L^T (L in the lower triangle of sVb), or a failed pivot.  One barrier per
+  // step: step j updates the trailing lower triangle from the unscaled column j,
+  // A[i][c] -= A[i][j] A[c][j] / A[j][j] (thread (ty, tx) of a 32 x 32 grid takes i in
+  // {ty, ty + 32}, c in {tx, tx + 32}), while column j - 1, no longer read, is scaled into L.
+  {
+    const int ty = tid >> 5, tx = tid & 31;
     double mx = 0.0;
     for (int j = 0; j < K; ++j) mx = fmax(mx, sVb[j * n + j]);
-    red[kRedDiag] = mx;
-    red[kRedFail] = 0.0;
+    const double thr = 1e-10 * mx;
+    bool fail = false;
+    int j = 0;
+    for (; j < K; ++j) {
+      const double piv = sVb[j * n + j];
+      if (j > 0) {  // column j - 1 into L
+        const double pj = sVb[(j - 1) * n + j - 1];  // its pivot, still unscaled
+        const double inv = 1.0 / sqrt(pj);
+        for (int i = j + tid; i < K; i += kTC) sVb[i * n + j - 1] *= inv;
+      }
+      if (!(piv > thr)) {  // uniform: every thread reads the same pivot
+        fail = true;
+        break;
+      }
+      const double rp = 1.0 / piv;
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        const int i = ty + 32 * a;
+        if (i <= j || i >= K) continue;
+        const double aij = sVb[i * n + j] * rp;
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int c = tx + 32 * b;
+          if (c <= j || c > i) continue;
+          sVb[i * n + c] -= aij * sVb[c * n + j];
+        }
+      }
+      __syncthreads();
+    }
+    if (!fail)  // the diagonal of L (the last column has nothing below it)
+      for (int i = tid; i < K; i += kTC) sVb[i * n + i] = sqrt(sVb[i * n + i]);
+    if (tid == 0) red[kRedFail] = fail ? 1.0 : 0.0;
   }
   __syncthreads();
-  const double thr = 1e-10 * red[kRedDiag];
-  for (int j = 0; j < K; ++j) {
-    if (tid == 0) {
-      const double piv = sVb[j * n + j];
-      if (!(piv > thr)) red[kRedFail] = 1.0;
-      sVb[j * n + j] = sqrt(fmax(piv, 0.0));
-    }
-    __syncthreads();
-    if (red[kRedFail] != 0.0) break;
-    const double ljj = sVb[j * n + j];
-    for (int i = j + 1 + tid; i < K; i += kTC) sVb[i * n + j] /= ljj;
-    __syncthreads();
-    const int rem = K - j - 1;
-    for (int e = tid; e < rem * rem; e += kTC) {
-      const int i = j + 1 + e / rem, c = j + 1 + e % rem;
-      if (c <= i) sVb[i * n + c] -= sVb[i * n + j] * sVb[c * n + j];
-    }
-    __syncthreads();
-  }
   const bool chol = red[kRedFail] == 0.0;
   if (chol) {
     // 3. T = Gm L (into sV), P^T P = L^T T (upper triangle, packed; zero padding)
@@ -533,25 +851,51 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
     }
     __syncthreads();
   }
-  jacobi_packed<double>(sA, sV, n, cs, pairs, red);  // sV = Vp
-  __syncthreads();
-  if (tid == 0) {
-    // order by decreasing eigenvalue (insertion sort on indices)
-    for (int j = 0; j < K; ++j) { sEig[j] = sA[pk(j, j, n)]; sOrd[j] = j; }
-    for (int i = 1; i < K; ++i) {
-      const int key = sOrd[i];
-      int j = i - 1;
-      while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
-      sOrd[j + 1] = key;
+  // sV = Vp: the leading r_a eigenpairs from the tridiagonal path, or every pair by Jacobi
+  // when its check fails
+  const int ra = (int)(r_a < kp ? r_a : kp);
+  if (eig_top(sA, n, K, ra, sV, sG, sT[0], sT[1], sT[2], sT[3], sT[4], sEig, red)) {
+    for (int j = tid; j < K; j += kTC) sOrd[j] = j;
+  } else {
+    jacobi_packed<double>(sA, sV, n, cs, pairs, red);
+    __syncthreads();
+    if (tid == 0) {
+      // order by decreasing eigenvalue (insertion sort on indices)
+      for (int j = 0; j < K; ++j) { sEig[j] = sA[pk(j, j, n)]; sOrd[j] = j; }
+      for (int i = 1; i < K; ++i) {
+        const int key = sOrd[i];
+        int j = i - 1;
+        while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
+        sOrd[j + 1] = key;
+      }
     }
   }
-  if (chol) {  // Z = L^{-T} Vp (into sG, Gm no longer needed): one column per thread
-    for (int a = tid; a < n; a += kTC)
+  __syncthreads();
+  if (chol) {  // Z = L^{-T} Vp for the kept columns (into sG): 16 lanes per column, entries
+               // x = t + 16 q of the column in registers while the substitution runs upwards
+    const int a = tid >> 4, t = tid & 15;
+    if (a < ra) {
+      const int col = sOrd[a];
+      double zq[4] = {0.0, 0.0, 0.0, 0.0};
       for (int c = K - 1; c >= 0; --c) {
-        double s = sV[c * n + a];
-        for (int x = c + 1; x < K; ++x) s -= sVb[x * n + c] * sG[x * n + a];
-        sG[c * n + a] = s / sVb[c * n + c];
+        double sum = 0.0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int x = t + 16 * q;
+          if (x > c && x < K) sum += sVb[x * n + c] * zq[q];
+        }
+        sum = seg16_sum(sum);
+        const double zc = (sV[c * n + col] - sum) / sVb[c * n + c];
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          if (c == t + 16 * q) zq[q] = zc;
       }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int x = t + 16 * q;
+        if (x < K) sG[x * n + col] = zq[q];
+      }
+    }
   }
   __syncthreads();
   const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
@@ -560,7 +904,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
   for (int e = tid; e < (int)(r_a * kp); e += kTC) {
-    const int a = e / K, c = e % K;
+    const int a = e % (int)r_a, c = e / (int)r_a;  // lanes along a: rows of sVb read once per wave
     const int col = sOrd[a];
     const double sa = sqrt(fmax(sEig[col], 0.0));
     double u = 0.0, v = 0.0;

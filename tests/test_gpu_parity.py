@@ -291,6 +291,46 @@ def test_truncation_matches_explicit_svd(d, kp, r):
     np.testing.assert_allclose(A.T @ b[0].cpu().numpy().T, W[0].cpu().numpy(), atol=1e-4 * np.abs(Wr_o).max())
 
 
+@pytest.mark.parametrize("kp,r", [(64, 32), (32, 8)])
+def test_truncation_repeated_leading_values(kp, r):
+    """Repeated singular values among the r kept (a triple and a pair): the eigenvectors of the
+    repeated eigenvalues cannot be told apart by the tridiagonal solves, so the core's check
+    sends the eigensolve to Jacobi.  M and B~ from a Hadamard matrix / 8 (orthogonal and exact
+    in float), so that W = M B~ has exactly the chosen singular values; W_r against the
+    oracle's dense SVD (the kept subspace is unique: sigma_r > sigma_{r+1})."""
+    import torch
+    import oracle
+    from scipy.linalg import hadamard
+    from paper_2608_03020_amd import loca
+    d = 150
+    log(f"case truncation_repeated: d={d} kp={kp} r_a={r}")
+    H = hadamard(64).astype(np.float64) / 8.0  # its first kp columns are orthonormal
+    sig = np.concatenate([[6.0, 6.0, 6.0, 5.0, 5.0], np.linspace(4.0, 0.5, kp - 5)])
+    Mh = np.zeros((d, kp), dtype=np.float32)
+    Mh[:64] = (H[:, :kp] * sig).astype(np.float32)
+    Rh = np.zeros((kp, d), dtype=np.float32)
+    Rh[:, 10:10 + 64] = H[:, :kp].T.astype(np.float32)
+    Wd = Mh.astype(np.float64) @ Rh.astype(np.float64)
+    Wr_o, s_o = oracle.truncate_dense(Wd, r)
+    assert np.allclose(s_o[:kp], sig, rtol=1e-6) and np.ptp(s_o[:3]) < 1e-12 * s_o[0]
+    a = torch.empty((1, r, d), device="cuda")
+    b = torch.empty((1, d, r), device="cuda")
+    s = torch.empty((1, kp), device="cuda")
+    W = torch.empty((1, d, d), device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, 1, 0, d, kp, r_a=r))
+    loca.loca_lowrank_truncate(torch.from_numpy(Mh)[None].cuda(), torch.from_numpy(Rh)[None].cuda(), r, a, b, s,
+                               info, ws, w_dense_out=W)
+    torch.cuda.synchronize()
+    e_w = rel(W[0].cpu().numpy(), Wr_o)
+    e_s = rel(s[0].cpu().numpy(), s_o[:kp])
+    A = a[0].cpu().numpy().astype(np.float64)
+    log(f"truncation (repeated leading values): W_r {e_w:.2e} sigma {e_s:.2e} "
+        f"orth {np.abs(A @ A.T - np.eye(r)).max():.2e}")
+    assert e_w < 1e-5 and e_s < 1e-5
+    assert np.abs(A @ A.T - np.eye(r)).max() < 1e-5
+
+
 @pytest.mark.parametrize("d,n,k,r_a,mode", [(300, 500, 16, 8, "bf16"), (1100, 2400, 48, 40, "bf16"),
                                              (130, 700, 64, 64, "bf16"), (200, 150, 16, 16, "fp32")])
 def test_projected_form_matches_oracle(d, n, k, r_a, mode):
