@@ -292,18 +292,22 @@ constexpr int kRedEig = 43;  // reduction-scratch slot: a check of eig_top faile
 //      w = p - (tau/2)(p^T v) v and the rank-2 update A -= v w^T + w v^T over a 32 x 32
 //      grid of threads; the reflector is stored in row k right of the diagonal;
 //   2. every eigenvalue of T by multisection of Sturm counts: 16 lanes per eigenvalue test
-//      the 15 interior points of 16 equal steps of its interval, 15 times for the r largest
-//      (the Gershgorin interval shrunk 2^60 times, past the double precision of its end
-//      points) and 11 times for the others (2^44: their only use is the float sigma);
+//      the 15 interior points of 16 equal steps of its interval, 13 times for the r largest
+//      (the widened Gershgorin interval, at most 2.2 ||T||, shrunk 2^52 times: a few units
+//      of double rounding of ||T||, the accuracy of the Sturm counts themselves) and 10
+//      times for the others (2^40: their only use is the float sigma);
 //      the pivots' reciprocals from the hardware approximation and one Newton step;
 //   3. the eigenvector of T for each of the r largest (one lane each) from the twisted
 //      factorization of T - lambda I: the pivots of the top-down and bottom-up LDL^T, the
 //      twist index where their combination is smallest, and one solve that starts there;
 //   4. x = Q z (the reflectors applied in reverse order; 16 lanes per vector).
-// Then a check: every residual ||A x - lambda x|| within 1e-11 of the largest |lambda| and
-// every pair of the r vectors orthonormal within 1e-9.  It fails when eigenvalues among the
-// r largest lie too close together for the twisted solves to separate their vectors (a
-// repeated or clustered leading spectrum); the caller then runs Jacobi on A.  On success
+// The path is left (false returned, and the caller runs Jacobi on A) before the
+// eigenvalues when fewer than r of them exceed 1e-12 ||T|| (one Sturm count: A of rank
+// below r, whose numerical zeros among the r largest have no separable vectors), before
+// the vectors when two of the r largest lie within 1e-10 of the largest |lambda| (a
+// repeated value), and after them when the check fails: every residual ||A x - lambda x||
+// within 1e-11 of the largest |lambda| and every pair of the r vectors orthonormal within
+// 1e-9.  On success
 // eig[j] is the j-th largest eigenvalue (j < K) and column j of V (row-major, stride n) its
 // unit eigenvector for j < r; the other entries of V are zero.  Z: r x K doubles of scratch;
 // dT, eT, e2, tauH, pbuf: 64 doubles each.  Run by the kTC threads of one workgroup.
@@ -328,9 +332,10 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
       const double x0 = V[k * n + k + 1];
       double tau = 0.0, alpha = x0, v0 = x0;
       if (ss > 0.0) {
-        alpha = x0 >= 0.0 ? -sqrt(ss) : sqrt(ss);
+        const double nx = ss > 1e-280 ? ss * rsq64(ss) : sqrt(ss);  // ||x||
+        alpha = x0 >= 0.0 ? -nx : nx;
         v0 = x0 - alpha;
-        tau = 2.0 / (ss - x0 * x0 + v0 * v0);
+        tau = 2.0 * rcp64(ss - x0 * x0 + v0 * v0);
       }
       if (tid == 0) {
         tauH[k] = tau;
@@ -397,13 +402,24 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
   glo -= 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
   ghi += 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
   __syncthreads();
+  {  // fewer than r eigenvalues above 1e-12 ||T||: the r largest hold a cluster of
+     // numerical zeros (A of rank below r), so Jacobi at once (every thread counts alike)
+    const double x0 = 1e-12 * tnorm;
+    double q = safe_pivot(dT[0] - x0, pivmin);
+    int below = q < 0.0;
+    for (int i = 1; i < K; ++i) {
+      q = safe_pivot((dT[i] - x0) - e2[i - 1] * rcp64_1(q), pivmin);
+      below += q < 0.0;
+    }
+    if (K - below < r) return false;
+  }
   // 2. multisection: group g = tid / 16 finds the g-th smallest eigenvalue, lane t of the
-  // group testing point t + 1 of 16 equal steps (the last one is hi); 15 steps (60 bits)
-  // for the r largest, whose vectors follow, 11 (44 bits) for the others
+  // group testing point t + 1 of 16 equal steps (the last one is hi); 13 steps (52 bits)
+  // for the r largest, whose vectors follow, 10 (40 bits) for the others
   {
     const int g = tid >> 4, t = tid & 15;
     const int j = g < K ? g : K - 1;
-    const int steps = K - 1 - j < r ? 15 : 11;
+    const int steps = K - 1 - j < r ? 13 : 10;
     double lo = glo, hi = ghi;
     for (int it = 0; it < steps; ++it) {
       const double h = (hi - lo) * (1.0 / 16.0);
@@ -425,6 +441,15 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
     if (g < K && t == 0) eig[K - 1 - g] = 0.5 * (lo + hi);
   }
   __syncthreads();
+  // eigenvalues among the r largest closer than 1e-10 of the largest |lambda| (a repeated
+  // value, or a numerically zero cluster when A has rank below r) cannot get orthogonal
+  // vectors from the twisted solves: Jacobi at once
+  {
+    const double sc = fmax(fabs(eig[0]), fabs(eig[K - 1]));
+    if (tid + 1 < r && !(eig[tid] - eig[tid + 1] > 1e-10 * sc)) red[kRedEig] = 1.0;
+  }
+  __syncthreads();
+  if (red[kRedEig] != 0.0) return false;
   // 3. twisted factorizations (lane a: the a-th largest eigenvalue; scratch row Z + a K)
   if (tid < r) {
     const double lam = eig[tid];
@@ -432,14 +457,14 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
     double dp = safe_pivot(dT[0] - lam, pivmin);
     w[0] = dp;
     for (int i = 0; i + 1 < K; ++i) {
-      dp = safe_pivot((dT[i + 1] - lam) - e2[i] / dp, pivmin);
+      dp = safe_pivot((dT[i + 1] - lam) - e2[i] * rcp64(dp), pivmin);
       w[i + 1] = dp;
     }
     double dm = safe_pivot(dT[K - 1] - lam, pivmin);
     int rr = K - 1;
     double gmin = fabs(w[K - 1]);
     for (int i = K - 2; i >= 0; --i) {
-      const double u = eT[i] / dm;
+      const double u = eT[i] * rcp64(dm);
       const double dmi = safe_pivot((dT[i] - lam) - u * eT[i], pivmin);
       const double gam = w[i] + dmi - (dT[i] - lam);
       if (fabs(gam) < gmin) {
@@ -460,7 +485,7 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
     if (rr > 0) {  // z_i = -l_i z_{i+1} with l_i = e_i / (top-down pivot i), recomputed
       double dq = safe_pivot(dT[0] - lam, pivmin);
       for (int i = 0; i < rr; ++i) {
-        const double l = eT[i] / dq;
+        const double l = eT[i] * rcp64(dq);
         w[i] = l;
         dq = safe_pivot((dT[i + 1] - lam) - l * eT[i], pivmin);
       }
@@ -471,7 +496,7 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
         nrm += zz * zz;
       }
     }
-    const double sc = 1.0 / sqrt(nrm);
+    const double sc = rsq64(nrm);
     for (int i = 0; i < K; ++i) w[i] *= sc;
   }
   __syncthreads();
@@ -761,14 +786,14 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
       const double piv = sVb[j * n + j];
       if (j > 0) {  // column j - 1 into L
         const double pj = sVb[(j - 1) * n + j - 1];  // its pivot, still unscaled
-        const double inv = 1.0 / sqrt(pj);
+        const double inv = rsq64(pj);
         for (int i = j + tid; i < K; i += kTC) sVb[i * n + j - 1] *= inv;
       }
       if (!(piv > thr)) {  // uniform: every thread reads the same pivot
         fail = true;
         break;
       }
-      const double rp = 1.0 / piv;
+      const double rp = rcp64(piv);
 #pragma unroll
       for (int a = 0; a < 2; ++a) {
         const int i = ty + 32 * a;
