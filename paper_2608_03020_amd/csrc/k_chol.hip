@@ -944,12 +944,33 @@ __global__ __launch_bounds__(512) void k_panel_x6(int64_t d, int64_t k0, int64_t
 // the fp32 rows of U read straight from F.  Stages of 16 rows x 256 columns (16 KB per
 // panel) stream into a four-slot LDS ring by direct copies, three stages ahead; the 16-byte
 // chunks of stage row r sit XOR-swizzled by 8 (r / 8), so that the two half-waves of an
-// operand read (rows r and r + 8) fall on different banks.  Every operand is split into
-// its three bf16 parts in registers (split3, hardware conversions) and feeds the six kept
-// products, smallest first.  A diagonal tile needs one panel (its second ring panel reads
-// nothing).  Tiles, waves and the XCD-aware workgroup order are those of the Gram kernel.
+// operand read (rows r and r + 8) fall on different banks.  The factor of the equilibrated
+// matrix (unit diagonal) has |U[kk][i]| <= 1, so every operand, scaled by 2^8, is split in
+// registers into two fp16 parts, u = h + l with h = fp16(2^8 u) and l = fp16(2^8 u - h)
+// (22 bits of u; a part past the fp16 range cannot occur), and the three kept products
+// l h, h l, h h (smallest first) run on the fp16 matrix cores, accumulated in fp32 and
+// scaled back by 2^-16 (exact) when F is updated: half the matrix-core work of a three-part
+// bf16 split, with product errors of the order of the fp32 accumulation's own rounding.
+// A diagonal tile needs one panel (its second ring panel reads nothing).  Tiles, waves and
+// the XCD-aware workgroup order are those of the Gram kernel.
 // Requires d % 4 == 0, kw % 16 == 0 and 4 d^2 < 2^31 bytes per matrix.
 constexpr int kS32BK = 16;  // K rows per stage
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2_v __attribute__((ext_vector_type(2)));
+LOCA_DEV f32x16_t mfma32h(f16x8_t a, f16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+// (2^8 a0, 2^8 a1) = h + l as packed fp16 pairs (a0 in the low halves); the difference is
+// exact in float
+LOCA_DEV void split2h_pair(float a0, float a1, uint32_t& hp, uint32_t& lp) {
+  const float s0 = a0 * 256.f, s1 = a1 * 256.f;
+  const f32x2_v v = {s0, s1};
+  const f16x2_v h = __builtin_convertvector(v, f16x2_v);
+  const float r0 = s0 - (float)h[0], r1 = s1 - (float)h[1];
+  const f32x2_v r = {r0, r1};
+  hp = __builtin_bit_cast(uint32_t, h);
+  lp = __builtin_bit_cast(uint32_t, __builtin_convertvector(r, f16x2_v));
+}
 // the 8 fp32 operand values of lane `lane` (rows 8 (lane / 32) + e of the stage, column
 // c0 + lane % 32 of the panel) from a swizzled stage, split into three MFMA operands
 LOCA_DEV void frag_f32_split(const float* stage, int c0, int lane, bf16x8_t& fh, bf16x8_t& fm, bf16x8_t& fl) {
@@ -964,6 +985,20 @@ LOCA_DEV void frag_f32_split(const float* stage, int c0, int lane, bf16x8_t& fh,
   fh = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
   fm = __builtin_bit_cast(bf16x8_t, make_uint4(m[0], m[1], m[2], m[3]));
   fl = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+}
+// the 8 fp32 operand values of lane `lane` (as for frag_f32_split), split into two fp16
+// MFMA operands of 2^8 times their value
+LOCA_DEV void frag_f32_split2h(const float* stage, int c0, int lane, f16x8_t& fh, f16x8_t& fl) {
+  const int hw = lane >> 5, cc = c0 + (lane & 31);
+  const float* p = stage + 8 * hw * 256 + 4 * ((cc >> 2) ^ (8 * hw)) + (cc & 3);
+  float v[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = p[e * 256];
+  uint32_t h[4], l[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) split2h_pair(v[2 * e], v[2 * e + 1], h[e], l[e]);
+  fh = __builtin_bit_cast(f16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+  fl = __builtin_bit_cast(f16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
 }
 __global__ __launch_bounds__(512) void k_syrk_f32_dl(int64_t d, int64_t k0, int64_t kw, int64_t off,
                                                      float* __restrict__ Fall, int ntile) {
@@ -1024,24 +1059,21 @@ __global__ __launch_bounds__(512) void k_syrk_f32_dl(int64_t d, int64_t k0, int6
   auto step = [&](float* cur, float* fill, int kt) {
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * NCP));  // stage kt landed (this thread's copies)
     barrier_nofence();                               // ... everyone's; slot `fill` no longer read
-    bf16x8_t bh[NBN], bm[NBN], bl[NBN];
+    f16x8_t bh[NBN], bl[NBN];
 #pragma unroll
-    for (int b = 0; b < NBN; ++b) frag_f32_split(cur + bpanel, wj * WN + 32 * b, lane, bh[b], bm[b], bl[b]);
+    for (int b = 0; b < NBN; ++b) frag_f32_split2h(cur + bpanel, wj * WN + 32 * b, lane, bh[b], bl[b]);
 #pragma unroll
     for (int a = 0; a < NBM; ++a) {
       __builtin_amdgcn_sched_barrier(0);
       issue(fill, kt + 3, a);
       __builtin_amdgcn_sched_barrier(0);
-      bf16x8_t ah, am, al;
-      frag_f32_split(cur, wi * WM + 32 * a, lane, ah, am, al);
+      f16x8_t ah, al;
+      frag_f32_split2h(cur, wi * WM + 32 * a, lane, ah, al);
 #pragma unroll
       for (int b = 0; b < NBN; ++b) {
-        acc[a][b] = mfma32(al, bh[b], acc[a][b]);
-        acc[a][b] = mfma32(ah, bl[b], acc[a][b]);
-        acc[a][b] = mfma32(am, bm[b], acc[a][b]);
-        acc[a][b] = mfma32(am, bh[b], acc[a][b]);
-        acc[a][b] = mfma32(ah, bm[b], acc[a][b]);
-        acc[a][b] = mfma32(ah, bh[b], acc[a][b]);
+        acc[a][b] = mfma32h(al, bh[b], acc[a][b]);
+        acc[a][b] = mfma32h(ah, bl[b], acc[a][b]);
+        acc[a][b] = mfma32h(ah, bh[b], acc[a][b]);
       }
     }
   };
@@ -1074,7 +1106,7 @@ __global__ __launch_bounds__(512) void k_syrk_f32_dl(int64_t d, int64_t k0, int6
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int64_t row = rb + mfma32_row(lane, r);
-        if (row < d && col < d && col >= row) F[row * d + col] = old[r] - acc[a][b][r];
+        if (row < d && col < d && col >= row) F[row * d + col] = old[r] - acc[a][b][r] * (1.0f / 65536.0f);
       }
     }
 }
