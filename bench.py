@@ -34,10 +34,10 @@ HBM_PEAK_GBS = 8000.0
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
 # kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 2844570.9, "write_kib": 777729.5, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "dced4c501bdce7f0"},
-    "c5": {"fetch_kib": 19734767.8, "write_kib": 2655246.3, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "dced4c501bdce7f0"},
+    "c3": {"fetch_kib": 2976083.7, "write_kib": 795925.1, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "2c72dad5c5db20bd"},
+    "c5": {"fetch_kib": 19014815.1, "write_kib": 2667088.3, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "2c72dad5c5db20bd"},
 }
 
 

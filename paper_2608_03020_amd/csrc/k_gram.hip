@@ -292,7 +292,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
                                                                 const uint16_t* __restrict__ zero16, int64_t b0,
                                                                 const uint16_t* __restrict__ Yhl_all, int64_t w2,
                                                                 int64_t w2p, float* __restrict__ Kraw_all,
-                                                                const float* __restrict__ wpad, int ncross) {
+                                                                const float* __restrict__ wpad, int ncross, int per) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -311,7 +311,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
 
   const int T = (int)((d + BM - 1) / BM);
   const int ntile = T * (T + 1) / 2, ntot = ntile + ncross;
-  const int logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  // Tile order.  per == 0: the XCD-aware order over all blocks of the launch (each XCD runs
+  // its own run of blocks).  per > 0: every block is cut into eight runs of per tiles, XCD
+  // x taking run x of each block in turn (the slots past the block's tiles exit), so that
+  // the XCDs work on the same block at the same time and its X is read from HBM about
+  // once, then shared through the last-level cache; taken when a run still fills most of
+  // an XCD's 32 compute units.
+  int logical;
+  if (per > 0) {
+    const int L = (int)blockIdx.x, x = L & 7, i = L >> 3;
+    const int t = x * per + i % per;
+    if (t >= ntot) return;
+    logical = (i / per) * ntot + t;
+  } else {
+    logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
+  }
   const int tl = logical % ntot;
   const bool ctile = tl >= ntile;  // a cross tile: row panel tl - ntile against the split targets
   int I, J;
@@ -800,9 +814,13 @@ template <bool BUF, bool WT>
 static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_t nbc, const uint16_t* zero16,
                            double* diag_part, const uint16_t* Yhl, int64_t w2, int64_t w2p, float* Kraw,
                            const float* wpad, int ncross) {
-  k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)((ntile + ncross) * nbc)), 512, 0, a.stream>>>(
+  // block-synchronous order when a block holds at least 24 tiles per XCD
+  const int64_t ntot = ntile + ncross, run = (ntot + 7) / 8;
+  const int per = run >= 24 ? (int)run : 0;
+  const int64_t grid = per > 0 ? 8 * run * nbc : ntot * nbc;
+  k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)grid), 512, 0, a.stream>>>(
       a.n, a.d, (const uint16_t*)a.x, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, Yhl, w2,
-      w2p, Kraw, wpad, ncross);
+      w2p, Kraw, wpad, ncross, per);
 }
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {
