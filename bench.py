@@ -34,10 +34,10 @@ HBM_PEAK_GBS = 8000.0
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
 # kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 2976083.7, "write_kib": 795925.1, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "2c72dad5c5db20bd"},
-    "c5": {"fetch_kib": 19014815.1, "write_kib": 2667088.3, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "2c72dad5c5db20bd"},
+    "c3": {"fetch_kib": 3745463.5, "write_kib": 780014.2, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "97d82c4331e648ac"},
+    "c5": {"fetch_kib": 19890750.5, "write_kib": 2663642.7, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "97d82c4331e648ac"},
 }
 
 

@@ -292,7 +292,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
                                                                 const uint16_t* __restrict__ zero16, int64_t b0,
                                                                 const uint16_t* __restrict__ Yhl_all, int64_t w2,
                                                                 int64_t w2p, float* __restrict__ Kraw_all,
-                                                                const float* __restrict__ wpad, int ncross, int per) {
+                                                                const float* __restrict__ wpad, int ncross, int per,
+                                                                int gx, int nblk) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -312,17 +313,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   const int T = (int)((d + BM - 1) / BM);
   const int ntile = T * (T + 1) / 2, ntot = ntile + ncross;
   // Tile order.  per == 0: the XCD-aware order over all blocks of the launch (each XCD runs
-  // its own run of blocks).  per > 0: every block is cut into eight runs of per tiles, XCD
-  // x taking run x of each block in turn (the slots past the block's tiles exit), so that
-  // the XCDs work on the same block at the same time and its X is read from HBM about
-  // once, then shared through the last-level cache; taken when a run still fills most of
-  // an XCD's 32 compute units.
+  // its own run of blocks).  per > 0: the XCDs form 8 / gx groups of gx, each block is cut
+  // into gx runs of per tiles, and XCD x takes run x % gx of every (8 / gx)-th block, from
+  // block x / gx on (the slots past a block's tiles, or past the last block, exit): the XCDs
+  // of a group work on the same block at the same time, so that the blocks in flight, 8 / gx
+  // of them, keep their X in the last-level cache and read it from HBM about once; taken
+  // when a run still fills most of an XCD's 32 compute units.
   int logical;
   if (per > 0) {
     const int L = (int)blockIdx.x, x = L & 7, i = L >> 3;
-    const int t = x * per + i % per;
-    if (t >= ntot) return;
-    logical = (i / per) * ntot + t;
+    const int t = (x % gx) * per + i % per;
+    const int blk = (i / per) * (8 / gx) + x / gx;
+    if (t >= ntot || blk >= nblk) return;
+    logical = blk * ntot + t;
   } else {
     logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
   }
@@ -814,13 +817,18 @@ template <bool BUF, bool WT>
 static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_t nbc, const uint16_t* zero16,
                            double* diag_part, const uint16_t* Yhl, int64_t w2, int64_t w2p, float* Kraw,
                            const float* wpad, int ncross) {
-  // block-synchronous order when a block holds at least 24 tiles per XCD
-  const int64_t ntot = ntile + ncross, run = (ntot + 7) / 8;
-  const int per = run >= 24 ? (int)run : 0;
-  const int64_t grid = per > 0 ? 8 * run * nbc : ntot * nbc;
+  // block-synchronous order with the widest XCD group (8, 4 or 2) whose runs hold at least
+  // 24 tiles, if there are blocks enough for every group; else the XCD-aware order
+  const int64_t ntot = ntile + ncross;
+  int gx = 0;
+  for (int g = 8; g >= 2 && gx == 0; g /= 2)
+    if ((ntot + g - 1) / g >= 24 && nbc >= 8 / g) gx = g;
+  const int64_t run = gx > 0 ? (ntot + gx - 1) / gx : 0;
+  const int64_t rounds = gx > 0 ? (nbc + 8 / gx - 1) / (8 / gx) : 0;
+  const int64_t grid = gx > 0 ? 8 * run * rounds : ntot * nbc;
   k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)grid), 512, 0, a.stream>>>(
       a.n, a.d, (const uint16_t*)a.x, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, Yhl, w2,
-      w2p, Kraw, wpad, ncross, per);
+      w2p, Kraw, wpad, ncross, (int)run, gx > 0 ? gx : 8, (int)nbc);
 }
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {

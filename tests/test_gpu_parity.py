@@ -76,8 +76,11 @@ CASES = {
     # two micro-batches; 128 right-hand sides in the solve and the large truncation core
     "bf16_d1288_k128": gen.custom_config("t16", blocks=2, d=1288, n=2700, micro=1500, C=6, k=128, r_a=16),
     # 19 x 19 tile rows plus 19 cross tiles per block (at least 24 tiles per XCD): the Gram launch
-    # in its block-synchronous order, two micro-batches
+    # in its block-synchronous order over all eight XCDs, two micro-batches
     "bf16_d4864_k64_sync": gen.custom_config("t18", blocks=1, d=4864, n=5200, micro=2600, C=5, k=64, r_a=8),
+    # 13 x 13 tile rows plus 13 cross tiles per block and two blocks: XCD groups of four, one
+    # block per group
+    "bf16_d3328_k64_groups": gen.custom_config("t19", blocks=2, d=3328, n=3500, C=4, k=64, r_a=8),
     # fp32 mode with fewer tokens than features (null space amplified by 1/lambda)
     "fp32_n150_d200": gen.custom_config("t3", blocks=2, d=200, n=150, C=2, k=8, r_a=8, mode="fp32",
                                         x_dist="gauss_outlier", n_outlier=3, outlier_scale=20.0, logit_std=2.0),
