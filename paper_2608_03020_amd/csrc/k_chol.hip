@@ -441,11 +441,15 @@ LOCA_DEV void zero16(f32x16_t& acc) {
 // One wave factors the 32 x 32 block B (upper part used) as U^T U, writes U over B (zero
 // below the diagonal) and X = U^{-1} to Xo.  Lane c < 32 holds column c (rows 0..31);
 // lanes 32..63 mirror lanes 0..31 and write nothing.  Step j of the factorization takes
-// the pivot from lane j and the scaled row j, U[j][i], from lanes i by cross-lane reads
-// (v_readlane into scalar registers), so no step waits on LDS; the inverse is built
-// bottom-up the same way, U[i][k] being lane k's entry of row i.  Square root and
-// reciprocal are the hardware ones (about 1 ulp).  The first non-positive pivot among the
-// first `valid` is reported (1-based, offset base).
+// the pivot from lane j (v_readlane; lane j forms it in step j - 1 from its own values,
+// so that the pivot does not wait for the row's round trip through LDS) and writes row j of
+// U, U[j][c] from lane c, straight to its place in B; the update A[i][c] -= U[j][i] U[j][c]
+// then reads that row back from LDS (one broadcast read per entry instead of a cross-lane
+// read each).  The inverse is
+// built bottom-up the same way, lane c finishing column c of X with row i of U read from
+// B.  A wave's LDS accesses complete in order, so each read sees the row just written.
+// 1/sqrt of the pivot and the reciprocals are the hardware ones (about 1 ulp).  The first
+// non-positive pivot among the first `valid` is reported (1-based, offset base).
 LOCA_DEV float lane_val(float v, int l) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
 }
@@ -455,29 +459,31 @@ LOCA_DEV void chol_inv32(float* B, int ld, float* Xo, int ldx, int lane, int val
   float a[32];
 #pragma unroll
   for (int r = 0; r < 32; ++r) a[r] = B[r * ld + c];
+  float piv = lane_val(a[0], 0);
+  int bad = 32;  // the first non-positive pivot (wave-uniform), reported after the loop
 #pragma unroll
   for (int j = 0; j < 32; ++j) {
-    const float piv = lane_val(a[j], j);
-    if (!(piv > 0.f) && j < valid && lane == 0) atomicCAS(info, 0, (int32_t)(base + j + 1));
-    const float ujj = __builtin_amdgcn_sqrtf(piv);
-    const float inv = __builtin_amdgcn_rcpf(ujj);
+    if (!(piv > 0.f) && j < valid && bad == 32) bad = j;
+    const float inv = __builtin_amdgcn_rsqf(piv);
+    const float ujj = piv * inv;
     const float uc = c > j ? a[j] * inv : (c == j ? ujj : 0.f);  // U[j][c]
     a[j] = uc;
+    // the next pivot from lane j + 1's own values (U[j][j + 1] is its uc), ahead of the
+    // row's round trip through LDS; the same fused operation as its update below
+    if (j < 31) piv = lane_val(fmaf(-uc, uc, a[j + 1]), j + 1);
+    if (wr) B[j * ld + c] = uc;
 #pragma unroll
-    for (int i = j + 1; i < 32; ++i) a[i] -= lane_val(uc, i) * uc;  // A[i][c] -= U[j][i] U[j][c]
+    for (int i = j + 1; i < 32; ++i) a[i] = fmaf(-B[j * ld + i], uc, a[i]);  // A[i][c] -= U[j][i] U[j][c]
   }
-  if (wr) {
-#pragma unroll
-    for (int r = 0; r < 32; ++r) B[r * ld + c] = r <= c ? a[r] : 0.f;
-  }
+  if (bad < 32 && lane == 0) atomicCAS(info, 0, (int32_t)(base + bad + 1));
   float x[32];
 #pragma unroll
   for (int i = 31; i >= 0; --i) {
     float part[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int k = i + 1; k < 32; ++k) part[k & 3] += lane_val(a[i], k) * x[k];  // U[i][k] x[k]
+    for (int k = i + 1; k < 32; ++k) part[k & 3] += B[i * ld + k] * x[k];  // U[i][k] x[k]
     const float tot = (part[0] + part[1]) + (part[2] + part[3]);
-    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - tot) * __builtin_amdgcn_rcpf(lane_val(a[i], i)) : 0.f;
+    x[i] = c >= i ? ((c == i ? 1.f : 0.f) - tot) * __builtin_amdgcn_rcpf(B[i * ld + i]) : 0.f;
   }
   if (wr) {
 #pragma unroll
