@@ -567,9 +567,15 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
   return red[kRedEig] == 0.0;
 }
 
-// The truncation core for 64 < kp <= 128 (see the file comment).  Per matrix the workspace
-// `big` holds Gm and T = Gm Vb (n x n fp64 each, n = kp rounded up to even) and a float copy
-// of Vb: big + mi * 2 kMaxKpBig^2 doubles, then after nm such pairs the float copies.
+// The truncation core for 64 < kp <= 128 (see the file comment).  As the core for kp <= 64:
+// Gb = R R^T = U^T U by Cholesky when every pivot exceeds 1e-10 of the largest diagonal
+// entry (then W = (M L)(L^{-1} R) with L = U^T, one eigensolve of P^T P = L^T Gm L, and
+// Ca[a][c] = (L Vp)[c][a] / s_a, Cb[c][a] = (L^{-T} Vp)[c][a] s_a), otherwise the
+// eigendecomposition of Gb by Jacobi and H as in the file comment.  The packed symmetric
+// matrix of the eigensolve lives in LDS, the eigenvectors in LDS as floats (rotations in
+// fp64).  Per matrix the workspace `big` holds two n x n fp64 matrices (n = kp rounded up to
+// even): Gm (then Gm L, then L^{-T} Vp) and L (or T = Gm Vb), from big + mi * 2 kMaxKpBig^2
+// doubles, then after nm such pairs a float copy of Vb per matrix.
 __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, int64_t r_a,
                                                         const double* __restrict__ Gpart, int nsplit,
                                                         double* __restrict__ big, double* __restrict__ Ca_all,
@@ -577,7 +583,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
                                                         int64_t sigma_bstride) {
   constexpr int KB2 = kMaxKpBig * kMaxKpBig;
   __shared__ double sA[kMaxKpBig * (kMaxKpBig + 1) / 2];
-  __shared__ float sV[KB2];
+  __shared__ __attribute__((aligned(16))) float sV[KB2];  // also eight rows of Gm (doubles) as scratch
   __shared__ double sH[kMaxKpBig], sHi[kMaxKpBig], sEig[kMaxKpBig];
   __shared__ int sOrd[kMaxKpBig];
   __shared__ __attribute__((aligned(16))) double cs[kMaxKpBig];
@@ -606,38 +612,129 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   }
   __threadfence();
   __syncthreads();
-  jacobi_packed(sA, sV, n, cs, pairs, red);
-  __syncthreads();
-  if (tid == 0) {
-    double lmax = 0.0;
-    for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
-    red[kRedMax] = lmax;
+  // 2. Gb = U^T U in place in sA (packed upper triangle), one barrier per row: step j updates
+  // the trailing rows from the unscaled row j, A[i][k] -= A[j][i] A[j][k] / A[j][j]
+  // (thread (ty, tx) of a 32 x 32 grid takes i in {ty + 32 a}, k in {tx + 32 b}), while row
+  // j - 1, no longer read, is scaled into U; a pivot at or below 1e-10 of the largest
+  // diagonal entry sends the core to the eigendecomposition of Gb instead (R close to rank
+  // deficient), as in the core for kp <= 64
+  bool chol = true;
+  {
+    const int ty = tid >> 5, tx = tid & 31;
+    double mx = 0.0;
+    for (int j = 0; j < K; ++j) mx = fmax(mx, sA[pk(j, j, n)]);
+    const double thr = 1e-10 * mx;
+    for (int j = 0; j < K; ++j) {
+      const double piv = sA[pk(j, j, n)];
+      if (j > 0) {
+        const double inv = rsq64(sA[pk(j - 1, j - 1, n)]);
+        for (int k = j + tid; k < K; k += kTC) sA[pk(j - 1, k, n)] *= inv;
+      }
+      if (!(piv > thr)) {  // uniform: every thread reads the same pivot
+        chol = false;
+        break;
+      }
+      const double rp = rcp64(piv);
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const int i = ty + 32 * a;
+        if (i <= j || i >= K) continue;
+        const double aji = sA[pk(j, i, n)] * rp;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int k = tx + 32 * b;
+          if (k < i || k >= K) continue;
+          sA[pk(i, k, n)] -= aji * sA[pk(j, k, n)];
+        }
+      }
+      __syncthreads();
+    }
+    if (chol)
+      for (int i = tid; i < K; i += kTC) sA[pk(i, i, n)] = sqrt(sA[pk(i, i, n)]);
   }
   __syncthreads();
-  for (int j = tid; j < n; j += kTC) {
-    const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
-    const bool keep = lb > 1e-14 * red[kRedMax] && lb > 0.0;
-    sH[j] = keep ? sqrt(lb) : 0.0;
-    sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+  if (chol) {
+    // 3. L = U^T (dense, lower) into T; T2 = Gm L over Gm, eight rows of Gm at a time
+    // through LDS; P^T P = L^T T2 (upper triangle, packed) into sA
+    for (int e = tid; e < n * n; e += kTC) {
+      const int x = e / n, j = e % n;
+      T[e] = (j <= x && x < K) ? sA[pk(j, x, n)] : 0.0;
+    }
+    __threadfence();
+    __syncthreads();
+    double* scr = reinterpret_cast<double*>(sV);
+    for (int x0 = 0; x0 < K; x0 += 8) {
+      for (int e = tid; e < 8 * n; e += kTC) {
+        const int r = e / n, y = e % n;
+        scr[e] = x0 + r < K ? Gm[(x0 + r) * n + y] : 0.0;
+      }
+      __syncthreads();
+      {
+        const int r = tid >> 7, j = tid & 127;
+        if (x0 + r < K && j < K) {
+          double sum = 0.0;
+          for (int y = j; y < K; ++y) sum += scr[r * n + y] * T[y * n + j];
+          Gm[(x0 + r) * n + j] = sum;
+        }
+      }
+      __syncthreads();
+    }
+    __threadfence();
+    __syncthreads();
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (i > j) continue;
+      double sum = 0.0;
+      if (j < K)
+        for (int x = i; x < K; ++x) sum += T[x * n + i] * Gm[x * n + j];
+      sA[pk(i, j, n)] = sum;
+    }
+    __syncthreads();
+  } else {
+    // 2'. Gb again, then Gb = Vb diag(lb) Vb^T by Jacobi; H = Vb diag(sqrt(lb)) over the kept
+    // directions
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (i > j) continue;
+      double gb = 0.0;
+      if (j < K)
+        for (int z = 0; z < nsplit; ++z) gb += GbP[z * kp * kp + i * kp + j];
+      sA[pk(i, j, n)] = gb;
+    }
+    __syncthreads();
+    jacobi_packed(sA, sV, n, cs, pairs, red);
+    __syncthreads();
+    if (tid == 0) {
+      double lmax = 0.0;
+      for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
+      red[kRedMax] = lmax;
+    }
+    __syncthreads();
+    for (int j = tid; j < n; j += kTC) {
+      const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
+      const bool keep = lb > 1e-14 * red[kRedMax] && lb > 0.0;
+      sH[j] = keep ? sqrt(lb) : 0.0;
+      sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+    }
+    // keep Vb; T = Gm Vb; P^T P = H Vb^T T H into sA
+    for (int e = tid; e < n * n; e += kTC) Vs[e] = sV[e];
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      double s = 0.0;
+      for (int c = 0; c < n; ++c) s += Gm[i * n + c] * (double)sV[c * n + j];
+      T[i * n + j] = s;
+    }
+    __threadfence();
+    __syncthreads();
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      if (i > j) continue;
+      double s = 0.0;
+      for (int c = 0; c < n; ++c) s += (double)sV[c * n + i] * T[c * n + j];
+      sA[pk(i, j, n)] = s * sH[i] * sH[j];
+    }
+    __syncthreads();
   }
-  // 2. keep Vb; T = Gm Vb; P = H Vb^T T H into sA
-  for (int e = tid; e < n * n; e += kTC) Vs[e] = sV[e];
-  for (int e = tid; e < n * n; e += kTC) {
-    const int i = e / n, j = e % n;
-    double s = 0.0;
-    for (int c = 0; c < n; ++c) s += Gm[i * n + c] * (double)sV[c * n + j];
-    T[i * n + j] = s;
-  }
-  __threadfence();
-  __syncthreads();
-  for (int e = tid; e < n * n; e += kTC) {
-    const int i = e / n, j = e % n;
-    if (i > j) continue;
-    double s = 0.0;
-    for (int c = 0; c < n; ++c) s += (double)sV[c * n + i] * T[c * n + j];
-    sA[pk(i, j, n)] = s * sH[i] * sH[j];
-  }
-  __syncthreads();
   jacobi_packed(sA, sV, n, cs, pairs, red);  // sV = Vp
   __syncthreads();
   if (tid == 0) {
@@ -655,15 +752,48 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
+  if (chol) {  // Z = L^{-T} Vp for the kept columns (over Gm): 16 lanes per column,
+               // entries x = t + 16 q of the column in registers, the substitution upwards
+    const int a = tid >> 4, t = tid & 15;
+    if (a < (int)r_a) {
+      const int col = sOrd[a];
+      double zq[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+      for (int c = K - 1; c >= 0; --c) {
+        double sum = 0.0;
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int x = t + 16 * q;
+          if (x > c && x < K) sum += T[x * n + c] * zq[q];
+        }
+        sum = seg16_sum(sum);
+        const double zc = ((double)sV[c * n + col] - sum) / T[c * n + c];
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (c == t + 16 * q) zq[q] = zc;
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int x = t + 16 * q;
+        if (x < K) Gm[x * n + col] = zq[q];
+      }
+    }
+    __threadfence();
+    __syncthreads();
+  }
   for (int e = tid; e < (int)(r_a * kp); e += kTC) {
-    const int a = e / K, c = e % K;
+    const int a = e % (int)r_a, c = e / (int)r_a;  // lanes along a
     const int col = sOrd[a];
     const double sa = sqrt(fmax(sEig[col], 0.0));
     double u = 0.0, v = 0.0;
-    for (int x = 0; x < n; ++x) {
-      const double vb = (double)Vs[c * n + x], vp = (double)sV[x * n + col];
-      u += vb * sH[x] * vp;
-      v += vb * sHi[x] * vp;
+    if (chol) {  // Ca from L Vp, Cb from Z
+      for (int x = 0; x <= c; ++x) u += T[c * n + x] * (double)sV[x * n + col];
+      v = Gm[c * n + col];
+    } else {
+      for (int x = 0; x < n; ++x) {
+        const double vb = (double)Vs[c * n + x], vp = (double)sV[x * n + col];
+        u += vb * sH[x] * vp;
+        v += vb * sHi[x] * vp;
+      }
     }
     const bool live = sa > 1e-30 * s1 && sa > 0.0;
     Ca[a * kp + c] = live ? u / sa : 0.0;
