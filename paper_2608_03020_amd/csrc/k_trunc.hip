@@ -265,6 +265,13 @@ LOCA_DEV double seg16_sum(double v) {
   v += dpp_d<0x128>(v);  // row_ror:8
   return v;
 }
+// Sum over aligned groups of 8 lanes (quad xor 1 and 2, then the half-row mirror).
+LOCA_DEV double seg8_sum(double v) {
+  v += dpp_d<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_d<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_d<0x141>(v);  // row_half_mirror
+  return v;
+}
 LOCA_DEV double readlane_d(double v, int l) {
   const long long b = __double_as_longlong(v);
   const int lo = __builtin_amdgcn_readlane((int)b, l);
@@ -311,13 +318,20 @@ constexpr int kRedEig = 43;  // reduction-scratch slot: a check of eig_top faile
 // eig[j] is the j-th largest eigenvalue (j < K) and column j of V (row-major, stride n) its
 // unit eigenvector for j < r; the other entries of V are zero.  Z: r x K doubles of scratch;
 // dT, eT, e2, tauH, pbuf: 64 doubles each.  Run by the kTC threads of one workgroup.
-LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z, double* dT, double* eT,
-                      double* e2, double* tauH, double* pbuf, double* eig, double* red) {
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
-  for (int e = tid; e < n * n; e += kTC) {
-    const int i = e / n, j = e % n;
-    V[e] = (i < K && j < K) ? A[pk(i, j, n)] : 0.0;
-  }
+template <int KM, bool PACKED, typename OutT>
+LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vout, double* Z, double* dT,
+                      double* eT, double* e2, double* tauH, double* pbuf, double* eig, double* red) {
+  static_assert(KM == 64 || KM == 128, "workgroup maps for K <= 64 or K <= 128");
+  constexpr int LPR = kTC / KM;  // lanes per row of p, and per eigenvalue in the multisection
+  constexpr int NX = KM / 64, NP = KM / LPR, NU = KM / 32, NZ = KM / 16;
+  const int tid = threadIdx.x, lane = tid & 63;
+  auto at = [&](int i, int j) -> double& { return PACKED ? W[pk(i, j, n)] : W[i * n + j]; };
+  auto segsum = [&](double v) { return LPR == 16 ? seg16_sum(v) : seg8_sum(v); };
+  if (!PACKED)
+    for (int e = tid; e < n * n; e += kTC) {
+      const int i = e / n, j = e % n;
+      W[e] = (i < K && j < K) ? A[pk(i, j, n)] : 0.0;
+    }
   if (tid == 0) red[kRedEig] = 0.0;
   __syncthreads();
   // 1. reduction to tridiagonal form
@@ -327,9 +341,16 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
       const int m = K - k - 1;  // entries right of the diagonal in row k
       // the reflector of row k, formed by every wave alike (row k is final since the
       // last barrier); row k keeps x until the step's end, v_0 is kept apart
-      const double x = lane < m ? V[k * n + k + 1 + lane] : 0.0;
-      const double ss = wave_sum_all(x * x);
-      const double x0 = V[k * n + k + 1];
+      double xs[NX];
+      double sq = 0.0;
+#pragma unroll
+      for (int u = 0; u < NX; ++u) {
+        const int c = lane + 64 * u;
+        xs[u] = c < m ? at(k, k + 1 + c) : 0.0;
+        sq += xs[u] * xs[u];
+      }
+      const double ss = wave_sum_all(sq);
+      const double x0 = at(k, k + 1);
       double tau = 0.0, alpha = x0, v0 = x0;
       if (ss > 0.0) {
         const double nx = ss > 1e-280 ? ss * rsq64(ss) : sqrt(ss);  // ||x||
@@ -340,51 +361,56 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
       if (tid == 0) {
         tauH[k] = tau;
         eT[k] = alpha;
-        dT[k] = V[k * n + k];
+        dT[k] = at(k, k);
       }
       if (tau != 0.0) {  // uniform: every wave has the same ss
-        {  // p_i = tau sum_c A[k+1+i][k+1+c] v_c, 16 lanes per row i
-          const int row = tid >> 4, part = tid & 15;
+        {  // p_i = tau sum_c A[k+1+i][k+1+c] v_c, LPR lanes per row i
+          const int row = tid / LPR, part = tid % LPR;
           double acc = 0.0;
           if (row < m)
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
-              const int c = part + 16 * u;
-              if (c < m) acc += V[(k + 1 + row) * n + k + 1 + c] * (c == 0 ? v0 : V[k * n + k + 1 + c]);
+            for (int u = 0; u < NP; ++u) {
+              const int c = part + LPR * u;
+              if (c < m) acc += at(k + 1 + row, k + 1 + c) * (c == 0 ? v0 : at(k, k + 1 + c));
             }
-          acc = seg16_sum(acc);
+          acc = segsum(acc);
           if (row < m && part == 0) pbuf[row] = tau * acc;
         }
         __syncthreads();
-        const double vl = lane == 0 ? v0 : x;
-        const double kk = 0.5 * tau * wave_sum_all(lane < m ? pbuf[lane] * vl : 0.0);
-        // A[k+1+i][k+1+c] -= v_i w_c + w_i v_c, w = p - kk v; thread (ty, tx) takes
-        // i in {ty, ty + 32}, c in {tx, tx + 32}
+        double pv = 0.0;
 #pragma unroll
-        for (int a = 0; a < 2; ++a) {
+        for (int u = 0; u < NX; ++u) {
+          const int c = lane + 64 * u;
+          if (c < m) pv += pbuf[c] * (c == 0 ? v0 : xs[u]);
+        }
+        const double kk = 0.5 * tau * wave_sum_all(pv);
+        // A[k+1+i][k+1+c] -= v_i w_c + w_i v_c, w = p - kk v (upper triangle only when
+        // packed); thread (ty, tx) takes i in {ty + 32 a}, c in {tx + 32 b}
+#pragma unroll
+        for (int a = 0; a < NU; ++a) {
           const int i = ty + 32 * a;
           if (i >= m) continue;
-          const double vi = i == 0 ? v0 : V[k * n + k + 1 + i];
+          const double vi = i == 0 ? v0 : at(k, k + 1 + i);
           const double wi = pbuf[i] - kk * vi;
 #pragma unroll
-          for (int b = 0; b < 2; ++b) {
+          for (int b = 0; b < NU; ++b) {
             const int c = tx + 32 * b;
-            if (c >= m) continue;
-            const double vc = c == 0 ? v0 : V[k * n + k + 1 + c];
+            if (c >= m || (PACKED && c < i)) continue;
+            const double vc = c == 0 ? v0 : at(k, k + 1 + c);
             const double wc = pbuf[c] - kk * vc;
-            V[(k + 1 + i) * n + k + 1 + c] -= vi * wc + wi * vc;
+            at(k + 1 + i, k + 1 + c) -= vi * wc + wi * vc;
           }
         }
       }
       __syncthreads();
-      if (tid == 0) V[k * n + k + 1] = v0;  // the reflector complete in row k (read only later)
+      if (tid == 0) at(k, k + 1) = v0;  // the reflector complete in row k (read only later)
     }
     if (tid == 0) {
       if (K >= 2) {
-        dT[K - 2] = V[(K - 2) * n + K - 2];
-        eT[K - 2] = V[(K - 2) * n + K - 1];
+        dT[K - 2] = at(K - 2, K - 2);
+        eT[K - 2] = at(K - 2, K - 1);
       }
-      dT[K - 1] = V[(K - 1) * n + K - 1];
+      dT[K - 1] = at(K - 1, K - 1);
     }
   }
   __syncthreads();
@@ -413,16 +439,18 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
     }
     if (K - below < r) return false;
   }
-  // 2. multisection: group g = tid / 16 finds the g-th smallest eigenvalue, lane t of the
-  // group testing point t + 1 of 16 equal steps (the last one is hi); 13 steps (52 bits)
-  // for the r largest, whose vectors follow, 10 (40 bits) for the others
+  // 2. multisection: group g = tid / LPR finds the g-th smallest eigenvalue, lane t of the
+  // group testing point t + 1 of LPR equal steps (the last one is hi); for the r largest,
+  // whose vectors follow, 52 bits or more of the interval (13 steps of 16, 18 of 8), for
+  // the others 40 or more (10 of 16, 14 of 8)
   {
-    const int g = tid >> 4, t = tid & 15;
+    constexpr int STEPS_V = LPR == 16 ? 13 : 18, STEPS_S = LPR == 16 ? 10 : 14;
+    const int g = tid / LPR, t = tid % LPR;
     const int j = g < K ? g : K - 1;
-    const int steps = K - 1 - j < r ? 13 : 10;
+    const int steps = K - 1 - j < r ? STEPS_V : STEPS_S;
     double lo = glo, hi = ghi;
     for (int it = 0; it < steps; ++it) {
-      const double h = (hi - lo) * (1.0 / 16.0);
+      const double h = (hi - lo) * (1.0 / LPR);
       const double x = lo + (double)(t + 1) * h;
       double q = safe_pivot(dT[0] - x, pivmin);
       int cnt = q < 0.0;
@@ -430,20 +458,19 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
         q = safe_pivot((dT[i] - x) - e2[i - 1] * rcp64_1(q), pivmin);
         cnt += q < 0.0;
       }
-      if (t == 15) cnt = K;
+      if (t == LPR - 1) cnt = K;
       const unsigned long long b = __ballot(cnt > j);
-      const unsigned seg = (unsigned)(b >> (lane & 48)) & 0xFFFFu;  // lane 15 of the group always set
+      const unsigned seg = (unsigned)(b >> (lane & (64 - LPR))) & ((1u << LPR) - 1u);  // last lane set
       const int f = __builtin_ctz(seg);
       const double nlo = f == 0 ? lo : lo + (double)f * h;
-      hi = f == 15 ? hi : lo + (double)(f + 1) * h;
+      hi = f == LPR - 1 ? hi : lo + (double)(f + 1) * h;
       lo = nlo;
     }
     if (g < K && t == 0) eig[K - 1 - g] = 0.5 * (lo + hi);
   }
   __syncthreads();
   // eigenvalues among the r largest closer than 1e-10 of the largest |lambda| (a repeated
-  // value, or a numerically zero cluster when A has rank below r) cannot get orthogonal
-  // vectors from the twisted solves: Jacobi at once
+  // value) cannot get orthogonal vectors from the twisted solves: Jacobi at once
   {
     const double sc = fmax(fabs(eig[0]), fabs(eig[K - 1]));
     if (tid + 1 < r && !(eig[tid] - eig[tid + 1] > 1e-10 * sc)) red[kRedEig] = 1.0;
@@ -504,9 +531,9 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
   {
     const int a = tid >> 4, t = tid & 15;
     const bool act = a < r;
-    double zr[4];
+    double zr[NZ];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < NZ; ++q) {
       const int i = t + 16 * q;
       zr[q] = (act && i < K) ? Z[a * K + i] : 0.0;
     }
@@ -515,31 +542,32 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
       if (tau == 0.0) continue;
       double dot = 0.0;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < NZ; ++q) {
         const int i = t + 16 * q;
-        if (i > k && i < K) dot += V[k * n + i] * zr[q];
+        if (i > k && i < K) dot += at(k, i) * zr[q];
       }
       const double f = tau * seg16_sum(dot);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < NZ; ++q) {
         const int i = t + 16 * q;
-        if (i > k && i < K) zr[q] -= f * V[k * n + i];
+        if (i > k && i < K) zr[q] -= f * at(k, i);
       }
     }
-    __syncthreads();  // the reflectors are read by every group before V is overwritten
+    __syncthreads();  // the reflectors and Z are read by every group before Vout is written
     for (int e = tid; e < n * n; e += kTC) {
       const int i = e / n, j = e % n;
-      if (j >= r || i >= K) V[e] = 0.0;
+      if (j >= r || i >= K) Vout[e] = (OutT)0;
     }
     if (act)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
+      for (int q = 0; q < NZ; ++q) {
         const int i = t + 16 * q;
-        if (i < K) V[i * n + a] = zr[q];
+        if (i < K) Vout[i * n + a] = (OutT)zr[q];
       }
   }
   __syncthreads();
-  // the check
+  // the check (vectors as stored: a float copy is held to float accuracy)
+  constexpr double kRes = sizeof(OutT) == 8 ? 1e-11 : 1e-5, kOrth = sizeof(OutT) == 8 ? 1e-9 : 1e-5;
   const double anorm = fmax(fabs(eig[0]), fabs(eig[K - 1]));
   {
     const int a = tid >> 4, t = tid & 15;
@@ -547,21 +575,21 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
     if (a < r) {
       const double lam = eig[a];
       for (int i = t; i < K; i += 16) {
-        double s = -lam * V[i * n + a];
-        for (int c = 0; c < K; ++c) s += A[pk(i, c, n)] * V[c * n + a];
+        double s = -lam * (double)Vout[i * n + a];
+        for (int c = 0; c < K; ++c) s += A[pk(i, c, n)] * (double)Vout[c * n + a];
         rs += s * s;
       }
     }
     rs = seg16_sum(rs);
-    const double tol = 1e-11 * anorm;
+    const double tol = kRes * anorm;
     if (a < r && t == 0 && !(rs <= tol * tol)) red[kRedEig] = 1.0;
   }
   for (int e = tid; e < r * r; e += kTC) {
     const int a = e / r, b = e % r;
     if (a > b) continue;
     double s = 0.0;
-    for (int i = 0; i < K; ++i) s += V[i * n + a] * V[i * n + b];
-    if (!(fabs(s - (a == b ? 1.0 : 0.0)) <= 1e-9)) red[kRedEig] = 1.0;
+    for (int i = 0; i < K; ++i) s += (double)Vout[i * n + a] * (double)Vout[i * n + b];
+    if (!(fabs(s - (a == b ? 1.0 : 0.0)) <= kOrth)) red[kRedEig] = 1.0;
   }
   __syncthreads();
   return red[kRedEig] == 0.0;
@@ -572,8 +600,9 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* V, double* Z
 // entry (then W = (M L)(L^{-1} R) with L = U^T, one eigensolve of P^T P = L^T Gm L, and
 // Ca[a][c] = (L Vp)[c][a] / s_a, Cb[c][a] = (L^{-T} Vp)[c][a] s_a), otherwise the
 // eigendecomposition of Gb by Jacobi and H as in the file comment.  The packed symmetric
-// matrix of the eigensolve lives in LDS, the eigenvectors in LDS as floats (rotations in
-// fp64).  Per matrix the workspace `big` holds two n x n fp64 matrices (n = kp rounded up to
+// matrix of the eigensolve lives in LDS; its kept pairs come from the tridiagonal path
+// (eig_top, reduced in place, the vectors stored as floats), Jacobi taking over (the
+// eigenvectors in LDS as floats, rotations in fp64) when its check fails.  Per matrix the workspace `big` holds two n x n fp64 matrices (n = kp rounded up to
 // even): Gm (then Gm L, then L^{-T} Vp) and L (or T = Gm Vb), from big + mi * 2 kMaxKpBig^2
 // doubles, then after nm such pairs a float copy of Vb per matrix.
 __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, int64_t r_a,
@@ -585,6 +614,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   __shared__ double sA[kMaxKpBig * (kMaxKpBig + 1) / 2];
   __shared__ __attribute__((aligned(16))) float sV[KB2];  // also eight rows of Gm (doubles) as scratch
   __shared__ double sH[kMaxKpBig], sHi[kMaxKpBig], sEig[kMaxKpBig];
+  __shared__ double sT[5][kMaxKpBig];  // the tridiagonal eigensolver's vectors
   __shared__ int sOrd[kMaxKpBig];
   __shared__ __attribute__((aligned(16))) double cs[kMaxKpBig];
   __shared__ __attribute__((aligned(16))) int pairs[kMaxKpBig];
@@ -735,15 +765,30 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
     }
     __syncthreads();
   }
-  jacobi_packed(sA, sV, n, cs, pairs, red);  // sV = Vp
+  // sV = Vp: the leading r_a eigenpairs from the tridiagonal path on sA in place (a copy of
+  // P^T P over Gm, no longer needed, for its check), or every pair by Jacobi when the check
+  // fails
+  const int np = n * (n + 1) / 2;
+  for (int e = tid; e < np; e += kTC) Gm[e] = sA[e];
+  __threadfence();
   __syncthreads();
-  if (tid == 0) {
-    for (int j = 0; j < K; ++j) { sEig[j] = sA[pk(j, j, n)]; sOrd[j] = j; }
-    for (int i = 1; i < K; ++i) {
-      const int key = sOrd[i];
-      int j = i - 1;
-      while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
-      sOrd[j + 1] = key;
+  const int ra = (int)(r_a < kp ? r_a : kp);
+  if (eig_top<kMaxKpBig, true, float>(Gm, n, K, ra, sA, sV, reinterpret_cast<double*>(sV), sT[0], sT[1], sT[2],
+                                      sT[3], sT[4], sEig, red)) {
+    for (int j = tid; j < K; j += kTC) sOrd[j] = j;
+  } else {
+    for (int e = tid; e < np; e += kTC) sA[e] = Gm[e];
+    __syncthreads();
+    jacobi_packed(sA, sV, n, cs, pairs, red);  // sV = Vp
+    __syncthreads();
+    if (tid == 0) {
+      for (int j = 0; j < K; ++j) { sEig[j] = sA[pk(j, j, n)]; sOrd[j] = j; }
+      for (int i = 1; i < K; ++i) {
+        const int key = sOrd[i];
+        int j = i - 1;
+        while (j >= 0 && sEig[sOrd[j]] < sEig[key]) { sOrd[j + 1] = sOrd[j]; --j; }
+        sOrd[j + 1] = key;
+      }
     }
   }
   __syncthreads();
@@ -1009,7 +1054,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   // sV = Vp: the leading r_a eigenpairs from the tridiagonal path, or every pair by Jacobi
   // when its check fails
   const int ra = (int)(r_a < kp ? r_a : kp);
-  if (eig_top(sA, n, K, ra, sV, sG, sT[0], sT[1], sT[2], sT[3], sT[4], sEig, red)) {
+  if (eig_top<kMaxKp, false, double>(sA, n, K, ra, sV, sV, sG, sT[0], sT[1], sT[2], sT[3], sT[4], sEig, red)) {
     for (int j = tid; j < K; j += kTC) sOrd[j] = j;
   } else {
     jacobi_packed<double>(sA, sV, n, cs, pairs, red);
