@@ -235,10 +235,11 @@ def test_ridge_solve_fp64_and_nonpd_pivot():
     assert info.item() == 71
 
 
-@pytest.mark.parametrize("kp,r", [(40, 12), (64, 30)])
+@pytest.mark.parametrize("kp,r", [(40, 12), (64, 30), (96, 40)])
 def test_truncation_rank_deficient_right_factor(kp, r):
-    """R with repeated rows (R R^T singular): the core takes the eigendecomposition of R R^T
-    instead of its Cholesky factor; W_r against the oracle's dense SVD."""
+    """R with repeated rows (R R^T singular): the core (for kp <= 64, and the one for
+    64 < kp <= 128) takes the eigendecomposition of R R^T instead of its Cholesky factor;
+    W_r against the oracle's dense SVD."""
     import torch
     import oracle
     from paper_2608_03020_amd import loca
@@ -297,25 +298,30 @@ def test_truncation_matches_explicit_svd(d, kp, r):
     np.testing.assert_allclose(A.T @ b[0].cpu().numpy().T, W[0].cpu().numpy(), atol=1e-4 * np.abs(Wr_o).max())
 
 
-@pytest.mark.parametrize("kp,r", [(64, 32), (32, 8)])
+@pytest.mark.parametrize("kp,r", [(64, 32), (32, 8), (96, 32)])
 def test_truncation_repeated_leading_values(kp, r):
     """Repeated singular values among the r kept (a triple and a pair): the eigenvectors of the
     repeated eigenvalues cannot be told apart by the tridiagonal solves, so the core's check
-    sends the eigensolve to Jacobi.  M and B~ from a Hadamard matrix / 8 (orthogonal and exact
-    in float), so that W = M B~ has exactly the chosen singular values; W_r against the
-    oracle's dense SVD (the kept subspace is unique: sigma_r > sigma_{r+1})."""
+    sends the eigensolve to Jacobi (both cores).  M and B~ from Hadamard matrices / 8
+    (orthogonal and exact in float; two blocks on disjoint rows past 64 columns), so that
+    W = M B~ has exactly the chosen singular values; W_r against the oracle's dense SVD (the
+    kept subspace is unique: sigma_r > sigma_{r+1})."""
     import torch
     import oracle
     from scipy.linalg import hadamard
     from paper_2608_03020_amd import loca
     d = 150
     log(f"case truncation_repeated: d={d} kp={kp} r_a={r}")
-    H = hadamard(64).astype(np.float64) / 8.0  # its first kp columns are orthonormal
+    H = hadamard(64).astype(np.float64) / 8.0  # orthogonal, exact in float
+    Q = np.zeros((128, kp))  # orthonormal columns: H's, then H's again on rows 64..127
+    Q[:64, :min(kp, 64)] = H[:, :min(kp, 64)]
+    if kp > 64:
+        Q[64:, 64:] = H[:, :kp - 64]
     sig = np.concatenate([[6.0, 6.0, 6.0, 5.0, 5.0], np.linspace(4.0, 0.5, kp - 5)])
     Mh = np.zeros((d, kp), dtype=np.float32)
-    Mh[:64] = (H[:, :kp] * sig).astype(np.float32)
+    Mh[:128] = (Q * sig).astype(np.float32)
     Rh = np.zeros((kp, d), dtype=np.float32)
-    Rh[:, 10:10 + 64] = H[:, :kp].T.astype(np.float32)
+    Rh[:, 10:10 + 128] = Q.T.astype(np.float32)
     Wd = Mh.astype(np.float64) @ Rh.astype(np.float64)
     Wr_o, s_o = oracle.truncate_dense(Wd, r)
     assert np.allclose(s_o[:kp], sig, rtol=1e-6) and np.ptp(s_o[:3]) < 1e-12 * s_o[0]
