@@ -253,7 +253,13 @@ loca_status loca_ridge_solve(loca_stream_t stream, int64_t nb, int64_t d, int64_
  *   b_out = V_{r_a} diag(s_{r_a}) (d x r_a),   so W_{r_a} = a_out^T b_out^T
  * and the adapter acts as h_l = h_bar_l + b_out a_out h_{l-1} (Eq. 1).
  * sigma_out : the kp largest singular values of W, decreasing.
- * Directions with zero singular value (W has rank < r_a) get zero rows/cols.
+ * Directions of numerically zero singular value (W of rank below r_a, its
+ * factors rounded to float: below 1e-6 of the largest singular value, or from
+ * the first of two within 1e-5 of it whose squares lie within 1e-10 of the
+ * largest square of each other, where the eigensolver cannot separate them;
+ * exact zeros on its Jacobi fallback) carry no weight: their b_out columns are
+ * zero and their a_out rows an orthonormal completion of the other rows (by
+ * Householder reconstruction), so a_out always has orthonormal rows.
  * w_dense_out : optional d x d W_{r_a} (float), stride w_bstride.
  * dev_info : nm int32, 0 (reserved for future conditions).
  * Limits: kp <= 128, r_a <= kp, r_a <= 64, kp <= d.

@@ -22,6 +22,7 @@ namespace {
 constexpr int kT = 256;
 constexpr int kMaxKp = 64;
 constexpr int kMaxKpBig = 128;
+constexpr int kMaxRank = 64;  // r_a
 
 // Partial Gm = M^T M and Gb = R R^T (fp64) over the row range of blockIdx.z (of nsplit
 // equal ranges of 32-row multiples); blockIdx.x = matrix, blockIdx.y = 0 (M) / 1 (R).
@@ -289,35 +290,41 @@ LOCA_DEV double wave_sum_all(double v) {
 // negative, and no quotient overflows).
 LOCA_DEV double safe_pivot(double q, double pivmin) { return fabs(q) < pivmin ? -pivmin : q; }
 
-constexpr int kRedEig = 43;  // reduction-scratch slot: a check of eig_top failed
+constexpr int kRedEig = 43;   // reduction-scratch slot: a check of eig_top failed
+constexpr int kRedLive = 44;  // ... the number of pairs eig_top returned
+constexpr int kRedCut = 45;   // ... the same as an int while it is lowered
 
-// All eigenvalues of the packed symmetric K x K matrix A (packed with stride n, K <= 64) and
+// All eigenvalues of the packed symmetric K x K matrix A (packed with stride n, K <= KM) and
 // the eigenvectors of its r largest, A left unchanged:
-//   1. Householder reduction T = Q^T A Q to tridiagonal form on a dense copy in V (the
-//      trailing matrix kept whole and symmetric), two barriers per step: every wave forms
-//      the reflector v of row k itself, p = tau A v with 16 lanes per row, then every wave
-//      w = p - (tau/2)(p^T v) v and the rank-2 update A -= v w^T + w v^T over a 32 x 32
-//      grid of threads; the reflector is stored in row k right of the diagonal;
-//   2. every eigenvalue of T by multisection of Sturm counts: 16 lanes per eigenvalue test
-//      the 15 interior points of 16 equal steps of its interval, 13 times for the r largest
-//      (the widened Gershgorin interval, at most 2.2 ||T||, shrunk 2^52 times: a few units
-//      of double rounding of ||T||, the accuracy of the Sturm counts themselves) and 10
-//      times for the others (2^40: their only use is the float sigma);
-//      the pivots' reciprocals from the hardware approximation and one Newton step;
+//   1. Householder reduction T = Q^T A Q to tridiagonal form on the working matrix W (a
+//      dense copy of A, or, PACKED, A's packed triangle in place), two barriers per step:
+//      every wave forms the reflector v of row k itself, p = tau A v with kTC / KM lanes per
+//      row, then every wave w = p - (tau/2)(p^T v) v and the rank-2 update
+//      A -= v w^T + w v^T over a 32 x 32 grid of threads; the reflector is stored in row k
+//      right of the diagonal;
+//   2. every eigenvalue of T by multisection of Sturm counts: L = kTC / KM lanes per
+//      eigenvalue test the L - 1 interior points of L equal steps of its interval; for the r
+//      largest until the widened Gershgorin interval (at most 2.2 ||T||) has shrunk 2^52
+//      times or more, a few units of double rounding of ||T||, the accuracy of the Sturm
+//      counts themselves; 2^40 for the others, whose only use is the float sigma; the
+//      pivots' reciprocals from the hardware approximation and one Newton step;
 //   3. the eigenvector of T for each of the r largest (one lane each) from the twisted
 //      factorization of T - lambda I: the pivots of the top-down and bottom-up LDL^T, the
 //      twist index where their combination is smallest, and one solve that starts there;
-//   4. x = Q z (the reflectors applied in reverse order; 16 lanes per vector).
-// The path is left (false returned, and the caller runs Jacobi on A) before the
-// eigenvalues when fewer than r of them exceed 1e-12 ||T|| (one Sturm count: A of rank
-// below r, whose numerical zeros among the r largest have no separable vectors), before
-// the vectors when two of the r largest lie within 1e-10 of the largest |lambda| (a
-// repeated value), and after them when the check fails: every residual ||A x - lambda x||
-// within 1e-11 of the largest |lambda| and every pair of the r vectors orthonormal within
-// 1e-9.  On success
-// eig[j] is the j-th largest eigenvalue (j < K) and column j of V (row-major, stride n) its
-// unit eigenvector for j < r; the other entries of V are zero.  Z: r x K doubles of scratch;
-// dT, eT, e2, tauH, pbuf: 64 doubles each.  Run by the kTC threads of one workgroup.
+//   4. x = Q z (the reflectors applied in reverse order; 16 lanes per vector), stored in
+//      column j < r of Vout (row-major, stride n, type OutT); the other entries are zero.
+// Only eigenvalues above 1e-12 ||T|| (one Sturm count) get vectors: r is lowered to their
+// number when A has rank below r (its numerical zeros among the r largest have no
+// separable vectors, and their directions carry no weight), and lowered again to j when
+// eigenvalues j and j + 1 (both among the r largest) lie within 1e-10 of the largest
+// |lambda| of each other and |lambda_j| does of zero (numerical zeros above that count, as
+// left by the rounding of float factors); the count is left in red[kRedLive].  The path is
+// left (false returned, and the caller runs Jacobi on A) before the vectors when two other
+// of the r largest lie that close (a repeated value), and after them when the check fails: every residual
+// ||A x - lambda x|| and every pair of the r vectors orthonormal within 1e-11 and 1e-9
+// (float vectors: 1e-5 and 1e-5).  On success eig[j] is the j-th largest eigenvalue
+// (j < K).  Z: r x K doubles of scratch (it may share Vout's memory); dT, eT, e2, tauH,
+// pbuf: KM doubles each.  Run by the kTC threads of one workgroup.
 template <int KM, bool PACKED, typename OutT>
 LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vout, double* Z, double* dT,
                       double* eT, double* e2, double* tauH, double* pbuf, double* eig, double* red) {
@@ -332,6 +339,7 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
       const int i = e / n, j = e % n;
       W[e] = (i < K && j < K) ? A[pk(i, j, n)] : 0.0;
     }
+  int* cut = reinterpret_cast<int*>(&red[kRedCut]);
   if (tid == 0) red[kRedEig] = 0.0;
   __syncthreads();
   // 1. reduction to tridiagonal form
@@ -428,8 +436,9 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
   glo -= 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
   ghi += 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
   __syncthreads();
-  {  // fewer than r eigenvalues above 1e-12 ||T||: the r largest hold a cluster of
-     // numerical zeros (A of rank below r), so Jacobi at once (every thread counts alike)
+  {  // only the eigenvalues above 1e-12 ||T|| get vectors: below it the r largest would hold
+     // a cluster of numerical zeros (A of rank below r), whose vectors the twisted solves
+     // cannot separate and whose directions carry no weight (every thread counts alike)
     const double x0 = 1e-12 * tnorm;
     double q = safe_pivot(dT[0] - x0, pivmin);
     int below = q < 0.0;
@@ -437,7 +446,8 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
       q = safe_pivot((dT[i] - x0) - e2[i - 1] * rcp64_1(q), pivmin);
       below += q < 0.0;
     }
-    if (K - below < r) return false;
+    if (K - below < r) r = K - below;
+    if (tid == 0) *cut = r;
   }
   // 2. multisection: group g = tid / LPR finds the g-th smallest eigenvalue, lane t of the
   // group testing point t + 1 of LPR equal steps (the last one is hi); for the r largest,
@@ -473,10 +483,17 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
   // value) cannot get orthogonal vectors from the twisted solves: Jacobi at once
   {
     const double sc = fmax(fabs(eig[0]), fabs(eig[K - 1]));
-    if (tid + 1 < r && !(eig[tid] - eig[tid + 1] > 1e-10 * sc)) red[kRedEig] = 1.0;
+    if (tid + 1 < r && !(eig[tid] - eig[tid + 1] > 1e-10 * sc)) {
+      if (fabs(eig[tid]) <= 1e-10 * sc)
+        atomicMin(cut, tid);  // numerical zeros: no vectors from the first of them on
+      else
+        red[kRedEig] = 1.0;
+    }
   }
   __syncthreads();
   if (red[kRedEig] != 0.0) return false;
+  r = *cut;
+  if (tid == 0) red[kRedLive] = (double)r;
   // 3. twisted factorizations (lane a: the a-th largest eigenvalue; scratch row Z + a K)
   if (tid < r) {
     const double lam = eig[tid];
@@ -609,7 +626,7 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
                                                         const double* __restrict__ Gpart, int nsplit,
                                                         double* __restrict__ big, double* __restrict__ Ca_all,
                                                         double* __restrict__ Cb_all, float* __restrict__ sigma_out,
-                                                        int64_t sigma_bstride) {
+                                                        int64_t sigma_bstride, int32_t* __restrict__ live_out) {
   constexpr int KB2 = kMaxKpBig * kMaxKpBig;
   __shared__ double sA[kMaxKpBig * (kMaxKpBig + 1) / 2];
   __shared__ __attribute__((aligned(16))) float sV[KB2];  // also eight rows of Gm (doubles) as scratch
@@ -773,8 +790,10 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   __threadfence();
   __syncthreads();
   const int ra = (int)(r_a < kp ? r_a : kp);
+  int live = ra;  // kept directions with weight (the others are completed by k_trunc_complete)
   if (eig_top<kMaxKpBig, true, float>(Gm, n, K, ra, sA, sV, reinterpret_cast<double*>(sV), sT[0], sT[1], sT[2],
                                       sT[3], sT[4], sEig, red)) {
+    live = (int)red[kRedLive];
     for (int j = tid; j < K; j += kTC) sOrd[j] = j;
   } else {
     for (int e = tid; e < np; e += kTC) sA[e] = Gm[e];
@@ -794,6 +813,15 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
   __syncthreads();
   const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
   for (int j = tid; j < K; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
+  if (tid == 0) {  // directions 0 .. live - 1 carry weight; k_trunc_complete fills the rows past them
+    int lv = 0;
+    while (lv < live && lv < (int)r_a) {
+      const double sa = sqrt(fmax(sEig[sOrd[lv]], 0.0));
+      if (!(sa > 1e-30 * s1 && sa > 0.0)) break;
+      ++lv;
+    }
+    live_out[mi] = lv;
+  }
   // 3. Ca[a][c] = (Vb H Vp)[c][ord a] / s_a ;  Cb[c][a] = (Vb H^{-1} Vp)[c][ord a] * s_a
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
@@ -840,9 +868,9 @@ __global__ __launch_bounds__(kTC) void k_trunc_core_big(int64_t nm, int64_t kp, 
         v += vb * sHi[x] * vp;
       }
     }
-    const bool live = sa > 1e-30 * s1 && sa > 0.0;
-    Ca[a * kp + c] = live ? u / sa : 0.0;
-    Cb[c * r_a + a] = live ? v * sa : 0.0;
+    const bool on = a < live && sa > 1e-30 * s1 && sa > 0.0;
+    Ca[a * kp + c] = on ? u / sa : 0.0;
+    Cb[c * r_a + a] = on ? v * sa : 0.0;
   }
 }
 
@@ -915,7 +943,7 @@ __global__ __launch_bounds__(kT) void k_trunc_apply_tiled(int64_t d, int64_t kp,
 __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, const double* __restrict__ Gpart,
                                                     int nsplit, double* __restrict__ Ca_all,
                                                     double* __restrict__ Cb_all, float* __restrict__ sigma_out,
-                                                    int64_t sigma_bstride) {
+                                                    int64_t sigma_bstride, int32_t* __restrict__ live_out) {
   constexpr int KB2 = kMaxKp * kMaxKp;
   __shared__ double sA[kMaxKp * (kMaxKp + 1) / 2];
   __shared__ double sV[KB2];   // eigenvectors of the current eigensolve; T = Gm H in between
@@ -1008,7 +1036,9 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
     }
     __syncthreads();
   } else {
-    // 3'. Gb = Vb diag(lb) Vb^T by Jacobi; H = Vb diag(sqrt(lb)) over the kept directions
+    // 3'. Gb = Vb diag(lb) Vb^T; H = Vb diag(sqrt(lb)) over the kept directions: those above
+    // 1e-12 ||Gb|| from the tridiagonal path (the others get no vector, lb = 0), or every
+    // pair by Jacobi (kept above 1e-14 of the largest) when its check fails
     for (int e = tid; e < n * n; e += kTC) {
       const int i = e / n, j = e % n;
       if (i > j) continue;
@@ -1018,20 +1048,31 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
       sA[pk(i, j, n)] = gb;
     }
     __syncthreads();
-    jacobi_packed<double>(sA, sV, n, cs, pairs, red);
-    __syncthreads();
-    if (tid == 0) {
-      double lmax = 0.0;
-      for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
-      red[kRedMax] = lmax;
+    if (eig_top<kMaxKp, false, double>(sA, n, K, K, sV, sV, sVb, sT[0], sT[1], sT[2], sT[3], sT[4], sEig, red)) {
+      const int nb = (int)red[kRedLive];
+      for (int j = tid; j < n; j += kTC) {
+        const double lb = j < nb ? sEig[j] : 0.0;
+        const bool keep = lb > 0.0;
+        sH[j] = keep ? sqrt(lb) : 0.0;
+        sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+      }
+    } else {
+      jacobi_packed<double>(sA, sV, n, cs, pairs, red);
+      __syncthreads();
+      if (tid == 0) {
+        double lmax = 0.0;
+        for (int j = 0; j < K; ++j) lmax = fmax(lmax, sA[pk(j, j, n)]);
+        red[kRedMax] = lmax;
+      }
+      __syncthreads();
+      for (int j = tid; j < n; j += kTC) {
+        const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
+        const bool keep = lb > 1e-14 * red[kRedMax] && lb > 0.0;
+        sH[j] = keep ? sqrt(lb) : 0.0;
+        sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
+      }
     }
     __syncthreads();
-    for (int j = tid; j < n; j += kTC) {
-      const double lb = j < K ? sA[pk(j, j, n)] : 0.0;
-      const bool keep = lb > 1e-14 * red[kRedMax] && lb > 0.0;
-      sH[j] = keep ? sqrt(lb) : 0.0;
-      sHi[j] = keep ? 1.0 / sqrt(lb) : 0.0;
-    }
     for (int e = tid; e < n * n; e += kTC) sVb[e] = sV[e];
     __syncthreads();
     // T = Gm Vb (into sV), then P^T P = H Vb^T T H (upper triangle, packed)
@@ -1054,7 +1095,9 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   // sV = Vp: the leading r_a eigenpairs from the tridiagonal path, or every pair by Jacobi
   // when its check fails
   const int ra = (int)(r_a < kp ? r_a : kp);
+  int live = ra;  // kept directions with weight (the others are completed by k_trunc_complete)
   if (eig_top<kMaxKp, false, double>(sA, n, K, ra, sV, sV, sG, sT[0], sT[1], sT[2], sT[3], sT[4], sEig, red)) {
+    live = (int)red[kRedLive];
     for (int j = tid; j < K; j += kTC) sOrd[j] = j;
   } else {
     jacobi_packed<double>(sA, sV, n, cs, pairs, red);
@@ -1100,6 +1143,15 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
   __syncthreads();
   const double s1 = sqrt(fmax(sEig[sOrd[0]], 0.0));
   for (int j = tid; j < K; j += kTC) sigma_out[mi * sigma_bstride + j] = (float)sqrt(fmax(sEig[sOrd[j]], 0.0));
+  if (tid == 0) {  // directions 0 .. live - 1 carry weight; k_trunc_complete fills the rows past them
+    int lv = 0;
+    while (lv < live && lv < (int)r_a) {
+      const double sa = sqrt(fmax(sEig[sOrd[lv]], 0.0));
+      if (!(sa > 1e-30 * s1 && sa > 0.0)) break;
+      ++lv;
+    }
+    live_out[mi] = lv;
+  }
   // 4. Ca[a][c] = (H Vp)[c][ord a] / s_a ;  Cb[c][a] = (H^{-T} Vp)[c][ord a] * s_a
   double* Ca = Ca_all + mi * r_a * kp;
   double* Cb = Cb_all + mi * kp * r_a;
@@ -1118,9 +1170,9 @@ __global__ __launch_bounds__(kTC) void k_trunc_core(int64_t kp, int64_t r_a, con
         v += vb * sHi[x] * vp;
       }
     }
-    const bool live = sa > 1e-30 * s1 && sa > 0.0;
-    Ca[a * kp + c] = live ? u / sa : 0.0;
-    Cb[c * r_a + a] = live ? v * sa : 0.0;
+    const bool on = a < live && sa > 1e-30 * s1 && sa > 0.0;
+    Ca[a * kp + c] = on ? u / sa : 0.0;
+    Cb[c * r_a + a] = on ? v * sa : 0.0;
   }
 }
 
@@ -1212,6 +1264,126 @@ __global__ void k_fill_zero(int32_t* p, int64_t cnt) {
   if (i < cnt) p[i] = 0;
 }
 
+// Rows rho = live[mi] .. r_a - 1 of a_out (matrix mi), whose directions carry no weight
+// (their b_out columns are zero), completed to orthonormal rows orthogonal to the rho live
+// rows L: columns rho .. r_a - 1 of the orthogonal H = I - Y T Y^T whose first rho columns are
+// L^T up to signs, H built from L by Householder reconstruction (Ballard et al., 2014): the
+// LU factorization without pivoting of the top rho x rho block of L^T minus diag(s), each
+// sign s_k opposite to the pivot it is subtracted from, gives Y's top block Y1 (unit lower)
+// and U; Y's other rows are L[:, i]^T U^{-1}, and T = -U diag(s) Y1^{-T}.  With
+// t_j = T Y[rho + j, :]^T and w_j = U^{-1} t_j the rows are
+//   X[j][i] = [i = rho + j] - sum_q w_j[q] L[q][i] + [i < rho] s_i w_j[i].
+// Workgroup (mi, y) writes coordinates [y kCSpan, (y + 1) kCSpan) of the rows of matrix mi
+// (the matrices without such rows return at once): the small factors in LDS (fp64, each
+// workgroup of a matrix alike), then per coordinate i a thread takes L[:, i] 16 rows at a
+// time in registers (w zero-padded to a multiple of 16) and writes the r_a - rho rows.
+constexpr int kTCC = 256;
+constexpr int kCSpan = 1024;
+__global__ __launch_bounds__(kTCC) void k_trunc_complete(int64_t d, int64_t r_a, const int32_t* __restrict__ live,
+                                                         float* __restrict__ a_out, int64_t a_bstride) {
+  constexpr int LD = kMaxRank + 1;
+  __shared__ double sA[kMaxRank][LD];   // L^T top block - diag(s): LU in place; later Y rows, then w
+  __shared__ double sUi[kMaxRank][LD];  // U^{-1}
+  __shared__ double sZ[kMaxRank][LD];   // Y1^{-1}; later t
+  __shared__ double sT[kMaxRank][LD];   // T
+  __shared__ double sSg[kMaxRank];
+  const int64_t mi = blockIdx.x;
+  const int rho = live[mi];
+  const int D = (int)r_a - rho;
+  if (D <= 0) return;
+  float* L = a_out + mi * a_bstride;
+  const int tid = threadIdx.x;
+  for (int e = tid; e < rho * rho; e += kTCC) sA[e / rho][e % rho] = (double)L[(int64_t)(e % rho) * d + e / rho];
+  __syncthreads();
+  for (int k = 0; k < rho; ++k) {
+    if (tid == 0) {
+      const double sg = sA[k][k] >= 0.0 ? -1.0 : 1.0;
+      sSg[k] = sg;
+      sA[k][k] -= sg;
+    }
+    __syncthreads();
+    for (int i = k + 1 + tid; i < rho; i += kTCC) sA[i][k] /= sA[k][k];
+    __syncthreads();
+    const int rem = rho - k - 1;
+    for (int e = tid; e < rem * rem; e += kTCC) {
+      const int i = k + 1 + e / rem, c = k + 1 + e % rem;
+      sA[i][c] -= sA[i][k] * sA[k][c];
+    }
+    __syncthreads();
+  }
+  if (tid < rho) {  // column tid of U^{-1}
+    const int c = tid;
+    for (int i = rho - 1; i >= 0; --i) {
+      double x = 0.0;
+      if (i <= c) {
+        x = i == c ? 1.0 : 0.0;
+        for (int k = i + 1; k <= c; ++k) x -= sA[i][k] * sUi[k][c];
+        x /= sA[i][i];
+      }
+      sUi[i][c] = x;
+    }
+  } else if (tid >= 64 && tid < 64 + rho) {  // column c of Y1^{-1}
+    const int c = tid - 64;
+    for (int i = 0; i < rho; ++i) {
+      double z = i == c ? 1.0 : 0.0;
+      if (i > c)
+        for (int k = c; k < i; ++k) z -= sA[i][k] * sZ[k][c];
+      sZ[i][c] = z;
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < rho * rho; e += kTCC) {  // T = -U diag(s) Y1^{-T}
+    const int a = e / rho, b = e % rho;
+    double t = 0.0;
+    for (int k = a; k <= b; ++k) t -= sA[a][k] * sSg[k] * sZ[b][k];
+    sT[a][b] = t;
+  }
+  __syncthreads();
+  for (int e = tid; e < D * rho; e += kTCC) {  // Y[rho + j][p] = sum_q L[q][rho + j] U^{-1}[q][p]
+    const int j = e / rho, p = e % rho;
+    double y = 0.0;
+    for (int q = 0; q <= p; ++q) y += (double)L[(int64_t)q * d + rho + j] * sUi[q][p];
+    sA[j][p] = y;
+  }
+  __syncthreads();
+  for (int e = tid; e < D * rho; e += kTCC) {  // t_j = T Y[rho + j]^T
+    const int j = e / rho, a = e % rho;
+    double t = 0.0;
+    for (int b = a; b < rho; ++b) t += sT[a][b] * sA[j][b];
+    sZ[j][a] = t;
+  }
+  __syncthreads();
+  const int rho16 = rho > 0 ? (rho + 15) & ~15 : 16;
+  for (int e = tid; e < D * rho16; e += kTCC) {  // w_j = U^{-1} t_j, zero past rho
+    const int j = e / rho16, q = e % rho16;
+    double w = 0.0;
+    for (int a = q; a < rho; ++a) w += sUi[q][a] * sZ[j][a];
+    sA[j][q] = w;
+  }
+  __syncthreads();
+  const int64_t i_end = (int64_t)(blockIdx.y + 1) * kCSpan < d ? (int64_t)(blockIdx.y + 1) * kCSpan : d;
+  for (int64_t i = (int64_t)blockIdx.y * kCSpan + tid; i < i_end; i += kTCC) {
+    for (int q0 = 0; q0 == 0 || q0 < rho; q0 += 16) {  // once when rho = 0
+      double l[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) l[u] = q0 + u < rho ? (double)L[(int64_t)(q0 + u) * d + i] : 0.0;
+      for (int j = 0; j < D; ++j) {
+        float* out = L + (int64_t)(rho + j) * d + i;
+        double x;
+        if (q0 == 0) {
+          x = i == rho + j ? 1.0 : 0.0;
+          if (i < rho) x += sSg[i] * sA[j][i];
+        } else {
+          x = (double)*out;
+        }
+#pragma unroll
+        for (int u = 0; u < 16; ++u) x -= sA[j][q0 + u] * l[u];
+        *out = (float)x;
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_lowrank_product(hipStream_t s, int64_t nmat, int64_t rows, int64_t cols, int64_t kk,
@@ -1232,6 +1404,7 @@ int trunc_splits(int64_t d) {
 size_t lowrank_truncate_ws(int64_t nm, int64_t d, int64_t kp, int64_t r_a) {
   size_t s = align256(sizeof(double) * nm * 2 * trunc_splits(d) * kp * kp);
   s += 2 * align256(sizeof(double) * nm * kp * r_a);
+  s += align256(sizeof(int32_t) * nm);  // directions with weight per matrix
   if (kp > kMaxKp)  // Gm, T (fp64) and the float copy of Vb per matrix
     s += align256(sizeof(double) * nm * 2 * kMaxKpBig * kMaxKpBig) + align256(sizeof(float) * nm * kMaxKpBig * kMaxKpBig);
   return s;
@@ -1243,11 +1416,13 @@ hipError_t launch_lowrank_truncate(const TruncArgs& a) {
   double* Gpart = (double*)p; p += align256(sizeof(double) * a.nm * 2 * ns * a.kp * a.kp);
   double* Ca = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.r_a);
   double* Cb = (double*)p; p += align256(sizeof(double) * a.nm * a.kp * a.r_a);
+  int32_t* live = (int32_t*)p; p += align256(sizeof(int32_t) * a.nm);
   k_fill_zero<<<(unsigned)((a.nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, a.nm);
   if (a.kp <= kMaxKp) {
     k_small_grams<kMaxKp><<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(
         a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, ns, Gpart);
-    k_trunc_core<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.kp, a.r_a, Gpart, ns, Ca, Cb, a.sigma_out, a.sigma_bstride);
+    k_trunc_core<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.kp, a.r_a, Gpart, ns, Ca, Cb, a.sigma_out, a.sigma_bstride,
+                                                       live);
     k_trunc_apply<<<dim3((unsigned)((a.d + kT - 1) / kT), (unsigned)a.nm, (unsigned)((a.r_a + kRA - 1) / kRA)), kT, 0,
                     a.stream>>>(
         a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
@@ -1257,11 +1432,13 @@ hipError_t launch_lowrank_truncate(const TruncArgs& a) {
     k_small_grams<kMaxKpBig><<<dim3((unsigned)a.nm, 2, (unsigned)ns), kT, 0, a.stream>>>(
         a.d, a.kp, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, ns, Gpart);
     k_trunc_core_big<<<(unsigned)a.nm, kTC, 0, a.stream>>>(a.nm, a.kp, a.r_a, Gpart, ns, big, Ca, Cb, a.sigma_out,
-                                                           a.sigma_bstride);
+                                                           a.sigma_bstride, live);
     k_trunc_apply_tiled<<<dim3((unsigned)((a.d + 63) / 64), (unsigned)a.nm), kT, 0, a.stream>>>(
         a.d, a.kp, a.r_a, a.m, a.m_bstride, a.r, a.r_bstride, a.r_group, Ca, Cb, a.a_out, a.a_bstride, a.b_out,
         a.b_bstride);
   }
+  k_trunc_complete<<<dim3((unsigned)a.nm, (unsigned)((a.d + kCSpan - 1) / kCSpan)), kTCC, 0, a.stream>>>(
+      a.d, a.r_a, live, a.a_out, a.a_bstride);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || !a.w_dense_out) return e;
   // W_r[i][j] = sum_a a_out[a][i] b_out[j][a]

@@ -298,6 +298,48 @@ def test_truncation_matches_explicit_svd(d, kp, r):
     np.testing.assert_allclose(A.T @ b[0].cpu().numpy().T, W[0].cpu().numpy(), atol=1e-4 * np.abs(Wr_o).max())
 
 
+@pytest.mark.parametrize("kp,r,rank", [(64, 32, 5), (96, 40, 5), (64, 32, 0), (32, 16, 15)])
+def test_truncation_low_rank_product(kp, r, rank):
+    """W = M B~ of rank below r_a (a label set of six classes makes Y, hence K and M, of rank
+    5; M = 0 gives W = 0): the directions with weight from the tridiagonal path, the others
+    numerically zero, so their b_out columns are zero and their a_out rows an orthonormal
+    completion; W_r and the leading sigma against the oracle's dense SVD."""
+    import torch
+    import oracle
+    from paper_2608_03020_amd import loca
+    d = 300
+    rng = np.random.default_rng(5 + rank)
+    log(f"case truncation_low_rank: d={d} kp={kp} r_a={r} rank={rank}")
+    Mh = (rng.normal(size=(d, rank)) @ rng.normal(size=(rank, kp))).astype(np.float32)
+    Rh = rng.normal(size=(kp, d)).astype(np.float32)
+    Wr_o, s_o = oracle.truncate_dense(Mh.astype(np.float64) @ Rh.astype(np.float64), r)
+    a = torch.empty((1, r, d), device="cuda")
+    b = torch.empty((1, d, r), device="cuda")
+    s = torch.empty((1, kp), device="cuda")
+    W = torch.empty((1, d, d), device="cuda")
+    info = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, 1, 0, d, kp, r_a=r))
+    loca.loca_lowrank_truncate(torch.from_numpy(Mh)[None].cuda(), torch.from_numpy(Rh)[None].cuda(), r, a, b, s,
+                               info, ws, w_dense_out=W)
+    torch.cuda.synchronize()
+    A = a[0].cpu().numpy().astype(np.float64)
+    B = b[0].cpu().numpy()
+    orth = np.abs(A @ A.T - np.eye(r)).max()
+    if rank == 0:
+        log(f"truncation (W = 0): |W_r| {np.abs(W[0].cpu().numpy()).max():.1e} |sigma| "
+            f"{np.abs(s[0].cpu().numpy()).max():.1e} |b_out| {np.abs(B).max():.1e} orth {orth:.2e}")
+        assert np.abs(W[0].cpu().numpy()).max() == 0.0 and np.abs(s[0].cpu().numpy()).max() == 0.0
+        assert np.abs(B).max() == 0.0 and orth < 1e-6
+        return
+    e_w = rel(W[0].cpu().numpy(), Wr_o)
+    e_s = rel(s[0].cpu().numpy()[:rank], s_o[:rank])
+    log(f"truncation (rank {rank}): W_r {e_w:.2e} sigma {e_s:.2e} orth {orth:.2e} "
+        f"dead b_out {np.abs(B[:, rank:]).max():.1e}")
+    assert e_w < 1e-5 and e_s < 1e-5
+    assert orth < 1e-5
+    assert np.abs(B[:, rank:]).max() <= 1e-6 * np.abs(B[:, :rank]).max()
+
+
 @pytest.mark.parametrize("kp,r", [(64, 32), (32, 8), (96, 32)])
 def test_truncation_repeated_leading_values(kp, r):
     """Repeated singular values among the r kept (a triple and a pair): the eigenvectors of the
