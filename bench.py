@@ -34,10 +34,10 @@ HBM_PEAK_GBS = 8000.0
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
 # kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 3745463.5, "write_kib": 780014.2, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "97d82c4331e648ac"},
-    "c5": {"fetch_kib": 19890750.5, "write_kib": 2663642.7, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "97d82c4331e648ac"},
+    "c3": {"fetch_kib": 3674125.0, "write_kib": 796091.5, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "619e103979d626b4"},
+    "c5": {"fetch_kib": 17482341.9, "write_kib": 2666688.7, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "619e103979d626b4"},
 }
 
 

@@ -24,6 +24,7 @@
 //
 // fp32 mode: X is fp32 and the statistics are fp64 (v_mfma_f64_16x16x4f64).
 #include <algorithm>
+#include <cmath>
 
 #include "loca_launch.h"
 
@@ -292,8 +293,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
                                                                 const uint16_t* __restrict__ zero16, int64_t b0,
                                                                 const uint16_t* __restrict__ Yhl_all, int64_t w2,
                                                                 int64_t w2p, float* __restrict__ Kraw_all,
-                                                                const float* __restrict__ wpad, int ncross, int per,
-                                                                int gx, int nblk) {
+                                                                const float* __restrict__ wpad, int ncross, int run,
+                                                                int per, int gx, int nblk) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -314,17 +315,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   const int ntile = T * (T + 1) / 2, ntot = ntile + ncross;
   // Tile order.  per == 0: the XCD-aware order over all blocks of the launch (each XCD runs
   // its own run of blocks).  per > 0: the XCDs form 8 / gx groups of gx, each block is cut
-  // into gx runs of per tiles, and XCD x takes run x % gx of every (8 / gx)-th block, from
-  // block x / gx on (the slots past a block's tiles, or past the last block, exit): the XCDs
-  // of a group work on the same block at the same time, so that the blocks in flight, 8 / gx
-  // of them, keep their X in the last-level cache and read it from HBM about once; taken
-  // when a run still fills most of an XCD's 32 compute units.
+  // into gx runs (run tiles each, the last one the rest, at most per), and XCD x takes run
+  // x % gx of every (8 / gx)-th block, from block x / gx on, in slots of per (the slots past
+  // a run, or past the last block, exit): the XCDs of a group work on the same block at the
+  // same time, so that the blocks in flight, 8 / gx of them, keep their X in the last-level
+  // cache and read it from HBM about once; taken when a run still fills most of an XCD's 32
+  // compute units.
   int logical;
   if (per > 0) {
     const int L = (int)blockIdx.x, x = L & 7, i = L >> 3;
-    const int t = (x % gx) * per + i % per;
+    const int xs = x % gx, u = i % per;
+    const int t = xs * run + u;
     const int blk = (i / per) * (8 / gx) + x / gx;
-    if (t >= ntot || blk >= nblk) return;
+    if ((xs < gx - 1 && u >= run) || t >= ntot || blk >= nblk) return;
     logical = blk * ntot + t;
   } else {
     logical = xcd_logical((int)blockIdx.x, (int)gridDim.x);
@@ -342,8 +345,24 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   const int64_t b = b0 + logical / ntot;
   const uint16_t* X = Xall + b * x_bstride;
   float* S = Sall + b * s_bstride;
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int wi = wid / WGN, wj = wid % WGN;
+  const int lane = threadIdx.x & 63, wid = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);  // uniform
+  int wi = wid / WGN, wj = wid % WGN;
+  // The waves of a cross tile whose columns lie wholly past the split targets' w2p would
+  // multiply zeros: they take the last wave slots and skip their fragments and products, so
+  // that with at most two column blocks of targets each SIMD (waves w and w + 4) holds one
+  // wave with products.
+  const int ncb = (int)((w2p + WN - 1) / WN);
+  if (WGM == 2 && WGN == 4 && ctile && ncb < WGN) {
+    if (wid < 2 * ncb) {
+      wi = wid / ncb;
+      wj = wid % ncb;
+    } else {
+      const int u = wid - 2 * ncb, ni = WGN - ncb;
+      wi = u / ni;
+      wj = ncb + u % ni;
+    }
+  }
+  const bool mm_on = !(ctile && wj * WN >= w2p);
   const bool active = !(diag && (wj + 1) * WN <= wi * WM);
   const bool fuse = diag && Yhl_all != nullptr && ncross == 0;  // this tile also forms the cross statistic
   const bool cross = fuse && !active && WGM == 2 && wj < 2;     // ... in this wave
@@ -405,8 +424,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   // The copies of a step are spread between its rows of MFMAs: a wave issues in order,
   // and copies issued back to back would queue at the address unit and hold up the
   // MFMAs behind them.  Every wave runs the same instruction stream (waves of a
-  // diagonal tile below its diagonal compute too and only skip the write-back), so
-  // the loop has no divergent branches.
+  // diagonal tile below its diagonal compute too and only skip the write-back; the
+  // cross-tile waves past the targets skip fragments and products on a branch that is
+  // uniform in the wave), so the loop has no divergent branches.
   bf16x8_t fa0[NBM], fb0[NBN], fa1[NBM], fb1[NBN], fl0[NBN], fl1[NBN];
   auto load_frags = [&](const uint16_t* buf, int ks, bf16x8_t (&fa)[NBM], bf16x8_t (&fb)[NBN]) {
 #pragma unroll
@@ -436,6 +456,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   auto step = [&](uint16_t* cur, uint16_t* nxt, uint16_t* fill, int kt) {
     __builtin_amdgcn_s_waitcnt(vmcnt_imm(NCP));  // stage kt + 1 landed (this thread's copies)
     barrier_nofence();                           // ... everyone's; slot `fill` no longer read
+    if (!mm_on) {  // copies only
+#pragma unroll
+      for (int j = 0; j < NCP; ++j) issue(fill, kt + kDLStages - 1, j);
+      return;
+    }
 #pragma unroll
     for (int sl = 0; sl < NSLOT; ++sl) {
       if ((sl * NCP) % NSLOT == 0) {
@@ -495,7 +520,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
         }
       }
   }
-  if (cross || ctile) {  // Kraw rows cI + arow0 + .., columns kc0 + .. < w2 (row stride w2)
+  if (cross || (ctile && mm_on)) {  // Kraw rows cI + arow0 + .., columns kc0 + .. < w2 (row stride w2)
     float* Kraw = Kraw_all + b * d * w2;
     const int kc0 = ctile ? bcol0 : 0;
 #pragma unroll
@@ -818,17 +843,25 @@ static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_
                            double* diag_part, const uint16_t* Yhl, int64_t w2, int64_t w2p, float* Kraw,
                            const float* wpad, int ncross) {
   // block-synchronous order with the widest XCD group (8, 4 or 2) whose runs hold at least
-  // 24 tiles, if there are blocks enough for every group; else the XCD-aware order
+  // 24 tiles, if there are blocks enough for every group; else the XCD-aware order.  The
+  // runs split a block's cost: a cross tile whose targets span at most two of the four
+  // column blocks (four waves with products, one per SIMD) is counted as 0.6 of a Gram tile,
+  // and the cross tiles, last in a block, go to the last run of its group.
   const int64_t ntot = ntile + ncross;
   int gx = 0;
   for (int g = 8; g >= 2 && gx == 0; g /= 2)
     if ((ntot + g - 1) / g >= 24 && nbc >= 8 / g) gx = g;
-  const int64_t run = gx > 0 ? (ntot + gx - 1) / gx : 0;
+  int64_t run = 0, per = 0;
+  if (gx > 0) {
+    const double cost = (double)ntile + (w2p <= 128 ? 0.6 : 1.0) * (double)ncross;
+    run = std::min<int64_t>((int64_t)std::ceil(cost / gx), gx > 1 ? ntot / (gx - 1) : ntot);
+    per = std::max<int64_t>(run, ntot - (gx - 1) * run);
+  }
   const int64_t rounds = gx > 0 ? (nbc + 8 / gx - 1) / (8 / gx) : 0;
-  const int64_t grid = gx > 0 ? 8 * run * rounds : ntot * nbc;
+  const int64_t grid = gx > 0 ? 8 * per * rounds : ntot * nbc;
   k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)grid), 512, 0, a.stream>>>(
       a.n, a.d, (const uint16_t*)a.x, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, Yhl, w2,
-      w2p, Kraw, wpad, ncross, (int)run, gx > 0 ? gx : 8, (int)nbc);
+      w2p, Kraw, wpad, ncross, (int)run, (int)per, gx > 0 ? gx : 8, (int)nbc);
 }
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {
