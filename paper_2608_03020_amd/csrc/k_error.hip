@@ -134,11 +134,14 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
   __shared__ __attribute__((aligned(16))) unsigned char lds[L::BYTES];
   __shared__ float sW[kSmallThreads];  // statistic weight of each token (0 past n)
   __shared__ double sred[kSmallThreads / 64];
-  float* sA = (float*)lds;  // C x k, row stride k
+  float* sA = (float*)lds;  // C x KB, zero past k (the products below need no bound)
   const int64_t b = blockIdx.y;
   const AT* Ab = A + b * a_bstride;
   const double* Gb = G + b * KB * KB;
-  for (int64_t e = threadIdx.x; e < C * k; e += blockDim.x) sA[e] = load_as_f32(Ab + e);
+  for (int64_t e = threadIdx.x; e < C * KB; e += blockDim.x) {
+    const int64_t c = e / KB, j = e % KB;
+    sA[e] = j < k ? load_as_f32(Ab + c * k + j) : 0.f;
+  }
   __syncthreads();
 
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -152,18 +155,41 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
     if (yt < 0 || yt >= C) {
       atomicMin(dev_info, (int32_t)(t + 1));
     } else {
-      float m = load_as_f32(zt);
-      for (int64_t c = 1; c < C; ++c) m = fmaxf(m, load_as_f32(zt + c));
+      // the logits in chunks of 8 classes, each chunk's loads issued together (held in
+      // registers for the three passes when C <= 8)
+      float zc[8];
+      auto chunk = [&](int64_t c0) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) zc[u] = c0 + u < C ? load_as_f32(zt + c0 + u) : -INFINITY;
+      };
+      chunk(0);
+      float m = zc[0];
+      for (int64_t c0 = 0; c0 < C; c0 += 8) {
+        if (c0 > 0) chunk(c0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (c0 + u < C) m = fmaxf(m, zc[u]);
+      }
       float s = 0.f;
-      for (int64_t c = 0; c < C; ++c) s += __expf(load_as_f32(zt + c) - m);
+      for (int64_t c0 = 0; c0 < C; c0 += 8) {
+        if (c0 > 0 || C > 8) chunk(c0);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (c0 + u < C) s += __expf(zc[u] - m);
+      }
       const float inv = 1.0f / s;
       const float wt = w ? w[t] : 1.0f;
-      for (int64_t c = 0; c < C; ++c) {
-        const float e = wt * (__expf(load_as_f32(zt + c) - m) * inv - (c == yt ? 1.0f : 0.0f));
-        if (e_out) e_out[t * C + c] = e;
+      for (int64_t c0 = 0; c0 < C; c0 += 8) {
+        if (c0 > 0 || C > 8) chunk(c0);
 #pragma unroll
-        for (int j = 0; j < KB; ++j)
-          if (j < k) y[j] = fmaf(e, sA[c * k + j], y[j]);
+        for (int u = 0; u < 8; ++u) {
+          const int64_t c = c0 + u;
+          if (c >= C) break;
+          const float e = wt * (__expf(zc[u] - m) * inv - (c == yt ? 1.0f : 0.0f));
+          if (e_out) e_out[t * C + c] = e;
+#pragma unroll
+          for (int j = 0; j < KB; ++j) y[j] = fmaf(e, sA[c * KB + j], y[j]);
+        }
       }
       wq = aw ? aw[t] : 1.0f;  // statistic weight of the position
     }
@@ -177,14 +203,33 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
   sW[threadIdx.x] = wq;
   wave_lds_sync();
 
-  // Y rows to HBM: each store instruction covers 64 / KB consecutive tokens x KB columns
+  // Y rows to HBM: each store instruction covers consecutive tokens' whole rows (with k = KB
+  // and 16-byte aligned rows, 16-byte stores of 256 / KB tokens, every value read from the
+  // tile before the first store)
   const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + 64 * wv;
   float* yb = y_out + b * y_bstride;
+  if (k == KB && (y_bstride & 3) == 0 && ((uintptr_t)y_out & 15) == 0) {
+    constexpr int R4 = KB / 4;  // 16-byte chunks per row, and per lane
+    float4 v[R4];
 #pragma unroll
-  for (int i = 0; i < KB; ++i) {
-    const int e = lane + 64 * i, p = e / KB, c = e % KB;
-    const int64_t tp = t0 + p;
-    if (tp < n && c < k) yb[tp * k + c] = sT[p * (KB + 1) + c];
+    for (int i = 0; i < R4; ++i) {
+      const int e = lane + 64 * i, p = e / R4, c4 = 4 * (e % R4);
+      const float* src = sT + p * (KB + 1) + c4;
+      v[i] = make_float4(src[0], src[1], src[2], src[3]);
+    }
+#pragma unroll
+    for (int i = 0; i < R4; ++i) {
+      const int e = lane + 64 * i, p = e / R4, c4 = 4 * (e % R4);
+      const int64_t tp = t0 + p;
+      if (tp < n) *(float4*)(yb + tp * KB + c4) = v[i];
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < KB; ++i) {
+      const int e = lane + 64 * i, p = e / KB, c = e % KB;
+      const int64_t tp = t0 + p;
+      if (tp < n && c < k) yb[tp * k + c] = sT[p * (KB + 1) + c];
+    }
   }
 
   // this wave's part of ||Q||^2

@@ -350,7 +350,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
   // The waves of a cross tile whose columns lie wholly past the split targets' w2p would
   // multiply zeros: they take the last wave slots and skip their fragments and products, so
   // that with at most two column blocks of targets each SIMD (waves w and w + 4) holds one
-  // wave with products.
+  // wave with products.  (The waves of a diagonal tile below its diagonal keep computing:
+  // skipping their products made the c5 call about 1% slower.)
   const int ncb = (int)((w2p + WN - 1) / WN);
   if (WGM == 2 && WGN == 4 && ctile && ncb < WGN) {
     if (wid < 2 * ncb) {
@@ -736,13 +737,15 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
 
 // ------------------------------------------------------------------ finalize: eta_bar and K
 
-// One workgroup per (block, 256 entries of K); its first wave forms ||X||^2 from the
+// One workgroup per (block, 256 V entries of K); its first wave forms ||X||^2 from the
 // diagonal tiles' partials (lane l sums partials l, l + 64, ... in order, then a fixed
-// butterfly across the lanes: deterministic) and eta-bar once for the workgroup.
+// butterfly across the lanes: deterministic) and eta-bar once for the workgroup.  A thread
+// takes V consecutive entries of a row of K (V = 4: 16-byte accesses, k % 4 == 0 and K's
+// rows 16-byte aligned), each formed alike.
 // dev_info (may be null) gets, per block, 0 or LOCA_INFO_NONFINITE when ||X||^2 or ||Q||^2
 // is not finite (a NaN or infinite entry of X, an entry whose square overflows, or a
 // non-finite error row in the head call).
-template <typename AccT>
+template <typename AccT, int V = 1>
 __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, const double* __restrict__ diag_part,
                                  loca_mb* __restrict__ mb, double eta, const AccT* __restrict__ Kraw, int split,
                                  AccT* __restrict__ Kall, int64_t k_bstride, int32_t* __restrict__ dev_info) {
@@ -767,15 +770,31 @@ __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, con
   }
   __syncthreads();
   const double eb = s_eb;
-  const uint32_t e = blockIdx.x * blockDim.x + threadIdx.x;  // d k < 2^31 (d, k <= 65535, 128)
+  const uint32_t e = V * (blockIdx.x * blockDim.x + threadIdx.x);  // d k < 2^31 (d, k <= 65535, 128)
   if (e >= (uint32_t)(d * k)) return;
   const uint32_t ku = (uint32_t)k, i = e / ku, c = e - i * ku;
   AccT* K = Kall + b * k_bstride;
   const uint32_t w = split ? 2 * ku : ku;
   const AccT* kr = Kraw + b * d * w + (int64_t)i * w;
-  double v = (double)kr[c];
-  if (split) v += (double)kr[c + ku];
-  K[e] = (AccT)((double)K[e] - eb * v);
+  if constexpr (V == 4) {
+    static_assert(sizeof(AccT) == 4, "16-byte accesses of floats");
+    const float4 k0 = *(const float4*)(kr + c);
+    const float4 k1 = split ? *(const float4*)(kr + c + ku) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4 o = *(const float4*)(K + e);
+    const float a0[4] = {k0.x, k0.y, k0.z, k0.w}, a1[4] = {k1.x, k1.y, k1.z, k1.w}, ov[4] = {o.x, o.y, o.z, o.w};
+    float r[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      double v = (double)a0[u];
+      if (split) v += (double)a1[u];
+      r[u] = (float)((double)ov[u] - eb * v);
+    }
+    *(float4*)(K + e) = make_float4(r[0], r[1], r[2], r[3]);
+  } else {
+    double v = (double)kr[c];
+    if (split) v += (double)kr[c + ku];
+    K[e] = (AccT)((double)K[e] - eb * v);
+  }
 }
 
 }  // namespace
@@ -787,6 +806,42 @@ __global__ void k_zero_bytes(uint32_t* p, int cnt) {
 // Yhl[b][t] = [bf16(y) | bf16(y - bf16(y)) | 0] (w2p columns, w2p % 8 == 0) from the float
 // targets, and the 256 zero bytes at the head of the workspace.  One thread per 8 columns of a
 // row (one 16-byte store); IT is the index type (32-bit while n w2p / 8 fits).
+// k_split_y8 (k % 8 == 0, so w2p = 2k, and Y's rows 32-byte aligned): a thread reads 8
+// consecutive targets of a row once (two 16-byte loads) and writes their high and low
+// parts (two 16-byte stores); the values are those of k_split_y.
+template <typename IT>
+__global__ void k_split_y8(int64_t n, int64_t k, const float* __restrict__ Yall, int64_t y_bstride,
+                           uint16_t* __restrict__ Yhl, uint32_t* __restrict__ zero_area) {
+  const int64_t b = blockIdx.y;
+  if (b == 0 && blockIdx.x == 0 && threadIdx.x < 64) zero_area[threadIdx.x] = 0u;
+  const IT g8 = (IT)(k / 8);
+  const IT e = (IT)blockIdx.x * (IT)blockDim.x + (IT)threadIdx.x;
+  if (e >= (IT)n * g8) return;
+  const IT t = e / g8;
+  const int c0 = 8 * (int)(e - t * g8);
+  const float* yr = Yall + b * y_bstride + (int64_t)t * k + c0;
+  const float4 v0 = *(const float4*)yr, v1 = *(const float4*)(yr + 4);
+  const float y[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+  uint32_t wh[4], wl[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t h2[2], l2[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const float x = y[2 * i + u];
+      const __bf16 hi = (__bf16)x;  // round to nearest even
+      const __bf16 lo = (__bf16)(x - (float)hi);
+      h2[u] = (uint32_t)__builtin_bit_cast(uint16_t, hi);
+      l2[u] = (uint32_t)__builtin_bit_cast(uint16_t, lo);
+    }
+    wh[i] = h2[0] | (h2[1] << 16);
+    wl[i] = l2[0] | (l2[1] << 16);
+  }
+  uint16_t* row = Yhl + b * n * 2 * k + (int64_t)t * 2 * k;
+  *(uint4*)(row + c0) = make_uint4(wh[0], wh[1], wh[2], wh[3]);
+  *(uint4*)(row + k + c0) = make_uint4(wl[0], wl[1], wl[2], wl[3]);
+}
+
 template <typename IT>
 __global__ void k_split_y(int64_t n, int64_t k, int64_t w2p, const float* __restrict__ Yall, int64_t y_bstride,
                           uint16_t* __restrict__ Yhl, uint32_t* __restrict__ zero_area) {
@@ -910,9 +965,14 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   const bool ctiles = dl && !fused;
   if (dl) {
     if (fused || ctiles) {
-      const int64_t groups = a.n * (w2p / 8);
+      const bool v8 = a.k % 8 == 0 && a.y_bstride % 8 == 0 && ((uintptr_t)a.y & 31) == 0;
+      const int64_t groups = v8 ? a.n * (a.k / 8) : a.n * (w2p / 8);
       dim3 gy((unsigned)((groups + 255) / 256), (unsigned)a.nb);
-      if (groups < ((int64_t)1 << 31))
+      if (v8 && groups < ((int64_t)1 << 31))
+        k_split_y8<uint32_t><<<gy, 256, 0, a.stream>>>(a.n, a.k, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
+      else if (v8)
+        k_split_y8<int64_t><<<gy, 256, 0, a.stream>>>(a.n, a.k, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
+      else if (groups < ((int64_t)1 << 31))
         k_split_y<uint32_t><<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
       else
         k_split_y<int64_t><<<gy, 256, 0, a.stream>>>(a.n, a.k, w2p, a.y, a.y_bstride, Yhl, (uint32_t*)a.ws);
@@ -969,9 +1029,15 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
-  k_stats_finalize<float><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
-                                                    (float*)a.K, a.k_bstride, a.dev_info);
+  if (a.k % 4 == 0 && a.k_bstride % 4 == 0 && ((uintptr_t)a.K & 15) == 0) {
+    dim3 g4((unsigned)((a.d * a.k / 4 + 255) / 256), (unsigned)a.nb);
+    k_stats_finalize<float, 4><<<g4, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
+                                                         (float*)a.K, a.k_bstride, a.dev_info);
+  } else {
+    dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
+    k_stats_finalize<float><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
+                                                      (float*)a.K, a.k_bstride, a.dev_info);
+  }
   return hipGetLastError();
 }
 

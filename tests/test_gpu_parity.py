@@ -161,6 +161,43 @@ def test_large_vocab_padded_logit_rows(k, blocks):
         assert ey < 1e-4 and eq < 2e-4
 
 
+@pytest.mark.parametrize("C,k,ldz,dt", [(9, 24, 9, "f32"), (17, 64, 24, "bf16"), (64, 32, 64, "f32"), (5, 64, 8, "bf16")])
+def test_register_head_many_classes(C, k, ldz, dt):
+    """The register head (C <= 64 classes, k <= 64) with its logits in chunks of 8 classes:
+    one chunk plus a tail of 1 (C = 9), three chunks in a padded buffer (C = 17 in rows of
+    24), eight chunks (C = 64), and C = 5 in rows of 8; 300 tokens (a ragged workgroup), two
+    blocks; E, Y and ||Q||^2 against the oracle."""
+    import torch
+    from paper_2608_03020_amd import loca
+    from paper_2608_03020_amd.step import BlockStep
+    import oracle
+    cfg = gen.custom_config(f"head{C}", blocks=2, d=256, n=300, C=C, k=k, r_a=8, logit_std=2.0,
+                            logit_dtype=dt, a_dtype="f32")
+    xs, zs, ys, As, Bs = host_inputs(cfg, [0, 1])
+    log(f"case register head: C={C} k={k} logits {dt} in rows of {ldz}, 2 blocks")
+    st = BlockStep(cfg, 2)
+    st.reset()
+    z = zs[0]
+    n = z.shape[0]
+    buf = np.zeros((n, ldz), z.dtype)
+    buf[:, :C] = z
+    zd = to_dev(buf)[:, :C]
+    e_out = torch.full((n, C), float("nan"), device="cuda")
+    loca.loca_error_targets(zd, to_dev(ys[0]), to_dev(np.stack(As)), to_dev(np.stack(Bs)), st.Y[:, :n], st.mb,
+                            st.info_err[:1], st.ws, e_out=e_out)
+    torch.cuda.synchronize()
+    assert int(st.info_err[0].item()) == 0
+    E = oracle.head_error(gen.as_f64(z, dt), ys[0])
+    ee = rel(e_out.cpu().numpy(), E)
+    q2 = loca.mb_view(st.mb)["sum_q2"]
+    for b in range(2):
+        Y, Q = oracle.credit(E, np.asarray(As[b], np.float64), np.asarray(Bs[b], np.float64))
+        ey = rel(st.Y[b, :n].cpu().numpy(), Y)
+        eq = abs(q2[b] - np.sum(Q ** 2)) / np.sum(Q ** 2)
+        log(f"block {b}: E rel err {ee:.2e}, Y rel err {ey:.2e}, ||Q||^2 rel err {eq:.2e}")
+        assert ee < 1e-5 and ey < 1e-5 and eq < 1e-5
+
+
 def test_dense_targets_and_cross_statistic():
     """T = -eta_bar Y B~ (dense) and Z = X^T T = K B~ against the oracle's dense Z."""
     import torch
