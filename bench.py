@@ -34,10 +34,10 @@ HBM_PEAK_GBS = 8000.0
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
 # kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 3674125.0, "write_kib": 796091.5, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "619e103979d626b4"},
-    "c5": {"fetch_kib": 17482341.9, "write_kib": 2666688.7, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "619e103979d626b4"},
+    "c3": {"fetch_kib": 3716693.5, "write_kib": 791629.8, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "715eff64eb510a5b"},
+    "c5": {"fetch_kib": 17925713.9, "write_kib": 2658928.0, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "715eff64eb510a5b"},
 }
 
 
