@@ -1222,13 +1222,14 @@ __global__ __launch_bounds__(kT) void k_back_step(int64_t d, int64_t m, int64_t 
 // ------------------------------------------------------------------ back substitution, float
 
 // One launch per row block p (descending) of U M' = Y, right-looking, with M'_p already
-// in Mp: workgroups x >= 1 apply R_r -= U_{r,p} M'_p to four row blocks r above p each;
+// in Mp: workgroups x >= 1 apply R_r -= U_{r,p} M'_p to kBackPer row blocks r above p each;
 // workgroup 0 applies it to the block q just above p and then forms M'_q = U_qq^{-1} R_q
 // (U_qq^{-1} sits in the diagonal block of F), so the next launch finds M'_q in Mp.  With
 // `init`, workgroup 0 only forms M'_p of the last block.  The first operand of every
 // product streams from F into registers: MFMA j of a K range of 32 takes k = 16 h + j
 // in lane half h, for both operands, so a lane reads 16 consecutive floats of its row.
 // The second operand (M'_p, or the updated R_q) sits transposed in LDS.
+constexpr int kBackPer = 2;  // row blocks per updating workgroup (the launch waits on its slowest)
 template <int NQ, bool V4>
 __global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p, int init, const float* __restrict__ Fall,
                                                  float* __restrict__ Rall, float* __restrict__ Mpall) {
@@ -1345,8 +1346,8 @@ __global__ __launch_bounds__(kT) void k_back_f32(int64_t d, int64_t m, int64_t p
     store_mp(r0, P, acc);
     return;
   }
-  for (int c = 0; c < 4; ++c) {
-    const int64_t q0 = nab - 2 - 4 * ((int64_t)blockIdx.x - 1) - c;
+  for (int c = 0; c < kBackPer; ++c) {
+    const int64_t q0 = nab - 2 - kBackPer * ((int64_t)blockIdx.x - 1) - c;
     if (q0 < 0) break;
     const int64_t r0 = q0 * P;
     // the old values of the block's right-hand sides are loaded before the product
@@ -1578,7 +1579,8 @@ hipError_t run_group(const SolveArgs& a, int64_t b0, int64_t nbg, hipStream_t st
     if ((e = emit([=]() { return back(plast, 1, 1); })) != hipSuccess) return e;
     for (int64_t pp = plast; pp >= P; pp -= P) {
       const int64_t nab = pp / P;
-      if ((e = emit([=]() { return back(pp, 0, (unsigned)(1 + (nab - 1 + 3) / 4)); })) != hipSuccess) return e;
+      if ((e = emit([=]() { return back(pp, 0, (unsigned)(1 + (nab - 1 + kBackPer - 1) / kBackPer)); })) != hipSuccess)
+        return e;
     }
   } else {
     for (int64_t pp = ((d - 1) / P) * P; pp >= 0; pp -= P) {
