@@ -1598,31 +1598,66 @@ __global__ __launch_bounds__(256) void k_proj_sa_mfma(int64_t d, int64_t r_a, co
 }
 
 // G[b] = PA T1 (r_a x r_a) and AK[b] = PA K (r_a x k), fp64, in two passes: partial sums
-// over kProjSplit ranges of the rows (grid.z), then a fixed-order sum.
-constexpr int kProjSplit = 16;
-template <typename ST>
-__global__ void k_proj_small_part(int64_t d, int64_t k, int64_t r_a, const float* __restrict__ PA,
-                                  int64_t pa_bstride, const double* __restrict__ T1, const ST* __restrict__ K,
-                                  int64_t k_bstride, double* __restrict__ part) {
+// over kProjSplit ranges of the rows (grid.z), then a fixed-order sum.  In the first, thread
+// c of a workgroup takes column c of [T1 | K] and forms its entries for all RA rows of PA
+// (RA sums in registers, rows a >= r_a zero); the rows of PA come 64 entries at a time
+// through LDS, read four at a time by every thread alike (broadcast).
+constexpr int kProjSplit = 64;
+constexpr int kProjT = 192;  // threads: columns of [T1 | K] (r_a + k <= 64 + 128 by the API limits)
+constexpr int kProjI = 64;   // rows of PA per LDS stage
+template <typename ST, int RA>
+__global__ __launch_bounds__(kProjT) void k_proj_small_part(int64_t d, int64_t k, int64_t r_a,
+                                                            const float* __restrict__ PA, int64_t pa_bstride,
+                                                            const double* __restrict__ T1, const ST* __restrict__ K,
+                                                            int64_t k_bstride, double* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) float sP[RA][kProjI];
   const int64_t b = blockIdx.y, z = blockIdx.z;
   const int64_t nout = r_a * r_a + r_a * k;
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= nout) return;
+  const int c = (int)threadIdx.x;  // column of [T1 | K]
+  const bool on = c < r_a + k;
   const int64_t chunk = (d + kProjSplit - 1) / kProjSplit;
   const int64_t i0 = z * chunk, i1 = i0 + chunk < d ? i0 + chunk : d;
   const float* P = PA + b * pa_bstride;
-  double s = 0.0;
-  if (e < r_a * r_a) {
-    const int64_t a = e / r_a, c = e % r_a;
-    const double* T = T1 + b * d * r_a;
-    for (int64_t i = i0; i < i1; ++i) s += (double)P[a * d + i] * T[i * r_a + c];
-  } else {
-    const int64_t f = e - r_a * r_a;
-    const int64_t a = f / k, c = f % k;
-    const ST* Kb = K + b * k_bstride;
-    for (int64_t i = i0; i < i1; ++i) s += (double)P[a * d + i] * (double)Kb[i * k + c];
+  const bool t1 = c < r_a;
+  const double* T = T1 + b * d * r_a + (t1 ? c : 0);
+  const ST* Kc = K + b * k_bstride + (t1 ? 0 : c - r_a);
+  double s[RA];
+#pragma unroll
+  for (int a = 0; a < RA; ++a) s[a] = 0.0;
+  for (int64_t is = i0; is < i1; is += kProjI) {
+    const int ni = (int)(i1 - is < kProjI ? i1 - is : kProjI);
+    __syncthreads();  // the previous stage is no longer read
+    for (int e = c; e < RA * kProjI; e += kProjT) {
+      const int a = e / kProjI, ii = e % kProjI;
+      sP[a][ii] = (a < r_a && ii < ni) ? P[a * d + is + ii] : 0.f;
+    }
+    __syncthreads();
+    if (on)
+      for (int ii = 0; ii < ni; ii += 4) {
+        double v[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int64_t i = is + ii + u;
+          v[u] = ii + u < ni ? (t1 ? T[i * r_a] : (double)Kc[i * k]) : 0.0;
+        }
+#pragma unroll
+        for (int a = 0; a < RA; ++a) {
+          const float4 p4 = *(const float4*)&sP[a][ii];
+          s[a] += (double)p4.x * v[0];
+          s[a] += (double)p4.y * v[1];
+          s[a] += (double)p4.z * v[2];
+          s[a] += (double)p4.w * v[3];
+        }
+      }
   }
-  part[(b * kProjSplit + z) * nout + e] = s;
+  if (!on) return;
+  double* out = part + (b * kProjSplit + z) * nout;
+#pragma unroll
+  for (int a = 0; a < RA; ++a) {
+    if (a >= r_a) break;
+    if (t1) out[a * r_a + c] = s[a];
+    else out[r_a * r_a + a * k + (c - r_a)] = s[a];
+  }
 }
 __global__ void k_proj_small_sum(int64_t k, int64_t r_a, const double* __restrict__ part, double* __restrict__ G,
                                  double* __restrict__ AK, float* __restrict__ g_out) {
@@ -1678,13 +1713,16 @@ __global__ __launch_bounds__(64) void k_proj_chol(int64_t r_a, const double* __r
 
 // One thread per row i of B*: C[i] = B_cur[i] G + sum_c B~[c][i] AK[:, c], then the row
 // solve x (L L^T) = C[i] (forward with L, backward with L^T), fp64, RA >= r_a registers.
-// The small operands (AK, G, L) are read at wave-uniform addresses.
+// AK sits transposed in LDS ([c][a], zero for a >= r_a), read by every thread alike
+// (broadcast); G and L are read at wave-uniform addresses.  The row of B* leaves in 16-byte
+// stores when r_a % 4 == 0.
 template <int RA>
 __global__ __launch_bounds__(256) void k_proj_rows(int64_t d, int64_t k, int64_t r_a, const double* __restrict__ G,
                                                    const double* __restrict__ AK, const double* __restrict__ Lw,
                                                    const float* __restrict__ Bt, int64_t b_bstride,
                                                    const float* __restrict__ Bc, int64_t bc_bstride, int nl,
                                                    float* __restrict__ out, int64_t bo_bstride) {
+  __shared__ __attribute__((aligned(16))) double sAK[128 * RA];  // [c][a], k <= 128
   const int64_t mi = blockIdx.y;
   const int64_t b = mi / nl;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -1693,14 +1731,20 @@ __global__ __launch_bounds__(256) void k_proj_rows(int64_t d, int64_t k, int64_t
   const float* Btb = Bt + b * b_bstride;
   const double* AKb = AK + b * r_a * k;
   const double* L = Lw + mi * r_a * r_a;
+  const int kk = (int)k;
+  for (int e = threadIdx.x; e < kk * RA; e += 256) {
+    const int c = e / RA, a = e % RA;
+    sAK[e] = a < r_a ? AKb[a * k + c] : 0.0;
+  }
+  __syncthreads();
   double x[RA];
 #pragma unroll
   for (int a = 0; a < RA; ++a) x[a] = 0.0;
-  for (int64_t c = 0; c < k; ++c) {
-    const double bt = (double)Btb[c * d + ic];
+  for (int c = 0; c < kk; ++c) {
+    const double bt = (double)Btb[(int64_t)c * d + ic];
+    const double* row = sAK + c * RA;
 #pragma unroll
-    for (int a = 0; a < RA; ++a)
-      if (a < r_a) x[a] += bt * AKb[a * k + c];
+    for (int a = 0; a < RA; ++a) x[a] += bt * row[a];
   }
   if (Bc) {
     const float* Bci = Bc + b * bc_bstride + ic * r_a;
@@ -1733,9 +1777,15 @@ __global__ __launch_bounds__(256) void k_proj_rows(int64_t d, int64_t k, int64_t
   }
   if (ok) {
     float* o = out + mi * bo_bstride + i * r_a;
+    if ((r_a & 3) == 0 && (bo_bstride & 3) == 0 && ((uintptr_t)out & 15) == 0) {
 #pragma unroll
-    for (int a = 0; a < RA; ++a)
-      if (a < r_a) o[a] = (float)x[a];
+      for (int a = 0; a < RA; a += 4)
+        if (a < r_a) *(float4*)(o + a) = make_float4((float)x[a], (float)x[a + 1], (float)x[a + 2], (float)x[a + 3]);
+    } else {
+#pragma unroll
+      for (int a = 0; a < RA; ++a)
+        if (a < r_a) o[a] = (float)x[a];
+    }
   }
 }
 
@@ -1772,11 +1822,16 @@ hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
   const int64_t nm = a.nb * a.n_lambda;
   k_fill_zero<<<(unsigned)((nm + 255) / 256), 256, 0, a.stream>>>(a.dev_info, nm);
   dim3 g1((unsigned)((a.d * a.r_a + 255) / 256), (unsigned)a.nb);
-  dim3 g2((unsigned)((a.r_a * a.r_a + a.r_a * a.k + 255) / 256), (unsigned)a.nb, kProjSplit);
+  if (a.r_a + a.k > kProjT) return hipErrorInvalidValue;  // one thread per column of [T1 | K]
+  dim3 g2(1u, (unsigned)a.nb, kProjSplit);
   if (a.acc == LOCA_F64) {
     k_proj_sa<double><<<g1, 256, 0, a.stream>>>(a.d, a.r_a, (const double*)a.S, a.s_bstride, a.proj_a, a.pa_bstride, T1);
-    k_proj_small_part<double><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
-                                                        (const double*)a.K, a.k_bstride, gpart);
+    if (a.r_a <= 32)
+      k_proj_small_part<double, 32><<<g2, kProjT, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
+                                                                  (const double*)a.K, a.k_bstride, gpart);
+    else
+      k_proj_small_part<double, 64><<<g2, kProjT, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
+                                                                  (const double*)a.K, a.k_bstride, gpart);
   } else {
     dim3 gp((unsigned)((a.d + kPS - 1) / kPS), (unsigned)a.nb);
     const float* Sf = (const float*)a.S;
@@ -1793,8 +1848,12 @@ hipError_t launch_ridge_solve_projected(const ProjArgs& a) {
       else LOCA_PROJ_SA(64, false);
     }
 #undef LOCA_PROJ_SA
-    k_proj_small_part<float><<<g2, 256, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
-                                                       (const float*)a.K, a.k_bstride, gpart);
+    if (a.r_a <= 32)
+      k_proj_small_part<float, 32><<<g2, kProjT, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
+                                                                 (const float*)a.K, a.k_bstride, gpart);
+    else
+      k_proj_small_part<float, 64><<<g2, kProjT, 0, a.stream>>>(a.d, a.k, a.r_a, a.proj_a, a.pa_bstride, T1,
+                                                                 (const float*)a.K, a.k_bstride, gpart);
   }
   dim3 g2s((unsigned)((a.r_a * a.r_a + a.r_a * a.k + 255) / 256), (unsigned)a.nb);
   k_proj_small_sum<<<g2s, 256, 0, a.stream>>>(a.k, a.r_a, gpart, G, AK, a.g_out);
