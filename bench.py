@@ -111,10 +111,11 @@ def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, 
     and credit coordinates (from the event error_record[m] when given), then the
     statistics (bracketed by the events of `record[m]` when given); then the ridge
     solves, the truncation and, with the projections `proj` (nb, r_a, d), the
-    paper-literal projected solve (bracketed by `solve_record`: start, between the
-    solves and the truncation and between the truncation and the projected solve when
-    it has four events, end).  Optional: statistic weights a_all (n,), a current
-    adapter lp (nb, d, r_prev), rp (nb, r_prev, d)."""
+    paper-literal projected solve, which needs only the statistics and runs on a stream
+    of its own beside the ridge solves (bracketed by `solve_record`: start, between the
+    solves and the truncation and after the truncation when it has four events, end,
+    after the step's stream has waited for the projected solve).  Optional: statistic
+    weights a_all (n,), a current adapter lp (nb, d, r_prev), rp (nb, r_prev, d)."""
     from paper_2608_03020_amd import loca
     step.reset()
     for m in range(cfg.n_micro):
@@ -551,7 +552,7 @@ def measure(args, name, nb_override=0, keep=False):
         "statistics": sum(stats_ms) / K,
         "ridge_solves": sum(e[0].elapsed_time(e[1]) for e in ev_sol) / K,
         "truncation": sum(e[1].elapsed_time(e[2]) for e in ev_sol) / K,
-        "projected_solve": sum(e[2].elapsed_time(e[3]) for e in ev_sol) / K,
+        "wait_for_projected_solve": sum(e[2].elapsed_time(e[3]) for e in ev_sol) / K,
     }
     out = {
         "value": nb * cfg.n / (ms_step * 1e-3),

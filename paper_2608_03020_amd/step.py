@@ -56,20 +56,27 @@ class BlockStep:
         self.projected = projected
         if projected:
             self.B_proj = torch.empty((nb, nl, d, r_a), dtype=torch.float32, device=device)
+            # the projected solve reads only the statistics: it runs on a stream of its own
+            # (default priority) beside the ridge solves, with a workspace of its own
+            self.ws_proj = loca.alloc_workspace(
+                loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE_PROJECTED, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
+                device)
+            self.side = torch.cuda.Stream(device=device)
         ws = max(
             loca.workspace_size(loca.LOCA_OP_ERROR_TARGETS, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
             loca.workspace_size(loca.LOCA_OP_ACCUMULATE_STATS, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
             loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE, nb, n_mb, d, kp, cfg.C, r_a, nl, self.acc),
             loca.workspace_size(loca.LOCA_OP_LOWRANK_TRUNCATE, nb * nl, n_mb, d, kp, cfg.C, r_a, nl, self.acc),
-            loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE_PROJECTED, nb, n_mb, d, k, cfg.C, r_a, nl, self.acc),
         )
         self.ws = loca.alloc_workspace(ws, device)
         if poison:
-            # NaN in every output and all-ones bytes in the workspace, so that a region a
+            # NaN in every output and all-ones bytes in the workspaces, so that a region a
             # call should write but does not shows up as NaN in the results
             for t in (self.Y, self.M, self.A_ad, self.B_ad, self.sigma) + ((self.B_proj,) if projected else ()):
                 t.fill_(float("nan"))
             self.ws.fill_(255)
+            if projected:
+                self.ws_proj.fill_(255)
 
     @property
     def info(self):
@@ -109,13 +116,21 @@ class BlockStep:
         With a current adapter W_prev = Lp Rp (lp: (nb, d, r_prev), rp: (nb, r_prev, d);
         the outer iteration past its first step, Theorem S6.1 with W_prev != 0), the solve
         takes the right-hand sides [S Lp | K] and W = M [Rp; B~] is truncated from its
-        factors; the stacked right factor is a copy (layout only).  mid_event, when given,
-        is recorded on the current stream between the solves and the truncation, and
-        trunc_event between the truncation and the projected solve."""
+        factors; the stacked right factor is a copy (layout only).  The projected solve
+        (with proj_a) needs only the statistics: it is issued first, on the side stream
+        after the statistics, and the current stream waits for it after the truncation.
+        mid_event, when given, is recorded on the current stream between the solves and the
+        truncation, and trunc_event after the truncation (before that wait)."""
         import torch
         cfg = self.cfg
         nl = len(cfg.lambdas)
         kp = self.r_prev + cfg.k
+        cur = stream if stream is not None else torch.cuda.current_stream()
+        side = self.projected and proj_a is not None
+        if side:
+            self.side.wait_stream(cur)  # the statistics have landed
+            loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj,
+                                            self.info_proj, self.ws_proj, stream=self.side)
         if self.r_prev > 0:
             assert lp is not None and rp is not None and lp.shape[-1] == self.r_prev
             loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info_solve, self.ws, lp=lp, rp=rp,
@@ -125,14 +140,13 @@ class BlockStep:
             loca.loca_ridge_solve(self.S, self.K, cfg.lambdas, self.M, self.info_solve, self.ws, stream=stream)
             right = credit_b
         if mid_event is not None:
-            mid_event.record(stream if stream is not None else torch.cuda.current_stream())
+            mid_event.record(cur)
         loca.loca_lowrank_truncate(self.M.view(self.nb * nl, cfg.d, kp), right, cfg.r_a, self.A_ad, self.B_ad,
                                    self.sigma, self.info_trunc, self.ws, r_group=nl, stream=stream)
         if trunc_event is not None:
-            trunc_event.record(stream if stream is not None else torch.cuda.current_stream())
-        if self.projected and proj_a is not None:
-            loca.loca_ridge_solve_projected(self.S, self.K, credit_b, proj_a, cfg.lambdas, self.B_proj,
-                                            self.info_proj, self.ws, stream=stream)
+            trunc_event.record(cur)
+        if side:
+            cur.wait_stream(self.side)
 
     def run(self, x_blocks, logits, labels, credit_a, credit_b, proj_a=None, stream=None, lp=None, rp=None):
         """One full pass over all micro-batches of all nb blocks (with the current adapter

@@ -8,6 +8,8 @@
 * Two host threads, each running statistics and then the ridge solve on its own
   stream and buffers, give the bits of the single-threaded runs (the solve's internal
   streams are shared between them).
+* The projected solve on the step's side stream, beside the ridge solves, gives the
+  bits of the same calls run alone.
 """
 import threading
 
@@ -226,3 +228,38 @@ def test_concurrent_solves_from_two_threads():
             for a, b in zip(got, ref[i]):
                 assert np.array_equal(a, b), (i, r)
             assert np.all(st.info.cpu().numpy() == 0)
+
+
+def test_projected_solve_beside_ridge_solves():
+    """The projected solve runs on the step's side stream beside the ridge solves (three
+    blocks, so the solves use their internal streams too); over three steps in a row M,
+    the truncation and B* equal, bit for bit, the ridge solve run alone and the projected
+    solve called alone on the same statistics."""
+    import torch
+    from paper_2608_03020_amd import loca
+    from paper_2608_03020_amd.step import BlockStep
+    cfg = gen.custom_config("side", blocks=3, d=1024, n=2048, micro=1024, C=5, k=16, r_a=8, lambdas=(1e-2, 1e-1))
+    xs, zs, ys, As, Bs = host_inputs(cfg, range(3), seed=3)
+    x_all = padded_rows(np.stack([np.concatenate(xb) for xb in xs]))
+    z_all, y_all = to_dev(np.concatenate(zs)), to_dev(np.concatenate(ys))
+    A, B = to_dev(np.stack(As)), to_dev(np.stack(Bs))
+    proj = gen.torch_gen_adapter_projection(cfg, 3)
+    log("case projected solve on the side stream: 3 blocks, 2 lambdas, 3 steps")
+    ref = BlockStep(cfg, 3)
+    ref.run(x_all, z_all, y_all, A, B)
+    nl = len(cfg.lambdas)
+    b_ref = torch.empty((3, nl, cfg.d, cfg.r_a), device="cuda")
+    info_ref = torch.zeros(3 * nl, dtype=torch.int32, device="cuda")
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_RIDGE_SOLVE_PROJECTED, 3, cfg.micro, cfg.d, cfg.k,
+                                                  cfg.C, cfg.r_a, nl, ref.acc))
+    loca.loca_ridge_solve_projected(ref.S, ref.K, B, proj, cfg.lambdas, b_ref, info_ref, ws)
+    torch.cuda.synchronize()
+    st = BlockStep(cfg, 3, projected=True, poison=True)
+    for rep in range(3):
+        st.B_proj.fill_(float("nan"))
+        st.run(x_all, z_all, y_all, A, B, proj_a=proj)
+        torch.cuda.synchronize()
+        assert np.array_equal(st.M.cpu().numpy(), ref.M.cpu().numpy()), rep
+        assert np.array_equal(st.sigma.cpu().numpy(), ref.sigma.cpu().numpy()), rep
+        assert np.array_equal(st.B_proj.cpu().numpy(), b_ref.cpu().numpy()), rep
+        assert np.all(st.info.cpu().numpy() == 0) and np.all(info_ref.cpu().numpy() == 0)
