@@ -20,6 +20,7 @@
 // Each vocabulary range leaves (m, s) per token and its partial output; a second kernel
 // combines the ranges in a fixed order in float64 and subtracts the label term.  Columns of
 // Vm beyond one 64-wide tile recompute the logits (c / 64 passes over W_u).
+#include "loca_bf16.h"
 #include "loca_launch.h"
 
 namespace loca {
@@ -46,11 +47,6 @@ LOCA_DEV int fz_swz(int r) { return (r >> 2) & 3; }
 // The Vm^T slice: 64 rows (columns of Vm) of 512 bytes (256 vocabulary entries), chunk c
 // of row r at position c ^ (r & 15).
 LOCA_DEV int fv_swz(int r) { return r & 15; }
-
-LOCA_DEV uint16_t rne_bf16(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (uint16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
-}
 
 // (m, s) of two disjoint parts of a row, combined
 LOCA_DEV void fz_combine(float& m, float& s, float m2, float s2) {
@@ -281,16 +277,13 @@ __global__ __launch_bounds__(kFT) void k_fused_head(int64_t n, int64_t V, int64_
           uint32_t hv[4], lv[4];
 #pragma unroll
           for (int e2 = 0; e2 < 4; ++e2) {
-            uint16_t hh[2], ll[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-              const int r = 8 * ks2 + 2 * e2 + u;
-              const float p = valid(mv, r) ? __expf(z[mv][mt][r] - m_run[mt]) : 0.f;
-              hh[u] = rne_bf16(p);
-              ll[u] = rne_bf16(p - __uint_as_float((uint32_t)hh[u] << 16));
-            }
-            hv[e2] = (uint32_t)hh[0] | ((uint32_t)hh[1] << 16);
-            lv[e2] = (uint32_t)ll[0] | ((uint32_t)ll[1] << 16);
+            // hi and lo parts rounded to nearest even by the hardware conversion, in pairs
+            const int r = 8 * ks2 + 2 * e2;
+            const float p0 = valid(mv, r) ? __expf(z[mv][mt][r] - m_run[mt]) : 0.f;
+            const float p1 = valid(mv, r + 1) ? __expf(z[mv][mt][r + 1] - m_run[mt]) : 0.f;
+            const uint32_t h2 = cvt_pk_bf16(p0, p1);
+            hv[e2] = h2;
+            lv[e2] = cvt_pk_bf16(p0 - bf16_lo(h2), p1 - bf16_hi(h2));
           }
           phi[mt] = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
           plo[mt] = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
@@ -455,6 +448,7 @@ __global__ __launch_bounds__(256) void k_fused_combine(int64_t n, int64_t c, int
 // ahead; one barrier per chunk.  ZT: bf16 (uint16_t, ld % 8 == 0) or float (ld % 4 == 0) logits with
 // 16-byte aligned rows; entries past V are masked, reads stay inside the row's stride.
 constexpr int kOnlineChunk = 64;
+constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kOnlineStages = 3;  // logits ring slots: two chunks in flight while one is read
 // LDS staging of a chunk's logits: 128 token rows of 64 entries (bf16: 128 bytes, 8 chunks of
 // 16 bytes; float: 256 bytes, 16 chunks), chunk c of row r at position c ^ swz(r), so that the
@@ -564,14 +558,19 @@ __global__ __launch_bounds__(256) void k_head_online(int64_t n, int64_t V, const
         }
       }
     }
-    const bool full = v0 + kOnlineChunk <= ve;
-    auto valid = [&](int ks, int e) { return full || v0 + 16 * ks + 8 * lh + e < ve; };
+    if (v0 + kOnlineChunk > ve) {  // the range's ragged last chunk: entries past ve out (p = 0)
+      const int rem = (int)(ve - v0);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          if (16 * ks + 8 * lh + e >= rem) zv[ks][e] = -__builtin_inff();
+    }
     float cm = -__builtin_inff();
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        if (valid(ks, e)) cm = fmaxf(cm, zv[ks][e]);
+      for (int e = 0; e < 8; ++e) cm = fmaxf(cm, zv[ks][e]);
     cm = fmaxf(cm, __shfl_xor(cm, 32));
     if (__any(cm > m_run)) {  // raise the running maximum of the tokens that need it
       const float mn = fmaxf(m_run, cm);
@@ -585,22 +584,21 @@ __global__ __launch_bounds__(256) void k_head_online(int64_t n, int64_t V, const
         for (int q = 0; q < 2; ++q) o[q][r] *= a_r;
       }
     }
+    const float m2 = m_run * kLog2e;  // exp(z - m) = 2^(z log2(e) - m log2(e))
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       uint32_t hv[4], lv[4];
 #pragma unroll
       for (int e2 = 0; e2 < 4; ++e2) {
-        uint16_t hh[2], ll[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          const int e = 2 * e2 + u;
-          const float p = valid(ks, e) ? __expf(zv[ks][e] - m_run) : 0.f;
-          s_lane += p;
-          hh[u] = rne_bf16(p);
-          ll[u] = rne_bf16(p - __uint_as_float((uint32_t)hh[u] << 16));
-        }
-        hv[e2] = (uint32_t)hh[0] | ((uint32_t)hh[1] << 16);
-        lv[e2] = (uint32_t)ll[0] | ((uint32_t)ll[1] << 16);
+        // p = exp(z - m), 0 for the masked entries (m_run is finite); hi and lo parts rounded
+        // to nearest even by the hardware conversion, two values per instruction
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(zv[ks][2 * e2], kLog2e, -m2)),
+                    p1 = __builtin_amdgcn_exp2f(fmaf(zv[ks][2 * e2 + 1], kLog2e, -m2));
+        s_lane += p0;
+        s_lane += p1;
+        const uint32_t h2 = cvt_pk_bf16(p0, p1);
+        hv[e2] = h2;
+        lv[e2] = cvt_pk_bf16(p0 - bf16_lo(h2), p1 - bf16_hi(h2));
       }
       const bf16x8_t phi = __builtin_bit_cast(bf16x8_t, make_uint4(hv[0], hv[1], hv[2], hv[3]));
       const bf16x8_t plo = __builtin_bit_cast(bf16x8_t, make_uint4(lv[0], lv[1], lv[2], lv[3]));
