@@ -483,31 +483,45 @@ __global__ __launch_bounds__(256) void k_q2_rows(int64_t n, int64_t k, const flo
   if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
 }
 
-// The same for k <= KB with G padded to KB x KB (zero past k): the row of Y in registers
-// (zero past k), G through scalar loads, the symmetric half of the products (fp64).
+// The same for k <= KB with G padded to KB x KB (zero past k): 16 lanes per token, lane p
+// forming r_a = sum_c G[a][c] y_c for its KB / 16 rows a = p + 16 u (G transposed in LDS,
+// so that the 16 lanes read consecutive a), then y_a r_a summed over its rows and over the
+// 16 lanes by a fixed butterfly (fp64); 16 tokens per workgroup.
 template <int KB>
 __global__ __launch_bounds__(256) void k_q2_rows_kb(int64_t n, int64_t k, const float* __restrict__ Y,
                                                     int64_t y_bstride, const double* __restrict__ G,
                                                     const float* __restrict__ aw, double* __restrict__ partial) {
+  constexpr int RPL = KB / 16;  // rows a per lane
+  __shared__ double sG[KB * KB];  // [c][a]
   __shared__ double sred[4];
   const int64_t b = blockIdx.y;
-  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const double* Gb = G + b * KB * KB;
+  for (int e = threadIdx.x; e < KB * KB; e += 256) sG[(e % KB) * KB + e / KB] = Gb[e];
+  __syncthreads();
+  const int p = threadIdx.x & 15;
+  const int64_t t = (int64_t)blockIdx.x * 16 + (threadIdx.x >> 4);
   double qv = 0.0;
   if (t < n) {
     const float* yt = Y + b * y_bstride + t * k;
-    double yd[KB];
+    double r[RPL];
 #pragma unroll
-    for (int j = 0; j < KB; ++j) yd[j] = j < k ? (double)yt[j] : 0.0;
+    for (int u = 0; u < RPL; ++u) r[u] = 0.0;
+    for (int c = 0; c < (int)k; ++c) {
+      const double yc = (double)yt[c];
 #pragma unroll
-    for (int a = 0; a < KB; ++a) {
-      double r = 0.5 * Gb[a * KB + a] * yd[a];
-#pragma unroll
-      for (int c2 = a + 1; c2 < KB; ++c2) r += Gb[a * KB + c2] * yd[c2];
-      qv += 2.0 * yd[a] * r;
+      for (int u = 0; u < RPL; ++u) r[u] += sG[c * KB + p + 16 * u] * yc;
     }
-    if (aw) qv *= (double)aw[t];
+#pragma unroll
+    for (int u = 0; u < RPL; ++u) {
+      const int a = p + 16 * u;
+      if (a < k) qv += (double)yt[a] * r[u];
+    }
   }
+  // the 16 lanes of a token, in a fixed order
+#pragma unroll
+  for (int off = 8; off >= 1; off >>= 1) qv += __shfl_xor(qv, off, 16);
+  if (aw && t < n) qv *= (double)aw[t];
+  if (p != 0) qv = 0.0;
   const double tot = block_sum(qv, sred);
   if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
 }
@@ -600,15 +614,17 @@ hipError_t launch_error_targets(const ErrorArgs& a) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (use_product(a)) {
-    // partials of k_q2_rows: one per 256 tokens (fewer than the large kernel's, which the
-    // workspace holds); the product's statistics and partial sums after them
+    // partials of k_q2_rows_kb: one per 16 tokens (as many as the large kernel's, which the
+    // workspace holds; k_q2_rows, for k > 64: one per 256); the product's statistics and
+    // partial sums after them
     char* pw = (char*)partial + align256(sizeof(double) * a.nb * parts);
     SoftmaxProductArgs sp{a.stream, a.n, a.C, a.logits, a.logits_dtype, a.ld_logits, a.labels, a.w,
                           (const uint16_t*)a.credit_a, a.nb, a.k, a.nb > 1 ? a.a_bstride : 0, a.y_out, a.k,
                           a.y_bstride, a.dev_info, pw};
     if ((e = launch_softmax_product(sp)) != hipSuccess) return e;
-    dim3 gq((unsigned)((a.n + 255) / 256), (unsigned)a.nb);
-    if (a.k > kSmallMaxK)
+    const bool kb = a.k <= kSmallMaxK;  // 16 tokens per workgroup, else 256
+    dim3 gq((unsigned)(kb ? (a.n + 15) / 16 : (a.n + 255) / 256), (unsigned)a.nb);
+    if (!kb)
       k_q2_rows<<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
     else if (lg == 16)
       k_q2_rows_kb<16><<<gq, 256, 0, a.stream>>>(a.n, a.k, a.y_out, a.y_bstride, G, a.a_w, partial);
