@@ -292,7 +292,6 @@ LOCA_DEV double safe_pivot(double q, double pivmin) { return fabs(q) < pivmin ? 
 
 constexpr int kRedEig = 43;   // reduction-scratch slot: a check of eig_top failed
 constexpr int kRedLive = 44;  // ... the number of pairs eig_top returned
-constexpr int kRedCut = 45;   // ... the same as an int while it is lowered
 
 // All eigenvalues of the packed symmetric K x K matrix A (packed with stride n, K <= KM) and
 // the eigenvectors of its r largest, A left unchanged:
@@ -339,7 +338,8 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
       const int i = e / n, j = e % n;
       W[e] = (i < K && j < K) ? A[pk(i, j, n)] : 0.0;
     }
-  int* cut = reinterpret_cast<int*>(&red[kRedCut]);
+  __shared__ int s_cut;  // the number of pairs while it is lowered
+  int* cut = &s_cut;
   if (tid == 0) red[kRedEig] = 0.0;
   __syncthreads();
   // 1. reduction to tridiagonal form
