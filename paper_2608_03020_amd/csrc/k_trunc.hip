@@ -436,6 +436,7 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
   glo -= 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
   ghi += 2.1 * tnorm * 2.220446049250313e-16 * K + 4.2 * pivmin;
   __syncthreads();
+  const int r_req = r;  // the pairs asked for: their eigenvalues all get the full precision
   {  // only the eigenvalues above 1e-12 ||T|| get vectors: below it the r largest would hold
      // a cluster of numerical zeros (A of rank below r), whose vectors the twisted solves
      // cannot separate and whose directions carry no weight (every thread counts alike)
@@ -450,14 +451,15 @@ LOCA_DEV bool eig_top(const double* A, int n, int K, int r, double* W, OutT* Vou
     if (tid == 0) *cut = r;
   }
   // 2. multisection: group g = tid / LPR finds the g-th smallest eigenvalue, lane t of the
-  // group testing point t + 1 of LPR equal steps (the last one is hi); for the r largest,
-  // whose vectors follow, 52 bits or more of the interval (13 steps of 16, 18 of 8), for
-  // the others 40 or more (10 of 16, 14 of 8)
+  // group testing point t + 1 of LPR equal steps (the last one is hi); for the r largest
+  // asked for (whose vectors follow, and whose singular values are reported to the same
+  // accuracy when they are numerical zeros), 52 bits or more of the interval (13 steps of
+  // 16, 18 of 8), for the others 40 or more (10 of 16, 14 of 8)
   {
     constexpr int STEPS_V = LPR == 16 ? 13 : 18, STEPS_S = LPR == 16 ? 10 : 14;
     const int g = tid / LPR, t = tid % LPR;
     const int j = g < K ? g : K - 1;
-    const int steps = K - 1 - j < r ? STEPS_V : STEPS_S;
+    const int steps = K - 1 - j < r_req ? STEPS_V : STEPS_S;
     double lo = glo, hi = ghi;
     for (int it = 0; it < steps; ++it) {
       const double h = (hi - lo) * (1.0 / LPR);
