@@ -132,7 +132,7 @@ def run_step(step, cfg, nb, x_all, z, y, A, B, stream, record=None, a_all=None, 
         if record is not None:
             record[m][0].record(stream)
         loca.loca_accumulate_stats(xm, yv, cfg.eta, step.mb, step.S, step.K, step.ws, a_w=aw,
-                                   dev_info=step.info_stats[m])
+                                   dev_info=step.info_stats[m], overwrite=m == 0)
         if record is not None:
             record[m][1].record(stream)
     if solve_record is not None:

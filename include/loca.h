@@ -186,8 +186,10 @@ size_t loca_error_targets_noalloc_max_bytes(void);
  *   mb[b].sum_x2 = sum_t a_t ||x_t||^2,  mb[b].eta_bar = eta sqrt(sum_x2/sum_q2) (Eq. 10),
  *   K_b += -eta_bar X_b^T diag(a) Y_b   (d x k),
  * with the statistic weights a (Section S7's weighted form; a = 1 when a_w is NULL).
- * The caller zeroes S and K before the first micro-batch.  Each mini-batch
- * uses its own eta_bar (Section S8).
+ * overwrite != 0 (the first micro-batch of a step): S = X_b^T diag(a) X_b and
+ * K = -eta_bar X_b^T diag(a) Y_b instead, the old contents of S and K never read (no
+ * clearing pass needed); overwrite == 0: the caller has zeroed S and K, or an earlier
+ * call of the step has written them.  Each mini-batch uses its own eta_bar (Section S8).
  * x : per block n x d, ldx >= d, x_bstride; BF16 (then acc = F32) or F32
  *     (then acc = F64).  BF16 requires ldx % 8 == 0 and a 16-byte aligned
  *     base; F32 requires ldx % 4 == 0 and 16-byte alignment.
@@ -209,7 +211,8 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
                                   const float* y, int64_t y_bstride, const float* a_w,
                                   double eta, loca_mb* mb,
                                   void* S, void* K, loca_dtype acc, int64_t s_bstride,
-                                  int64_t k_bstride, int32_t* dev_info, void* ws, size_t ws_bytes);
+                                  int64_t k_bstride, int overwrite, int32_t* dev_info, void* ws,
+                                  size_t ws_bytes);
 
 /* ---------------------------------------------------------------------------
  * (a5) Ridge solve in factored form (Eq. 7; Theorem S6.1; Section S7's

@@ -13,7 +13,10 @@
 // are computed.  Y (fp32) enters the cross product as two bf16 columns
 // (hi = bf16(y), lo = bf16(y - hi)), so products stay exact and the sum of the
 // two halves carries ~16 bits of y.  Every output element is owned by one
-// workgroup and summed in a fixed order: results are deterministic.
+// workgroup and summed in a fixed order: results are deterministic.  With the
+// overwrite flag (keep == 0 in the kernels; the first micro-batch of a step) S and K
+// take this micro-batch's statistics without their old contents being read, which
+// spares the caller a clearing pass over S and this call one read of it.
 //
 // Statistic weights a_t (Section S7's weighted form, S = X^T diag(a) X): in bf16 mode
 // the second operand of every Gram product is scaled in registers, a_t x_tj as a
@@ -143,7 +146,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16(int64_t n, int64_t
                                                              const uint16_t* __restrict__ Xall, int64_t ldx,
                                                              int64_t x_bstride, float* __restrict__ Sall,
                                                              int64_t s_bstride, double* __restrict__ diag_part,
-                                                             const float* __restrict__ wpad) {
+                                                             const float* __restrict__ wpad, int keep) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN;
   constexpr int NBM = WM / 32, NBN = WN / 32;
@@ -237,7 +240,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16(int64_t n, int64_t
           const int64_t col = cJ + wj * WN + 32 * q + mfma32_col(lane);
           ok[r] = row < d && col < d;
           idx[r] = row * d + col;
-          old[r] = ld_or_zero(S, idx[r], ok[r]);
+          old[r] = ld_or_zero(S, idx[r], keep && ok[r]);
           if (diag && ok[r] && row == col) dsum += (double)acc[m][q][r];
         }
 #pragma unroll
@@ -294,7 +297,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
                                                                 const uint16_t* __restrict__ Yhl_all, int64_t w2,
                                                                 int64_t w2p, float* __restrict__ Kraw_all,
                                                                 const float* __restrict__ wpad, int ncross, int run,
-                                                                int per, int gx, int nblk) {
+                                                                int per, int gx, int nblk, int keep) {
   constexpr int BM = 256, NT = 64 * WGM * WGN;
   constexpr int WM = BM / WGM, WN = BM / WGN, NBM = WM / 32, NBN = WN / 32;
   constexpr int TILE_ELEMS = kBK * BM;            // one panel stage (bf16 elements)
@@ -509,7 +512,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gram_bf16_dl(int64_t n, int6
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int64_t row = rb + mfma32_row(lane, r);
-          old[r] = ld_or_zero(S, row * d + col, row < d && col < d);
+          old[r] = ld_or_zero(S, row * d + col, keep && row < d && col < d);
         }
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -651,7 +654,7 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
                                                        int64_t y_bstride, double* __restrict__ Sall,
                                                        int64_t s_bstride, double* __restrict__ Kraw,
                                                        double* __restrict__ diag_part, int nS,
-                                                       const float* __restrict__ aw) {
+                                                       const float* __restrict__ aw, int keep) {
   __shared__ double sP[kBK64 * kLD64];
   __shared__ double sQ[kBK64 * kLD64];
   __shared__ double sred[kThreads / 64];
@@ -724,7 +727,7 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
           if (kjob) {
             Kb[row * k + col] = acc[m][q][r];
           } else {
-            S[row * d + col] += acc[m][q][r];
+            S[row * d + col] = (keep ? S[row * d + col] : 0.0) + acc[m][q][r];
             if (diag && row == col) dsum += acc[m][q][r];
           }
         }
@@ -741,14 +744,16 @@ __global__ __launch_bounds__(kThreads) void k_gram_f64(int64_t n, int64_t d, int
 // diagonal tiles' partials (lane l sums partials l, l + 64, ... in order, then a fixed
 // butterfly across the lanes: deterministic) and eta-bar once for the workgroup.  A thread
 // takes V consecutive entries of a row of K (V = 4: 16-byte accesses, k % 4 == 0 and K's
-// rows 16-byte aligned), each formed alike.
+// rows 16-byte aligned), each formed alike.  keep == 0: K is overwritten (its old
+// contents are not read).
 // dev_info (may be null) gets, per block, 0 or LOCA_INFO_NONFINITE when ||X||^2 or ||Q||^2
 // is not finite (a NaN or infinite entry of X, an entry whose square overflows, or a
 // non-finite error row in the head call).
 template <typename AccT, int V = 1>
 __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, const double* __restrict__ diag_part,
                                  loca_mb* __restrict__ mb, double eta, const AccT* __restrict__ Kraw, int split,
-                                 AccT* __restrict__ Kall, int64_t k_bstride, int32_t* __restrict__ dev_info) {
+                                 AccT* __restrict__ Kall, int64_t k_bstride, int32_t* __restrict__ dev_info,
+                                 int keep) {
   __shared__ double s_eb;
   const int64_t b = blockIdx.y;
   if (threadIdx.x < 64) {
@@ -780,7 +785,7 @@ __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, con
     static_assert(sizeof(AccT) == 4, "16-byte accesses of floats");
     const float4 k0 = *(const float4*)(kr + c);
     const float4 k1 = split ? *(const float4*)(kr + c + ku) : make_float4(0.f, 0.f, 0.f, 0.f);
-    const float4 o = *(const float4*)(K + e);
+    const float4 o = keep ? *(const float4*)(K + e) : make_float4(0.f, 0.f, 0.f, 0.f);
     const float a0[4] = {k0.x, k0.y, k0.z, k0.w}, a1[4] = {k1.x, k1.y, k1.z, k1.w}, ov[4] = {o.x, o.y, o.z, o.w};
     float r[4];
 #pragma unroll
@@ -793,7 +798,7 @@ __global__ void k_stats_finalize(int64_t n, int64_t d, int64_t k, int ntile, con
   } else {
     double v = (double)kr[c];
     if (split) v += (double)kr[c + ku];
-    K[e] = (AccT)((double)K[e] - eb * v);
+    K[e] = (AccT)((keep ? (double)K[e] : 0.0) - eb * v);
   }
 }
 
@@ -916,7 +921,7 @@ static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_
   const int64_t grid = gx > 0 ? 8 * per * rounds : ntot * nbc;
   k_gram_bf16_dl<2, 4, BUF, WT><<<dim3((unsigned)grid), 512, 0, a.stream>>>(
       a.n, a.d, (const uint16_t*)a.x, a.ldx, a.x_bstride, (float*)a.S, a.s_bstride, diag_part, zero16, b0, Yhl, w2,
-      w2p, Kraw, wpad, ncross, (int)run, (int)per, gx > 0 ? gx : 8, (int)nbc);
+      w2p, Kraw, wpad, ncross, (int)run, (int)per, gx > 0 ? gx : 8, (int)nbc, a.overwrite ? 0 : 1);
 }
 
 hipError_t launch_accumulate_stats(const StatsArgs& a) {
@@ -931,12 +936,13 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
     const int nK = T * (int)((a.k + kBM64 - 1) / kBM64);
     dim3 grid((unsigned)(nS + nK), (unsigned)a.nb);
     k_gram_f64<<<grid, kThreads, 0, a.stream>>>(a.n, a.d, a.k, (const float*)a.x, a.ldx, a.x_bstride, a.y,
-                                                a.y_bstride, (double*)a.S, a.s_bstride, Kraw, diag_part, nS, a.a_w);
+                                                a.y_bstride, (double*)a.S, a.s_bstride, Kraw, diag_part, nS, a.a_w,
+                                                a.overwrite ? 0 : 1);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
     k_stats_finalize<double><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 0,
-                                                       (double*)a.K, a.k_bstride, a.dev_info);
+                                                       (double*)a.K, a.k_bstride, a.dev_info, a.overwrite ? 0 : 1);
     return hipGetLastError();
   }
   float* Kraw = (float*)p;
@@ -998,17 +1004,17 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   } else if (big) {
     if (wt)
       k_gram_bf16<256, 2, 4, true><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
-                                                               a.s_bstride, diag_part, wpad);
+                                                               a.s_bstride, diag_part, wpad, a.overwrite ? 0 : 1);
     else
       k_gram_bf16<256, 2, 4, false><<<grid, 512, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
-                                                                a.s_bstride, diag_part, nullptr);
+                                                                a.s_bstride, diag_part, nullptr, a.overwrite ? 0 : 1);
   } else {
     if (wt)
       k_gram_bf16<128, 2, 2, true><<<grid, 256, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
-                                                               a.s_bstride, diag_part, wpad);
+                                                               a.s_bstride, diag_part, wpad, a.overwrite ? 0 : 1);
     else
       k_gram_bf16<128, 2, 2, false><<<grid, 256, 0, a.stream>>>(a.n, a.d, X, a.ldx, a.x_bstride, (float*)a.S,
-                                                                a.s_bstride, diag_part, nullptr);
+                                                                a.s_bstride, diag_part, nullptr, a.overwrite ? 0 : 1);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -1032,11 +1038,12 @@ hipError_t launch_accumulate_stats(const StatsArgs& a) {
   if (a.k % 4 == 0 && a.k_bstride % 4 == 0 && ((uintptr_t)a.K & 15) == 0) {
     dim3 g4((unsigned)((a.d * a.k / 4 + 255) / 256), (unsigned)a.nb);
     k_stats_finalize<float, 4><<<g4, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
-                                                         (float*)a.K, a.k_bstride, a.dev_info);
+                                                         (float*)a.K, a.k_bstride, a.dev_info,
+                                                         a.overwrite ? 0 : 1);
   } else {
     dim3 g2((unsigned)((a.d * a.k + 255) / 256), (unsigned)a.nb);
     k_stats_finalize<float><<<g2, 256, 0, a.stream>>>(a.n, a.d, a.k, T, diag_part, a.mb, a.eta, Kraw, 1,
-                                                      (float*)a.K, a.k_bstride, a.dev_info);
+                                                      (float*)a.K, a.k_bstride, a.dev_info, a.overwrite ? 0 : 1);
   }
   return hipGetLastError();
 }

@@ -143,8 +143,8 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
                                   loca_dtype x_dtype, int64_t ldx, int64_t x_bstride, const float* y,
                                   int64_t y_bstride, const float* a_w, double eta, loca_mb* mb, void* S, void* K,
                                   loca_dtype acc,
-                                  int64_t s_bstride, int64_t k_bstride, int32_t* dev_info, void* ws,
-                                  size_t ws_bytes) {
+                                  int64_t s_bstride, int64_t k_bstride, int overwrite, int32_t* dev_info,
+                                  void* ws, size_t ws_bytes) {
   if (nb < 1 || n < 1 || d < 1 || k < 1) return LOCA_E_ARG;
   if (!x || !y || !mb || !S || !K) return LOCA_E_ARG;
   if (!(eta >= 0.0) || eta == __builtin_inf()) return LOCA_E_ARG;
@@ -161,7 +161,7 @@ loca_status loca_accumulate_stats(loca_stream_t stream, int64_t nb, int64_t n, i
   loca_status st = check_ws(ws, ws_bytes, accumulate_stats_ws(nb, n, d, k, acc));
   if (st != LOCA_OK) return st;
   StatsArgs a{(hipStream_t)stream, nb, n, d, k, x, x_dtype, ldx, x_bstride, y, y_bstride, a_w, eta, mb, S, K, acc,
-              s_bstride, k_bstride, dev_info, (char*)ws};
+              s_bstride, k_bstride, dev_info, (char*)ws, overwrite != 0};
   return from_hip(launch_accumulate_stats(a));
 }
 

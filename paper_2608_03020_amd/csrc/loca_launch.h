@@ -85,6 +85,7 @@ struct StatsArgs {
   void* S; void* K; loca_dtype acc; int64_t s_bstride, k_bstride;
   int32_t* dev_info;
   char* ws;
+  bool overwrite;  // S and K are written, not accumulated into
 };
 size_t accumulate_stats_ws(int64_t nb, int64_t n, int64_t d, int64_t k, loca_dtype acc);
 hipError_t launch_accumulate_stats(const StatsArgs& a);

@@ -68,7 +68,7 @@ def load():
     lib.loca_error_targets_noalloc_max_bytes.argtypes = []
     lib.loca_error_targets_noalloc_max_bytes.restype = _SZ
     lib.loca_accumulate_stats.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I, _I64, _I64, _VP, _I64, _VP, _D,
-                                          _VP, _VP, _VP, _I, _I64, _I64, _VP, _VP, _SZ]
+                                          _VP, _VP, _VP, _I, _I64, _I64, _I, _VP, _VP, _SZ]
     lib.loca_ridge_solve.argtypes = [_VP, _I64, _I64, _I64, _VP, _VP, _I, _I64, _I64, _VP, _VP, _I64, _I64, _I64,
                                      _VP, _I64, _VP, _I64, _VP, _I64, _VP, _I64, _VP, _VP, _SZ]
     lib.loca_lowrank_truncate.argtypes = [_VP, _I64, _I64, _I64, _I64, _VP, _I64, _VP, _I64, _I64, _VP, _I64, _VP,
@@ -231,17 +231,18 @@ def error_targets_noalloc_max_bytes() -> int:
     return int(load().loca_error_targets_noalloc_max_bytes())
 
 
-def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, dev_info=None, stream=None):
+def loca_accumulate_stats(x, y, eta, mb, S, K, ws, *, a_w=None, dev_info=None, overwrite=False, stream=None):
     """x (nb, n, d) bf16 or fp32 (row stride may exceed d); y (nb, n, k); S (nb, d, d); K (nb, d, k);
     a_w (n,) float32 statistic weights, the array given to loca_error_targets (optional);
-    dev_info (nb,) int32 non-finite flags (optional)."""
+    dev_info (nb,) int32 non-finite flags (optional); overwrite: S and K take this
+    micro-batch's statistics instead of adding them (the first micro-batch of a step)."""
     nb, n, d = x.shape
     k = y.shape[-1]
     acc = _dtype(S)
     st = load().loca_accumulate_stats(
         _stream(stream), nb, n, d, k, _ptr(x, False), _dtype(x), x.stride(1), x.stride(0), _ptr(y), y.stride(0), _ptr(a_w),
         float(eta),
-        _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), _ptr(dev_info), _ptr(ws),
+        _ptr(mb), _ptr(S), _ptr(K), acc, S.stride(0), K.stride(0), int(bool(overwrite)), _ptr(dev_info), _ptr(ws),
         ws.numel() * ws.element_size())
     _check("loca_accumulate_stats", st)
 

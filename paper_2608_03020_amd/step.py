@@ -47,6 +47,7 @@ class BlockStep:
         self.info_trunc = torch.zeros(nb * nl, **i32)
         self.info_proj = torch.zeros(nb * nl, **i32)
         self._m = 0
+        self._gram = False
         self.r_prev = r_prev
         kp = r_prev + k  # right-hand sides of the solve: [S Lp | K]
         self.M = torch.empty((nb, nl, d, kp), dtype=torch.float32, device=device)
@@ -70,9 +71,11 @@ class BlockStep:
         )
         self.ws = loca.alloc_workspace(ws, device)
         if poison:
-            # NaN in every output and all-ones bytes in the workspaces, so that a region a
-            # call should write but does not shows up as NaN in the results
-            for t in (self.Y, self.M, self.A_ad, self.B_ad, self.sigma) + ((self.B_proj,) if projected else ()):
+            # NaN in every output (S and K too: the first micro-batch overwrites them, and
+            # the entries of S below the diagonal are never read) and all-ones bytes in the
+            # workspaces, so that a region a call should write but does not shows up as NaN
+            for t in (self.Y, self.M, self.A_ad, self.B_ad, self.sigma, self.S, self.K) + \
+                    ((self.B_proj,) if projected else ()):
                 t.fill_(float("nan"))
             self.ws.fill_(255)
             if projected:
@@ -87,10 +90,22 @@ class BlockStep:
                           self.info_proj])
 
     def reset(self):
-        self.S.zero_()
-        self.K.zero_()
+        # the first micro-batch's call overwrites S and K: no clearing pass
         self.mb_log = []
         self._m = 0  # every call rewrites its own dev_info slice
+        self._gram = False  # B~ B~^T not yet formed in this step
+
+    def resume(self, S, K, m_done: int):
+        """Continue a step from saved statistics (checkpoint and resume): S, K as they were
+        after the step's first m_done micro-batches (1 <= m_done < n_micro); the next
+        micro_batch call is micro-batch m_done and adds into them."""
+        if not 1 <= m_done < self.cfg.n_micro:
+            raise ValueError(f"m_done must lie in [1, {self.cfg.n_micro}), got {m_done}")
+        self.S.copy_(S)
+        self.K.copy_(K)
+        self.mb_log = []
+        self._m = m_done
+        self._gram = False
 
     def micro_batch(self, x_m, logits_m, labels_m, credit_a, credit_b, keep_log=False, stream=None, w=None, a=None):
         """Rows a1-a4 for one micro-batch: x_m (nb, n_m, d); w (n_m,) optional loss weights;
@@ -101,12 +116,13 @@ class BlockStep:
         if m >= self.cfg.n_micro:
             raise ValueError(f"more than {self.cfg.n_micro} micro-batches since reset()")
         self._m += 1
-        if m == 0:  # B~ is fixed for the step: its Gram serves every micro-batch
+        if not self._gram:  # B~ is fixed for the step: its Gram serves every micro-batch
             loca.loca_credit_gram(credit_b, self.G, self.ws, stream=stream)
+            self._gram = True
         loca.loca_error_targets(logits_m, labels_m, credit_a, credit_b, y, self.mb, self.info_err[m:m + 1], self.ws,
                                 w=w, a_w=a, nb=self.nb, credit_gram=self.G, stream=stream)
         loca.loca_accumulate_stats(x_m, y, self.cfg.eta, self.mb, self.S, self.K, self.ws, a_w=a,
-                                   dev_info=self.info_stats[m], stream=stream)
+                                   dev_info=self.info_stats[m], overwrite=m == 0, stream=stream)
         if keep_log:
             self.mb_log.append(self.mb.clone())
 

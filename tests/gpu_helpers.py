@@ -74,8 +74,10 @@ def run_gpu(cfg, xs, zs, ys, As, Bs, want_dense=True, proj=None, device="cuda"):
     step.solve(B, P)
     nl = len(cfg.lambdas)
     # every output of the step was NaN before the calls (poisoned): none may survive
+    # (S: its upper triangle, the part the statistics call maintains)
     for name, t in (("M", step.M), ("A", step.A_ad), ("B", step.B_ad), ("sigma", step.sigma),
-                    ("S", step.S), ("K", step.K)) + ((("B_proj", step.B_proj),) if proj is not None else ()):
+                    ("S", torch.triu(step.S)), ("K", step.K)) + \
+            ((("B_proj", step.B_proj),) if proj is not None else ()):
         assert not bool(torch.isnan(t).any()), f"{name} has unwritten (NaN) entries"
     out = {"S": step.S.cpu().numpy(), "K": step.K.cpu().numpy(), "Y": Ys, "mb": mbs,
            "M": step.M.cpu().numpy(), "sigma": step.sigma.cpu().numpy(), "A": step.A_ad.cpu().numpy(),

@@ -112,7 +112,7 @@ def test_credit_gram_rejects_and_layout(lib):
 def test_accumulate_stats_rejects(lib):
     so = lib.load()
     base = [None, 1, 64, 32, 4, FAKE, lib.LOCA_BF16, 32, 0, FAKE, 0, None, 0.01, FAKE, FAKE, FAKE, lib.LOCA_F32,
-            0, 0, None, None, 0]
+            0, 0, 1, None, None, 0]
 
     def call(**kw):
         idx = dict(nb=1, n=2, d=3, k=4, x=5, xdt=6, ldx=7, xbs=8, eta=12, S=14, acc=16)

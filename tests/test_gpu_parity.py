@@ -485,6 +485,47 @@ def test_tiny_width_and_single_token():
         assert abs(loca.mb_view(mb)["eta_bar"][0] - eb) < 1e-6 * eb
 
 
+@pytest.mark.parametrize("d,k,mode,weighted", [(1040, 8, "bf16", False), (1040, 40, "bf16", True),
+                                               (1024, 64, "bf16", False), (200, 24, "bf16", True),
+                                               (100, 12, "fp32", True)])
+def test_stats_overwrite_equals_cleared_accumulation(d, k, mode, weighted):
+    """The overwrite flag (the first micro-batch of a step) leaves S's upper triangle, K and
+    the micro-batch records bit for bit as the accumulating call on zeroed S and K, without
+    reading the old contents (NaN here); a second, accumulating micro-batch keeps them
+    equal.  Paths: the direct-to-LDS Gram kernel with the cross statistic fused (k = 8)
+    and as cross tiles (k = 40, 64), the register-staged kernel (d = 200), the fp64 kernel."""
+    import torch
+    from paper_2608_03020_amd import loca
+    nb, n = 2, 300
+    log(f"case stats overwrite: d={d} k={k} mode={mode} weighted={weighted}")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(d + k)
+    xt, acc_t = (torch.bfloat16, torch.float32) if mode == "bf16" else (torch.float32, torch.float64)
+    acc = loca.LOCA_F32 if mode == "bf16" else loca.LOCA_F64
+    ld = (d + 7) // 8 * 8
+    xs = [torch.randn((nb, n, ld), generator=g, device="cuda").to(xt)[:, :, :d] for _ in range(2)]
+    ys = [torch.randn((nb, n, k), generator=g, device="cuda") for _ in range(2)]
+    aws = [torch.rand(n, generator=g, device="cuda") if weighted else None for _ in range(2)]
+    ws = loca.alloc_workspace(loca.workspace_size(loca.LOCA_OP_ACCUMULATE_STATS, nb, n, d, k, acc=acc))
+    out = []
+    for ovw in (False, True):
+        fill = float("nan") if ovw else 0.0
+        S = torch.full((nb, d, d), fill, dtype=acc_t, device="cuda")
+        K = torch.full((nb, d, k), fill, dtype=acc_t, device="cuda")
+        res = []
+        for m in range(2):
+            mb = loca.new_mb(nb)
+            mb[:, 0] = 1.0 + m  # sum_q2
+            loca.loca_accumulate_stats(xs[m], ys[m], 0.5, mb, S, K, ws, a_w=aws[m], overwrite=ovw and m == 0)
+            torch.cuda.synchronize()
+            res.append((torch.triu(S).cpu().numpy(), K.cpu().numpy(), mb.cpu().numpy()))
+        out.append(res)
+    for m in range(2):
+        for a, b in zip(out[0][m], out[1][m]):
+            assert np.array_equal(a, b), m
+    assert not np.isnan(out[1][1][0]).any() and not np.isnan(out[1][1][1]).any()
+
+
 @pytest.mark.parametrize("C,k,ldt,adt", [(5, 32, "f32", "f32"), (4, 5, "f32", "f32"), (3001, 24, "f32", "f32"),
                                          (3001, 32, "bf16", "bf16"), (3001, 96, "bf16", "bf16"), (70, 72, "f32", "bf16")])
 def test_precomputed_credit_gram_gives_the_same_bits(C, k, ldt, adt):
@@ -568,8 +609,7 @@ def test_statistics_deterministic_and_resumable():
             if split is not None and m == split:
                 S_h, K_h = st.S.cpu().numpy().copy(), st.K.cpu().numpy().copy()
                 st = BlockStep(cfg, 2)
-                st.S.copy_(torch.from_numpy(S_h))
-                st.K.copy_(torch.from_numpy(K_h))
+                st.resume(torch.from_numpy(S_h), torch.from_numpy(K_h), m)
             lo, hi = cfg.micro_rows(m)
             st.micro_batch(x_all[:, lo:hi], z_all[lo:hi], y_all[lo:hi], A, B)
         torch.cuda.synchronize()
