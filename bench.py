@@ -34,10 +34,10 @@ HBM_PEAK_GBS = 8000.0
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
 # kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 3716693.5, "write_kib": 791629.8, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "715eff64eb510a5b"},
-    "c5": {"fetch_kib": 17925713.9, "write_kib": 2658928.0, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "715eff64eb510a5b"},
+    "c3": {"fetch_kib": 3423254.2, "write_kib": 774964.5, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "f594c4e78ae42ba0"},
+    "c5": {"fetch_kib": 18017120.1, "write_kib": 2699920.4, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "f594c4e78ae42ba0"},
 }
 
 
