@@ -113,6 +113,9 @@ static size_t credit_gram_part_ws(int64_t nb, int64_t k) { return align256(sizeo
 //     each lane multiplies its entries of M_w by those of G (KB x KB, zero past k; blocks off
 //     the diagonal count twice).
 // The tile reuses the A~ area once it is consumed.
+// HC > 0 (label sets of C <= HC classes): since y_t = e_t A~, the same sum is
+// sum_t a_t e_t H e_t^T with the C x C matrix H = A~ G A~^T (fp64, formed in LDS by every
+// workgroup), HC^2 fp64 FMAs per token in place of the matrix-core pass over the tile.
 static int64_t small_kb(int64_t k) { return k <= 16 ? 16 : k <= 32 ? 32 : 64; }
 template <int KB>
 struct SmallLds {
@@ -122,7 +125,7 @@ struct SmallLds {
   static constexpr int BYTES = IN > ST ? IN : ST;
 };
 
-template <typename LT, typename AT, int KB>
+template <typename LT, typename AT, int KB, int HC>
 __global__ __launch_bounds__(kSmallThreads) void k_error_small(
     int64_t n, int64_t C, int64_t k, const LT* __restrict__ logits, int64_t ld,
     const int32_t* __restrict__ labels, const float* __restrict__ w, const float* __restrict__ aw,
@@ -134,6 +137,8 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
   __shared__ __attribute__((aligned(16))) unsigned char lds[L::BYTES];
   __shared__ float sW[kSmallThreads];  // statistic weight of each token (0 past n)
   __shared__ double sred[kSmallThreads / 64];
+  __shared__ double sAG[HC > 0 ? HC * KB : 1];  // A~ G (HC x KB)
+  __shared__ double sH[HC > 0 ? HC * HC : 1];   // A~ G A~^T, zero past C
   float* sA = (float*)lds;  // C x KB, zero past k (the products below need no bound)
   const int64_t b = blockIdx.y;
   const AT* Ab = A + b * a_bstride;
@@ -143,12 +148,49 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
     sA[e] = j < k ? load_as_f32(Ab + c * k + j) : 0.f;
   }
   __syncthreads();
+  if constexpr (HC > 0) {
+    // A~ G: thread (j, iq) = (tid / 4, tid % 4) reads G[i][j] for its quarter of i once (the
+    // loads issued together) and adds it into all HC rows; the quarters meet by shuffles
+    static_assert(kSmallThreads == 4 * 64, "64 columns x 4 quarters");
+    const int j = (int)threadIdx.x >> 2, iq = (int)threadIdx.x & 3;
+    constexpr int IQ = KB / 4;
+    if (j < KB) {
+      double g[IQ];
+#pragma unroll
+      for (int ii = 0; ii < IQ; ++ii) g[ii] = Gb[(iq * IQ + ii) * KB + j];
+      double v[HC];
+#pragma unroll
+      for (int c = 0; c < HC; ++c) {
+        v[c] = 0.0;
+#pragma unroll
+        for (int ii = 0; ii < IQ; ++ii) v[c] = fma((double)sA[(c < C ? c : 0) * KB + iq * IQ + ii], g[ii], v[c]);
+      }
+#pragma unroll
+      for (int c = 0; c < HC; ++c) {
+        v[c] += __shfl_xor(v[c], 1, 64);
+        v[c] += __shfl_xor(v[c], 2, 64);
+        if (iq == 0) sAG[c * KB + j] = c < C ? v[c] : 0.0;
+      }
+    }
+    __syncthreads();
+    for (int e = (int)threadIdx.x; e < HC * HC; e += kSmallThreads) {
+      const int c = e / HC, c2 = e % HC;
+      double v = 0.0;
+      if (c < C && c2 < C)
+        for (int j = 0; j < KB; ++j) v = fma(sAG[c * KB + j], (double)sA[c2 * KB + j], v);
+      sH[e] = v;
+    }
+    // sH is read after the barrier below that retires the reads of sA
+  }
 
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   float y[KB];
 #pragma unroll
   for (int j = 0; j < KB; ++j) y[j] = 0.f;
   float wq = 0.f;  // weight of this token in ||Q||^2
+  float ev[HC > 0 ? HC : 1];  // this token's error row (HC > 0), zero past C
+#pragma unroll
+  for (int c = 0; c < (HC > 0 ? HC : 1); ++c) ev[c] = 0.f;
   if (t < n) {
     const LT* zt = logits + t * ld;
     const int32_t yt = labels[t];
@@ -179,16 +221,34 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
       }
       const float inv = 1.0f / s;
       const float wt = w ? w[t] : 1.0f;
-      for (int64_t c0 = 0; c0 < C; c0 += 8) {
-        if (c0 > 0 || C > 8) chunk(c0);
+      if constexpr (HC > 0) {  // the chunks unrolled, so that ev is indexed by constants
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int64_t c = c0 + u;
-          if (c >= C) break;
-          const float e = wt * (__expf(zc[u] - m) * inv - (c == yt ? 1.0f : 0.0f));
-          if (e_out) e_out[t * C + c] = e;
+        for (int c0 = 0; c0 < HC; c0 += 8) {
+          if (c0 >= C) break;
+          if (c0 > 0 || C > 8) chunk(c0);
 #pragma unroll
-          for (int j = 0; j < KB; ++j) y[j] = fmaf(e, sA[c * KB + j], y[j]);
+          for (int u = 0; u < 8; ++u) {
+            const int c = c0 + u;
+            if (c >= C) break;
+            const float e = wt * (__expf(zc[u] - m) * inv - (c == yt ? 1.0f : 0.0f));
+            if (e_out) e_out[t * C + c] = e;
+            ev[c] = e;
+#pragma unroll
+            for (int j = 0; j < KB; ++j) y[j] = fmaf(e, sA[c * KB + j], y[j]);
+          }
+        }
+      } else {
+        for (int64_t c0 = 0; c0 < C; c0 += 8) {
+          if (c0 > 0 || C > 8) chunk(c0);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            const int64_t c = c0 + u;
+            if (c >= C) break;
+            const float e = wt * (__expf(zc[u] - m) * inv - (c == yt ? 1.0f : 0.0f));
+            if (e_out) e_out[t * C + c] = e;
+#pragma unroll
+            for (int j = 0; j < KB; ++j) y[j] = fmaf(e, sA[c * KB + j], y[j]);
+          }
         }
       }
       wq = aw ? aw[t] : 1.0f;  // statistic weight of the position
@@ -230,6 +290,20 @@ __global__ __launch_bounds__(kSmallThreads) void k_error_small(
       const int64_t tp = t0 + p;
       if (tp < n && c < k) yb[tp * k + c] = sT[p * (KB + 1) + c];
     }
+  }
+
+  if constexpr (HC > 0) {  // a_t e_t H e_t^T of this thread's token (ev and wq zero past n)
+    double q = 0.0;
+#pragma unroll
+    for (int c = 0; c < HC; ++c) {
+      double u = 0.0;
+#pragma unroll
+      for (int c2 = 0; c2 < HC; ++c2) u = fma(sH[c * HC + c2], (double)ev[c2], u);
+      q = fma((double)ev[c], u, q);
+    }
+    const double tot = block_sum((double)wq * q, sred);
+    if (threadIdx.x == 0) partial[b * gridDim.x + blockIdx.x] = tot;
+    return;
   }
 
   // this wave's part of ||Q||^2
@@ -568,13 +642,20 @@ static hipError_t dispatch_error(const ErrorArgs& a, double* G, double* partial,
   const AT* A = (const AT*)a.credit_a;
   if (use_small(a.C, a.k)) {
     dim3 grid((unsigned)((a.n + kSmallThreads - 1) / kSmallThreads), (unsigned)a.nb);
-#define LOCA_SMALL(KB)                                                                              \
-  k_error_small<LT, AT, KB><<<grid, kSmallThreads, 0, a.stream>>>(                                  \
+    // ||Q||^2 through the C x C matrix A~ G A~^T for label sets of at most 16 classes,
+    // else on the fp64 matrix cores from the tile of Y
+#define LOCA_SMALL(KB, HC)                                                                          \
+  k_error_small<LT, AT, KB, HC><<<grid, kSmallThreads, 0, a.stream>>>(                              \
       a.n, a.C, a.k, z, a.ld_logits, a.labels, a.w, a.a_w, A, a.a_bstride, G, a.y_out, a.y_bstride, a.e_out, \
       partial, a.dev_info)
-    if (a.k <= 16) LOCA_SMALL(16);
-    else if (a.k <= 32) LOCA_SMALL(32);
-    else LOCA_SMALL(64);
+#define LOCA_SMALL_KB(KB)                      \
+  if (a.C <= 8) LOCA_SMALL(KB, 8);             \
+  else if (a.C <= 16) LOCA_SMALL(KB, 16);      \
+  else LOCA_SMALL(KB, 0);
+    if (a.k <= 16) { LOCA_SMALL_KB(16) }
+    else if (a.k <= 32) { LOCA_SMALL_KB(32) }
+    else { LOCA_SMALL_KB(64) }
+#undef LOCA_SMALL_KB
 #undef LOCA_SMALL
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
