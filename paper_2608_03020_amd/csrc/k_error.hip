@@ -27,59 +27,70 @@ constexpr int kSmallMaxK = 64;
 constexpr int kMaxK = 128;
 
 // G_b = B~_b B~_b^T (k x k, float64) in two passes.  k_credit_gram_part: one workgroup per
-// (32 x 32 tile on or above the diagonal, one of kCGSplit ranges of the width d, block);
-// the tile's 32 + 32 rows of B~ stream through LDS in 64-column chunks (the next chunk
-// loaded while the current one is used) and each wave forms a 16 x 16 block of the tile on
-// the fp64 matrix cores, in the order of the columns.  k_credit_gram_sum adds the kCGSplit partials of an entry in a fixed
-// order and writes it and its mirror: deterministic.
-constexpr int kCGSplit = 8, kCGC = 64;
+// (one of kCGSplit ranges of the width d, block): the k rows of B~ over the range stream
+// through LDS in 64-column chunks (each load instruction one row's 64 consecutive columns;
+// the next chunk held in registers while the current one is used), and the four waves take
+// the 16 x 16 blocks on or above the diagonal in turn (block u to wave u % 4), each formed on
+// the fp64 matrix cores in the order of the columns; every row of B~ is read once.
+// k_credit_gram_sum adds the kCGSplit partials of an entry in a fixed order and writes it
+// and its mirror: deterministic.
+constexpr int kCGSplit = 8, kCGC = 64, kCGLd = kCGC + 4;  // row stride 68: conflict-free MFMA reads
+template <int KR>  // rows staged: k rounded up to a multiple of 16 (at most 128)
 __global__ __launch_bounds__(256) void k_credit_gram_part(int64_t k, int64_t d, const float* __restrict__ B,
                                                           int64_t b_bstride, double* __restrict__ part) {
-  __shared__ float sa[32][kCGC + 1], sc[32][kCGC + 1];
-  const int T = (int)((k + 31) / 32);
-  int u = blockIdx.x, I = 0;
-  while (u >= T - I) { u -= T - I; ++I; }
-  const int J = I + u;
-  const int64_t s = blockIdx.y, b = blockIdx.z;
+  constexpr int NB16 = KR / 16, NUP = NB16 * (NB16 + 1) / 2, PER = (NUP + 3) / 4, RPT = KR / 4;
+  __shared__ float sB[KR * kCGLd];
+  const int64_t s = blockIdx.x, b = blockIdx.y;
   const float* Bb = B + b * b_bstride;
-  const int64_t a0 = 32 * (int64_t)I, c0 = 32 * (int64_t)J;
   const int64_t chunk = ((d + kCGSplit - 1) / kCGSplit + kCGC - 1) / kCGC * kCGC;
   const int64_t i0 = s * chunk, i1 = i0 + chunk < d ? i0 + chunk : d;
-  const int t = threadIdx.x;
-  const int lrow = t >> 3, lcol = 8 * (t & 7);  // this thread's staging: row lrow, columns lcol .. lcol + 7
-  // wave (wa, wc) forms the 16 x 16 block (a0 + 16 wa, c0 + 16 wc) of the tile on the fp64
-  // matrix cores (v_mfma_f64_16x16x4f64; products of floats are exact in fp64)
-  const int lane = t & 63, wa = (t >> 6) >> 1, wc = (t >> 6) & 1, kr = lane >> 4, cr = lane & 15;
-  f64x4_t acc = {0.0, 0.0, 0.0, 0.0};
-  float va[8], vc[8];
-  auto load = [&](int64_t j0) {
+  const int t = threadIdx.x, lc = t & 63, wv = t >> 6, kr = (t & 63) >> 4, cr = t & 15;
+  // this wave's blocks (I, J), I <= J, in row-major order of the upper triangle
+  int bI[PER], bJ[PER];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int64_t col = j0 + lcol + e;
-      const bool okc = col < i1;
-      va[e] = (okc && a0 + lrow < k) ? Bb[(a0 + lrow) * d + col] : 0.f;
-      vc[e] = (okc && c0 + lrow < k) ? Bb[(c0 + lrow) * d + col] : 0.f;
+  for (int q = 0; q < PER; ++q) {
+    int u = wv + 4 * q, I = 0;
+    while (I < NB16 && u >= NB16 - I) { u -= NB16 - I; ++I; }
+    bI[q] = I;
+    bJ[q] = I + u;  // I == NB16 past the last block: no such block
+  }
+  f64x4_t acc[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) acc[q] = f64x4_t{0.0, 0.0, 0.0, 0.0};
+  float v[RPT];  // rows wv + 4 e, column lc of the chunk
+  auto load = [&](int64_t j0) {
+    const int64_t col = j0 + lc;
+#pragma unroll
+    for (int e = 0; e < RPT; ++e) {
+      const int r = wv + 4 * e;
+      v[e] = (r < k && col < i1) ? Bb[r * d + col] : 0.f;
     }
   };
   if (i0 < i1) load(i0);
   for (int64_t j0 = i0; j0 < i1; j0 += kCGC) {
     __syncthreads();  // the previous chunk is no longer read
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      sa[lrow][lcol + e] = va[e];
-      sc[lrow][lcol + e] = vc[e];
-    }
+    for (int e = 0; e < RPT; ++e) sB[(wv + 4 * e) * kCGLd + lc] = v[e];
     __syncthreads();
     if (j0 + kCGC < i1) load(j0 + kCGC);
 #pragma unroll
-    for (int kk = 0; kk < kCGC; kk += 4)  // A[i][x] = B~[a][x], B[x][j] = B~[c][x]
-      acc = mfma_f64((double)sa[16 * wa + cr][kk + kr], (double)sc[16 * wc + cr][kk + kr], acc);
-  }
-  double* P = part + ((s * (int64_t)gridDim.z + b) * k) * k;
+    for (int q = 0; q < PER; ++q) {
+      if (bI[q] >= NB16) break;
+      const float* ra = sB + (16 * bI[q] + cr) * kCGLd + kr;  // A[i][x] = B~[16 I + i][x]
+      const float* rc = sB + (16 * bJ[q] + cr) * kCGLd + kr;  // B[x][j] = B~[16 J + j][x]
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int64_t row = a0 + 16 * wa + kr + 4 * r, col = c0 + 16 * wc + cr;
-    if (row < k && col < k) P[row * k + col] = acc[r];
+      for (int kk = 0; kk < kCGC; kk += 4) acc[q] = mfma_f64((double)ra[kk], (double)rc[kk], acc[q]);
+    }
+  }
+  double* P = part + ((s * (int64_t)gridDim.y + b) * k) * k;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    if (bI[q] >= NB16) break;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = 16 * bI[q] + kr + 4 * r, col = 16 * bJ[q] + cr;
+      if (row < k && col < k) P[row * k + col] = acc[q][r];
+    }
   }
 }
 // G is written with row stride ldg >= k, zero in the rows and columns past k.
@@ -97,9 +108,11 @@ __global__ void k_credit_gram_sum(int64_t k, int64_t ldg, int64_t nb, const doub
 }
 static void launch_credit_gram(hipStream_t st, int64_t nb, int64_t k, int64_t d, const float* B, int64_t b_bstride,
                                double* part, double* G, int64_t ldg) {
-  const int T = (int)((k + 31) / 32);
-  k_credit_gram_part<<<dim3((unsigned)(T * (T + 1) / 2), kCGSplit, (unsigned)nb), 256, 0, st>>>(k, d, B, b_bstride,
-                                                                                                  part);
+  const dim3 g((unsigned)kCGSplit, (unsigned)nb);
+  if (k <= 16) k_credit_gram_part<16><<<g, 256, 0, st>>>(k, d, B, b_bstride, part);
+  else if (k <= 32) k_credit_gram_part<32><<<g, 256, 0, st>>>(k, d, B, b_bstride, part);
+  else if (k <= 64) k_credit_gram_part<64><<<g, 256, 0, st>>>(k, d, B, b_bstride, part);
+  else k_credit_gram_part<128><<<g, 256, 0, st>>>(k, d, B, b_bstride, part);
   k_credit_gram_sum<<<dim3((unsigned)((ldg * ldg + 255) / 256), (unsigned)nb), 256, 0, st>>>(k, ldg, nb, part, G);
 }
 static size_t credit_gram_part_ws(int64_t nb, int64_t k) { return align256(sizeof(double) * kCGSplit * nb * k * k); }
