@@ -470,10 +470,13 @@ static unsigned write_e_rows(int64_t n) { return (unsigned)(n < 65535 ? n : 6553
 // has already written in place, whatever the order of the blocks.
 __global__ void k_error_finalize(int64_t n, int64_t nparts, const double* __restrict__ partial,
                                  loca_mb* __restrict__ mb, int32_t* __restrict__ dev_info) {
+  // one wave: lane l adds partials l, l + 64, ... in order, then a fixed butterfly across
+  // the lanes (deterministic)
   const int64_t b = blockIdx.x;
+  double part = 0.0;
+  for (int64_t i = threadIdx.x; i < nparts; i += 64) part += partial[b * nparts + i];
+  const double s = wave_sum(part);
   if (threadIdx.x != 0) return;
-  double s = 0.0;
-  for (int64_t i = 0; i < nparts; ++i) s += partial[b * nparts + i];
   if (dev_info) {
     if (!__builtin_isfinite(s)) atomicMin(dev_info, (int32_t)LOCA_INFO_NONFINITE);
     if (b == 0) atomicCAS(dev_info, INT32_MAX, 0);
