@@ -902,14 +902,16 @@ template <bool BUF, bool WT>
 static void launch_gram_dl(const StatsArgs& a, int64_t ntile, int64_t b0, int64_t nbc, const uint16_t* zero16,
                            double* diag_part, const uint16_t* Yhl, int64_t w2, int64_t w2p, float* Kraw,
                            const float* wpad, int ncross) {
-  // block-synchronous order with the widest XCD group (8, 4 or 2) whose runs hold at least
-  // 24 tiles, if there are blocks enough for every group; else the XCD-aware order.  The
+  // block-synchronous order with XCD groups of four (else two) whose runs hold at least 24
+  // tiles, if there are blocks enough for every group; else the XCD-aware order.  Groups of
+  // eight (every XCD on one block) were slower where runs of 24 allowed them (d = 5120:
+  // statistics call +0.4%; two blocks' X of 84 MB each still fit the last-level cache).  The
   // runs split a block's cost: a cross tile whose targets span at most two of the four
   // column blocks (four waves with products, one per SIMD) is counted as 0.6 of a Gram tile,
   // and the cross tiles, last in a block, go to the last run of its group.
   const int64_t ntot = ntile + ncross;
   int gx = 0;
-  for (int g = 8; g >= 2 && gx == 0; g /= 2)
+  for (int g = 4; g >= 2 && gx == 0; g /= 2)
     if ((ntot + g - 1) / g >= 24 && nbc >= 8 / g) gx = g;
   int64_t run = 0, per = 0;
   if (gx > 0) {
