@@ -34,10 +34,10 @@ HBM_PEAK_GBS = 8000.0
 # Valid only for the kernel source it was taken on (digest of k_gram.hip + loca_common.h, the
 # kernel file and the device helpers it includes).
 TRAFFIC = {
-    "c3": {"fetch_kib": 3423254.2, "write_kib": 774964.5, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "f594c4e78ae42ba0"},
-    "c5": {"fetch_kib": 18017120.1, "write_kib": 2699920.4, "fetch_scale": 1.0, "write_scale": 1.0,
-           "src_digest": "f594c4e78ae42ba0"},
+    "c3": {"fetch_kib": 3388361.0, "write_kib": 778898.2, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "8e73809de34918f3"},
+    "c5": {"fetch_kib": 15697122.3, "write_kib": 2700420.1, "fetch_scale": 1.0, "write_scale": 1.0,
+           "src_digest": "8e73809de34918f3"},
 }
 
 
